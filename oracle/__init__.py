@@ -1,0 +1,196 @@
+"""CPU oracle for the Gaussian-relaxed scheduling objective (fp64).
+
+TEST INFRASTRUCTURE ONLY: only `tests/`, `__graft_entry__.smoke()` and the
+CPU-baseline leg of `bench.py` may import this package.  It shares no code with
+the GPU library (`paper_2602_20427_amd`), and the library never imports it.
+
+`gaus_oracle.c` holds the arithmetic; this module builds it with gcc, loads it
+with ctypes and converts numpy arrays.  `brute.py` enumerates all schedules of
+tiny instances for the pins.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "gaus_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+OK, E_INVALID, E_CYCLE, E_HORIZON, E_NOT_CONVERGED, E_OVERFLOW, E_NOMEM = 0, 1, 2, 3, 4, 5, 7
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle (plain C, fp64, OpenMP) into oracle/liboracle.so."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared", "-D_GNU_SOURCE",
+               "-Wall", "-Wextra", "-Wno-unused-parameter", "-o", tmp, _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+class _Problem(C.Structure):
+    _fields_ = [("n", C.c_int32), ("e", C.c_int32),
+                ("row_ptr", C.c_void_p), ("col", C.c_void_p), ("delay", C.c_void_p),
+                ("rtype", C.c_void_p), ("K", C.c_int32), ("cap", C.c_void_p),
+                ("D", C.c_int32), ("II", C.c_int32), ("nb", C.c_int32),
+                ("bsrc", C.c_void_p), ("bdst", C.c_void_p), ("bdist", C.c_void_p)]
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        lib = C.CDLL(_LIB)
+        P = C.POINTER(_Problem)
+        vp, i32, i64, dbl = C.c_void_p, C.c_int32, C.c_int64, C.c_double
+        lib.orc_loss_grad.argtypes = [P, vp, vp, vp, dbl, dbl, dbl, vp, vp, vp, vp, vp]
+        lib.orc_loss_grad.restype = C.c_int
+        lib.orc_edge_terms_double_sum.argtypes = [P, vp, vp, vp]
+        lib.orc_edge_terms_double_sum.restype = None
+        lib.orc_adam.argtypes = [i64, vp, vp, vp, vp, i32, dbl, dbl, dbl, dbl]
+        lib.orc_adam.restype = None
+        lib.orc_legalize.argtypes = [P, vp, vp]
+        lib.orc_legalize.restype = C.c_int
+        lib.orc_asap_alap.argtypes = [P, vp, vp]
+        lib.orc_asap_alap.restype = C.c_int
+        lib.orc_topo.argtypes = [P, vp, vp]
+        lib.orc_topo.restype = C.c_int
+        lib.orc_init_state.argtypes = [P, i32, vp, dbl, dbl, vp, vp]
+        lib.orc_init_state.restype = C.c_int
+        lib.orc_mass.argtypes = [dbl, dbl, i32, i32]
+        lib.orc_mass.restype = dbl
+        lib.orc_num_threads.argtypes = []
+        lib.orc_num_threads.restype = C.c_int
+        _lib = lib
+    return _lib
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(C.c_void_p)
+
+
+class OracleProblem:
+    """Holds contiguous copies of a problem's arrays for the C oracle."""
+
+    def __init__(self, prob):
+        self.n = int(prob.n_ops)
+        self.D = int(prob.D)
+        self.II = int(prob.II)
+        self.K = int(prob.n_types)
+        self.row_ptr = np.ascontiguousarray(prob.row_ptr, np.int32)
+        self.col = np.ascontiguousarray(prob.col_idx, np.int32)
+        self.delay = np.ascontiguousarray(prob.delay, np.int32)
+        self.rtype = np.ascontiguousarray(prob.rtype, np.int32)
+        self.cap = np.ascontiguousarray(prob.capacity, np.float64)
+        self.bsrc = np.ascontiguousarray(prob.back_src, np.int32)
+        self.bdst = np.ascontiguousarray(prob.back_dst, np.int32)
+        self.bdist = np.ascontiguousarray(prob.back_dist, np.int32)
+        self.s = _Problem(self.n, int(self.row_ptr[-1]), _ptr(self.row_ptr), _ptr(self.col),
+                          _ptr(self.delay), _ptr(self.rtype), self.K, _ptr(self.cap),
+                          self.D, self.II, int(self.bsrc.shape[0]), _ptr(self.bsrc),
+                          _ptr(self.bdst), _ptr(self.bdist))
+
+    @property
+    def T(self) -> int:
+        return self.II if self.II > 0 else self.D
+
+
+def _op(prob):
+    return prob if isinstance(prob, OracleProblem) else OracleProblem(prob)
+
+
+def num_threads() -> int:
+    return int(_load().orc_num_threads())
+
+
+def loss_grad(prob, mu, sigma, lam, alpha, rho, grad=True, tie_tol=1e-4):
+    """Per restart b: terms [B,5] = (L, V_dep, V_res, V_rec, L_com), U [B,K,T],
+    g_mu, g_sigma [B,N] (fp64), ties [B] (count of near-tie usage cells)."""
+    lib, op = _load(), _op(prob)
+    mu = np.atleast_2d(np.asarray(mu, np.float64))
+    sigma = np.atleast_2d(np.asarray(sigma, np.float64))
+    lam = np.atleast_2d(np.asarray(lam, np.float64))
+    B = mu.shape[0]
+    terms = np.zeros((B, 5)); U = np.zeros((B, op.K, op.T))
+    gm = np.zeros((B, op.n)); gs = np.zeros((B, op.n)); ties = np.zeros(B, np.int64)
+    for b in range(B):
+        m = np.ascontiguousarray(mu[b]); s = np.ascontiguousarray(sigma[b])
+        l = np.ascontiguousarray(lam[b if lam.shape[0] > 1 else 0])
+        t = np.zeros(5); u = np.zeros((op.K, op.T)); nt = np.zeros(1, np.int64)
+        g1 = np.zeros(op.n); g2 = np.zeros(op.n)
+        rc = lib.orc_loss_grad(C.byref(op.s), _ptr(m), _ptr(s), _ptr(l), float(alpha), float(rho),
+                               float(tie_tol), _ptr(t), _ptr(u),
+                               _ptr(g1) if grad else None, _ptr(g2) if grad else None, _ptr(nt))
+        if rc != OK:
+            raise RuntimeError(f"oracle loss_grad failed: {rc}")
+        terms[b] = t; U[b] = u; gm[b] = g1; gs[b] = g2; ties[b] = nt[0]
+    return terms, U, gm, gs, ties
+
+
+def edge_terms_double_sum(prob, mu, sigma):
+    """(V_dep, L_com, V_rec) from the paper's literal double sums (tiny only)."""
+    lib, op = _load(), _op(prob)
+    m = np.ascontiguousarray(mu, np.float64); s = np.ascontiguousarray(sigma, np.float64)
+    out = np.zeros(3)
+    lib.orc_edge_terms_double_sum(C.byref(op.s), _ptr(m), _ptr(s), _ptr(out))
+    return out
+
+
+def adam(theta, m, v, g, t, lr, b1=0.9, b2=0.999, eps=1e-8):
+    """One Adam step in fp64; returns new (theta, m, v)."""
+    lib = _load()
+    th = np.ascontiguousarray(theta, np.float64).copy()
+    mm = np.ascontiguousarray(m, np.float64).copy()
+    vv = np.ascontiguousarray(v, np.float64).copy()
+    gg = np.ascontiguousarray(g, np.float64)
+    lib.orc_adam(th.size, _ptr(th), _ptr(mm), _ptr(vv), _ptr(gg), int(t), float(lr), float(b1),
+                 float(b2), float(eps))
+    return th, mm, vv
+
+
+def legalize(prob, mu):
+    """Legalize each restart of mu [B,N] float32: (sched int64 [B,N], status [B])."""
+    lib, op = _load(), _op(prob)
+    mu = np.atleast_2d(np.asarray(mu, np.float32))
+    out = np.zeros(mu.shape, np.int64); st = np.zeros(mu.shape[0], np.int32)
+    for b in range(mu.shape[0]):
+        m = np.ascontiguousarray(mu[b]); s = np.zeros(op.n, np.int64)
+        st[b] = lib.orc_legalize(C.byref(op.s), _ptr(m), _ptr(s))
+        out[b] = s
+    return out, st
+
+
+def asap_alap(prob):
+    lib, op = _load(), _op(prob)
+    a = np.zeros(op.n, np.int64); l = np.zeros(op.n, np.int64)
+    rc = lib.orc_asap_alap(C.byref(op.s), _ptr(a), _ptr(l))
+    return a, l, rc
+
+
+def topo(prob):
+    lib, op = _load(), _op(prob)
+    lev = np.zeros(op.n, np.int32); order = np.zeros(op.n, np.int32)
+    rc = lib.orc_topo(C.byref(op.s), _ptr(lev), _ptr(order))
+    return lev, order, rc
+
+
+def init_state(prob, B, u, kappa=1.0 / 6.0, sigma_min=0.05):
+    lib, op = _load(), _op(prob)
+    uu = np.ascontiguousarray(np.broadcast_to(u, (B, op.n)), np.float64)
+    mu = np.zeros((B, op.n)); sg = np.zeros((B, op.n))
+    rc = lib.orc_init_state(C.byref(op.s), int(B), _ptr(uu), float(kappa), float(sigma_min),
+                            _ptr(mu), _ptr(sg))
+    return mu, sg, rc
+
+
+def mass(mu, sigma, d, D):
+    return float(_load().orc_mass(float(mu), float(sigma), int(d), int(D)))

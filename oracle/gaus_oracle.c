@@ -1,0 +1,525 @@
+/*
+ * gaus_oracle.c -- CPU oracle for the Gaussian-relaxed scheduling objective.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the
+ * benchmark's CPU-baseline leg may load or call this code.  It shares no code,
+ * header, table or constant with the GPU library: it is a plain, slow, fp64
+ * restatement of the method of "GauS: Differentiable Scheduling Optimization
+ * via Gaussian Reparameterization" (arXiv 2602.20427), written so that it can
+ * be checked against the paper by eye:
+ *
+ *   - masses P_i^d                : Sec. 3.2, eq:round and its footnote
+ *                                   (bin 0 open to -inf, bin D-1 open to +inf)
+ *   - expected usage              : App. B.2 (Res^), App. B.3 (modulo fold, MRes^)
+ *   - resource violation          : App. B.2, eq:relu
+ *   - dependency violation        : Sec. 3.2, eq:dep (with producer delay)
+ *   - expected edge length        : App. B.1 (L^_Com)
+ *   - recurrence violation        : App. B.3 (V^_Rec, with producer delay)
+ *   - augmented Lagrangian        : Sec. 3.3, eq. (11) and Alg. 1
+ *   - Adam                        : App. C.1 hyper-parameters; Kingma & Ba (2015)
+ *   - legalization                : App. A, Alg. 3 (regular), Alg. 4 (modulo)
+ *
+ * Readings of the paper used here (where it is silent or inconsistent):
+ *   R1  a dependency (i->j) is violated iff d_j < d_i + delta_i; delta = 0 gives
+ *       eq:dep exactly, delta = 1 matches the "+1" of Alg. 3.
+ *   R2  a back edge (j->i, k) (producer j, consumer i) is violated iff
+ *       d_j + delta_j > d_i + k*II; the outer sum runs over all d_i >= 0.
+ *   R5  the modulo fold only includes steps inside [0, D-1].
+ *   R6  each op uses one unit of its own resource type; capacity per type.
+ *   R7  ReLU'(0) = 0 (strict indicator U > C).
+ *   R8  one multiplier per constraint family (dep, res, rec) per restart.
+ *   R12 ASAP/ALAP with delays; sinks' ALAP is D-1 (start steps live in [0,D-1]).
+ *   R13 Alg. 4 sources get t_min = 0; predecessors contribute s_u + delta_u.
+ *   R14 Alg. 4 first clamps the rounded schedule to [0, D-1]; statuses
+ *       NOT_CONVERGED (pass cap N reached) and OVERFLOW (some s > D-1).
+ *   R4  rounding is half-up: s = floor(mu) + [mu - floor(mu) >= 1/2].
+ *
+ * The gradient is the analytic derivative of the forward below (derived by
+ * writing every term as a function of the CDF values at the D-1 interior bin
+ * edges and applying the chain rule; see orc_loss_grad).  It is pinned against
+ * central finite differences and against fp64 autograd in the tests.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+typedef struct {
+    int32_t n, e;              /* ops, forward edges */
+    const int32_t *row_ptr;    /* [n+1] CSR by producer */
+    const int32_t *col;        /* [e] consumers */
+    const int32_t *delay;      /* [n] Lat(v_i) */
+    const int32_t *rtype;      /* [n] resource type in [0,K) */
+    int32_t K;
+    const double *cap;         /* [K] capacity per type */
+    int32_t D, II;             /* horizon; initiation interval (0 = regular) */
+    int32_t nb;                /* back edges */
+    const int32_t *bsrc;       /* [nb] producer v_j */
+    const int32_t *bdst;       /* [nb] consumer v_i */
+    const int32_t *bdist;      /* [nb] iteration distance k */
+} orc_problem;
+
+enum { ORC_OK = 0, ORC_E_INVALID = 1, ORC_E_CYCLE = 2, ORC_E_HORIZON = 3,
+       ORC_E_NOT_CONVERGED = 4, ORC_E_OVERFLOW = 5, ORC_E_NOMEM = 7 };
+
+int orc_num_threads(void) {
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+/* ---------------------------------------------------------------- Gaussian */
+
+/* standard normal CDF and its upper tail, via the complementary error function */
+static double Phi(double z) { return 0.5 * erfc(-z / M_SQRT2); }
+static double Qtail(double z) { return 0.5 * erfc(z / M_SQRT2); }
+static double phi(double z) { return exp(-0.5 * z * z) / sqrt(2.0 * M_PI); }
+
+/* eq:round: P_i^d = Phi((d+1/2-mu)/sigma) - Phi((d-1/2-mu)/sigma); the lower
+ * limit of bin 0 is -inf and the upper limit of bin D-1 is +inf (footnote).
+ * When both limits lie in the upper half the difference is taken between
+ * upper-tail values, which loses no relative precision. */
+double orc_mass(double mu, double sigma, int32_t d, int32_t D) {
+    double lo = (d == 0) ? -INFINITY : (d - 0.5 - mu) / sigma;
+    double hi = (d == D - 1) ? INFINITY : (d + 0.5 - mu) / sigma;
+    if (lo > 0.0) return Qtail(lo) - Qtail(hi);
+    return Phi(hi) - Phi(lo);
+}
+
+/* CDF of the rounded start step at bin edge t: F(t) = P(d <= t).  Equals the
+ * running sum of the masses up to t (telescoping of eq:round); F(t)=0 for
+ * t < 0 and F(t)=1 for t >= D-1 because of the open end bins. */
+static double cdf_row(const double *F, int64_t u, int32_t D) {
+    if (u < 0) return 0.0;
+    if (u >= D - 1) return 1.0;
+    return F[u];
+}
+
+static double mass_row(const double *P, int64_t a, int32_t D) {
+    if (a < 0 || a > D - 1) return 0.0;
+    return P[a];
+}
+
+/* ------------------------------------------------------------ graph helpers */
+
+typedef struct {
+    int32_t *pred_ptr, *pred;      /* CSC: predecessors of each op */
+    int32_t *bin_ptr, *bin;        /* back edges by consumer (ids into bsrc..) */
+    int32_t *bout_ptr, *bout;      /* back edges by producer */
+} orc_adj;
+
+static void adj_free(orc_adj *a) {
+    free(a->pred_ptr); free(a->pred); free(a->bin_ptr); free(a->bin);
+    free(a->bout_ptr); free(a->bout);
+}
+
+static int adj_build(const orc_problem *p, orc_adj *a) {
+    int32_t n = p->n;
+    memset(a, 0, sizeof(*a));
+    a->pred_ptr = calloc((size_t)n + 1, sizeof(int32_t));
+    a->pred = malloc(sizeof(int32_t) * (size_t)(p->e > 0 ? p->e : 1));
+    a->bin_ptr = calloc((size_t)n + 1, sizeof(int32_t));
+    a->bout_ptr = calloc((size_t)n + 1, sizeof(int32_t));
+    a->bin = malloc(sizeof(int32_t) * (size_t)(p->nb > 0 ? p->nb : 1));
+    a->bout = malloc(sizeof(int32_t) * (size_t)(p->nb > 0 ? p->nb : 1));
+    if (!a->pred_ptr || !a->pred || !a->bin_ptr || !a->bout_ptr || !a->bin || !a->bout) {
+        adj_free(a); return ORC_E_NOMEM;
+    }
+    for (int32_t i = 0; i < n; ++i)
+        for (int32_t e = p->row_ptr[i]; e < p->row_ptr[i + 1]; ++e) a->pred_ptr[p->col[e] + 1]++;
+    for (int32_t i = 0; i < n; ++i) a->pred_ptr[i + 1] += a->pred_ptr[i];
+    int32_t *fill = calloc((size_t)n + 1, sizeof(int32_t));
+    if (!fill) { adj_free(a); return ORC_E_NOMEM; }
+    for (int32_t i = 0; i < n; ++i)              /* producers in id order */
+        for (int32_t e = p->row_ptr[i]; e < p->row_ptr[i + 1]; ++e) {
+            int32_t j = p->col[e];
+            a->pred[a->pred_ptr[j] + fill[j]++] = i;
+        }
+    for (int32_t b = 0; b < p->nb; ++b) { a->bin_ptr[p->bdst[b] + 1]++; a->bout_ptr[p->bsrc[b] + 1]++; }
+    for (int32_t i = 0; i < n; ++i) { a->bin_ptr[i + 1] += a->bin_ptr[i]; a->bout_ptr[i + 1] += a->bout_ptr[i]; }
+    memset(fill, 0, sizeof(int32_t) * ((size_t)n + 1));
+    int32_t *fill2 = calloc((size_t)n + 1, sizeof(int32_t));
+    if (!fill2) { free(fill); adj_free(a); return ORC_E_NOMEM; }
+    for (int32_t b = 0; b < p->nb; ++b) {
+        a->bin[a->bin_ptr[p->bdst[b]] + fill[p->bdst[b]]++] = b;
+        a->bout[a->bout_ptr[p->bsrc[b]] + fill2[p->bsrc[b]]++] = b;
+    }
+    free(fill); free(fill2);
+    return ORC_OK;
+}
+
+/* Kahn's algorithm.  level[v] = 0 for sources, else 1 + max level of its
+ * predecessors; order = ops sorted by (level, id).  Returns ORC_E_CYCLE if the
+ * forward edges are not acyclic. */
+int orc_topo(const orc_problem *p, int32_t *level, int32_t *order) {
+    int32_t n = p->n;
+    orc_adj a;
+    if (adj_build(p, &a)) return ORC_E_NOMEM;
+    int32_t *indeg = malloc(sizeof(int32_t) * (size_t)(n > 0 ? n : 1));
+    int32_t *queue = malloc(sizeof(int32_t) * (size_t)(n > 0 ? n : 1));
+    if (!indeg || !queue) { free(indeg); free(queue); adj_free(&a); return ORC_E_NOMEM; }
+    for (int32_t v = 0; v < n; ++v) { indeg[v] = a.pred_ptr[v + 1] - a.pred_ptr[v]; level[v] = 0; }
+    int32_t head = 0, tail = 0;
+    for (int32_t v = 0; v < n; ++v) if (indeg[v] == 0) queue[tail++] = v;
+    while (head < tail) {
+        int32_t u = queue[head++];
+        for (int32_t e = p->row_ptr[u]; e < p->row_ptr[u + 1]; ++e) {
+            int32_t v = p->col[e];
+            if (level[u] + 1 > level[v]) level[v] = level[u] + 1;
+            if (--indeg[v] == 0) queue[tail++] = v;
+        }
+    }
+    int rc = (tail == n) ? ORC_OK : ORC_E_CYCLE;
+    if (rc == ORC_OK) {
+        /* counting sort by level, ids ascending inside a level */
+        int32_t maxl = 0;
+        for (int32_t v = 0; v < n; ++v) if (level[v] > maxl) maxl = level[v];
+        int32_t *cnt = calloc((size_t)maxl + 2, sizeof(int32_t));
+        if (!cnt) rc = ORC_E_NOMEM;
+        else {
+            for (int32_t v = 0; v < n; ++v) cnt[level[v] + 1]++;
+            for (int32_t l = 0; l <= maxl; ++l) cnt[l + 1] += cnt[l];
+            for (int32_t v = 0; v < n; ++v) order[cnt[level[v]]++] = v;
+            free(cnt);
+        }
+    }
+    free(indeg); free(queue); adj_free(&a);
+    return rc;
+}
+
+/* ASAP / ALAP start steps with delays (reading R12):
+ *   ASAP_v = max over preds u of ASAP_u + delta_u   (0 for sources)
+ *   ALAP_v = min over succs w of ALAP_w - delta_v   (D-1 for sinks)
+ * Returns ORC_E_HORIZON when some ASAP_v > ALAP_v (the critical path does not
+ * fit in D steps). */
+int orc_asap_alap(const orc_problem *p, int64_t *asap, int64_t *alap) {
+    int32_t n = p->n;
+    int32_t *level = malloc(sizeof(int32_t) * (size_t)(n > 0 ? n : 1));
+    int32_t *order = malloc(sizeof(int32_t) * (size_t)(n > 0 ? n : 1));
+    if (!level || !order) { free(level); free(order); return ORC_E_NOMEM; }
+    int rc = orc_topo(p, level, order);
+    if (rc == ORC_OK) {
+        for (int32_t v = 0; v < n; ++v) asap[v] = 0;
+        for (int32_t q = 0; q < n; ++q) {
+            int32_t u = order[q];
+            for (int32_t e = p->row_ptr[u]; e < p->row_ptr[u + 1]; ++e) {
+                int32_t v = p->col[e];
+                if (asap[u] + p->delay[u] > asap[v]) asap[v] = asap[u] + p->delay[u];
+            }
+        }
+        for (int32_t q = n - 1; q >= 0; --q) {
+            int32_t v = order[q];
+            int64_t best = (int64_t)p->D - 1;
+            for (int32_t e = p->row_ptr[v]; e < p->row_ptr[v + 1]; ++e) {
+                int64_t c = alap[p->col[e]] - p->delay[v];
+                if (c < best) best = c;
+            }
+            alap[v] = best;
+        }
+        for (int32_t v = 0; v < n; ++v) if (asap[v] > alap[v]) { rc = ORC_E_HORIZON; break; }
+    }
+    free(level); free(order);
+    return rc;
+}
+
+/* -------------------------------------------------------- forward+backward */
+
+/*
+ * One restart.  Inputs mu, sigma [n] (float32 values promoted to double),
+ * lam[3] = (lambda_dep, lambda_res, lambda_rec).  Outputs:
+ *   terms[5] = (L_total, V_dep, V_res, V_rec, L_com)
+ *   U[K*T]   expected (folded) usage, T = II if II > 0 else D
+ *   g_mu, g_sigma [n]  dL_total/dmu, dL_total/dsigma (may be NULL: forward only)
+ *   n_ties   number of (k, slot) cells with |U - C| < tie_tol * max(1, C)
+ */
+int orc_loss_grad(const orc_problem *p, const double *mu, const double *sigma,
+                  const double *lam, double alpha, double rho, double tie_tol,
+                  double *terms, double *U, double *g_mu, double *g_sigma, int64_t *n_ties) {
+    const int32_t n = p->n, D = p->D, K = p->K, II = p->II;
+    const int32_t T = (II > 0) ? II : D;
+    if (D < 1 || n < 0 || K < 1) return ORC_E_INVALID;
+    orc_adj a;
+    if (adj_build(p, &a)) return ORC_E_NOMEM;
+    /* F[i][t], t = 0..D-2 (interior bin edges); P[i][d], d = 0..D-1 */
+    const int64_t DF = (D > 1) ? D - 1 : 1;
+    double *F = malloc(sizeof(double) * (size_t)n * (size_t)DF + 8);
+    double *P = malloc(sizeof(double) * (size_t)n * (size_t)D + 8);
+    double *vd = calloc((size_t)n + 1, sizeof(double));
+    double *lc = calloc((size_t)n + 1, sizeof(double));
+    double *vr = calloc((size_t)p->nb + 1, sizeof(double));
+    if (!F || !P || !vd || !lc || !vr) {
+        free(F); free(P); free(vd); free(lc); free(vr); adj_free(&a); return ORC_E_NOMEM;
+    }
+
+    /* eq:round masses and the CDF at interior bin edges */
+    #pragma omp parallel for schedule(dynamic, 16)
+    for (int32_t i = 0; i < n; ++i) {
+        for (int32_t t = 0; t < D - 1; ++t) F[(int64_t)i * DF + t] = Phi((t + 0.5 - mu[i]) / sigma[i]);
+        for (int32_t d = 0; d < D; ++d) P[(int64_t)i * D + d] = orc_mass(mu[i], sigma[i], d, D);
+    }
+
+    /* expected usage per type and (modulo) slot: App. B.2 / B.3 */
+    #pragma omp parallel for schedule(dynamic, 4)
+    for (int64_t cell = 0; cell < (int64_t)K * T; ++cell) {
+        int32_t k = (int32_t)(cell / T), s = (int32_t)(cell % T);
+        double acc = 0.0;
+        for (int32_t i = 0; i < n; ++i) {
+            if (p->rtype[i] != k) continue;
+            for (int32_t d = s; d < D; d += T) acc += P[(int64_t)i * D + d];
+        }
+        U[cell] = acc;
+    }
+    double V_res = 0.0;
+    int64_t ties = 0;
+    for (int64_t cell = 0; cell < (int64_t)K * T; ++cell) {
+        double c = p->cap[cell / T];
+        double ex = U[cell] - c;
+        if (ex > 0.0) V_res += ex;                        /* eq:relu */
+        if (fabs(ex) < tie_tol * (c > 1.0 ? c : 1.0)) ties++;
+    }
+
+    /* dependency violations and edge lengths, summed per producer */
+    #pragma omp parallel for schedule(dynamic, 16)
+    for (int32_t i = 0; i < n; ++i) {
+        const double *Pi = P + (int64_t)i * D, *Fi = F + (int64_t)i * DF;
+        double sd = 0.0, sc = 0.0;
+        for (int32_t e = p->row_ptr[i]; e < p->row_ptr[i + 1]; ++e) {
+            const double *Fj = F + (int64_t)p->col[e] * DF;
+            /* P(d_j < d_i + delta_i) = sum_a P_i^a * P(d_j <= a + delta_i - 1) */
+            for (int32_t aa = 0; aa < D; ++aa) sd += Pi[aa] * cdf_row(Fj, (int64_t)aa + p->delay[i] - 1, D);
+            /* E[(d_j - d_i)^+] = sum_t P(d_i <= t) P(d_j > t) */
+            for (int32_t t = 0; t < D - 1; ++t) sc += Fi[t] * (1.0 - Fj[t]);
+        }
+        vd[i] = sd; lc[i] = sc;
+    }
+    /* recurrence violations: P(d_j + delta_j > d_i + k*II) */
+    #pragma omp parallel for schedule(dynamic, 4)
+    for (int32_t b = 0; b < p->nb; ++b) {
+        int32_t j = p->bsrc[b], i = p->bdst[b];
+        int64_t off = (int64_t)p->bdist[b] * II - p->delay[j];
+        const double *Pi = P + (int64_t)i * D, *Fj = F + (int64_t)j * DF;
+        double s = 0.0;
+        for (int32_t aa = 0; aa < D; ++aa) s += Pi[aa] * (1.0 - cdf_row(Fj, aa + off, D));
+        vr[b] = s;
+    }
+    double V_dep = 0.0, L_com = 0.0, V_rec = 0.0;
+    for (int32_t i = 0; i < n; ++i) { V_dep += vd[i]; L_com += lc[i]; }
+    for (int32_t b = 0; b < p->nb; ++b) V_rec += vr[b];
+
+    /* augmented Lagrangian, eq. (11) */
+    double V[3] = {V_dep, V_res, V_rec};
+    double L = alpha * L_com;
+    for (int c = 0; c < 3; ++c) L += lam[c] * V[c] + 0.5 * rho * V[c] * V[c];
+    terms[0] = L; terms[1] = V_dep; terms[2] = V_res; terms[3] = V_rec; terms[4] = L_com;
+    if (n_ties) *n_ties = ties;
+
+    if (g_mu && g_sigma) {
+        const double w_dep = lam[0] + rho * V_dep, w_res = lam[1] + rho * V_res, w_rec = lam[2] + rho * V_rec;
+        #pragma omp parallel
+        {
+            double *G = malloc(sizeof(double) * (size_t)D + 8);
+            #pragma omp for schedule(dynamic, 16)
+            for (int32_t i = 0; i < n; ++i) {
+                const int32_t k = p->rtype[i];
+                /* G(d) = dL/dP_i^d, holding the CDFs of the other ops fixed */
+                for (int32_t d = 0; d < D; ++d) {
+                    double g = (U[(int64_t)k * T + (d % T)] > p->cap[k]) ? w_res : 0.0;
+                    for (int32_t e = p->row_ptr[i]; e < p->row_ptr[i + 1]; ++e)
+                        g += w_dep * cdf_row(F + (int64_t)p->col[e] * DF, (int64_t)d + p->delay[i] - 1, D);
+                    for (int32_t q = a.bin_ptr[i]; q < a.bin_ptr[i + 1]; ++q) {
+                        int32_t b = a.bin[q], j = p->bsrc[b];
+                        int64_t u = (int64_t)d + (int64_t)p->bdist[b] * II - p->delay[j];
+                        g += w_rec * (1.0 - cdf_row(F + (int64_t)j * DF, u, D));
+                    }
+                    G[d] = g;
+                }
+                /* H(t) = dL/dF_i(t) at the interior bin edges t = 0..D-2 */
+                double gm = 0.0, gs = 0.0;
+                for (int32_t t = 0; t < D - 1; ++t) {
+                    double h = G[t] - G[t + 1];   /* P_i^t = F(t)-F(t-1), P_i^{t+1} = F(t+1)-F(t) */
+                    for (int32_t e = p->row_ptr[i]; e < p->row_ptr[i + 1]; ++e)
+                        h += alpha * (1.0 - F[(int64_t)p->col[e] * DF + t]);          /* as producer in L_com */
+                    for (int32_t q = a.pred_ptr[i]; q < a.pred_ptr[i + 1]; ++q) {
+                        int32_t hh = a.pred[q];
+                        h -= alpha * F[(int64_t)hh * DF + t];                           /* as consumer in L_com */
+                        h += w_dep * mass_row(P + (int64_t)hh * D, (int64_t)t - p->delay[hh] + 1, D); /* as consumer in V_dep */
+                    }
+                    for (int32_t q = a.bout_ptr[i]; q < a.bout_ptr[i + 1]; ++q) {      /* as producer in V_rec */
+                        int32_t b = a.bout[q], ic = p->bdst[b];
+                        int64_t aa = (int64_t)t - (int64_t)p->bdist[b] * II + p->delay[i];
+                        h -= w_rec * mass_row(P + (int64_t)ic * D, aa, D);
+                    }
+                    double z = (t + 0.5 - mu[i]) / sigma[i];
+                    double dF_dmu = -phi(z) / sigma[i];
+                    double dF_dsigma = -phi(z) * z / sigma[i];
+                    gm += h * dF_dmu;
+                    gs += h * dF_dsigma;
+                }
+                g_mu[i] = gm; g_sigma[i] = gs;
+            }
+            free(G);
+        }
+    }
+    free(F); free(P); free(vd); free(lc); free(vr); adj_free(&a);
+    return ORC_OK;
+}
+
+/* The paper's formulas written as literal double sums over (d_i, d_j) (with the
+ * producer delay of reading R1/R2).  O(E * D^2): tiny instances only. */
+void orc_edge_terms_double_sum(const orc_problem *p, const double *mu, const double *sigma, double out[3]) {
+    const int32_t D = p->D;
+    double vdep = 0.0, lcom = 0.0, vrec = 0.0;
+    for (int32_t i = 0; i < p->n; ++i)
+        for (int32_t e = p->row_ptr[i]; e < p->row_ptr[i + 1]; ++e) {
+            int32_t j = p->col[e];
+            for (int32_t di = 0; di < D; ++di) {
+                double pi = orc_mass(mu[i], sigma[i], di, D);
+                for (int32_t dj = 0; dj < D; ++dj) {
+                    double pj = orc_mass(mu[j], sigma[j], dj, D);
+                    if (dj < di + p->delay[i]) vdep += pi * pj;        /* eq:dep */
+                    if (dj >= di) lcom += pi * pj * (dj - di);          /* App. B.1 */
+                }
+            }
+        }
+    for (int32_t b = 0; b < p->nb; ++b) {
+        int32_t j = p->bsrc[b], i = p->bdst[b];
+        for (int32_t di = 0; di < D; ++di) {
+            double pi = orc_mass(mu[i], sigma[i], di, D);
+            for (int32_t dj = 0; dj < D; ++dj)
+                if ((int64_t)dj + p->delay[j] > (int64_t)di + (int64_t)p->bdist[b] * p->II)   /* App. B.3 */
+                    vrec += pi * orc_mass(mu[j], sigma[j], dj, D);
+        }
+    }
+    out[0] = vdep; out[1] = lcom; out[2] = vrec;
+}
+
+/* ------------------------------------------------------------------ Adam */
+
+/* One Adam step (Kingma & Ba 2015, bias-corrected, no weight decay) on n
+ * parameters; t is the step number after incrementing (t >= 1). */
+void orc_adam(int64_t n, double *theta, double *m, double *v, const double *g, int32_t t,
+              double lr, double b1, double b2, double eps) {
+    double c1 = 1.0 - pow(b1, t), c2 = 1.0 - pow(b2, t);
+    for (int64_t i = 0; i < n; ++i) {
+        m[i] = b1 * m[i] + (1.0 - b1) * g[i];
+        v[i] = b2 * v[i] + (1.0 - b2) * g[i] * g[i];
+        double mh = m[i] / c1, vh = v[i] / c2;
+        theta[i] -= lr * mh / (sqrt(vh) + eps);
+    }
+}
+
+/* ------------------------------------------------------------ legalization */
+
+/* half-up rounding of a float32 value, after clamping it to [-1, D]; a NaN
+ * is treated as -1 */
+static int64_t round_half_up(float muf, int32_t D) {
+    double m = (double)muf;
+    if (!(m >= -1.0)) m = -1.0;
+    if (m > (double)D) m = (double)D;
+    double fl = floor(m);
+    return (int64_t)fl + ((m - fl) >= 0.5 ? 1 : 0);
+}
+
+/*
+ * Legalize one restart.  mu [n] float32; out s [n] int64; status returned.
+ *   II == 0 : Alg. 3 -- clamp to [ASAP, ALAP], one pass in topological order
+ *             raising s_v to max over preds of s_u + delta_u.
+ *   II >  0 : Alg. 4 -- clamp to [0, D-1], then passes in topological order
+ *             raising s_v to max(t_min, t_back) until a pass changes nothing,
+ *             at most n passes.
+ */
+int orc_legalize(const orc_problem *p, const float *mu, int64_t *s) {
+    const int32_t n = p->n, D = p->D;
+    int32_t *level = malloc(sizeof(int32_t) * (size_t)(n > 0 ? n : 1));
+    int32_t *order = malloc(sizeof(int32_t) * (size_t)(n > 0 ? n : 1));
+    int64_t *asap = malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+    int64_t *alap = malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+    orc_adj a;
+    if (!level || !order || !asap || !alap || adj_build(p, &a)) {
+        free(level); free(order); free(asap); free(alap); return ORC_E_NOMEM;
+    }
+    int rc = orc_topo(p, level, order);
+    if (rc == ORC_OK && p->II == 0) rc = orc_asap_alap(p, asap, alap);
+    if (rc != ORC_OK) { free(level); free(order); free(asap); free(alap); adj_free(&a); return rc; }
+
+    for (int32_t v = 0; v < n; ++v) s[v] = round_half_up(mu[v], D);
+    if (p->II == 0) {
+        for (int32_t v = 0; v < n; ++v) {
+            if (s[v] < asap[v]) s[v] = asap[v];
+            if (s[v] > alap[v]) s[v] = alap[v];
+        }
+        for (int32_t q = 0; q < n; ++q) {
+            int32_t v = order[q];
+            if (a.pred_ptr[v + 1] == a.pred_ptr[v]) continue;
+            int64_t treq = INT64_MIN;
+            for (int32_t r = a.pred_ptr[v]; r < a.pred_ptr[v + 1]; ++r) {
+                int32_t u = a.pred[r];
+                if (s[u] + p->delay[u] > treq) treq = s[u] + p->delay[u];
+            }
+            if (treq > s[v]) s[v] = treq;
+        }
+    } else {
+        for (int32_t v = 0; v < n; ++v) {
+            if (s[v] < 0) s[v] = 0;
+            if (s[v] > D - 1) s[v] = D - 1;
+        }
+        int converged = 0;
+        for (int32_t pass = 0; pass < (n > 0 ? n : 1); ++pass) {
+            int changed = 0;
+            for (int32_t q = 0; q < n; ++q) {
+                int32_t v = order[q];
+                int64_t tmin = 0, tback = 0;
+                for (int32_t r = a.pred_ptr[v]; r < a.pred_ptr[v + 1]; ++r) {
+                    int32_t u = a.pred[r];
+                    if (s[u] + p->delay[u] > tmin) tmin = s[u] + p->delay[u];
+                }
+                for (int32_t r = a.bin_ptr[v]; r < a.bin_ptr[v + 1]; ++r) {
+                    int32_t b = a.bin[r], j = p->bsrc[b];
+                    int64_t c = s[j] + p->delay[j] - (int64_t)p->bdist[b] * p->II;
+                    if (c > tback) tback = c;
+                }
+                int64_t treq = tmin > tback ? tmin : tback;
+                if (treq > s[v]) { s[v] = treq; changed = 1; }
+            }
+            if (!changed) { converged = 1; break; }
+        }
+        if (!converged) rc = ORC_E_NOT_CONVERGED;
+        else {
+            for (int32_t v = 0; v < n; ++v) if (s[v] > D - 1) { rc = ORC_E_OVERFLOW; break; }
+        }
+    }
+    free(level); free(order); free(asap); free(alap); adj_free(&a);
+    return rc;
+}
+
+/* ---------------------------------------------------------- initial state */
+
+/* Paper's initialization (Sec. 3.3 "Initialization", Alg. 1):
+ *   sigma = max(kappa * (ALAP - ASAP), sigma_min)
+ *   mu    = (ASAP + ALAP) / 2 for restart 0; restarts b >= 1 place mu at
+ *           ASAP + u * (ALAP - ASAP) with u ~ U[0,1) given by the caller. */
+int orc_init_state(const orc_problem *p, int32_t B, const double *u, double kappa, double sigma_min,
+                   double *mu, double *sigma) {
+    const int32_t n = p->n;
+    int64_t *asap = malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+    int64_t *alap = malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+    if (!asap || !alap) { free(asap); free(alap); return ORC_E_NOMEM; }
+    int rc = orc_asap_alap(p, asap, alap);
+    if (rc == ORC_OK) {
+        for (int32_t b = 0; b < B; ++b)
+            for (int32_t v = 0; v < n; ++v) {
+                double slack = (double)(alap[v] - asap[v]);
+                double sg = kappa * slack;
+                sigma[(int64_t)b * n + v] = sg > sigma_min ? sg : sigma_min;
+                mu[(int64_t)b * n + v] = (b == 0) ? 0.5 * (double)(asap[v] + alap[v])
+                                                  : (double)asap[v] + u[(int64_t)b * n + v] * slack;
+            }
+    }
+    free(asap); free(alap);
+    return rc;
+}

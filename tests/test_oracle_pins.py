@@ -1,0 +1,483 @@
+"""Pins of the CPU oracle against facts that do not come from the oracle itself.
+
+Each test names the passage of the paper (arXiv 2602.20427) or the piece of
+mathematics it relies on.  A plausible slip in the oracle (a dropped term, a
+wrong sign or index, a transposed operand) breaks at least one of them.
+"""
+import itertools
+import json
+import os
+
+import numpy as np
+import pytest
+
+from paper_2602_20427_amd.workloads import Problem, make_problem
+from oracle import brute
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def tiny_problem(rng, n, D, II=0, n_back=0, max_delay=2, K=2):
+    """Random DAG on ops 0..n-1 (ids are a topological order)."""
+    rows = []
+    for i in range(n):
+        tg = [j for j in range(i + 1, n) if rng.random() < 0.5]
+        rows.append(tg)
+    row_ptr = np.zeros(n + 1, np.int32)
+    row_ptr[1:] = np.cumsum([len(r) for r in rows])
+    col = np.array([j for r in rows for j in r], np.int32)
+    delay = rng.integers(0, max_delay + 1, size=n).astype(np.int32)
+    rtype = rng.integers(0, K, size=n).astype(np.int32)
+    cap = rng.uniform(0.3, 1.5, size=K).astype(np.float32)
+    bs, bd, bk = [], [], []
+    for _ in range(n_back):
+        j = int(rng.integers(1, n)); i = int(rng.integers(0, j))   # no self back edges
+        bs.append(j); bd.append(i); bk.append(int(rng.integers(1, 3)))
+    return Problem(n_ops=n, row_ptr=row_ptr, col_idx=col, delay=delay, rtype=rtype, capacity=cap,
+                   D=D, II=II, back_src=np.array(bs, np.int32), back_dst=np.array(bd, np.int32),
+                   back_dist=np.array(bk, np.int32))
+
+
+def masses(orc, mu, sigma, D):
+    return np.array([[orc.mass(m, s, d, D) for d in range(D)] for m, s in zip(mu, sigma)])
+
+
+# ----------------------------------------------------------------- P1, P2
+
+def test_p1_masses_sum_to_one(orc):
+    """eq:round with the open end bins (footnote of Sec. 3.2): the masses of
+    every op telescope to exactly 1, wherever mu lies."""
+    rng = np.random.default_rng(1)
+    for D in (1, 2, 7, 64):
+        for _ in range(50):
+            mu = rng.uniform(-3 * D - 5, 3 * D + 5)
+            sg = np.exp(rng.uniform(np.log(0.01), np.log(5 * D + 1)))
+            P = [orc.mass(mu, sg, d, D) for d in range(D)]
+            assert min(P) >= 0.0
+            assert abs(sum(P) - 1.0) < 1e-14
+
+
+def test_p2_moments_inside_horizon(orc):
+    """Horizon covers the Gaussian: by Poisson summation the mean of the
+    rounded variable is mu and its variance sigma^2 + 1/12 (Sheppard), up to
+    terms of size exp(-2 pi^2 sigma^2)."""
+    D = 200
+    for mu, sg in [(100.0, 1.0), (73.3, 2.5), (120.77, 4.0), (99.5, 1.7)]:
+        P = np.array([orc.mass(mu, sg, d, D) for d in range(D)])
+        d = np.arange(D)
+        mean = (P * d).sum()
+        var = (P * (d - mean) ** 2).sum()
+        assert abs(mean - mu) < 1e-8
+        assert abs(var - (sg * sg + 1.0 / 12.0)) < 1e-7
+
+
+def test_p2b_mass_is_normal_bin_probability(orc):
+    """eq:round at an interior bin equals the integral of the normal pdf over
+    [d-1/2, d+1/2] (checked by Simpson quadrature, not by erf)."""
+    from math import exp, pi, sqrt
+    mu, sg, D = 5.3, 1.7, 12
+    for d in range(1, D - 1):
+        a, b = d - 0.5, d + 0.5
+        xs = np.linspace(a, b, 2001)
+        f = np.exp(-0.5 * ((xs - mu) / sg) ** 2) / (sg * sqrt(2 * pi))
+        h = (b - a) / 2000
+        simpson = h / 3 * (f[0] + f[-1] + 4 * f[1:-1:2].sum() + 2 * f[2:-1:2].sum())
+        assert abs(orc.mass(mu, sg, d, D) - simpson) < 1e-13
+
+
+# ------------------------------------------------------------- P3, P5
+
+def _sigma0_problem():
+    """Hand-built instance and integer schedule with hand-counted costs
+    (tests/golden/sigma0_hand_counts.json)."""
+    with open(os.path.join(GOLDEN, "sigma0_hand_counts.json")) as f:
+        g = json.load(f)
+    p = Problem(n_ops=g["n"], row_ptr=np.array(g["row_ptr"], np.int32),
+                col_idx=np.array(g["col_idx"], np.int32), delay=np.array(g["delay"], np.int32),
+                rtype=np.array(g["rtype"], np.int32), capacity=np.array(g["capacity"], np.float32),
+                D=g["D"], II=g["II"], back_src=np.array(g["back_src"], np.int32),
+                back_dst=np.array(g["back_dst"], np.int32), back_dist=np.array(g["back_dist"], np.int32))
+    return p, g
+
+
+def test_p3_sigma_to_zero_hand_counts(orc):
+    """sigma -> 0: the relaxed terms become the discrete ones of Sec. 2.1 for
+    the rounded schedule.  The expected values were counted by hand."""
+    p, g = _sigma0_problem()
+    mu = np.array(g["mu"], np.float64)
+    sg = np.full(p.n_ops, 1e-5)
+    terms, U, _, _, _ = orc.loss_grad(p, mu, sg, [0.0, 0.0, 0.0], 0.0, 0.0, grad=False)
+    assert terms[0, 1] == g["expected"]["V_dep"]
+    assert terms[0, 4] == g["expected"]["L_com"]
+    assert terms[0, 3] == g["expected"]["V_rec"]
+    assert np.array_equal(U[0], np.array(g["expected"]["U"], np.float64))
+    assert terms[0, 2] == g["expected"]["V_res"]
+
+
+def test_p3_sigma_to_zero_random(orc):
+    """Same limit on random DAGs: usage is the integer histogram of
+    round-half-up(mu) clamped to the horizon; V_dep, L_com, V_rec count."""
+    rng = np.random.default_rng(3)
+    for trial in range(20):
+        II = [0, 3, 4][trial % 3]
+        p = tiny_problem(rng, 7, 9, II=II, n_back=2 if II else 0)
+        s_int = rng.integers(-2, 11, size=7)
+        frac = rng.uniform(-0.45, 0.45, size=7)
+        mu = s_int + frac
+        sg = np.full(7, 1e-5)
+        terms, U, _, _, _ = orc.loss_grad(p, mu, sg, [0, 0, 0], 0.0, 0.0, grad=False)
+        s = np.clip(s_int, 0, p.D - 1)
+        T = II if II else p.D
+        H = np.zeros((p.n_types, T))
+        for i in range(7):
+            H[p.rtype[i], s[i] % T] += 1
+        src, dst = p.edges()
+        vdep = sum(int(s[b] < s[a] + p.delay[a]) for a, b in zip(src, dst))
+        lcom = sum(max(int(s[b] - s[a]), 0) for a, b in zip(src, dst))
+        vrec = sum(int(s[j] + p.delay[j] > s[i] + k * II)
+                   for j, i, k in zip(p.back_src, p.back_dst, p.back_dist))
+        assert np.array_equal(U[0], H)
+        assert terms[0, 1] == vdep and terms[0, 4] == lcom and terms[0, 3] == vrec
+
+
+def test_p5_feasible_schedule_has_no_violation(orc):
+    """A feasible schedule found by brute force gives V_dep = V_rec = 0 in the
+    sigma -> 0 limit; an infeasible one gives the exact violation count."""
+    rng = np.random.default_rng(5)
+    found = 0
+    for trial in range(40):
+        II = 4 if trial % 2 else 0
+        p = tiny_problem(rng, 4, 5, II=II, n_back=1 if II else 0)
+        for s in itertools.product(range(p.D), repeat=4):
+            if brute.feasible(p, s):
+                mu = np.array(s, np.float64) + 0.2
+                terms, *_ = orc.loss_grad(p, mu, np.full(4, 1e-5), [0, 0, 0], 0.0, 0.0, grad=False)
+                assert terms[0, 1] == 0.0 and terms[0, 3] == 0.0
+                found += 1
+                break
+    assert found > 10
+
+
+# ------------------------------------------------------------- P4, P6
+
+@pytest.mark.parametrize("II,n_back", [(0, 0), (2, 2), (3, 1), (5, 1)])
+def test_p4_brute_force_expectations(orc, II, n_back):
+    """Independence of the operators (Sec. 3.1): enumerate all D^N schedules,
+    weight each by the product of masses and compare the exact expectations of
+    the discrete costs of Sec. 2.1 with the oracle's closed sums."""
+    rng = np.random.default_rng(40 + II)
+    for _ in range(6):
+        N, D = 4, 5
+        p = tiny_problem(rng, N, D, II=II, n_back=n_back)
+        mu = rng.uniform(-1, D, size=N)
+        sg = np.exp(rng.uniform(np.log(0.2), np.log(3.0), size=N))
+        P = masses(orc, mu, sg, D)
+        ex = brute.expectations(p, P)
+        terms, U, *_ = orc.loss_grad(p, mu, sg, [0, 0, 0], 0.0, 0.0, grad=False)
+        assert abs(terms[0, 1] - ex["V_dep"]) < 1e-12
+        assert abs(terms[0, 4] - ex["L_com"]) < 1e-12
+        assert abs(terms[0, 3] - ex["V_rec"]) < 1e-12
+        assert np.abs(U[0] - ex["U"]).max() < 1e-12
+
+
+def test_p6_literal_double_sums(orc):
+    """eq:dep, the L_Com expectation of App. B.1 and V_Rec of App. B.3 written
+    as the printed double sums agree with the oracle's single sums."""
+    rng = np.random.default_rng(6)
+    for trial in range(12):
+        II = [0, 3, 6][trial % 3]
+        p = tiny_problem(rng, 6, 11, II=II, n_back=3 if II else 0, max_delay=3)
+        mu = rng.uniform(-2, 12, size=6)
+        sg = np.exp(rng.uniform(np.log(0.1), np.log(6.0), size=6))
+        terms, *_ = orc.loss_grad(p, mu, sg, [0, 0, 0], 0.0, 0.0, grad=False)
+        ds = orc.edge_terms_double_sum(p, mu, sg)
+        assert abs(terms[0, 1] - ds[0]) < 1e-12
+        assert abs(terms[0, 4] - ds[1]) < 1e-11
+        assert abs(terms[0, 3] - ds[2]) < 1e-12
+
+
+def test_p6_eq_dep_with_zero_delay_is_printed_formula(orc):
+    """With delta = 0 the dependency term is exactly eq:dep as printed:
+    sum over d_i >= 1 and d_j <= d_i - 1 of P_i P_j."""
+    rng = np.random.default_rng(66)
+    p = tiny_problem(rng, 5, 8)
+    p.delay[:] = 0
+    mu = rng.uniform(0, 8, size=5); sg = rng.uniform(0.3, 2.0, size=5)
+    P = masses(orc, mu, sg, 8)
+    src, dst = p.edges()
+    ref = sum(P[i, di] * P[j, dj] for i, j in zip(src, dst) for di in range(1, 8) for dj in range(di))
+    terms, *_ = orc.loss_grad(p, mu, sg, [0, 0, 0], 0.0, 0.0, grad=False)
+    assert abs(terms[0, 1] - ref) < 1e-13
+
+
+# ------------------------------------------------------------------- P7
+
+def _total(orc, p, mu, sg, lam, alpha, rho):
+    terms, *_ = orc.loss_grad(p, mu, sg, lam, alpha, rho, grad=False)
+    return terms[0, 0]
+
+
+@pytest.mark.parametrize("II,n_back", [(0, 0), (4, 2)])
+def test_p7_gradient_finite_differences(orc, II, n_back):
+    """Analytic gradient of the augmented Lagrangian vs central differences of
+    the oracle's own forward, away from ReLU kinks."""
+    rng = np.random.default_rng(70 + II)
+    checked = 0
+    for _ in range(8):
+        p = tiny_problem(rng, 7, 12, II=II, n_back=n_back, max_delay=2)
+        mu = rng.uniform(0, 12, size=7); sg = np.exp(rng.uniform(np.log(0.5), np.log(4.0), size=7))
+        lam = rng.uniform(0.1, 1.0, size=3); alpha, rho = 0.37, 0.2
+        terms, U, gm, gs, ties = orc.loss_grad(p, mu, sg, lam, alpha, rho, tie_tol=1e-3)
+        if ties[0]:
+            continue
+        h = 1e-6
+        fd_m = np.zeros(7); fd_s = np.zeros(7)
+        for i in range(7):
+            e = np.zeros(7); e[i] = h * max(1.0, abs(mu[i]))
+            fd_m[i] = (_total(orc, p, mu + e, sg, lam, alpha, rho) - _total(orc, p, mu - e, sg, lam, alpha, rho)) / (2 * e[i])
+            e = np.zeros(7); e[i] = h * max(1.0, sg[i])
+            fd_s[i] = (_total(orc, p, mu, sg + e, lam, alpha, rho) - _total(orc, p, mu, sg - e, lam, alpha, rho)) / (2 * e[i])
+        scale = max(np.abs(gm[0]).max(), np.abs(gs[0]).max(), 1e-3)
+        assert np.abs(gm[0] - fd_m).max() < 1e-6 * scale + 1e-8
+        assert np.abs(gs[0] - fd_s).max() < 1e-6 * scale + 1e-8
+        checked += 1
+    assert checked >= 4
+
+
+torch = pytest.importorskip("torch")
+
+
+def _torch_total(p, mu, sg, lam, alpha, rho):
+    """The objective written with fp64 torch ops straight from the paper's
+    printed double sums (a second, independent formulation)."""
+    D = p.D
+    d = torch.arange(D, dtype=torch.float64)
+    nd = torch.special.ndtr
+    hi = nd((d[None, :] + 0.5 - mu[:, None]) / sg[:, None])
+    lo = nd((d[None, :] - 0.5 - mu[:, None]) / sg[:, None])
+    hi = torch.cat([hi[:, :-1], torch.ones_like(hi[:, :1])], 1)      # bin D-1 open to +inf
+    lo = torch.cat([torch.zeros_like(lo[:, :1]), lo[:, 1:]], 1)      # bin 0 open to -inf
+    P = hi - lo                                                      # eq:round
+    T = p.II if p.II else D
+    onehot = torch.zeros(p.n_types, p.n_ops, dtype=torch.float64)
+    onehot[torch.as_tensor(p.rtype, dtype=torch.long), torch.arange(p.n_ops)] = 1.0
+    fold = torch.zeros(D, T, dtype=torch.float64)
+    fold[torch.arange(D), torch.arange(D) % T] = 1.0
+    U = onehot @ P @ fold                                            # App. B.2/B.3
+    cap = torch.as_tensor(p.capacity, dtype=torch.float64)[:, None]
+    V_res = torch.relu(U - cap).sum()                                # eq:relu
+    src, dst = p.edges()
+    di = d[:, None]; dj = d[None, :]
+    V_dep = 0; L_com = 0; V_rec = 0
+    for a, b in zip(src, dst):
+        outer = P[a][:, None] * P[b][None, :]
+        V_dep = V_dep + (outer * (dj < di + int(p.delay[a])).double()).sum()   # eq:dep
+        L_com = L_com + (outer * torch.clamp(dj - di, min=0)).sum()             # App. B.1
+    for j, i, k in zip(p.back_src, p.back_dst, p.back_dist):
+        outer = P[i][:, None] * P[j][None, :]                                  # rows d_i, cols d_j
+        V_rec = V_rec + (outer * (dj + int(p.delay[j]) > di + int(k) * p.II).double()).sum()
+    V = [V_dep, V_res, V_rec]
+    L = alpha * L_com
+    for c in range(3):
+        L = L + lam[c] * V[c] + 0.5 * rho * V[c] ** 2                  # eq. (11)
+    return L
+
+
+@pytest.mark.parametrize("II,n_back", [(0, 0), (3, 2), (5, 3)])
+def test_p7_gradient_matches_autograd_of_double_sums(orc, II, n_back):
+    """The oracle's hand-derived backward equals fp64 autograd of the literal
+    double-sum formulation (independent code, independent derivation)."""
+    rng = np.random.default_rng(700 + II)
+    done = 0
+    for _ in range(6):
+        p = tiny_problem(rng, 6, 10, II=II, n_back=n_back, max_delay=3, K=2)
+        mu = rng.uniform(-1, 10, size=6); sg = np.exp(rng.uniform(np.log(0.3), np.log(5.0), size=6))
+        lam = rng.uniform(0.05, 1.0, size=3).tolist(); alpha, rho = 0.29, 0.13
+        terms, U, gm, gs, ties = orc.loss_grad(p, mu, sg, lam, alpha, rho, tie_tol=1e-6)
+        if ties[0]:
+            continue
+        tm = torch.tensor(mu, dtype=torch.float64, requires_grad=True)
+        ts = torch.tensor(sg, dtype=torch.float64, requires_grad=True)
+        L = _torch_total(p, tm, ts, lam, alpha, rho)
+        L.backward()
+        assert abs(L.item() - terms[0, 0]) < 1e-11
+        assert np.abs(tm.grad.numpy() - gm[0]).max() < 1e-10
+        assert np.abs(ts.grad.numpy() - gs[0]).max() < 1e-10
+        done += 1
+    assert done >= 3
+
+
+# ------------------------------------------------------------- P8, P9
+
+def test_p8_usage_conserves_ops(orc):
+    """App. B.3: folding only redistributes mass, so every type's usage sums
+    to its op count, folded or not."""
+    p = make_problem("small", seed=2, n_ops=300)
+    rng = np.random.default_rng(8)
+    mu = rng.uniform(-5, 260, size=300); sg = np.exp(rng.uniform(-1, 3, size=300))
+    for II in (0, 17, 64):
+        p.II = II
+        _, U, *_ = orc.loss_grad(p, mu, sg, [0, 0, 0], 0.0, 0.0, grad=False)
+        counts = np.bincount(p.rtype, minlength=p.n_types)
+        assert np.allclose(U[0].sum(axis=1), counts, atol=1e-9)
+    p.II = 0
+
+
+def test_p9_fold_with_large_II_is_identity(orc):
+    """II >= D: every step is its own slot (App. B.3 with one term)."""
+    rng = np.random.default_rng(9)
+    p = tiny_problem(rng, 6, 10)
+    mu = rng.uniform(0, 10, size=6); sg = rng.uniform(0.3, 3, size=6)
+    _, U0, *_ = orc.loss_grad(p, mu, sg, [0, 0, 0], 0.0, 0.0, grad=False)
+    p.II = 10
+    _, U1, *_ = orc.loss_grad(p, mu, sg, [0, 0, 0], 0.0, 0.0, grad=False)
+    assert np.array_equal(U0, U1)
+    p.II = 13
+    _, U2, *_ = orc.loss_grad(p, mu, sg, [0, 0, 0], 0.0, 0.0, grad=False)
+    assert np.array_equal(U2[0][:, :10], U0[0]) and np.all(U2[0][:, 10:] == 0)
+
+
+# ------------------------------------------------------------- P10, P13, P14
+
+def test_p10_adam_first_step_closed_form(orc):
+    """Kingma & Ba: from m = v = 0, the bias-corrected first step is
+    -lr * g / (|g| + eps)."""
+    rng = np.random.default_rng(10)
+    g = rng.normal(size=50) * 10 ** rng.uniform(-6, 3, size=50)
+    th = rng.normal(size=50)
+    lr, eps = 0.01, 1e-8
+    t2, m2, v2 = orc.adam(th, np.zeros(50), np.zeros(50), g, 1, lr, eps=eps)
+    assert np.allclose(t2 - th, -lr * g / (np.abs(g) + eps), rtol=1e-12, atol=1e-15)
+    assert np.allclose(m2, 0.1 * g) and np.allclose(v2, 0.001 * g * g)
+
+
+def test_p10_adam_second_step(orc):
+    """Second step written out from the published update rule."""
+    g1, g2, th, lr = 0.3, -0.7, 1.0, 0.05
+    t1, m1, v1 = orc.adam(np.array([th]), np.zeros(1), np.zeros(1), np.array([g1]), 1, lr)
+    t2, m2, v2 = orc.adam(t1, m1, v1, np.array([g2]), 2, lr)
+    m = 0.9 * 0.1 * g1 + 0.1 * g2
+    v = 0.999 * 0.001 * g1 * g1 + 0.001 * g2 * g2
+    ref = t1[0] - lr * (m / (1 - 0.81)) / (np.sqrt(v / (1 - 0.999 ** 2)) + 1e-8)
+    assert abs(t2[0] - ref) < 1e-15
+
+
+def test_p13_separated_and_coincident_edges(orc):
+    """Well separated endpoints: E[(d_j-d_i)^+] -> mu_j - mu_i and the
+    violation probability -> 0.  A coincident pair with delta = 0 has
+    P(d_j < d_i) = (1 - sum_d P_d^2) / 2 by symmetry."""
+    p = Problem(n_ops=2, row_ptr=np.array([0, 1, 1], np.int32), col_idx=np.array([1], np.int32),
+                delay=np.array([0, 0], np.int32), rtype=np.array([0, 0], np.int32),
+                capacity=np.array([5.0], np.float32), D=200)
+    terms, *_ = orc.loss_grad(p, np.array([40.0, 160.0]), np.array([2.0, 3.0]), [0, 0, 0], 0, 0, grad=False)
+    assert abs(terms[0, 4] - 120.0) < 1e-9 and terms[0, 1] < 1e-12
+    sg = 2.3
+    terms, *_ = orc.loss_grad(p, np.array([100.2, 100.2]), np.array([sg, sg]), [0, 0, 0], 0, 0, grad=False)
+    P = np.array([orc.mass(100.2, sg, d, 200) for d in range(200)])
+    assert abs(terms[0, 1] - (1 - (P * P).sum()) / 2) < 1e-13
+
+
+def test_p14_isolated_op_below_capacity_has_zero_gradient(orc):
+    """An op with no edges only enters through usage; when no usage cell
+    exceeds capacity its gradient is exactly zero."""
+    rng = np.random.default_rng(14)
+    p = tiny_problem(rng, 5, 12)
+    # append an isolated op 5
+    p = Problem(n_ops=6, row_ptr=np.append(p.row_ptr, p.row_ptr[-1]).astype(np.int32),
+                col_idx=p.col_idx, delay=np.append(p.delay, 1).astype(np.int32),
+                rtype=np.append(p.rtype, 0).astype(np.int32), capacity=np.array([10.0, 10.0], np.float32), D=12)
+    mu = rng.uniform(0, 12, size=6); sg = rng.uniform(0.5, 3, size=6)
+    terms, U, gm, gs, _ = orc.loss_grad(p, mu, sg, [0.5, 0.5, 0.5], 0.3, 0.1)
+    assert terms[0, 2] == 0.0
+    assert gm[0, 5] == 0.0 and gs[0, 5] == 0.0
+
+
+# ------------------------------------------------------------------- P12
+
+def _round_half_up(mu, D):
+    m = np.clip(np.where(np.isnan(mu), -1.0, mu.astype(np.float64)), -1.0, D)
+    return np.floor(m).astype(np.int64) + ((m - np.floor(m)) >= 0.5)
+
+
+def test_rounding_half_up_edges(orc):
+    """Rounding to the nearest step (Sec. 3.2, Sampling) with ties up,
+    computed exactly on the float32 value."""
+    p = Problem(n_ops=1, row_ptr=np.array([0, 0], np.int32), col_idx=np.zeros(0, np.int32),
+                delay=np.array([1], np.int32), rtype=np.array([0], np.int32),
+                capacity=np.array([1.0], np.float32), D=10, II=5)
+    cases = {0.5: 1, 0.49999997: 0, 2.5: 3, 2.4999998: 2, -0.5: 0, -0.50000006: 0, 9.5: 9,
+             1e30: 9, -1e30: 0, float("nan"): 0, 3.0: 3, 8.499999: 8}
+    for m, want in cases.items():
+        s, st = orc.legalize(p, np.array([[m]], np.float32))
+        assert st[0] == 0 and s[0, 0] == want, (m, s)
+
+
+@pytest.mark.parametrize("II", [0, 3, 4])
+def test_p12_legalize_is_least_feasible_schedule(orc, II):
+    """Alg. 3 / Alg. 4 return the componentwise least feasible schedule above
+    the clamped rounding (the update is monotone and inflationary), found here
+    by enumeration; idempotent on feasible input."""
+    rng = np.random.default_rng(120 + II)
+    compared = 0
+    for trial in range(60):
+        n = 5
+        p = tiny_problem(rng, n, 7, II=II, n_back=2 if II else 0, max_delay=2)
+        mu = rng.uniform(-1.5, 8, size=n).astype(np.float32)
+        s, st = orc.legalize(p, mu[None, :])
+        a, l, rc = orc.asap_alap(p)
+        if II == 0:
+            if rc != 0:
+                assert st[0] == 3
+                continue
+            s0 = np.clip(_round_half_up(mu, p.D), a, l)
+            ref = brute.least_feasible_above(p, s0, l)
+            assert st[0] == 0 and ref is not None and np.array_equal(s[0], ref)
+        else:
+            s0 = np.clip(_round_half_up(mu, p.D), 0, p.D - 1)
+            ref = brute.least_feasible_above(p, s0, np.full(n, p.D - 1))
+            if st[0] == 0:
+                assert ref is not None and np.array_equal(s[0], ref)
+            else:
+                assert st[0] in (4, 5) and ref is None
+        if st[0] == 0:
+            assert brute.feasible(p, s[0])
+            s2, st2 = orc.legalize(p, s[0][None, :].astype(np.float32))
+            assert st2[0] == 0 and np.array_equal(s2[0], s[0])
+            compared += 1
+    assert compared >= 20
+
+
+def test_asap_alap_hand_example(orc):
+    """R12 on a hand-checked chain 0 -> 1 -> 3, 0 -> 2 -> 3 with delays 2,1,3,1
+    and D = 10: ASAP = (0,2,2,5), ALAP = (4,8,6,9)."""
+    p = Problem(n_ops=4, row_ptr=np.array([0, 2, 3, 4, 4], np.int32), col_idx=np.array([1, 2, 3, 3], np.int32),
+                delay=np.array([2, 1, 3, 1], np.int32), rtype=np.zeros(4, np.int32),
+                capacity=np.array([1.0], np.float32), D=10)
+    a, l, rc = orc.asap_alap(p)
+    assert rc == 0 and a.tolist() == [0, 2, 2, 5] and l.tolist() == [4, 8, 6, 9]
+    p.D = 6                       # sink's ASAP is 5: the smallest horizon that fits
+    *_, rc = orc.asap_alap(p)
+    assert rc == 0
+    p.D = 5
+    *_, rc = orc.asap_alap(p)
+    assert rc == 3
+
+
+def test_cycle_detected(orc):
+    p = Problem(n_ops=3, row_ptr=np.array([0, 1, 2, 3], np.int32), col_idx=np.array([1, 2, 0], np.int32),
+                delay=np.ones(3, np.int32), rtype=np.zeros(3, np.int32), capacity=np.array([1.0], np.float32), D=10)
+    *_, rc = orc.topo(p)
+    assert rc == 2
+
+
+def test_init_state_paper_rule(orc):
+    """Sec. 3.3 Initialization: mu = (ASAP+ALAP)/2, sigma = kappa (ALAP-ASAP),
+    floored at sigma_min; later restarts draw inside [ASAP, ALAP]."""
+    p = make_problem("small", seed=0, n_ops=200)
+    a, l, rc = orc.asap_alap(p)
+    u = np.random.default_rng(0).random((3, 200))
+    mu, sg, rc2 = orc.init_state(p, 3, u, kappa=1 / 6, sigma_min=0.05)
+    assert rc == 0 and rc2 == 0
+    assert np.allclose(mu[0], (a + l) / 2)
+    assert np.allclose(sg[0], np.maximum((l - a) / 6, 0.05))
+    assert np.all(mu[1:] >= a - 1e-12) and np.all(mu[1:] <= l + 1e-12)
