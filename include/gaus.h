@@ -1,0 +1,174 @@
+/*
+ * gaus.h -- C ABI of libgaus, the MI355X (gfx950) hot path of GauS:
+ * differentiable scheduling by Gaussian reparameterization
+ * (arXiv 2602.20427).
+ *
+ * Each operator v_i of a DAG G=(V,E) has a Gaussian start time
+ * X_i ~ N(mu_i, sigma_i^2) (Sec. 3.1).  Rounding X_i to the nearest step gives
+ * per-step masses P_i^d over the horizon {0..D-1} (Sec. 3.2, eq:round; bin 0
+ * open to -inf, bin D-1 open to +inf).  One iteration, for each of B
+ * independent restarts, evaluates
+ *     L = alpha*L_com + sum_{c in {dep,res,rec}} (lambda_c V_c + rho/2 V_c^2)
+ * (augmented Lagrangian, Sec. 3.3 eq. (11)), with
+ *     V_res = sum_k sum_t ReLU(U_k(t) - C_k)          (App. B.2 eq:relu; usage
+ *             U folded modulo II when II > 0, App. B.3)
+ *     V_dep = expected violated dependencies          (Sec. 3.2 eq:dep; edge
+ *             (i->j) violated iff d_j < d_i + Lat(v_i))
+ *     V_rec = expected violated recurrences           (App. B.3; back edge
+ *             (j->i,k) violated iff d_j + Lat(v_j) > d_i + k*II)
+ *     L_com = expected total edge length E[(d_j-d_i)^+]  (App. B.1)
+ * its exact gradient w.r.t. (mu, sigma), and an Adam update (App. C.1), then
+ * lambda_c <- lambda_c + rho*V_c (Alg. 1).  Legalization turns rounded means
+ * into feasible integer schedules (App. A, Alg. 3 and Alg. 4).
+ *
+ * Conventions for every entry point:
+ *   - Every entry returns a gaus_status; nothing aborts or throws across the
+ *     ABI.  gaus_last_error() gives a per-context message.
+ *   - Op ids are the caller's.  The library may reorder internally but every
+ *     output is indexed by the caller's ids.
+ *   - "device" pointers are HIP device memory on the device that was current
+ *     at gaus_init; "host" pointers are ordinary host memory.
+ *   - Device work is enqueued on the stream given to gaus_init and is
+ *     asynchronous unless stated otherwise.  Device faults surface as
+ *     GAUS_E_DEVICE at the next synchronizing call.
+ *   - A context is used by one host thread at a time; distinct contexts are
+ *     independent.
+ */
+#ifndef GAUS_H
+#define GAUS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct gaus_ctx gaus_ctx;
+
+typedef enum {
+    GAUS_OK = 0,
+    GAUS_E_INVALID_ARG = 1,    /* bad pointer, size, range or CSR structure */
+    GAUS_E_CYCLE = 2,          /* forward edges are not acyclic */
+    GAUS_E_HORIZON = 3,        /* critical path does not fit: some ASAP > ALAP */
+    GAUS_E_NOT_CONVERGED = 4,  /* modulo legalization hit its pass cap (N passes) */
+    GAUS_E_OVERFLOW = 5,       /* legalized start step beyond D-1 */
+    GAUS_E_DEVICE = 6,         /* HIP runtime / kernel error */
+    GAUS_E_NOMEM = 7           /* host or device allocation failed */
+} gaus_status;
+
+/* Problem statement (Sec. 2.1).  All pointers are HOST memory, read only
+ * during gaus_init (copied); the caller may free them afterwards. */
+typedef struct {
+    int32_t n_ops;             /* N >= 1 */
+    int32_t n_edges;           /* E >= 0 */
+    const int32_t *row_ptr;    /* [N+1] CSR by producer: row_ptr[0]=0, nondecreasing, row_ptr[N]=E */
+    const int32_t *col_idx;    /* [E] consumer of each edge, in [0,N); the graph must be acyclic */
+    const int32_t *delay;      /* [N] Lat(v_i), 0 <= Lat <= 2^20 */
+    const int32_t *rtype;      /* [N] resource type in [0,K); each op uses one unit of it */
+    int32_t n_types;           /* K >= 1 */
+    const float *capacity;     /* [K] capacity C_k per step (or per modulo slot), finite, >= 0 */
+    int32_t D;                 /* horizon: start steps in [0, D-1]; 1 <= D <= 2^22 */
+    int32_t II;                /* 0 = regular scheduling; > 0 = fold usage modulo II */
+    int32_t n_back;            /* number of back edges; must be 0 when II == 0 */
+    const int32_t *back_src;   /* [n_back] producer v_j of each back edge */
+    const int32_t *back_dst;   /* [n_back] consumer v_i (!= v_j) */
+    const int32_t *back_dist;  /* [n_back] iteration distance k >= 1, k*II <= 2^30 */
+} gaus_problem;
+
+/* Hyper-parameters.  gaus_default_hparams() fills the paper's values
+ * (App. C.1: Adam lr 1e-2, rho 1e-4, kappa 1/6; Sec. 3.3: lambda0 1e-6) and
+ * this library's choices for the unstated ones (Adam betas/eps as in
+ * Kingma & Ba, alpha_com 0.01, sigma_min 0.05). */
+typedef struct {
+    float lr, beta1, beta2, eps;   /* Adam */
+    float rho;                     /* ALM penalty */
+    float lambda0;                 /* initial multipliers */
+    float alpha_com;               /* weight alpha of the expected edge length L_com */
+    float sigma_min;               /* sigma is clamped to >= sigma_min after each update */
+    float kappa;                   /* initial sigma = kappa * (ALAP - ASAP) */
+} gaus_hparams;
+
+void gaus_default_hparams(gaus_hparams *hp);
+
+/* Validate and preprocess a problem for B restarts, allocate device copies and
+ * workspace on the current HIP device.  hip_stream is a hipStream_t (NULL =
+ * default stream).  Synchronous.  On failure *out is set to NULL and nothing
+ * is allocated; the message is available from gaus_last_error(NULL).
+ * Errors: INVALID_ARG, CYCLE, HORIZON, NOMEM, DEVICE. */
+gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp, int32_t B,
+                      void *hip_stream, gaus_ctx **out);
+
+/* Bind the optimizer state used by gaus_step / gaus_adam_from_grad.  All
+ * DEVICE pointers, owned by the caller (the library never frees them) and
+ * kept for the context's lifetime or until re-bound:
+ *   mu, sigma  [B][N] float;  adam_m, adam_v [2][B][N] float (0 = mu, 1 = sigma);
+ *   lambda     [B][3] float (dep, res, rec);  adam_t [1] int32 (steps taken). */
+gaus_status gaus_bind_state(gaus_ctx *ctx, float *mu, float *sigma, float *adam_m, float *adam_v,
+                            float *lambda, int32_t *adam_t);
+
+/* One forward + backward at (mu, sigma) with multipliers lambda, for all B
+ * restarts.  Inputs DEVICE: mu, sigma [B][N], lambda [B][3].  Outputs DEVICE:
+ * terms [B][5] = (L, V_dep, V_res, V_rec, L_com), grad_mu, grad_sigma [B][N]
+ * (dL/dmu, dL/dsigma).  Asynchronous.  Errors: INVALID_ARG (null pointer). */
+gaus_status gaus_loss_grad(gaus_ctx *ctx, const float *mu, const float *sigma, const float *lambda,
+                           float *terms, float *grad_mu, float *grad_sigma);
+
+/* n_iters iterations of Alg. 1's update on the bound state: forward,
+ * backward, Adam on mu and sigma, sigma <- max(sigma, sigma_min),
+ * lambda_c <- lambda_c + rho * V_c (this iteration's V), adam_t += 1.
+ * terms_last (DEVICE [B][5] or NULL) receives the last iteration's terms.
+ * Asynchronous.  Errors: INVALID_ARG (state not bound, n_iters < 0). */
+gaus_status gaus_step(gaus_ctx *ctx, int32_t n_iters, float *terms_last);
+
+/* The update half of gaus_step from a given gradient: Adam on the bound
+ * (mu, sigma) with g_mu, g_sigma (DEVICE [B][N]), the sigma clamp, and
+ * lambda_c += rho * terms[b][1+c] with terms DEVICE [B][5]; adam_t += 1.
+ * Asynchronous.  Used to check the optimizer step on its own. */
+gaus_status gaus_adam_from_grad(gaus_ctx *ctx, const float *g_mu, const float *g_sigma,
+                                const float *terms);
+
+/* Round each restart's means half-up to integer steps and legalize them
+ * (App. A): II == 0 -> Alg. 3 (clamp to [ASAP, ALAP], one topological pass
+ * raising s_v to max over preds u of s_u + Lat(u)); II > 0 -> Alg. 4 (clamp to
+ * [0, D-1], passes raising s_v to max(t_min, t_back) until none changes, at
+ * most N passes).  mu DEVICE [B][N]; sched DEVICE [B][N] int32 (values above
+ * INT32_MAX are saturated); status HOST [B] receives GAUS_OK,
+ * GAUS_E_NOT_CONVERGED or GAUS_E_OVERFLOW per restart.  Synchronizes. */
+gaus_status gaus_legalize(gaus_ctx *ctx, const float *mu, int32_t *sched, int32_t *status);
+
+/* Paper initialization (Sec. 3.3, Alg. 1): sigma = max(kappa*(ALAP-ASAP),
+ * sigma_min); restart 0 gets mu = (ASAP+ALAP)/2, restart b >= 1 gets
+ * mu = ASAP + u[b][i]*(ALAP-ASAP) with u HOST [B][N] double in [0,1) (may be
+ * NULL when B == 1).  mu, sigma DEVICE [B][N].  Synchronizes. */
+gaus_status gaus_init_state(gaus_ctx *ctx, const double *u, float *mu, float *sigma);
+
+/* ASAP / ALAP start steps with delays (ASAP of sources 0, ALAP of sinks D-1).
+ * asap, alap HOST [N].  Host only. */
+gaus_status gaus_asap_alap(const gaus_ctx *ctx, int32_t *asap, int32_t *alap);
+
+/* Expected usage U [B][K][T] (T = II if II > 0 else D) of the last forward
+ * pass, copied to DEVICE memory U.  Asynchronous. */
+gaus_status gaus_get_usage(gaus_ctx *ctx, float *U);
+
+/* Wait for all work enqueued by this context; reports device errors. */
+gaus_status gaus_sync(gaus_ctx *ctx);
+
+/* Problem sizes after preprocessing: N, E, K, D, II, T, n_back, B. */
+gaus_status gaus_get_dims(const gaus_ctx *ctx, int32_t dims[8]);
+
+/* Message of the last failed call on ctx (or of the last failed gaus_init
+ * when ctx is NULL).  Never NULL. */
+const char *gaus_last_error(const gaus_ctx *ctx);
+
+/* Static name of a status code. */
+const char *gaus_status_string(gaus_status s);
+
+/* Release the context's device copies and workspace (not the caller's
+ * buffers).  Synchronizes the stream first.  NULL is ignored. */
+void gaus_destroy(gaus_ctx *ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GAUS_H */

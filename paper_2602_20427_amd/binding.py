@@ -1,0 +1,227 @@
+"""Thin ctypes binding of libgaus (include/gaus.h).
+
+Argument marshalling only: every step of the scheduling hot path runs in the
+gfx950 kernels of libgaus.so.  Device buffers are torch tensors on the current
+HIP device; their data pointers and the current HIP stream are handed to the
+library.  If the library has not been built this module raises on first use:
+there is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libgaus.so")
+
+OK, E_INVALID_ARG, E_CYCLE, E_HORIZON, E_NOT_CONVERGED, E_OVERFLOW, E_DEVICE, E_NOMEM = range(8)
+
+# symbols declared in include/gaus.h
+EXPORTS = ("gaus_default_hparams", "gaus_init", "gaus_bind_state", "gaus_loss_grad", "gaus_step",
+           "gaus_adam_from_grad", "gaus_legalize", "gaus_init_state", "gaus_asap_alap",
+           "gaus_get_usage", "gaus_sync", "gaus_get_dims", "gaus_last_error", "gaus_status_string",
+           "gaus_destroy")
+
+
+class GausError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{_status_name(status)}: {msg}")
+        self.status = status
+
+
+class _Problem(C.Structure):
+    _fields_ = [("n_ops", C.c_int32), ("n_edges", C.c_int32), ("row_ptr", C.c_void_p),
+                ("col_idx", C.c_void_p), ("delay", C.c_void_p), ("rtype", C.c_void_p),
+                ("n_types", C.c_int32), ("capacity", C.c_void_p), ("D", C.c_int32), ("II", C.c_int32),
+                ("n_back", C.c_int32), ("back_src", C.c_void_p), ("back_dst", C.c_void_p),
+                ("back_dist", C.c_void_p)]
+
+
+class HParams(C.Structure):
+    _fields_ = [("lr", C.c_float), ("beta1", C.c_float), ("beta2", C.c_float), ("eps", C.c_float),
+                ("rho", C.c_float), ("lambda0", C.c_float), ("alpha_com", C.c_float),
+                ("sigma_min", C.c_float), ("kappa", C.c_float)]
+
+
+_lib = None
+
+
+def load():
+    """Load libgaus.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                           "(hipcc --offload-arch=gfx950); there is no CPU fallback")
+    lib = C.CDLL(LIB_PATH)
+    vp, i32 = C.c_void_p, C.c_int32
+    sig = {
+        "gaus_default_hparams": ([C.POINTER(HParams)], None),
+        "gaus_init": ([C.POINTER(_Problem), C.POINTER(HParams), i32, vp, C.POINTER(vp)], C.c_int),
+        "gaus_bind_state": ([vp] * 7, C.c_int),
+        "gaus_loss_grad": ([vp] * 7, C.c_int),
+        "gaus_step": ([vp, i32, vp], C.c_int),
+        "gaus_adam_from_grad": ([vp] * 4, C.c_int),
+        "gaus_legalize": ([vp] * 4, C.c_int),
+        "gaus_init_state": ([vp] * 4, C.c_int),
+        "gaus_asap_alap": ([vp] * 3, C.c_int),
+        "gaus_get_usage": ([vp] * 2, C.c_int),
+        "gaus_sync": ([vp], C.c_int),
+        "gaus_get_dims": ([vp, vp], C.c_int),
+        "gaus_last_error": ([vp], C.c_char_p),
+        "gaus_status_string": ([C.c_int], C.c_char_p),
+        "gaus_destroy": ([vp], None),
+    }
+    for name, (args, res) in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = res
+    _lib = lib
+    return lib
+
+
+def _status_name(s: int) -> str:
+    try:
+        return load().gaus_status_string(int(s)).decode()
+    except Exception:
+        return str(s)
+
+
+def default_hparams() -> HParams:
+    hp = HParams()
+    load().gaus_default_hparams(C.byref(hp))
+    return hp
+
+
+def _np_ptr(a: np.ndarray):
+    return a.ctypes.data_as(C.c_void_p)
+
+
+def _dptr(t, dtype, shape, name):
+    import torch
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise TypeError(f"{name}: expected a device tensor")
+    if t.dtype != dtype or tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+        raise ValueError(f"{name}: expected contiguous {dtype} {tuple(shape)}, got {t.dtype} {tuple(t.shape)}")
+    return C.c_void_p(t.data_ptr())
+
+
+class Context:
+    """One gaus_ctx: a validated problem on the current device for B restarts."""
+
+    def __init__(self, problem, B: int, hparams: HParams | None = None, stream=None):
+        import torch
+        lib = load()
+        self._arrays = [np.ascontiguousarray(problem.row_ptr, np.int32),
+                        np.ascontiguousarray(problem.col_idx, np.int32),
+                        np.ascontiguousarray(problem.delay, np.int32),
+                        np.ascontiguousarray(problem.rtype, np.int32),
+                        np.ascontiguousarray(problem.capacity, np.float32),
+                        np.ascontiguousarray(problem.back_src, np.int32),
+                        np.ascontiguousarray(problem.back_dst, np.int32),
+                        np.ascontiguousarray(problem.back_dist, np.int32)]
+        rp, col, dl, rt, cap, bs, bd, bk = self._arrays
+        self._p = _Problem(int(problem.n_ops), int(rp[-1]), _np_ptr(rp), _np_ptr(col), _np_ptr(dl),
+                           _np_ptr(rt), int(cap.shape[0]), _np_ptr(cap), int(problem.D), int(problem.II),
+                           int(bs.shape[0]), _np_ptr(bs), _np_ptr(bd), _np_ptr(bk))
+        self.hp = hparams if hparams is not None else default_hparams()
+        self.B = int(B)
+        if stream is None:
+            stream = torch.cuda.current_stream()
+        self.stream = stream
+        h = C.c_void_p()
+        st = lib.gaus_init(C.byref(self._p), C.byref(self.hp), self.B, C.c_void_p(stream.cuda_stream),
+                           C.byref(h))
+        if st != OK:
+            raise GausError(st, lib.gaus_last_error(None).decode())
+        self._h = h
+        dims = np.zeros(8, np.int32)
+        self._check(lib.gaus_get_dims(self._h, _np_ptr(dims)))
+        self.N, self.E, self.K, self.D, self.II, self.T, self.n_back, _ = (int(x) for x in dims)
+
+    def _check(self, st):
+        if st != OK:
+            raise GausError(st, load().gaus_last_error(self._h).decode())
+
+    def close(self):
+        if getattr(self, "_h", None):
+            load().gaus_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # --- entry points (same names as the C ABI, without the prefix) ---
+    def bind_state(self, mu, sigma, adam_m, adam_v, lam, adam_t):
+        import torch
+        B, N = self.B, self.N
+        f = torch.float32
+        self._bound = (mu, sigma, adam_m, adam_v, lam, adam_t)
+        self._check(load().gaus_bind_state(
+            self._h, _dptr(mu, f, (B, N), "mu"), _dptr(sigma, f, (B, N), "sigma"),
+            _dptr(adam_m, f, (2, B, N), "adam_m"), _dptr(adam_v, f, (2, B, N), "adam_v"),
+            _dptr(lam, f, (B, 3), "lambda"), _dptr(adam_t, torch.int32, (1,), "adam_t")))
+
+    def loss_grad(self, mu, sigma, lam, terms, grad_mu, grad_sigma):
+        import torch
+        B, N = self.B, self.N
+        f = torch.float32
+        self._check(load().gaus_loss_grad(
+            self._h, _dptr(mu, f, (B, N), "mu"), _dptr(sigma, f, (B, N), "sigma"),
+            _dptr(lam, f, (B, 3), "lambda"), _dptr(terms, f, (B, 5), "terms"),
+            _dptr(grad_mu, f, (B, N), "grad_mu"), _dptr(grad_sigma, f, (B, N), "grad_sigma")))
+
+    def step(self, n_iters: int, terms_last=None):
+        import torch
+        tp = None if terms_last is None else _dptr(terms_last, torch.float32, (self.B, 5), "terms_last")
+        self._check(load().gaus_step(self._h, int(n_iters), tp))
+
+    def adam_from_grad(self, g_mu, g_sigma, terms):
+        import torch
+        B, N = self.B, self.N
+        f = torch.float32
+        self._check(load().gaus_adam_from_grad(
+            self._h, _dptr(g_mu, f, (B, N), "g_mu"), _dptr(g_sigma, f, (B, N), "g_sigma"),
+            _dptr(terms, f, (B, 5), "terms")))
+
+    def legalize(self, mu, sched):
+        """Returns the per-restart status array (host)."""
+        import torch
+        status = np.zeros(self.B, np.int32)
+        self._check(load().gaus_legalize(self._h, _dptr(mu, torch.float32, (self.B, self.N), "mu"),
+                                         _dptr(sched, torch.int32, (self.B, self.N), "sched"),
+                                         _np_ptr(status)))
+        return status
+
+    def init_state(self, mu, sigma, u=None):
+        import torch
+        B, N = self.B, self.N
+        uu = None
+        if u is not None:
+            uu = np.ascontiguousarray(np.broadcast_to(u, (B, N)), np.float64)
+        self._check(load().gaus_init_state(self._h, None if uu is None else _np_ptr(uu),
+                                           _dptr(mu, torch.float32, (B, N), "mu"),
+                                           _dptr(sigma, torch.float32, (B, N), "sigma")))
+
+    def asap_alap(self):
+        a = np.zeros(self.N, np.int32)
+        l = np.zeros(self.N, np.int32)
+        self._check(load().gaus_asap_alap(self._h, _np_ptr(a), _np_ptr(l)))
+        return a, l
+
+    def get_usage(self, U):
+        import torch
+        self._check(load().gaus_get_usage(self._h, _dptr(U, torch.float32, (self.B, self.K, self.T), "U")))
+
+    def sync(self):
+        self._check(load().gaus_sync(self._h))
+
+
+def init_error() -> str:
+    return load().gaus_last_error(None).decode()

@@ -1,0 +1,471 @@
+// Host side of libgaus: problem validation and preprocessing, device buffers,
+// launch configuration and the extern "C" entry points declared in gaus.h.
+#include "../../include/gaus.h"
+#include "gaus_internal.h"
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+using namespace gaus;
+
+namespace {
+
+thread_local std::string g_init_error = "no error";
+
+
+}  // namespace
+
+struct gaus_ctx {
+    Graph g{};
+    Work w{};
+    HP hp{};
+    LaunchCfg lc{};
+    hipStream_t stream = nullptr;
+    int device = 0;
+    std::vector<void *> allocs;
+    std::vector<int> asap, alap;
+    std::string err = "no error";
+    // bound optimizer state (caller-owned device memory)
+    float *mu = nullptr, *sigma = nullptr, *m = nullptr, *v = nullptr, *lambda = nullptr;
+    int *adam_t = nullptr;
+    bool bound = false;
+};
+
+namespace {
+
+gaus_status fail(gaus_ctx *c, gaus_status s, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    if (c) c->err = buf;
+    else g_init_error = buf;
+    return s;
+}
+
+gaus_status hip_fail(gaus_ctx *c, hipError_t e, const char *what) {
+    return fail(c, GAUS_E_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+void free_all(gaus_ctx *c) {
+    for (void *p : c->allocs) (void)hipFree(p);
+    c->allocs.clear();
+}
+
+template <class T>
+gaus_status dalloc(gaus_ctx *c, T **out, size_t count) {
+    void *p = nullptr;
+    const size_t bytes = std::max<size_t>(count, 1) * sizeof(T);
+    hipError_t e = hipMalloc(&p, bytes);
+    if (e != hipSuccess) return fail(nullptr, GAUS_E_NOMEM, "hipMalloc(%zu bytes): %s", bytes, hipGetErrorString(e));
+    c->allocs.push_back(p);
+    *out = static_cast<T *>(p);
+    return GAUS_OK;
+}
+
+template <class T>
+gaus_status dupload(gaus_ctx *c, const T **out, const std::vector<T> &h) {
+    T *d = nullptr;
+    gaus_status s = dalloc(c, &d, h.size());
+    if (s != GAUS_OK) return s;
+    if (!h.empty()) {
+        hipError_t e = hipMemcpy(d, h.data(), h.size() * sizeof(T), hipMemcpyHostToDevice);
+        if (e != hipSuccess) return fail(nullptr, GAUS_E_DEVICE, "hipMemcpy: %s", hipGetErrorString(e));
+    }
+    *out = d;
+    return GAUS_OK;
+}
+
+// Preprocessed host copy of a validated problem.
+struct HostGraph {
+    int N = 0, E = 0, K = 0, D = 0, II = 0, nb = 0;
+    std::vector<int> row_ptr, col, delay, rtype, bsrc, bdst, bdist;
+    std::vector<float> cap;
+    std::vector<int> pred_ptr, pred_eid, pred_src;
+    std::vector<int> bin_ptr, bin, bout_ptr, bout;
+    std::vector<int> level, lvl_ptr, lvl_ops;
+    std::vector<int> asap, alap;
+    std::vector<int> perm, grp_start, type_grp;
+};
+
+gaus_status validate(const gaus_problem *p, int32_t B) {
+    if (!p) return fail(nullptr, GAUS_E_INVALID_ARG, "problem is NULL");
+    if (p->n_ops < 1) return fail(nullptr, GAUS_E_INVALID_ARG, "n_ops must be >= 1 (got %d)", p->n_ops);
+    if (p->n_edges < 0) return fail(nullptr, GAUS_E_INVALID_ARG, "n_edges must be >= 0");
+    if (p->n_types < 1) return fail(nullptr, GAUS_E_INVALID_ARG, "n_types must be >= 1");
+    if (p->D < 1 || p->D > (1 << 22)) return fail(nullptr, GAUS_E_INVALID_ARG, "D must be in [1, 2^22] (got %d)", p->D);
+    if (p->II < 0) return fail(nullptr, GAUS_E_INVALID_ARG, "II must be >= 0");
+    if (p->n_back < 0) return fail(nullptr, GAUS_E_INVALID_ARG, "n_back must be >= 0");
+    if (p->n_back > 0 && p->II == 0) return fail(nullptr, GAUS_E_INVALID_ARG, "back edges require II > 0");
+    if (B < 1 || B > 65535) return fail(nullptr, GAUS_E_INVALID_ARG, "B must be in [1, 65535] (got %d)", B);
+    if (!p->row_ptr || !p->delay || !p->rtype || !p->capacity || (p->n_edges > 0 && !p->col_idx) ||
+        (p->n_back > 0 && (!p->back_src || !p->back_dst || !p->back_dist)))
+        return fail(nullptr, GAUS_E_INVALID_ARG, "null array pointer in problem");
+    const int N = p->n_ops;
+    if (p->row_ptr[0] != 0 || p->row_ptr[N] != p->n_edges)
+        return fail(nullptr, GAUS_E_INVALID_ARG, "row_ptr must start at 0 and end at n_edges");
+    for (int i = 0; i < N; ++i)
+        if (p->row_ptr[i + 1] < p->row_ptr[i]) return fail(nullptr, GAUS_E_INVALID_ARG, "row_ptr decreases at %d", i);
+    for (int e = 0; e < p->n_edges; ++e)
+        if (p->col_idx[e] < 0 || p->col_idx[e] >= N) return fail(nullptr, GAUS_E_INVALID_ARG, "col_idx[%d] out of range", e);
+    for (int i = 0; i < N; ++i) {
+        if (p->delay[i] < 0 || p->delay[i] > (1 << 20)) return fail(nullptr, GAUS_E_INVALID_ARG, "delay[%d] out of [0, 2^20]", i);
+        if (p->rtype[i] < 0 || p->rtype[i] >= p->n_types) return fail(nullptr, GAUS_E_INVALID_ARG, "rtype[%d] out of range", i);
+    }
+    for (int k = 0; k < p->n_types; ++k)
+        if (!std::isfinite(p->capacity[k]) || p->capacity[k] < 0.0f)
+            return fail(nullptr, GAUS_E_INVALID_ARG, "capacity[%d] must be finite and >= 0", k);
+    for (int e = 0; e < p->n_back; ++e) {
+        const int j = p->back_src[e], i = p->back_dst[e], k = p->back_dist[e];
+        if (j < 0 || j >= N || i < 0 || i >= N) return fail(nullptr, GAUS_E_INVALID_ARG, "back edge %d: op out of range", e);
+        if (i == j) return fail(nullptr, GAUS_E_INVALID_ARG, "back edge %d is a self loop (Lat <= k*II is a static check)", e);
+        if (k < 1 || (long long)k * p->II > (1LL << 30)) return fail(nullptr, GAUS_E_INVALID_ARG, "back edge %d: need 1 <= k, k*II <= 2^30", e);
+    }
+    return GAUS_OK;
+}
+
+gaus_status preprocess(const gaus_problem *p, HostGraph &h) {
+    const int N = p->n_ops, E = p->n_edges;
+    h.N = N; h.E = E; h.K = p->n_types; h.D = p->D; h.II = p->II; h.nb = p->n_back;
+    h.row_ptr.assign(p->row_ptr, p->row_ptr + N + 1);
+    h.col.assign(p->col_idx, p->col_idx + E);
+    h.delay.assign(p->delay, p->delay + N);
+    h.rtype.assign(p->rtype, p->rtype + N);
+    h.cap.assign(p->capacity, p->capacity + h.K);
+    h.bsrc.assign(p->back_src, p->back_src + h.nb);
+    h.bdst.assign(p->back_dst, p->back_dst + h.nb);
+    h.bdist.assign(p->back_dist, p->back_dist + h.nb);
+
+    // CSC (predecessors in producer-id order, with the CSR edge id)
+    h.pred_ptr.assign(N + 1, 0);
+    for (int e = 0; e < E; ++e) h.pred_ptr[h.col[e] + 1]++;
+    for (int i = 0; i < N; ++i) h.pred_ptr[i + 1] += h.pred_ptr[i];
+    h.pred_eid.assign(E, 0); h.pred_src.assign(E, 0);
+    {
+        std::vector<int> fill(N, 0);
+        for (int i = 0; i < N; ++i)
+            for (int e = h.row_ptr[i]; e < h.row_ptr[i + 1]; ++e) {
+                const int j = h.col[e];
+                const int q = h.pred_ptr[j] + fill[j]++;
+                h.pred_eid[q] = e; h.pred_src[q] = i;
+            }
+    }
+    // back edges by consumer and by producer
+    h.bin_ptr.assign(N + 1, 0); h.bout_ptr.assign(N + 1, 0);
+    for (int e = 0; e < h.nb; ++e) { h.bin_ptr[h.bdst[e] + 1]++; h.bout_ptr[h.bsrc[e] + 1]++; }
+    for (int i = 0; i < N; ++i) { h.bin_ptr[i + 1] += h.bin_ptr[i]; h.bout_ptr[i + 1] += h.bout_ptr[i]; }
+    h.bin.assign(h.nb, 0); h.bout.assign(h.nb, 0);
+    {
+        std::vector<int> f1(N, 0), f2(N, 0);
+        for (int e = 0; e < h.nb; ++e) {
+            h.bin[h.bin_ptr[h.bdst[e]] + f1[h.bdst[e]]++] = e;
+            h.bout[h.bout_ptr[h.bsrc[e]] + f2[h.bsrc[e]]++] = e;
+        }
+    }
+    // Kahn levels; ops by (level, id)
+    h.level.assign(N, 0);
+    {
+        std::vector<int> indeg(N), queue;
+        queue.reserve(N);
+        for (int i = 0; i < N; ++i) indeg[i] = h.pred_ptr[i + 1] - h.pred_ptr[i];
+        for (int i = 0; i < N; ++i) if (indeg[i] == 0) queue.push_back(i);
+        for (size_t qh = 0; qh < queue.size(); ++qh) {
+            const int u = queue[qh];
+            for (int e = h.row_ptr[u]; e < h.row_ptr[u + 1]; ++e) {
+                const int v = h.col[e];
+                h.level[v] = std::max(h.level[v], h.level[u] + 1);
+                if (--indeg[v] == 0) queue.push_back(v);
+            }
+        }
+        if ((int)queue.size() != N) return fail(nullptr, GAUS_E_CYCLE, "forward edges contain a cycle");
+        const int L = 1 + *std::max_element(h.level.begin(), h.level.end());
+        h.lvl_ptr.assign(L + 1, 0);
+        for (int i = 0; i < N; ++i) h.lvl_ptr[h.level[i] + 1]++;
+        for (int l = 0; l < L; ++l) h.lvl_ptr[l + 1] += h.lvl_ptr[l];
+        h.lvl_ops.assign(N, 0);
+        std::vector<int> fill(L, 0);
+        for (int i = 0; i < N; ++i) h.lvl_ops[h.lvl_ptr[h.level[i]] + fill[h.level[i]]++] = i;
+    }
+    // ASAP / ALAP with delays; sinks' ALAP = D-1
+    {
+        std::vector<long long> as(N, 0), al(N, 0);
+        for (int q = 0; q < N; ++q) {
+            const int u = h.lvl_ops[q];
+            for (int e = h.row_ptr[u]; e < h.row_ptr[u + 1]; ++e) {
+                const int v = h.col[e];
+                as[v] = std::max(as[v], as[u] + h.delay[u]);
+            }
+        }
+        for (int q = N - 1; q >= 0; --q) {
+            const int v = h.lvl_ops[q];
+            long long best = (long long)h.D - 1;
+            for (int e = h.row_ptr[v]; e < h.row_ptr[v + 1]; ++e) best = std::min(best, al[h.col[e]] - h.delay[v]);
+            al[v] = best;
+        }
+        for (int i = 0; i < N; ++i)
+            if (as[i] > al[i])
+                return fail(nullptr, GAUS_E_HORIZON, "critical path does not fit the horizon: ASAP[%d]=%lld > ALAP=%lld (D=%d)",
+                            i, as[i], al[i], h.D);
+        h.asap.assign(as.begin(), as.end());
+        h.alap.assign(al.begin(), al.end());
+    }
+    return GAUS_OK;
+}
+
+// Launch shape of the op kernel and op grouping.
+void choose_config(HostGraph &h, int B, LaunchCfg &lc, int &tile, int &ntiles) {
+    if (h.D <= 64) { lc.bs = 64; lc.spt = 1; }
+    else if (h.D <= 512) { lc.bs = 256; lc.spt = 1; }
+    else { lc.bs = 256; lc.spt = 4; }
+    tile = lc.bs * lc.spt;
+    ntiles = (h.D + tile - 1) / tile;
+    // group size: enough work-groups to fill 256 CUs several times over
+    const long long target = 2048;
+    long long per = (long long)h.N * B * ntiles / target;
+    int G = (int)std::min<long long>(256, std::max<long long>(4, per));
+    // ops sorted by (type, id), cut into type-pure groups of <= G ops
+    h.perm.resize(h.N);
+    for (int i = 0; i < h.N; ++i) h.perm[i] = i;
+    std::stable_sort(h.perm.begin(), h.perm.end(), [&](int a, int b) { return h.rtype[a] < h.rtype[b]; });
+    h.grp_start.clear();
+    h.type_grp.assign(h.K + 1, 0);
+    int q = 0;
+    for (int k = 0; k < h.K; ++k) {
+        h.type_grp[k] = (int)h.grp_start.size();
+        int cnt = 0;
+        while (q + cnt < h.N && h.rtype[h.perm[q + cnt]] == k) ++cnt;
+        for (int s = 0; s < cnt; s += G) h.grp_start.push_back(q + s);
+        q += cnt;
+    }
+    h.type_grp[h.K] = (int)h.grp_start.size();
+    h.grp_start.push_back(h.N);
+}
+
+}  // namespace
+
+extern "C" {
+
+void gaus_default_hparams(gaus_hparams *hp) {
+    if (!hp) return;
+    hp->lr = 1e-2f;
+    hp->beta1 = 0.9f;
+    hp->beta2 = 0.999f;
+    hp->eps = 1e-8f;
+    hp->rho = 1e-4f;
+    hp->lambda0 = 1e-6f;
+    hp->alpha_com = 0.01f;
+    hp->sigma_min = 0.05f;
+    hp->kappa = 1.0f / 6.0f;
+}
+
+const char *gaus_status_string(gaus_status s) {
+    switch (s) {
+        case GAUS_OK: return "GAUS_OK";
+        case GAUS_E_INVALID_ARG: return "GAUS_E_INVALID_ARG";
+        case GAUS_E_CYCLE: return "GAUS_E_CYCLE";
+        case GAUS_E_HORIZON: return "GAUS_E_HORIZON";
+        case GAUS_E_NOT_CONVERGED: return "GAUS_E_NOT_CONVERGED";
+        case GAUS_E_OVERFLOW: return "GAUS_E_OVERFLOW";
+        case GAUS_E_DEVICE: return "GAUS_E_DEVICE";
+        case GAUS_E_NOMEM: return "GAUS_E_NOMEM";
+    }
+    return "GAUS_E_UNKNOWN";
+}
+
+const char *gaus_last_error(const gaus_ctx *ctx) {
+    return ctx ? ctx->err.c_str() : g_init_error.c_str();
+}
+
+gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32_t B, void *hip_stream,
+                      gaus_ctx **out) {
+    if (!out) return fail(nullptr, GAUS_E_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    gaus_status s = validate(prob, B);
+    if (s != GAUS_OK) return s;
+    HostGraph h;
+    s = preprocess(prob, h);
+    if (s != GAUS_OK) return s;
+
+    gaus_ctx *c = new (std::nothrow) gaus_ctx();
+    if (!c) return fail(nullptr, GAUS_E_NOMEM, "host allocation failed");
+    gaus_hparams hp;
+    if (hp_in) hp = *hp_in; else gaus_default_hparams(&hp);
+    c->hp = HP{hp.lr, hp.beta1, hp.beta2, hp.eps, hp.rho, hp.lambda0, hp.alpha_com, hp.sigma_min, hp.kappa};
+    c->stream = static_cast<hipStream_t>(hip_stream);
+    (void)hipGetDevice(&c->device);
+    int tile = 0, ntiles = 0;
+    choose_config(h, B, c->lc, tile, ntiles);
+
+    Graph &g = c->g;
+    g.N = h.N; g.E = h.E; g.K = h.K; g.D = h.D; g.II = h.II; g.T = h.II > 0 ? h.II : h.D;
+    g.nb = h.nb; g.B = B; g.tile = tile; g.ntiles = ntiles;
+    g.ngroups = (int)h.grp_start.size() - 1;
+    g.nlevels = (int)h.lvl_ptr.size() - 1;
+    std::vector<float> cap(h.cap);
+    const size_t BN = (size_t)B * h.N;
+#define UP(field, vec) do { s = dupload(c, &g.field, vec); if (s != GAUS_OK) goto fail_alloc; } while (0)
+    UP(row_ptr, h.row_ptr); UP(col, h.col); UP(pred_ptr, h.pred_ptr); UP(pred_eid, h.pred_eid);
+    UP(pred_src, h.pred_src); UP(delay, h.delay); UP(rtype, h.rtype); UP(cap, cap);
+    UP(bsrc, h.bsrc); UP(bdst, h.bdst); UP(bdist, h.bdist); UP(bin_ptr, h.bin_ptr); UP(bin, h.bin);
+    UP(bout_ptr, h.bout_ptr); UP(bout, h.bout); UP(perm, h.perm); UP(grp_start, h.grp_start);
+    UP(type_grp, h.type_grp); UP(lvl_ptr, h.lvl_ptr); UP(lvl_ops, h.lvl_ops); UP(asap, h.asap);
+    UP(alap, h.alap);
+#undef UP
+#define AL(field, n) do { s = dalloc(c, &c->w.field, (n)); if (s != GAUS_OK) goto fail_alloc; } while (0)
+    AL(Upart, (size_t)B * g.ngroups * h.D);
+    AL(ppart, BN * ntiles * kPP);
+    AL(cpart, (size_t)B * h.E * ntiles * kCP);
+    AL(bpart, (size_t)B * h.nb * ntiles * kBP);
+    AL(U, (size_t)B * h.K * g.T);
+    AL(trans, (size_t)B * h.K * h.D);
+    AL(ntrans, (size_t)B * h.K);
+    AL(terms, (size_t)B * 5);
+    AL(wts, (size_t)B * 4);
+    AL(adamf, (size_t)B * 2);
+    AL(s64, BN);
+    AL(s64b, BN);
+    AL(status, (size_t)B);
+#undef AL
+    {
+        hipError_t e = hipMemset(c->w.U, 0, sizeof(float) * (size_t)B * h.K * g.T);
+        if (e == hipSuccess) e = hipDeviceSynchronize();
+        if (e != hipSuccess) { s = fail(nullptr, GAUS_E_DEVICE, "init: %s", hipGetErrorString(e)); goto fail_alloc; }
+    }
+    c->asap = h.asap;
+    c->alap = h.alap;
+    *out = c;
+    return GAUS_OK;
+fail_alloc:
+    free_all(c);
+    delete c;
+    return s;
+}
+
+void gaus_destroy(gaus_ctx *ctx) {
+    if (!ctx) return;
+    (void)hipStreamSynchronize(ctx->stream);
+    free_all(ctx);
+    delete ctx;
+}
+
+gaus_status gaus_bind_state(gaus_ctx *ctx, float *mu, float *sigma, float *adam_m, float *adam_v,
+                            float *lambda, int32_t *adam_t) {
+    if (!ctx) return GAUS_E_INVALID_ARG;
+    if (!mu || !sigma || !adam_m || !adam_v || !lambda || !adam_t)
+        return fail(ctx, GAUS_E_INVALID_ARG, "bind_state: null pointer");
+    ctx->mu = mu; ctx->sigma = sigma; ctx->m = adam_m; ctx->v = adam_v; ctx->lambda = lambda;
+    ctx->adam_t = adam_t;
+    ctx->bound = true;
+    return GAUS_OK;
+}
+
+gaus_status gaus_loss_grad(gaus_ctx *ctx, const float *mu, const float *sigma, const float *lambda,
+                           float *terms, float *grad_mu, float *grad_sigma) {
+    if (!ctx) return GAUS_E_INVALID_ARG;
+    if (!mu || !sigma || !lambda || !terms || !grad_mu || !grad_sigma)
+        return fail(ctx, GAUS_E_INVALID_ARG, "loss_grad: null pointer");
+    IterArgs a{};
+    a.mu = mu; a.sigma = sigma; a.lambda_in = lambda; a.terms_out = terms;
+    a.gmu = grad_mu; a.gsig = grad_sigma; a.mode = 0;
+    hipError_t e = enqueue_iteration(ctx->g, ctx->w, ctx->hp, ctx->lc, a, ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "loss_grad launch");
+    return GAUS_OK;
+}
+
+gaus_status gaus_step(gaus_ctx *ctx, int32_t n_iters, float *terms_last) {
+    if (!ctx) return GAUS_E_INVALID_ARG;
+    if (!ctx->bound) return fail(ctx, GAUS_E_INVALID_ARG, "step: state not bound");
+    if (n_iters < 0) return fail(ctx, GAUS_E_INVALID_ARG, "step: n_iters < 0");
+    for (int it = 0; it < n_iters; ++it) {
+        IterArgs a{};
+        a.mu = ctx->mu; a.sigma = ctx->sigma; a.lambda_in = ctx->lambda; a.lambda_out = ctx->lambda;
+        a.adam_t = ctx->adam_t; a.terms_out = (it == n_iters - 1) ? terms_last : nullptr;
+        a.mu_io = ctx->mu; a.sig_io = ctx->sigma; a.m = ctx->m; a.v = ctx->v; a.mode = 1;
+        hipError_t e = enqueue_iteration(ctx->g, ctx->w, ctx->hp, ctx->lc, a, ctx->stream);
+        if (e != hipSuccess) return hip_fail(ctx, e, "step launch");
+    }
+    return GAUS_OK;
+}
+
+gaus_status gaus_adam_from_grad(gaus_ctx *ctx, const float *g_mu, const float *g_sigma, const float *terms) {
+    if (!ctx) return GAUS_E_INVALID_ARG;
+    if (!ctx->bound) return fail(ctx, GAUS_E_INVALID_ARG, "adam_from_grad: state not bound");
+    if (!g_mu || !g_sigma || !terms) return fail(ctx, GAUS_E_INVALID_ARG, "adam_from_grad: null pointer");
+    hipError_t e = enqueue_adam_from_grad(ctx->g, ctx->w, ctx->hp, g_mu, g_sigma, terms, ctx->mu, ctx->sigma,
+                                          ctx->m, ctx->v, ctx->lambda, ctx->adam_t, ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "adam_from_grad launch");
+    return GAUS_OK;
+}
+
+gaus_status gaus_legalize(gaus_ctx *ctx, const float *mu, int32_t *sched, int32_t *status) {
+    if (!ctx) return GAUS_E_INVALID_ARG;
+    if (!mu || !sched || !status) return fail(ctx, GAUS_E_INVALID_ARG, "legalize: null pointer");
+    hipError_t e = enqueue_legalize(ctx->g, ctx->w, mu, sched, ctx->stream);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(status, ctx->w.status, sizeof(int) * ctx->g.B, hipMemcpyDeviceToHost, ctx->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "legalize");
+    return GAUS_OK;
+}
+
+gaus_status gaus_init_state(gaus_ctx *ctx, const double *u, float *mu, float *sigma) {
+    if (!ctx) return GAUS_E_INVALID_ARG;
+    if (!mu || !sigma) return fail(ctx, GAUS_E_INVALID_ARG, "init_state: null pointer");
+    const int B = ctx->g.B, N = ctx->g.N;
+    if (B > 1 && !u) return fail(ctx, GAUS_E_INVALID_ARG, "init_state: u is required when B > 1");
+    std::vector<float> hm((size_t)B * N), hs((size_t)B * N);
+    for (int b = 0; b < B; ++b)
+        for (int i = 0; i < N; ++i) {
+            const double slack = (double)ctx->alap[i] - ctx->asap[i];
+            const double sg = std::max((double)ctx->hp.kappa * slack, (double)ctx->hp.sigma_min);
+            const double m = b == 0 ? 0.5 * ((double)ctx->asap[i] + ctx->alap[i])
+                                    : ctx->asap[i] + u[(size_t)b * N + i] * slack;
+            hm[(size_t)b * N + i] = (float)m;
+            hs[(size_t)b * N + i] = (float)sg;
+        }
+    hipError_t e = hipMemcpyAsync(mu, hm.data(), hm.size() * sizeof(float), hipMemcpyHostToDevice, ctx->stream);
+    if (e == hipSuccess) e = hipMemcpyAsync(sigma, hs.data(), hs.size() * sizeof(float), hipMemcpyHostToDevice, ctx->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "init_state");
+    return GAUS_OK;
+}
+
+gaus_status gaus_asap_alap(const gaus_ctx *ctx, int32_t *asap, int32_t *alap) {
+    if (!ctx || !asap || !alap) return GAUS_E_INVALID_ARG;
+    std::copy(ctx->asap.begin(), ctx->asap.end(), asap);
+    std::copy(ctx->alap.begin(), ctx->alap.end(), alap);
+    return GAUS_OK;
+}
+
+gaus_status gaus_get_usage(gaus_ctx *ctx, float *U) {
+    if (!ctx) return GAUS_E_INVALID_ARG;
+    if (!U) return fail(ctx, GAUS_E_INVALID_ARG, "get_usage: null pointer");
+    const size_t bytes = sizeof(float) * (size_t)ctx->g.B * ctx->g.K * ctx->g.T;
+    hipError_t e = hipMemcpyAsync(U, ctx->w.U, bytes, hipMemcpyDeviceToDevice, ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "get_usage");
+    return GAUS_OK;
+}
+
+gaus_status gaus_sync(gaus_ctx *ctx) {
+    if (!ctx) return GAUS_E_INVALID_ARG;
+    hipError_t e = hipStreamSynchronize(ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "sync");
+    return GAUS_OK;
+}
+
+gaus_status gaus_get_dims(const gaus_ctx *ctx, int32_t dims[8]) {
+    if (!ctx || !dims) return GAUS_E_INVALID_ARG;
+    const Graph &g = ctx->g;
+    dims[0] = g.N; dims[1] = g.E; dims[2] = g.K; dims[3] = g.D; dims[4] = g.II; dims[5] = g.T;
+    dims[6] = g.nb; dims[7] = g.B;
+    return GAUS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,93 @@
+// Internal declarations shared by the host side (gaus_host.cpp) and the
+// gfx950 kernels (gaus_kernels.hip).  Not part of the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstddef>
+#include <cstdint>
+
+namespace gaus {
+
+// Partial-sum record widths.
+constexpr int kPP = 6;   // per (restart, op, tile): V_dep, L_com, dVdep/dmu_i, dVdep/dsigma_i,
+                         //   dLcom/dmu_i, dLcom/dsigma_i  (producer side of the op's out-edges)
+constexpr int kCP = 4;   // per (restart, edge, tile): dVdep/dmu_j, dVdep/dsigma_j,
+                         //   dLcom/dmu_j, dLcom/dsigma_j (consumer side)
+constexpr int kBP = 5;   // per (restart, back edge, tile): V_rec, dVrec/dmu_j, dVrec/dsigma_j
+                         //   (producer j), dVrec/dmu_i, dVrec/dsigma_i (consumer i)
+constexpr int kHalo = 256;  // largest producer delay handled from the LDS row window
+
+// Device copy of the preprocessed problem (all pointers are device memory).
+struct Graph {
+    int N, E, K, D, II, T, nb, B;
+    int tile, ntiles;          // steps per tile of the op kernel, tiles per restart
+    int ngroups;               // type-pure op groups (one work-group each per tile)
+    int nlevels;               // topological levels (legalization)
+    const int *row_ptr, *col;            // CSR by producer
+    const int *pred_ptr, *pred_eid;      // CSC: CSR edge id of each in-edge
+    const int *pred_src;                 // CSC: producer of each in-edge
+    const int *delay, *rtype;
+    const float *cap;
+    const int *bsrc, *bdst, *bdist;      // back edges (producer j, consumer i, k)
+    const int *bin_ptr, *bin;            // back edges by consumer
+    const int *bout_ptr, *bout;          // back edges by producer
+    const int *perm;                     // ops sorted by (type, id)
+    const int *grp_start;                // [ngroups+1] ranges of perm
+    const int *type_grp;                 // [K+1] groups of type k: [type_grp[k], type_grp[k+1])
+    const int *lvl_ptr, *lvl_ops;        // ops by (topological level, id)
+    const int *asap, *alap;
+};
+
+// Library-owned device workspace.
+struct Work {
+    float *Upart;     // [B][ngroups][D]   per-group unfolded usage partials
+    float *ppart;     // [B][N][ntiles][kPP]
+    float *cpart;     // [B][E][ntiles][kCP]
+    float *bpart;     // [B][nb][ntiles][kBP]
+    float *U;         // [B][K][T]         expected (folded) usage
+    int *trans;       // [B][K][D]         signed (t+1) of each ReLU-indicator change at bin edge t
+    int *ntrans;      // [B][K]
+    float *terms;     // [B][5]            L, V_dep, V_res, V_rec, L_com of the last forward
+    float *wts;       // [B][4]            w_dep, w_res, w_rec, unused
+    float *adamf;     // [B][2]            Adam bias corrections 1-beta1^t, 1-beta2^t
+    long long *s64;   // [B][N]            legalization workspace
+    long long *s64b;  // [B][N]            legalization snapshot (back edges)
+    int *status;      // [B]               legalization status
+};
+
+struct HP {
+    float lr, b1, b2, eps, rho, lambda0, alpha, sigma_min, kappa;
+};
+
+// Kernel-side configuration chosen on the host from (N, D, B).
+struct LaunchCfg {
+    int bs;    // threads per work-group of the op kernel (64 or 256)
+    int spt;   // steps per thread (1 or 4)
+};
+
+// Enqueue one forward+backward.  mode 0: write terms/grad to the outputs;
+// mode 1: Adam step in place on (mu, sigma, m, v), lambda update, adam_t++.
+struct IterArgs {
+    const float *mu, *sigma;        // inputs (mode 1: the bound state)
+    const float *lambda_in;         // [B][3]
+    float *lambda_out;              // mode 1: updated multipliers (may alias lambda_in)
+    int *adam_t;                    // mode 1
+    float *terms_out;               // [B][5] or null
+    float *gmu, *gsig;              // mode 0 outputs
+    float *mu_io, *sig_io, *m, *v;  // mode 1 state
+    int mode;
+};
+
+hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const LaunchCfg &lc,
+                             const IterArgs &a, hipStream_t st);
+
+// Adam + sigma clamp + lambda += rho*V (from terms) + adam_t++ from a given gradient.
+hipError_t enqueue_adam_from_grad(const Graph &g, const Work &w, const HP &hp, const float *gmu,
+                                  const float *gsig, const float *terms, float *mu, float *sigma,
+                                  float *m, float *v, float *lambda, int *adam_t, hipStream_t st);
+
+// Round + legalize every restart; writes sched [B][N] and w.status [B].
+hipError_t enqueue_legalize(const Graph &g, const Work &w, const float *mu, int *sched,
+                            hipStream_t st);
+
+}  // namespace gaus

@@ -1,0 +1,740 @@
+// gfx950 kernels of the GauS hot path: masses, folded usage, resource /
+// dependency / recurrence penalties, expected edge length, their analytic
+// gradient, Adam, and Alg. 3/4 legalization.
+//
+// Notation (arXiv 2602.20427): op i has start step d_i ~ round(N(mu_i, sigma_i^2)).
+// F_i(t) = P(d_i <= t) at the interior bin edges t = 0..D-2 (eq:round with the
+// open end bins: F_i(t) = 0 for t < 0 and 1 for t >= D-1), P_i^d = F_i(d) - F_i(d-1).
+// Every term of the objective is a sum over steps of products of F's and P's
+// of the two end points of an edge, so all kernels iterate over a step index u
+// and evaluate F, dF/dmu, dF/dsigma from (mu, sigma) on the fly: nothing of size
+// B*N*D is ever stored.
+//
+// Reductions use fixed trees and per-(tile, group) partial buffers, never
+// floating-point atomics, so results are bitwise reproducible.
+#include "gaus_internal.h"
+#include "gaus_erfcx_coeffs.h"
+
+namespace gaus {
+
+namespace {
+
+constexpr float kInvSqrt2 = 0.70710678118654752f;
+constexpr float kInvSqrt2Pi = 0.39894228040143268f;
+constexpr float kHalfLog2e = 0.72134752044448170f;  // log2(e)/2
+
+// Tail of the standard normal and the Gaussian factor: tail = Phi(-|z|),
+// g = exp(-z^2/2).  Phi(-|z|) = erfc(x)/2 with x = |z|/sqrt(2) and
+// erfc(x) = exp(-x^2) * t * Q(t), t = 1/(1 + p x), Q a fitted polynomial
+// (gaus_erfcx_coeffs.h).  exp(-x^2) equals g, which the gradient needs, so
+// both come from one exp.
+__device__ __forceinline__ void normal_tail_pdf(float z, float &tail, float &g) {
+    const float x = fabsf(z) * kInvSqrt2;
+    g = __builtin_amdgcn_exp2f(-(z * z) * kHalfLog2e);
+    const float t = __builtin_amdgcn_rcpf(fmaf(GAUS_ERFCX_P, x, 1.0f));
+    float q = gaus_erfcx_q[GAUS_ERFCX_DEG];
+#pragma unroll
+    for (int k = GAUS_ERFCX_DEG - 1; k >= 0; --k) q = fmaf(q, t, gaus_erfcx_q[k]);
+    tail = 0.5f * g * (t * q);
+}
+
+// A CDF value F is kept as a signed tail: +Phi(-|z|) below the median
+// (F = tail) and -Phi(-|z|) at or above it (F = 1 - tail; -0.0 for F = 1).
+// Differences of neighbouring CDF values (the masses P_i^d) are then formed
+// from tails, without the cancellation of 1 - F near F = 1.
+__device__ __forceinline__ bool st_upper(float st) { return __builtin_signbit(st); }
+__device__ __forceinline__ float st_F(float st) { return st_upper(st) ? 1.0f + st : st; }
+__device__ __forceinline__ float st_1mF(float st) { return st_upper(st) ? -st : 1.0f - st; }
+// F(hi) - F(lo) for bin edges lo < hi
+__device__ __forceinline__ float st_mass(float lo, float hi) {
+    const bool ul = st_upper(lo), uh = st_upper(hi);
+    if (ul) return hi - lo;                  // both above: tail(lo) - tail(hi)
+    if (!uh) return hi - lo;                 // both below: tail(hi) - tail(lo)
+    return (1.0f + hi) - lo;                 // straddles the median
+}
+
+// Signed-tail CDF and its derivatives at bin edge v of an op (mu, rs = 1/sigma,
+// cinv = 1/(sigma sqrt(2 pi))): dF/dmu = -phi(z)/sigma, dF/dsigma = -phi(z) z/sigma.
+// Outside the interior edges F is the constant 0 (v < 0) or 1 (v >= D-1).
+__device__ __forceinline__ void cdf_at(long long v, int D, float mu, float rs, float cinv, float &st,
+                                       float &Fm, float &Fs) {
+    if (v < 0) { st = 0.0f; Fm = 0.0f; Fs = 0.0f; return; }
+    if (v >= D - 1) { st = -0.0f; Fm = 0.0f; Fs = 0.0f; return; }
+    const float z = ((float)v + 0.5f - mu) * rs;
+    float tail, g;
+    normal_tail_pdf(z, tail, g);
+    st = (z >= 0.0f) ? -tail : tail;
+    Fm = -g * cinv;
+    Fs = Fm * z;
+}
+
+__device__ __forceinline__ float st_at(long long v, int D, float mu, float rs) {
+    if (v < 0) return 0.0f;
+    if (v >= D - 1) return -0.0f;
+    const float z = ((float)v + 0.5f - mu) * rs;
+    float tail, g;
+    normal_tail_pdf(z, tail, g);
+    return (z >= 0.0f) ? -tail : tail;
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
+    return x;
+}
+
+// Sum NV values over the work-group; thread c < NV receives total c.
+// slot: LDS scratch [NW][8]; callers alternate between two slots so that only
+// one barrier per reduction is needed.
+template <int NV, int BS>
+__device__ __forceinline__ float block_sum(float (&v)[NV], float (*slot)[8]) {
+    constexpr int NW = BS / 64;
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+#pragma unroll
+    for (int c = 0; c < NV; ++c) v[c] = wave_sum(v[c]);
+    if (lane == 0) {
+#pragma unroll
+        for (int c = 0; c < NV; ++c) slot[wid][c] = v[c];
+    }
+    __syncthreads();
+    float r = 0.0f;
+    if (threadIdx.x < NV) {
+#pragma unroll
+        for (int w = 0; w < NW; ++w) r += slot[w][threadIdx.x];
+    }
+    return r;
+}
+
+__device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Op kernel.  Work-group = (op group, step tile, restart).  Threads own steps
+// u = t0 + k*BS + tid (k < SPT).  For each op i of the group (all of one
+// resource type, out-degree m, delay s = Lat(v_i)):
+//   * its CDF row over the tile plus a left halo of s steps goes to LDS; the
+//     mass P_i^u is added to the group's usage;
+//   * for each out-edge (i -> j) the consumer's CDF and Gaussian factor are
+//     evaluated once per step.  The consumer-side derivatives of this edge are
+//       dVdep/dth_j = sum_u A(u) F_j'(u),   A(u) = P_i^{u-s+1}
+//       dLcom/dth_j = -sum_u F_i(u) F_j'(u)
+//     and the successor CDF sum S_i(u) = sum_j F_j(u) is accumulated split
+//     into lower-side CDFs, upper tails and a count of successors past their
+//     median, so that S_i, m - S_i and S_i(u) - S_i(u-1) keep full precision;
+//   * after the out-edges the producer-side terms follow from S_i:
+//       V_dep          = sum_u A(u) S_i(u) + m (1 - F_i(D-1-s))
+//       L_com          = sum_u F_i(u) (m - S_i(u))
+//       dVdep/dth_i    = -sum_u F_i'(u-s) (S_i(u) - S_i(u-1))
+//       dLcom/dth_i    = sum_u F_i'(u) (m - S_i(u))
+//     (u over the interior edges 0..D-2 except in dVdep/dth_i, which runs to
+//     u = D-1 with S_i(D-1) = m: the consumers' bin D-1 is open to +inf).
+// ---------------------------------------------------------------------------
+template <int BS, int SPT>
+__global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ mu,
+                                            const float *__restrict__ sigma, Work W) {
+    constexpr int TILE = BS * SPT;
+    constexpr int WIN = TILE + kHalo + 1;
+    __shared__ float sT[WIN], sFm[WIN], sFs[WIN];
+    __shared__ float sRed[2][BS / 64][8];
+    __shared__ float sPrev[3];
+
+    const int grp = blockIdx.x, tile = blockIdx.y, b = blockIdx.z;
+    const int tid = threadIdx.x;
+    const int D = G.D, N = G.N;
+    const int t0 = tile * TILE;
+    const float *mub = mu + (size_t)b * N;
+    const float *sgb = sigma + (size_t)b * N;
+
+    const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
+    float accU[SPT];
+#pragma unroll
+    for (int k = 0; k < SPT; ++k) accU[k] = 0.0f;
+    int par = 0;
+
+    for (int q = q0; q < q1; ++q) {
+        const int i = uniform(G.perm[q]);
+        const float m_i = mub[i], s_i = sgb[i];
+        const float rs = 1.0f / s_i;
+        const float cinv = rs * kInvSqrt2Pi;
+        const int s = uniform(G.delay[i]);
+        const int e0 = uniform(G.row_ptr[i]), e1 = uniform(G.row_ptr[i + 1]);
+        const int m = e1 - e0;
+        const bool win_shift = (m > 0) && (s <= kHalo);
+        const int Lh = win_shift ? (s > 1 ? s : 1) : 1;
+
+        // row window: positions v = t0 - Lh + p, p in [0, TILE + Lh]
+        for (int p = tid; p < TILE + Lh + 1; p += BS) {
+            float st, Fm, Fs;
+            cdf_at(t0 - Lh + p, D, m_i, rs, cinv, st, Fm, Fs);
+            sT[p] = st; sFm[p] = Fm; sFs[p] = Fs;
+        }
+        __syncthreads();
+
+        float rF[SPT], rFm[SPT], rFs[SPT], rA[SPT], rFms[SPT], rFss[SPT];
+        float tail1mF = 0.0f;  // 1 - F_i(D-1-s), held by the thread owning u = D-1
+#pragma unroll
+        for (int k = 0; k < SPT; ++k) {
+            const int u = t0 + k * BS + tid;
+            const int p = u - t0 + Lh;
+            rF[k] = st_F(sT[p]); rFm[k] = sFm[p]; rFs[k] = sFs[p];
+            if (u < D) accU[k] += st_mass(sT[p - 1], sT[p]);
+            rA[k] = 0.0f; rFms[k] = 0.0f; rFss[k] = 0.0f;
+            if (m > 0 && u < D) {
+                if (win_shift) {
+                    rA[k] = st_mass(sT[p - s], sT[p - s + 1]);
+                    rFms[k] = sFm[p - s]; rFss[k] = sFs[p - s];
+                    if (u == D - 1) tail1mF = st_1mF(sT[p - s]);
+                } else {
+                    float st0, Fm0, Fs0, st1, Fm1, Fs1;
+                    cdf_at((long long)u - s, D, m_i, rs, cinv, st0, Fm0, Fs0);
+                    cdf_at((long long)u - s + 1, D, m_i, rs, cinv, st1, Fm1, Fs1);
+                    rA[k] = st_mass(st0, st1); rFms[k] = Fm0; rFss[k] = Fs0;
+                    if (u == D - 1) tail1mF = st_1mF(st0);
+                }
+            }
+        }
+        __syncthreads();  // the window may be overwritten from here on
+
+        float SL[SPT], SU[SPT], SC[SPT];
+#pragma unroll
+        for (int k = 0; k < SPT; ++k) { SL[k] = 0.0f; SU[k] = 0.0f; SC[k] = 0.0f; }
+        float pL = 0.0f, pU = 0.0f, pC = 0.0f;   // S_i(t0-1), thread 0 only
+
+        for (int e = e0; e < e1; ++e) {
+            const int j = uniform(G.col[e]);
+            const float m_j = mub[j], s_j = sgb[j];
+            const float rsj = 1.0f / s_j;
+            float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int k = 0; k < SPT; ++k) {
+                const int u = t0 + k * BS + tid;
+                if (u < D - 1) {
+                    const float z = ((float)u + 0.5f - m_j) * rsj;
+                    float tl, gj;
+                    normal_tail_pdf(z, tl, gj);
+                    const bool up = z >= 0.0f;
+                    SL[k] += up ? 0.0f : tl;
+                    SU[k] += up ? tl : 0.0f;
+                    SC[k] += up ? 1.0f : 0.0f;
+                    const float gz = gj * z;
+                    acc[0] = fmaf(rA[k], gj, acc[0]);
+                    acc[1] = fmaf(rA[k], gz, acc[1]);
+                    acc[2] = fmaf(rF[k], gj, acc[2]);
+                    acc[3] = fmaf(rF[k], gz, acc[3]);
+                }
+            }
+            if (tid == 0 && t0 > 0) {
+                const float z = ((float)(t0 - 1) + 0.5f - m_j) * rsj;
+                float tl, gj;
+                normal_tail_pdf(z, tl, gj);
+                if (z >= 0.0f) { pU += tl; pC += 1.0f; } else { pL += tl; }
+            }
+            const float r = block_sum<4, BS>(acc, sRed[par]);
+            par ^= 1;
+            if (tid < 4) {
+                // F_j'(u) = -g_j/(sigma_j sqrt(2 pi)) [* z for sigma]; L_com enters with a minus
+                const float cj = rsj * kInvSqrt2Pi;
+                const float val = (tid < 2) ? -cj * r : cj * r;
+                W.cpart[(((size_t)b * G.E + e) * G.ntiles + tile) * kCP + tid] = val;
+            }
+        }
+
+        float pr[6] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+        if (m > 0) {
+            const float mf = (float)m;
+            // S_i(D-1) = m: every consumer is at or before step D-1
+#pragma unroll
+            for (int k = 0; k < SPT; ++k) {
+                const int u = t0 + k * BS + tid;
+                if (u == D - 1) { SL[k] = 0.0f; SU[k] = 0.0f; SC[k] = mf; }
+                if (u < D) { sT[u - t0] = SL[k]; sFm[u - t0] = SU[k]; sFs[u - t0] = SC[k]; }
+            }
+            if (tid == 0) { sPrev[0] = pL; sPrev[1] = pU; sPrev[2] = pC; }
+            __syncthreads();
+#pragma unroll
+            for (int k = 0; k < SPT; ++k) {
+                const int u = t0 + k * BS + tid;
+                if (u >= D) continue;
+                const int ix = u - t0;
+                const float L1 = ix ? sT[ix - 1] : sPrev[0];
+                const float U1 = ix ? sFm[ix - 1] : sPrev[1];
+                const float C1 = ix ? sFs[ix - 1] : sPrev[2];
+                const float dS = ((SL[k] - L1) + (SC[k] - C1)) - (SU[k] - U1);
+                pr[2] = fmaf(-rFms[k], dS, pr[2]);
+                pr[3] = fmaf(-rFss[k], dS, pr[3]);
+                if (u < D - 1) {
+                    const float S = (SL[k] + SC[k]) - SU[k];
+                    const float rest = ((mf - SC[k]) - SL[k]) + SU[k];
+                    pr[0] = fmaf(rA[k], S, pr[0]);
+                    pr[1] = fmaf(rF[k], rest, pr[1]);
+                    pr[4] = fmaf(rFm[k], rest, pr[4]);
+                    pr[5] = fmaf(rFs[k], rest, pr[5]);
+                } else {
+                    pr[0] = fmaf(mf, tail1mF, pr[0]);
+                }
+            }
+            const float r = block_sum<6, BS>(pr, sRed[par]);
+            par ^= 1;
+            if (tid < kPP) W.ppart[(((size_t)b * N + i) * G.ntiles + tile) * kPP + tid] = r;
+        } else if (tid < kPP) {
+            W.ppart[(((size_t)b * N + i) * G.ntiles + tile) * kPP + tid] = 0.0f;
+        }
+    }
+
+    float *up = W.Upart + ((size_t)b * G.ngroups + grp) * D;
+#pragma unroll
+    for (int k = 0; k < SPT; ++k) {
+        const int u = t0 + k * BS + tid;
+        if (u < D) up[u] = accU[k];
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Back-edge kernel (modulo scheduling).  Work-group = (back-edge block, tile,
+// restart); one back edge (j -> i, k) at a time, c = k*II - Lat_j:
+//   V_rec       = F_i(-c-1) + sum_u P_i^{u-c} (1 - F_j(u))
+//   dVrec/dth_j = -sum_u F_j'(u) P_i^{u-c}
+//   dVrec/dth_i =  sum_t F_i'(t) P_j^{t+c+1}
+// with u, t over the interior edges 0..D-2.
+// ---------------------------------------------------------------------------
+template <int BS, int SPT>
+__global__ __launch_bounds__(BS) void k_back(Graph G, const float *__restrict__ mu,
+                                             const float *__restrict__ sigma, Work W,
+                                             int edges_per_block) {
+    constexpr int TILE = BS * SPT;
+    __shared__ float sRed[2][BS / 64][8];
+    const int tile = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
+    const int D = G.D, N = G.N;
+    const int t0 = tile * TILE;
+    const int be0 = blockIdx.x * edges_per_block;
+    const int be1 = min(be0 + edges_per_block, G.nb);
+    int par = 0;
+    for (int e = be0; e < be1; ++e) {
+        const int j = uniform(G.bsrc[e]), i = uniform(G.bdst[e]);
+        const long long c = (long long)G.bdist[e] * G.II - G.delay[j];
+        const float mj = mu[(size_t)b * N + j], sj = sigma[(size_t)b * N + j];
+        const float mi = mu[(size_t)b * N + i], si = sigma[(size_t)b * N + i];
+        const float rsj = 1.0f / sj, rsi = 1.0f / si;
+        const float cj = rsj * kInvSqrt2Pi, ci = rsi * kInvSqrt2Pi;
+        float acc[5] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int k = 0; k < SPT; ++k) {
+            const int u = t0 + k * BS + tid;
+            if (u < D - 1) {
+                float sj_, Fmj, Fsj, si_, Fmi, Fsi;
+                cdf_at(u, D, mj, rsj, cj, sj_, Fmj, Fsj);
+                cdf_at(u, D, mi, rsi, ci, si_, Fmi, Fsi);
+                const float Pi = st_mass(st_at((long long)u - c - 1, D, mi, rsi), st_at((long long)u - c, D, mi, rsi));
+                const float Pj = st_mass(st_at((long long)u + c, D, mj, rsj), st_at((long long)u + c + 1, D, mj, rsj));
+                acc[0] = fmaf(Pi, st_1mF(sj_), acc[0]);
+                acc[1] = fmaf(-Fmj, Pi, acc[1]);
+                acc[2] = fmaf(-Fsj, Pi, acc[2]);
+                acc[3] = fmaf(Fmi, Pj, acc[3]);
+                acc[4] = fmaf(Fsi, Pj, acc[4]);
+            }
+        }
+        if (tile == 0 && tid == 0) acc[0] += st_F(st_at(-c - 1, D, mi, rsi));
+        const float r = block_sum<5, BS>(acc, sRed[par]);
+        par ^= 1;
+        if (tid < kBP) W.bpart[(((size_t)b * G.nb + e) * G.ntiles + tile) * kBP + tid] = r;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Usage: U[b][k][slot] = sum over type-k groups and steps t = slot (mod T).
+// ---------------------------------------------------------------------------
+__global__ void k_usage(Graph G, Work W) {
+    const int b = blockIdx.y;
+    const int cell = blockIdx.x * blockDim.x + threadIdx.x;
+    if (cell >= G.K * G.T) return;
+    const int k = cell / G.T, slot = cell % G.T;
+    float acc = 0.0f;
+    for (int g = G.type_grp[k]; g < G.type_grp[k + 1]; ++g) {
+        const float *up = W.Upart + ((size_t)b * G.ngroups + g) * G.D;
+        for (int t = slot; t < G.D; t += G.T) acc += up[t];
+    }
+    W.U[(size_t)b * G.K * G.T + cell] = acc;
+}
+
+// ---------------------------------------------------------------------------
+// Per-restart scalars.  One work-group of 1024 threads per restart:
+// V_res (eq:relu), the sign changes of the ReLU indicator along the bin edges,
+// V_dep / L_com / V_rec from the partials, the augmented Lagrangian (eq. 11),
+// the weights w_c = lambda_c + rho V_c, and in step mode the multiplier update
+// lambda_c += rho V_c and the Adam bias corrections.
+// ---------------------------------------------------------------------------
+constexpr int kTermsBS = 1024;
+
+__device__ float block_sum1024(float x, float *scratch /*[16]*/) {
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    x = wave_sum(x);
+    if (lane == 0) scratch[wid] = x;
+    __syncthreads();
+    float r = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kTermsBS / 64; ++w) r += scratch[w];
+    __syncthreads();
+    return r;
+}
+
+__global__ __launch_bounds__(kTermsBS) void k_terms(Graph G, Work W, HP hp,
+                                                    const float *__restrict__ lambda_in,
+                                                    float *lambda_out, const int *adam_t,
+                                                    float *terms_out) {
+    __shared__ float scratch[kTermsBS / 64];
+    __shared__ int wcount[kTermsBS / 64];
+    __shared__ int base;
+    const int b = blockIdx.x, tid = threadIdx.x;
+    const int lane = tid & 63, wid = tid >> 6;
+    const int K = G.K, T = G.T, D = G.D;
+    const float *U = W.U + (size_t)b * K * T;
+
+    float vres = 0.0f;
+    for (int c = tid; c < K * T; c += kTermsBS) {
+        const float ex = U[c] - G.cap[c / T];
+        if (ex > 0.0f) vres += ex;
+    }
+    vres = block_sum1024(vres, scratch);
+
+    // ReLU-indicator changes I(t mod T) != I((t+1) mod T) at bin edges t = 0..D-2,
+    // compacted in increasing t (wave ballots + a work-group prefix).
+    for (int k = 0; k < K; ++k) {
+        const float ck = G.cap[k];
+        const float *Uk = U + (size_t)k * T;
+        int *out = W.trans + ((size_t)b * K + k) * D;
+        if (tid == 0) base = 0;
+        __syncthreads();
+        for (int t0 = 0; t0 < D - 1; t0 += kTermsBS) {
+            const int t = t0 + tid;
+            int sgn = 0;
+            if (t < D - 1) {
+                const int a = Uk[t % T] > ck, c = Uk[(t + 1) % T] > ck;
+                sgn = a - c;
+            }
+            const unsigned long long bal = __ballot(sgn != 0);
+            const int before = __popcll(bal & ((1ull << lane) - 1ull));
+            if (lane == 0) wcount[wid] = __popcll(bal);
+            __syncthreads();
+            int off = base;
+            for (int w = 0; w < wid; ++w) off += wcount[w];
+            if (sgn != 0) out[off + before] = sgn * (t + 1);
+            __syncthreads();
+            if (tid == 0) {
+                int tot = 0;
+                for (int w = 0; w < kTermsBS / 64; ++w) tot += wcount[w];
+                base += tot;
+            }
+            __syncthreads();
+        }
+        if (tid == 0) W.ntrans[(size_t)b * K + k] = base;
+        __syncthreads();
+    }
+
+    float vdep = 0.0f, lcom = 0.0f, vrec = 0.0f;
+    const size_t np = (size_t)G.N * G.ntiles;
+    const float *pp = W.ppart + (size_t)b * np * kPP;
+    for (size_t r = tid; r < np; r += kTermsBS) { vdep += pp[r * kPP + 0]; lcom += pp[r * kPP + 1]; }
+    const size_t nbp = (size_t)G.nb * G.ntiles;
+    const float *bp = W.bpart + (size_t)b * nbp * kBP;
+    for (size_t r = tid; r < nbp; r += kTermsBS) vrec += bp[r * kBP + 0];
+    vdep = block_sum1024(vdep, scratch);
+    lcom = block_sum1024(lcom, scratch);
+    vrec = block_sum1024(vrec, scratch);
+
+    if (tid == 0) {
+        const float V[3] = {vdep, vres, vrec};
+        const float *lam = lambda_in + (size_t)b * 3;
+        float L = hp.alpha * lcom;
+        float w[3];
+        for (int c = 0; c < 3; ++c) {
+            L += lam[c] * V[c] + 0.5f * hp.rho * V[c] * V[c];
+            w[c] = lam[c] + hp.rho * V[c];
+        }
+        float *tm = W.terms + (size_t)b * 5;
+        tm[0] = L; tm[1] = vdep; tm[2] = vres; tm[3] = vrec; tm[4] = lcom;
+        if (terms_out) for (int c = 0; c < 5; ++c) terms_out[(size_t)b * 5 + c] = tm[c];
+        float *wt = W.wts + (size_t)b * 4;
+        wt[0] = w[0]; wt[1] = w[1]; wt[2] = w[2]; wt[3] = 0.0f;
+        if (lambda_out) for (int c = 0; c < 3; ++c) lambda_out[(size_t)b * 3 + c] = fmaf(hp.rho, V[c], lam[c]);
+        if (adam_t) {
+            const int t = *adam_t + 1;
+            W.adamf[(size_t)b * 2 + 0] = 1.0f - powf(hp.b1, (float)t);
+            W.adamf[(size_t)b * 2 + 1] = 1.0f - powf(hp.b2, (float)t);
+        }
+    }
+}
+
+// Adam (Kingma & Ba), bias-corrected.  Every rounding step is spelled out
+// (no implicit multiply-add contraction) so that the fused step and the
+// separate optimizer kernel produce identical bits.
+__device__ __forceinline__ void adam_update(float &th, float &m, float &v, float g, float lr, float b1,
+                                            float b2, float eps, float c1, float c2) {
+    m = fmaf(b1, m, __fmul_rn(1.0f - b1, g));
+    v = fmaf(b2, v, __fmul_rn(__fmul_rn(1.0f - b2, g), g));
+    const float denom = __fadd_rn(sqrtf(__fdiv_rn(v, c2)), eps);
+    th = __fsub_rn(th, __fdiv_rn(__fmul_rn(lr, __fdiv_rn(m, c1)), denom));
+}
+
+// dL/dtheta from the four constraint/objective derivatives, fixed rounding order.
+__device__ __forceinline__ float combine_grad(float w_res, float r, float w_dep, float d, float w_rec,
+                                              float q, float alpha, float c) {
+    return fmaf(alpha, c, fmaf(w_rec, q, fmaf(w_dep, d, __fmul_rn(w_res, r))));
+}
+
+// ---------------------------------------------------------------------------
+// Gradient assembly (+ Adam in step mode).  Thread per (restart, op):
+//   dL/dth_i = w_res dVres/dth_i + w_dep dVdep/dth_i + w_rec dVrec/dth_i + alpha dLcom/dth_i
+// dVres/dth_i = sum over bin edges t where the ReLU indicator of the op's type
+// changes of (I(t) - I(t+1)) F_i'(t); the other pieces are sums of partials
+// (own tiles, in-edges through the CSC, back edges on either side).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_final(Graph G, Work W, HP hp, const float *mu,
+                                               const float *sigma, float *gmu,
+                                               float *gsig, float *mu_io, float *sig_io, float *am,
+                                               float *av, int *adam_t, int mode) {
+    const int b = blockIdx.y;
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= G.N) return;
+    const int N = G.N, nt = G.ntiles;
+    const size_t bi = (size_t)b * N + i;
+    const float m_i = mu[bi], s_i = sigma[bi];
+    const float rs = 1.0f / s_i, cinv = rs * kInvSqrt2Pi;
+    const float *wt = W.wts + (size_t)b * 4;
+    const float w_dep = wt[0], w_res = wt[1], w_rec = wt[2];
+
+    // resource term through the indicator changes of this op's type
+    const int k = G.rtype[i];
+    const int nt_k = W.ntrans[(size_t)b * G.K + k];
+    const int *tr = W.trans + ((size_t)b * G.K + k) * G.D;
+    float rm = 0.0f, rsg = 0.0f;
+    for (int q = 0; q < nt_k; ++q) {
+        const int code = tr[q];
+        const float sgn = code > 0 ? 1.0f : -1.0f;
+        const int t = (code > 0 ? code : -code) - 1;
+        const float z = ((float)t + 0.5f - m_i) * rs;
+        const float g = __builtin_amdgcn_exp2f(-(z * z) * kHalfLog2e);
+        const float Fm = -g * cinv;
+        rm = fmaf(sgn, Fm, rm);
+        rsg = fmaf(sgn, Fm * z, rsg);
+    }
+
+    float dm = 0.0f, ds = 0.0f, cm = 0.0f, cs = 0.0f;
+    const float *pp = W.ppart + bi * nt * kPP;
+    for (int tl = 0; tl < nt; ++tl) {
+        dm += pp[tl * kPP + 2]; ds += pp[tl * kPP + 3];
+        cm += pp[tl * kPP + 4]; cs += pp[tl * kPP + 5];
+    }
+    for (int q = G.pred_ptr[i]; q < G.pred_ptr[i + 1]; ++q) {
+        const float *cp = W.cpart + (((size_t)b * G.E + G.pred_eid[q]) * nt) * kCP;
+        for (int tl = 0; tl < nt; ++tl) {
+            dm += cp[tl * kCP + 0]; ds += cp[tl * kCP + 1];
+            cm += cp[tl * kCP + 2]; cs += cp[tl * kCP + 3];
+        }
+    }
+    float qm = 0.0f, qs = 0.0f;
+    for (int q = G.bout_ptr[i]; q < G.bout_ptr[i + 1]; ++q) {
+        const float *bp = W.bpart + (((size_t)b * G.nb + G.bout[q]) * nt) * kBP;
+        for (int tl = 0; tl < nt; ++tl) { qm += bp[tl * kBP + 1]; qs += bp[tl * kBP + 2]; }
+    }
+    for (int q = G.bin_ptr[i]; q < G.bin_ptr[i + 1]; ++q) {
+        const float *bp = W.bpart + (((size_t)b * G.nb + G.bin[q]) * nt) * kBP;
+        for (int tl = 0; tl < nt; ++tl) { qm += bp[tl * kBP + 3]; qs += bp[tl * kBP + 4]; }
+    }
+    const float g_mu = combine_grad(w_res, rm, w_dep, dm, w_rec, qm, hp.alpha, cm);
+    const float g_sg = combine_grad(w_res, rsg, w_dep, ds, w_rec, qs, hp.alpha, cs);
+
+    if (mode == 0) {
+        gmu[bi] = g_mu;
+        gsig[bi] = g_sg;
+    } else {
+        const float c1 = W.adamf[(size_t)b * 2 + 0], c2 = W.adamf[(size_t)b * 2 + 1];
+        const size_t half = (size_t)G.B * N;
+        float th = mu_io[bi], mm = am[bi], vv = av[bi];
+        adam_update(th, mm, vv, g_mu, hp.lr, hp.b1, hp.b2, hp.eps, c1, c2);
+        mu_io[bi] = th; am[bi] = mm; av[bi] = vv;
+        th = sig_io[bi]; mm = am[half + bi]; vv = av[half + bi];
+        adam_update(th, mm, vv, g_sg, hp.lr, hp.b1, hp.b2, hp.eps, c1, c2);
+        sig_io[bi] = fmaxf(th, hp.sigma_min);
+        am[half + bi] = mm; av[half + bi] = vv;
+        if (b == 0 && i == 0) *adam_t += 1;
+    }
+}
+
+// lambda += rho V (V from terms) and the Adam bias corrections; one thread per restart.
+__global__ void k_lambda_from_terms(int B, HP hp, const float *terms, float *lambda,
+                                    const int *adam_t, float *adamf) {
+    const int b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= B) return;
+    for (int c = 0; c < 3; ++c)
+        lambda[(size_t)b * 3 + c] = fmaf(hp.rho, terms[(size_t)b * 5 + 1 + c], lambda[(size_t)b * 3 + c]);
+    const int t = *adam_t + 1;
+    adamf[(size_t)b * 2 + 0] = 1.0f - powf(hp.b1, (float)t);
+    adamf[(size_t)b * 2 + 1] = 1.0f - powf(hp.b2, (float)t);
+}
+
+__global__ __launch_bounds__(256) void k_adam(int B, int N, HP hp, const float *adamf,
+                                              const float *gmu, const float *gsig, float *mu,
+                                              float *sigma, float *am, float *av, int *adam_t) {
+    const int b = blockIdx.y;
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= N) return;
+    const size_t bi = (size_t)b * N + i, half = (size_t)B * N;
+    const float c1 = adamf[(size_t)b * 2 + 0], c2 = adamf[(size_t)b * 2 + 1];
+    float th = mu[bi], mm = am[bi], vv = av[bi];
+    adam_update(th, mm, vv, gmu[bi], hp.lr, hp.b1, hp.b2, hp.eps, c1, c2);
+    mu[bi] = th; am[bi] = mm; av[bi] = vv;
+    th = sigma[bi]; mm = am[half + bi]; vv = av[half + bi];
+    adam_update(th, mm, vv, gsig[bi], hp.lr, hp.b1, hp.b2, hp.eps, c1, c2);
+    sigma[bi] = fmaxf(th, hp.sigma_min);
+    am[half + bi] = mm; av[half + bi] = vv;
+    if (b == 0 && i == 0) *adam_t += 1;
+}
+
+// ---------------------------------------------------------------------------
+// Legalization (App. A).  One work-group per restart sweeps the topological
+// levels; ops of one level have no forward edges between them, so a level is
+// processed in parallel and the sweep equals the paper's sequential pass.
+// Modulo: back-edge requirements read the schedule as it was at the start of
+// the pass; the iteration is monotone and inflationary, so when it stops it has
+// reached the least fixed point above the clamped rounding, as Alg. 4 does.
+// ---------------------------------------------------------------------------
+constexpr int kLegBS = 1024;
+
+__device__ __forceinline__ long long round_half_up(float mu, int D) {
+    float m = fmaxf(mu, -1.0f);              // NaN -> -1
+    m = fminf(m, (float)D);
+    const float fl = floorf(m);
+    return (long long)fl + ((m - fl) >= 0.5f ? 1 : 0);
+}
+
+__global__ __launch_bounds__(kLegBS) void k_legalize(Graph G, Work W, const float *__restrict__ mu,
+                                                     int *sched) {
+    __shared__ int changed, over;
+    const int b = blockIdx.x, tid = threadIdx.x;
+    const int N = G.N, D = G.D;
+    long long *s = W.s64 + (size_t)b * N;
+    long long *sp = W.s64b + (size_t)b * N;
+    for (int v = tid; v < N; v += kLegBS) {
+        long long r = round_half_up(mu[(size_t)b * N + v], D);
+        const long long lo = G.II == 0 ? G.asap[v] : 0, hi = G.II == 0 ? G.alap[v] : D - 1;
+        r = r < lo ? lo : (r > hi ? hi : r);
+        s[v] = r;
+    }
+    __syncthreads();
+    int st = 0;
+    if (G.II == 0) {
+        for (int l = 1; l < G.nlevels; ++l) {
+            for (int q = G.lvl_ptr[l] + tid; q < G.lvl_ptr[l + 1]; q += kLegBS) {
+                const int v = G.lvl_ops[q];
+                long long req = s[v];
+                for (int r = G.pred_ptr[v]; r < G.pred_ptr[v + 1]; ++r) {
+                    const int u = G.pred_src[r];
+                    const long long c = s[u] + G.delay[u];
+                    req = c > req ? c : req;
+                }
+                s[v] = req;
+            }
+            __syncthreads();
+        }
+    } else {
+        int converged = 0;
+        for (int pass = 0; pass < (N > 0 ? N : 1); ++pass) {
+            for (int v = tid; v < N; v += kLegBS) sp[v] = s[v];
+            if (tid == 0) changed = 0;
+            __syncthreads();
+            for (int l = 0; l < G.nlevels; ++l) {
+                for (int q = G.lvl_ptr[l] + tid; q < G.lvl_ptr[l + 1]; q += kLegBS) {
+                    const int v = G.lvl_ops[q];
+                    long long req = 0;
+                    for (int r = G.pred_ptr[v]; r < G.pred_ptr[v + 1]; ++r) {
+                        const int u = G.pred_src[r];
+                        const long long c = s[u] + G.delay[u];
+                        req = c > req ? c : req;
+                    }
+                    for (int r = G.bin_ptr[v]; r < G.bin_ptr[v + 1]; ++r) {
+                        const int e = G.bin[r], j = G.bsrc[e];
+                        const long long c = sp[j] + G.delay[j] - (long long)G.bdist[e] * G.II;
+                        req = c > req ? c : req;
+                    }
+                    if (req > s[v]) { s[v] = req; changed = 1; }
+                }
+                __syncthreads();
+            }
+            const int ch = changed;
+            __syncthreads();
+            if (!ch) { converged = 1; break; }
+        }
+        if (!converged) {
+            st = 4;  // GAUS_E_NOT_CONVERGED
+        } else {
+            if (tid == 0) over = 0;
+            __syncthreads();
+            for (int v = tid; v < N; v += kLegBS)
+                if (s[v] > D - 1) over = 1;
+            __syncthreads();
+            st = over ? 5 : 0;  // GAUS_E_OVERFLOW
+        }
+    }
+    for (int v = tid; v < N; v += kLegBS) {
+        const long long x = s[v];
+        sched[(size_t)b * N + v] = x > 2147483647LL ? 2147483647 : (int)x;
+    }
+    if (tid == 0) W.status[b] = st;
+}
+
+// ---------------------------------------------------------------------------
+// Host-side enqueue helpers
+// ---------------------------------------------------------------------------
+template <int BS, int SPT>
+static void launch_ops(const Graph &g, const Work &w, const float *mu, const float *sigma,
+                       hipStream_t st) {
+    dim3 grid(g.ngroups, g.ntiles, g.B);
+    hipLaunchKernelGGL((k_ops<BS, SPT>), grid, dim3(BS), 0, st, g, mu, sigma, w);
+    if (g.nb > 0) {
+        const int epb = 4;
+        dim3 gb((g.nb + epb - 1) / epb, g.ntiles, g.B);
+        hipLaunchKernelGGL((k_back<BS, SPT>), gb, dim3(BS), 0, st, g, mu, sigma, w, epb);
+    }
+}
+
+hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const LaunchCfg &lc,
+                             const IterArgs &a, hipStream_t st) {
+    if (lc.bs == 64 && lc.spt == 1) launch_ops<64, 1>(g, w, a.mu, a.sigma, st);
+    else if (lc.bs == 256 && lc.spt == 1) launch_ops<256, 1>(g, w, a.mu, a.sigma, st);
+    else if (lc.bs == 256 && lc.spt == 4) launch_ops<256, 4>(g, w, a.mu, a.sigma, st);
+    else return hipErrorInvalidValue;
+    {
+        const int cells = g.K * g.T;
+        dim3 grid((cells + 255) / 256, g.B);
+        hipLaunchKernelGGL(k_usage, grid, dim3(256), 0, st, g, w);
+    }
+    hipLaunchKernelGGL(k_terms, dim3(g.B), dim3(kTermsBS), 0, st, g, w, hp, a.lambda_in,
+                       a.mode == 1 ? a.lambda_out : nullptr, a.mode == 1 ? a.adam_t : nullptr,
+                       a.terms_out);
+    {
+        dim3 grid((g.N + 255) / 256, g.B);
+        hipLaunchKernelGGL(k_final, grid, dim3(256), 0, st, g, w, hp, a.mu, a.sigma, a.gmu, a.gsig,
+                           a.mu_io, a.sig_io, a.m, a.v, a.adam_t, a.mode);
+    }
+    return hipGetLastError();
+}
+
+hipError_t enqueue_adam_from_grad(const Graph &g, const Work &w, const HP &hp, const float *gmu,
+                                  const float *gsig, const float *terms, float *mu, float *sigma,
+                                  float *m, float *v, float *lambda, int *adam_t, hipStream_t st) {
+    hipLaunchKernelGGL(k_lambda_from_terms, dim3((g.B + 255) / 256), dim3(256), 0, st, g.B, hp,
+                       terms, lambda, adam_t, w.adamf);
+    dim3 grid((g.N + 255) / 256, g.B);
+    hipLaunchKernelGGL(k_adam, grid, dim3(256), 0, st, g.B, g.N, hp, w.adamf, gmu, gsig, mu, sigma,
+                       m, v, adam_t);
+    return hipGetLastError();
+}
+
+hipError_t enqueue_legalize(const Graph &g, const Work &w, const float *mu, int *sched,
+                            hipStream_t st) {
+    hipLaunchKernelGGL(k_legalize, dim3(g.B), dim3(kLegBS), 0, st, g, w, mu, sched);
+    return hipGetLastError();
+}
+
+}  // namespace gaus

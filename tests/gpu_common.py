@@ -1,0 +1,65 @@
+"""Shared helpers of the GPU parity tests: run the HIP path through the C ABI
+and the CPU oracle on the same seeded inputs, and compare them."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+
+from paper_2602_20427_amd import binding as bd
+
+# fp32 GPU vs fp64 oracle: loss terms within 1e-5 of max(|x*|, 1), gradients
+# within 1e-5 of the largest gradient entry (per restart and tensor), usage
+# normwise, Adam elementwise from the same gradient.
+TOL = 1e-5
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def hparams(alpha=0.01, rho=1e-4, lr=1e-2):
+    hp = bd.default_hparams()
+    hp.alpha_com = alpha
+    hp.rho = rho
+    hp.lr = lr
+    return hp
+
+
+def gpu_loss_grad(prob, mu, sigma, lam, hp):
+    import torch
+    B, N = mu.shape
+    ctx = bd.Context(prob, B, hp)
+    dev = torch.device("cuda")
+    m = torch.from_numpy(np.ascontiguousarray(mu, np.float32)).to(dev)
+    s = torch.from_numpy(np.ascontiguousarray(sigma, np.float32)).to(dev)
+    l = torch.from_numpy(np.ascontiguousarray(lam, np.float32)).to(dev)
+    terms = torch.zeros(B, 5, device=dev)
+    gm = torch.zeros(B, N, device=dev)
+    gs = torch.zeros(B, N, device=dev)
+    ctx.loss_grad(m, s, l, terms, gm, gs)
+    U = torch.zeros(B, ctx.K, ctx.T, device=dev)
+    ctx.get_usage(U)
+    ctx.sync()
+    out = dict(terms=terms.cpu().numpy().astype(np.float64), gm=gm.cpu().numpy().astype(np.float64),
+               gs=gs.cpu().numpy().astype(np.float64), U=U.cpu().numpy().astype(np.float64))
+    ctx.close()
+    return out
+
+
+def compare_restart(g, o_terms, o_U, o_gm, o_gs, b, what=""):
+    """Assert the parity bar for restart b; returns the worst relative errors."""
+    t, ot = g["terms"][b], o_terms
+    err_t = np.abs(t - ot) / np.maximum(np.abs(ot), 1.0)
+    names = ["L", "V_dep", "V_res", "V_rec", "L_com"]
+    assert err_t.max() <= TOL, f"{what} b={b} terms {dict(zip(names, t))} vs {dict(zip(names, ot))} err {err_t}"
+    eu = np.abs(g["U"][b] - o_U).max() / max(np.abs(o_U).max(), 1.0)
+    assert eu <= TOL, f"{what} b={b} usage err {eu}"
+    res = {"terms": float(err_t.max()), "U": float(eu)}
+    for name, gg, oo in (("g_mu", g["gm"][b], o_gm), ("g_sigma", g["gs"][b], o_gs)):
+        scale = np.abs(oo).max()
+        e = np.abs(gg - oo).max() / scale if scale > 0 else np.abs(gg).max()
+        assert e <= TOL, f"{what} b={b} {name} normwise err {e} (scale {scale})"
+        res[name] = float(e)
+    return res

@@ -1,0 +1,292 @@
+"""Parity of the gfx950 HIP path (through the C ABI) with the fp64 CPU oracle
+on identical seeded inputs."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2602_20427_amd import binding as bd
+from paper_2602_20427_amd.workloads import (CONFIGS, Problem, make_problem, random_state,
+                                            restart_uniforms, uniform_state)
+from tests.gpu_common import TOL, compare_restart, gpu_loss_grad, hparams, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    oracle.build(force=False)
+    bd.load()
+    yield
+
+
+def _check(prob, mu, sigma, lam, hp, restarts, what):
+    say(f"[parity] {what}: N={prob.n_ops} E={prob.n_edges} nb={prob.n_back} D={prob.D} II={prob.II} B={mu.shape[0]}")
+    g = gpu_loss_grad(prob, mu, sigma, lam, hp)
+    compared = 0
+    for b in restarts:
+        ot, oU, ogm, ogs, ties = oracle.loss_grad(prob, mu[b:b + 1].astype(np.float64),
+                                                  sigma[b:b + 1].astype(np.float64), lam[b:b + 1],
+                                                  hp.alpha_com, hp.rho, tie_tol=1e-4)
+        if ties[0]:
+            say(f"  b={b}: {ties[0]} near-tie usage cells, comparing terms/usage only")
+            err_t = np.abs(g["terms"][b] - ot[0]) / np.maximum(np.abs(ot[0]), 1.0)
+            assert err_t.max() <= TOL
+            continue
+        r = compare_restart(g, ot[0], oU[0], ogm[0], ogs[0], b, what)
+        say(f"  b={b}: " + " ".join(f"{k}={v:.2e}" for k, v in r.items()))
+        compared += 1
+    assert compared >= 1
+    return g
+
+
+def _lam(B, seed, lo=0.05, hi=1.0):
+    return np.random.default_rng(seed).uniform(lo, hi, size=(B, 3)).astype(np.float32)
+
+
+@pytest.mark.parametrize("cfg", ["tiny", "small"])
+def test_loss_grad_random_state(cfg):
+    """Narrow and mixed regimes: random mu (some outside the horizon), sigma in [0.3, 8]."""
+    p = make_problem(cfg, seed=0)
+    B = CONFIGS[cfg].B
+    mu, sg = random_state(p.n_ops, p.D, B, seed=1)
+    _check(p, mu, sg, _lam(B, 2), hparams(alpha=0.37, rho=0.05), range(B), f"{cfg}/random")
+
+
+@pytest.mark.parametrize("cfg", ["tiny", "small", "medium", "pipelined"])
+def test_loss_grad_paper_init(cfg):
+    """Timing state: the paper's ASAP/ALAP initialization (dense regime)."""
+    p = make_problem(cfg, seed=0)
+    B = CONFIGS[cfg].B
+    if CONFIGS[cfg].init == "uniform":
+        mu, sg = uniform_state(p.n_ops, p.D, B, seed=0, sigma0=CONFIGS[cfg].sigma0)
+    else:
+        u = restart_uniforms(p.n_ops, B, seed=0)
+        mu, sg, rc = oracle.init_state(p, B, u)
+        assert rc == 0
+        mu, sg = mu.astype(np.float32), sg.astype(np.float32)
+    restarts = [0, B - 1] if B > 2 else range(B)
+    _check(p, mu, sg, _lam(B, 3), hparams(alpha=0.01, rho=1e-3), restarts, f"{cfg}/init")
+
+
+def test_loss_grad_pipelined_random():
+    p = make_problem("pipelined", seed=0)
+    B = 4
+    mu, sg = random_state(p.n_ops, p.D, B, seed=5, sigma_range=(0.5, 40.0))
+    _check(p, mu, sg, _lam(B, 6), hparams(alpha=0.2, rho=0.01), range(B), "pipelined/random")
+
+
+def _ragged_problem(seed, N=700, D=1500, II=0, n_back=0, big_delay=True):
+    """Several tiles with a ragged tail (D % 1024 != 0), type-group
+    boundaries, sinks, and a few producer delays above the LDS halo."""
+    rng = np.random.default_rng(seed)
+    rows = []
+    for i in range(N):
+        k = rng.poisson(2.0)
+        tg = np.unique(rng.integers(i + 1, min(N, i + 60), size=k)) if i < N - 1 else np.zeros(0, int)
+        rows.append(tg)
+    row_ptr = np.zeros(N + 1, np.int32)
+    row_ptr[1:] = np.cumsum([len(r) for r in rows])
+    col = np.concatenate(rows).astype(np.int32)
+    delay = rng.integers(0, 4, size=N).astype(np.int32)
+    if big_delay:
+        delay[rng.choice(N - 100, size=3, replace=False)] = [300, 257, 600]
+    rtype = rng.integers(0, 3, size=N).astype(np.int32)
+    cap = np.array([3.0, 1.5, 0.7], np.float32)
+    bs, bd_, bk = [], [], []
+    for _ in range(n_back):
+        j = int(rng.integers(1, N)); i = int(rng.integers(0, j))
+        bs.append(j); bd_.append(i); bk.append(int(rng.integers(1, 4)))
+    return Problem(n_ops=N, row_ptr=row_ptr, col_idx=col, delay=delay, rtype=rtype, capacity=cap, D=D, II=II,
+                   back_src=np.array(bs, np.int32), back_dst=np.array(bd_, np.int32),
+                   back_dist=np.array(bk, np.int32))
+
+
+@pytest.mark.parametrize("II,n_back", [(0, 0), (37, 25), (2000, 10)])
+def test_loss_grad_ragged_tiles_and_big_delays(II, n_back):
+    p = _ragged_problem(11 + II, II=II, n_back=n_back)
+    B = 3
+    rng = np.random.default_rng(12)
+    mu = rng.uniform(-20, p.D + 20, size=(B, p.n_ops)).astype(np.float32)
+    sg = np.exp(rng.uniform(np.log(0.2), np.log(300.0), size=(B, p.n_ops))).astype(np.float32)
+    _check(p, mu, sg, _lam(B, 13), hparams(alpha=0.3, rho=0.02), range(B), f"ragged II={II}")
+
+
+def test_small_edge_cases():
+    """D = 1 (one bin holds all mass), a single op, no edges."""
+    for D, N, with_edges in ((1, 5, True), (2, 1, False), (3, 4, False), (64, 1, False)):
+        rows = [[j for j in range(i + 1, N) if (i + j) % 2] if with_edges else [] for i in range(N)]
+        row_ptr = np.zeros(N + 1, np.int32); row_ptr[1:] = np.cumsum([len(r) for r in rows])
+        col = np.array([j for r in rows for j in r], np.int32)
+        p = Problem(n_ops=N, row_ptr=row_ptr, col_idx=col, delay=np.zeros(N, np.int32),
+                    rtype=np.zeros(N, np.int32), capacity=np.array([0.5], np.float32), D=D)
+        mu, sg = random_state(N, D, 2, seed=D + N)
+        _check(p, mu, sg, _lam(2, 4), hparams(alpha=0.5, rho=0.1), range(2), f"edge D={D} N={N}")
+
+
+def test_sigma_to_zero_usage_bit_exact():
+    """sigma -> 0: usage is the integer histogram of the rounded schedule,
+    bit for bit; the violation and edge-length terms are exact counts."""
+    for II in (0, 5):
+        p = _ragged_problem(21, N=300, D=200, II=II, n_back=8 if II else 0, big_delay=False)
+        rng = np.random.default_rng(22)
+        s_int = rng.integers(-3, 205, size=(2, p.n_ops))
+        mu = (s_int + rng.uniform(-0.4, 0.4, size=s_int.shape)).astype(np.float32)
+        sg = np.full(mu.shape, 1e-5, np.float32)
+        g = gpu_loss_grad(p, mu, sg, np.zeros((2, 3), np.float32), hparams(alpha=0.0, rho=0.0))
+        for b in range(2):
+            ot, oU, *_ = oracle.loss_grad(p, mu[b:b + 1].astype(np.float64), sg[b:b + 1].astype(np.float64),
+                                          [0, 0, 0], 0.0, 0.0, grad=False)
+            assert np.array_equal(g["U"][b], oU[0])
+            # V_dep, V_rec, L_com are integer counts; V_res = sum (U - C)^+ has
+            # non-integer capacities and is compared within the float tolerance
+            for c in (1, 3, 4):
+                assert g["terms"][b][c] == ot[0][c], (c, g["terms"][b], ot[0])
+            assert abs(g["terms"][b][2] - ot[0][2]) <= TOL * max(ot[0][2], 1.0)
+            assert np.all(g["gm"][b] == 0) and np.all(g["gs"][b] == 0)
+
+
+def test_deterministic_bitwise():
+    p = make_problem("small", seed=3)
+    mu, sg = random_state(p.n_ops, p.D, 4, seed=3, sigma_range=(0.5, 60))
+    lam = _lam(4, 3)
+    a = gpu_loss_grad(p, mu, sg, lam, hparams())
+    b = gpu_loss_grad(p, mu, sg, lam, hparams())
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
+
+
+def _state(ctx, mu, sg, lam):
+    import torch
+    dev = torch.device("cuda")
+    B, N = mu.shape
+    st = dict(mu=torch.from_numpy(mu).to(dev), sigma=torch.from_numpy(sg).to(dev),
+              m=torch.zeros(2, B, N, device=dev), v=torch.zeros(2, B, N, device=dev),
+              lam=torch.from_numpy(lam).to(dev), t=torch.zeros(1, dtype=torch.int32, device=dev))
+    ctx.bind_state(st["mu"], st["sigma"], st["m"], st["v"], st["lam"], st["t"])
+    return st
+
+
+def test_adam_from_grad_matches_oracle():
+    """Adam (Kingma & Ba) + sigma clamp + lambda update, fed the GPU's own
+    gradient, against the fp64 oracle's Adam on the same gradient."""
+    import torch
+    p = make_problem("small", seed=4)
+    B = 4
+    hp = hparams(alpha=0.1, rho=0.01, lr=0.05)
+    mu, sg = random_state(p.n_ops, p.D, B, seed=4, sigma_range=(0.04, 30))
+    lam = _lam(B, 5)
+    ctx = bd.Context(p, B, hp)
+    st = _state(ctx, mu.copy(), sg.copy(), lam.copy())
+    dev = torch.device("cuda")
+    terms = torch.zeros(B, 5, device=dev)
+    gm = torch.zeros(B, p.n_ops, device=dev); gs = torch.zeros(B, p.n_ops, device=dev)
+    m_o = np.zeros((2, B, p.n_ops)); v_o = np.zeros((2, B, p.n_ops))
+    th_mu, th_sg, lam_o = mu.astype(np.float64), sg.astype(np.float64), lam.astype(np.float64)
+    for it in range(1, 4):
+        ctx.loss_grad(st["mu"], st["sigma"], st["lam"], terms, gm, gs)
+        ctx.adam_from_grad(gm, gs, terms)
+        ctx.sync()
+        g1 = gm.cpu().numpy().astype(np.float64); g2 = gs.cpu().numpy().astype(np.float64)
+        tt = terms.cpu().numpy().astype(np.float64)
+        # oracle Adam from the GPU gradient, starting from the GPU's pre-step state
+        for b in range(B):
+            th_mu[b], m_o[0, b], v_o[0, b] = oracle.adam(th_mu[b], m_o[0, b], v_o[0, b], g1[b], it, hp.lr)
+            th_sg[b], m_o[1, b], v_o[1, b] = oracle.adam(th_sg[b], m_o[1, b], v_o[1, b], g2[b], it, hp.lr)
+        th_sg = np.maximum(th_sg, float(np.float32(hp.sigma_min)))
+        lam_o = lam_o + float(np.float32(hp.rho)) * tt[:, 1:4]
+        gmu_ = st["mu"].cpu().numpy(); gsg_ = st["sigma"].cpu().numpy()
+        assert np.all(np.abs(gmu_ - th_mu) <= TOL * np.maximum(np.abs(th_mu), 1.0))
+        assert np.all(np.abs(gsg_ - th_sg) <= TOL * np.maximum(np.abs(th_sg), 1.0))
+        assert np.allclose(st["lam"].cpu().numpy(), lam_o, rtol=1e-6, atol=1e-7)
+        assert int(st["t"].item()) == it
+        # continue from the GPU state so that rounding does not accumulate
+        th_mu, th_sg = gmu_.astype(np.float64), gsg_.astype(np.float64)
+        m_o = st["m"].cpu().numpy().astype(np.float64); v_o = st["v"].cpu().numpy().astype(np.float64)
+    ctx.close()
+
+
+def test_step_equals_loss_grad_plus_adam_bitwise():
+    """gaus_step fuses exactly loss_grad + adam_from_grad (same kernels)."""
+    import torch
+    p = make_problem("pipelined", seed=1, n_ops=800)
+    B = 3
+    hp = hparams(alpha=0.05, rho=0.01, lr=0.02)
+    mu, sg = random_state(p.n_ops, p.D, B, seed=8, sigma_range=(0.3, 50))
+    lam = _lam(B, 9)
+    ca = bd.Context(p, B, hp); sa = _state(ca, mu.copy(), sg.copy(), lam.copy())
+    cb = bd.Context(p, B, hp); sb = _state(cb, mu.copy(), sg.copy(), lam.copy())
+    dev = torch.device("cuda")
+    terms_a = torch.zeros(B, 5, device=dev)
+    ca.step(5, terms_a)
+    terms = torch.zeros(B, 5, device=dev)
+    gm = torch.zeros(B, p.n_ops, device=dev); gs = torch.zeros(B, p.n_ops, device=dev)
+    for _ in range(5):
+        cb.loss_grad(sb["mu"], sb["sigma"], sb["lam"], terms, gm, gs)
+        cb.adam_from_grad(gm, gs, terms)
+    ca.sync(); cb.sync()
+    for k in ("mu", "sigma", "m", "v", "lam", "t"):
+        assert torch.equal(sa[k], sb[k]), k
+    assert torch.equal(terms_a, terms)
+    ca.close(); cb.close()
+
+
+@pytest.mark.parametrize("cfg,II", [("small", 0), ("medium", 0), ("pipelined", 64)])
+def test_legalize_bit_exact(cfg, II):
+    import torch
+    p = make_problem(cfg, seed=2)
+    B = 4
+    rng = np.random.default_rng(30)
+    mu = rng.uniform(-3, p.D + 3, size=(B, p.n_ops)).astype(np.float32)
+    mu[0, :50] = np.floor(mu[0, :50]) + 0.5           # exact ties round up
+    mu[1, :5] = [np.nan, np.inf, -np.inf, 0.49999997, -0.5]
+    if B > 2:                                          # a nearly legal restart
+        a, l, _ = oracle.asap_alap(p)
+        mu[2] = ((a + l) / 2).astype(np.float32)
+    say(f"[legalize] {cfg} N={p.n_ops} nb={p.n_back} II={p.II}")
+    ctx = bd.Context(p, B, hparams())
+    dev = torch.device("cuda")
+    sched = torch.zeros(B, p.n_ops, dtype=torch.int32, device=dev)
+    st = ctx.legalize(torch.from_numpy(mu).to(dev), sched)
+    s_o, st_o = oracle.legalize(p, mu)
+    assert np.array_equal(st, st_o), (st, st_o)
+    for b in range(B):
+        if st_o[b] in (0, 5):   # converged: the least fixed point is unique
+            assert np.array_equal(sched[b].cpu().numpy().astype(np.int64), s_o[b]), b
+    ctx.close()
+
+
+def test_legalize_infeasible_recurrence():
+    """A recurrence that no II-periodic schedule satisfies never converges."""
+    import torch
+    p = Problem(n_ops=3, row_ptr=np.array([0, 1, 2, 2], np.int32), col_idx=np.array([1, 2], np.int32),
+                delay=np.array([5, 1, 1], np.int32), rtype=np.zeros(3, np.int32),
+                capacity=np.array([1.0], np.float32), D=40, II=2, back_src=np.array([1], np.int32),
+                back_dst=np.array([0], np.int32), back_dist=np.array([1], np.int32))
+    ctx = bd.Context(p, 1, hparams())
+    sched = torch.zeros(1, 3, dtype=torch.int32, device="cuda")
+    st = ctx.legalize(torch.tensor([[0.0, 6.0, 8.0]], device="cuda"), sched)
+    _, st_o = oracle.legalize(p, np.array([[0.0, 6.0, 8.0]], np.float32))
+    assert st[0] == st_o[0] == bd.E_NOT_CONVERGED
+    ctx.close()
+
+
+def test_init_state_matches_oracle():
+    import torch
+    p = make_problem("medium", seed=0)
+    B = 3
+    u = restart_uniforms(p.n_ops, B, seed=0)
+    ctx = bd.Context(p, B, hparams())
+    mu = torch.zeros(B, p.n_ops, device="cuda"); sg = torch.zeros(B, p.n_ops, device="cuda")
+    ctx.init_state(mu, sg, u)
+    hp = hparams()
+    mo, so, rc = oracle.init_state(p, B, u, kappa=float(np.float32(hp.kappa)),
+                                   sigma_min=float(np.float32(hp.sigma_min)))
+    assert rc == 0
+    assert np.array_equal(mu.cpu().numpy(), mo.astype(np.float32))
+    assert np.array_equal(sg.cpu().numpy(), so.astype(np.float32))
+    a, l = ctx.asap_alap()
+    ao, lo, _ = oracle.asap_alap(p)
+    assert np.array_equal(a, ao) and np.array_equal(l, lo)
+    ctx.close()
