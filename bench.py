@@ -1,0 +1,222 @@
+#!/usr/bin/env python3
+"""Throughput of the GauS hot path on one MI355X.
+
+One step = one iteration of the relaxed-schedule optimization for all B
+restarts of a synthetic workload: CDFs and masses of every (restart, op,
+step), folded usage and the capacity penalty, dependency / recurrence /
+edge-length terms over the edges, the analytic gradient, Adam and the
+multiplier update (gaus_step).  The timed region also runs one rounding +
+legalization of every restart (gaus_legalize), so every step of the path is
+inside it.  Inputs are resident in HBM before timing starts.
+
+Prints one JSON line with the metric (op-step evaluations per second =
+B*N*D / seconds per step), the roofline of the dominant kernel (the op
+kernel, timed with HIP events on the library's stream) and the CPU oracle
+timed on a bounded sample of the same workload.
+
+  python bench.py [--steps K] [--warmup W] [--workload large]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+METRIC = "op-step evals/sec (fwd+bwd+Adam), ms/iteration, % roofline at 50k ops"
+
+# VALU cost model of one iteration (per-unit algorithmic work):
+#   per op-bin-edge (B*N*(D-1) units): 20 FMA-class instructions plus 2
+#     transcendental evaluations (the CDF needs an exp and a reciprocal; the
+#     Gaussian factor of the gradient shares the exp);
+#   per edge-step (B*(E+E_B)*(D-1) units): 10 FMA-class instructions (the
+#     products and sums of the edge terms and their derivatives, with both
+#     end points' rows available).
+# A transcendental occupies TRANS_WEIGHT FMA issue slots: the measured ratio of
+# the v_fma_f32 to the v_exp_f32 rate on gfx950 (gaus_microbench:
+# 100.4 vs 21.2 per clock per CU).  One slot = one fp32 FMA = 2 flops; the
+# peak is MI355X's 157.3 TFLOP/s fp32 vector rate.
+FMA_PER_OP_STEP = 20.0
+TRANS_PER_OP_STEP = 2.0
+FMA_PER_EDGE_STEP = 10.0
+TRANS_WEIGHT = 100.4 / 21.2
+PEAK_TFLOPS = 157.3
+PMC_SUMMARY = os.path.join(ROOT, "profiles", "k_ops_large_pmc.md")
+KERNEL_SRC = os.path.join(ROOT, "paper_2602_20427_amd", "csrc", "gaus_kernels.hip")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def algorithmic_flops(N, E, nb, D, B):
+    units_op = B * N * (D - 1)
+    units_edge = B * (E + nb) * (D - 1)
+    slots = units_op * (FMA_PER_OP_STEP + TRANS_PER_OP_STEP * TRANS_WEIGHT) + units_edge * FMA_PER_EDGE_STEP
+    return 2.0 * slots
+
+
+def pmc_traffic(workload):
+    """HBM bytes per op-kernel launch from the committed rocprofv3 counter
+    summary, if it was taken on the current kernel source; else None."""
+    if workload != "large" or not os.path.exists(PMC_SUMMARY):
+        return None
+    txt = open(PMC_SUMMARY).read()
+    h = re.search(r"kernel_source_sha256:\s*([0-9a-f]+)", txt)
+    v = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", txt)
+    if not h or not v or h.group(1) != kernel_source_hash():
+        return None
+    return float(v.group(1))
+
+
+def describe(cfg, prob):
+    return (f"{cfg.name}: random layered DAG, {prob.n_ops} ops, {cfg.n_layers} layers, "
+            f"out-degree Poisson({cfg.out_degree}), {prob.n_edges} edges, {prob.n_back} back edges, "
+            f"{prob.n_types} resource types, D={prob.D}, II={prob.II}, B={cfg.B} restarts, "
+            f"fp32, paper initialization (sigma = kappa*(ALAP-ASAP))" if cfg.init != "uniform" else
+            f"{cfg.name}: random layered DAG, {prob.n_ops} ops, D={prob.D}, B={cfg.B}, mu~U[0,D), sigma={cfg.sigma0}")
+
+
+def cpu_baseline(prob, mu, sigma, lam, hp, n_restarts):
+    """The oracle as it stands, on n_restarts of the workload: one fused
+    iteration (loss, gradient, Adam) each from the same state."""
+    import numpy as np
+    import oracle
+    oracle.build(force=False)
+    t0 = time.perf_counter()
+    for b in range(n_restarts):
+        _, _, gm, gs, _ = oracle.loss_grad(prob, mu[b:b + 1].astype(np.float64), sigma[b:b + 1].astype(np.float64),
+                                           lam[b:b + 1].astype(np.float64), hp.alpha_com, hp.rho)
+        z = np.zeros(prob.n_ops)
+        oracle.adam(mu[b].astype(np.float64), z, z, gm[0], 1, hp.lr)
+        oracle.adam(sigma[b].astype(np.float64), z, z, gs[0], 1, hp.lr)
+    dt = time.perf_counter() - t0
+    return {"value": n_restarts * prob.n_ops * prob.D / dt, "unit": "op-step evals/s",
+            "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"{n_restarts} of {mu.shape[0]} restarts of the same workload and state, one fused "
+                      f"iteration (loss, gradient, Adam) each, fp64 C oracle with OpenMP; {dt:.2f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="large")
+    ap.add_argument("--cpu-restarts", type=int, default=2, help="restarts in the CPU-oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="after the run, copy this many MiB once (counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build runs the scheduling hot path on one GPU; multi-GPU runs "
+              "(--gpus > 1) are not supported", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2602_20427_amd import binding as bd
+    from paper_2602_20427_amd.workloads import CONFIGS, make_problem, restart_uniforms, uniform_state
+
+    assert torch.cuda.is_available(), "bench.py needs an MI355X"
+    cfg = CONFIGS[args.workload]
+    log(f"[bench] workload {cfg.name}: building problem")
+    prob = make_problem(cfg, seed=0)
+    B, N, D = cfg.B, prob.n_ops, prob.D
+    hp = bd.default_hparams()
+    hp.lr = cfg.lr
+    dev = torch.device("cuda")
+    ctx = bd.Context(prob, B, hp)
+    mu = torch.zeros(B, N, device=dev)
+    sigma = torch.zeros(B, N, device=dev)
+    if cfg.init == "uniform":
+        m0, s0 = uniform_state(N, D, B, seed=0, sigma0=cfg.sigma0)
+        mu.copy_(torch.from_numpy(m0)); sigma.copy_(torch.from_numpy(s0))
+    else:
+        ctx.init_state(mu, sigma, restart_uniforms(N, B, seed=0))
+    lam = torch.full((B, 3), hp.lambda0, device=dev)
+    m = torch.zeros(2, B, N, device=dev)
+    v = torch.zeros(2, B, N, device=dev)
+    t = torch.zeros(1, dtype=torch.int32, device=dev)
+    # state of the CPU-baseline sample: the timing state before any step
+    mu0, sg0, lam0 = mu.cpu().numpy(), sigma.cpu().numpy(), lam.cpu().numpy()
+    ctx.bind_state(mu, sigma, m, v, lam, t)
+    terms = torch.zeros(B, 5, device=dev)
+    sched = torch.zeros(B, N, dtype=torch.int32, device=dev)
+
+    log(f"[bench] warmup {args.warmup} steps")
+    ctx.step(args.warmup, terms)
+    ctx.sync()
+    torch.cuda.synchronize()
+
+    log(f"[bench] timing {args.steps} steps + 1 legalization")
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    ctx.kernel_timing(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev[0].record(stream)
+    ctx.step(args.steps, terms)
+    ev[1].record(stream)
+    status = ctx.legalize(mu, sched)
+    ev[2].record(stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ops_ms_total, ops_launches = ctx.kernel_timing_read()
+    ctx.kernel_timing(False)
+    step_ms_events = ev[0].elapsed_time(ev[1]) / args.steps
+    legalize_ms = ev[1].elapsed_time(ev[2])
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    tt = terms.cpu().numpy()
+    log(f"[bench] {ms_per_step:.3f} ms/step wall; gaus_step {step_ms_events:.3f} ms/iter (events); "
+        f"legalize {legalize_ms:.3f} ms; op kernel {ops_ms_total / max(ops_launches, 1):.3f} ms x {ops_launches}")
+    log(f"[bench] last terms restart 0: L={tt[0, 0]:.6g} V_dep={tt[0, 1]:.6g} V_res={tt[0, 2]:.6g} "
+        f"V_rec={tt[0, 3]:.6g} L_com={tt[0, 4]:.6g}; legalize status {status.tolist()}")
+
+    value = B * N * D / (ms_per_step * 1e-3)
+    ops_ms = ops_ms_total / max(ops_launches, 1)
+    flops = algorithmic_flops(N, prob.n_edges, prob.n_back, D, B)
+    achieved = flops / (ops_ms * 1e-3) / 1e12
+    traffic = pmc_traffic(args.workload)
+    out = {
+        "metric": METRIC, "value": value, "unit": "op-step evals/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": describe(cfg, prob), "B": B, "N": N, "E": prob.n_edges,
+                   "n_back": prob.n_back, "D": D, "II": prob.II},
+        "ms_per_iteration_events": step_ms_events, "legalize_ms": legalize_ms,
+        "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / PEAK_TFLOPS, "traffic": traffic,
+                     "kernel": "k_ops", "kernel_ms": ops_ms,
+                     "model": f"{FMA_PER_OP_STEP:g} FMA + {TRANS_PER_OP_STEP:g} transcendental "
+                              f"(x{TRANS_WEIGHT:.2f} FMA slots) per op-bin-edge, {FMA_PER_EDGE_STEP:g} FMA per "
+                              f"edge-step, 2 flops per FMA slot"},
+    }
+    if not args.no_cpu_baseline:
+        log(f"[bench] CPU oracle on {args.cpu_restarts} restarts")
+        out["cpu_baseline"] = cpu_baseline(prob, mu0, sg0, lam0, hp, min(args.cpu_restarts, B))
+    if args.copy_probe_mib > 0:
+        n = args.copy_probe_mib * (1 << 20) // 4
+        a = torch.ones(n, device=dev)
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        log(f"[bench] copy probe: {args.copy_probe_mib} MiB read + {args.copy_probe_mib} MiB written")
+    ctx.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

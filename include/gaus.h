@@ -150,6 +150,17 @@ gaus_status gaus_asap_alap(const gaus_ctx *ctx, int32_t *asap, int32_t *alap);
  * pass, copied to DEVICE memory U.  Asynchronous. */
 gaus_status gaus_get_usage(gaus_ctx *ctx, float *U);
 
+/* Profiling hook.  While enabled, every launch of the op kernel (the
+ * per-step kernel that dominates an iteration: CDFs, masses, usage, edge
+ * terms and their derivatives) is bracketed by a pair of HIP events recorded
+ * on the context's stream.  Enabling or disabling discards pending events. */
+gaus_status gaus_kernel_timing(gaus_ctx *ctx, int32_t enable);
+
+/* Total duration in milliseconds of the op-kernel launches bracketed since
+ * timing was enabled or last read, and their number (HOST outputs).
+ * Synchronizes the stream, then resets the accumulation. */
+gaus_status gaus_kernel_timing_read(gaus_ctx *ctx, double *total_ms, int32_t *launches);
+
 /* Wait for all work enqueued by this context; reports device errors. */
 gaus_status gaus_sync(gaus_ctx *ctx);
 

@@ -21,8 +21,8 @@ OK, E_INVALID_ARG, E_CYCLE, E_HORIZON, E_NOT_CONVERGED, E_OVERFLOW, E_DEVICE, E_
 # symbols declared in include/gaus.h
 EXPORTS = ("gaus_default_hparams", "gaus_init", "gaus_bind_state", "gaus_loss_grad", "gaus_step",
            "gaus_adam_from_grad", "gaus_legalize", "gaus_init_state", "gaus_asap_alap",
-           "gaus_get_usage", "gaus_sync", "gaus_get_dims", "gaus_last_error", "gaus_status_string",
-           "gaus_destroy")
+           "gaus_get_usage", "gaus_kernel_timing", "gaus_kernel_timing_read", "gaus_sync",
+           "gaus_get_dims", "gaus_last_error", "gaus_status_string", "gaus_destroy")
 
 
 class GausError(RuntimeError):
@@ -69,6 +69,8 @@ def load():
         "gaus_init_state": ([vp] * 4, C.c_int),
         "gaus_asap_alap": ([vp] * 3, C.c_int),
         "gaus_get_usage": ([vp] * 2, C.c_int),
+        "gaus_kernel_timing": ([vp, i32], C.c_int),
+        "gaus_kernel_timing_read": ([vp, vp, vp], C.c_int),
         "gaus_sync": ([vp], C.c_int),
         "gaus_get_dims": ([vp, vp], C.c_int),
         "gaus_last_error": ([vp], C.c_char_p),
@@ -218,6 +220,16 @@ class Context:
     def get_usage(self, U):
         import torch
         self._check(load().gaus_get_usage(self._h, _dptr(U, torch.float32, (self.B, self.K, self.T), "U")))
+
+    def kernel_timing(self, enable: bool):
+        self._check(load().gaus_kernel_timing(self._h, 1 if enable else 0))
+
+    def kernel_timing_read(self):
+        """(total milliseconds, launches) of the bracketed op-kernel launches."""
+        ms = C.c_double()
+        n = C.c_int32()
+        self._check(load().gaus_kernel_timing_read(self._h, C.byref(ms), C.byref(n)))
+        return ms.value, n.value
 
     def sync(self):
         self._check(load().gaus_sync(self._h))

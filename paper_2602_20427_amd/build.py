@@ -9,6 +9,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libgaus.so")
+MICROBENCH = os.path.join(PKG, "gaus_microbench")
 SOURCES = ["gaus_host.cpp", "gaus_kernels.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
@@ -44,6 +45,13 @@ def build(verbose: bool = False) -> str:
     os.replace(tmp, LIB)
     for o in objs:
         os.remove(o)
+    # unit-rate microbenchmark (standalone executable)
+    cmd = [HIPCC, *DEVICE_FLAGS, "-O3", "-std=c++17", "-o", MICROBENCH + ".tmp",
+           os.path.join(CSRC, "gaus_microbench.hip")]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"microbenchmark build failed:\n{r.stdout}{r.stderr}")
+    os.replace(MICROBENCH + ".tmp", MICROBENCH)
     return LIB
 
 

@@ -35,6 +35,10 @@ struct gaus_ctx {
     float *mu = nullptr, *sigma = nullptr, *m = nullptr, *v = nullptr, *lambda = nullptr;
     int *adam_t = nullptr;
     bool bound = false;
+    // op-kernel timing (gaus_kernel_timing)
+    bool timing = false;
+    std::vector<hipEvent_t> ev_pool;   // pairs: [2k] begin, [2k+1] end
+    size_t ev_used = 0;                 // pairs recorded since the last read
 };
 
 namespace {
@@ -57,6 +61,27 @@ gaus_status hip_fail(gaus_ctx *c, hipError_t e, const char *what) {
 void free_all(gaus_ctx *c) {
     for (void *p : c->allocs) (void)hipFree(p);
     c->allocs.clear();
+    for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
+    c->ev_pool.clear();
+    c->ev_used = 0;
+}
+
+// Next pair of timing events, or nulls when timing is off.
+hipError_t next_event_pair(gaus_ctx *c, hipEvent_t &b, hipEvent_t &e) {
+    b = e = nullptr;
+    if (!c->timing) return hipSuccess;
+    if (2 * c->ev_used + 2 > c->ev_pool.size()) {
+        for (int k = 0; k < 2; ++k) {
+            hipEvent_t ev;
+            hipError_t r = hipEventCreate(&ev);
+            if (r != hipSuccess) return r;
+            c->ev_pool.push_back(ev);
+        }
+    }
+    b = c->ev_pool[2 * c->ev_used];
+    e = c->ev_pool[2 * c->ev_used + 1];
+    c->ev_used++;
+    return hipSuccess;
 }
 
 template <class T>
@@ -374,7 +399,9 @@ gaus_status gaus_loss_grad(gaus_ctx *ctx, const float *mu, const float *sigma, c
     IterArgs a{};
     a.mu = mu; a.sigma = sigma; a.lambda_in = lambda; a.terms_out = terms;
     a.gmu = grad_mu; a.gsig = grad_sigma; a.mode = 0;
-    hipError_t e = enqueue_iteration(ctx->g, ctx->w, ctx->hp, ctx->lc, a, ctx->stream);
+    hipError_t e = next_event_pair(ctx, a.ops_begin, a.ops_end);
+    if (e != hipSuccess) return hip_fail(ctx, e, "timing events");
+    e = enqueue_iteration(ctx->g, ctx->w, ctx->hp, ctx->lc, a, ctx->stream);
     if (e != hipSuccess) return hip_fail(ctx, e, "loss_grad launch");
     return GAUS_OK;
 }
@@ -388,7 +415,9 @@ gaus_status gaus_step(gaus_ctx *ctx, int32_t n_iters, float *terms_last) {
         a.mu = ctx->mu; a.sigma = ctx->sigma; a.lambda_in = ctx->lambda; a.lambda_out = ctx->lambda;
         a.adam_t = ctx->adam_t; a.terms_out = (it == n_iters - 1) ? terms_last : nullptr;
         a.mu_io = ctx->mu; a.sig_io = ctx->sigma; a.m = ctx->m; a.v = ctx->v; a.mode = 1;
-        hipError_t e = enqueue_iteration(ctx->g, ctx->w, ctx->hp, ctx->lc, a, ctx->stream);
+        hipError_t e = next_event_pair(ctx, a.ops_begin, a.ops_end);
+        if (e != hipSuccess) return hip_fail(ctx, e, "timing events");
+        e = enqueue_iteration(ctx->g, ctx->w, ctx->hp, ctx->lc, a, ctx->stream);
         if (e != hipSuccess) return hip_fail(ctx, e, "step launch");
     }
     return GAUS_OK;
@@ -450,6 +479,33 @@ gaus_status gaus_get_usage(gaus_ctx *ctx, float *U) {
     const size_t bytes = sizeof(float) * (size_t)ctx->g.B * ctx->g.K * ctx->g.T;
     hipError_t e = hipMemcpyAsync(U, ctx->w.U, bytes, hipMemcpyDeviceToDevice, ctx->stream);
     if (e != hipSuccess) return hip_fail(ctx, e, "get_usage");
+    return GAUS_OK;
+}
+
+gaus_status gaus_kernel_timing(gaus_ctx *ctx, int32_t enable) {
+    if (!ctx) return GAUS_E_INVALID_ARG;
+    hipError_t e = hipStreamSynchronize(ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "kernel_timing");
+    ctx->timing = enable != 0;
+    ctx->ev_used = 0;
+    return GAUS_OK;
+}
+
+gaus_status gaus_kernel_timing_read(gaus_ctx *ctx, double *total_ms, int32_t *launches) {
+    if (!ctx) return GAUS_E_INVALID_ARG;
+    if (!total_ms || !launches) return fail(ctx, GAUS_E_INVALID_ARG, "kernel_timing_read: null pointer");
+    hipError_t e = hipStreamSynchronize(ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "kernel_timing_read");
+    double tot = 0.0;
+    for (size_t k = 0; k < ctx->ev_used; ++k) {
+        float ms = 0.0f;
+        e = hipEventElapsedTime(&ms, ctx->ev_pool[2 * k], ctx->ev_pool[2 * k + 1]);
+        if (e != hipSuccess) return hip_fail(ctx, e, "kernel_timing_read");
+        tot += ms;
+    }
+    *total_ms = tot;
+    *launches = (int32_t)ctx->ev_used;
+    ctx->ev_used = 0;
     return GAUS_OK;
 }
 

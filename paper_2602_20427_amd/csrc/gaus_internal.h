@@ -76,6 +76,7 @@ struct IterArgs {
     float *gmu, *gsig;              // mode 0 outputs
     float *mu_io, *sig_io, *m, *v;  // mode 1 state
     int mode;
+    hipEvent_t ops_begin, ops_end;  // optional events around the op kernel
 };
 
 hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const LaunchCfg &lc,

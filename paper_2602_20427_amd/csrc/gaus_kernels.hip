@@ -691,19 +691,29 @@ static void launch_ops(const Graph &g, const Work &w, const float *mu, const flo
                        hipStream_t st) {
     dim3 grid(g.ngroups, g.ntiles, g.B);
     hipLaunchKernelGGL((k_ops<BS, SPT>), grid, dim3(BS), 0, st, g, mu, sigma, w);
-    if (g.nb > 0) {
-        const int epb = 4;
-        dim3 gb((g.nb + epb - 1) / epb, g.ntiles, g.B);
-        hipLaunchKernelGGL((k_back<BS, SPT>), gb, dim3(BS), 0, st, g, mu, sigma, w, epb);
-    }
+}
+
+template <int BS, int SPT>
+static void launch_back(const Graph &g, const Work &w, const float *mu, const float *sigma,
+                        hipStream_t st) {
+    const int epb = 4;
+    dim3 gb((g.nb + epb - 1) / epb, g.ntiles, g.B);
+    hipLaunchKernelGGL((k_back<BS, SPT>), gb, dim3(BS), 0, st, g, mu, sigma, w, epb);
 }
 
 hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const LaunchCfg &lc,
                              const IterArgs &a, hipStream_t st) {
+    if (a.ops_begin) (void)hipEventRecord(a.ops_begin, st);
     if (lc.bs == 64 && lc.spt == 1) launch_ops<64, 1>(g, w, a.mu, a.sigma, st);
     else if (lc.bs == 256 && lc.spt == 1) launch_ops<256, 1>(g, w, a.mu, a.sigma, st);
     else if (lc.bs == 256 && lc.spt == 4) launch_ops<256, 4>(g, w, a.mu, a.sigma, st);
     else return hipErrorInvalidValue;
+    if (a.ops_end) (void)hipEventRecord(a.ops_end, st);
+    if (g.nb > 0) {
+        if (lc.bs == 64) launch_back<64, 1>(g, w, a.mu, a.sigma, st);
+        else if (lc.spt == 1) launch_back<256, 1>(g, w, a.mu, a.sigma, st);
+        else launch_back<256, 4>(g, w, a.mu, a.sigma, st);
+    }
     {
         const int cells = g.K * g.T;
         dim3 grid((cells + 255) / 256, g.B);
