@@ -172,8 +172,11 @@ def main():
     ev[2].record(stream)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    ops_ms_total, ops_launches = ctx.kernel_timing_read()
+    ktimes = ctx.kernel_timing_read()
     ctx.kernel_timing(False)
+    # the dominant kernel: step-by-step op kernel or chunk-polynomial kernel
+    kname = max(ktimes, key=lambda k: ktimes[k][0])
+    ops_ms_total, ops_launches = ktimes[kname]
     step_ms_events = ev[0].elapsed_time(ev[1]) / args.steps
     legalize_ms = ev[1].elapsed_time(ev[2])
     ms_per_step = (t1 - t0) * 1e3 / args.steps

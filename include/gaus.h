@@ -86,6 +86,9 @@ typedef struct {
     float alpha_com;               /* weight alpha of the expected edge length L_com */
     float sigma_min;               /* sigma is clamped to >= sigma_min after each update */
     float kappa;                   /* initial sigma = kappa * (ALAP - ASAP) */
+    int32_t poly_chunk;            /* chunk width W of the polynomial evaluation of wide
+                                      Gaussians: 0 = chosen from D, < 0 = off (every op
+                                      evaluated step by step), else 16/32/64/128/256 */
 } gaus_hparams;
 
 void gaus_default_hparams(gaus_hparams *hp);
@@ -150,15 +153,16 @@ gaus_status gaus_asap_alap(const gaus_ctx *ctx, int32_t *asap, int32_t *alap);
  * pass, copied to DEVICE memory U.  Asynchronous. */
 gaus_status gaus_get_usage(gaus_ctx *ctx, float *U);
 
-/* Profiling hook.  While enabled, every launch of the op kernel (the
- * per-step kernel that dominates an iteration: CDFs, masses, usage, edge
- * terms and their derivatives) is bracketed by a pair of HIP events recorded
- * on the context's stream.  Enabling or disabling discards pending events. */
+/* Profiling hook.  While enabled, every launch of the two kernels that carry
+ * the per-step work of an iteration -- [0] the step-by-step op kernel and
+ * [1] the chunk-polynomial kernel (CDFs, masses, usage, edge terms and their
+ * derivatives) -- is bracketed by a pair of HIP events recorded on the
+ * context's stream.  Enabling or disabling discards pending events. */
 gaus_status gaus_kernel_timing(gaus_ctx *ctx, int32_t enable);
 
-/* Total duration in milliseconds of the op-kernel launches bracketed since
- * timing was enabled or last read, and their number (HOST outputs).
- * Synchronizes the stream, then resets the accumulation. */
+/* Total duration in milliseconds of the bracketed launches of each of the two
+ * kernels since timing was enabled or last read, and their numbers (HOST
+ * outputs, [2] each).  Synchronizes the stream, then resets. */
 gaus_status gaus_kernel_timing_read(gaus_ctx *ctx, double *total_ms, int32_t *launches);
 
 /* Wait for all work enqueued by this context; reports device errors. */
@@ -166,6 +170,10 @@ gaus_status gaus_sync(gaus_ctx *ctx);
 
 /* Problem sizes after preprocessing: N, E, K, D, II, T, n_back, B. */
 gaus_status gaus_get_dims(const gaus_ctx *ctx, int32_t dims[8]);
+
+/* Chunk-polynomial configuration: enabled (0/1), chunk width W, number of
+ * chunks, left strip width.  Ops whose sigma >= 2(W-1) and Lat <= 8 use it. */
+gaus_status gaus_get_poly_config(const gaus_ctx *ctx, int32_t cfg[4]);
 
 /* Message of the last failed call on ctx (or of the last failed gaus_init
  * when ctx is NULL).  Never NULL. */

@@ -22,7 +22,8 @@ OK, E_INVALID_ARG, E_CYCLE, E_HORIZON, E_NOT_CONVERGED, E_OVERFLOW, E_DEVICE, E_
 EXPORTS = ("gaus_default_hparams", "gaus_init", "gaus_bind_state", "gaus_loss_grad", "gaus_step",
            "gaus_adam_from_grad", "gaus_legalize", "gaus_init_state", "gaus_asap_alap",
            "gaus_get_usage", "gaus_kernel_timing", "gaus_kernel_timing_read", "gaus_sync",
-           "gaus_get_dims", "gaus_last_error", "gaus_status_string", "gaus_destroy")
+           "gaus_get_dims", "gaus_get_poly_config", "gaus_last_error", "gaus_status_string",
+           "gaus_destroy")
 
 
 class GausError(RuntimeError):
@@ -42,7 +43,7 @@ class _Problem(C.Structure):
 class HParams(C.Structure):
     _fields_ = [("lr", C.c_float), ("beta1", C.c_float), ("beta2", C.c_float), ("eps", C.c_float),
                 ("rho", C.c_float), ("lambda0", C.c_float), ("alpha_com", C.c_float),
-                ("sigma_min", C.c_float), ("kappa", C.c_float)]
+                ("sigma_min", C.c_float), ("kappa", C.c_float), ("poly_chunk", C.c_int32)]
 
 
 _lib = None
@@ -73,6 +74,7 @@ def load():
         "gaus_kernel_timing_read": ([vp, vp, vp], C.c_int),
         "gaus_sync": ([vp], C.c_int),
         "gaus_get_dims": ([vp, vp], C.c_int),
+        "gaus_get_poly_config": ([vp, vp], C.c_int),
         "gaus_last_error": ([vp], C.c_char_p),
         "gaus_status_string": ([C.c_int], C.c_char_p),
         "gaus_destroy": ([vp], None),
@@ -225,11 +227,17 @@ class Context:
         self._check(load().gaus_kernel_timing(self._h, 1 if enable else 0))
 
     def kernel_timing_read(self):
-        """(total milliseconds, launches) of the bracketed op-kernel launches."""
-        ms = C.c_double()
-        n = C.c_int32()
-        self._check(load().gaus_kernel_timing_read(self._h, C.byref(ms), C.byref(n)))
-        return ms.value, n.value
+        """{kernel: (total milliseconds, launches)} for the step-by-step op
+        kernel ("ops") and the chunk-polynomial kernel ("poly")."""
+        ms = (C.c_double * 2)()
+        n = (C.c_int32 * 2)()
+        self._check(load().gaus_kernel_timing_read(self._h, ms, n))
+        return {"ops": (ms[0], n[0]), "poly": (ms[1], n[1])}
+
+    def poly_config(self):
+        cfg = np.zeros(4, np.int32)
+        self._check(load().gaus_get_poly_config(self._h, _np_ptr(cfg)))
+        return {"enabled": bool(cfg[0]), "W": int(cfg[1]), "chunks": int(cfg[2]), "L0": int(cfg[3])}
 
     def sync(self):
         self._check(load().gaus_sync(self._h))

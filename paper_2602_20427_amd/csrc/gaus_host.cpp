@@ -35,10 +35,12 @@ struct gaus_ctx {
     float *mu = nullptr, *sigma = nullptr, *m = nullptr, *v = nullptr, *lambda = nullptr;
     int *adam_t = nullptr;
     bool bound = false;
-    // op-kernel timing (gaus_kernel_timing)
+    PolyArgs pa{};
+    // kernel timing (gaus_kernel_timing): per iteration two pairs of events,
+    // [4k, 4k+1] around the op kernel and [4k+2, 4k+3] around the polynomial kernel
     bool timing = false;
-    std::vector<hipEvent_t> ev_pool;   // pairs: [2k] begin, [2k+1] end
-    size_t ev_used = 0;                 // pairs recorded since the last read
+    std::vector<hipEvent_t> ev_pool;
+    size_t ev_used = 0;                 // iterations recorded since the last read
 };
 
 namespace {
@@ -66,22 +68,54 @@ void free_all(gaus_ctx *c) {
     c->ev_used = 0;
 }
 
-// Next pair of timing events, or nulls when timing is off.
-hipError_t next_event_pair(gaus_ctx *c, hipEvent_t &b, hipEvent_t &e) {
-    b = e = nullptr;
+// Timing events of the next iteration (nulls when timing is off).
+hipError_t next_events(gaus_ctx *c, IterArgs &a) {
+    a.ops_begin = a.ops_end = a.poly_begin = a.poly_end = nullptr;
     if (!c->timing) return hipSuccess;
-    if (2 * c->ev_used + 2 > c->ev_pool.size()) {
-        for (int k = 0; k < 2; ++k) {
-            hipEvent_t ev;
-            hipError_t r = hipEventCreate(&ev);
-            if (r != hipSuccess) return r;
-            c->ev_pool.push_back(ev);
-        }
+    while (4 * c->ev_used + 4 > c->ev_pool.size()) {
+        hipEvent_t ev;
+        hipError_t r = hipEventCreate(&ev);
+        if (r != hipSuccess) return r;
+        c->ev_pool.push_back(ev);
     }
-    b = c->ev_pool[2 * c->ev_used];
-    e = c->ev_pool[2 * c->ev_used + 1];
+    hipEvent_t *e = &c->ev_pool[4 * c->ev_used];
+    a.ops_begin = e[0]; a.ops_end = e[1];
+    if (c->pa.enabled) { a.poly_begin = e[2]; a.poly_end = e[3]; }
     c->ev_used++;
     return hipSuccess;
+}
+
+// Chunk width, strip and constant tables of the polynomial path.
+void setup_poly(int D, int requested, PolyArgs &pa) {
+    pa = PolyArgs{};
+    if (requested < 0) return;
+    const int widths[] = {16, 32, 64, 128, 256};
+    int W = 0, nc = 0;
+    for (int w : widths) {
+        if (requested > 0 && w != requested) continue;
+        const int n = (D - 2 - kSmax) / w;
+        if (n <= kMaxChunks) { W = w; nc = n; break; }
+    }
+    if (W == 0 || nc < 4) return;
+    pa.enabled = 1;
+    pa.W = W; pa.nc = nc;
+    pa.L0 = D - 2 - nc * W;
+    pa.SP = pa.L0 + 2;
+    const double lam = (W - 1) / 2.0;
+    pa.lam = (float)lam;
+    pa.sig_thr = (float)(lam / kRhoMax);
+    for (int k = 0; k <= 2 * kDeg; ++k) {
+        double acc = 0.0;
+        for (int i = 0; i < W; ++i) acc += std::pow((i - lam) / lam, k);
+        pa.H[k] = (k & 1) ? 0.0f : (float)acc;   // symmetric points: odd moments vanish
+    }
+    auto binom = [](int n, int r) { double v = 1.0; for (int q = 1; q <= r; ++q) v = v * (n - r + q) / q; return v; };
+    for (int k = 0; k < kNC; ++k)
+        for (int j = 0; j <= kShiftTerms; ++j) {
+            const double pw = std::pow(-1.0 / lam, j);
+            pa.cP[k][j] = j == 0 ? 0.0f : (float)(-binom(k + j, j) * pw);
+            pa.cA[k][j] = (float)(-(k + 1) * binom(k + 1 + j, j) * pw / lam);
+        }
 }
 
 template <class T>
@@ -254,7 +288,8 @@ void choose_config(HostGraph &h, int B, LaunchCfg &lc, int &tile, int &ntiles) {
     // group size: enough work-groups to fill 256 CUs several times over
     const long long target = 2048;
     long long per = (long long)h.N * B * ntiles / target;
-    int G = (int)std::min<long long>(256, std::max<long long>(4, per));
+    // at most one op per thread of the op kernel's work-group (it flags the group's ops in parallel)
+    int G = (int)std::min<long long>(lc.bs, std::max<long long>(4, per));
     // ops sorted by (type, id), cut into type-pure groups of <= G ops
     h.perm.resize(h.N);
     for (int i = 0; i < h.N; ++i) h.perm[i] = i;
@@ -288,6 +323,7 @@ void gaus_default_hparams(gaus_hparams *hp) {
     hp->alpha_com = 0.01f;
     hp->sigma_min = 0.05f;
     hp->kappa = 1.0f / 6.0f;
+    hp->poly_chunk = 0;
 }
 
 const char *gaus_status_string(gaus_status s) {
@@ -327,6 +363,12 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     (void)hipGetDevice(&c->device);
     int tile = 0, ntiles = 0;
     choose_config(h, B, c->lc, tile, ntiles);
+    if (hp.poly_chunk > 0 && hp.poly_chunk != 16 && hp.poly_chunk != 32 && hp.poly_chunk != 64 &&
+        hp.poly_chunk != 128 && hp.poly_chunk != 256) {
+        delete c;
+        return fail(nullptr, GAUS_E_INVALID_ARG, "poly_chunk must be 0, negative, or one of 16/32/64/128/256");
+    }
+    setup_poly(h.D, hp.poly_chunk, c->pa);
 
     Graph &g = c->g;
     g.N = h.N; g.E = h.E; g.K = h.K; g.D = h.D; g.II = h.II; g.T = h.II > 0 ? h.II : h.D;
@@ -354,12 +396,19 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     AL(terms, (size_t)B * 5);
     AL(wts, (size_t)B * 4);
     AL(adamf, (size_t)B * 2);
+    AL(cls, BN);
+    AL(ppoly, BN * kPP);
+    AL(cpoly, (size_t)B * h.E * kCP);
+    AL(Ucoef, (size_t)B * g.ngroups * kMaxChunks * kNC);
+    AL(Ustrip, (size_t)B * g.ngroups * 320);
     AL(s64, BN);
     AL(s64b, BN);
     AL(status, (size_t)B);
 #undef AL
     {
         hipError_t e = hipMemset(c->w.U, 0, sizeof(float) * (size_t)B * h.K * g.T);
+        if (e == hipSuccess) e = hipMemset(c->w.ppoly, 0, sizeof(float) * BN * kPP);
+        if (e == hipSuccess) e = hipMemset(c->w.cls, 0, BN);
         if (e == hipSuccess) e = hipDeviceSynchronize();
         if (e != hipSuccess) { s = fail(nullptr, GAUS_E_DEVICE, "init: %s", hipGetErrorString(e)); goto fail_alloc; }
     }
@@ -399,9 +448,9 @@ gaus_status gaus_loss_grad(gaus_ctx *ctx, const float *mu, const float *sigma, c
     IterArgs a{};
     a.mu = mu; a.sigma = sigma; a.lambda_in = lambda; a.terms_out = terms;
     a.gmu = grad_mu; a.gsig = grad_sigma; a.mode = 0;
-    hipError_t e = next_event_pair(ctx, a.ops_begin, a.ops_end);
+    hipError_t e = next_events(ctx, a);
     if (e != hipSuccess) return hip_fail(ctx, e, "timing events");
-    e = enqueue_iteration(ctx->g, ctx->w, ctx->hp, ctx->lc, a, ctx->stream);
+    e = enqueue_iteration(ctx->g, ctx->w, ctx->hp, ctx->lc, ctx->pa, a, ctx->stream);
     if (e != hipSuccess) return hip_fail(ctx, e, "loss_grad launch");
     return GAUS_OK;
 }
@@ -415,9 +464,9 @@ gaus_status gaus_step(gaus_ctx *ctx, int32_t n_iters, float *terms_last) {
         a.mu = ctx->mu; a.sigma = ctx->sigma; a.lambda_in = ctx->lambda; a.lambda_out = ctx->lambda;
         a.adam_t = ctx->adam_t; a.terms_out = (it == n_iters - 1) ? terms_last : nullptr;
         a.mu_io = ctx->mu; a.sig_io = ctx->sigma; a.m = ctx->m; a.v = ctx->v; a.mode = 1;
-        hipError_t e = next_event_pair(ctx, a.ops_begin, a.ops_end);
+        hipError_t e = next_events(ctx, a);
         if (e != hipSuccess) return hip_fail(ctx, e, "timing events");
-        e = enqueue_iteration(ctx->g, ctx->w, ctx->hp, ctx->lc, a, ctx->stream);
+        e = enqueue_iteration(ctx->g, ctx->w, ctx->hp, ctx->lc, ctx->pa, a, ctx->stream);
         if (e != hipSuccess) return hip_fail(ctx, e, "step launch");
     }
     return GAUS_OK;
@@ -496,15 +545,17 @@ gaus_status gaus_kernel_timing_read(gaus_ctx *ctx, double *total_ms, int32_t *la
     if (!total_ms || !launches) return fail(ctx, GAUS_E_INVALID_ARG, "kernel_timing_read: null pointer");
     hipError_t e = hipStreamSynchronize(ctx->stream);
     if (e != hipSuccess) return hip_fail(ctx, e, "kernel_timing_read");
-    double tot = 0.0;
-    for (size_t k = 0; k < ctx->ev_used; ++k) {
-        float ms = 0.0f;
-        e = hipEventElapsedTime(&ms, ctx->ev_pool[2 * k], ctx->ev_pool[2 * k + 1]);
-        if (e != hipSuccess) return hip_fail(ctx, e, "kernel_timing_read");
-        tot += ms;
-    }
-    *total_ms = tot;
-    *launches = (int32_t)ctx->ev_used;
+    double tot[2] = {0.0, 0.0};
+    for (size_t k = 0; k < ctx->ev_used; ++k)
+        for (int q = 0; q < (ctx->pa.enabled ? 2 : 1); ++q) {
+            float ms = 0.0f;
+            e = hipEventElapsedTime(&ms, ctx->ev_pool[4 * k + 2 * q], ctx->ev_pool[4 * k + 2 * q + 1]);
+            if (e != hipSuccess) return hip_fail(ctx, e, "kernel_timing_read");
+            tot[q] += ms;
+        }
+    total_ms[0] = tot[0]; total_ms[1] = tot[1];
+    launches[0] = (int32_t)ctx->ev_used;
+    launches[1] = ctx->pa.enabled ? (int32_t)ctx->ev_used : 0;
     ctx->ev_used = 0;
     return GAUS_OK;
 }
@@ -521,6 +572,12 @@ gaus_status gaus_get_dims(const gaus_ctx *ctx, int32_t dims[8]) {
     const Graph &g = ctx->g;
     dims[0] = g.N; dims[1] = g.E; dims[2] = g.K; dims[3] = g.D; dims[4] = g.II; dims[5] = g.T;
     dims[6] = g.nb; dims[7] = g.B;
+    return GAUS_OK;
+}
+
+gaus_status gaus_get_poly_config(const gaus_ctx *ctx, int32_t cfg[4]) {
+    if (!ctx || !cfg) return GAUS_E_INVALID_ARG;
+    cfg[0] = ctx->pa.enabled; cfg[1] = ctx->pa.W; cfg[2] = ctx->pa.nc; cfg[3] = ctx->pa.L0;
     return GAUS_OK;
 }
 

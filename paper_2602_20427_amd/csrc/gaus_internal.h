@@ -17,6 +17,27 @@ constexpr int kBP = 5;   // per (restart, back edge, tile): V_rec, dVrec/dmu_j, 
                          //   (producer j), dVrec/dmu_i, dVrec/dsigma_i (consumer i)
 constexpr int kHalo = 256;  // largest producer delay handled from the LDS row window
 
+// Chunk-polynomial path (dense regime).  On a chunk of W consecutive steps
+// with radius rho = ((W-1)/2)/sigma <= kRhoMax the CDF row of an op is a
+// degree-kDeg polynomial to ~1e-10; sums over steps become dot products.
+constexpr int kDeg = 8;                       // polynomial degree
+constexpr int kNC = kDeg + 1;                 // coefficients per vector
+constexpr int kShiftTerms = 6;                // terms of the one-step shift series
+constexpr int kTN = kDeg + kShiftTerms + 2;   // scaled derivatives T_0 .. T_{kTN-1}
+constexpr int kSmax = 8;                      // largest producer delay on that path
+constexpr float kRhoMax = 0.25f;
+constexpr int kMaxChunks = 64;                // one chunk per lane of a wave
+
+struct PolyArgs {
+    int enabled;          // 0: every op takes the per-step path
+    int W, nc, L0;        // chunk width, chunks, left strip [0, L0); chunks cover [L0, D-2)
+    int SP;               // strip positions: [0, L0) and {D-2, D-1}
+    float lam, sig_thr;   // chunk half-width (W-1)/2; ops with sigma >= sig_thr are polynomial
+    float H[2 * kDeg + 1];               // sum over a chunk's points of x^k, x in [-1, 1]
+    float cP[kNC][kShiftTerms + 1];      // mass coefficients from the scaled derivatives
+    float cA[kNC][kShiftTerms + 1];      // dF/dmu one step back from the scaled derivatives
+};
+
 // Device copy of the preprocessed problem (all pointers are device memory).
 struct Graph {
     int N, E, K, D, II, T, nb, B;
@@ -50,6 +71,11 @@ struct Work {
     float *terms;     // [B][5]            L, V_dep, V_res, V_rec, L_com of the last forward
     float *wts;       // [B][4]            w_dep, w_res, w_rec, unused
     float *adamf;     // [B][2]            Adam bias corrections 1-beta1^t, 1-beta2^t
+    unsigned char *cls;  // [B][N]          1 = op on the chunk-polynomial path this iteration
+    float *ppoly;     // [B][N][kPP]       producer partials of the polynomial path
+    float *cpoly;     // [B][E][kCP]       consumer partials of polynomial edges
+    float *Ucoef;     // [B][ngroups][kMaxChunks][kNC]  usage coefficients per chunk
+    float *Ustrip;    // [B][ngroups][SP]  usage at the strip positions
     long long *s64;   // [B][N]            legalization workspace
     long long *s64b;  // [B][N]            legalization snapshot (back edges)
     int *status;      // [B]               legalization status
@@ -76,11 +102,12 @@ struct IterArgs {
     float *gmu, *gsig;              // mode 0 outputs
     float *mu_io, *sig_io, *m, *v;  // mode 1 state
     int mode;
-    hipEvent_t ops_begin, ops_end;  // optional events around the op kernel
+    hipEvent_t ops_begin, ops_end;    // optional events around the step-by-step op kernel
+    hipEvent_t poly_begin, poly_end;  // optional events around the polynomial kernel
 };
 
 hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const LaunchCfg &lc,
-                             const IterArgs &a, hipStream_t st);
+                             const PolyArgs &pa, const IterArgs &a, hipStream_t st);
 
 // Adam + sigma clamp + lambda += rho*V (from terms) + adam_t++ from a given gradient.
 hipError_t enqueue_adam_from_grad(const Graph &g, const Work &w, const HP &hp, const float *gmu,

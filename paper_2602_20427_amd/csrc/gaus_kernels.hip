@@ -152,14 +152,42 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
     for (int k = 0; k < SPT; ++k) accU[k] = 0.0f;
     int par = 0;
 
+    // Which ops of the group have step-by-step work: thread t looks at op q0+t
+    // (groups hold at most as many ops as the work-group has threads).  Ops and
+    // edges on the chunk-polynomial path are left to k_poly; an op with none
+    // of its own work gets zero partials here.
+    __shared__ int sDirect[BS];   // 0: nothing; else 1 + number of step-by-step out-edges
+    const unsigned char *clsb = W.cls + (size_t)b * N;
+    {
+        int flag = 0;
+        if (q0 + tid < q1) {
+            const int i = G.perm[q0 + tid];
+            const int e0 = G.row_ptr[i], e1 = G.row_ptr[i + 1];
+            const bool poly_i = clsb[i] != 0;
+            int m = 0;
+            for (int e = e0; e < e1; ++e) m += (poly_i && clsb[G.col[e]]) ? 0 : 1;
+            flag = (!poly_i || m > 0) ? 1 + m : 0;
+            if (!flag) {
+                float *pp = W.ppart + (((size_t)b * N + i) * G.ntiles + tile) * kPP;
+#pragma unroll
+                for (int c = 0; c < kPP; ++c) pp[c] = 0.0f;
+            }
+        }
+        if (tid < BS) sDirect[tid] = flag;
+    }
+    __syncthreads();
+
     for (int q = q0; q < q1; ++q) {
+        const int flag = sDirect[q - q0];
+        if (flag == 0) continue;
         const int i = uniform(G.perm[q]);
+        const int e0 = uniform(G.row_ptr[i]), e1 = uniform(G.row_ptr[i + 1]);
+        const bool poly_i = clsb[i] != 0;
+        const int m = uniform(flag - 1);
         const float m_i = mub[i], s_i = sgb[i];
         const float rs = 1.0f / s_i;
         const float cinv = rs * kInvSqrt2Pi;
         const int s = uniform(G.delay[i]);
-        const int e0 = uniform(G.row_ptr[i]), e1 = uniform(G.row_ptr[i + 1]);
-        const int m = e1 - e0;
         const bool win_shift = (m > 0) && (s <= kHalo);
         const int Lh = win_shift ? (s > 1 ? s : 1) : 1;
 
@@ -178,7 +206,7 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
             const int u = t0 + k * BS + tid;
             const int p = u - t0 + Lh;
             rF[k] = st_F(sT[p]); rFm[k] = sFm[p]; rFs[k] = sFs[p];
-            if (u < D) accU[k] += st_mass(sT[p - 1], sT[p]);
+            if (u < D && !poly_i) accU[k] += st_mass(sT[p - 1], sT[p]);
             rA[k] = 0.0f; rFms[k] = 0.0f; rFss[k] = 0.0f;
             if (m > 0 && u < D) {
                 if (win_shift) {
@@ -203,6 +231,7 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
 
         for (int e = e0; e < e1; ++e) {
             const int j = uniform(G.col[e]);
+            if (poly_i && clsb[j]) continue;  // polynomial edge
             const float m_j = mub[j], s_j = sgb[j];
             const float rsj = 1.0f / s_j;
             float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -291,6 +320,341 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
 }
 
 // ---------------------------------------------------------------------------
+// Chunk-polynomial path (dense regime).
+//
+// Chunks of W steps tile [L0, D-2); a chunk's points are x = (u - t_mid)/lam in
+// [-1, 1], lam = (W-1)/2.  Around the chunk centre an op's CDF is
+// F(u) = Phi(z0 + rho x), rho = lam/sigma, and its Taylor coefficients in x are
+// the scaled derivatives T_n = Phi^(n)(z0) rho^n / n!, which obey
+//   T_1 = phi(z0) rho,
+//   T_{n+1} = -(z0 rho/(n+1)) T_n - ((n-1) rho^2/(n(n+1))) T_{n-1}
+// (the Hermite recursion of the derivatives of phi, scaled).  From one set of
+// T's follow, with constant coefficients:
+//   F:         f_k = T_k
+//   dF/dmu:    a_k = -(k+1) T_{k+1} / lam
+//   dF/dsigma: e_k = z0 a_k + rho a_{k-1}         (dF/dsigma = z dF/dmu)
+//   mass F(v) - F(v-1):  m_k = sum_{j>=1} cP[k][j] T_{k+j}   (one step = lam^-1 in x)
+//   dF/dmu at v-1:       a1_k = sum_{j>=0} cA[k][j] T_{k+1+j}
+// With rho <= kRhoMax the truncation error is ~1e-10.  Every sum over the
+// chunk's steps of a product p(u) q(u) equals sum_k (H p)_k q_k with the chunk
+// moments H_n = sum_x x^n, so an edge costs 10 dot products of length kNC.
+// The strip [0, L0) u {D-2, D-1} (boundary conventions of the open end bins,
+// zero derivatives outside the interior edges) is evaluated step by step.
+// ---------------------------------------------------------------------------
+__global__ void k_classify(Graph G, PolyArgs pa, const float *__restrict__ sigma, Work W) {
+    const int b = blockIdx.y;
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= G.N) return;
+    const float s = sigma[(size_t)b * G.N + i];
+    W.cls[(size_t)b * G.N + i] = (pa.enabled && s >= pa.sig_thr && G.delay[i] <= kSmax) ? 1 : 0;
+}
+
+namespace {
+
+struct Expansion {
+    float T[kTN];   // scaled derivatives, T[0] = F(z0)
+    float G0;       // 1 - F(z0), from the tail
+    float z0, rho;
+};
+
+constexpr float rcpi(int n) { return 1.0f / (float)n; }
+
+__device__ __forceinline__ void expand(float mu, float rs, float tcen, float lam, Expansion &e) {
+    e.rho = lam * rs;
+    e.z0 = (tcen + 0.5f - mu) * rs;
+    float tail, g;
+    normal_tail_pdf(e.z0, tail, g);
+    const bool up = e.z0 >= 0.0f;
+    e.T[0] = up ? 1.0f - tail : tail;
+    e.G0 = up ? tail : 1.0f - tail;
+    e.T[1] = g * kInvSqrt2Pi * e.rho;
+    const float zr = e.z0 * e.rho, r2 = e.rho * e.rho;
+#pragma unroll
+    for (int n = 1; n < kTN - 1; ++n)
+        e.T[n + 1] = -(zr * rcpi(n + 1)) * e.T[n] - ((float)(n - 1) * r2 * rcpi(n * (n + 1))) * e.T[n - 1];
+}
+
+__device__ __forceinline__ void vec_dFdmu(const Expansion &e, float inv_lam, float (&a)[kNC]) {
+#pragma unroll
+    for (int k = 0; k < kNC; ++k) a[k] = -(float)(k + 1) * inv_lam * e.T[k + 1];
+}
+
+__device__ __forceinline__ void vec_times_z(const float (&a)[kNC], float zc, float rho, float (&o)[kNC]) {
+    o[0] = zc * a[0];
+#pragma unroll
+    for (int k = 1; k < kNC; ++k) o[k] = fmaf(zc, a[k], rho * a[k - 1]);
+}
+
+__device__ __forceinline__ void vec_mass(const Expansion &e, const PolyArgs &pa, float (&m)[kNC]) {
+#pragma unroll
+    for (int k = 0; k < kNC; ++k) {
+        float acc = 0.0f;
+#pragma unroll
+        for (int j = kShiftTerms; j >= 1; --j) acc = fmaf(pa.cP[k][j], e.T[k + j], acc);
+        m[k] = acc;
+    }
+}
+
+__device__ __forceinline__ void vec_dFdmu_back(const Expansion &e, const PolyArgs &pa, float (&a)[kNC]) {
+#pragma unroll
+    for (int k = 0; k < kNC; ++k) {
+        float acc = 0.0f;
+#pragma unroll
+        for (int j = kShiftTerms; j >= 0; --j) acc = fmaf(pa.cA[k][j], e.T[k + 1 + j], acc);
+        a[k] = acc;
+    }
+}
+
+// (H p)_k = sum_l H_{k+l} p_l; the chunk points are symmetric, odd moments vanish
+__device__ __forceinline__ void vec_moments(const float (&p)[kNC], const PolyArgs &pa, float (&o)[kNC]) {
+#pragma unroll
+    for (int k = 0; k < kNC; ++k) {
+        float acc = 0.0f;
+#pragma unroll
+        for (int l = 0; l < kNC; ++l)
+            if (((k + l) & 1) == 0) acc = fmaf(pa.H[k + l], p[l], acc);
+        o[k] = acc;
+    }
+}
+
+__device__ __forceinline__ float vdot(const float (&a)[kNC], const float (&b)[kNC]) {
+    float acc = 0.0f;
+#pragma unroll
+    for (int k = 0; k < kNC; ++k) acc = fmaf(a[k], b[k], acc);
+    return acc;
+}
+
+// dot with 1 - F given F's coefficients and the precise 1 - F(z0)
+__device__ __forceinline__ float vdot_1mF(const float (&a)[kNC], const Expansion &e) {
+    float acc = a[0] * e.G0;
+#pragma unroll
+    for (int k = 1; k < kNC; ++k) acc = fmaf(-a[k], e.T[k], acc);
+    return acc;
+}
+
+__device__ __forceinline__ float vdot_F(const float (&a)[kNC], const Expansion &e) {
+    float acc = 0.0f;
+#pragma unroll
+    for (int k = 0; k < kNC; ++k) acc = fmaf(a[k], e.T[k], acc);
+    return acc;
+}
+
+}  // namespace
+
+constexpr int kPolyWaves = 4;
+constexpr int kStripMax = 320;                  // >= kSmax + largest W + 2
+constexpr int kStripPasses = (kStripMax + 63) / 64;
+constexpr int kOpsPerWaveMax = 64;              // group size <= kPolyWaves * 64
+
+// Work-group = (op group, restart), kPolyWaves waves; each wave takes the
+// group's ops in turn.  For a polynomial op: lanes = strip positions for the
+// step-by-step part, lanes = chunks for the polynomial part; per polynomial
+// out-edge the consumer-side derivatives of both parts are reduced together.
+__global__ __launch_bounds__(64 * kPolyWaves) __attribute__((amdgpu_waves_per_eu(3)))
+void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__restrict__ sigma, Work W) {
+    // dynamic LDS: per wave 7 rows of SP strip values, then per wave SP strip usages
+    extern __shared__ float sDyn[];
+    __shared__ float sUc[kPolyWaves][kMaxChunks][kNC];
+    const int SP = pa.SP;
+    const int grp = blockIdx.x, b = blockIdx.y;
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int N = G.N, D = G.D;
+    const float *mub = mu + (size_t)b * N;
+    const float *sgb = sigma + (size_t)b * N;
+    const unsigned char *clsb = W.cls + (size_t)b * N;
+    const float lam = pa.lam, inv_lam = 1.0f / pa.lam;
+    const bool cact = lane < pa.nc;
+    const float tcen = (float)(pa.L0 + lane * pa.W) + lam;
+
+    float uc[kNC];
+#pragma unroll
+    for (int k = 0; k < kNC; ++k) uc[k] = 0.0f;
+    float us[kStripPasses];
+#pragma unroll
+    for (int ps = 0; ps < kStripPasses; ++ps) us[ps] = 0.0f;
+    float *own = sDyn + (size_t)wv * 7 * SP;
+    float *sUs = sDyn + (size_t)kPolyWaves * 7 * SP;
+
+    // this wave's ops q = q0 + wv + kPolyWaves*l, parameters loaded by lane l
+    const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
+    const int nq = (q1 - q0 - wv + kPolyWaves - 1) / kPolyWaves;
+    int l_i = 0, l_cls = 0, l_s = 0, l_e0 = 0, l_e1 = 0;
+    float l_mu = 0.0f, l_sg = 1.0f;
+    if (lane < nq) {
+        l_i = G.perm[q0 + wv + kPolyWaves * lane];
+        l_cls = clsb[l_i];
+        l_mu = mub[l_i]; l_sg = sgb[l_i];
+        l_s = G.delay[l_i];
+        l_e0 = G.row_ptr[l_i]; l_e1 = G.row_ptr[l_i + 1];
+    }
+    for (int oq = 0; oq < nq; ++oq) {
+        const int i = __builtin_amdgcn_readlane(l_i, oq);
+        float *pp = W.ppoly + ((size_t)b * N + i) * kPP;
+        if (!__builtin_amdgcn_readlane(l_cls, oq)) {
+            if (lane < kPP) pp[lane] = 0.0f;
+            continue;
+        }
+        const float m_i = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, l_mu), oq));
+        const float s_i = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, l_sg), oq));
+        const float rs = 1.0f / s_i, cinv = rs * kInvSqrt2Pi;
+        const int s = __builtin_amdgcn_readlane(l_s, oq);
+        const int e0 = __builtin_amdgcn_readlane(l_e0, oq), e1 = __builtin_amdgcn_readlane(l_e1, oq);
+        float pr[kPP] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+        // the op's polynomial out-edges, loaded by lane (batches of 64)
+        int x_j = 0, x_ok = 0;
+        float x_mu = 0.0f, x_sg = 1.0f;
+
+        // (1) strip: own CDF values per position, kept in this wave's LDS rows
+#pragma unroll
+        for (int ps = 0; ps < kStripPasses; ++ps) {
+            const int p = ps * 64 + lane;
+            if (p < SP) {
+                const int u = p < pa.L0 ? p : D - 2 + (p - pa.L0);
+                float st, Fm, Fs, st0, Fm0, Fs0;
+                cdf_at(u, D, m_i, rs, cinv, st, Fm, Fs);
+                us[ps] += st_mass(st_at((long long)u - 1, D, m_i, rs), st);
+                cdf_at((long long)u - s, D, m_i, rs, cinv, st0, Fm0, Fs0);
+                const float st1 = st_at((long long)u - s + 1, D, m_i, rs);
+                own[0 * SP + p] = st_F(st);
+                own[1 * SP + p] = Fm;
+                own[2 * SP + p] = Fs;
+                own[3 * SP + p] = st_mass(st0, st1);
+                own[4 * SP + p] = Fm0;
+                own[5 * SP + p] = Fs0;
+                own[6 * SP + p] = st_1mF(st0);
+            }
+        }
+
+        // (2) chunk: producer vectors multiplied by the chunk moments
+        float HF[kNC], HFm[kNC], HFs[kNC], HA[kNC], HFm1[kNC], HFs1[kNC];
+        if (cact) {
+            Expansion ea;
+            expand(m_i, rs, tcen, lam, ea);
+            float v[kNC], w[kNC];
+            vec_mass(ea, pa, v);
+#pragma unroll
+            for (int k = 0; k < kNC; ++k) uc[k] += v[k];
+#pragma unroll
+            for (int k = 0; k < kNC; ++k) w[k] = ea.T[k];
+            vec_moments(w, pa, HF);
+            vec_dFdmu(ea, inv_lam, v);
+            vec_moments(v, pa, HFm);
+            vec_times_z(v, ea.z0, ea.rho, w);
+            vec_moments(w, pa, HFs);
+            // shifted functions: A(u) = mass at u-s+1, dF(u-s)
+            Expansion es;
+            if (s != 1) expand(m_i, rs, tcen - (float)(s - 1), lam, es);
+            const Expansion &ex = (s != 1) ? es : ea;
+            vec_mass(ex, pa, v);
+            vec_moments(v, pa, HA);
+            vec_dFdmu_back(ex, pa, v);
+            vec_moments(v, pa, HFm1);
+            vec_times_z(v, ex.z0 - rs, ex.rho, w);
+            vec_moments(w, pa, HFs1);
+        } else {
+#pragma unroll
+            for (int k = 0; k < kNC; ++k) { HF[k] = HFm[k] = HFs[k] = HA[k] = HFm1[k] = HFs1[k] = 0.0f; }
+        }
+
+        // (3) polynomial out-edges
+        for (int e = e0; e < e1; ++e) {
+            const int eb = (e - e0) & 63;
+            if (eb == 0) {
+                x_ok = 0;
+                if (e + lane < e1) {
+                    x_j = G.col[e + lane];
+                    x_ok = clsb[x_j];
+                    x_mu = mub[x_j]; x_sg = sgb[x_j];
+                }
+            }
+            if (!__builtin_amdgcn_readlane(x_ok, eb)) continue;  // step-by-step edge, done by k_ops
+            const float m_j = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x_mu), eb));
+            const float s_j = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x_sg), eb));
+            const float rsj = 1.0f / s_j, cj = rsj * kInvSqrt2Pi;
+            float cc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int ps = 0; ps < kStripPasses; ++ps) {
+                const int p = ps * 64 + lane;
+                if (p < SP) {
+                    const int u = p < pa.L0 ? p : D - 2 + (p - pa.L0);
+                    float stj, Fmj, Fsj;
+                    cdf_at(u, D, m_j, rsj, cj, stj, Fmj, Fsj);
+                    const float Pj = st_mass(st_at((long long)u - 1, D, m_j, rsj), stj);
+                    const float F = own[0 * SP + p], Fm = own[1 * SP + p];
+                    const float Fs = own[2 * SP + p], A = own[3 * SP + p];
+                    pr[2] = fmaf(-own[4 * SP + p], Pj, pr[2]);
+                    pr[3] = fmaf(-own[5 * SP + p], Pj, pr[3]);
+                    if (u < D - 1) {
+                        const float omF = st_1mF(stj);
+                        pr[0] = fmaf(A, st_F(stj), pr[0]);
+                        pr[1] = fmaf(F, omF, pr[1]);
+                        pr[4] = fmaf(Fm, omF, pr[4]);
+                        pr[5] = fmaf(Fs, omF, pr[5]);
+                        cc[0] = fmaf(A, Fmj, cc[0]);
+                        cc[1] = fmaf(A, Fsj, cc[1]);
+                        cc[2] = fmaf(-F, Fmj, cc[2]);
+                        cc[3] = fmaf(-F, Fsj, cc[3]);
+                    } else {
+                        pr[0] += own[6 * SP + p];
+                    }
+                }
+            }
+            if (cact) {
+                Expansion ej;
+                expand(m_j, rsj, tcen, lam, ej);
+                float a[kNC], v[kNC];
+                pr[0] += vdot_F(HA, ej);
+                pr[1] += vdot_1mF(HF, ej);
+                pr[4] += vdot_1mF(HFm, ej);
+                pr[5] += vdot_1mF(HFs, ej);
+                vec_dFdmu(ej, inv_lam, a);
+                cc[0] += vdot(HA, a);
+                cc[2] -= vdot(HF, a);
+                vec_times_z(a, ej.z0, ej.rho, v);
+                cc[1] += vdot(HA, v);
+                cc[3] -= vdot(HF, v);
+                vec_mass(ej, pa, v);
+                pr[2] -= vdot(HFm1, v);
+                pr[3] -= vdot(HFs1, v);
+            }
+#pragma unroll
+            for (int c = 0; c < 4; ++c) cc[c] = wave_sum(cc[c]);
+            if (lane < kCP) W.cpoly[((size_t)b * G.E + e) * kCP + lane] = cc[lane];
+        }
+#pragma unroll
+        for (int c = 0; c < kPP; ++c) pr[c] = wave_sum(pr[c]);
+        if (lane < kPP) pp[lane] = pr[lane];
+    }
+
+    // usage of the group: combine the waves' chunk coefficients and strip values
+#pragma unroll
+    for (int k = 0; k < kNC; ++k) sUc[wv][lane][k] = uc[k];
+#pragma unroll
+    for (int ps = 0; ps < kStripPasses; ++ps) {
+        const int p = ps * 64 + lane;
+        if (p < SP) sUs[wv * SP + p] = us[ps];
+    }
+    __syncthreads();
+    float *ucg = W.Ucoef + ((size_t)b * G.ngroups + grp) * kMaxChunks * kNC;
+    for (int x = threadIdx.x; x < kMaxChunks * kNC; x += 64 * kPolyWaves) {
+        const int c = x / kNC, k = x % kNC;
+        float acc = 0.0f;
+#pragma unroll
+        for (int w = 0; w < kPolyWaves; ++w) acc += sUc[w][c][k];
+        ucg[x] = acc;
+    }
+    float *usg = W.Ustrip + ((size_t)b * G.ngroups + grp) * kStripMax;
+    for (int p = threadIdx.x; p < kStripMax; p += 64 * kPolyWaves) {
+        float acc = 0.0f;
+        if (p < SP) {
+#pragma unroll
+            for (int w = 0; w < kPolyWaves; ++w) acc += sUs[w * SP + p];
+        }
+        usg[p] = acc;
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Back-edge kernel (modulo scheduling).  Work-group = (back-edge block, tile,
 // restart); one back edge (j -> i, k) at a time, c = k*II - Lat_j:
 //   V_rec       = F_i(-c-1) + sum_u P_i^{u-c} (1 - F_j(u))
@@ -344,15 +708,41 @@ __global__ __launch_bounds__(BS) void k_back(Graph G, const float *__restrict__ 
 // ---------------------------------------------------------------------------
 // Usage: U[b][k][slot] = sum over type-k groups and steps t = slot (mod T).
 // ---------------------------------------------------------------------------
-__global__ void k_usage(Graph G, Work W) {
+// Usage of the polynomial ops at step t: their mass coefficients summed over
+// the type's groups, evaluated at t (chunk part), or the strip values.
+__device__ __forceinline__ float poly_usage_at(const Graph &G, const PolyArgs &pa, const Work &W, int b,
+                                               int k, int t) {
+    float acc = 0.0f;
+    if (t >= pa.L0 && t < G.D - 2) {
+        const int c = (t - pa.L0) / pa.W;
+        const float x = ((float)(t - pa.L0 - c * pa.W) - pa.lam) / pa.lam;
+        for (int g = G.type_grp[k]; g < G.type_grp[k + 1]; ++g) {
+            const float *cf = W.Ucoef + (((size_t)b * G.ngroups + g) * kMaxChunks + c) * kNC;
+            float v = cf[kNC - 1];
+#pragma unroll
+            for (int q = kNC - 2; q >= 0; --q) v = fmaf(v, x, cf[q]);
+            acc += v;
+        }
+    } else {
+        const int p = t < pa.L0 ? t : pa.L0 + (t - (G.D - 2));
+        for (int g = G.type_grp[k]; g < G.type_grp[k + 1]; ++g)
+            acc += W.Ustrip[((size_t)b * G.ngroups + g) * kStripMax + p];
+    }
+    return acc;
+}
+
+__global__ void k_usage(Graph G, PolyArgs pa, Work W) {
     const int b = blockIdx.y;
     const int cell = blockIdx.x * blockDim.x + threadIdx.x;
     if (cell >= G.K * G.T) return;
     const int k = cell / G.T, slot = cell % G.T;
     float acc = 0.0f;
-    for (int g = G.type_grp[k]; g < G.type_grp[k + 1]; ++g) {
-        const float *up = W.Upart + ((size_t)b * G.ngroups + g) * G.D;
-        for (int t = slot; t < G.D; t += G.T) acc += up[t];
+    for (int t = slot; t < G.D; t += G.T) {
+        float ut = 0.0f;
+        for (int g = G.type_grp[k]; g < G.type_grp[k + 1]; ++g)
+            ut += W.Upart[((size_t)b * G.ngroups + g) * G.D + t];
+        if (pa.enabled) ut += poly_usage_at(G, pa, W, b, k, t);
+        acc += ut;
     }
     W.U[(size_t)b * G.K * G.T + cell] = acc;
 }
@@ -435,6 +825,8 @@ __global__ __launch_bounds__(kTermsBS) void k_terms(Graph G, Work W, HP hp,
     const size_t np = (size_t)G.N * G.ntiles;
     const float *pp = W.ppart + (size_t)b * np * kPP;
     for (size_t r = tid; r < np; r += kTermsBS) { vdep += pp[r * kPP + 0]; lcom += pp[r * kPP + 1]; }
+    const float *ppy = W.ppoly + (size_t)b * G.N * kPP;
+    for (int r = tid; r < G.N; r += kTermsBS) { vdep += ppy[(size_t)r * kPP + 0]; lcom += ppy[(size_t)r * kPP + 1]; }
     const size_t nbp = (size_t)G.nb * G.ntiles;
     const float *bp = W.bpart + (size_t)b * nbp * kBP;
     for (size_t r = tid; r < nbp; r += kTermsBS) vrec += bp[r * kBP + 0];
@@ -525,8 +917,17 @@ __global__ __launch_bounds__(256) void k_final(Graph G, Work W, HP hp, const flo
         dm += pp[tl * kPP + 2]; ds += pp[tl * kPP + 3];
         cm += pp[tl * kPP + 4]; cs += pp[tl * kPP + 5];
     }
+    const float *ppy = W.ppoly + bi * kPP;
+    dm += ppy[2]; ds += ppy[3]; cm += ppy[4]; cs += ppy[5];
+    const bool poly_i = W.cls[bi] != 0;
     for (int q = G.pred_ptr[i]; q < G.pred_ptr[i + 1]; ++q) {
-        const float *cp = W.cpart + (((size_t)b * G.E + G.pred_eid[q]) * nt) * kCP;
+        const int e = G.pred_eid[q];
+        if (poly_i && W.cls[(size_t)b * N + G.pred_src[q]]) {
+            const float *cp = W.cpoly + ((size_t)b * G.E + e) * kCP;
+            dm += cp[0]; ds += cp[1]; cm += cp[2]; cs += cp[3];
+            continue;
+        }
+        const float *cp = W.cpart + (((size_t)b * G.E + e) * nt) * kCP;
         for (int tl = 0; tl < nt; ++tl) {
             dm += cp[tl * kCP + 0]; ds += cp[tl * kCP + 1];
             cm += cp[tl * kCP + 2]; cs += cp[tl * kCP + 3];
@@ -702,13 +1103,23 @@ static void launch_back(const Graph &g, const Work &w, const float *mu, const fl
 }
 
 hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const LaunchCfg &lc,
-                             const IterArgs &a, hipStream_t st) {
+                             const PolyArgs &pa, const IterArgs &a, hipStream_t st) {
+    {
+        dim3 grid((g.N + 255) / 256, g.B);
+        hipLaunchKernelGGL(k_classify, grid, dim3(256), 0, st, g, pa, a.sigma, w);
+    }
     if (a.ops_begin) (void)hipEventRecord(a.ops_begin, st);
     if (lc.bs == 64 && lc.spt == 1) launch_ops<64, 1>(g, w, a.mu, a.sigma, st);
     else if (lc.bs == 256 && lc.spt == 1) launch_ops<256, 1>(g, w, a.mu, a.sigma, st);
     else if (lc.bs == 256 && lc.spt == 4) launch_ops<256, 4>(g, w, a.mu, a.sigma, st);
     else return hipErrorInvalidValue;
     if (a.ops_end) (void)hipEventRecord(a.ops_end, st);
+    if (pa.enabled) {
+        if (a.poly_begin) (void)hipEventRecord(a.poly_begin, st);
+        const size_t lds = sizeof(float) * (size_t)kPolyWaves * 8 * pa.SP;
+        hipLaunchKernelGGL(k_poly, dim3(g.ngroups, g.B), dim3(64 * kPolyWaves), lds, st, g, pa, a.mu, a.sigma, w);
+        if (a.poly_end) (void)hipEventRecord(a.poly_end, st);
+    }
     if (g.nb > 0) {
         if (lc.bs == 64) launch_back<64, 1>(g, w, a.mu, a.sigma, st);
         else if (lc.spt == 1) launch_back<256, 1>(g, w, a.mu, a.sigma, st);
@@ -717,7 +1128,7 @@ hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const 
     {
         const int cells = g.K * g.T;
         dim3 grid((cells + 255) / 256, g.B);
-        hipLaunchKernelGGL(k_usage, grid, dim3(256), 0, st, g, w);
+        hipLaunchKernelGGL(k_usage, grid, dim3(256), 0, st, g, pa, w);
     }
     hipLaunchKernelGGL(k_terms, dim3(g.B), dim3(kTermsBS), 0, st, g, w, hp, a.lambda_in,
                        a.mode == 1 ? a.lambda_out : nullptr, a.mode == 1 ? a.adam_t : nullptr,

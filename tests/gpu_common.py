@@ -19,11 +19,13 @@ def say(*a):
     sys.stdout.flush()
 
 
-def hparams(alpha=0.01, rho=1e-4, lr=1e-2):
+def hparams(alpha=0.01, rho=1e-4, lr=1e-2, poly_chunk=0):
+    """poly_chunk: 0 = library's choice, < 0 = polynomial path off, else W."""
     hp = bd.default_hparams()
     hp.alpha_com = alpha
     hp.rho = rho
     hp.lr = lr
+    hp.poly_chunk = poly_chunk
     return hp
 
 
@@ -31,6 +33,7 @@ def gpu_loss_grad(prob, mu, sigma, lam, hp):
     import torch
     B, N = mu.shape
     ctx = bd.Context(prob, B, hp)
+    say(f"  [ctx] poly {ctx.poly_config()}")
     dev = torch.device("cuda")
     m = torch.from_numpy(np.ascontiguousarray(mu, np.float32)).to(dev)
     s = torch.from_numpy(np.ascontiguousarray(sigma, np.float32)).to(dev)

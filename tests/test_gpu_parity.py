@@ -54,8 +54,9 @@ def test_loss_grad_random_state(cfg):
     _check(p, mu, sg, _lam(B, 2), hparams(alpha=0.37, rho=0.05), range(B), f"{cfg}/random")
 
 
+@pytest.mark.parametrize("poly", [0, -1])
 @pytest.mark.parametrize("cfg", ["tiny", "small", "medium", "pipelined"])
-def test_loss_grad_paper_init(cfg):
+def test_loss_grad_paper_init(cfg, poly):
     """Timing state: the paper's ASAP/ALAP initialization (dense regime)."""
     p = make_problem(cfg, seed=0)
     B = CONFIGS[cfg].B
@@ -67,7 +68,8 @@ def test_loss_grad_paper_init(cfg):
         assert rc == 0
         mu, sg = mu.astype(np.float32), sg.astype(np.float32)
     restarts = [0, B - 1] if B > 2 else range(B)
-    _check(p, mu, sg, _lam(B, 3), hparams(alpha=0.01, rho=1e-3), restarts, f"{cfg}/init")
+    _check(p, mu, sg, _lam(B, 3), hparams(alpha=0.01, rho=1e-3, poly_chunk=poly), restarts,
+           f"{cfg}/init poly={poly}")
 
 
 def test_loss_grad_pipelined_random():
@@ -103,14 +105,31 @@ def _ragged_problem(seed, N=700, D=1500, II=0, n_back=0, big_delay=True):
                    back_dist=np.array(bk, np.int32))
 
 
+@pytest.mark.parametrize("poly", [0, 32, -1])
 @pytest.mark.parametrize("II,n_back", [(0, 0), (37, 25), (2000, 10)])
-def test_loss_grad_ragged_tiles_and_big_delays(II, n_back):
+def test_loss_grad_ragged_tiles_and_big_delays(II, n_back, poly):
+    """Mixed regimes: sigma from 0.2 to 300 puts ops on both the polynomial and
+    the step-by-step path, and edges between them."""
     p = _ragged_problem(11 + II, II=II, n_back=n_back)
     B = 3
     rng = np.random.default_rng(12)
     mu = rng.uniform(-20, p.D + 20, size=(B, p.n_ops)).astype(np.float32)
     sg = np.exp(rng.uniform(np.log(0.2), np.log(300.0), size=(B, p.n_ops))).astype(np.float32)
-    _check(p, mu, sg, _lam(B, 13), hparams(alpha=0.3, rho=0.02), range(B), f"ragged II={II}")
+    _check(p, mu, sg, _lam(B, 13), hparams(alpha=0.3, rho=0.02, poly_chunk=poly), range(B),
+           f"ragged II={II} poly={poly}")
+
+
+@pytest.mark.parametrize("W", [16, 32, 64, 128, 256])
+def test_polynomial_path_chunk_widths(W):
+    """Every chunk width on a wide-sigma state (all ops polynomial where the
+    width allows), delays 0..8, means partly outside the horizon."""
+    p = _ragged_problem(40 + W, N=400, D=min(3000, 60 * W + 10), big_delay=False)
+    p.delay[:] = np.random.default_rng(W).integers(0, 9, size=p.n_ops).astype(np.int32)
+    B = 2
+    rng = np.random.default_rng(41)
+    mu = rng.uniform(-200, p.D + 200, size=(B, p.n_ops)).astype(np.float32)
+    sg = rng.uniform(2.0 * W, 1500.0, size=(B, p.n_ops)).astype(np.float32)
+    _check(p, mu, sg, _lam(B, 42), hparams(alpha=0.2, rho=0.01, poly_chunk=W), range(B), f"chunk W={W}")
 
 
 def test_small_edge_cases():
