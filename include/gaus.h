@@ -88,7 +88,7 @@ typedef struct {
     float kappa;                   /* initial sigma = kappa * (ALAP - ASAP) */
     int32_t poly_chunk;            /* chunk width W of the polynomial evaluation of wide
                                       Gaussians: 0 = chosen from D, < 0 = off (every op
-                                      evaluated step by step), else 16/32/64/128/256 */
+                                      evaluated step by step), else W in [16, 256] */
 } gaus_hparams;
 
 void gaus_default_hparams(gaus_hparams *hp);

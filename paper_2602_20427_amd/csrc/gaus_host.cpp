@@ -89,14 +89,21 @@ hipError_t next_events(gaus_ctx *c, IterArgs &a) {
 void setup_poly(int D, int requested, PolyArgs &pa) {
     pa = PolyArgs{};
     if (requested < 0) return;
-    const int widths[] = {16, 32, 64, 128, 256};
-    int W = 0, nc = 0;
-    for (int w : widths) {
+    // Chunks tile [L0, D-2) with nc <= 64 chunks (one per lane); the strip
+    // [0, L0) u {D-2, D-1} is evaluated step by step in passes of 64 lanes.
+    // Take the fewest strip passes, then the smallest W (the lowest sigma
+    // threshold 2(W-1) for the polynomial path).
+    int W = 0, nc = 0, best_passes = 1 << 30;
+    for (int w = 16; w <= 256; ++w) {
         if (requested > 0 && w != requested) continue;
-        const int n = (D - 2 - kSmax) / w;
-        if (n <= kMaxChunks) { W = w; nc = n; break; }
+        const int n = std::min(kMaxChunks, (D - 2 - kSmax) / w);
+        if (n < 4) continue;
+        const int sp = D - 2 - n * w + 2;
+        if (sp > 320) continue;
+        const int passes = (sp + 63) / 64;
+        if (passes < best_passes) { best_passes = passes; W = w; nc = n; }
     }
-    if (W == 0 || nc < 4) return;
+    if (W == 0) return;
     pa.enabled = 1;
     pa.W = W; pa.nc = nc;
     pa.L0 = D - 2 - nc * W;
@@ -151,7 +158,7 @@ struct HostGraph {
     std::vector<int> bin_ptr, bin, bout_ptr, bout;
     std::vector<int> level, lvl_ptr, lvl_ops;
     std::vector<int> asap, alap;
-    std::vector<int> perm, grp_start, type_grp;
+    std::vector<int> perm, grp_start, type_grp, grp_of;
 };
 
 gaus_status validate(const gaus_problem *p, int32_t B) {
@@ -306,6 +313,9 @@ void choose_config(HostGraph &h, int B, LaunchCfg &lc, int &tile, int &ntiles) {
     }
     h.type_grp[h.K] = (int)h.grp_start.size();
     h.grp_start.push_back(h.N);
+    h.grp_of.assign(h.N, 0);
+    for (size_t gi = 0; gi + 1 < h.grp_start.size(); ++gi)
+        for (int q = h.grp_start[gi]; q < h.grp_start[gi + 1]; ++q) h.grp_of[h.perm[q]] = (int)gi;
 }
 
 }  // namespace
@@ -363,10 +373,9 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     (void)hipGetDevice(&c->device);
     int tile = 0, ntiles = 0;
     choose_config(h, B, c->lc, tile, ntiles);
-    if (hp.poly_chunk > 0 && hp.poly_chunk != 16 && hp.poly_chunk != 32 && hp.poly_chunk != 64 &&
-        hp.poly_chunk != 128 && hp.poly_chunk != 256) {
+    if (hp.poly_chunk > 0 && (hp.poly_chunk < 16 || hp.poly_chunk > 256)) {
         delete c;
-        return fail(nullptr, GAUS_E_INVALID_ARG, "poly_chunk must be 0, negative, or one of 16/32/64/128/256");
+        return fail(nullptr, GAUS_E_INVALID_ARG, "poly_chunk must be 0 (auto), negative (off) or in [16, 256]");
     }
     setup_poly(h.D, hp.poly_chunk, c->pa);
 
@@ -383,6 +392,7 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     UP(bsrc, h.bsrc); UP(bdst, h.bdst); UP(bdist, h.bdist); UP(bin_ptr, h.bin_ptr); UP(bin, h.bin);
     UP(bout_ptr, h.bout_ptr); UP(bout, h.bout); UP(perm, h.perm); UP(grp_start, h.grp_start);
     UP(type_grp, h.type_grp); UP(lvl_ptr, h.lvl_ptr); UP(lvl_ops, h.lvl_ops); UP(asap, h.asap);
+    UP(grp_of, h.grp_of);
     UP(alap, h.alap);
 #undef UP
 #define AL(field, n) do { s = dalloc(c, &c->w.field, (n)); if (s != GAUS_OK) goto fail_alloc; } while (0)
@@ -397,6 +407,11 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     AL(wts, (size_t)B * 4);
     AL(adamf, (size_t)B * 2);
     AL(cls, BN);
+    AL(dflag, BN);
+    AL(gflag, (size_t)B * g.ngroups);
+    AL(gsum_ops, (size_t)B * g.ngroups * ntiles * 2);
+    AL(gsum_poly, (size_t)B * g.ngroups * 2);
+    AL(vres_part, (size_t)B * h.K);
     AL(ppoly, BN * kPP);
     AL(cpoly, (size_t)B * h.E * kCP);
     AL(Ucoef, (size_t)B * g.ngroups * kMaxChunks * kNC);
@@ -409,6 +424,7 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
         hipError_t e = hipMemset(c->w.U, 0, sizeof(float) * (size_t)B * h.K * g.T);
         if (e == hipSuccess) e = hipMemset(c->w.ppoly, 0, sizeof(float) * BN * kPP);
         if (e == hipSuccess) e = hipMemset(c->w.cls, 0, BN);
+        if (e == hipSuccess) e = hipMemset(c->w.gsum_poly, 0, sizeof(float) * (size_t)B * g.ngroups * 2);
         if (e == hipSuccess) e = hipDeviceSynchronize();
         if (e != hipSuccess) { s = fail(nullptr, GAUS_E_DEVICE, "init: %s", hipGetErrorString(e)); goto fail_alloc; }
     }

@@ -22,7 +22,7 @@ constexpr int kHalo = 256;  // largest producer delay handled from the LDS row w
 // degree-kDeg polynomial to ~1e-10; sums over steps become dot products.
 constexpr int kDeg = 8;                       // polynomial degree
 constexpr int kNC = kDeg + 1;                 // coefficients per vector
-constexpr int kShiftTerms = 6;                // terms of the one-step shift series
+constexpr int kShiftTerms = 4;                // terms of the one-step shift series
 constexpr int kTN = kDeg + kShiftTerms + 2;   // scaled derivatives T_0 .. T_{kTN-1}
 constexpr int kSmax = 8;                      // largest producer delay on that path
 constexpr float kRhoMax = 0.25f;
@@ -56,6 +56,7 @@ struct Graph {
     const int *grp_start;                // [ngroups+1] ranges of perm
     const int *type_grp;                 // [K+1] groups of type k: [type_grp[k], type_grp[k+1])
     const int *lvl_ptr, *lvl_ops;        // ops by (topological level, id)
+    const int *grp_of;                   // [N] group of each op
     const int *asap, *alap;
 };
 
@@ -72,6 +73,11 @@ struct Work {
     float *wts;       // [B][4]            w_dep, w_res, w_rec, unused
     float *adamf;     // [B][2]            Adam bias corrections 1-beta1^t, 1-beta2^t
     unsigned char *cls;  // [B][N]          1 = op on the chunk-polynomial path this iteration
+    unsigned char *dflag;  // [B][N]        1 = op has step-by-step work (own terms or out-edges)
+    int *gflag;       // [B][ngroups]      1 = some op of the group has step-by-step work
+    float *gsum_ops;  // [B][ngroups][ntiles][2]  V_dep, L_com of a k_ops work-group
+    float *gsum_poly; // [B][ngroups][2]   V_dep, L_com of a k_poly work-group
+    float *vres_part; // [B][K]            V_res of one resource type
     float *ppoly;     // [B][N][kPP]       producer partials of the polynomial path
     float *cpoly;     // [B][E][kCP]       consumer partials of polynomial edges
     float *Ucoef;     // [B][ngroups][kMaxChunks][kNC]  usage coefficients per chunk

@@ -15,6 +15,8 @@
 #include "gaus_internal.h"
 #include "gaus_erfcx_coeffs.h"
 
+#include <algorithm>
+
 namespace gaus {
 
 namespace {
@@ -152,29 +154,28 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
     for (int k = 0; k < SPT; ++k) accU[k] = 0.0f;
     int par = 0;
 
-    // Which ops of the group have step-by-step work: thread t looks at op q0+t
-    // (groups hold at most as many ops as the work-group has threads).  Ops and
-    // edges on the chunk-polynomial path are left to k_poly; an op with none
-    // of its own work gets zero partials here.
+    // Groups without step-by-step work leave nothing here: their readers skip
+    // them (group and op flags).  Otherwise thread t looks at op q0+t (groups
+    // hold at most as many ops as the work-group has threads); ops and edges
+    // on the chunk-polynomial path are left to k_poly.
+    if (!W.gflag[(size_t)b * G.ngroups + grp]) return;
     __shared__ int sDirect[BS];   // 0: nothing; else 1 + number of step-by-step out-edges
     const unsigned char *clsb = W.cls + (size_t)b * N;
     {
         int flag = 0;
         if (q0 + tid < q1) {
             const int i = G.perm[q0 + tid];
-            const int e0 = G.row_ptr[i], e1 = G.row_ptr[i + 1];
-            const bool poly_i = clsb[i] != 0;
-            int m = 0;
-            for (int e = e0; e < e1; ++e) m += (poly_i && clsb[G.col[e]]) ? 0 : 1;
-            flag = (!poly_i || m > 0) ? 1 + m : 0;
-            if (!flag) {
-                float *pp = W.ppart + (((size_t)b * N + i) * G.ntiles + tile) * kPP;
-#pragma unroll
-                for (int c = 0; c < kPP; ++c) pp[c] = 0.0f;
+            if (W.dflag[(size_t)b * N + i]) {
+                const int e0 = G.row_ptr[i], e1 = G.row_ptr[i + 1];
+                const bool poly_i = clsb[i] != 0;
+                int m = 0;
+                for (int e = e0; e < e1; ++e) m += (poly_i && clsb[G.col[e]]) ? 0 : 1;
+                flag = 1 + m;
             }
         }
-        if (tid < BS) sDirect[tid] = flag;
+        sDirect[tid] = flag;
     }
+    float gsum0 = 0.0f, gsum1 = 0.0f;  // V_dep, L_com of the work-group (threads 0, 1)
     __syncthreads();
 
     for (int q = q0; q < q1; ++q) {
@@ -306,9 +307,16 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
             const float r = block_sum<6, BS>(pr, sRed[par]);
             par ^= 1;
             if (tid < kPP) W.ppart[(((size_t)b * N + i) * G.ntiles + tile) * kPP + tid] = r;
+            if (tid == 0) gsum0 += r;
+            if (tid == 1) gsum1 += r;
         } else if (tid < kPP) {
             W.ppart[(((size_t)b * N + i) * G.ntiles + tile) * kPP + tid] = 0.0f;
         }
+    }
+    {
+        float *gs = W.gsum_ops + (((size_t)b * G.ngroups + grp) * G.ntiles + tile) * 2;
+        if (tid == 0) gs[0] = gsum0;
+        if (tid == 1) gs[1] = gsum1;
     }
 
     float *up = W.Upart + ((size_t)b * G.ngroups + grp) * D;
@@ -344,9 +352,23 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
 __global__ void k_classify(Graph G, PolyArgs pa, const float *__restrict__ sigma, Work W) {
     const int b = blockIdx.y;
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < G.ngroups) W.gflag[(size_t)b * G.ngroups + i] = 0;
     if (i >= G.N) return;
     const float s = sigma[(size_t)b * G.N + i];
     W.cls[(size_t)b * G.N + i] = (pa.enabled && s >= pa.sig_thr && G.delay[i] <= kSmax) ? 1 : 0;
+}
+
+// Which ops (and groups) have step-by-step work this iteration: ops off the
+// polynomial path, and polynomial ops with an out-edge to such an op.
+__global__ void k_flags(Graph G, Work W) {
+    const int b = blockIdx.y;
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= G.N) return;
+    const unsigned char *clsb = W.cls + (size_t)b * G.N;
+    int d = clsb[i] ? 0 : 1;
+    for (int e = G.row_ptr[i]; e < G.row_ptr[i + 1] && !d; ++e) d = clsb[G.col[e]] ? 0 : 1;
+    W.dflag[(size_t)b * G.N + i] = (unsigned char)d;
+    if (d) atomicOr(&W.gflag[(size_t)b * G.ngroups + G.grp_of[i]], 1);
 }
 
 namespace {
@@ -455,6 +477,7 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
     // dynamic LDS: per wave 7 rows of SP strip values, then per wave SP strip usages
     extern __shared__ float sDyn[];
     __shared__ float sUc[kPolyWaves][kMaxChunks][kNC];
+    __shared__ float sGs[kPolyWaves][2];
     const int SP = pa.SP;
     const int grp = blockIdx.x, b = blockIdx.y;
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
@@ -487,6 +510,7 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
         l_s = G.delay[l_i];
         l_e0 = G.row_ptr[l_i]; l_e1 = G.row_ptr[l_i + 1];
     }
+    float gsum0 = 0.0f, gsum1 = 0.0f;  // V_dep, L_com of this wave's ops
     for (int oq = 0; oq < nq; ++oq) {
         const int i = __builtin_amdgcn_readlane(l_i, oq);
         float *pp = W.ppoly + ((size_t)b * N + i) * kPP;
@@ -624,7 +648,10 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
 #pragma unroll
         for (int c = 0; c < kPP; ++c) pr[c] = wave_sum(pr[c]);
         if (lane < kPP) pp[lane] = pr[lane];
+        gsum0 += pr[0];
+        gsum1 += pr[1];
     }
+    if (lane == 0) { sGs[wv][0] = gsum0; sGs[wv][1] = gsum1; }
 
     // usage of the group: combine the waves' chunk coefficients and strip values
 #pragma unroll
@@ -642,6 +669,12 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
 #pragma unroll
         for (int w = 0; w < kPolyWaves; ++w) acc += sUc[w][c][k];
         ucg[x] = acc;
+    }
+    if (threadIdx.x < 2) {
+        float acc = 0.0f;
+#pragma unroll
+        for (int w = 0; w < kPolyWaves; ++w) acc += sGs[w][threadIdx.x];
+        W.gsum_poly[((size_t)b * G.ngroups + grp) * 2 + threadIdx.x] = acc;
     }
     float *usg = W.Ustrip + ((size_t)b * G.ngroups + grp) * kStripMax;
     for (int p = threadIdx.x; p < kStripMax; p += 64 * kPolyWaves) {
@@ -708,51 +741,77 @@ __global__ __launch_bounds__(BS) void k_back(Graph G, const float *__restrict__ 
 // ---------------------------------------------------------------------------
 // Usage: U[b][k][slot] = sum over type-k groups and steps t = slot (mod T).
 // ---------------------------------------------------------------------------
-// Usage of the polynomial ops at step t: their mass coefficients summed over
-// the type's groups, evaluated at t (chunk part), or the strip values.
-__device__ __forceinline__ float poly_usage_at(const Graph &G, const PolyArgs &pa, const Work &W, int b,
-                                               int k, int t) {
-    float acc = 0.0f;
-    if (t >= pa.L0 && t < G.D - 2) {
-        const int c = (t - pa.L0) / pa.W;
-        const float x = ((float)(t - pa.L0 - c * pa.W) - pa.lam) / pa.lam;
-        for (int g = G.type_grp[k]; g < G.type_grp[k + 1]; ++g) {
-            const float *cf = W.Ucoef + (((size_t)b * G.ngroups + g) * kMaxChunks + c) * kNC;
-            float v = cf[kNC - 1];
-#pragma unroll
-            for (int q = kNC - 2; q >= 0; --q) v = fmaf(v, x, cf[q]);
-            acc += v;
-        }
-    } else {
-        const int p = t < pa.L0 ? t : pa.L0 + (t - (G.D - 2));
-        for (int g = G.type_grp[k]; g < G.type_grp[k + 1]; ++g)
-            acc += W.Ustrip[((size_t)b * G.ngroups + g) * kStripMax + p];
-    }
-    return acc;
-}
+// Usage per (type, restart): U(t) = step-by-step group partials (active groups
+// only) + the polynomial ops' mass coefficients summed over the type's groups
+// and evaluated at t (chunk part) or their strip values; then the fold mod T.
+constexpr int kUsageBS = 256;
 
-__global__ void k_usage(Graph G, PolyArgs pa, Work W) {
-    const int b = blockIdx.y;
-    const int cell = blockIdx.x * blockDim.x + threadIdx.x;
-    if (cell >= G.K * G.T) return;
-    const int k = cell / G.T, slot = cell % G.T;
-    float acc = 0.0f;
-    for (int t = slot; t < G.D; t += G.T) {
-        float ut = 0.0f;
-        for (int g = G.type_grp[k]; g < G.type_grp[k + 1]; ++g)
-            ut += W.Upart[((size_t)b * G.ngroups + g) * G.D + t];
-        if (pa.enabled) ut += poly_usage_at(G, pa, W, b, k, t);
-        acc += ut;
+__global__ __launch_bounds__(kUsageBS) void k_usage(Graph G, PolyArgs pa, Work W) {
+    __shared__ float sC[kMaxChunks * kNC];
+    __shared__ float sS[kStripMax];
+    constexpr int kMaxAct = 1024;
+    __shared__ int sAct[kMaxAct];
+    __shared__ int sNact;
+    const int k = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+    const int g0 = G.type_grp[k], g1 = G.type_grp[k + 1];
+    const int D = G.D, T = G.T;
+    // the type's groups with step-by-step partials (-1: too many to list)
+    if (tid == 0) {
+        int n = 0;
+        for (int g = g0; g < g1 && n >= 0; ++g)
+            if (W.gflag[(size_t)b * G.ngroups + g]) {
+                if (n < kMaxAct) sAct[n++] = g;
+                else n = -1;
+            }
+        sNact = n;
     }
-    W.U[(size_t)b * G.K * G.T + cell] = acc;
+    if (pa.enabled) {
+        for (int x = tid; x < pa.nc * kNC; x += kUsageBS) {
+            float acc = 0.0f;
+            for (int g = g0; g < g1; ++g) acc += W.Ucoef[((size_t)b * G.ngroups + g) * kMaxChunks * kNC + x];
+            sC[x] = acc;
+        }
+        for (int p = tid; p < pa.SP; p += kUsageBS) {
+            float acc = 0.0f;
+            for (int g = g0; g < g1; ++g) acc += W.Ustrip[((size_t)b * G.ngroups + g) * kStripMax + p];
+            sS[p] = acc;
+        }
+    }
+    __syncthreads();
+    const int nact = sNact;
+    for (int slot = tid; slot < T; slot += kUsageBS) {
+        float acc = 0.0f;
+        for (int t = slot; t < D; t += T) {
+            float ut = 0.0f;
+            if (nact >= 0) {
+                for (int q = 0; q < nact; ++q) ut += W.Upart[((size_t)b * G.ngroups + sAct[q]) * D + t];
+            } else {
+                for (int g = g0; g < g1; ++g)
+                    if (W.gflag[(size_t)b * G.ngroups + g]) ut += W.Upart[((size_t)b * G.ngroups + g) * D + t];
+            }
+            if (pa.enabled) {
+                if (t >= pa.L0 && t < D - 2) {
+                    const int c = (t - pa.L0) / pa.W;
+                    const float x = ((float)(t - pa.L0 - c * pa.W) - pa.lam) / pa.lam;
+                    const float *cf = sC + c * kNC;
+                    float v = cf[kNC - 1];
+#pragma unroll
+                    for (int q = kNC - 2; q >= 0; --q) v = fmaf(v, x, cf[q]);
+                    ut += v;
+                } else {
+                    ut += sS[t < pa.L0 ? t : pa.L0 + (t - (D - 2))];
+                }
+            }
+            acc += ut;
+        }
+        W.U[((size_t)b * G.K + k) * T + slot] = acc;
+    }
 }
 
 // ---------------------------------------------------------------------------
-// Per-restart scalars.  One work-group of 1024 threads per restart:
-// V_res (eq:relu), the sign changes of the ReLU indicator along the bin edges,
-// V_dep / L_com / V_rec from the partials, the augmented Lagrangian (eq. 11),
-// the weights w_c = lambda_c + rho V_c, and in step mode the multiplier update
-// lambda_c += rho V_c and the Adam bias corrections.
+// Per (type, restart): the type's share of V_res (eq:relu) and the bin edges
+// t = 0..D-2 where its ReLU indicator I(t mod T) != I((t+1) mod T) changes,
+// compacted in increasing t (wave ballots + a work-group prefix).
 // ---------------------------------------------------------------------------
 constexpr int kTermsBS = 1024;
 
@@ -768,71 +827,92 @@ __device__ float block_sum1024(float x, float *scratch /*[16]*/) {
     return r;
 }
 
-__global__ __launch_bounds__(kTermsBS) void k_terms(Graph G, Work W, HP hp,
-                                                    const float *__restrict__ lambda_in,
-                                                    float *lambda_out, const int *adam_t,
-                                                    float *terms_out) {
+__global__ __launch_bounds__(kTermsBS) void k_vres(Graph G, Work W) {
     __shared__ float scratch[kTermsBS / 64];
     __shared__ int wcount[kTermsBS / 64];
     __shared__ int base;
-    const int b = blockIdx.x, tid = threadIdx.x;
+    const int k = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
     const int lane = tid & 63, wid = tid >> 6;
-    const int K = G.K, T = G.T, D = G.D;
-    const float *U = W.U + (size_t)b * K * T;
+    const int T = G.T, D = G.D;
+    const float ck = G.cap[k];
+    const float *Uk = W.U + ((size_t)b * G.K + k) * T;
 
     float vres = 0.0f;
-    for (int c = tid; c < K * T; c += kTermsBS) {
-        const float ex = U[c] - G.cap[c / T];
+    for (int c = tid; c < T; c += kTermsBS) {
+        const float ex = Uk[c] - ck;
         if (ex > 0.0f) vres += ex;
     }
     vres = block_sum1024(vres, scratch);
+    if (tid == 0) W.vres_part[(size_t)b * G.K + k] = vres;
 
-    // ReLU-indicator changes I(t mod T) != I((t+1) mod T) at bin edges t = 0..D-2,
-    // compacted in increasing t (wave ballots + a work-group prefix).
-    for (int k = 0; k < K; ++k) {
-        const float ck = G.cap[k];
-        const float *Uk = U + (size_t)k * T;
-        int *out = W.trans + ((size_t)b * K + k) * D;
-        if (tid == 0) base = 0;
-        __syncthreads();
-        for (int t0 = 0; t0 < D - 1; t0 += kTermsBS) {
-            const int t = t0 + tid;
-            int sgn = 0;
-            if (t < D - 1) {
-                const int a = Uk[t % T] > ck, c = Uk[(t + 1) % T] > ck;
-                sgn = a - c;
-            }
-            const unsigned long long bal = __ballot(sgn != 0);
-            const int before = __popcll(bal & ((1ull << lane) - 1ull));
-            if (lane == 0) wcount[wid] = __popcll(bal);
-            __syncthreads();
-            int off = base;
-            for (int w = 0; w < wid; ++w) off += wcount[w];
-            if (sgn != 0) out[off + before] = sgn * (t + 1);
-            __syncthreads();
-            if (tid == 0) {
-                int tot = 0;
-                for (int w = 0; w < kTermsBS / 64; ++w) tot += wcount[w];
-                base += tot;
-            }
-            __syncthreads();
+    int *out = W.trans + ((size_t)b * G.K + k) * D;
+    if (tid == 0) base = 0;
+    __syncthreads();
+    for (int t0 = 0; t0 < D - 1; t0 += kTermsBS) {
+        const int t = t0 + tid;
+        int sgn = 0;
+        if (t < D - 1) {
+            const int a = Uk[t % T] > ck, c = Uk[(t + 1) % T] > ck;
+            sgn = a - c;
         }
-        if (tid == 0) W.ntrans[(size_t)b * K + k] = base;
+        const unsigned long long bal = __ballot(sgn != 0);
+        const int before = __popcll(bal & ((1ull << lane) - 1ull));
+        if (lane == 0) wcount[wid] = __popcll(bal);
+        __syncthreads();
+        int off = base;
+        for (int w = 0; w < wid; ++w) off += wcount[w];
+        if (sgn != 0) out[off + before] = sgn * (t + 1);
+        __syncthreads();
+        if (tid == 0) {
+            int tot = 0;
+            for (int w = 0; w < kTermsBS / 64; ++w) tot += wcount[w];
+            base += tot;
+        }
         __syncthreads();
     }
+    if (tid == 0) W.ntrans[(size_t)b * G.K + k] = base;
+}
 
-    float vdep = 0.0f, lcom = 0.0f, vrec = 0.0f;
-    const size_t np = (size_t)G.N * G.ntiles;
-    const float *pp = W.ppart + (size_t)b * np * kPP;
-    for (size_t r = tid; r < np; r += kTermsBS) { vdep += pp[r * kPP + 0]; lcom += pp[r * kPP + 1]; }
-    const float *ppy = W.ppoly + (size_t)b * G.N * kPP;
-    for (int r = tid; r < G.N; r += kTermsBS) { vdep += ppy[(size_t)r * kPP + 0]; lcom += ppy[(size_t)r * kPP + 1]; }
+// ---------------------------------------------------------------------------
+// Per restart: V_res, V_dep, L_com, V_rec from the partials, the augmented
+// Lagrangian (eq. 11), the weights w_c = lambda_c + rho V_c, and in step mode
+// the multiplier update lambda_c += rho V_c and the Adam bias corrections.
+// ---------------------------------------------------------------------------
+constexpr int kCombineBS = 256;
+
+__device__ float block_sum256(float x, float *scratch /*[4]*/) {
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    x = wave_sum(x);
+    if (lane == 0) scratch[wid] = x;
+    __syncthreads();
+    const float r = (scratch[0] + scratch[1]) + (scratch[2] + scratch[3]);
+    __syncthreads();
+    return r;
+}
+
+__global__ __launch_bounds__(kCombineBS) void k_combine(Graph G, Work W, HP hp,
+                                                        const float *__restrict__ lambda_in,
+                                                        float *lambda_out, const int *adam_t,
+                                                        float *terms_out) {
+    __shared__ float scratch[kCombineBS / 64];
+    const int b = blockIdx.x, tid = threadIdx.x;
+    float vres = 0.0f, vdep = 0.0f, lcom = 0.0f, vrec = 0.0f;
+    for (int k = tid; k < G.K; k += kCombineBS) vres += W.vres_part[(size_t)b * G.K + k];
+    for (int g = tid; g < G.ngroups; g += kCombineBS) {
+        const float *gp = W.gsum_poly + ((size_t)b * G.ngroups + g) * 2;
+        vdep += gp[0]; lcom += gp[1];
+        if (W.gflag[(size_t)b * G.ngroups + g]) {
+            const float *go = W.gsum_ops + ((size_t)b * G.ngroups + g) * G.ntiles * 2;
+            for (int tl = 0; tl < G.ntiles; ++tl) { vdep += go[2 * tl]; lcom += go[2 * tl + 1]; }
+        }
+    }
     const size_t nbp = (size_t)G.nb * G.ntiles;
     const float *bp = W.bpart + (size_t)b * nbp * kBP;
-    for (size_t r = tid; r < nbp; r += kTermsBS) vrec += bp[r * kBP + 0];
-    vdep = block_sum1024(vdep, scratch);
-    lcom = block_sum1024(lcom, scratch);
-    vrec = block_sum1024(vrec, scratch);
+    for (size_t r = tid; r < nbp; r += kCombineBS) vrec += bp[r * kBP + 0];
+    vres = block_sum256(vres, scratch);
+    vdep = block_sum256(vdep, scratch);
+    lcom = block_sum256(lcom, scratch);
+    vrec = block_sum256(vrec, scratch);
 
     if (tid == 0) {
         const float V[3] = {vdep, vres, vrec};
@@ -912,10 +992,12 @@ __global__ __launch_bounds__(256) void k_final(Graph G, Work W, HP hp, const flo
     }
 
     float dm = 0.0f, ds = 0.0f, cm = 0.0f, cs = 0.0f;
-    const float *pp = W.ppart + bi * nt * kPP;
-    for (int tl = 0; tl < nt; ++tl) {
-        dm += pp[tl * kPP + 2]; ds += pp[tl * kPP + 3];
-        cm += pp[tl * kPP + 4]; cs += pp[tl * kPP + 5];
+    if (W.dflag[bi]) {
+        const float *pp = W.ppart + bi * nt * kPP;
+        for (int tl = 0; tl < nt; ++tl) {
+            dm += pp[tl * kPP + 2]; ds += pp[tl * kPP + 3];
+            cm += pp[tl * kPP + 4]; cs += pp[tl * kPP + 5];
+        }
     }
     const float *ppy = W.ppoly + bi * kPP;
     dm += ppy[2]; ds += ppy[3]; cm += ppy[4]; cs += ppy[5];
@@ -1105,8 +1187,10 @@ static void launch_back(const Graph &g, const Work &w, const float *mu, const fl
 hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const LaunchCfg &lc,
                              const PolyArgs &pa, const IterArgs &a, hipStream_t st) {
     {
-        dim3 grid((g.N + 255) / 256, g.B);
+        dim3 grid((std::max(g.N, g.ngroups) + 255) / 256, g.B);
         hipLaunchKernelGGL(k_classify, grid, dim3(256), 0, st, g, pa, a.sigma, w);
+        dim3 grid2((g.N + 255) / 256, g.B);
+        hipLaunchKernelGGL(k_flags, grid2, dim3(256), 0, st, g, w);
     }
     if (a.ops_begin) (void)hipEventRecord(a.ops_begin, st);
     if (lc.bs == 64 && lc.spt == 1) launch_ops<64, 1>(g, w, a.mu, a.sigma, st);
@@ -1125,12 +1209,9 @@ hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const 
         else if (lc.spt == 1) launch_back<256, 1>(g, w, a.mu, a.sigma, st);
         else launch_back<256, 4>(g, w, a.mu, a.sigma, st);
     }
-    {
-        const int cells = g.K * g.T;
-        dim3 grid((cells + 255) / 256, g.B);
-        hipLaunchKernelGGL(k_usage, grid, dim3(256), 0, st, g, pa, w);
-    }
-    hipLaunchKernelGGL(k_terms, dim3(g.B), dim3(kTermsBS), 0, st, g, w, hp, a.lambda_in,
+    hipLaunchKernelGGL(k_usage, dim3(g.K, g.B), dim3(kUsageBS), 0, st, g, pa, w);
+    hipLaunchKernelGGL(k_vres, dim3(g.K, g.B), dim3(kTermsBS), 0, st, g, w);
+    hipLaunchKernelGGL(k_combine, dim3(g.B), dim3(kCombineBS), 0, st, g, w, hp, a.lambda_in,
                        a.mode == 1 ? a.lambda_out : nullptr, a.mode == 1 ? a.adam_t : nullptr,
                        a.terms_out);
     {
