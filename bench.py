@@ -10,9 +10,9 @@ legalization of every restart (gaus_legalize), so every step of the path is
 inside it.  Inputs are resident in HBM before timing starts.
 
 Prints one JSON line with the metric (op-step evaluations per second =
-B*N*D / seconds per step), the roofline of the dominant kernel (the op
-kernel, timed with HIP events on the library's stream) and the CPU oracle
-timed on a bounded sample of the same workload.
+B*N*D / seconds per step), the roofline of the dominant kernel (timed with
+HIP events on the library's stream) and the CPU oracle timed on a bounded
+sample of the same workload.
 
   python bench.py [--steps K] [--warmup W] [--workload large]
 """
@@ -40,13 +40,21 @@ METRIC = "op-step evals/sec (fwd+bwd+Adam), ms/iteration, % roofline at 50k ops"
 # the v_fma_f32 to the v_exp_f32 rate on gfx950 (gaus_microbench:
 # 100.4 vs 21.2 per clock per CU).  One slot = one fp32 FMA = 2 flops; the
 # peak is MI355X's 157.3 TFLOP/s fp32 vector rate.
+#
+# The units of one launch of a kernel are the op-bin-edges and edge-steps it
+# is responsible for: the chunk-polynomial kernel (k_poly) owns the (restart,
+# op) pairs classified onto its path and the edges with both ends there
+# (gaus_poly_census); the step-by-step kernel (k_ops) owns the rest of the
+# forward edges and ops.  k_poly reaches its units through per-chunk
+# polynomial expansions, so its figure is an effective rate of this per-unit
+# model, not an instruction-issue rate.
 FMA_PER_OP_STEP = 20.0
 TRANS_PER_OP_STEP = 2.0
 FMA_PER_EDGE_STEP = 10.0
 TRANS_WEIGHT = 100.4 / 21.2
 PEAK_TFLOPS = 157.3
-PMC_SUMMARY = os.path.join(ROOT, "profiles", "k_ops_large_pmc.md")
 KERNEL_SRC = os.path.join(ROOT, "paper_2602_20427_amd", "csrc", "gaus_kernels.hip")
+KERNEL_NAMES = {"ops": "k_ops", "poly": "k_poly"}
 
 
 def log(*a):
@@ -58,19 +66,18 @@ def kernel_source_hash() -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def algorithmic_flops(N, E, nb, D, B):
-    units_op = B * N * (D - 1)
-    units_edge = B * (E + nb) * (D - 1)
+def model_flops(units_op, units_edge):
     slots = units_op * (FMA_PER_OP_STEP + TRANS_PER_OP_STEP * TRANS_WEIGHT) + units_edge * FMA_PER_EDGE_STEP
     return 2.0 * slots
 
 
-def pmc_traffic(workload):
-    """HBM bytes per op-kernel launch from the committed rocprofv3 counter
+def pmc_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
     summary, if it was taken on the current kernel source; else None."""
-    if workload != "large" or not os.path.exists(PMC_SUMMARY):
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_pmc.md")
+    if not os.path.exists(path):
         return None
-    txt = open(PMC_SUMMARY).read()
+    txt = open(path).read()
     h = re.search(r"kernel_source_sha256:\s*([0-9a-f]+)", txt)
     v = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", txt)
     if not h or not v or h.group(1) != kernel_source_hash():
@@ -174,37 +181,53 @@ def main():
     t1 = time.perf_counter()
     ktimes = ctx.kernel_timing_read()
     ctx.kernel_timing(False)
-    # the dominant kernel: step-by-step op kernel or chunk-polynomial kernel
-    kname = max(ktimes, key=lambda k: ktimes[k][0])
-    ops_ms_total, ops_launches = ktimes[kname]
+    census = ctx.poly_census()
     step_ms_events = ev[0].elapsed_time(ev[1]) / args.steps
     legalize_ms = ev[1].elapsed_time(ev[2])
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     tt = terms.cpu().numpy()
+
+    # units of each per-step kernel (see the cost model above)
+    E = prob.n_edges
+    units = {"poly": (census["ops"] * (D - 1), census["edges"] * (D - 1)),
+             "ops": ((B * N - census["ops"]) * (D - 1), (B * E - census["edges"]) * (D - 1))}
+    kern = {}
+    for k, (tot_ms, n) in ktimes.items():
+        if n == 0:
+            continue
+        kms = tot_ms / n
+        fl = model_flops(*units[k])
+        kern[KERNEL_NAMES[k]] = {"ms": kms, "launches": n, "op_bin_edges": units[k][0],
+                                 "edge_steps": units[k][1], "model_tflops": fl / 1e12,
+                                 "achieved_tflops": fl / (kms * 1e-3) / 1e12}
+    dom = max(kern, key=lambda k: kern[k]["ms"])
     log(f"[bench] {ms_per_step:.3f} ms/step wall; gaus_step {step_ms_events:.3f} ms/iter (events); "
-        f"legalize {legalize_ms:.3f} ms; op kernel {ops_ms_total / max(ops_launches, 1):.3f} ms x {ops_launches}")
+        f"legalize {legalize_ms:.3f} ms; " +
+        "; ".join(f"{k} {v['ms']:.3f} ms x {v['launches']}" for k, v in kern.items()))
+    log(f"[bench] polynomial path: {census['ops']} of {B * N} (restart, op) pairs, "
+        f"{census['edges']} of {B * E} (restart, edge) pairs")
     log(f"[bench] last terms restart 0: L={tt[0, 0]:.6g} V_dep={tt[0, 1]:.6g} V_res={tt[0, 2]:.6g} "
         f"V_rec={tt[0, 3]:.6g} L_com={tt[0, 4]:.6g}; legalize status {status.tolist()}")
 
     value = B * N * D / (ms_per_step * 1e-3)
-    ops_ms = ops_ms_total / max(ops_launches, 1)
-    flops = algorithmic_flops(N, prob.n_edges, prob.n_back, D, B)
-    achieved = flops / (ops_ms * 1e-3) / 1e12
-    traffic = pmc_traffic(args.workload)
+    achieved = kern[dom]["achieved_tflops"]
+    whole = model_flops(B * N * (D - 1), B * (E + prob.n_back) * (D - 1))
     out = {
         "metric": METRIC, "value": value, "unit": "op-step evals/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": describe(cfg, prob), "B": B, "N": N, "E": prob.n_edges,
+        "config": {"workload": describe(cfg, prob), "B": B, "N": N, "E": E,
                    "n_back": prob.n_back, "D": D, "II": prob.II},
         "ms_per_iteration_events": step_ms_events, "legalize_ms": legalize_ms,
         "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_TFLOPS, "traffic": traffic,
-                     "kernel": "k_ops", "kernel_ms": ops_ms,
+                     "frac": achieved / PEAK_TFLOPS, "traffic": pmc_traffic(dom, args.workload),
+                     "kernel": dom, "kernel_ms": kern[dom]["ms"],
                      "model": f"{FMA_PER_OP_STEP:g} FMA + {TRANS_PER_OP_STEP:g} transcendental "
                               f"(x{TRANS_WEIGHT:.2f} FMA slots) per op-bin-edge, {FMA_PER_EDGE_STEP:g} FMA per "
-                              f"edge-step, 2 flops per FMA slot"},
+                              f"edge-step, 2 flops per FMA slot; units = those the kernel owns"},
+        "kernels": kern,
+        "iteration_model_tflops_per_s": whole / (step_ms_events * 1e-3) / 1e12,
     }
     if not args.no_cpu_baseline:
         log(f"[bench] CPU oracle on {args.cpu_restarts} restarts")

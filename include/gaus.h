@@ -175,6 +175,13 @@ gaus_status gaus_get_dims(const gaus_ctx *ctx, int32_t dims[8]);
  * chunks, left strip width.  Ops whose sigma >= 2(W-1) and Lat <= 8 use it. */
 gaus_status gaus_get_poly_config(const gaus_ctx *ctx, int32_t cfg[4]);
 
+/* Census of the last iteration's classification (HOST output, [2]):
+ * [0] (restart, op) pairs on the chunk-polynomial path, [1] (restart, edge)
+ * pairs whose producer and consumer both are (the edge terms that kernel
+ * evaluates).  The rest are evaluated step by step.  Synchronizes the stream;
+ * zeros before the first iteration. */
+gaus_status gaus_poly_census(gaus_ctx *ctx, int64_t counts[2]);
+
 /* Message of the last failed call on ctx (or of the last failed gaus_init
  * when ctx is NULL).  Never NULL. */
 const char *gaus_last_error(const gaus_ctx *ctx);

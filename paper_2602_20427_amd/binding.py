@@ -22,7 +22,7 @@ OK, E_INVALID_ARG, E_CYCLE, E_HORIZON, E_NOT_CONVERGED, E_OVERFLOW, E_DEVICE, E_
 EXPORTS = ("gaus_default_hparams", "gaus_init", "gaus_bind_state", "gaus_loss_grad", "gaus_step",
            "gaus_adam_from_grad", "gaus_legalize", "gaus_init_state", "gaus_asap_alap",
            "gaus_get_usage", "gaus_kernel_timing", "gaus_kernel_timing_read", "gaus_sync",
-           "gaus_get_dims", "gaus_get_poly_config", "gaus_last_error", "gaus_status_string",
+           "gaus_get_dims", "gaus_get_poly_config", "gaus_poly_census", "gaus_last_error", "gaus_status_string",
            "gaus_destroy")
 
 
@@ -75,6 +75,7 @@ def load():
         "gaus_sync": ([vp], C.c_int),
         "gaus_get_dims": ([vp, vp], C.c_int),
         "gaus_get_poly_config": ([vp, vp], C.c_int),
+        "gaus_poly_census": ([vp, vp], C.c_int),
         "gaus_last_error": ([vp], C.c_char_p),
         "gaus_status_string": ([C.c_int], C.c_char_p),
         "gaus_destroy": ([vp], None),
@@ -238,6 +239,13 @@ class Context:
         cfg = np.zeros(4, np.int32)
         self._check(load().gaus_get_poly_config(self._h, _np_ptr(cfg)))
         return {"enabled": bool(cfg[0]), "W": int(cfg[1]), "chunks": int(cfg[2]), "L0": int(cfg[3])}
+
+    def poly_census(self):
+        """(restart, op) and (restart, edge) pairs evaluated by the chunk-
+        polynomial kernel in the last iteration."""
+        c = np.zeros(2, np.int64)
+        self._check(load().gaus_poly_census(self._h, _np_ptr(c)))
+        return {"ops": int(c[0]), "edges": int(c[1])}
 
     def sync(self):
         self._check(load().gaus_sync(self._h))

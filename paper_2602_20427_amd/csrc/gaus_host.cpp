@@ -597,4 +597,30 @@ gaus_status gaus_get_poly_config(const gaus_ctx *ctx, int32_t cfg[4]) {
     return GAUS_OK;
 }
 
+gaus_status gaus_poly_census(gaus_ctx *ctx, int64_t counts[2]) {
+    if (!ctx) return GAUS_E_INVALID_ARG;
+    if (!counts) return fail(ctx, GAUS_E_INVALID_ARG, "poly_census: null pointer");
+    const Graph &g = ctx->g;
+    hipError_t e = hipStreamSynchronize(ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "poly_census");
+    std::vector<unsigned char> cls((size_t)g.B * g.N);
+    std::vector<int> rp(g.N + 1), col(std::max(g.E, 1));
+    e = hipMemcpy(cls.data(), ctx->w.cls, cls.size(), hipMemcpyDeviceToHost);
+    if (e == hipSuccess) e = hipMemcpy(rp.data(), g.row_ptr, sizeof(int) * rp.size(), hipMemcpyDeviceToHost);
+    if (e == hipSuccess && g.E > 0) e = hipMemcpy(col.data(), g.col, sizeof(int) * g.E, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(ctx, e, "poly_census");
+    int64_t nop = 0, ned = 0;
+    for (int b = 0; b < g.B; ++b) {
+        const unsigned char *c = cls.data() + (size_t)b * g.N;
+        for (int i = 0; i < g.N; ++i) {
+            if (!c[i]) continue;
+            ++nop;
+            for (int q = rp[i]; q < rp[i + 1]; ++q) ned += c[col[q]] ? 1 : 0;
+        }
+    }
+    counts[0] = nop;
+    counts[1] = ned;
+    return GAUS_OK;
+}
+
 }  // extern "C"

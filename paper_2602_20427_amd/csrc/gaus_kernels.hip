@@ -79,10 +79,59 @@ __device__ __forceinline__ float st_at(long long v, int D, float mu, float rs) {
     return (z >= 0.0f) ? -tail : tail;
 }
 
-__device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
+// Wave-wide sums with DPP lane moves (fused into the adds) inside rows of 16
+// lanes and the gfx950 lane-swap instructions across rows.
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float x) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+constexpr int kDppXor1 = 0xB1;        // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;        // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141;
+constexpr int kDppMirror = 0x140;
+constexpr int kDppRor4 = 0x124;
+constexpr int kDppRor8 = 0x128;
+
+// sum over lanes l, l^16, l^32, l^48 (LDS swizzle inside halves, LDS
+// permute across them); each pair is added in both lanes in the same order
+__device__ __forceinline__ float cross_rows_sum(float x) {
+    constexpr int kSwizzleXor16 = 0x1F | (0x10 << 10);   // bit mode: and 31, xor 16
+    x += __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), kSwizzleXor16));
+    const int lane = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+    x += __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute((lane ^ 32) << 2, __builtin_bit_cast(int, x)));
     return x;
+}
+
+// Sum over the 64 lanes; every lane receives the same total.
+__device__ __forceinline__ float wave_sum(float x) {
+    x += dpp_mov<kDppXor1>(x);
+    x += dpp_mov<kDppXor2>(x);
+    x += dpp_mov<kDppHalfMirror>(x);
+    x += dpp_mov<kDppMirror>(x);
+    return cross_rows_sum(x);
+}
+
+// Four sums at once: lane l < 4 receives the total of value wave4_comp(l).
+__device__ __forceinline__ int wave4_comp(int lane) { return 2 * (lane & 1) + ((lane >> 1) & 1); }
+
+__device__ __forceinline__ float wave_sum4(float v0, float v1, float v2, float v3, int lane) {
+    const bool b0 = lane & 1, b1 = lane & 2;
+    const float a = (b0 ? v2 : v0) + dpp_mov<kDppXor1>(b0 ? v0 : v2);   // value 2*b0
+    const float c = (b0 ? v3 : v1) + dpp_mov<kDppXor1>(b0 ? v1 : v3);   // value 2*b0+1
+    float x = (b1 ? c : a) + dpp_mov<kDppXor2>(b1 ? a : c);             // value 2*b0+b1
+    x += dpp_mov<kDppRor4>(x);
+    x += dpp_mov<kDppRor8>(x);
+    return cross_rows_sum(x);
+}
+
+// Two sums at once: lane l < 2 receives the total of value l.
+__device__ __forceinline__ float wave_sum2(float v0, float v1, int lane) {
+    const bool b0 = lane & 1;
+    float x = (b0 ? v1 : v0) + dpp_mov<kDppXor1>(b0 ? v0 : v1);
+    x += dpp_mov<kDppXor2>(x);
+    x += dpp_mov<kDppRor4>(x);
+    x += dpp_mov<kDppRor8>(x);
+    return cross_rows_sum(x);
 }
 
 // Sum NV values over the work-group; thread c < NV receives total c.
@@ -510,7 +559,7 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
         l_s = G.delay[l_i];
         l_e0 = G.row_ptr[l_i]; l_e1 = G.row_ptr[l_i + 1];
     }
-    float gsum0 = 0.0f, gsum1 = 0.0f;  // V_dep, L_com of this wave's ops
+    float gsum = 0.0f;  // V_dep, L_com of this wave's ops (lanes 0 and 2)
     for (int oq = 0; oq < nq; ++oq) {
         const int i = __builtin_amdgcn_readlane(l_i, oq);
         float *pp = W.ppoly + ((size_t)b * N + i) * kPP;
@@ -641,17 +690,17 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
                 pr[2] -= vdot(HFm1, v);
                 pr[3] -= vdot(HFs1, v);
             }
-#pragma unroll
-            for (int c = 0; c < 4; ++c) cc[c] = wave_sum(cc[c]);
-            if (lane < kCP) W.cpoly[((size_t)b * G.E + e) * kCP + lane] = cc[lane];
+            const float ct = wave_sum4(cc[0], cc[1], cc[2], cc[3], lane);
+            if (lane < kCP) W.cpoly[((size_t)b * G.E + e) * kCP + wave4_comp(lane)] = ct;
         }
-#pragma unroll
-        for (int c = 0; c < kPP; ++c) pr[c] = wave_sum(pr[c]);
-        if (lane < kPP) pp[lane] = pr[lane];
-        gsum0 += pr[0];
-        gsum1 += pr[1];
+        const float pt4 = wave_sum4(pr[0], pr[1], pr[2], pr[3], lane);
+        const float pt2 = wave_sum2(pr[4], pr[5], lane);
+        if (lane < 4) pp[wave4_comp(lane)] = pt4;
+        if (lane < 2) pp[4 + lane] = pt2;
+        gsum += pt4;   // lane 0: V_dep, lane 2: L_com
     }
-    if (lane == 0) { sGs[wv][0] = gsum0; sGs[wv][1] = gsum1; }
+    if (lane == 0) sGs[wv][0] = gsum;
+    if (lane == 2) sGs[wv][1] = gsum;
 
     // usage of the group: combine the waves' chunk coefficients and strip values
 #pragma unroll
