@@ -99,7 +99,7 @@ void setup_poly(int D, int requested, PolyArgs &pa) {
         const int n = std::min(kMaxChunks, (D - 2 - kSmax) / w);
         if (n < 4) continue;
         const int sp = D - 2 - n * w + 2;
-        if (sp > 320) continue;
+        if (sp > kStripMax) continue;
         const int passes = (sp + 63) / 64;
         if (passes < best_passes) { best_passes = passes; W = w; nc = n; }
     }
@@ -412,10 +412,11 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     AL(gsum_ops, (size_t)B * g.ngroups * ntiles * 2);
     AL(gsum_poly, (size_t)B * g.ngroups * 2);
     AL(vres_part, (size_t)B * h.K);
+    AL(Ucoef_k, (size_t)B * h.K * (kMaxChunks * kNC + kStripMax));
     AL(ppoly, BN * kPP);
     AL(cpoly, (size_t)B * h.E * kCP);
     AL(Ucoef, (size_t)B * g.ngroups * kMaxChunks * kNC);
-    AL(Ustrip, (size_t)B * g.ngroups * 320);
+    AL(Ustrip, (size_t)B * g.ngroups * kStripMax);
     AL(s64, BN);
     AL(s64b, BN);
     AL(status, (size_t)B);

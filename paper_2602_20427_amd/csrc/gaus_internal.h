@@ -27,6 +27,7 @@ constexpr int kTN = kDeg + kShiftTerms + 2;   // scaled derivatives T_0 .. T_{kT
 constexpr int kSmax = 8;                      // largest producer delay on that path
 constexpr float kRhoMax = 0.25f;
 constexpr int kMaxChunks = 64;                // one chunk per lane of a wave
+constexpr int kStripMax = 320;                 // step-by-step strip positions per op, at most
 
 struct PolyArgs {
     int enabled;          // 0: every op takes the per-step path
@@ -78,6 +79,7 @@ struct Work {
     float *gsum_ops;  // [B][ngroups][ntiles][2]  V_dep, L_com of a k_ops work-group
     float *gsum_poly; // [B][ngroups][2]   V_dep, L_com of a k_poly work-group
     float *vres_part; // [B][K]            V_res of one resource type
+    float *Ucoef_k;   // [B][K][64*kNC + 320]  polynomial usage coefficients and strip values per type
     float *ppoly;     // [B][N][kPP]       producer partials of the polynomial path
     float *cpoly;     // [B][E][kCP]       consumer partials of polynomial edges
     float *Ucoef;     // [B][ngroups][kMaxChunks][kNC]  usage coefficients per chunk

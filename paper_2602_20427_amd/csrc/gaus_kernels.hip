@@ -513,7 +513,6 @@ __device__ __forceinline__ float vdot_F(const float (&a)[kNC], const Expansion &
 }  // namespace
 
 constexpr int kPolyWaves = 4;
-constexpr int kStripMax = 320;                  // >= kSmax + largest W + 2
 constexpr int kStripPasses = (kStripMax + 63) / 64;
 constexpr int kOpsPerWaveMax = 64;              // group size <= kPolyWaves * 64
 
@@ -790,71 +789,103 @@ __global__ __launch_bounds__(BS) void k_back(Graph G, const float *__restrict__ 
 // ---------------------------------------------------------------------------
 // Usage: U[b][k][slot] = sum over type-k groups and steps t = slot (mod T).
 // ---------------------------------------------------------------------------
-// Usage per (type, restart): U(t) = step-by-step group partials (active groups
-// only) + the polynomial ops' mass coefficients summed over the type's groups
-// and evaluated at t (chunk part) or their strip values; then the fold mod T.
+// Polynomial usage per (type, restart): the groups' chunk coefficients and
+// strip values summed over the type's groups (64 entries x 4 group slices per
+// work-group, combined in a fixed order).
+constexpr int kUcEntries = kMaxChunks * kNC + kStripMax;   // per (restart, type)
+
+__global__ __launch_bounds__(256) void k_ucoef(Graph G, PolyArgs pa, Work W) {
+    __shared__ float part[4][64];
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    const int x = blockIdx.x * 64 + tx, k = blockIdx.y, b = blockIdx.z;
+    const int g0 = G.type_grp[k], g1 = G.type_grp[k + 1];
+    const int ncoef = pa.nc * kNC;
+    float acc = 0.0f;
+    if (x < ncoef) {
+        for (int g = g0 + ty; g < g1; g += 4)
+            acc += W.Ucoef[((size_t)b * G.ngroups + g) * kMaxChunks * kNC + x];
+    } else if (x < ncoef + pa.SP) {
+        for (int g = g0 + ty; g < g1; g += 4)
+            acc += W.Ustrip[((size_t)b * G.ngroups + g) * kStripMax + (x - ncoef)];
+    }
+    part[ty][tx] = acc;
+    __syncthreads();
+    if (ty == 0 && x < ncoef + pa.SP)
+        W.Ucoef_k[((size_t)b * G.K + k) * kUcEntries + x] = (part[0][tx] + part[1][tx]) + (part[2][tx] + part[3][tx]);
+}
+
+// Usage U(slot) per (slot block, type, restart): step-by-step partials of the
+// type's active groups plus the polynomial part (chunk polynomial at t, or
+// the strip value), summed over t = slot mod T.
 constexpr int kUsageBS = 256;
 
 __global__ __launch_bounds__(kUsageBS) void k_usage(Graph G, PolyArgs pa, Work W) {
-    __shared__ float sC[kMaxChunks * kNC];
-    __shared__ float sS[kStripMax];
     constexpr int kMaxAct = 1024;
+    __shared__ float sC[kUcEntries];
     __shared__ int sAct[kMaxAct];
-    __shared__ int sNact;
-    const int k = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+    __shared__ int wcount[kUsageBS / 64];
+    __shared__ int base;
+    const int k = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
+    const int lane = tid & 63, wid = tid >> 6;
     const int g0 = G.type_grp[k], g1 = G.type_grp[k + 1];
     const int D = G.D, T = G.T;
-    // the type's groups with step-by-step partials (-1: too many to list)
-    if (tid == 0) {
-        int n = 0;
-        for (int g = g0; g < g1 && n >= 0; ++g)
-            if (W.gflag[(size_t)b * G.ngroups + g]) {
-                if (n < kMaxAct) sAct[n++] = g;
-                else n = -1;
-            }
-        sNact = n;
+
+    // the type's groups with step-by-step partials, compacted in order
+    if (tid == 0) base = 0;
+    __syncthreads();
+    for (int c0 = g0; c0 < g1; c0 += kUsageBS) {
+        const int g = c0 + tid;
+        const bool f = g < g1 && W.gflag[(size_t)b * G.ngroups + g] != 0;
+        const unsigned long long bal = __ballot(f);
+        const int before = __popcll(bal & ((1ull << lane) - 1ull));
+        if (lane == 0) wcount[wid] = __popcll(bal);
+        __syncthreads();
+        int off = base;
+        for (int w = 0; w < wid; ++w) off += wcount[w];
+        if (f && off + before < kMaxAct) sAct[off + before] = g;
+        __syncthreads();
+        if (tid == 0) {
+            int tot = 0;
+            for (int w = 0; w < kUsageBS / 64; ++w) tot += wcount[w];
+            base += tot;
+        }
+        __syncthreads();
     }
+    const int nact = base;   // > kMaxAct: scan the flags instead of the list
     if (pa.enabled) {
-        for (int x = tid; x < pa.nc * kNC; x += kUsageBS) {
-            float acc = 0.0f;
-            for (int g = g0; g < g1; ++g) acc += W.Ucoef[((size_t)b * G.ngroups + g) * kMaxChunks * kNC + x];
-            sC[x] = acc;
-        }
-        for (int p = tid; p < pa.SP; p += kUsageBS) {
-            float acc = 0.0f;
-            for (int g = g0; g < g1; ++g) acc += W.Ustrip[((size_t)b * G.ngroups + g) * kStripMax + p];
-            sS[p] = acc;
-        }
+        const float *src = W.Ucoef_k + ((size_t)b * G.K + k) * kUcEntries;
+        const int n = pa.nc * kNC + pa.SP;
+        for (int x = tid; x < n; x += kUsageBS) sC[x] = src[x];
     }
     __syncthreads();
-    const int nact = sNact;
-    for (int slot = tid; slot < T; slot += kUsageBS) {
-        float acc = 0.0f;
-        for (int t = slot; t < D; t += T) {
-            float ut = 0.0f;
-            if (nact >= 0) {
-                for (int q = 0; q < nact; ++q) ut += W.Upart[((size_t)b * G.ngroups + sAct[q]) * D + t];
-            } else {
-                for (int g = g0; g < g1; ++g)
-                    if (W.gflag[(size_t)b * G.ngroups + g]) ut += W.Upart[((size_t)b * G.ngroups + g) * D + t];
-            }
-            if (pa.enabled) {
-                if (t >= pa.L0 && t < D - 2) {
-                    const int c = (t - pa.L0) / pa.W;
-                    const float x = ((float)(t - pa.L0 - c * pa.W) - pa.lam) / pa.lam;
-                    const float *cf = sC + c * kNC;
-                    float v = cf[kNC - 1];
-#pragma unroll
-                    for (int q = kNC - 2; q >= 0; --q) v = fmaf(v, x, cf[q]);
-                    ut += v;
-                } else {
-                    ut += sS[t < pa.L0 ? t : pa.L0 + (t - (D - 2))];
-                }
-            }
-            acc += ut;
+    const int slot = blockIdx.x * kUsageBS + tid;
+    if (slot >= T) return;
+    const int ncoef = pa.nc * kNC;
+    float acc = 0.0f;
+    for (int t = slot; t < D; t += T) {
+        float ut = 0.0f;
+        if (nact <= kMaxAct) {
+            for (int q = 0; q < nact; ++q) ut += W.Upart[((size_t)b * G.ngroups + sAct[q]) * D + t];
+        } else {
+            for (int g = g0; g < g1; ++g)
+                if (W.gflag[(size_t)b * G.ngroups + g]) ut += W.Upart[((size_t)b * G.ngroups + g) * D + t];
         }
-        W.U[((size_t)b * G.K + k) * T + slot] = acc;
+        if (pa.enabled) {
+            if (t >= pa.L0 && t < D - 2) {
+                const int c = (t - pa.L0) / pa.W;
+                const float x = ((float)(t - pa.L0 - c * pa.W) - pa.lam) / pa.lam;
+                const float *cf = sC + c * kNC;
+                float v = cf[kNC - 1];
+#pragma unroll
+                for (int q = kNC - 2; q >= 0; --q) v = fmaf(v, x, cf[q]);
+                ut += v;
+            } else {
+                ut += sC[ncoef + (t < pa.L0 ? t : pa.L0 + (t - (D - 2)))];
+            }
+        }
+        acc += ut;
     }
+    W.U[((size_t)b * G.K + k) * T + slot] = acc;
 }
 
 // ---------------------------------------------------------------------------
@@ -1258,7 +1289,9 @@ hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const 
         else if (lc.spt == 1) launch_back<256, 1>(g, w, a.mu, a.sigma, st);
         else launch_back<256, 4>(g, w, a.mu, a.sigma, st);
     }
-    hipLaunchKernelGGL(k_usage, dim3(g.K, g.B), dim3(kUsageBS), 0, st, g, pa, w);
+    if (pa.enabled)
+        hipLaunchKernelGGL(k_ucoef, dim3((pa.nc * kNC + pa.SP + 63) / 64, g.K, g.B), dim3(256), 0, st, g, pa, w);
+    hipLaunchKernelGGL(k_usage, dim3((g.T + kUsageBS - 1) / kUsageBS, g.K, g.B), dim3(kUsageBS), 0, st, g, pa, w);
     hipLaunchKernelGGL(k_vres, dim3(g.K, g.B), dim3(kTermsBS), 0, st, g, w);
     hipLaunchKernelGGL(k_combine, dim3(g.B), dim3(kCombineBS), 0, st, g, w, hp, a.lambda_in,
                        a.mode == 1 ? a.lambda_out : nullptr, a.mode == 1 ? a.adam_t : nullptr,
