@@ -43,6 +43,8 @@ struct gaus_ctx {
     size_t ev_used = 0;                 // iterations recorded since the last read
 };
 
+constexpr int kPolySplitMax = 4;   // polynomial work-groups per op group, at most
+
 namespace {
 
 gaus_status fail(gaus_ctx *c, gaus_status s, const char *fmt, ...) {
@@ -111,18 +113,11 @@ void setup_poly(int D, int requested, PolyArgs &pa) {
     const double lam = (W - 1) / 2.0;
     pa.lam = (float)lam;
     pa.sig_thr = (float)(lam / kRhoMax);
-    for (int k = 0; k <= 2 * kDeg; ++k) {
+    for (int k = 0; k <= kDeg; ++k) {
         double acc = 0.0;
-        for (int i = 0; i < W; ++i) acc += std::pow((i - lam) / lam, k);
-        pa.H[k] = (k & 1) ? 0.0f : (float)acc;   // symmetric points: odd moments vanish
+        for (int i = 0; i < W; ++i) acc += std::pow(i - lam, 2 * k);
+        pa.H[k] = (float)acc;   // symmetric points: odd moments vanish
     }
-    auto binom = [](int n, int r) { double v = 1.0; for (int q = 1; q <= r; ++q) v = v * (n - r + q) / q; return v; };
-    for (int k = 0; k < kNC; ++k)
-        for (int j = 0; j <= kShiftTerms; ++j) {
-            const double pw = std::pow(-1.0 / lam, j);
-            pa.cP[k][j] = j == 0 ? 0.0f : (float)(-binom(k + j, j) * pw);
-            pa.cA[k][j] = (float)(-(k + 1) * binom(k + 1 + j, j) * pw / lam);
-        }
 }
 
 template <class T>
@@ -383,6 +378,13 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     g.N = h.N; g.E = h.E; g.K = h.K; g.D = h.D; g.II = h.II; g.T = h.II > 0 ? h.II : h.D;
     g.nb = h.nb; g.B = B; g.tile = tile; g.ntiles = ntiles;
     g.ngroups = (int)h.grp_start.size() - 1;
+    if (c->pa.enabled) {
+        // polynomial work-groups per op group: at most 16 ops per wave, so that
+        // every SIMD receives many short waves and the last ones end together
+        int gmax = 1;
+        for (int q = 0; q < g.ngroups; ++q) gmax = std::max(gmax, h.grp_start[q + 1] - h.grp_start[q]);
+        c->pa.split = std::max(1, std::min(kPolySplitMax, (gmax + 63) / 64));
+    }
     g.nlevels = (int)h.lvl_ptr.size() - 1;
     std::vector<float> cap(h.cap);
     const size_t BN = (size_t)B * h.N;
@@ -410,13 +412,13 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     AL(dflag, BN);
     AL(gflag, (size_t)B * g.ngroups);
     AL(gsum_ops, (size_t)B * g.ngroups * ntiles * 2);
-    AL(gsum_poly, (size_t)B * g.ngroups * 2);
+    AL(gsum_poly, (size_t)B * g.ngroups * c->pa.split * 2);
     AL(vres_part, (size_t)B * h.K);
     AL(Ucoef_k, (size_t)B * h.K * (kMaxChunks * kNC + kStripMax));
     AL(ppoly, BN * kPP);
     AL(cpoly, (size_t)B * h.E * kCP);
-    AL(Ucoef, (size_t)B * g.ngroups * kMaxChunks * kNC);
-    AL(Ustrip, (size_t)B * g.ngroups * kStripMax);
+    AL(Ucoef, (size_t)B * g.ngroups * c->pa.split * kMaxChunks * kNC);
+    AL(Ustrip, (size_t)B * g.ngroups * c->pa.split * kStripMax);
     AL(s64, BN);
     AL(s64b, BN);
     AL(status, (size_t)B);
@@ -425,7 +427,7 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
         hipError_t e = hipMemset(c->w.U, 0, sizeof(float) * (size_t)B * h.K * g.T);
         if (e == hipSuccess) e = hipMemset(c->w.ppoly, 0, sizeof(float) * BN * kPP);
         if (e == hipSuccess) e = hipMemset(c->w.cls, 0, BN);
-        if (e == hipSuccess) e = hipMemset(c->w.gsum_poly, 0, sizeof(float) * (size_t)B * g.ngroups * 2);
+        if (e == hipSuccess) e = hipMemset(c->w.gsum_poly, 0, sizeof(float) * (size_t)B * g.ngroups * c->pa.split * 2);
         if (e == hipSuccess) e = hipDeviceSynchronize();
         if (e != hipSuccess) { s = fail(nullptr, GAUS_E_DEVICE, "init: %s", hipGetErrorString(e)); goto fail_alloc; }
     }

@@ -18,8 +18,8 @@ constexpr int kBP = 5;   // per (restart, back edge, tile): V_rec, dVrec/dmu_j, 
 constexpr int kHalo = 256;  // largest producer delay handled from the LDS row window
 
 // Chunk-polynomial path (dense regime).  On a chunk of W consecutive steps
-// with radius rho = ((W-1)/2)/sigma <= kRhoMax the CDF row of an op is a
-// degree-kDeg polynomial to ~1e-10; sums over steps become dot products.
+// with rho = ((W-1)/2)/sigma <= kRhoMax the CDF row of an op is a degree-kDeg
+// polynomial in the step offset to ~1e-10; sums over steps become dot products.
 constexpr int kDeg = 8;                       // polynomial degree
 constexpr int kNC = kDeg + 1;                 // coefficients per vector
 constexpr int kShiftTerms = 4;                // terms of the one-step shift series
@@ -33,10 +33,9 @@ struct PolyArgs {
     int enabled;          // 0: every op takes the per-step path
     int W, nc, L0;        // chunk width, chunks, left strip [0, L0); chunks cover [L0, D-2)
     int SP;               // strip positions: [0, L0) and {D-2, D-1}
+    int split;            // work-groups per op group in the polynomial kernel
     float lam, sig_thr;   // chunk half-width (W-1)/2; ops with sigma >= sig_thr are polynomial
-    float H[2 * kDeg + 1];               // sum over a chunk's points of x^k, x in [-1, 1]
-    float cP[kNC][kShiftTerms + 1];      // mass coefficients from the scaled derivatives
-    float cA[kNC][kShiftTerms + 1];      // dF/dmu one step back from the scaled derivatives
+    float H[kDeg + 1];    // even moments: H[k] = sum over a chunk's points y of y^(2k)
 };
 
 // Device copy of the preprocessed problem (all pointers are device memory).
@@ -77,12 +76,12 @@ struct Work {
     unsigned char *dflag;  // [B][N]        1 = op has step-by-step work (own terms or out-edges)
     int *gflag;       // [B][ngroups]      1 = some op of the group has step-by-step work
     float *gsum_ops;  // [B][ngroups][ntiles][2]  V_dep, L_com of a k_ops work-group
-    float *gsum_poly; // [B][ngroups][2]   V_dep, L_com of a k_poly work-group
+    float *gsum_poly; // [B][ngroups*split][2]  V_dep, L_com of a k_poly work-group
     float *vres_part; // [B][K]            V_res of one resource type
     float *Ucoef_k;   // [B][K][64*kNC + 320]  polynomial usage coefficients and strip values per type
     float *ppoly;     // [B][N][kPP]       producer partials of the polynomial path
     float *cpoly;     // [B][E][kCP]       consumer partials of polynomial edges
-    float *Ucoef;     // [B][ngroups][kMaxChunks][kNC]  usage coefficients per chunk
+    float *Ucoef;     // [B][ngroups*split][kMaxChunks][kNC]  usage coefficients per chunk
     float *Ustrip;    // [B][ngroups][SP]  usage at the strip positions
     long long *s64;   // [B][N]            legalization workspace
     long long *s64b;  // [B][N]            legalization snapshot (back edges)

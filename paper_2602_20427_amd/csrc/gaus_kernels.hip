@@ -379,22 +379,23 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
 // ---------------------------------------------------------------------------
 // Chunk-polynomial path (dense regime).
 //
-// Chunks of W steps tile [L0, D-2); a chunk's points are x = (u - t_mid)/lam in
-// [-1, 1], lam = (W-1)/2.  Around the chunk centre an op's CDF is
-// F(u) = Phi(z0 + rho x), rho = lam/sigma, and its Taylor coefficients in x are
-// the scaled derivatives T_n = Phi^(n)(z0) rho^n / n!, which obey
-//   T_1 = phi(z0) rho,
-//   T_{n+1} = -(z0 rho/(n+1)) T_n - ((n-1) rho^2/(n(n+1))) T_{n-1}
+// Chunks of W steps tile [L0, D-2); a chunk's points are y = u - t_mid in
+// [-lam, lam], lam = (W-1)/2.  Around the chunk centre an op's CDF is
+// F(u) = Phi(z0 + r y), r = 1/sigma, and its Taylor coefficients in y are
+// T_n = Phi^(n)(z0) r^n / n!, which obey
+//   T_1 = phi(z0) r,
+//   T_{n+1} = -(z0 r/(n+1)) T_n - ((n-1) r^2/(n(n+1))) T_{n-1}
 // (the Hermite recursion of the derivatives of phi, scaled).  From one set of
-// T's follow, with constant coefficients:
+// T's follow, with constant integer coefficients (one step = 1 in y):
 //   F:         f_k = T_k
-//   dF/dmu:    a_k = -(k+1) T_{k+1} / lam
-//   dF/dsigma: e_k = z0 a_k + rho a_{k-1}         (dF/dsigma = z dF/dmu)
-//   mass F(v) - F(v-1):  m_k = sum_{j>=1} cP[k][j] T_{k+j}   (one step = lam^-1 in x)
-//   dF/dmu at v-1:       a1_k = sum_{j>=0} cA[k][j] T_{k+1+j}
-// With rho <= kRhoMax the truncation error is ~1e-10.  Every sum over the
-// chunk's steps of a product p(u) q(u) equals sum_k (H p)_k q_k with the chunk
-// moments H_n = sum_x x^n, so an edge costs 10 dot products of length kNC.
+//   dF/dmu:    a_k = -(k+1) T_{k+1}
+//   dF/dsigma: e_k = z0 a_k + r a_{k-1}           (dF/dsigma = z dF/dmu)
+//   mass F(v) - F(v-1):  m_k = -sum_{j>=1} C(k+j,j) (-1)^j T_{k+j}
+//   dF/dmu at v-1:       a1_k = -sum_{j>=0} (k+j+1) C(k+j,j) (-1)^j T_{k+1+j}
+// The series converge like powers of rho = lam r; with rho <= kRhoMax the
+// truncation error is ~1e-10.  Every sum over the chunk's steps of a product
+// p(u) q(u) equals sum_k (H p)_k q_k with the chunk moments H_n = sum_y y^n,
+// so an edge costs 10 dot products of length kNC.
 // The strip [0, L0) u {D-2, D-1} (boundary conventions of the open end bins,
 // zero derivatives outside the interior edges) is evaluated step by step.
 // ---------------------------------------------------------------------------
@@ -423,55 +424,69 @@ __global__ void k_flags(Graph G, Work W) {
 namespace {
 
 struct Expansion {
-    float T[kTN];   // scaled derivatives, T[0] = F(z0)
+    float T[kTN];   // Taylor coefficients in y, T[0] = F(z0)
     float G0;       // 1 - F(z0), from the tail
-    float z0, rho;
+    float z0, r;
 };
 
-constexpr float rcpi(int n) { return 1.0f / (float)n; }
+constexpr double binom_d(int n, int k) {
+    double v = 1.0;
+    for (int q = 1; q <= k; ++q) v = v * (double)(n - k + q) / (double)q;
+    return v;
+}
+// coefficient of T_{k+j} in the mass coefficient m_k (j >= 1)
+constexpr float mass_coef(int k, int j) { return (float)(-binom_d(k + j, j) * ((j & 1) ? -1.0 : 1.0)); }
+// coefficient of T_{k+1+j} in dF/dmu one step back, a1_k (j >= 0)
+constexpr float back_coef(int k, int j) {
+    return (float)(-(double)(k + j + 1) * binom_d(k + j, j) * ((j & 1) ? -1.0 : 1.0));
+}
 
-__device__ __forceinline__ void expand(float mu, float rs, float tcen, float lam, Expansion &e) {
-    e.rho = lam * rs;
+__device__ __forceinline__ void expand(float mu, float rs, float tcen, Expansion &e) {
+    e.r = rs;
     e.z0 = (tcen + 0.5f - mu) * rs;
     float tail, g;
     normal_tail_pdf(e.z0, tail, g);
     const bool up = e.z0 >= 0.0f;
     e.T[0] = up ? 1.0f - tail : tail;
     e.G0 = up ? tail : 1.0f - tail;
-    e.T[1] = g * kInvSqrt2Pi * e.rho;
-    const float zr = e.z0 * e.rho, r2 = e.rho * e.rho;
+    e.T[1] = g * (kInvSqrt2Pi * rs);
+    const float zr = e.z0 * rs, r2 = rs * rs;
+    e.T[2] = (zr * -0.5f) * e.T[1];
 #pragma unroll
-    for (int n = 1; n < kTN - 1; ++n)
-        e.T[n + 1] = -(zr * rcpi(n + 1)) * e.T[n] - ((float)(n - 1) * r2 * rcpi(n * (n + 1))) * e.T[n - 1];
+    for (int n = 2; n < kTN - 1; ++n) {
+        const float c1 = -1.0f / (float)(n + 1);
+        const float c2 = -(float)(n - 1) / (float)(n * (n + 1));
+        e.T[n + 1] = fmaf(zr * c1, e.T[n], (r2 * c2) * e.T[n - 1]);
+    }
 }
 
-__device__ __forceinline__ void vec_dFdmu(const Expansion &e, float inv_lam, float (&a)[kNC]) {
+__device__ __forceinline__ void vec_dFdmu(const Expansion &e, float (&a)[kNC]) {
 #pragma unroll
-    for (int k = 0; k < kNC; ++k) a[k] = -(float)(k + 1) * inv_lam * e.T[k + 1];
+    for (int k = 0; k < kNC; ++k) a[k] = -(float)(k + 1) * e.T[k + 1];
 }
 
-__device__ __forceinline__ void vec_times_z(const float (&a)[kNC], float zc, float rho, float (&o)[kNC]) {
+__device__ __forceinline__ void vec_times_z(const float (&a)[kNC], float zc, float r, float (&o)[kNC]) {
     o[0] = zc * a[0];
 #pragma unroll
-    for (int k = 1; k < kNC; ++k) o[k] = fmaf(zc, a[k], rho * a[k - 1]);
+    for (int k = 1; k < kNC; ++k) o[k] = fmaf(zc, a[k], r * a[k - 1]);
 }
 
-__device__ __forceinline__ void vec_mass(const Expansion &e, const PolyArgs &pa, float (&m)[kNC]) {
+__device__ __forceinline__ void vec_mass(const Expansion &e, float (&m)[kNC]) {
 #pragma unroll
     for (int k = 0; k < kNC; ++k) {
         float acc = 0.0f;
 #pragma unroll
-        for (int j = kShiftTerms; j >= 1; --j) acc = fmaf(pa.cP[k][j], e.T[k + j], acc);
+        for (int j = kShiftTerms; j >= 1; --j) acc = fmaf(mass_coef(k, j), e.T[k + j], acc);
         m[k] = acc;
     }
 }
 
-__device__ __forceinline__ void vec_dFdmu_back(const Expansion &e, const PolyArgs &pa, float (&a)[kNC]) {
+__device__ __forceinline__ void vec_dFdmu_back(const Expansion &e, float (&a)[kNC]) {
 #pragma unroll
     for (int k = 0; k < kNC; ++k) {
         float acc = 0.0f;
 #pragma unroll
-        for (int j = kShiftTerms; j >= 0; --j) acc = fmaf(pa.cA[k][j], e.T[k + 1 + j], acc);
+        for (int j = kShiftTerms; j >= 0; --j) acc = fmaf(back_coef(k, j), e.T[k + 1 + j], acc);
         a[k] = acc;
     }
 }
@@ -483,7 +498,7 @@ __device__ __forceinline__ void vec_moments(const float (&p)[kNC], const PolyArg
         float acc = 0.0f;
 #pragma unroll
         for (int l = 0; l < kNC; ++l)
-            if (((k + l) & 1) == 0) acc = fmaf(pa.H[k + l], p[l], acc);
+            if (((k + l) & 1) == 0) acc = fmaf(pa.H[(k + l) / 2], p[l], acc);
         o[k] = acc;
     }
 }
@@ -526,16 +541,16 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
     extern __shared__ float sDyn[];
     __shared__ float sUc[kPolyWaves][kMaxChunks][kNC];
     __shared__ float sGs[kPolyWaves][2];
-    const int SP = pa.SP;
-    const int grp = blockIdx.x, b = blockIdx.y;
+    const int SP = pa.SP, split = pa.split;
+    const int grp = blockIdx.x / split, sub = blockIdx.x - grp * split, b = blockIdx.y;
+    const size_t slot_id = ((size_t)b * G.ngroups + grp) * split + sub;   // per-work-group outputs
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     const int N = G.N, D = G.D;
     const float *mub = mu + (size_t)b * N;
     const float *sgb = sigma + (size_t)b * N;
     const unsigned char *clsb = W.cls + (size_t)b * N;
-    const float lam = pa.lam, inv_lam = 1.0f / pa.lam;
     const bool cact = lane < pa.nc;
-    const float tcen = (float)(pa.L0 + lane * pa.W) + lam;
+    const float tcen = (float)(pa.L0 + lane * pa.W) + pa.lam;
 
     float uc[kNC];
 #pragma unroll
@@ -546,13 +561,15 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
     float *own = sDyn + (size_t)wv * 7 * SP;
     float *sUs = sDyn + (size_t)kPolyWaves * 7 * SP;
 
-    // this wave's ops q = q0 + wv + kPolyWaves*l, parameters loaded by lane l
+    // the work-group's ops are q = q0 + sub + split*j; this wave's are
+    // j = wv + kPolyWaves*l, parameters loaded by lane l
     const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
-    const int nq = (q1 - q0 - wv + kPolyWaves - 1) / kPolyWaves;
+    const int nj = (q1 - q0 - sub + split - 1) / split;
+    const int nq = (nj - wv + kPolyWaves - 1) / kPolyWaves;
     int l_i = 0, l_cls = 0, l_s = 0, l_e0 = 0, l_e1 = 0;
     float l_mu = 0.0f, l_sg = 1.0f;
     if (lane < nq) {
-        l_i = G.perm[q0 + wv + kPolyWaves * lane];
+        l_i = G.perm[q0 + sub + split * (wv + kPolyWaves * lane)];
         l_cls = clsb[l_i];
         l_mu = mub[l_i]; l_sg = sgb[l_i];
         l_s = G.delay[l_i];
@@ -601,27 +618,27 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
         float HF[kNC], HFm[kNC], HFs[kNC], HA[kNC], HFm1[kNC], HFs1[kNC];
         if (cact) {
             Expansion ea;
-            expand(m_i, rs, tcen, lam, ea);
+            expand(m_i, rs, tcen, ea);
             float v[kNC], w[kNC];
-            vec_mass(ea, pa, v);
+            vec_mass(ea, v);
 #pragma unroll
             for (int k = 0; k < kNC; ++k) uc[k] += v[k];
 #pragma unroll
             for (int k = 0; k < kNC; ++k) w[k] = ea.T[k];
             vec_moments(w, pa, HF);
-            vec_dFdmu(ea, inv_lam, v);
+            vec_dFdmu(ea, v);
             vec_moments(v, pa, HFm);
-            vec_times_z(v, ea.z0, ea.rho, w);
+            vec_times_z(v, ea.z0, ea.r, w);
             vec_moments(w, pa, HFs);
             // shifted functions: A(u) = mass at u-s+1, dF(u-s)
             Expansion es;
-            if (s != 1) expand(m_i, rs, tcen - (float)(s - 1), lam, es);
+            if (s != 1) expand(m_i, rs, tcen - (float)(s - 1), es);
             const Expansion &ex = (s != 1) ? es : ea;
-            vec_mass(ex, pa, v);
+            vec_mass(ex, v);
             vec_moments(v, pa, HA);
-            vec_dFdmu_back(ex, pa, v);
+            vec_dFdmu_back(ex, v);
             vec_moments(v, pa, HFm1);
-            vec_times_z(v, ex.z0 - rs, ex.rho, w);
+            vec_times_z(v, ex.z0 - rs, ex.r, w);
             vec_moments(w, pa, HFs1);
         } else {
 #pragma unroll
@@ -673,19 +690,19 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
             }
             if (cact) {
                 Expansion ej;
-                expand(m_j, rsj, tcen, lam, ej);
+                expand(m_j, rsj, tcen, ej);
                 float a[kNC], v[kNC];
                 pr[0] += vdot_F(HA, ej);
                 pr[1] += vdot_1mF(HF, ej);
                 pr[4] += vdot_1mF(HFm, ej);
                 pr[5] += vdot_1mF(HFs, ej);
-                vec_dFdmu(ej, inv_lam, a);
+                vec_dFdmu(ej, a);
                 cc[0] += vdot(HA, a);
                 cc[2] -= vdot(HF, a);
-                vec_times_z(a, ej.z0, ej.rho, v);
+                vec_times_z(a, ej.z0, ej.r, v);
                 cc[1] += vdot(HA, v);
                 cc[3] -= vdot(HF, v);
-                vec_mass(ej, pa, v);
+                vec_mass(ej, v);
                 pr[2] -= vdot(HFm1, v);
                 pr[3] -= vdot(HFs1, v);
             }
@@ -710,7 +727,7 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
         if (p < SP) sUs[wv * SP + p] = us[ps];
     }
     __syncthreads();
-    float *ucg = W.Ucoef + ((size_t)b * G.ngroups + grp) * kMaxChunks * kNC;
+    float *ucg = W.Ucoef + slot_id * kMaxChunks * kNC;
     for (int x = threadIdx.x; x < kMaxChunks * kNC; x += 64 * kPolyWaves) {
         const int c = x / kNC, k = x % kNC;
         float acc = 0.0f;
@@ -722,9 +739,9 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
         float acc = 0.0f;
 #pragma unroll
         for (int w = 0; w < kPolyWaves; ++w) acc += sGs[w][threadIdx.x];
-        W.gsum_poly[((size_t)b * G.ngroups + grp) * 2 + threadIdx.x] = acc;
+        W.gsum_poly[slot_id * 2 + threadIdx.x] = acc;
     }
-    float *usg = W.Ustrip + ((size_t)b * G.ngroups + grp) * kStripMax;
+    float *usg = W.Ustrip + slot_id * kStripMax;
     for (int p = threadIdx.x; p < kStripMax; p += 64 * kPolyWaves) {
         float acc = 0.0f;
         if (p < SP) {
@@ -798,15 +815,15 @@ __global__ __launch_bounds__(256) void k_ucoef(Graph G, PolyArgs pa, Work W) {
     __shared__ float part[4][64];
     const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
     const int x = blockIdx.x * 64 + tx, k = blockIdx.y, b = blockIdx.z;
-    const int g0 = G.type_grp[k], g1 = G.type_grp[k + 1];
+    // the type's polynomial work-groups: slots [g0*split, g1*split) of restart b
+    const int g0 = G.type_grp[k] * pa.split, g1 = G.type_grp[k + 1] * pa.split;
+    const size_t rb = (size_t)b * G.ngroups * pa.split;
     const int ncoef = pa.nc * kNC;
     float acc = 0.0f;
     if (x < ncoef) {
-        for (int g = g0 + ty; g < g1; g += 4)
-            acc += W.Ucoef[((size_t)b * G.ngroups + g) * kMaxChunks * kNC + x];
+        for (int g = g0 + ty; g < g1; g += 4) acc += W.Ucoef[(rb + g) * kMaxChunks * kNC + x];
     } else if (x < ncoef + pa.SP) {
-        for (int g = g0 + ty; g < g1; g += 4)
-            acc += W.Ustrip[((size_t)b * G.ngroups + g) * kStripMax + (x - ncoef)];
+        for (int g = g0 + ty; g < g1; g += 4) acc += W.Ustrip[(rb + g) * kStripMax + (x - ncoef)];
     }
     part[ty][tx] = acc;
     __syncthreads();
@@ -873,7 +890,7 @@ __global__ __launch_bounds__(kUsageBS) void k_usage(Graph G, PolyArgs pa, Work W
         if (pa.enabled) {
             if (t >= pa.L0 && t < D - 2) {
                 const int c = (t - pa.L0) / pa.W;
-                const float x = ((float)(t - pa.L0 - c * pa.W) - pa.lam) / pa.lam;
+                const float x = (float)(t - pa.L0 - c * pa.W) - pa.lam;
                 const float *cf = sC + c * kNC;
                 float v = cf[kNC - 1];
 #pragma unroll
@@ -970,7 +987,7 @@ __device__ float block_sum256(float x, float *scratch /*[4]*/) {
     return r;
 }
 
-__global__ __launch_bounds__(kCombineBS) void k_combine(Graph G, Work W, HP hp,
+__global__ __launch_bounds__(kCombineBS) void k_combine(Graph G, PolyArgs pa, Work W, HP hp,
                                                         const float *__restrict__ lambda_in,
                                                         float *lambda_out, const int *adam_t,
                                                         float *terms_out) {
@@ -978,9 +995,12 @@ __global__ __launch_bounds__(kCombineBS) void k_combine(Graph G, Work W, HP hp,
     const int b = blockIdx.x, tid = threadIdx.x;
     float vres = 0.0f, vdep = 0.0f, lcom = 0.0f, vrec = 0.0f;
     for (int k = tid; k < G.K; k += kCombineBS) vres += W.vres_part[(size_t)b * G.K + k];
-    for (int g = tid; g < G.ngroups; g += kCombineBS) {
-        const float *gp = W.gsum_poly + ((size_t)b * G.ngroups + g) * 2;
+    const int npoly = G.ngroups * pa.split;
+    for (int g = tid; g < npoly; g += kCombineBS) {
+        const float *gp = W.gsum_poly + ((size_t)b * npoly + g) * 2;
         vdep += gp[0]; lcom += gp[1];
+    }
+    for (int g = tid; g < G.ngroups; g += kCombineBS) {
         if (W.gflag[(size_t)b * G.ngroups + g]) {
             const float *go = W.gsum_ops + ((size_t)b * G.ngroups + g) * G.ntiles * 2;
             for (int tl = 0; tl < G.ntiles; ++tl) { vdep += go[2 * tl]; lcom += go[2 * tl + 1]; }
@@ -1281,7 +1301,8 @@ hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const 
     if (pa.enabled) {
         if (a.poly_begin) (void)hipEventRecord(a.poly_begin, st);
         const size_t lds = sizeof(float) * (size_t)kPolyWaves * 8 * pa.SP;
-        hipLaunchKernelGGL(k_poly, dim3(g.ngroups, g.B), dim3(64 * kPolyWaves), lds, st, g, pa, a.mu, a.sigma, w);
+        hipLaunchKernelGGL(k_poly, dim3(g.ngroups * pa.split, g.B), dim3(64 * kPolyWaves), lds, st, g, pa, a.mu,
+                           a.sigma, w);
         if (a.poly_end) (void)hipEventRecord(a.poly_end, st);
     }
     if (g.nb > 0) {
@@ -1293,7 +1314,7 @@ hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const 
         hipLaunchKernelGGL(k_ucoef, dim3((pa.nc * kNC + pa.SP + 63) / 64, g.K, g.B), dim3(256), 0, st, g, pa, w);
     hipLaunchKernelGGL(k_usage, dim3((g.T + kUsageBS - 1) / kUsageBS, g.K, g.B), dim3(kUsageBS), 0, st, g, pa, w);
     hipLaunchKernelGGL(k_vres, dim3(g.K, g.B), dim3(kTermsBS), 0, st, g, w);
-    hipLaunchKernelGGL(k_combine, dim3(g.B), dim3(kCombineBS), 0, st, g, w, hp, a.lambda_in,
+    hipLaunchKernelGGL(k_combine, dim3(g.B), dim3(kCombineBS), 0, st, g, pa, w, hp, a.lambda_in,
                        a.mode == 1 ? a.lambda_out : nullptr, a.mode == 1 ? a.adam_t : nullptr,
                        a.terms_out);
     {
