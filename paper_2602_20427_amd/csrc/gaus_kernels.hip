@@ -528,13 +528,15 @@ __device__ __forceinline__ float vdot_F(const float (&a)[kNC], const Expansion &
 }  // namespace
 
 constexpr int kPolyWaves = 4;
-constexpr int kStripPasses = (kStripMax + 63) / 64;
+constexpr int kStripPassesMax = (kStripMax + 63) / 64;
 constexpr int kOpsPerWaveMax = 64;              // group size <= kPolyWaves * 64
 
 // Work-group = (op group, restart), kPolyWaves waves; each wave takes the
 // group's ops in turn.  For a polynomial op: lanes = strip positions for the
 // step-by-step part, lanes = chunks for the polynomial part; per polynomial
 // out-edge the consumer-side derivatives of both parts are reduced together.
+// NP: strip passes of 64 lanes, ceil(SP / 64).
+template <int NP>
 __global__ __launch_bounds__(64 * kPolyWaves) __attribute__((amdgpu_waves_per_eu(3)))
 void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__restrict__ sigma, Work W) {
     // dynamic LDS: per wave 7 rows of SP strip values, then per wave SP strip usages
@@ -555,9 +557,9 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
     float uc[kNC];
 #pragma unroll
     for (int k = 0; k < kNC; ++k) uc[k] = 0.0f;
-    float us[kStripPasses];
+    float us[NP];
 #pragma unroll
-    for (int ps = 0; ps < kStripPasses; ++ps) us[ps] = 0.0f;
+    for (int ps = 0; ps < NP; ++ps) us[ps] = 0.0f;
     float *own = sDyn + (size_t)wv * 7 * SP;
     float *sUs = sDyn + (size_t)kPolyWaves * 7 * SP;
 
@@ -595,7 +597,7 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
 
         // (1) strip: own CDF values per position, kept in this wave's LDS rows
 #pragma unroll
-        for (int ps = 0; ps < kStripPasses; ++ps) {
+        for (int ps = 0; ps < NP; ++ps) {
             const int p = ps * 64 + lane;
             if (p < SP) {
                 const int u = p < pa.L0 ? p : D - 2 + (p - pa.L0);
@@ -662,7 +664,7 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
             const float rsj = 1.0f / s_j, cj = rsj * kInvSqrt2Pi;
             float cc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-            for (int ps = 0; ps < kStripPasses; ++ps) {
+            for (int ps = 0; ps < NP; ++ps) {
                 const int p = ps * 64 + lane;
                 if (p < SP) {
                     const int u = p < pa.L0 ? p : D - 2 + (p - pa.L0);
@@ -722,7 +724,7 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
 #pragma unroll
     for (int k = 0; k < kNC; ++k) sUc[wv][lane][k] = uc[k];
 #pragma unroll
-    for (int ps = 0; ps < kStripPasses; ++ps) {
+    for (int ps = 0; ps < NP; ++ps) {
         const int p = ps * 64 + lane;
         if (p < SP) sUs[wv * SP + p] = us[ps];
     }
@@ -1301,8 +1303,15 @@ hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const 
     if (pa.enabled) {
         if (a.poly_begin) (void)hipEventRecord(a.poly_begin, st);
         const size_t lds = sizeof(float) * (size_t)kPolyWaves * 8 * pa.SP;
-        hipLaunchKernelGGL(k_poly, dim3(g.ngroups * pa.split, g.B), dim3(64 * kPolyWaves), lds, st, g, pa, a.mu,
-                           a.sigma, w);
+        const dim3 grid(g.ngroups * pa.split, g.B), block(64 * kPolyWaves);
+        switch ((pa.SP + 63) / 64) {
+        case 1: hipLaunchKernelGGL(k_poly<1>, grid, block, lds, st, g, pa, a.mu, a.sigma, w); break;
+        case 2: hipLaunchKernelGGL(k_poly<2>, grid, block, lds, st, g, pa, a.mu, a.sigma, w); break;
+        case 3: hipLaunchKernelGGL(k_poly<3>, grid, block, lds, st, g, pa, a.mu, a.sigma, w); break;
+        case 4: hipLaunchKernelGGL(k_poly<4>, grid, block, lds, st, g, pa, a.mu, a.sigma, w); break;
+        case kStripPassesMax: hipLaunchKernelGGL(k_poly<kStripPassesMax>, grid, block, lds, st, g, pa, a.mu, a.sigma, w); break;
+        default: return hipErrorInvalidValue;
+        }
         if (a.poly_end) (void)hipEventRecord(a.poly_end, st);
     }
     if (g.nb > 0) {
