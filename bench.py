@@ -38,7 +38,7 @@ METRIC = "op-step evals/sec (fwd+bwd+Adam), ms/iteration, % roofline at 50k ops"
 #     end points' rows available).
 # A transcendental occupies TRANS_WEIGHT FMA issue slots: the measured ratio of
 # the v_fma_f32 to the v_exp_f32 rate on gfx950 (gaus_microbench:
-# 100.4 vs 21.2 per clock per CU).  One slot = one fp32 FMA = 2 flops; the
+# 101.7 vs 21.2 per clock per CU).  One slot = one fp32 FMA = 2 flops; the
 # peak is MI355X's 157.3 TFLOP/s fp32 vector rate.
 #
 # The units of one launch of a kernel are the op-bin-edges and edge-steps it
@@ -51,8 +51,13 @@ METRIC = "op-step evals/sec (fwd+bwd+Adam), ms/iteration, % roofline at 50k ops"
 FMA_PER_OP_STEP = 20.0
 TRANS_PER_OP_STEP = 2.0
 FMA_PER_EDGE_STEP = 10.0
-TRANS_WEIGHT = 100.4 / 21.2
+FMA_LANES_PER_CLK_CU = 101.7
+EXP_LANES_PER_CLK_CU = 21.2
+TRANS_WEIGHT = FMA_LANES_PER_CLK_CU / EXP_LANES_PER_CLK_CU
 PEAK_TFLOPS = 157.3
+# issue-rate reference: the measured v_fma_f32 rate above
+N_CU = 256
+CLOCK_HZ = 2.4e9
 KERNEL_SRC = os.path.join(ROOT, "paper_2602_20427_amd", "csrc", "gaus_kernels.hip")
 KERNEL_NAMES = {"ops": "k_ops", "poly": "k_poly"}
 
@@ -71,10 +76,11 @@ def model_flops(units_op, units_edge):
     return 2.0 * slots
 
 
-def pmc_traffic(kernel, workload):
-    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
-    summary, if it was taken on the current kernel source; else None."""
-    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_pmc.md")
+def pmc_traffic(profile):
+    """HBM bytes per launch from the committed rocprofv3 counter summary
+    profiles/<profile>_pmc.md, if it was taken on the current kernel source;
+    else None."""
+    path = os.path.join(ROOT, "profiles", f"{profile}_pmc.md")
     if not os.path.exists(path):
         return None
     txt = open(path).read()
@@ -83,6 +89,25 @@ def pmc_traffic(kernel, workload):
     if not h or not v or h.group(1) != kernel_source_hash():
         return None
     return float(v.group(1))
+
+
+def pmc_issue(profile, kernel_ms):
+    """VALU issue rate from the committed rocprofv3 SQ-counter summary
+    profiles/<profile>_pmc.md (taken on the current kernel source), against
+    the measured v_fma_f32 issue rate of the chip; else None."""
+    path = os.path.join(ROOT, "profiles", f"{profile}_pmc.md")
+    if not os.path.exists(path):
+        return None
+    txt = open(path).read()
+    h = re.search(r"kernel_source_sha256:\s*([0-9a-f]+)", txt)
+    v = re.search(r"valu_instructions_per_launch:\s*([0-9.eE+]+)", txt)
+    if not h or not v or h.group(1) != kernel_source_hash():
+        return None
+    lane_ops = float(v.group(1)) * 64
+    rate = lane_ops / (kernel_ms * 1e-3)
+    peak = FMA_LANES_PER_CLK_CU * N_CU * CLOCK_HZ
+    return {"valu_lane_ops_per_launch": lane_ops, "achieved_lane_ops_per_s": rate,
+            "peak_lane_ops_per_s": peak, "frac": rate / peak}
 
 
 def describe(cfg, prob):
@@ -121,6 +146,8 @@ def main():
     ap.add_argument("--workload", default="large")
     ap.add_argument("--cpu-restarts", type=int, default=2, help="restarts in the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--poly-chunk", type=int, default=0,
+                    help="chunk width of the polynomial path: 0 = library's choice, -1 = off (every op step by step)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the run, copy this many MiB once (counter calibration)")
     args = ap.parse_args()
@@ -142,6 +169,7 @@ def main():
     B, N, D = cfg.B, prob.n_ops, prob.D
     hp = bd.default_hparams()
     hp.lr = cfg.lr
+    hp.poly_chunk = args.poly_chunk
     dev = torch.device("cuda")
     ctx = bd.Context(prob, B, hp)
     mu = torch.zeros(B, N, device=dev)
@@ -182,6 +210,7 @@ def main():
     ktimes = ctx.kernel_timing_read()
     ctx.kernel_timing(False)
     census = ctx.poly_census()
+    poly_cfg = ctx.poly_config()
     step_ms_events = ev[0].elapsed_time(ev[1]) / args.steps
     legalize_ms = ev[1].elapsed_time(ev[2])
     ms_per_step = (t1 - t0) * 1e3 / args.steps
@@ -211,6 +240,9 @@ def main():
 
     value = B * N * D / (ms_per_step * 1e-3)
     achieved = kern[dom]["achieved_tflops"]
+    # committed counter summary of this kernel and launch configuration
+    profile = f"{dom}_{args.workload}" + ("" if args.poly_chunk == 0 else
+                                          "_direct" if args.poly_chunk < 0 else f"_w{args.poly_chunk}")
     whole = model_flops(B * N * (D - 1), B * (E + prob.n_back) * (D - 1))
     out = {
         "metric": METRIC, "value": value, "unit": "op-step evals/s", "n_gpus": 1,
@@ -220,12 +252,18 @@ def main():
         "config": {"workload": describe(cfg, prob), "B": B, "N": N, "E": E,
                    "n_back": prob.n_back, "D": D, "II": prob.II},
         "ms_per_iteration_events": step_ms_events, "legalize_ms": legalize_ms,
+        "poly_path": dict(poly_cfg, ops=census["ops"], edges=census["edges"]),
         "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_TFLOPS, "traffic": pmc_traffic(dom, args.workload),
+                     "frac": achieved / PEAK_TFLOPS,
+                     "traffic": pmc_traffic(profile),
                      "kernel": dom, "kernel_ms": kern[dom]["ms"],
                      "model": f"{FMA_PER_OP_STEP:g} FMA + {TRANS_PER_OP_STEP:g} transcendental "
                               f"(x{TRANS_WEIGHT:.2f} FMA slots) per op-bin-edge, {FMA_PER_EDGE_STEP:g} FMA per "
-                              f"edge-step, 2 flops per FMA slot; units = those the kernel owns"},
+                              f"edge-step, 2 flops per FMA slot; units = those the kernel owns",
+                     "note": "k_poly reaches its op-bin-edges through per-chunk polynomial expansions and "
+                             "needs fewer operations than this per-step model charges, so frac can exceed 1; "
+                             "'issue' gives its measured VALU issue rate"},
+        "issue": pmc_issue(profile, kern[dom]["ms"]),
         "kernels": kern,
         "iteration_model_tflops_per_s": whole / (step_ms_events * 1e-3) / 1e12,
     }

@@ -72,6 +72,52 @@ def test_loss_grad_paper_init(cfg, poly):
            f"{cfg}/init poly={poly}")
 
 
+def test_loss_grad_large_full_size():
+    """The 50k-op workload at its full size (B=8, D=4096) in the launch
+    configuration bench.py times (library defaults: chunk-polynomial path with
+    the automatic chunk width), from the paper's initialization; restarts 0
+    and 7 against the oracle."""
+    cfg = CONFIGS["large"]
+    p = make_problem(cfg, seed=0)
+    B = cfg.B
+    u = restart_uniforms(p.n_ops, B, seed=0)
+    mu, sg, rc = oracle.init_state(p, B, u)
+    assert rc == 0
+    mu, sg = mu.astype(np.float32), sg.astype(np.float32)
+    hp = bd.default_hparams()
+    hp.lr = cfg.lr
+    _check(p, mu, sg, np.full((B, 3), hp.lambda0, np.float32), hp, [0, B - 1], "large/init bench config")
+
+
+def test_loss_grad_large_after_steps():
+    """The 50k-op workload after 20 fused steps on the GPU (moved means and
+    widths, nonzero multipliers): the state is read back and the loss and
+    gradient of that state are compared with the oracle."""
+    import torch
+    cfg = CONFIGS["large"]
+    p = make_problem(cfg, seed=0)
+    B = cfg.B
+    hp = bd.default_hparams()
+    hp.lr = 0.5                     # large steps: states far from the initialization
+    hp.rho = 1e-2
+    ctx = bd.Context(p, B, hp)
+    dev = torch.device("cuda")
+    mu = torch.zeros(B, p.n_ops, device=dev)
+    sg = torch.zeros(B, p.n_ops, device=dev)
+    ctx.init_state(mu, sg, restart_uniforms(p.n_ops, B, seed=0))
+    lam = torch.full((B, 3), 0.5, device=dev)
+    m = torch.zeros(2, B, p.n_ops, device=dev)
+    v = torch.zeros(2, B, p.n_ops, device=dev)
+    t = torch.zeros(1, dtype=torch.int32, device=dev)
+    ctx.bind_state(mu, sg, m, v, lam, t)
+    ctx.step(20)
+    ctx.sync()
+    say(f"  [large] after 20 steps: poly census {ctx.poly_census()}")
+    mu_h, sg_h, lam_h = mu.cpu().numpy(), sg.cpu().numpy(), lam.cpu().numpy()
+    ctx.close()
+    _check(p, mu_h, sg_h, lam_h, hp, [0, B - 1], "large/after 20 steps")
+
+
 def test_loss_grad_pipelined_random():
     p = make_problem("pipelined", seed=0)
     B = 4
