@@ -52,7 +52,7 @@ def _load():
         lib = C.CDLL(_LIB)
         P = C.POINTER(_Problem)
         vp, i32, i64, dbl = C.c_void_p, C.c_int32, C.c_int64, C.c_double
-        lib.orc_loss_grad.argtypes = [P, vp, vp, vp, dbl, dbl, dbl, vp, vp, vp, vp, vp]
+        lib.orc_loss_grad.argtypes = [P, vp, vp, vp, dbl, dbl, dbl, dbl, dbl, vp, vp, vp, vp, vp]
         lib.orc_loss_grad.restype = C.c_int
         lib.orc_edge_terms_double_sum.argtypes = [P, vp, vp, vp]
         lib.orc_edge_terms_double_sum.restype = None
@@ -112,23 +112,24 @@ def num_threads() -> int:
     return int(_load().orc_num_threads())
 
 
-def loss_grad(prob, mu, sigma, lam, alpha, rho, grad=True, tie_tol=1e-4):
-    """Per restart b: terms [B,5] = (L, V_dep, V_res, V_rec, L_com), U [B,K,T],
-    g_mu, g_sigma [B,N] (fp64), ties [B] (count of near-tie usage cells)."""
+def loss_grad(prob, mu, sigma, lam, alpha, rho, grad=True, tie_tol=1e-4, beta=0.0, tau=1e-2):
+    """Per restart b: terms [B,6] = (L, V_dep, V_res, V_rec, L_com, L_res),
+    U [B,K,T], g_mu, g_sigma [B,N] (fp64), ties [B] (count of near-tie usage
+    cells).  beta weights the smooth peak L_res (temperature tau) in L."""
     lib, op = _load(), _op(prob)
     mu = np.atleast_2d(np.asarray(mu, np.float64))
     sigma = np.atleast_2d(np.asarray(sigma, np.float64))
     lam = np.atleast_2d(np.asarray(lam, np.float64))
     B = mu.shape[0]
-    terms = np.zeros((B, 5)); U = np.zeros((B, op.K, op.T))
+    terms = np.zeros((B, 6)); U = np.zeros((B, op.K, op.T))
     gm = np.zeros((B, op.n)); gs = np.zeros((B, op.n)); ties = np.zeros(B, np.int64)
     for b in range(B):
         m = np.ascontiguousarray(mu[b]); s = np.ascontiguousarray(sigma[b])
         l = np.ascontiguousarray(lam[b if lam.shape[0] > 1 else 0])
-        t = np.zeros(5); u = np.zeros((op.K, op.T)); nt = np.zeros(1, np.int64)
+        t = np.zeros(6); u = np.zeros((op.K, op.T)); nt = np.zeros(1, np.int64)
         g1 = np.zeros(op.n); g2 = np.zeros(op.n)
         rc = lib.orc_loss_grad(C.byref(op.s), _ptr(m), _ptr(s), _ptr(l), float(alpha), float(rho),
-                               float(tie_tol), _ptr(t), _ptr(u),
+                               float(beta), float(tau), float(tie_tol), _ptr(t), _ptr(u),
                                _ptr(g1) if grad else None, _ptr(g2) if grad else None, _ptr(nt))
         if rc != OK:
             raise RuntimeError(f"oracle loss_grad failed: {rc}")

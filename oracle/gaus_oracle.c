@@ -15,6 +15,8 @@
  *   - dependency violation        : Sec. 3.2, eq:dep (with producer delay)
  *   - expected edge length        : App. B.1 (L^_Com)
  *   - recurrence violation        : App. B.3 (V^_Rec, with producer delay)
+ *   - smooth peak usage L_Res     : App. B.2 (LogSumExp over steps, temperature
+ *                                   tau; Sec. 3.2 eq:max), App. B.3 (modulo slots)
  *   - augmented Lagrangian        : Sec. 3.3, eq. (11) and Alg. 1
  *   - Adam                        : App. C.1 hyper-parameters; Kingma & Ba (2015)
  *   - legalization                : App. A, Alg. 3 (regular), Alg. 4 (modulo)
@@ -33,6 +35,10 @@
  *   R14 Alg. 4 first clamps the rounded schedule to [0, D-1]; statuses
  *       NOT_CONVERGED (pass cap N reached) and OVERFLOW (some s > D-1).
  *   R4  rounding is half-up: s = floor(mu) + [mu - floor(mu) >= 1/2].
+ *   R17 with K resource types the smooth peak is taken per type over its
+ *       usage slots and summed over types: L_Res = sum_k tau log sum_t
+ *       exp(U_k(t)/tau) (slots t < II when II > 0: the modulo peak MRes);
+ *       it enters the objective with weight beta (Formulation A: beta = 1).
  *
  * The gradient is the analytic derivative of the forward below (derived by
  * writing every term as a function of the CDF values at the D-1 interior bin
@@ -231,14 +237,15 @@ int orc_asap_alap(const orc_problem *p, int64_t *asap, int64_t *alap) {
 
 /*
  * One restart.  Inputs mu, sigma [n] (float32 values promoted to double),
- * lam[3] = (lambda_dep, lambda_res, lambda_rec).  Outputs:
- *   terms[5] = (L_total, V_dep, V_res, V_rec, L_com)
+ * lam[3] = (lambda_dep, lambda_res, lambda_rec), beta and tau of the smooth
+ * peak term.  Outputs:
+ *   terms[6] = (L_total, V_dep, V_res, V_rec, L_com, L_res)
  *   U[K*T]   expected (folded) usage, T = II if II > 0 else D
  *   g_mu, g_sigma [n]  dL_total/dmu, dL_total/dsigma (may be NULL: forward only)
  *   n_ties   number of (k, slot) cells with |U - C| < tie_tol * max(1, C)
  */
 int orc_loss_grad(const orc_problem *p, const double *mu, const double *sigma,
-                  const double *lam, double alpha, double rho, double tie_tol,
+                  const double *lam, double alpha, double rho, double beta, double tau, double tie_tol,
                   double *terms, double *U, double *g_mu, double *g_sigma, int64_t *n_ties) {
     const int32_t n = p->n, D = p->D, K = p->K, II = p->II;
     const int32_t T = (II > 0) ? II : D;
@@ -282,6 +289,22 @@ int orc_loss_grad(const orc_problem *p, const double *mu, const double *sigma,
         if (ex > 0.0) V_res += ex;                        /* eq:relu */
         if (fabs(ex) < tie_tol * (c > 1.0 ? c : 1.0)) ties++;
     }
+    /* smooth peak per type, tau log sum_t exp(U/tau), shifted by the maximum;
+     * soft[k][t] = its derivative with respect to U_k(t) (a softmax) */
+    double L_res = 0.0;
+    double *soft = calloc((size_t)K * T + 1, sizeof(double));
+    if (!soft) { free(F); free(P); free(vd); free(lc); free(vr); adj_free(&a); return ORC_E_NOMEM; }
+    if (beta != 0.0) {
+        for (int32_t k = 0; k < K; ++k) {
+            const double *Uk = U + (int64_t)k * T;
+            double m = Uk[0];
+            for (int32_t t = 1; t < T; ++t) if (Uk[t] > m) m = Uk[t];
+            double z = 0.0;
+            for (int32_t t = 0; t < T; ++t) z += exp((Uk[t] - m) / tau);
+            L_res += m + tau * log(z);
+            for (int32_t t = 0; t < T; ++t) soft[(int64_t)k * T + t] = exp((Uk[t] - m) / tau) / z;
+        }
+    }
 
     /* dependency violations and edge lengths, summed per producer */
     #pragma omp parallel for schedule(dynamic, 16)
@@ -313,9 +336,10 @@ int orc_loss_grad(const orc_problem *p, const double *mu, const double *sigma,
 
     /* augmented Lagrangian, eq. (11) */
     double V[3] = {V_dep, V_res, V_rec};
-    double L = alpha * L_com;
+    double L = alpha * L_com + beta * L_res;
     for (int c = 0; c < 3; ++c) L += lam[c] * V[c] + 0.5 * rho * V[c] * V[c];
     terms[0] = L; terms[1] = V_dep; terms[2] = V_res; terms[3] = V_rec; terms[4] = L_com;
+    terms[5] = L_res;
     if (n_ties) *n_ties = ties;
 
     if (g_mu && g_sigma) {
@@ -329,6 +353,7 @@ int orc_loss_grad(const orc_problem *p, const double *mu, const double *sigma,
                 /* G(d) = dL/dP_i^d, holding the CDFs of the other ops fixed */
                 for (int32_t d = 0; d < D; ++d) {
                     double g = (U[(int64_t)k * T + (d % T)] > p->cap[k]) ? w_res : 0.0;
+                    g += beta * soft[(int64_t)k * T + (d % T)];
                     for (int32_t e = p->row_ptr[i]; e < p->row_ptr[i + 1]; ++e)
                         g += w_dep * cdf_row(F + (int64_t)p->col[e] * DF, (int64_t)d + p->delay[i] - 1, D);
                     for (int32_t q = a.bin_ptr[i]; q < a.bin_ptr[i + 1]; ++q) {
@@ -365,7 +390,7 @@ int orc_loss_grad(const orc_problem *p, const double *mu, const double *sigma,
             free(G);
         }
     }
-    free(F); free(P); free(vd); free(lc); free(vr); adj_free(&a);
+    free(F); free(P); free(vd); free(lc); free(vr); free(soft); adj_free(&a);
     return ORC_OK;
 }
 

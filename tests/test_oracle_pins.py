@@ -212,31 +212,34 @@ def test_p6_eq_dep_with_zero_delay_is_printed_formula(orc):
 
 # ------------------------------------------------------------------- P7
 
-def _total(orc, p, mu, sg, lam, alpha, rho):
-    terms, *_ = orc.loss_grad(p, mu, sg, lam, alpha, rho, grad=False)
+def _total(orc, p, mu, sg, lam, alpha, rho, beta=0.0, tau=1e-2):
+    terms, *_ = orc.loss_grad(p, mu, sg, lam, alpha, rho, grad=False, beta=beta, tau=tau)
     return terms[0, 0]
 
 
-@pytest.mark.parametrize("II,n_back", [(0, 0), (4, 2)])
-def test_p7_gradient_finite_differences(orc, II, n_back):
-    """Analytic gradient of the augmented Lagrangian vs central differences of
-    the oracle's own forward, away from ReLU kinks."""
-    rng = np.random.default_rng(70 + II)
+@pytest.mark.parametrize("II,n_back,beta,tau", [(0, 0, 0.0, 1e-2), (4, 2, 0.0, 1e-2),
+                                                (0, 0, 0.7, 0.3), (4, 2, 1.3, 0.05)])
+def test_p7_gradient_finite_differences(orc, II, n_back, beta, tau):
+    """Analytic gradient of the augmented Lagrangian (with the smooth peak
+    term when beta > 0) vs central differences of the oracle's own forward,
+    away from ReLU kinks."""
+    rng = np.random.default_rng(70 + II + int(100 * beta))
     checked = 0
     for _ in range(8):
         p = tiny_problem(rng, 7, 12, II=II, n_back=n_back, max_delay=2)
         mu = rng.uniform(0, 12, size=7); sg = np.exp(rng.uniform(np.log(0.5), np.log(4.0), size=7))
         lam = rng.uniform(0.1, 1.0, size=3); alpha, rho = 0.37, 0.2
-        terms, U, gm, gs, ties = orc.loss_grad(p, mu, sg, lam, alpha, rho, tie_tol=1e-3)
+        terms, U, gm, gs, ties = orc.loss_grad(p, mu, sg, lam, alpha, rho, tie_tol=1e-3, beta=beta, tau=tau)
         if ties[0]:
             continue
         h = 1e-6
         fd_m = np.zeros(7); fd_s = np.zeros(7)
+        tot = lambda m, s: _total(orc, p, m, s, lam, alpha, rho, beta, tau)
         for i in range(7):
             e = np.zeros(7); e[i] = h * max(1.0, abs(mu[i]))
-            fd_m[i] = (_total(orc, p, mu + e, sg, lam, alpha, rho) - _total(orc, p, mu - e, sg, lam, alpha, rho)) / (2 * e[i])
+            fd_m[i] = (tot(mu + e, sg) - tot(mu - e, sg)) / (2 * e[i])
             e = np.zeros(7); e[i] = h * max(1.0, sg[i])
-            fd_s[i] = (_total(orc, p, mu, sg + e, lam, alpha, rho) - _total(orc, p, mu, sg - e, lam, alpha, rho)) / (2 * e[i])
+            fd_s[i] = (tot(mu, sg + e) - tot(mu, sg - e)) / (2 * e[i])
         scale = max(np.abs(gm[0]).max(), np.abs(gs[0]).max(), 1e-3)
         assert np.abs(gm[0] - fd_m).max() < 1e-6 * scale + 1e-8
         assert np.abs(gs[0] - fd_s).max() < 1e-6 * scale + 1e-8
@@ -247,7 +250,7 @@ def test_p7_gradient_finite_differences(orc, II, n_back):
 torch = pytest.importorskip("torch")
 
 
-def _torch_total(p, mu, sg, lam, alpha, rho):
+def _torch_total(p, mu, sg, lam, alpha, rho, beta=0.0, tau=1e-2):
     """The objective written with fp64 torch ops straight from the paper's
     printed double sums (a second, independent formulation)."""
     D = p.D
@@ -280,25 +283,29 @@ def _torch_total(p, mu, sg, lam, alpha, rho):
     L = alpha * L_com
     for c in range(3):
         L = L + lam[c] * V[c] + 0.5 * rho * V[c] ** 2                  # eq. (11)
+    if beta:
+        L = L + beta * (tau * torch.logsumexp(U / tau, dim=1)).sum()   # App. B.2, eq:max
     return L
 
 
-@pytest.mark.parametrize("II,n_back", [(0, 0), (3, 2), (5, 3)])
-def test_p7_gradient_matches_autograd_of_double_sums(orc, II, n_back):
+@pytest.mark.parametrize("II,n_back,beta,tau", [(0, 0, 0.0, 1e-2), (3, 2, 0.0, 1e-2), (5, 3, 0.0, 1e-2),
+                                                (0, 0, 1.0, 1e-2), (0, 0, 0.6, 0.2), (3, 2, 1.0, 0.05)])
+def test_p7_gradient_matches_autograd_of_double_sums(orc, II, n_back, beta, tau):
     """The oracle's hand-derived backward equals fp64 autograd of the literal
-    double-sum formulation (independent code, independent derivation)."""
-    rng = np.random.default_rng(700 + II)
+    double-sum formulation (independent code, independent derivation), with
+    the smooth peak written with the library LogSumExp when beta > 0."""
+    rng = np.random.default_rng(700 + II + int(100 * beta))
     done = 0
     for _ in range(6):
         p = tiny_problem(rng, 6, 10, II=II, n_back=n_back, max_delay=3, K=2)
         mu = rng.uniform(-1, 10, size=6); sg = np.exp(rng.uniform(np.log(0.3), np.log(5.0), size=6))
         lam = rng.uniform(0.05, 1.0, size=3).tolist(); alpha, rho = 0.29, 0.13
-        terms, U, gm, gs, ties = orc.loss_grad(p, mu, sg, lam, alpha, rho, tie_tol=1e-6)
+        terms, U, gm, gs, ties = orc.loss_grad(p, mu, sg, lam, alpha, rho, tie_tol=1e-6, beta=beta, tau=tau)
         if ties[0]:
             continue
         tm = torch.tensor(mu, dtype=torch.float64, requires_grad=True)
         ts = torch.tensor(sg, dtype=torch.float64, requires_grad=True)
-        L = _torch_total(p, tm, ts, lam, alpha, rho)
+        L = _torch_total(p, tm, ts, lam, alpha, rho, beta, tau)
         L.backward()
         assert abs(L.item() - terms[0, 0]) < 1e-11
         assert np.abs(tm.grad.numpy() - gm[0]).max() < 1e-10
@@ -481,3 +488,38 @@ def test_init_state_paper_rule(orc):
     assert np.allclose(mu[0], (a + l) / 2)
     assert np.allclose(sg[0], np.maximum((l - a) / 6, 0.05))
     assert np.all(mu[1:] >= a - 1e-12) and np.all(mu[1:] <= l + 1e-12)
+
+
+# ------------------------------------------------------------------- P15
+
+def test_p15_smooth_peak_single_slot_is_op_count(orc):
+    """II = 1 folds every step onto one slot, where each type's usage is its
+    op count (the masses sum to 1): the smooth peak is exactly sum_k n_k and
+    does not depend on (mu, sigma), so its gradient vanishes."""
+    rng = np.random.default_rng(150)
+    for _ in range(4):
+        p = tiny_problem(rng, 6, 9, II=1, K=3)
+        mu = rng.uniform(-2, 11, size=6); sg = rng.uniform(0.3, 4.0, size=6)
+        terms, U, gm, gs, _ = orc.loss_grad(p, mu, sg, [0, 0, 0], 0.0, 0.0, beta=1.0, tau=0.01)
+        counts = np.bincount(p.rtype, minlength=3)
+        assert np.allclose(U[0, :, 0], counts, atol=1e-12)
+        assert abs(terms[0, 5] - counts.sum()) < 1e-9
+        assert abs(terms[0, 0] - counts.sum()) < 1e-9
+        assert np.abs(gm).max() < 1e-9 and np.abs(gs).max() < 1e-9
+
+
+def test_p15_smooth_peak_bounds_and_limits(orc):
+    """max_t U <= tau log sum_t exp(U/tau) <= max_t U + tau log T per type; as
+    tau -> infinity, L_res - K tau log T -> sum_k mean_t U_k(t) = N / T."""
+    rng = np.random.default_rng(151)
+    for II in (0, 3):
+        p = tiny_problem(rng, 7, 10, II=II, K=2)
+        T = II if II else p.D
+        mu = rng.uniform(0, 10, size=7); sg = rng.uniform(0.4, 3.0, size=7)
+        for tau in (1e-3, 0.05, 1.0):
+            terms, U, *_ = orc.loss_grad(p, mu, sg, [0, 0, 0], 0.0, 0.0, grad=False, beta=1.0, tau=tau)
+            mx = U[0].max(axis=1).sum()
+            assert mx - 1e-12 <= terms[0, 5] <= mx + 2 * tau * np.log(T) + 1e-12
+        tau = 1e7
+        terms, U, *_ = orc.loss_grad(p, mu, sg, [0, 0, 0], 0.0, 0.0, grad=False, beta=1.0, tau=tau)
+        assert abs(terms[0, 5] - 2 * tau * np.log(T) - p.n_ops / T) < 1e-5
