@@ -148,6 +148,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--poly-chunk", type=int, default=0,
                     help="chunk width of the polynomial path: 0 = library's choice, -1 = off (every op step by step)")
+    ap.add_argument("--lse-beta", type=float, default=0.0,
+                    help="weight of the smooth peak usage term (LogSumExp, temperature --tau); 0 = off")
+    ap.add_argument("--tau", type=float, default=1e-2)
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the run, copy this many MiB once (counter calibration)")
     args = ap.parse_args()
@@ -170,6 +173,8 @@ def main():
     hp = bd.default_hparams()
     hp.lr = cfg.lr
     hp.poly_chunk = args.poly_chunk
+    hp.beta_res = args.lse_beta
+    hp.tau = args.tau
     dev = torch.device("cuda")
     ctx = bd.Context(prob, B, hp)
     mu = torch.zeros(B, N, device=dev)
@@ -186,7 +191,7 @@ def main():
     # state of the CPU-baseline sample: the timing state before any step
     mu0, sg0, lam0 = mu.cpu().numpy(), sigma.cpu().numpy(), lam.cpu().numpy()
     ctx.bind_state(mu, sigma, m, v, lam, t)
-    terms = torch.zeros(B, 5, device=dev)
+    terms = torch.zeros(B, bd.N_TERMS, device=dev)
     sched = torch.zeros(B, N, dtype=torch.int32, device=dev)
 
     log(f"[bench] warmup {args.warmup} steps")
@@ -243,6 +248,8 @@ def main():
     # committed counter summary of this kernel and launch configuration
     profile = f"{dom}_{args.workload}" + ("" if args.poly_chunk == 0 else
                                           "_direct" if args.poly_chunk < 0 else f"_w{args.poly_chunk}")
+    if args.lse_beta:
+        profile += "_lse"
     whole = model_flops(B * N * (D - 1), B * (E + prob.n_back) * (D - 1))
     out = {
         "metric": METRIC, "value": value, "unit": "op-step evals/s", "n_gpus": 1,
@@ -250,7 +257,9 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": describe(cfg, prob), "B": B, "N": N, "E": E,
-                   "n_back": prob.n_back, "D": D, "II": prob.II},
+                   "n_back": prob.n_back, "D": D, "II": prob.II,
+                   "objective": "alpha L_com + ALM(V_dep, V_res, V_rec)" +
+                                (f" + {args.lse_beta:g} L_res (tau {args.tau:g})" if args.lse_beta else "")},
         "ms_per_iteration_events": step_ms_events, "legalize_ms": legalize_ms,
         "poly_path": dict(poly_cfg, ops=census["ops"], edges=census["edges"]),
         "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_TFLOPS, "unit": "TFLOP/s",

@@ -76,9 +76,10 @@ typedef struct {
 } gaus_problem;
 
 /* Hyper-parameters.  gaus_default_hparams() fills the paper's values
- * (App. C.1: Adam lr 1e-2, rho 1e-4, kappa 1/6; Sec. 3.3: lambda0 1e-6) and
- * this library's choices for the unstated ones (Adam betas/eps as in
- * Kingma & Ba, alpha_com 0.01, sigma_min 0.05). */
+ * (App. C.1: Adam lr 1e-2, rho 1e-4, kappa 1/6, LogSumExp temperature 1e-2;
+ * Sec. 3.3: lambda0 1e-6) and this library's choices for the unstated ones
+ * (Adam betas/eps as in Kingma & Ba, alpha_com 0.01, sigma_min 0.05,
+ * beta_res 0: the smooth peak term is off unless asked for). */
 typedef struct {
     float lr, beta1, beta2, eps;   /* Adam */
     float rho;                     /* ALM penalty */
@@ -89,6 +90,11 @@ typedef struct {
     int32_t poly_chunk;            /* chunk width W of the polynomial evaluation of wide
                                       Gaussians: 0 = chosen from D, < 0 = off (every op
                                       evaluated step by step), else W in [16, 256] */
+    float beta_res;                /* weight of the smooth peak usage L_res in L (>= 0;
+                                      1 with alpha_com gives Formulation A, Sec. 4.1) */
+    float tau;                     /* its temperature (> 0): L_res = sum_k tau log sum_t
+                                      exp(U_k(t)/tau), App. B.2 and eq:max; slots t < II
+                                      when II > 0 (App. B.3) */
 } gaus_hparams;
 
 void gaus_default_hparams(gaus_hparams *hp);
@@ -111,21 +117,23 @@ gaus_status gaus_bind_state(gaus_ctx *ctx, float *mu, float *sigma, float *adam_
 
 /* One forward + backward at (mu, sigma) with multipliers lambda, for all B
  * restarts.  Inputs DEVICE: mu, sigma [B][N], lambda [B][3].  Outputs DEVICE:
- * terms [B][5] = (L, V_dep, V_res, V_rec, L_com), grad_mu, grad_sigma [B][N]
- * (dL/dmu, dL/dsigma).  Asynchronous.  Errors: INVALID_ARG (null pointer). */
+ * terms [B][6] = (L, V_dep, V_res, V_rec, L_com, L_res), grad_mu, grad_sigma
+ * [B][N] (dL/dmu, dL/dsigma), where L = alpha_com L_com + beta_res L_res +
+ * sum_c (lambda_c V_c + rho/2 V_c^2) (Sec. 3.3 eq. 11; L_res is 0 when
+ * beta_res = 0).  Asynchronous.  Errors: INVALID_ARG (null pointer). */
 gaus_status gaus_loss_grad(gaus_ctx *ctx, const float *mu, const float *sigma, const float *lambda,
                            float *terms, float *grad_mu, float *grad_sigma);
 
 /* n_iters iterations of Alg. 1's update on the bound state: forward,
  * backward, Adam on mu and sigma, sigma <- max(sigma, sigma_min),
  * lambda_c <- lambda_c + rho * V_c (this iteration's V), adam_t += 1.
- * terms_last (DEVICE [B][5] or NULL) receives the last iteration's terms.
+ * terms_last (DEVICE [B][6] or NULL) receives the last iteration's terms.
  * Asynchronous.  Errors: INVALID_ARG (state not bound, n_iters < 0). */
 gaus_status gaus_step(gaus_ctx *ctx, int32_t n_iters, float *terms_last);
 
 /* The update half of gaus_step from a given gradient: Adam on the bound
  * (mu, sigma) with g_mu, g_sigma (DEVICE [B][N]), the sigma clamp, and
- * lambda_c += rho * terms[b][1+c] with terms DEVICE [B][5]; adam_t += 1.
+ * lambda_c += rho * terms[b][1+c] with terms DEVICE [B][6]; adam_t += 1.
  * Asynchronous.  Used to check the optimizer step on its own. */
 gaus_status gaus_adam_from_grad(gaus_ctx *ctx, const float *g_mu, const float *g_sigma,
                                 const float *terms);

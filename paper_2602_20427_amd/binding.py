@@ -43,7 +43,10 @@ class _Problem(C.Structure):
 class HParams(C.Structure):
     _fields_ = [("lr", C.c_float), ("beta1", C.c_float), ("beta2", C.c_float), ("eps", C.c_float),
                 ("rho", C.c_float), ("lambda0", C.c_float), ("alpha_com", C.c_float),
-                ("sigma_min", C.c_float), ("kappa", C.c_float), ("poly_chunk", C.c_int32)]
+                ("sigma_min", C.c_float), ("kappa", C.c_float), ("poly_chunk", C.c_int32),
+                ("beta_res", C.c_float), ("tau", C.c_float)]
+
+N_TERMS = 6   # L, V_dep, V_res, V_rec, L_com, L_res
 
 
 _lib = None
@@ -179,12 +182,12 @@ class Context:
         f = torch.float32
         self._check(load().gaus_loss_grad(
             self._h, _dptr(mu, f, (B, N), "mu"), _dptr(sigma, f, (B, N), "sigma"),
-            _dptr(lam, f, (B, 3), "lambda"), _dptr(terms, f, (B, 5), "terms"),
+            _dptr(lam, f, (B, 3), "lambda"), _dptr(terms, f, (B, N_TERMS), "terms"),
             _dptr(grad_mu, f, (B, N), "grad_mu"), _dptr(grad_sigma, f, (B, N), "grad_sigma")))
 
     def step(self, n_iters: int, terms_last=None):
         import torch
-        tp = None if terms_last is None else _dptr(terms_last, torch.float32, (self.B, 5), "terms_last")
+        tp = None if terms_last is None else _dptr(terms_last, torch.float32, (self.B, N_TERMS), "terms_last")
         self._check(load().gaus_step(self._h, int(n_iters), tp))
 
     def adam_from_grad(self, g_mu, g_sigma, terms):
@@ -193,7 +196,7 @@ class Context:
         f = torch.float32
         self._check(load().gaus_adam_from_grad(
             self._h, _dptr(g_mu, f, (B, N), "g_mu"), _dptr(g_sigma, f, (B, N), "g_sigma"),
-            _dptr(terms, f, (B, 5), "terms")))
+            _dptr(terms, f, (B, N_TERMS), "terms")))
 
     def legalize(self, mu, sched):
         """Returns the per-restart status array (host)."""

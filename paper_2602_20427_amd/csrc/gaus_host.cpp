@@ -329,6 +329,8 @@ void gaus_default_hparams(gaus_hparams *hp) {
     hp->sigma_min = 0.05f;
     hp->kappa = 1.0f / 6.0f;
     hp->poly_chunk = 0;
+    hp->beta_res = 0.0f;
+    hp->tau = 1e-2f;
 }
 
 const char *gaus_status_string(gaus_status s) {
@@ -363,7 +365,8 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     if (!c) return fail(nullptr, GAUS_E_NOMEM, "host allocation failed");
     gaus_hparams hp;
     if (hp_in) hp = *hp_in; else gaus_default_hparams(&hp);
-    c->hp = HP{hp.lr, hp.beta1, hp.beta2, hp.eps, hp.rho, hp.lambda0, hp.alpha_com, hp.sigma_min, hp.kappa};
+    c->hp = HP{hp.lr,        hp.beta1,     hp.beta2,     hp.eps,   hp.rho,     hp.lambda0,
+               hp.alpha_com, hp.sigma_min, hp.kappa,     hp.beta_res, hp.tau};
     c->stream = static_cast<hipStream_t>(hip_stream);
     (void)hipGetDevice(&c->device);
     int tile = 0, ntiles = 0;
@@ -371,6 +374,10 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     if (hp.poly_chunk > 0 && (hp.poly_chunk < 16 || hp.poly_chunk > 256)) {
         delete c;
         return fail(nullptr, GAUS_E_INVALID_ARG, "poly_chunk must be 0 (auto), negative (off) or in [16, 256]");
+    }
+    if (!(hp.beta_res >= 0.0f) || !std::isfinite(hp.beta_res) || !(hp.tau > 0.0f) || !std::isfinite(hp.tau)) {
+        delete c;
+        return fail(nullptr, GAUS_E_INVALID_ARG, "beta_res must be finite and >= 0, tau finite and > 0");
     }
     setup_poly(h.D, hp.poly_chunk, c->pa);
 
@@ -405,7 +412,13 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     AL(U, (size_t)B * h.K * g.T);
     AL(trans, (size_t)B * h.K * h.D);
     AL(ntrans, (size_t)B * h.K);
-    AL(terms, (size_t)B * 5);
+    AL(terms, (size_t)B * kTerms);
+    AL(lres_part, (size_t)B * h.K);
+    AL(soft, (size_t)B * h.K * g.T);
+    AL(lmom, (size_t)B * h.K * kMaxChunks * kNC);
+    AL(lstrip, (size_t)B * h.K * kStripMax);
+    AL(lpart, BN * ntiles * 2);
+    AL(lpoly, BN * 2);
     AL(wts, (size_t)B * 4);
     AL(adamf, (size_t)B * 2);
     AL(cls, BN);

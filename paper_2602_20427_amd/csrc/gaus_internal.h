@@ -16,6 +16,7 @@ constexpr int kCP = 4;   // per (restart, edge, tile): dVdep/dmu_j, dVdep/dsigma
 constexpr int kBP = 5;   // per (restart, back edge, tile): V_rec, dVrec/dmu_j, dVrec/dsigma_j
                          //   (producer j), dVrec/dmu_i, dVrec/dsigma_i (consumer i)
 constexpr int kHalo = 256;  // largest producer delay handled from the LDS row window
+constexpr int kTerms = 6;   // per restart: L, V_dep, V_res, V_rec, L_com, L_res
 
 // Chunk-polynomial path (dense regime).  On a chunk of W consecutive steps
 // with rho = ((W-1)/2)/sigma <= kRhoMax the CDF row of an op is a degree-kDeg
@@ -69,7 +70,13 @@ struct Work {
     float *U;         // [B][K][T]         expected (folded) usage
     int *trans;       // [B][K][D]         signed (t+1) of each ReLU-indicator change at bin edge t
     int *ntrans;      // [B][K]
-    float *terms;     // [B][5]            L, V_dep, V_res, V_rec, L_com of the last forward
+    float *terms;     // [B][kTerms]       L, V_dep, V_res, V_rec, L_com, L_res of the last forward
+    float *lres_part; // [B][K]            smooth peak of one type's usage
+    float *soft;      // [B][K][T]         beta * dL_res/dU (softmax over the type's slots)
+    float *lmom;      // [B][K][64][kNC]   chunk moments of the softmax differences at the bin edges
+    float *lstrip;    // [B][K][kStripMax] the same differences at the strip positions
+    float *lpart;     // [B][N][tiles][2]  smooth-peak gradient (mu, sigma) of step-by-step ops, per tile
+    float *lpoly;     // [B][N][2]         the same for ops on the polynomial path
     float *wts;       // [B][4]            w_dep, w_res, w_rec, unused
     float *adamf;     // [B][2]            Adam bias corrections 1-beta1^t, 1-beta2^t
     unsigned char *cls;  // [B][N]          1 = op on the chunk-polynomial path this iteration
@@ -90,6 +97,7 @@ struct Work {
 
 struct HP {
     float lr, b1, b2, eps, rho, lambda0, alpha, sigma_min, kappa;
+    float beta, tau;   // weight and temperature of the smooth peak usage L_res
 };
 
 // Kernel-side configuration chosen on the host from (N, D, B).
@@ -105,7 +113,7 @@ struct IterArgs {
     const float *lambda_in;         // [B][3]
     float *lambda_out;              // mode 1: updated multipliers (may alias lambda_in)
     int *adam_t;                    // mode 1
-    float *terms_out;               // [B][5] or null
+    float *terms_out;               // [B][kTerms] or null
     float *gmu, *gsig;              // mode 0 outputs
     float *mu_io, *sig_io, *m, *v;  // mode 1 state
     int mode;

@@ -124,6 +124,18 @@ __device__ __forceinline__ float wave_sum4(float v0, float v1, float v2, float v
     return cross_rows_sum(x);
 }
 
+// Maximum over the 64 lanes; every lane receives it.
+__device__ __forceinline__ float wave_max(float x) {
+    x = fmaxf(x, dpp_mov<kDppXor1>(x));
+    x = fmaxf(x, dpp_mov<kDppXor2>(x));
+    x = fmaxf(x, dpp_mov<kDppHalfMirror>(x));
+    x = fmaxf(x, dpp_mov<kDppMirror>(x));
+    constexpr int kSwizzleXor16 = 0x1F | (0x10 << 10);
+    x = fmaxf(x, __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), kSwizzleXor16)));
+    const int lane = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+    return fmaxf(x, __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute((lane ^ 32) << 2, __builtin_bit_cast(int, x))));
+}
+
 // Two sums at once: lane l < 2 receives the total of value l.
 __device__ __forceinline__ float wave_sum2(float v0, float v1, int lane) {
     const bool b0 = lane & 1;
@@ -755,6 +767,174 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
 }
 
 // ---------------------------------------------------------------------------
+// Gradient of the smooth peak usage.  With c_k(d) = beta dL_res/dU_k(d mod T)
+// (the softmax written by k_vres), summation by parts onto the interior bin
+// edges gives
+//   dL/dth_i += sum_{t=0}^{D-2} (c(t) - c(t+1)) dF_i(t)/dth_i,
+// a dense weight per bin edge.  Step-by-step ops take it per step
+// (k_lse_ops); polynomial ops take it per chunk as the moments
+// M_n = sum_y (c(t) - c(t+1)) y^n (k_lse_mom), dotted with the chunk
+// coefficients of dF/dmu and dF/dsigma (k_lse_poly).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float soft_diff(const float *sk, int t, int T) {
+    return sk[t % T] - sk[(t + 1) % T];
+}
+
+template <int BS, int SPT>
+__global__ __launch_bounds__(BS) void k_lse_ops(Graph G, const float *__restrict__ mu,
+                                                const float *__restrict__ sigma, Work W) {
+    constexpr int TILE = BS * SPT;
+    __shared__ float sW[TILE];
+    __shared__ int sI[BS];
+    __shared__ float sMu[BS], sRs[BS];
+    __shared__ float sRed[2][BS / 64][8];
+    const int grp = blockIdx.x, tile = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
+    const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
+    const int N = G.N, D = G.D, T = G.T;
+    const int t0 = tile * TILE;
+    int direct = 0;
+    if (q0 + tid < q1) {
+        const int i = G.perm[q0 + tid];
+        const size_t bi = (size_t)b * N + i;
+        direct = W.cls[bi] ? 0 : 1;
+        sI[tid] = direct ? i : -1;
+        sMu[tid] = mu[bi];
+        sRs[tid] = 1.0f / sigma[bi];
+    } else if (tid < BS) {
+        sI[tid] = -1;
+    }
+    if (!__syncthreads_or(direct)) return;   // every op of the group is polynomial
+    const float *sk = W.soft + ((size_t)b * G.K + G.rtype[G.perm[q0]]) * T;
+    for (int x = tid; x < TILE; x += BS) {
+        const int t = t0 + x;
+        sW[x] = t <= D - 2 ? soft_diff(sk, t, T) : 0.0f;
+    }
+    __syncthreads();
+    int par = 0;
+    for (int q = 0; q < q1 - q0; ++q) {
+        const int i = sI[q];
+        if (i < 0) continue;
+        const float m = sMu[q], rs = sRs[q], cinv = rs * kInvSqrt2Pi;
+        float acc[2] = {0.0f, 0.0f};
+#pragma unroll
+        for (int j = 0; j < SPT; ++j) {
+            const int x = tid + j * BS;
+            const float w = sW[x];
+            if (w != 0.0f) {
+                const float z = ((float)(t0 + x) + 0.5f - m) * rs;
+                const float Fm = -__builtin_amdgcn_exp2f(-(z * z) * kHalfLog2e) * cinv;
+                acc[0] = fmaf(w, Fm, acc[0]);
+                acc[1] = fmaf(w, Fm * z, acc[1]);
+            }
+        }
+        const float r = block_sum<2, BS>(acc, sRed[par]);
+        par ^= 1;
+        if (tid < 2) W.lpart[(((size_t)b * N + i) * G.ntiles + tile) * 2 + tid] = r;
+    }
+}
+
+__global__ __launch_bounds__(256) void k_lse_mom(Graph G, PolyArgs pa, Work W) {
+    __shared__ float sRed[4][kNC];
+    const int c = blockIdx.x, k = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
+    const int lane = tid & 63, wid = tid >> 6;
+    const int T = G.T, D = G.D;
+    const float *sk = W.soft + ((size_t)b * G.K + k) * T;
+    if (c == pa.nc) {   // the strip: weights per position (none at D-1, not a bin edge)
+        float *dst = W.lstrip + ((size_t)b * G.K + k) * kStripMax;
+        for (int p = tid; p < pa.SP; p += 256) {
+            const int u = p < pa.L0 ? p : D - 2 + (p - pa.L0);
+            dst[p] = u <= D - 2 ? soft_diff(sk, u, T) : 0.0f;
+        }
+        return;
+    }
+    float mom[kNC];
+#pragma unroll
+    for (int n = 0; n < kNC; ++n) mom[n] = 0.0f;
+    if (tid < pa.W) {
+        const int t = pa.L0 + c * pa.W + tid;
+        const float y = (float)tid - pa.lam;
+        float yp = soft_diff(sk, t, T);
+#pragma unroll
+        for (int n = 0; n < kNC; ++n) { mom[n] = yp; yp *= y; }
+    }
+#pragma unroll
+    for (int n = 0; n < kNC; ++n) {
+        const float r = wave_sum(mom[n]);
+        if (lane == 0) sRed[wid][n] = r;
+    }
+    __syncthreads();
+    if (tid < kNC)
+        W.lmom[(((size_t)b * G.K + k) * kMaxChunks + c) * kNC + tid] =
+            (sRed[0][tid] + sRed[1][tid]) + (sRed[2][tid] + sRed[3][tid]);
+}
+
+template <int NP>
+__global__ __launch_bounds__(64 * kPolyWaves) void k_lse_poly(Graph G, PolyArgs pa, const float *__restrict__ mu,
+                                                              const float *__restrict__ sigma, Work W) {
+    const int SP = pa.SP, split = pa.split;
+    const int grp = blockIdx.x / split, sub = blockIdx.x - grp * split, b = blockIdx.y;
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int N = G.N, D = G.D;
+    const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
+    if (q1 <= q0) return;
+    const int nj = (q1 - q0 - sub + split - 1) / split;
+    const int nq = (nj - wv + kPolyWaves - 1) / kPolyWaves;
+    int l_i = 0, l_cls = 0;
+    float l_mu = 0.0f, l_sg = 1.0f;
+    if (lane < nq) {
+        l_i = G.perm[q0 + sub + split * (wv + kPolyWaves * lane)];
+        const size_t bi = (size_t)b * N + l_i;
+        l_cls = W.cls[bi];
+        l_mu = mu[bi]; l_sg = sigma[bi];
+    }
+    // this lane's chunk moments and strip weights of the group's type
+    const int k = G.rtype[G.perm[q0]];
+    const bool cact = lane < pa.nc;
+    float mom[kNC];
+    const float *msrc = W.lmom + (((size_t)b * G.K + k) * kMaxChunks + lane) * kNC;
+#pragma unroll
+    for (int n = 0; n < kNC; ++n) mom[n] = cact ? msrc[n] : 0.0f;
+    float sw[NP];
+    const float *ssrc = W.lstrip + ((size_t)b * G.K + k) * kStripMax;
+#pragma unroll
+    for (int ps = 0; ps < NP; ++ps) {
+        const int p = ps * 64 + lane;
+        sw[ps] = p < SP ? ssrc[p] : 0.0f;
+    }
+    const float tcen = (float)(pa.L0 + lane * pa.W) + pa.lam;
+    for (int oq = 0; oq < nq; ++oq) {
+        if (!__builtin_amdgcn_readlane(l_cls, oq)) continue;
+        const int i = __builtin_amdgcn_readlane(l_i, oq);
+        const float m_i = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, l_mu), oq));
+        const float s_i = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, l_sg), oq));
+        const float rs = 1.0f / s_i, cinv = rs * kInvSqrt2Pi;
+        float gm = 0.0f, gs = 0.0f;
+#pragma unroll
+        for (int ps = 0; ps < NP; ++ps) {
+            const int p = ps * 64 + lane;
+            if (p < SP) {
+                const int u = p < pa.L0 ? p : D - 2 + (p - pa.L0);
+                const float z = ((float)u + 0.5f - m_i) * rs;
+                const float Fm = -__builtin_amdgcn_exp2f(-(z * z) * kHalfLog2e) * cinv;
+                gm = fmaf(sw[ps], Fm, gm);
+                gs = fmaf(sw[ps], Fm * z, gs);
+            }
+        }
+        if (cact) {
+            Expansion e;
+            expand(m_i, rs, tcen, e);
+            float a[kNC], v[kNC];
+            vec_dFdmu(e, a);
+            vec_times_z(a, e.z0, e.r, v);
+            gm += vdot(a, mom);
+            gs += vdot(v, mom);
+        }
+        const float r = wave_sum2(gm, gs, lane);
+        if (lane < 2) W.lpoly[((size_t)b * N + i) * 2 + lane] = r;
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Back-edge kernel (modulo scheduling).  Work-group = (back-edge block, tile,
 // restart); one back edge (j -> i, k) at a time, c = k*II - Lat_j:
 //   V_rec       = F_i(-c-1) + sum_u P_i^{u-c} (1 - F_j(u))
@@ -926,7 +1106,22 @@ __device__ float block_sum1024(float x, float *scratch /*[16]*/) {
     return r;
 }
 
-__global__ __launch_bounds__(kTermsBS) void k_vres(Graph G, Work W) {
+__device__ float block_max1024(float x, float *scratch /*[16]*/) {
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    x = wave_max(x);
+    if (lane == 0) scratch[wid] = x;
+    __syncthreads();
+    float r = scratch[0];
+#pragma unroll
+    for (int w = 1; w < kTermsBS / 64; ++w) r = fmaxf(r, scratch[w]);
+    __syncthreads();
+    return r;
+}
+
+// Per (type, restart) also the smooth peak (App. B.2, eq:max)
+//   L_res,k = tau log sum_t exp(U_k(t)/tau) = M + tau log sum_t exp((U_k(t) - M)/tau),
+// M = max_t U_k(t), and beta times its derivative (the softmax) per slot.
+__global__ __launch_bounds__(kTermsBS) void k_vres(Graph G, Work W, HP hp) {
     __shared__ float scratch[kTermsBS / 64];
     __shared__ int wcount[kTermsBS / 64];
     __shared__ int base;
@@ -943,6 +1138,22 @@ __global__ __launch_bounds__(kTermsBS) void k_vres(Graph G, Work W) {
     }
     vres = block_sum1024(vres, scratch);
     if (tid == 0) W.vres_part[(size_t)b * G.K + k] = vres;
+
+    if (hp.beta != 0.0f) {
+        float mx = -INFINITY;
+        for (int c = tid; c < T; c += kTermsBS) mx = fmaxf(mx, Uk[c]);
+        mx = block_max1024(mx, scratch);
+        const float itau = 1.0f / hp.tau;
+        float z = 0.0f;
+        for (int c = tid; c < T; c += kTermsBS) z += expf((Uk[c] - mx) * itau);
+        z = block_sum1024(z, scratch);
+        if (tid == 0) W.lres_part[(size_t)b * G.K + k] = mx + hp.tau * logf(z);
+        const float bz = hp.beta / z;
+        float *sk = W.soft + ((size_t)b * G.K + k) * T;
+        for (int c = tid; c < T; c += kTermsBS) sk[c] = bz * expf((Uk[c] - mx) * itau);
+    } else if (tid == 0) {
+        W.lres_part[(size_t)b * G.K + k] = 0.0f;
+    }
 
     int *out = W.trans + ((size_t)b * G.K + k) * D;
     if (tid == 0) base = 0;
@@ -995,8 +1206,11 @@ __global__ __launch_bounds__(kCombineBS) void k_combine(Graph G, PolyArgs pa, Wo
                                                         float *terms_out) {
     __shared__ float scratch[kCombineBS / 64];
     const int b = blockIdx.x, tid = threadIdx.x;
-    float vres = 0.0f, vdep = 0.0f, lcom = 0.0f, vrec = 0.0f;
-    for (int k = tid; k < G.K; k += kCombineBS) vres += W.vres_part[(size_t)b * G.K + k];
+    float vres = 0.0f, vdep = 0.0f, lcom = 0.0f, vrec = 0.0f, lres = 0.0f;
+    for (int k = tid; k < G.K; k += kCombineBS) {
+        vres += W.vres_part[(size_t)b * G.K + k];
+        lres += W.lres_part[(size_t)b * G.K + k];
+    }
     const int npoly = G.ngroups * pa.split;
     for (int g = tid; g < npoly; g += kCombineBS) {
         const float *gp = W.gsum_poly + ((size_t)b * npoly + g) * 2;
@@ -1015,19 +1229,20 @@ __global__ __launch_bounds__(kCombineBS) void k_combine(Graph G, PolyArgs pa, Wo
     vdep = block_sum256(vdep, scratch);
     lcom = block_sum256(lcom, scratch);
     vrec = block_sum256(vrec, scratch);
+    lres = block_sum256(lres, scratch);
 
     if (tid == 0) {
         const float V[3] = {vdep, vres, vrec};
         const float *lam = lambda_in + (size_t)b * 3;
-        float L = hp.alpha * lcom;
+        float L = fmaf(hp.beta, lres, hp.alpha * lcom);
         float w[3];
         for (int c = 0; c < 3; ++c) {
             L += lam[c] * V[c] + 0.5f * hp.rho * V[c] * V[c];
             w[c] = lam[c] + hp.rho * V[c];
         }
-        float *tm = W.terms + (size_t)b * 5;
-        tm[0] = L; tm[1] = vdep; tm[2] = vres; tm[3] = vrec; tm[4] = lcom;
-        if (terms_out) for (int c = 0; c < 5; ++c) terms_out[(size_t)b * 5 + c] = tm[c];
+        float *tm = W.terms + (size_t)b * kTerms;
+        tm[0] = L; tm[1] = vdep; tm[2] = vres; tm[3] = vrec; tm[4] = lcom; tm[5] = lres;
+        if (terms_out) for (int c = 0; c < kTerms; ++c) terms_out[(size_t)b * kTerms + c] = tm[c];
         float *wt = W.wts + (size_t)b * 4;
         wt[0] = w[0]; wt[1] = w[1]; wt[2] = w[2]; wt[3] = 0.0f;
         if (lambda_out) for (int c = 0; c < 3; ++c) lambda_out[(size_t)b * 3 + c] = fmaf(hp.rho, V[c], lam[c]);
@@ -1126,8 +1341,19 @@ __global__ __launch_bounds__(256) void k_final(Graph G, Work W, HP hp, const flo
         const float *bp = W.bpart + (((size_t)b * G.nb + G.bin[q]) * nt) * kBP;
         for (int tl = 0; tl < nt; ++tl) { qm += bp[tl * kBP + 3]; qs += bp[tl * kBP + 4]; }
     }
-    const float g_mu = combine_grad(w_res, rm, w_dep, dm, w_rec, qm, hp.alpha, cm);
-    const float g_sg = combine_grad(w_res, rsg, w_dep, ds, w_rec, qs, hp.alpha, cs);
+    float g_mu = combine_grad(w_res, rm, w_dep, dm, w_rec, qm, hp.alpha, cm);
+    float g_sg = combine_grad(w_res, rsg, w_dep, ds, w_rec, qs, hp.alpha, cs);
+    if (hp.beta != 0.0f) {   // smooth peak usage, already weighted by beta
+        float lm = 0.0f, ls = 0.0f;
+        if (poly_i) {
+            lm = W.lpoly[bi * 2 + 0]; ls = W.lpoly[bi * 2 + 1];
+        } else {
+            const float *lp = W.lpart + bi * nt * 2;
+            for (int tl = 0; tl < nt; ++tl) { lm += lp[tl * 2 + 0]; ls += lp[tl * 2 + 1]; }
+        }
+        g_mu = __fadd_rn(g_mu, lm);
+        g_sg = __fadd_rn(g_sg, ls);
+    }
 
     if (mode == 0) {
         gmu[bi] = g_mu;
@@ -1152,7 +1378,7 @@ __global__ void k_lambda_from_terms(int B, HP hp, const float *terms, float *lam
     const int b = blockIdx.x * blockDim.x + threadIdx.x;
     if (b >= B) return;
     for (int c = 0; c < 3; ++c)
-        lambda[(size_t)b * 3 + c] = fmaf(hp.rho, terms[(size_t)b * 5 + 1 + c], lambda[(size_t)b * 3 + c]);
+        lambda[(size_t)b * 3 + c] = fmaf(hp.rho, terms[(size_t)b * kTerms + 1 + c], lambda[(size_t)b * 3 + c]);
     const int t = *adam_t + 1;
     adamf[(size_t)b * 2 + 0] = 1.0f - powf(hp.b1, (float)t);
     adamf[(size_t)b * 2 + 1] = 1.0f - powf(hp.b2, (float)t);
@@ -1322,10 +1548,30 @@ hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const 
     if (pa.enabled)
         hipLaunchKernelGGL(k_ucoef, dim3((pa.nc * kNC + pa.SP + 63) / 64, g.K, g.B), dim3(256), 0, st, g, pa, w);
     hipLaunchKernelGGL(k_usage, dim3((g.T + kUsageBS - 1) / kUsageBS, g.K, g.B), dim3(kUsageBS), 0, st, g, pa, w);
-    hipLaunchKernelGGL(k_vres, dim3(g.K, g.B), dim3(kTermsBS), 0, st, g, w);
+    hipLaunchKernelGGL(k_vres, dim3(g.K, g.B), dim3(kTermsBS), 0, st, g, w, hp);
     hipLaunchKernelGGL(k_combine, dim3(g.B), dim3(kCombineBS), 0, st, g, pa, w, hp, a.lambda_in,
                        a.mode == 1 ? a.lambda_out : nullptr, a.mode == 1 ? a.adam_t : nullptr,
                        a.terms_out);
+    if (hp.beta != 0.0f) {   // gradient of the smooth peak usage
+        const dim3 gops(g.ngroups, g.ntiles, g.B);
+        if (lc.bs == 64) hipLaunchKernelGGL((k_lse_ops<64, 1>), gops, dim3(64), 0, st, g, a.mu, a.sigma, w);
+        else if (lc.spt == 1) hipLaunchKernelGGL((k_lse_ops<256, 1>), gops, dim3(256), 0, st, g, a.mu, a.sigma, w);
+        else hipLaunchKernelGGL((k_lse_ops<256, 4>), gops, dim3(256), 0, st, g, a.mu, a.sigma, w);
+        if (pa.enabled) {
+            hipLaunchKernelGGL(k_lse_mom, dim3(pa.nc + 1, g.K, g.B), dim3(256), 0, st, g, pa, w);
+            const dim3 grid(g.ngroups * pa.split, g.B), block(64 * kPolyWaves);
+            switch ((pa.SP + 63) / 64) {
+            case 1: hipLaunchKernelGGL(k_lse_poly<1>, grid, block, 0, st, g, pa, a.mu, a.sigma, w); break;
+            case 2: hipLaunchKernelGGL(k_lse_poly<2>, grid, block, 0, st, g, pa, a.mu, a.sigma, w); break;
+            case 3: hipLaunchKernelGGL(k_lse_poly<3>, grid, block, 0, st, g, pa, a.mu, a.sigma, w); break;
+            case 4: hipLaunchKernelGGL(k_lse_poly<4>, grid, block, 0, st, g, pa, a.mu, a.sigma, w); break;
+            case kStripPassesMax:
+                hipLaunchKernelGGL(k_lse_poly<kStripPassesMax>, grid, block, 0, st, g, pa, a.mu, a.sigma, w);
+                break;
+            default: return hipErrorInvalidValue;
+            }
+        }
+    }
     {
         dim3 grid((g.N + 255) / 256, g.B);
         hipLaunchKernelGGL(k_final, grid, dim3(256), 0, st, g, w, hp, a.mu, a.sigma, a.gmu, a.gsig,

@@ -19,13 +19,16 @@ def say(*a):
     sys.stdout.flush()
 
 
-def hparams(alpha=0.01, rho=1e-4, lr=1e-2, poly_chunk=0):
-    """poly_chunk: 0 = library's choice, < 0 = polynomial path off, else W."""
+def hparams(alpha=0.01, rho=1e-4, lr=1e-2, poly_chunk=0, beta=0.0, tau=1e-2):
+    """poly_chunk: 0 = library's choice, < 0 = polynomial path off, else W;
+    beta, tau: weight and temperature of the smooth peak usage term."""
     hp = bd.default_hparams()
     hp.alpha_com = alpha
     hp.rho = rho
     hp.lr = lr
     hp.poly_chunk = poly_chunk
+    hp.beta_res = beta
+    hp.tau = tau
     return hp
 
 
@@ -38,7 +41,7 @@ def gpu_loss_grad(prob, mu, sigma, lam, hp):
     m = torch.from_numpy(np.ascontiguousarray(mu, np.float32)).to(dev)
     s = torch.from_numpy(np.ascontiguousarray(sigma, np.float32)).to(dev)
     l = torch.from_numpy(np.ascontiguousarray(lam, np.float32)).to(dev)
-    terms = torch.zeros(B, 5, device=dev)
+    terms = torch.zeros(B, bd.N_TERMS, device=dev)
     gm = torch.zeros(B, N, device=dev)
     gs = torch.zeros(B, N, device=dev)
     ctx.loss_grad(m, s, l, terms, gm, gs)
@@ -55,7 +58,7 @@ def compare_restart(g, o_terms, o_U, o_gm, o_gs, b, what=""):
     """Assert the parity bar for restart b; returns the worst relative errors."""
     t, ot = g["terms"][b], o_terms
     err_t = np.abs(t - ot) / np.maximum(np.abs(ot), 1.0)
-    names = ["L", "V_dep", "V_res", "V_rec", "L_com"]
+    names = ["L", "V_dep", "V_res", "V_rec", "L_com", "L_res"]
     assert err_t.max() <= TOL, f"{what} b={b} terms {dict(zip(names, t))} vs {dict(zip(names, ot))} err {err_t}"
     eu = np.abs(g["U"][b] - o_U).max() / max(np.abs(o_U).max(), 1.0)
     assert eu <= TOL, f"{what} b={b} usage err {eu}"

@@ -28,7 +28,8 @@ def _check(prob, mu, sigma, lam, hp, restarts, what):
     for b in restarts:
         ot, oU, ogm, ogs, ties = oracle.loss_grad(prob, mu[b:b + 1].astype(np.float64),
                                                   sigma[b:b + 1].astype(np.float64), lam[b:b + 1],
-                                                  hp.alpha_com, hp.rho, tie_tol=1e-4)
+                                                  hp.alpha_com, hp.rho, tie_tol=1e-4,
+                                                  beta=hp.beta_res, tau=hp.tau)
         if ties[0]:
             say(f"  b={b}: {ties[0]} near-tie usage cells, comparing terms/usage only")
             err_t = np.abs(g["terms"][b] - ot[0]) / np.maximum(np.abs(ot[0]), 1.0)
@@ -245,7 +246,7 @@ def test_adam_from_grad_matches_oracle():
     ctx = bd.Context(p, B, hp)
     st = _state(ctx, mu.copy(), sg.copy(), lam.copy())
     dev = torch.device("cuda")
-    terms = torch.zeros(B, 5, device=dev)
+    terms = torch.zeros(B, bd.N_TERMS, device=dev)
     gm = torch.zeros(B, p.n_ops, device=dev); gs = torch.zeros(B, p.n_ops, device=dev)
     m_o = np.zeros((2, B, p.n_ops)); v_o = np.zeros((2, B, p.n_ops))
     th_mu, th_sg, lam_o = mu.astype(np.float64), sg.astype(np.float64), lam.astype(np.float64)
@@ -283,9 +284,9 @@ def test_step_equals_loss_grad_plus_adam_bitwise():
     ca = bd.Context(p, B, hp); sa = _state(ca, mu.copy(), sg.copy(), lam.copy())
     cb = bd.Context(p, B, hp); sb = _state(cb, mu.copy(), sg.copy(), lam.copy())
     dev = torch.device("cuda")
-    terms_a = torch.zeros(B, 5, device=dev)
+    terms_a = torch.zeros(B, bd.N_TERMS, device=dev)
     ca.step(5, terms_a)
-    terms = torch.zeros(B, 5, device=dev)
+    terms = torch.zeros(B, bd.N_TERMS, device=dev)
     gm = torch.zeros(B, p.n_ops, device=dev); gs = torch.zeros(B, p.n_ops, device=dev)
     for _ in range(5):
         cb.loss_grad(sb["mu"], sb["sigma"], sb["lam"], terms, gm, gs)
