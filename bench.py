@@ -58,7 +58,10 @@ PEAK_TFLOPS = 157.3
 # issue-rate reference: the measured v_fma_f32 rate above
 N_CU = 256
 CLOCK_HZ = 2.4e9
-KERNEL_SRC = os.path.join(ROOT, "paper_2602_20427_amd", "csrc", "gaus_kernels.hip")
+CSRC = os.path.join(ROOT, "paper_2602_20427_amd", "csrc")
+# the sources a kernel is built from (its file and the shared device headers)
+KERNEL_SOURCES = {"k_poly": "gaus_poly.hip", "k_ops": "gaus_step.hip"}
+SHARED_HEADERS = ("gaus_device.h", "gaus_internal.h", "gaus_erfcx_coeffs.h")
 KERNEL_NAMES = {"ops": "k_ops", "poly": "k_poly"}
 
 
@@ -66,9 +69,12 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_source_hash() -> str:
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+def kernel_source_hash(kernel: str) -> str:
+    h = hashlib.sha256()
+    for name in (KERNEL_SOURCES[kernel], *SHARED_HEADERS):
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def model_flops(units_op, units_edge):
@@ -76,34 +82,33 @@ def model_flops(units_op, units_edge):
     return 2.0 * slots
 
 
-def pmc_traffic(profile):
-    """HBM bytes per launch from the committed rocprofv3 counter summary
-    profiles/<profile>_pmc.md, if it was taken on the current kernel source;
-    else None."""
+def pmc_value(kernel, profile, key):
+    """A figure from the committed rocprofv3 counter summary
+    profiles/<profile>_pmc.md, if it was taken on the kernel's current
+    sources; else None."""
     path = os.path.join(ROOT, "profiles", f"{profile}_pmc.md")
     if not os.path.exists(path):
         return None
     txt = open(path).read()
     h = re.search(r"kernel_source_sha256:\s*([0-9a-f]+)", txt)
-    v = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", txt)
-    if not h or not v or h.group(1) != kernel_source_hash():
+    v = re.search(key + r":\s*([0-9.eE+]+)", txt)
+    if not h or not v or h.group(1) != kernel_source_hash(kernel):
         return None
     return float(v.group(1))
 
 
-def pmc_issue(profile, kernel_ms):
-    """VALU issue rate from the committed rocprofv3 SQ-counter summary
-    profiles/<profile>_pmc.md (taken on the current kernel source), against
-    the measured v_fma_f32 issue rate of the chip; else None."""
-    path = os.path.join(ROOT, "profiles", f"{profile}_pmc.md")
-    if not os.path.exists(path):
+def pmc_traffic(kernel, profile):
+    """HBM bytes per launch from the committed counter summary, or None."""
+    return pmc_value(kernel, profile, "traffic_bytes_per_launch")
+
+
+def pmc_issue(kernel, profile, kernel_ms):
+    """VALU issue rate from the committed SQ-counter summary, against the
+    measured v_fma_f32 issue rate of the chip; else None."""
+    valu = pmc_value(kernel, profile, "valu_instructions_per_launch")
+    if valu is None:
         return None
-    txt = open(path).read()
-    h = re.search(r"kernel_source_sha256:\s*([0-9a-f]+)", txt)
-    v = re.search(r"valu_instructions_per_launch:\s*([0-9.eE+]+)", txt)
-    if not h or not v or h.group(1) != kernel_source_hash():
-        return None
-    lane_ops = float(v.group(1)) * 64
+    lane_ops = valu * 64
     rate = lane_ops / (kernel_ms * 1e-3)
     peak = FMA_LANES_PER_CLK_CU * N_CU * CLOCK_HZ
     return {"valu_lane_ops_per_launch": lane_ops, "achieved_lane_ops_per_s": rate,
@@ -264,7 +269,7 @@ def main():
         "poly_path": dict(poly_cfg, ops=census["ops"], edges=census["edges"]),
         "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_TFLOPS,
-                     "traffic": pmc_traffic(profile),
+                     "traffic": pmc_traffic(dom, profile),
                      "kernel": dom, "kernel_ms": kern[dom]["ms"],
                      "model": f"{FMA_PER_OP_STEP:g} FMA + {TRANS_PER_OP_STEP:g} transcendental "
                               f"(x{TRANS_WEIGHT:.2f} FMA slots) per op-bin-edge, {FMA_PER_EDGE_STEP:g} FMA per "
@@ -272,7 +277,7 @@ def main():
                      "note": "k_poly reaches its op-bin-edges through per-chunk polynomial expansions and "
                              "needs fewer operations than this per-step model charges, so frac can exceed 1; "
                              "'issue' gives its measured VALU issue rate"},
-        "issue": pmc_issue(profile, kern[dom]["ms"]),
+        "issue": pmc_issue(dom, profile, kern[dom]["ms"]),
         "kernels": kern,
         "iteration_model_tflops_per_s": whole / (step_ms_events * 1e-3) / 1e12,
     }

@@ -1,0 +1,278 @@
+// Device-side helpers shared by the gfx950 kernels of the GauS hot path:
+// the normal CDF / density, signed-tail CDF values, wave and work-group
+// reductions, and the chunk-polynomial expansions.  Header-only, included by
+// every kernel source.
+#pragma once
+
+#include "gaus_internal.h"
+#include "gaus_erfcx_coeffs.h"
+
+namespace gaus {
+
+namespace {
+
+constexpr float kInvSqrt2 = 0.70710678118654752f;
+constexpr float kInvSqrt2Pi = 0.39894228040143268f;
+constexpr float kHalfLog2e = 0.72134752044448170f;  // log2(e)/2
+
+// Tail of the standard normal and the Gaussian factor: tail = Phi(-|z|),
+// g = exp(-z^2/2).  Phi(-|z|) = erfc(x)/2 with x = |z|/sqrt(2) and
+// erfc(x) = exp(-x^2) * t * Q(t), t = 1/(1 + p x), Q a fitted polynomial
+// (gaus_erfcx_coeffs.h).  exp(-x^2) equals g, which the gradient needs, so
+// both come from one exp.
+__device__ __forceinline__ void normal_tail_pdf(float z, float &tail, float &g) {
+    const float x = fabsf(z) * kInvSqrt2;
+    g = __builtin_amdgcn_exp2f(-(z * z) * kHalfLog2e);
+    const float t = __builtin_amdgcn_rcpf(fmaf(GAUS_ERFCX_P, x, 1.0f));
+    float q = gaus_erfcx_q[GAUS_ERFCX_DEG];
+#pragma unroll
+    for (int k = GAUS_ERFCX_DEG - 1; k >= 0; --k) q = fmaf(q, t, gaus_erfcx_q[k]);
+    tail = 0.5f * g * (t * q);
+}
+
+// A CDF value F is kept as a signed tail: +Phi(-|z|) below the median
+// (F = tail) and -Phi(-|z|) at or above it (F = 1 - tail; -0.0 for F = 1).
+// Differences of neighbouring CDF values (the masses P_i^d) are then formed
+// from tails, without the cancellation of 1 - F near F = 1.
+__device__ __forceinline__ bool st_upper(float st) { return __builtin_signbit(st); }
+__device__ __forceinline__ float st_F(float st) { return st_upper(st) ? 1.0f + st : st; }
+__device__ __forceinline__ float st_1mF(float st) { return st_upper(st) ? -st : 1.0f - st; }
+// F(hi) - F(lo) for bin edges lo < hi
+__device__ __forceinline__ float st_mass(float lo, float hi) {
+    const bool ul = st_upper(lo), uh = st_upper(hi);
+    if (ul) return hi - lo;                  // both above: tail(lo) - tail(hi)
+    if (!uh) return hi - lo;                 // both below: tail(hi) - tail(lo)
+    return (1.0f + hi) - lo;                 // straddles the median
+}
+
+// Signed-tail CDF and its derivatives at bin edge v of an op (mu, rs = 1/sigma,
+// cinv = 1/(sigma sqrt(2 pi))): dF/dmu = -phi(z)/sigma, dF/dsigma = -phi(z) z/sigma.
+// Outside the interior edges F is the constant 0 (v < 0) or 1 (v >= D-1).
+__device__ __forceinline__ void cdf_at(long long v, int D, float mu, float rs, float cinv, float &st,
+                                       float &Fm, float &Fs) {
+    if (v < 0) { st = 0.0f; Fm = 0.0f; Fs = 0.0f; return; }
+    if (v >= D - 1) { st = -0.0f; Fm = 0.0f; Fs = 0.0f; return; }
+    const float z = ((float)v + 0.5f - mu) * rs;
+    float tail, g;
+    normal_tail_pdf(z, tail, g);
+    st = (z >= 0.0f) ? -tail : tail;
+    Fm = -g * cinv;
+    Fs = Fm * z;
+}
+
+__device__ __forceinline__ float st_at(long long v, int D, float mu, float rs) {
+    if (v < 0) return 0.0f;
+    if (v >= D - 1) return -0.0f;
+    const float z = ((float)v + 0.5f - mu) * rs;
+    float tail, g;
+    normal_tail_pdf(z, tail, g);
+    return (z >= 0.0f) ? -tail : tail;
+}
+
+// Wave-wide sums with DPP lane moves (fused into the adds) inside rows of 16
+// lanes and the gfx950 lane-swap instructions across rows.
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float x) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+constexpr int kDppXor1 = 0xB1;        // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;        // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141;
+constexpr int kDppMirror = 0x140;
+constexpr int kDppRor4 = 0x124;
+constexpr int kDppRor8 = 0x128;
+
+// sum over lanes l, l^16, l^32, l^48 (LDS swizzle inside halves, LDS
+// permute across them); each pair is added in both lanes in the same order
+__device__ __forceinline__ float cross_rows_sum(float x) {
+    constexpr int kSwizzleXor16 = 0x1F | (0x10 << 10);   // bit mode: and 31, xor 16
+    x += __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), kSwizzleXor16));
+    const int lane = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+    x += __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute((lane ^ 32) << 2, __builtin_bit_cast(int, x)));
+    return x;
+}
+
+// Sum over the 64 lanes; every lane receives the same total.
+__device__ __forceinline__ float wave_sum(float x) {
+    x += dpp_mov<kDppXor1>(x);
+    x += dpp_mov<kDppXor2>(x);
+    x += dpp_mov<kDppHalfMirror>(x);
+    x += dpp_mov<kDppMirror>(x);
+    return cross_rows_sum(x);
+}
+
+// Four sums at once: lane l < 4 receives the total of value wave4_comp(l).
+__device__ __forceinline__ int wave4_comp(int lane) { return 2 * (lane & 1) + ((lane >> 1) & 1); }
+
+__device__ __forceinline__ float wave_sum4(float v0, float v1, float v2, float v3, int lane) {
+    const bool b0 = lane & 1, b1 = lane & 2;
+    const float a = (b0 ? v2 : v0) + dpp_mov<kDppXor1>(b0 ? v0 : v2);   // value 2*b0
+    const float c = (b0 ? v3 : v1) + dpp_mov<kDppXor1>(b0 ? v1 : v3);   // value 2*b0+1
+    float x = (b1 ? c : a) + dpp_mov<kDppXor2>(b1 ? a : c);             // value 2*b0+b1
+    x += dpp_mov<kDppRor4>(x);
+    x += dpp_mov<kDppRor8>(x);
+    return cross_rows_sum(x);
+}
+
+// Maximum over the 64 lanes; every lane receives it.
+__device__ __forceinline__ float wave_max(float x) {
+    x = fmaxf(x, dpp_mov<kDppXor1>(x));
+    x = fmaxf(x, dpp_mov<kDppXor2>(x));
+    x = fmaxf(x, dpp_mov<kDppHalfMirror>(x));
+    x = fmaxf(x, dpp_mov<kDppMirror>(x));
+    constexpr int kSwizzleXor16 = 0x1F | (0x10 << 10);
+    x = fmaxf(x, __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), kSwizzleXor16)));
+    const int lane = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+    return fmaxf(x, __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute((lane ^ 32) << 2, __builtin_bit_cast(int, x))));
+}
+
+// Two sums at once: lane l < 2 receives the total of value l.
+__device__ __forceinline__ float wave_sum2(float v0, float v1, int lane) {
+    const bool b0 = lane & 1;
+    float x = (b0 ? v1 : v0) + dpp_mov<kDppXor1>(b0 ? v0 : v1);
+    x += dpp_mov<kDppXor2>(x);
+    x += dpp_mov<kDppRor4>(x);
+    x += dpp_mov<kDppRor8>(x);
+    return cross_rows_sum(x);
+}
+
+// Sum NV values over the work-group; thread c < NV receives total c.
+// slot: LDS scratch [NW][8]; callers alternate between two slots so that only
+// one barrier per reduction is needed.
+template <int NV, int BS>
+__device__ __forceinline__ float block_sum(float (&v)[NV], float (*slot)[8]) {
+    constexpr int NW = BS / 64;
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+#pragma unroll
+    for (int c = 0; c < NV; ++c) v[c] = wave_sum(v[c]);
+    if (lane == 0) {
+#pragma unroll
+        for (int c = 0; c < NV; ++c) slot[wid][c] = v[c];
+    }
+    __syncthreads();
+    float r = 0.0f;
+    if (threadIdx.x < NV) {
+#pragma unroll
+        for (int w = 0; w < NW; ++w) r += slot[w][threadIdx.x];
+    }
+    return r;
+}
+
+__device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+
+
+struct Expansion {
+    float T[kTN];   // Taylor coefficients in y, T[0] = F(z0)
+    float G0;       // 1 - F(z0), from the tail
+    float z0, r;
+};
+
+constexpr double binom_d(int n, int k) {
+    double v = 1.0;
+    for (int q = 1; q <= k; ++q) v = v * (double)(n - k + q) / (double)q;
+    return v;
+}
+// coefficient of T_{k+j} in the mass coefficient m_k (j >= 1)
+constexpr float mass_coef(int k, int j) { return (float)(-binom_d(k + j, j) * ((j & 1) ? -1.0 : 1.0)); }
+// coefficient of T_{k+1+j} in dF/dmu one step back, a1_k (j >= 0)
+constexpr float back_coef(int k, int j) {
+    return (float)(-(double)(k + j + 1) * binom_d(k + j, j) * ((j & 1) ? -1.0 : 1.0));
+}
+
+__device__ __forceinline__ void expand(float mu, float rs, float tcen, Expansion &e) {
+    e.r = rs;
+    e.z0 = (tcen + 0.5f - mu) * rs;
+    float tail, g;
+    normal_tail_pdf(e.z0, tail, g);
+    const bool up = e.z0 >= 0.0f;
+    e.T[0] = up ? 1.0f - tail : tail;
+    e.G0 = up ? tail : 1.0f - tail;
+    e.T[1] = g * (kInvSqrt2Pi * rs);
+    const float zr = e.z0 * rs, r2 = rs * rs;
+    e.T[2] = (zr * -0.5f) * e.T[1];
+#pragma unroll
+    for (int n = 2; n < kTN - 1; ++n) {
+        const float c1 = -1.0f / (float)(n + 1);
+        const float c2 = -(float)(n - 1) / (float)(n * (n + 1));
+        e.T[n + 1] = fmaf(zr * c1, e.T[n], (r2 * c2) * e.T[n - 1]);
+    }
+}
+
+__device__ __forceinline__ void vec_dFdmu(const Expansion &e, float (&a)[kNC]) {
+#pragma unroll
+    for (int k = 0; k < kNC; ++k) a[k] = -(float)(k + 1) * e.T[k + 1];
+}
+
+__device__ __forceinline__ void vec_times_z(const float (&a)[kNC], float zc, float r, float (&o)[kNC]) {
+    o[0] = zc * a[0];
+#pragma unroll
+    for (int k = 1; k < kNC; ++k) o[k] = fmaf(zc, a[k], r * a[k - 1]);
+}
+
+__device__ __forceinline__ void vec_mass(const Expansion &e, float (&m)[kNC]) {
+#pragma unroll
+    for (int k = 0; k < kNC; ++k) {
+        float acc = 0.0f;
+#pragma unroll
+        for (int j = kShiftTerms; j >= 1; --j) acc = fmaf(mass_coef(k, j), e.T[k + j], acc);
+        m[k] = acc;
+    }
+}
+
+__device__ __forceinline__ void vec_dFdmu_back(const Expansion &e, float (&a)[kNC]) {
+#pragma unroll
+    for (int k = 0; k < kNC; ++k) {
+        float acc = 0.0f;
+#pragma unroll
+        for (int j = kShiftTerms; j >= 0; --j) acc = fmaf(back_coef(k, j), e.T[k + 1 + j], acc);
+        a[k] = acc;
+    }
+}
+
+// (H p)_k = sum_l H_{k+l} p_l; the chunk points are symmetric, odd moments vanish
+__device__ __forceinline__ void vec_moments(const float (&p)[kNC], const PolyArgs &pa, float (&o)[kNC]) {
+#pragma unroll
+    for (int k = 0; k < kNC; ++k) {
+        float acc = 0.0f;
+#pragma unroll
+        for (int l = 0; l < kNC; ++l)
+            if (((k + l) & 1) == 0) acc = fmaf(pa.H[(k + l) / 2], p[l], acc);
+        o[k] = acc;
+    }
+}
+
+__device__ __forceinline__ float vdot(const float (&a)[kNC], const float (&b)[kNC]) {
+    float acc = 0.0f;
+#pragma unroll
+    for (int k = 0; k < kNC; ++k) acc = fmaf(a[k], b[k], acc);
+    return acc;
+}
+
+// dot with 1 - F given F's coefficients and the precise 1 - F(z0)
+__device__ __forceinline__ float vdot_1mF(const float (&a)[kNC], const Expansion &e) {
+    float acc = a[0] * e.G0;
+#pragma unroll
+    for (int k = 1; k < kNC; ++k) acc = fmaf(-a[k], e.T[k], acc);
+    return acc;
+}
+
+__device__ __forceinline__ float vdot_F(const float (&a)[kNC], const Expansion &e) {
+    float acc = 0.0f;
+#pragma unroll
+    for (int k = 0; k < kNC; ++k) acc = fmaf(a[k], e.T[k], acc);
+    return acc;
+}
+
+// weight difference c(t) - c(t+1) of a per-slot table folded mod T
+__device__ __forceinline__ float soft_diff(const float *sk, int t, int T) {
+    return sk[t % T] - sk[(t + 1) % T];
+}
+
+}  // namespace
+
+constexpr int kPolyWaves = 4;
+constexpr int kStripPassesMax = (kStripMax + 63) / 64;
+constexpr int kOpsPerWaveMax = 64;              // group size <= kPolyWaves * 64
+
+}  // namespace gaus

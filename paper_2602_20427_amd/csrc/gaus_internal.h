@@ -124,6 +124,18 @@ struct IterArgs {
 hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const LaunchCfg &lc,
                              const PolyArgs &pa, const IterArgs &a, hipStream_t st);
 
+// Per-step kernels (gaus_step.hip: step by step; gaus_poly.hip: chunk polynomials).
+hipError_t launch_ops(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu, const float *sigma,
+                      hipStream_t st);
+hipError_t launch_back(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu, const float *sigma,
+                       hipStream_t st);
+hipError_t launch_lse_ops(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu,
+                          const float *sigma, hipStream_t st);
+hipError_t launch_poly(const Graph &g, const Work &w, const PolyArgs &pa, const float *mu, const float *sigma,
+                       hipStream_t st);
+hipError_t launch_lse_poly(const Graph &g, const Work &w, const PolyArgs &pa, const float *mu,
+                           const float *sigma, hipStream_t st);
+
 // Adam + sigma clamp + lambda += rho*V (from terms) + adam_t++ from a given gradient.
 hipError_t enqueue_adam_from_grad(const Graph &g, const Work &w, const HP &hp, const float *gmu,
                                   const float *gsig, const float *terms, float *mu, float *sigma,

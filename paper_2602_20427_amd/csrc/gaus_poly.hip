@@ -1,0 +1,380 @@
+// gfx950 kernels of the chunk-polynomial evaluation (dense regime): k_poly
+// (forward terms, usage coefficients and the edge derivatives of ops whose
+// width allows it) and k_lse_mom / k_lse_poly (gradient of the smooth peak
+// usage for those ops).  The method is described at k_classify in
+// gaus_kernels.hip.
+#include "gaus_device.h"
+
+namespace gaus {
+
+
+// Work-group = (op group, restart), kPolyWaves waves; each wave takes the
+// group's ops in turn.  For a polynomial op: lanes = strip positions for the
+// step-by-step part, lanes = chunks for the polynomial part; per polynomial
+// out-edge the consumer-side derivatives of both parts are reduced together.
+// NP: strip passes of 64 lanes, ceil(SP / 64).
+template <int NP>
+__global__ __launch_bounds__(64 * kPolyWaves) __attribute__((amdgpu_waves_per_eu(3)))
+void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__restrict__ sigma, Work W) {
+    // dynamic LDS: per wave 7 rows of SP strip values, then per wave SP strip usages
+    extern __shared__ float sDyn[];
+    __shared__ float sUc[kPolyWaves][kMaxChunks][kNC];
+    __shared__ float sGs[kPolyWaves][2];
+    const int SP = pa.SP, split = pa.split;
+    const int grp = blockIdx.x / split, sub = blockIdx.x - grp * split, b = blockIdx.y;
+    const size_t slot_id = ((size_t)b * G.ngroups + grp) * split + sub;   // per-work-group outputs
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int N = G.N, D = G.D;
+    const float *mub = mu + (size_t)b * N;
+    const float *sgb = sigma + (size_t)b * N;
+    const unsigned char *clsb = W.cls + (size_t)b * N;
+    const bool cact = lane < pa.nc;
+    const float tcen = (float)(pa.L0 + lane * pa.W) + pa.lam;
+
+    float uc[kNC];
+#pragma unroll
+    for (int k = 0; k < kNC; ++k) uc[k] = 0.0f;
+    float us[NP];
+#pragma unroll
+    for (int ps = 0; ps < NP; ++ps) us[ps] = 0.0f;
+    float *own = sDyn + (size_t)wv * 7 * SP;
+    float *sUs = sDyn + (size_t)kPolyWaves * 7 * SP;
+
+    // the work-group's ops are q = q0 + sub + split*j; this wave's are
+    // j = wv + kPolyWaves*l, parameters loaded by lane l
+    const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
+    const int nj = (q1 - q0 - sub + split - 1) / split;
+    const int nq = (nj - wv + kPolyWaves - 1) / kPolyWaves;
+    int l_i = 0, l_cls = 0, l_s = 0, l_e0 = 0, l_e1 = 0;
+    float l_mu = 0.0f, l_sg = 1.0f;
+    if (lane < nq) {
+        l_i = G.perm[q0 + sub + split * (wv + kPolyWaves * lane)];
+        l_cls = clsb[l_i];
+        l_mu = mub[l_i]; l_sg = sgb[l_i];
+        l_s = G.delay[l_i];
+        l_e0 = G.row_ptr[l_i]; l_e1 = G.row_ptr[l_i + 1];
+    }
+    float gsum = 0.0f;  // V_dep, L_com of this wave's ops (lanes 0 and 2)
+    for (int oq = 0; oq < nq; ++oq) {
+        const int i = __builtin_amdgcn_readlane(l_i, oq);
+        float *pp = W.ppoly + ((size_t)b * N + i) * kPP;
+        if (!__builtin_amdgcn_readlane(l_cls, oq)) {
+            if (lane < kPP) pp[lane] = 0.0f;
+            continue;
+        }
+        const float m_i = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, l_mu), oq));
+        const float s_i = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, l_sg), oq));
+        const float rs = 1.0f / s_i, cinv = rs * kInvSqrt2Pi;
+        const int s = __builtin_amdgcn_readlane(l_s, oq);
+        const int e0 = __builtin_amdgcn_readlane(l_e0, oq), e1 = __builtin_amdgcn_readlane(l_e1, oq);
+        float pr[kPP] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+        // the op's polynomial out-edges, loaded by lane (batches of 64)
+        int x_j = 0, x_ok = 0;
+        float x_mu = 0.0f, x_sg = 1.0f;
+
+        // (1) strip: own CDF values per position, kept in this wave's LDS rows
+#pragma unroll
+        for (int ps = 0; ps < NP; ++ps) {
+            const int p = ps * 64 + lane;
+            if (p < SP) {
+                const int u = p < pa.L0 ? p : D - 2 + (p - pa.L0);
+                float st, Fm, Fs, st0, Fm0, Fs0;
+                cdf_at(u, D, m_i, rs, cinv, st, Fm, Fs);
+                us[ps] += st_mass(st_at((long long)u - 1, D, m_i, rs), st);
+                cdf_at((long long)u - s, D, m_i, rs, cinv, st0, Fm0, Fs0);
+                const float st1 = st_at((long long)u - s + 1, D, m_i, rs);
+                own[0 * SP + p] = st_F(st);
+                own[1 * SP + p] = Fm;
+                own[2 * SP + p] = Fs;
+                own[3 * SP + p] = st_mass(st0, st1);
+                own[4 * SP + p] = Fm0;
+                own[5 * SP + p] = Fs0;
+                own[6 * SP + p] = st_1mF(st0);
+            }
+        }
+
+        // (2) chunk: producer vectors multiplied by the chunk moments
+        float HF[kNC], HFm[kNC], HFs[kNC], HA[kNC], HFm1[kNC], HFs1[kNC];
+        if (cact) {
+            Expansion ea;
+            expand(m_i, rs, tcen, ea);
+            float v[kNC], w[kNC];
+            vec_mass(ea, v);
+#pragma unroll
+            for (int k = 0; k < kNC; ++k) uc[k] += v[k];
+#pragma unroll
+            for (int k = 0; k < kNC; ++k) w[k] = ea.T[k];
+            vec_moments(w, pa, HF);
+            vec_dFdmu(ea, v);
+            vec_moments(v, pa, HFm);
+            vec_times_z(v, ea.z0, ea.r, w);
+            vec_moments(w, pa, HFs);
+            // shifted functions: A(u) = mass at u-s+1, dF(u-s)
+            Expansion es;
+            if (s != 1) expand(m_i, rs, tcen - (float)(s - 1), es);
+            const Expansion &ex = (s != 1) ? es : ea;
+            vec_mass(ex, v);
+            vec_moments(v, pa, HA);
+            vec_dFdmu_back(ex, v);
+            vec_moments(v, pa, HFm1);
+            vec_times_z(v, ex.z0 - rs, ex.r, w);
+            vec_moments(w, pa, HFs1);
+        } else {
+#pragma unroll
+            for (int k = 0; k < kNC; ++k) { HF[k] = HFm[k] = HFs[k] = HA[k] = HFm1[k] = HFs1[k] = 0.0f; }
+        }
+
+        // (3) polynomial out-edges
+        for (int e = e0; e < e1; ++e) {
+            const int eb = (e - e0) & 63;
+            if (eb == 0) {
+                x_ok = 0;
+                if (e + lane < e1) {
+                    x_j = G.col[e + lane];
+                    x_ok = clsb[x_j];
+                    x_mu = mub[x_j]; x_sg = sgb[x_j];
+                }
+            }
+            if (!__builtin_amdgcn_readlane(x_ok, eb)) continue;  // step-by-step edge, done by k_ops
+            const float m_j = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x_mu), eb));
+            const float s_j = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x_sg), eb));
+            const float rsj = 1.0f / s_j, cj = rsj * kInvSqrt2Pi;
+            float cc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int ps = 0; ps < NP; ++ps) {
+                const int p = ps * 64 + lane;
+                if (p < SP) {
+                    const int u = p < pa.L0 ? p : D - 2 + (p - pa.L0);
+                    float stj, Fmj, Fsj;
+                    cdf_at(u, D, m_j, rsj, cj, stj, Fmj, Fsj);
+                    const float Pj = st_mass(st_at((long long)u - 1, D, m_j, rsj), stj);
+                    const float F = own[0 * SP + p], Fm = own[1 * SP + p];
+                    const float Fs = own[2 * SP + p], A = own[3 * SP + p];
+                    pr[2] = fmaf(-own[4 * SP + p], Pj, pr[2]);
+                    pr[3] = fmaf(-own[5 * SP + p], Pj, pr[3]);
+                    if (u < D - 1) {
+                        const float omF = st_1mF(stj);
+                        pr[0] = fmaf(A, st_F(stj), pr[0]);
+                        pr[1] = fmaf(F, omF, pr[1]);
+                        pr[4] = fmaf(Fm, omF, pr[4]);
+                        pr[5] = fmaf(Fs, omF, pr[5]);
+                        cc[0] = fmaf(A, Fmj, cc[0]);
+                        cc[1] = fmaf(A, Fsj, cc[1]);
+                        cc[2] = fmaf(-F, Fmj, cc[2]);
+                        cc[3] = fmaf(-F, Fsj, cc[3]);
+                    } else {
+                        pr[0] += own[6 * SP + p];
+                    }
+                }
+            }
+            if (cact) {
+                Expansion ej;
+                expand(m_j, rsj, tcen, ej);
+                float a[kNC], v[kNC];
+                pr[0] += vdot_F(HA, ej);
+                pr[1] += vdot_1mF(HF, ej);
+                pr[4] += vdot_1mF(HFm, ej);
+                pr[5] += vdot_1mF(HFs, ej);
+                vec_dFdmu(ej, a);
+                cc[0] += vdot(HA, a);
+                cc[2] -= vdot(HF, a);
+                vec_times_z(a, ej.z0, ej.r, v);
+                cc[1] += vdot(HA, v);
+                cc[3] -= vdot(HF, v);
+                vec_mass(ej, v);
+                pr[2] -= vdot(HFm1, v);
+                pr[3] -= vdot(HFs1, v);
+            }
+            const float ct = wave_sum4(cc[0], cc[1], cc[2], cc[3], lane);
+            if (lane < kCP) W.cpoly[((size_t)b * G.E + e) * kCP + wave4_comp(lane)] = ct;
+        }
+        const float pt4 = wave_sum4(pr[0], pr[1], pr[2], pr[3], lane);
+        const float pt2 = wave_sum2(pr[4], pr[5], lane);
+        if (lane < 4) pp[wave4_comp(lane)] = pt4;
+        if (lane < 2) pp[4 + lane] = pt2;
+        gsum += pt4;   // lane 0: V_dep, lane 2: L_com
+    }
+    if (lane == 0) sGs[wv][0] = gsum;
+    if (lane == 2) sGs[wv][1] = gsum;
+
+    // usage of the group: combine the waves' chunk coefficients and strip values
+#pragma unroll
+    for (int k = 0; k < kNC; ++k) sUc[wv][lane][k] = uc[k];
+#pragma unroll
+    for (int ps = 0; ps < NP; ++ps) {
+        const int p = ps * 64 + lane;
+        if (p < SP) sUs[wv * SP + p] = us[ps];
+    }
+    __syncthreads();
+    float *ucg = W.Ucoef + slot_id * kMaxChunks * kNC;
+    for (int x = threadIdx.x; x < kMaxChunks * kNC; x += 64 * kPolyWaves) {
+        const int c = x / kNC, k = x % kNC;
+        float acc = 0.0f;
+#pragma unroll
+        for (int w = 0; w < kPolyWaves; ++w) acc += sUc[w][c][k];
+        ucg[x] = acc;
+    }
+    if (threadIdx.x < 2) {
+        float acc = 0.0f;
+#pragma unroll
+        for (int w = 0; w < kPolyWaves; ++w) acc += sGs[w][threadIdx.x];
+        W.gsum_poly[slot_id * 2 + threadIdx.x] = acc;
+    }
+    float *usg = W.Ustrip + slot_id * kStripMax;
+    for (int p = threadIdx.x; p < kStripMax; p += 64 * kPolyWaves) {
+        float acc = 0.0f;
+        if (p < SP) {
+#pragma unroll
+            for (int w = 0; w < kPolyWaves; ++w) acc += sUs[w * SP + p];
+        }
+        usg[p] = acc;
+    }
+}
+
+
+// ---------------------------------------------------------------------------
+// Gradient of the smooth peak usage.  With c_k(d) = beta dL_res/dU_k(d mod T)
+// (the softmax written by k_vres), summation by parts onto the interior bin
+// edges gives
+//   dL/dth_i += sum_{t=0}^{D-2} (c(t) - c(t+1)) dF_i(t)/dth_i,
+// a dense weight per bin edge.  Step-by-step ops take it per step
+// (k_lse_ops); polynomial ops take it per chunk as the moments
+// M_n = sum_y (c(t) - c(t+1)) y^n (k_lse_mom), dotted with the chunk
+// coefficients of dF/dmu and dF/dsigma (k_lse_poly).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_lse_mom(Graph G, PolyArgs pa, Work W) {
+    __shared__ float sRed[4][kNC];
+    const int c = blockIdx.x, k = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
+    const int lane = tid & 63, wid = tid >> 6;
+    const int T = G.T, D = G.D;
+    const float *sk = W.soft + ((size_t)b * G.K + k) * T;
+    if (c == pa.nc) {   // the strip: weights per position (none at D-1, not a bin edge)
+        float *dst = W.lstrip + ((size_t)b * G.K + k) * kStripMax;
+        for (int p = tid; p < pa.SP; p += 256) {
+            const int u = p < pa.L0 ? p : D - 2 + (p - pa.L0);
+            dst[p] = u <= D - 2 ? soft_diff(sk, u, T) : 0.0f;
+        }
+        return;
+    }
+    float mom[kNC];
+#pragma unroll
+    for (int n = 0; n < kNC; ++n) mom[n] = 0.0f;
+    if (tid < pa.W) {
+        const int t = pa.L0 + c * pa.W + tid;
+        const float y = (float)tid - pa.lam;
+        float yp = soft_diff(sk, t, T);
+#pragma unroll
+        for (int n = 0; n < kNC; ++n) { mom[n] = yp; yp *= y; }
+    }
+#pragma unroll
+    for (int n = 0; n < kNC; ++n) {
+        const float r = wave_sum(mom[n]);
+        if (lane == 0) sRed[wid][n] = r;
+    }
+    __syncthreads();
+    if (tid < kNC)
+        W.lmom[(((size_t)b * G.K + k) * kMaxChunks + c) * kNC + tid] =
+            (sRed[0][tid] + sRed[1][tid]) + (sRed[2][tid] + sRed[3][tid]);
+}
+
+
+template <int NP>
+__global__ __launch_bounds__(64 * kPolyWaves) void k_lse_poly(Graph G, PolyArgs pa, const float *__restrict__ mu,
+                                                              const float *__restrict__ sigma, Work W) {
+    const int SP = pa.SP, split = pa.split;
+    const int grp = blockIdx.x / split, sub = blockIdx.x - grp * split, b = blockIdx.y;
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int N = G.N, D = G.D;
+    const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
+    if (q1 <= q0) return;
+    const int nj = (q1 - q0 - sub + split - 1) / split;
+    const int nq = (nj - wv + kPolyWaves - 1) / kPolyWaves;
+    int l_i = 0, l_cls = 0;
+    float l_mu = 0.0f, l_sg = 1.0f;
+    if (lane < nq) {
+        l_i = G.perm[q0 + sub + split * (wv + kPolyWaves * lane)];
+        const size_t bi = (size_t)b * N + l_i;
+        l_cls = W.cls[bi];
+        l_mu = mu[bi]; l_sg = sigma[bi];
+    }
+    // this lane's chunk moments and strip weights of the group's type
+    const int k = G.rtype[G.perm[q0]];
+    const bool cact = lane < pa.nc;
+    float mom[kNC];
+    const float *msrc = W.lmom + (((size_t)b * G.K + k) * kMaxChunks + lane) * kNC;
+#pragma unroll
+    for (int n = 0; n < kNC; ++n) mom[n] = cact ? msrc[n] : 0.0f;
+    float sw[NP];
+    const float *ssrc = W.lstrip + ((size_t)b * G.K + k) * kStripMax;
+#pragma unroll
+    for (int ps = 0; ps < NP; ++ps) {
+        const int p = ps * 64 + lane;
+        sw[ps] = p < SP ? ssrc[p] : 0.0f;
+    }
+    const float tcen = (float)(pa.L0 + lane * pa.W) + pa.lam;
+    for (int oq = 0; oq < nq; ++oq) {
+        if (!__builtin_amdgcn_readlane(l_cls, oq)) continue;
+        const int i = __builtin_amdgcn_readlane(l_i, oq);
+        const float m_i = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, l_mu), oq));
+        const float s_i = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, l_sg), oq));
+        const float rs = 1.0f / s_i, cinv = rs * kInvSqrt2Pi;
+        float gm = 0.0f, gs = 0.0f;
+#pragma unroll
+        for (int ps = 0; ps < NP; ++ps) {
+            const int p = ps * 64 + lane;
+            if (p < SP) {
+                const int u = p < pa.L0 ? p : D - 2 + (p - pa.L0);
+                const float z = ((float)u + 0.5f - m_i) * rs;
+                const float Fm = -__builtin_amdgcn_exp2f(-(z * z) * kHalfLog2e) * cinv;
+                gm = fmaf(sw[ps], Fm, gm);
+                gs = fmaf(sw[ps], Fm * z, gs);
+            }
+        }
+        if (cact) {
+            Expansion e;
+            expand(m_i, rs, tcen, e);
+            float a[kNC], v[kNC];
+            vec_dFdmu(e, a);
+            vec_times_z(a, e.z0, e.r, v);
+            gm += vdot(a, mom);
+            gs += vdot(v, mom);
+        }
+        const float r = wave_sum2(gm, gs, lane);
+        if (lane < 2) W.lpoly[((size_t)b * N + i) * 2 + lane] = r;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Launchers
+// ---------------------------------------------------------------------------
+hipError_t launch_poly(const Graph &g, const Work &w, const PolyArgs &pa, const float *mu, const float *sigma,
+                       hipStream_t st) {
+    const size_t lds = sizeof(float) * (size_t)kPolyWaves * 8 * pa.SP;
+    const dim3 grid(g.ngroups * pa.split, g.B), block(64 * kPolyWaves);
+    switch ((pa.SP + 63) / 64) {
+    case 1: hipLaunchKernelGGL(k_poly<1>, grid, block, lds, st, g, pa, mu, sigma, w); break;
+    case 2: hipLaunchKernelGGL(k_poly<2>, grid, block, lds, st, g, pa, mu, sigma, w); break;
+    case 3: hipLaunchKernelGGL(k_poly<3>, grid, block, lds, st, g, pa, mu, sigma, w); break;
+    case 4: hipLaunchKernelGGL(k_poly<4>, grid, block, lds, st, g, pa, mu, sigma, w); break;
+    case kStripPassesMax: hipLaunchKernelGGL(k_poly<kStripPassesMax>, grid, block, lds, st, g, pa, mu, sigma, w); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipSuccess;
+}
+
+hipError_t launch_lse_poly(const Graph &g, const Work &w, const PolyArgs &pa, const float *mu,
+                           const float *sigma, hipStream_t st) {
+    hipLaunchKernelGGL(k_lse_mom, dim3(pa.nc + 1, g.K, g.B), dim3(256), 0, st, g, pa, w);
+    const dim3 grid(g.ngroups * pa.split, g.B), block(64 * kPolyWaves);
+    switch ((pa.SP + 63) / 64) {
+    case 1: hipLaunchKernelGGL(k_lse_poly<1>, grid, block, 0, st, g, pa, mu, sigma, w); break;
+    case 2: hipLaunchKernelGGL(k_lse_poly<2>, grid, block, 0, st, g, pa, mu, sigma, w); break;
+    case 3: hipLaunchKernelGGL(k_lse_poly<3>, grid, block, 0, st, g, pa, mu, sigma, w); break;
+    case 4: hipLaunchKernelGGL(k_lse_poly<4>, grid, block, 0, st, g, pa, mu, sigma, w); break;
+    case kStripPassesMax: hipLaunchKernelGGL(k_lse_poly<kStripPassesMax>, grid, block, 0, st, g, pa, mu, sigma, w); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipSuccess;
+}
+
+}  // namespace gaus

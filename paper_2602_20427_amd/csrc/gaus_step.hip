@@ -1,0 +1,374 @@
+// gfx950 kernels of the step-by-step evaluation: every (restart, op, step)
+// evaluated directly (k_ops for the forward edges, k_back for back edges,
+// k_lse_ops for the gradient of the smooth peak usage).  See gaus_kernels.hip
+// for the notation.
+#include "gaus_device.h"
+
+namespace gaus {
+
+// ---------------------------------------------------------------------------
+// Op kernel.  Work-group = (op group, step tile, restart).  Threads own steps
+// u = t0 + k*BS + tid (k < SPT).  For each op i of the group (all of one
+// resource type, out-degree m, delay s = Lat(v_i)):
+//   * its CDF row over the tile plus a left halo of s steps goes to LDS; the
+//     mass P_i^u is added to the group's usage;
+//   * for each out-edge (i -> j) the consumer's CDF and Gaussian factor are
+//     evaluated once per step.  The consumer-side derivatives of this edge are
+//       dVdep/dth_j = sum_u A(u) F_j'(u),   A(u) = P_i^{u-s+1}
+//       dLcom/dth_j = -sum_u F_i(u) F_j'(u)
+//     and the successor CDF sum S_i(u) = sum_j F_j(u) is accumulated split
+//     into lower-side CDFs, upper tails and a count of successors past their
+//     median, so that S_i, m - S_i and S_i(u) - S_i(u-1) keep full precision;
+//   * after the out-edges the producer-side terms follow from S_i:
+//       V_dep          = sum_u A(u) S_i(u) + m (1 - F_i(D-1-s))
+//       L_com          = sum_u F_i(u) (m - S_i(u))
+//       dVdep/dth_i    = -sum_u F_i'(u-s) (S_i(u) - S_i(u-1))
+//       dLcom/dth_i    = sum_u F_i'(u) (m - S_i(u))
+//     (u over the interior edges 0..D-2 except in dVdep/dth_i, which runs to
+//     u = D-1 with S_i(D-1) = m: the consumers' bin D-1 is open to +inf).
+// ---------------------------------------------------------------------------
+template <int BS, int SPT>
+__global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ mu,
+                                            const float *__restrict__ sigma, Work W) {
+    constexpr int TILE = BS * SPT;
+    constexpr int WIN = TILE + kHalo + 1;
+    __shared__ float sT[WIN], sFm[WIN], sFs[WIN];
+    __shared__ float sRed[2][BS / 64][8];
+    __shared__ float sPrev[3];
+
+    const int grp = blockIdx.x, tile = blockIdx.y, b = blockIdx.z;
+    const int tid = threadIdx.x;
+    const int D = G.D, N = G.N;
+    const int t0 = tile * TILE;
+    const float *mub = mu + (size_t)b * N;
+    const float *sgb = sigma + (size_t)b * N;
+
+    const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
+    float accU[SPT];
+#pragma unroll
+    for (int k = 0; k < SPT; ++k) accU[k] = 0.0f;
+    int par = 0;
+
+    // Groups without step-by-step work leave nothing here: their readers skip
+    // them (group and op flags).  Otherwise thread t looks at op q0+t (groups
+    // hold at most as many ops as the work-group has threads); ops and edges
+    // on the chunk-polynomial path are left to k_poly.
+    if (!W.gflag[(size_t)b * G.ngroups + grp]) return;
+    __shared__ int sDirect[BS];   // 0: nothing; else 1 + number of step-by-step out-edges
+    const unsigned char *clsb = W.cls + (size_t)b * N;
+    {
+        int flag = 0;
+        if (q0 + tid < q1) {
+            const int i = G.perm[q0 + tid];
+            if (W.dflag[(size_t)b * N + i]) {
+                const int e0 = G.row_ptr[i], e1 = G.row_ptr[i + 1];
+                const bool poly_i = clsb[i] != 0;
+                int m = 0;
+                for (int e = e0; e < e1; ++e) m += (poly_i && clsb[G.col[e]]) ? 0 : 1;
+                flag = 1 + m;
+            }
+        }
+        sDirect[tid] = flag;
+    }
+    float gsum0 = 0.0f, gsum1 = 0.0f;  // V_dep, L_com of the work-group (threads 0, 1)
+    __syncthreads();
+
+    for (int q = q0; q < q1; ++q) {
+        const int flag = sDirect[q - q0];
+        if (flag == 0) continue;
+        const int i = uniform(G.perm[q]);
+        const int e0 = uniform(G.row_ptr[i]), e1 = uniform(G.row_ptr[i + 1]);
+        const bool poly_i = clsb[i] != 0;
+        const int m = uniform(flag - 1);
+        const float m_i = mub[i], s_i = sgb[i];
+        const float rs = 1.0f / s_i;
+        const float cinv = rs * kInvSqrt2Pi;
+        const int s = uniform(G.delay[i]);
+        const bool win_shift = (m > 0) && (s <= kHalo);
+        const int Lh = win_shift ? (s > 1 ? s : 1) : 1;
+
+        // row window: positions v = t0 - Lh + p, p in [0, TILE + Lh]
+        for (int p = tid; p < TILE + Lh + 1; p += BS) {
+            float st, Fm, Fs;
+            cdf_at(t0 - Lh + p, D, m_i, rs, cinv, st, Fm, Fs);
+            sT[p] = st; sFm[p] = Fm; sFs[p] = Fs;
+        }
+        __syncthreads();
+
+        float rF[SPT], rFm[SPT], rFs[SPT], rA[SPT], rFms[SPT], rFss[SPT];
+        float tail1mF = 0.0f;  // 1 - F_i(D-1-s), held by the thread owning u = D-1
+#pragma unroll
+        for (int k = 0; k < SPT; ++k) {
+            const int u = t0 + k * BS + tid;
+            const int p = u - t0 + Lh;
+            rF[k] = st_F(sT[p]); rFm[k] = sFm[p]; rFs[k] = sFs[p];
+            if (u < D && !poly_i) accU[k] += st_mass(sT[p - 1], sT[p]);
+            rA[k] = 0.0f; rFms[k] = 0.0f; rFss[k] = 0.0f;
+            if (m > 0 && u < D) {
+                if (win_shift) {
+                    rA[k] = st_mass(sT[p - s], sT[p - s + 1]);
+                    rFms[k] = sFm[p - s]; rFss[k] = sFs[p - s];
+                    if (u == D - 1) tail1mF = st_1mF(sT[p - s]);
+                } else {
+                    float st0, Fm0, Fs0, st1, Fm1, Fs1;
+                    cdf_at((long long)u - s, D, m_i, rs, cinv, st0, Fm0, Fs0);
+                    cdf_at((long long)u - s + 1, D, m_i, rs, cinv, st1, Fm1, Fs1);
+                    rA[k] = st_mass(st0, st1); rFms[k] = Fm0; rFss[k] = Fs0;
+                    if (u == D - 1) tail1mF = st_1mF(st0);
+                }
+            }
+        }
+        __syncthreads();  // the window may be overwritten from here on
+
+        float SL[SPT], SU[SPT], SC[SPT];
+#pragma unroll
+        for (int k = 0; k < SPT; ++k) { SL[k] = 0.0f; SU[k] = 0.0f; SC[k] = 0.0f; }
+        float pL = 0.0f, pU = 0.0f, pC = 0.0f;   // S_i(t0-1), thread 0 only
+
+        for (int e = e0; e < e1; ++e) {
+            const int j = uniform(G.col[e]);
+            if (poly_i && clsb[j]) continue;  // polynomial edge
+            const float m_j = mub[j], s_j = sgb[j];
+            const float rsj = 1.0f / s_j;
+            float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int k = 0; k < SPT; ++k) {
+                const int u = t0 + k * BS + tid;
+                if (u < D - 1) {
+                    const float z = ((float)u + 0.5f - m_j) * rsj;
+                    float tl, gj;
+                    normal_tail_pdf(z, tl, gj);
+                    const bool up = z >= 0.0f;
+                    SL[k] += up ? 0.0f : tl;
+                    SU[k] += up ? tl : 0.0f;
+                    SC[k] += up ? 1.0f : 0.0f;
+                    const float gz = gj * z;
+                    acc[0] = fmaf(rA[k], gj, acc[0]);
+                    acc[1] = fmaf(rA[k], gz, acc[1]);
+                    acc[2] = fmaf(rF[k], gj, acc[2]);
+                    acc[3] = fmaf(rF[k], gz, acc[3]);
+                }
+            }
+            if (tid == 0 && t0 > 0) {
+                const float z = ((float)(t0 - 1) + 0.5f - m_j) * rsj;
+                float tl, gj;
+                normal_tail_pdf(z, tl, gj);
+                if (z >= 0.0f) { pU += tl; pC += 1.0f; } else { pL += tl; }
+            }
+            const float r = block_sum<4, BS>(acc, sRed[par]);
+            par ^= 1;
+            if (tid < 4) {
+                // F_j'(u) = -g_j/(sigma_j sqrt(2 pi)) [* z for sigma]; L_com enters with a minus
+                const float cj = rsj * kInvSqrt2Pi;
+                const float val = (tid < 2) ? -cj * r : cj * r;
+                W.cpart[(((size_t)b * G.E + e) * G.ntiles + tile) * kCP + tid] = val;
+            }
+        }
+
+        float pr[6] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+        if (m > 0) {
+            const float mf = (float)m;
+            // S_i(D-1) = m: every consumer is at or before step D-1
+#pragma unroll
+            for (int k = 0; k < SPT; ++k) {
+                const int u = t0 + k * BS + tid;
+                if (u == D - 1) { SL[k] = 0.0f; SU[k] = 0.0f; SC[k] = mf; }
+                if (u < D) { sT[u - t0] = SL[k]; sFm[u - t0] = SU[k]; sFs[u - t0] = SC[k]; }
+            }
+            if (tid == 0) { sPrev[0] = pL; sPrev[1] = pU; sPrev[2] = pC; }
+            __syncthreads();
+#pragma unroll
+            for (int k = 0; k < SPT; ++k) {
+                const int u = t0 + k * BS + tid;
+                if (u >= D) continue;
+                const int ix = u - t0;
+                const float L1 = ix ? sT[ix - 1] : sPrev[0];
+                const float U1 = ix ? sFm[ix - 1] : sPrev[1];
+                const float C1 = ix ? sFs[ix - 1] : sPrev[2];
+                const float dS = ((SL[k] - L1) + (SC[k] - C1)) - (SU[k] - U1);
+                pr[2] = fmaf(-rFms[k], dS, pr[2]);
+                pr[3] = fmaf(-rFss[k], dS, pr[3]);
+                if (u < D - 1) {
+                    const float S = (SL[k] + SC[k]) - SU[k];
+                    const float rest = ((mf - SC[k]) - SL[k]) + SU[k];
+                    pr[0] = fmaf(rA[k], S, pr[0]);
+                    pr[1] = fmaf(rF[k], rest, pr[1]);
+                    pr[4] = fmaf(rFm[k], rest, pr[4]);
+                    pr[5] = fmaf(rFs[k], rest, pr[5]);
+                } else {
+                    pr[0] = fmaf(mf, tail1mF, pr[0]);
+                }
+            }
+            const float r = block_sum<6, BS>(pr, sRed[par]);
+            par ^= 1;
+            if (tid < kPP) W.ppart[(((size_t)b * N + i) * G.ntiles + tile) * kPP + tid] = r;
+            if (tid == 0) gsum0 += r;
+            if (tid == 1) gsum1 += r;
+        } else if (tid < kPP) {
+            W.ppart[(((size_t)b * N + i) * G.ntiles + tile) * kPP + tid] = 0.0f;
+        }
+    }
+    {
+        float *gs = W.gsum_ops + (((size_t)b * G.ngroups + grp) * G.ntiles + tile) * 2;
+        if (tid == 0) gs[0] = gsum0;
+        if (tid == 1) gs[1] = gsum1;
+    }
+
+    float *up = W.Upart + ((size_t)b * G.ngroups + grp) * D;
+#pragma unroll
+    for (int k = 0; k < SPT; ++k) {
+        const int u = t0 + k * BS + tid;
+        if (u < D) up[u] = accU[k];
+    }
+}
+
+
+// ---------------------------------------------------------------------------
+// Back-edge kernel (modulo scheduling).  Work-group = (back-edge block, tile,
+// restart); one back edge (j -> i, k) at a time, c = k*II - Lat_j:
+//   V_rec       = F_i(-c-1) + sum_u P_i^{u-c} (1 - F_j(u))
+//   dVrec/dth_j = -sum_u F_j'(u) P_i^{u-c}
+//   dVrec/dth_i =  sum_t F_i'(t) P_j^{t+c+1}
+// with u, t over the interior edges 0..D-2.
+// ---------------------------------------------------------------------------
+template <int BS, int SPT>
+__global__ __launch_bounds__(BS) void k_back(Graph G, const float *__restrict__ mu,
+                                             const float *__restrict__ sigma, Work W,
+                                             int edges_per_block) {
+    constexpr int TILE = BS * SPT;
+    __shared__ float sRed[2][BS / 64][8];
+    const int tile = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
+    const int D = G.D, N = G.N;
+    const int t0 = tile * TILE;
+    const int be0 = blockIdx.x * edges_per_block;
+    const int be1 = min(be0 + edges_per_block, G.nb);
+    int par = 0;
+    for (int e = be0; e < be1; ++e) {
+        const int j = uniform(G.bsrc[e]), i = uniform(G.bdst[e]);
+        const long long c = (long long)G.bdist[e] * G.II - G.delay[j];
+        const float mj = mu[(size_t)b * N + j], sj = sigma[(size_t)b * N + j];
+        const float mi = mu[(size_t)b * N + i], si = sigma[(size_t)b * N + i];
+        const float rsj = 1.0f / sj, rsi = 1.0f / si;
+        const float cj = rsj * kInvSqrt2Pi, ci = rsi * kInvSqrt2Pi;
+        float acc[5] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int k = 0; k < SPT; ++k) {
+            const int u = t0 + k * BS + tid;
+            if (u < D - 1) {
+                float sj_, Fmj, Fsj, si_, Fmi, Fsi;
+                cdf_at(u, D, mj, rsj, cj, sj_, Fmj, Fsj);
+                cdf_at(u, D, mi, rsi, ci, si_, Fmi, Fsi);
+                const float Pi = st_mass(st_at((long long)u - c - 1, D, mi, rsi), st_at((long long)u - c, D, mi, rsi));
+                const float Pj = st_mass(st_at((long long)u + c, D, mj, rsj), st_at((long long)u + c + 1, D, mj, rsj));
+                acc[0] = fmaf(Pi, st_1mF(sj_), acc[0]);
+                acc[1] = fmaf(-Fmj, Pi, acc[1]);
+                acc[2] = fmaf(-Fsj, Pi, acc[2]);
+                acc[3] = fmaf(Fmi, Pj, acc[3]);
+                acc[4] = fmaf(Fsi, Pj, acc[4]);
+            }
+        }
+        if (tile == 0 && tid == 0) acc[0] += st_F(st_at(-c - 1, D, mi, rsi));
+        const float r = block_sum<5, BS>(acc, sRed[par]);
+        par ^= 1;
+        if (tid < kBP) W.bpart[(((size_t)b * G.nb + e) * G.ntiles + tile) * kBP + tid] = r;
+    }
+}
+
+
+// ---------------------------------------------------------------------------
+// Gradient of the smooth peak usage.  With c_k(d) = beta dL_res/dU_k(d mod T)
+// (the softmax written by k_vres), summation by parts onto the interior bin
+// edges gives
+//   dL/dth_i += sum_{t=0}^{D-2} (c(t) - c(t+1)) dF_i(t)/dth_i,
+// a dense weight per bin edge.  Step-by-step ops take it per step
+// (k_lse_ops); polynomial ops take it per chunk as the moments
+// M_n = sum_y (c(t) - c(t+1)) y^n (k_lse_mom), dotted with the chunk
+// coefficients of dF/dmu and dF/dsigma (k_lse_poly).
+// ---------------------------------------------------------------------------
+template <int BS, int SPT>
+__global__ __launch_bounds__(BS) void k_lse_ops(Graph G, const float *__restrict__ mu,
+                                                const float *__restrict__ sigma, Work W) {
+    constexpr int TILE = BS * SPT;
+    __shared__ float sW[TILE];
+    __shared__ int sI[BS];
+    __shared__ float sMu[BS], sRs[BS];
+    __shared__ float sRed[2][BS / 64][8];
+    const int grp = blockIdx.x, tile = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
+    const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
+    const int N = G.N, D = G.D, T = G.T;
+    const int t0 = tile * TILE;
+    int direct = 0;
+    if (q0 + tid < q1) {
+        const int i = G.perm[q0 + tid];
+        const size_t bi = (size_t)b * N + i;
+        direct = W.cls[bi] ? 0 : 1;
+        sI[tid] = direct ? i : -1;
+        sMu[tid] = mu[bi];
+        sRs[tid] = 1.0f / sigma[bi];
+    } else if (tid < BS) {
+        sI[tid] = -1;
+    }
+    if (!__syncthreads_or(direct)) return;   // every op of the group is polynomial
+    const float *sk = W.soft + ((size_t)b * G.K + G.rtype[G.perm[q0]]) * T;
+    for (int x = tid; x < TILE; x += BS) {
+        const int t = t0 + x;
+        sW[x] = t <= D - 2 ? soft_diff(sk, t, T) : 0.0f;
+    }
+    __syncthreads();
+    int par = 0;
+    for (int q = 0; q < q1 - q0; ++q) {
+        const int i = sI[q];
+        if (i < 0) continue;
+        const float m = sMu[q], rs = sRs[q], cinv = rs * kInvSqrt2Pi;
+        float acc[2] = {0.0f, 0.0f};
+#pragma unroll
+        for (int j = 0; j < SPT; ++j) {
+            const int x = tid + j * BS;
+            const float w = sW[x];
+            if (w != 0.0f) {
+                const float z = ((float)(t0 + x) + 0.5f - m) * rs;
+                const float Fm = -__builtin_amdgcn_exp2f(-(z * z) * kHalfLog2e) * cinv;
+                acc[0] = fmaf(w, Fm, acc[0]);
+                acc[1] = fmaf(w, Fm * z, acc[1]);
+            }
+        }
+        const float r = block_sum<2, BS>(acc, sRed[par]);
+        par ^= 1;
+        if (tid < 2) W.lpart[(((size_t)b * N + i) * G.ntiles + tile) * 2 + tid] = r;
+    }
+}
+
+
+// ---------------------------------------------------------------------------
+// Launchers
+// ---------------------------------------------------------------------------
+hipError_t launch_ops(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu, const float *sigma,
+                      hipStream_t st) {
+    const dim3 grid(g.ngroups, g.ntiles, g.B);
+    if (lc.bs == 64 && lc.spt == 1) hipLaunchKernelGGL((k_ops<64, 1>), grid, dim3(64), 0, st, g, mu, sigma, w);
+    else if (lc.bs == 256 && lc.spt == 1) hipLaunchKernelGGL((k_ops<256, 1>), grid, dim3(256), 0, st, g, mu, sigma, w);
+    else if (lc.bs == 256 && lc.spt == 4) hipLaunchKernelGGL((k_ops<256, 4>), grid, dim3(256), 0, st, g, mu, sigma, w);
+    else return hipErrorInvalidValue;
+    return hipSuccess;
+}
+
+hipError_t launch_back(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu, const float *sigma,
+                       hipStream_t st) {
+    const int epb = 4;
+    const dim3 grid((g.nb + epb - 1) / epb, g.ntiles, g.B);
+    if (lc.bs == 64) hipLaunchKernelGGL((k_back<64, 1>), grid, dim3(64), 0, st, g, mu, sigma, w, epb);
+    else if (lc.spt == 1) hipLaunchKernelGGL((k_back<256, 1>), grid, dim3(256), 0, st, g, mu, sigma, w, epb);
+    else hipLaunchKernelGGL((k_back<256, 4>), grid, dim3(256), 0, st, g, mu, sigma, w, epb);
+    return hipSuccess;
+}
+
+hipError_t launch_lse_ops(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu,
+                          const float *sigma, hipStream_t st) {
+    const dim3 grid(g.ngroups, g.ntiles, g.B);
+    if (lc.bs == 64) hipLaunchKernelGGL((k_lse_ops<64, 1>), grid, dim3(64), 0, st, g, mu, sigma, w);
+    else if (lc.spt == 1) hipLaunchKernelGGL((k_lse_ops<256, 1>), grid, dim3(256), 0, st, g, mu, sigma, w);
+    else hipLaunchKernelGGL((k_lse_ops<256, 4>), grid, dim3(256), 0, st, g, mu, sigma, w);
+    return hipSuccess;
+}
+
+}  // namespace gaus
