@@ -38,7 +38,8 @@ class _Problem(C.Structure):
                 ("row_ptr", C.c_void_p), ("col", C.c_void_p), ("delay", C.c_void_p),
                 ("rtype", C.c_void_p), ("K", C.c_int32), ("cap", C.c_void_p),
                 ("D", C.c_int32), ("II", C.c_int32), ("nb", C.c_int32),
-                ("bsrc", C.c_void_p), ("bdst", C.c_void_p), ("bdist", C.c_void_p)]
+                ("bsrc", C.c_void_p), ("bdst", C.c_void_p), ("bdist", C.c_void_p),
+                ("bmem", C.c_void_p)]
 
 
 _lib = None
@@ -52,7 +53,7 @@ def _load():
         lib = C.CDLL(_LIB)
         P = C.POINTER(_Problem)
         vp, i32, i64, dbl = C.c_void_p, C.c_int32, C.c_int64, C.c_double
-        lib.orc_loss_grad.argtypes = [P, vp, vp, vp, dbl, dbl, dbl, dbl, dbl, vp, vp, vp, vp, vp]
+        lib.orc_loss_grad.argtypes = [P, vp, vp, vp, dbl, dbl, dbl, dbl, dbl, dbl, vp, vp, vp, vp, vp, vp]
         lib.orc_loss_grad.restype = C.c_int
         lib.orc_edge_terms_double_sum.argtypes = [P, vp, vp, vp]
         lib.orc_edge_terms_double_sum.restype = None
@@ -94,10 +95,12 @@ class OracleProblem:
         self.bsrc = np.ascontiguousarray(prob.back_src, np.int32)
         self.bdst = np.ascontiguousarray(prob.back_dst, np.int32)
         self.bdist = np.ascontiguousarray(prob.back_dist, np.int32)
+        mem = getattr(prob, "mem_units", None)
+        self.bmem = np.ascontiguousarray(np.ones(self.n) if mem is None else mem, np.float64)
         self.s = _Problem(self.n, int(self.row_ptr[-1]), _ptr(self.row_ptr), _ptr(self.col),
                           _ptr(self.delay), _ptr(self.rtype), self.K, _ptr(self.cap),
                           self.D, self.II, int(self.bsrc.shape[0]), _ptr(self.bsrc),
-                          _ptr(self.bdst), _ptr(self.bdist))
+                          _ptr(self.bdst), _ptr(self.bdist), _ptr(self.bmem))
 
     @property
     def T(self) -> int:
@@ -112,28 +115,35 @@ def num_threads() -> int:
     return int(_load().orc_num_threads())
 
 
-def loss_grad(prob, mu, sigma, lam, alpha, rho, grad=True, tie_tol=1e-4, beta=0.0, tau=1e-2):
-    """Per restart b: terms [B,6] = (L, V_dep, V_res, V_rec, L_com, L_res),
+def loss_grad(prob, mu, sigma, lam, alpha, rho, grad=True, tie_tol=1e-4, beta=0.0, tau=1e-2, gamma=0.0,
+              mreg_out=None):
+    """Per restart b: terms [B,7] = (L, V_dep, V_res, V_rec, L_com, L_res, L_mem),
     U [B,K,T], g_mu, g_sigma [B,N] (fp64), ties [B] (count of near-tie usage
-    cells).  beta weights the smooth peak L_res (temperature tau) in L."""
+    cells).  beta weights the smooth peak usage L_res, gamma the smooth peak
+    storage L_mem (both temperature tau) in L.  mreg_out [B,T], if given,
+    receives the expected (folded) storage units per slot."""
     lib, op = _load(), _op(prob)
     mu = np.atleast_2d(np.asarray(mu, np.float64))
     sigma = np.atleast_2d(np.asarray(sigma, np.float64))
     lam = np.atleast_2d(np.asarray(lam, np.float64))
     B = mu.shape[0]
-    terms = np.zeros((B, 6)); U = np.zeros((B, op.K, op.T))
+    terms = np.zeros((B, 7)); U = np.zeros((B, op.K, op.T))
     gm = np.zeros((B, op.n)); gs = np.zeros((B, op.n)); ties = np.zeros(B, np.int64)
     for b in range(B):
         m = np.ascontiguousarray(mu[b]); s = np.ascontiguousarray(sigma[b])
         l = np.ascontiguousarray(lam[b if lam.shape[0] > 1 else 0])
-        t = np.zeros(6); u = np.zeros((op.K, op.T)); nt = np.zeros(1, np.int64)
+        t = np.zeros(7); u = np.zeros((op.K, op.T)); nt = np.zeros(1, np.int64)
+        mr = np.zeros(op.T) if mreg_out is not None else None
         g1 = np.zeros(op.n); g2 = np.zeros(op.n)
         rc = lib.orc_loss_grad(C.byref(op.s), _ptr(m), _ptr(s), _ptr(l), float(alpha), float(rho),
-                               float(beta), float(tau), float(tie_tol), _ptr(t), _ptr(u),
+                               float(beta), float(tau), float(gamma), float(tie_tol), _ptr(t), _ptr(u),
+                               _ptr(mr) if mr is not None else None,
                                _ptr(g1) if grad else None, _ptr(g2) if grad else None, _ptr(nt))
         if rc != OK:
             raise RuntimeError(f"oracle loss_grad failed: {rc}")
         terms[b] = t; U[b] = u; gm[b] = g1; gs[b] = g2; ties[b] = nt[0]
+        if mr is not None:
+            mreg_out[b] = mr
     return terms, U, gm, gs, ties
 
 

@@ -17,6 +17,10 @@
  *   - recurrence violation        : App. B.3 (V^_Rec, with producer delay)
  *   - smooth peak usage L_Res     : App. B.2 (LogSumExp over steps, temperature
  *                                   tau; Sec. 3.2 eq:max), App. B.3 (modulo slots)
+ *   - expected storage Reg^(d)    : Sec. 3.2 eq:active (b_i units held from d_i
+ *                                   until the last successor starts), its modulo
+ *                                   fold MReg^ (App. B.3) and smooth peak L_Mem
+ *                                   (eq:max)
  *   - augmented Lagrangian        : Sec. 3.3, eq. (11) and Alg. 1
  *   - Adam                        : App. C.1 hyper-parameters; Kingma & Ba (2015)
  *   - legalization                : App. A, Alg. 3 (regular), Alg. 4 (modulo)
@@ -39,6 +43,11 @@
  *       usage slots and summed over types: L_Res = sum_k tau log sum_t
  *       exp(U_k(t)/tau) (slots t < II when II > 0: the modulo peak MRes);
  *       it enters the objective with weight beta (Formulation A: beta = 1).
+ *   R18 the storage term is eq:active as printed (F_i(d) (1 - prod_succ F_j(d)),
+ *       so an op without successors holds nothing; the paper's sink node is
+ *       an ordinary op of the caller's graph); folded like usage (R5, k >= 0
+ *       as in the printed sum); L_Mem = tau log sum_t exp(MReg(t)/tau) enters
+ *       the objective with weight gamma (Formulations B and C: gamma = 1).
  *
  * The gradient is the analytic derivative of the forward below (derived by
  * writing every term as a function of the CDF values at the D-1 interior bin
@@ -66,6 +75,7 @@ typedef struct {
     const int32_t *bsrc;       /* [nb] producer v_j */
     const int32_t *bdst;       /* [nb] consumer v_i */
     const int32_t *bdist;      /* [nb] iteration distance k */
+    const double *bmem;        /* [n] storage units b_i of each op's output */
 } orc_problem;
 
 enum { ORC_OK = 0, ORC_E_INVALID = 1, ORC_E_CYCLE = 2, ORC_E_HORIZON = 3,
@@ -238,15 +248,17 @@ int orc_asap_alap(const orc_problem *p, int64_t *asap, int64_t *alap) {
 /*
  * One restart.  Inputs mu, sigma [n] (float32 values promoted to double),
  * lam[3] = (lambda_dep, lambda_res, lambda_rec), beta and tau of the smooth
- * peak term.  Outputs:
- *   terms[6] = (L_total, V_dep, V_res, V_rec, L_com, L_res)
+ * peak usage term, gamma of the smooth peak storage term.  Outputs:
+ *   terms[7] = (L_total, V_dep, V_res, V_rec, L_com, L_res, L_mem)
+ *   Mreg[T]  expected (folded) storage units per slot (may be NULL)
  *   U[K*T]   expected (folded) usage, T = II if II > 0 else D
  *   g_mu, g_sigma [n]  dL_total/dmu, dL_total/dsigma (may be NULL: forward only)
  *   n_ties   number of (k, slot) cells with |U - C| < tie_tol * max(1, C)
  */
 int orc_loss_grad(const orc_problem *p, const double *mu, const double *sigma,
-                  const double *lam, double alpha, double rho, double beta, double tau, double tie_tol,
-                  double *terms, double *U, double *g_mu, double *g_sigma, int64_t *n_ties) {
+                  const double *lam, double alpha, double rho, double beta, double tau, double gamma,
+                  double tie_tol, double *terms, double *U, double *Mreg, double *g_mu, double *g_sigma,
+                  int64_t *n_ties) {
     const int32_t n = p->n, D = p->D, K = p->K, II = p->II;
     const int32_t T = (II > 0) ? II : D;
     if (D < 1 || n < 0 || K < 1) return ORC_E_INVALID;
@@ -306,6 +318,38 @@ int orc_loss_grad(const orc_problem *p, const double *mu, const double *sigma,
         }
     }
 
+    /* expected storage units per step, eq:active, folded like the usage;
+     * L_mem and its derivative with respect to MReg(t) (a softmax) */
+    double L_mem = 0.0;
+    double *mreg = calloc((size_t)T + 1, sizeof(double));
+    double *msoft = calloc((size_t)T + 1, sizeof(double));
+    if (!mreg || !msoft) {
+        free(mreg); free(msoft); free(soft); free(F); free(P); free(vd); free(lc); free(vr); adj_free(&a);
+        return ORC_E_NOMEM;
+    }
+    if (gamma != 0.0 || Mreg) {
+        for (int32_t d = 0; d < D; ++d) {
+            double r = 0.0;
+            for (int32_t i = 0; i < n; ++i) {
+                if (p->row_ptr[i + 1] == p->row_ptr[i]) continue;   /* no successor: holds nothing */
+                double q = 1.0;                                     /* P(every successor started by d) */
+                for (int32_t e = p->row_ptr[i]; e < p->row_ptr[i + 1]; ++e)
+                    q *= cdf_row(F + (int64_t)p->col[e] * DF, d, D);
+                r += p->bmem[i] * cdf_row(F + (int64_t)i * DF, d, D) * (1.0 - q);
+            }
+            mreg[d % T] += r;
+        }
+        if (Mreg) for (int32_t t = 0; t < T; ++t) Mreg[t] = mreg[t];
+    }
+    if (gamma != 0.0) {
+        double m = mreg[0];
+        for (int32_t t = 1; t < T; ++t) if (mreg[t] > m) m = mreg[t];
+        double z = 0.0;
+        for (int32_t t = 0; t < T; ++t) z += exp((mreg[t] - m) / tau);
+        L_mem = m + tau * log(z);
+        for (int32_t t = 0; t < T; ++t) msoft[t] = exp((mreg[t] - m) / tau) / z;
+    }
+
     /* dependency violations and edge lengths, summed per producer */
     #pragma omp parallel for schedule(dynamic, 16)
     for (int32_t i = 0; i < n; ++i) {
@@ -336,10 +380,10 @@ int orc_loss_grad(const orc_problem *p, const double *mu, const double *sigma,
 
     /* augmented Lagrangian, eq. (11) */
     double V[3] = {V_dep, V_res, V_rec};
-    double L = alpha * L_com + beta * L_res;
+    double L = alpha * L_com + beta * L_res + gamma * L_mem;
     for (int c = 0; c < 3; ++c) L += lam[c] * V[c] + 0.5 * rho * V[c] * V[c];
     terms[0] = L; terms[1] = V_dep; terms[2] = V_res; terms[3] = V_rec; terms[4] = L_com;
-    terms[5] = L_res;
+    terms[5] = L_res; terms[6] = L_mem;
     if (n_ties) *n_ties = ties;
 
     if (g_mu && g_sigma) {
@@ -379,6 +423,23 @@ int orc_loss_grad(const orc_problem *p, const double *mu, const double *sigma,
                         int64_t aa = (int64_t)t - (int64_t)p->bdist[b] * II + p->delay[i];
                         h -= w_rec * mass_row(P + (int64_t)ic * D, aa, D);
                     }
+                    if (gamma != 0.0) {   /* eq:active: as the op itself and as a successor */
+                        double ws = gamma * msoft[t % T], own = 0.0;
+                        if (p->row_ptr[i + 1] > p->row_ptr[i]) {
+                            double q = 1.0;
+                            for (int32_t e = p->row_ptr[i]; e < p->row_ptr[i + 1]; ++e)
+                                q *= F[(int64_t)p->col[e] * DF + t];
+                            own = p->bmem[i] * (1.0 - q);
+                        }
+                        for (int32_t q2 = a.pred_ptr[i]; q2 < a.pred_ptr[i + 1]; ++q2) {
+                            int32_t hh = a.pred[q2];
+                            double others = 1.0;       /* the other successors of hh, started by t */
+                            for (int32_t e = p->row_ptr[hh]; e < p->row_ptr[hh + 1]; ++e)
+                                if (p->col[e] != i) others *= F[(int64_t)p->col[e] * DF + t];
+                            own -= p->bmem[hh] * F[(int64_t)hh * DF + t] * others;
+                        }
+                        h += ws * own;
+                    }
                     double z = (t + 0.5 - mu[i]) / sigma[i];
                     double dF_dmu = -phi(z) / sigma[i];
                     double dF_dsigma = -phi(z) * z / sigma[i];
@@ -390,7 +451,7 @@ int orc_loss_grad(const orc_problem *p, const double *mu, const double *sigma,
             free(G);
         }
     }
-    free(F); free(P); free(vd); free(lc); free(vr); free(soft); adj_free(&a);
+    free(F); free(P); free(vd); free(lc); free(vr); free(soft); free(mreg); free(msoft); adj_free(&a);
     return ORC_OK;
 }
 

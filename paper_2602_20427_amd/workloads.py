@@ -83,6 +83,7 @@ class Problem:
     back_dist: np.ndarray = field(default_factory=lambda: np.zeros(0, np.int32))
     layer: np.ndarray | None = None
     name: str = ""
+    mem_units: np.ndarray | None = None   # float32 [N] storage units b_i (None: 1 each)
 
     @property
     def n_edges(self) -> int:

@@ -212,29 +212,32 @@ def test_p6_eq_dep_with_zero_delay_is_printed_formula(orc):
 
 # ------------------------------------------------------------------- P7
 
-def _total(orc, p, mu, sg, lam, alpha, rho, beta=0.0, tau=1e-2):
-    terms, *_ = orc.loss_grad(p, mu, sg, lam, alpha, rho, grad=False, beta=beta, tau=tau)
+def _total(orc, p, mu, sg, lam, alpha, rho, beta=0.0, tau=1e-2, gamma=0.0):
+    terms, *_ = orc.loss_grad(p, mu, sg, lam, alpha, rho, grad=False, beta=beta, tau=tau, gamma=gamma)
     return terms[0, 0]
 
 
-@pytest.mark.parametrize("II,n_back,beta,tau", [(0, 0, 0.0, 1e-2), (4, 2, 0.0, 1e-2),
-                                                (0, 0, 0.7, 0.3), (4, 2, 1.3, 0.05)])
-def test_p7_gradient_finite_differences(orc, II, n_back, beta, tau):
+@pytest.mark.parametrize("II,n_back,beta,tau,gamma", [(0, 0, 0.0, 1e-2, 0.0), (4, 2, 0.0, 1e-2, 0.0),
+                                                      (0, 0, 0.7, 0.3, 0.0), (4, 2, 1.3, 0.05, 0.0),
+                                                      (0, 0, 0.0, 0.2, 0.9), (4, 2, 0.5, 0.1, 1.1)])
+def test_p7_gradient_finite_differences(orc, II, n_back, beta, tau, gamma):
     """Analytic gradient of the augmented Lagrangian (with the smooth peak
-    term when beta > 0) vs central differences of the oracle's own forward,
-    away from ReLU kinks."""
-    rng = np.random.default_rng(70 + II + int(100 * beta))
+    usage term when beta > 0 and the smooth peak storage term when gamma > 0)
+    vs central differences of the oracle's own forward, away from ReLU kinks."""
+    rng = np.random.default_rng(70 + II + int(100 * beta) + int(1000 * gamma))
     checked = 0
     for _ in range(8):
         p = tiny_problem(rng, 7, 12, II=II, n_back=n_back, max_delay=2)
+        p.mem_units = rng.uniform(0.5, 3.0, size=7)
         mu = rng.uniform(0, 12, size=7); sg = np.exp(rng.uniform(np.log(0.5), np.log(4.0), size=7))
         lam = rng.uniform(0.1, 1.0, size=3); alpha, rho = 0.37, 0.2
-        terms, U, gm, gs, ties = orc.loss_grad(p, mu, sg, lam, alpha, rho, tie_tol=1e-3, beta=beta, tau=tau)
+        terms, U, gm, gs, ties = orc.loss_grad(p, mu, sg, lam, alpha, rho, tie_tol=1e-3, beta=beta, tau=tau,
+                                               gamma=gamma)
         if ties[0]:
             continue
         h = 1e-6
         fd_m = np.zeros(7); fd_s = np.zeros(7)
-        tot = lambda m, s: _total(orc, p, m, s, lam, alpha, rho, beta, tau)
+        tot = lambda m, s: _total(orc, p, m, s, lam, alpha, rho, beta, tau, gamma)
         for i in range(7):
             e = np.zeros(7); e[i] = h * max(1.0, abs(mu[i]))
             fd_m[i] = (tot(mu + e, sg) - tot(mu - e, sg)) / (2 * e[i])
@@ -250,7 +253,7 @@ def test_p7_gradient_finite_differences(orc, II, n_back, beta, tau):
 torch = pytest.importorskip("torch")
 
 
-def _torch_total(p, mu, sg, lam, alpha, rho, beta=0.0, tau=1e-2):
+def _torch_total(p, mu, sg, lam, alpha, rho, beta=0.0, tau=1e-2, gamma=0.0):
     """The objective written with fp64 torch ops straight from the paper's
     printed double sums (a second, independent formulation)."""
     D = p.D
@@ -285,27 +288,47 @@ def _torch_total(p, mu, sg, lam, alpha, rho, beta=0.0, tau=1e-2):
         L = L + lam[c] * V[c] + 0.5 * rho * V[c] ** 2                  # eq. (11)
     if beta:
         L = L + beta * (tau * torch.logsumexp(U / tau, dim=1)).sum()   # App. B.2, eq:max
+    if gamma:
+        Fc = torch.cumsum(P, dim=1)                  # sum_{d' <= d} P^{d'}, second line of eq:active
+        bm = torch.as_tensor(p.mem_units, dtype=torch.float64)
+        reg = torch.zeros(D, dtype=torch.float64)
+        for i in range(p.n_ops):
+            succ = p.col_idx[p.row_ptr[i]:p.row_ptr[i + 1]]
+            if len(succ) == 0:
+                continue
+            q = torch.ones(D, dtype=torch.float64)
+            for j in succ:
+                q = q * Fc[j]
+            reg = reg + bm[i] * Fc[i] * (1 - q)
+        mreg = reg @ fold                                                # App. B.3
+        L = L + gamma * tau * torch.logsumexp(mreg / tau, dim=0)      # eq:max
     return L
 
 
-@pytest.mark.parametrize("II,n_back,beta,tau", [(0, 0, 0.0, 1e-2), (3, 2, 0.0, 1e-2), (5, 3, 0.0, 1e-2),
-                                                (0, 0, 1.0, 1e-2), (0, 0, 0.6, 0.2), (3, 2, 1.0, 0.05)])
-def test_p7_gradient_matches_autograd_of_double_sums(orc, II, n_back, beta, tau):
+@pytest.mark.parametrize("II,n_back,beta,tau,gamma", [(0, 0, 0.0, 1e-2, 0.0), (3, 2, 0.0, 1e-2, 0.0),
+                                                      (5, 3, 0.0, 1e-2, 0.0), (0, 0, 1.0, 1e-2, 0.0),
+                                                      (0, 0, 0.6, 0.2, 0.0), (3, 2, 1.0, 0.05, 0.0),
+                                                      (0, 0, 0.0, 0.1, 1.0), (3, 2, 0.4, 0.05, 0.8),
+                                                      (0, 0, 0.0, 1e-2, 1.0)])
+def test_p7_gradient_matches_autograd_of_double_sums(orc, II, n_back, beta, tau, gamma):
     """The oracle's hand-derived backward equals fp64 autograd of the literal
     double-sum formulation (independent code, independent derivation), with
-    the smooth peak written with the library LogSumExp when beta > 0."""
-    rng = np.random.default_rng(700 + II + int(100 * beta))
+    the smooth peaks written with the library LogSumExp when beta or gamma
+    > 0 and the storage term from cumulative masses (eq:active)."""
+    rng = np.random.default_rng(700 + II + int(100 * beta) + int(1000 * gamma))
     done = 0
     for _ in range(6):
         p = tiny_problem(rng, 6, 10, II=II, n_back=n_back, max_delay=3, K=2)
+        p.mem_units = rng.uniform(0.5, 3.0, size=6)
         mu = rng.uniform(-1, 10, size=6); sg = np.exp(rng.uniform(np.log(0.3), np.log(5.0), size=6))
         lam = rng.uniform(0.05, 1.0, size=3).tolist(); alpha, rho = 0.29, 0.13
-        terms, U, gm, gs, ties = orc.loss_grad(p, mu, sg, lam, alpha, rho, tie_tol=1e-6, beta=beta, tau=tau)
+        terms, U, gm, gs, ties = orc.loss_grad(p, mu, sg, lam, alpha, rho, tie_tol=1e-6, beta=beta, tau=tau,
+                                               gamma=gamma)
         if ties[0]:
             continue
         tm = torch.tensor(mu, dtype=torch.float64, requires_grad=True)
         ts = torch.tensor(sg, dtype=torch.float64, requires_grad=True)
-        L = _torch_total(p, tm, ts, lam, alpha, rho, beta, tau)
+        L = _torch_total(p, tm, ts, lam, alpha, rho, beta, tau, gamma)
         L.backward()
         assert abs(L.item() - terms[0, 0]) < 1e-11
         assert np.abs(tm.grad.numpy() - gm[0]).max() < 1e-10
@@ -523,3 +546,61 @@ def test_p15_smooth_peak_bounds_and_limits(orc):
         tau = 1e7
         terms, U, *_ = orc.loss_grad(p, mu, sg, [0, 0, 0], 0.0, 0.0, grad=False, beta=1.0, tau=tau)
         assert abs(terms[0, 5] - 2 * tau * np.log(T) - p.n_ops / T) < 1e-5
+
+
+# ------------------------------------------------------------------- P16
+
+def test_p16_storage_sigma_to_zero_hand_counts(orc):
+    """sigma -> 0: eq:active becomes the integer storage profile of eq:mem for
+    the rounded schedule (tests/golden/sigma0_storage_counts.json, hand
+    counted), per step and folded mod II."""
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "sigma0_storage_counts.json")))
+    n = g["n"]
+    for II, key in ((0, "expected_per_step"), (g["II_fold"], "expected_folded")):
+        p = Problem(n_ops=n, row_ptr=np.array(g["row_ptr"], np.int32), col_idx=np.array(g["col_idx"], np.int32),
+                    delay=np.zeros(n, np.int32), rtype=np.zeros(n, np.int32),
+                    capacity=np.array([10.0], np.float32), D=g["D"], II=II,
+                    mem_units=np.array(g["mem_units"], np.float64))
+        T = II if II else g["D"]
+        mr = np.zeros((1, T))
+        orc.loss_grad(p, np.array(g["mu"]), np.full(n, 1e-6), [0, 0, 0], 0.0, 0.0, grad=False, mreg_out=mr)
+        assert np.array_equal(mr[0], np.array(g[key], np.float64)), (mr[0], g[key])
+
+
+@pytest.mark.parametrize("II", [0, 3])
+def test_p16_storage_equals_brute_force_expectation(orc, II):
+    """eq:active (independent ops: F_i (1 - prod F_j)) equals the expectation
+    of the discrete storage profile of eq:mem over all D^N schedules, per
+    step, folded mod II."""
+    rng = np.random.default_rng(160 + II)
+    for _ in range(3):
+        n, D = 4, 5
+        p = tiny_problem(rng, n, D, II=II)
+        p.mem_units = rng.uniform(0.5, 2.0, size=n)
+        mu = rng.uniform(-0.5, 5, size=n); sg = rng.uniform(0.3, 2.0, size=n)
+        P = masses(orc, mu, sg, D)
+        T = II if II else D
+        ref = np.zeros(T)
+        succ = [p.col_idx[p.row_ptr[i]:p.row_ptr[i + 1]] for i in range(n)]
+        for s in itertools.product(range(D), repeat=n):
+            w = np.prod([P[i, s[i]] for i in range(n)])
+            for d in range(D):
+                held = sum(p.mem_units[i] for i in range(n) if len(succ[i]) and s[i] <= d < max(s[j] for j in succ[i]))
+                ref[d % T] += w * held
+        mr = np.zeros((1, T))
+        orc.loss_grad(p, mu, sg, [0, 0, 0], 0.0, 0.0, grad=False, mreg_out=mr)
+        assert np.abs(mr[0] - ref).max() < 1e-12
+
+
+def test_p16_storage_smooth_peak_bounds(orc):
+    """max_t MReg <= L_mem <= max_t MReg + tau log T."""
+    rng = np.random.default_rng(161)
+    for II in (0, 4):
+        p = tiny_problem(rng, 7, 11, II=II)
+        p.mem_units = rng.uniform(0.5, 2.0, size=7)
+        T = II if II else p.D
+        mu = rng.uniform(0, 11, size=7); sg = rng.uniform(0.4, 3.0, size=7)
+        for tau in (1e-3, 0.05, 1.0):
+            mr = np.zeros((1, T))
+            terms, *_ = orc.loss_grad(p, mu, sg, [0, 0, 0], 0.0, 0.0, grad=False, gamma=1.0, tau=tau, mreg_out=mr)
+            assert mr[0].max() - 1e-12 <= terms[0, 6] <= mr[0].max() + tau * np.log(T) + 1e-12
