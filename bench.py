@@ -132,7 +132,8 @@ def cpu_baseline(prob, mu, sigma, lam, hp, n_restarts):
     t0 = time.perf_counter()
     for b in range(n_restarts):
         _, _, gm, gs, _ = oracle.loss_grad(prob, mu[b:b + 1].astype(np.float64), sigma[b:b + 1].astype(np.float64),
-                                           lam[b:b + 1].astype(np.float64), hp.alpha_com, hp.rho)
+                                           lam[b:b + 1].astype(np.float64), hp.alpha_com, hp.rho,
+                                           beta=hp.beta_res, tau=hp.tau, gamma=hp.gamma_mem)
         z = np.zeros(prob.n_ops)
         oracle.adam(mu[b].astype(np.float64), z, z, gm[0], 1, hp.lr)
         oracle.adam(sigma[b].astype(np.float64), z, z, gs[0], 1, hp.lr)
@@ -156,6 +157,9 @@ def main():
     ap.add_argument("--lse-beta", type=float, default=0.0,
                     help="weight of the smooth peak usage term (LogSumExp, temperature --tau); 0 = off")
     ap.add_argument("--tau", type=float, default=1e-2)
+    ap.add_argument("--mem-gamma", type=float, default=0.0,
+                    help="weight of the smooth peak storage term (storage units of 1-32 bits per op and a "
+                         "sink op are added to the workload); 0 = off")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the run, copy this many MiB once (counter calibration)")
     args = ap.parse_args()
@@ -168,18 +172,21 @@ def main():
     import numpy as np
     import torch
     from paper_2602_20427_amd import binding as bd
-    from paper_2602_20427_amd.workloads import CONFIGS, make_problem, restart_uniforms, uniform_state
+    from paper_2602_20427_amd.workloads import CONFIGS, make_problem, restart_uniforms, uniform_state, with_storage
 
     assert torch.cuda.is_available(), "bench.py needs an MI355X"
     cfg = CONFIGS[args.workload]
     log(f"[bench] workload {cfg.name}: building problem")
     prob = make_problem(cfg, seed=0)
+    if args.mem_gamma:
+        prob = with_storage(prob, seed=1)
     B, N, D = cfg.B, prob.n_ops, prob.D
     hp = bd.default_hparams()
     hp.lr = cfg.lr
     hp.poly_chunk = args.poly_chunk
     hp.beta_res = args.lse_beta
     hp.tau = args.tau
+    hp.gamma_mem = args.mem_gamma
     dev = torch.device("cuda")
     ctx = bd.Context(prob, B, hp)
     mu = torch.zeros(B, N, device=dev)
@@ -255,6 +262,8 @@ def main():
                                           "_direct" if args.poly_chunk < 0 else f"_w{args.poly_chunk}")
     if args.lse_beta:
         profile += "_lse"
+    if args.mem_gamma:
+        profile += "_mem"
     whole = model_flops(B * N * (D - 1), B * (E + prob.n_back) * (D - 1))
     out = {
         "metric": METRIC, "value": value, "unit": "op-step evals/s", "n_gpus": 1,
@@ -264,7 +273,9 @@ def main():
         "config": {"workload": describe(cfg, prob), "B": B, "N": N, "E": E,
                    "n_back": prob.n_back, "D": D, "II": prob.II,
                    "objective": "alpha L_com + ALM(V_dep, V_res, V_rec)" +
-                                (f" + {args.lse_beta:g} L_res (tau {args.tau:g})" if args.lse_beta else "")},
+                                (f" + {args.lse_beta:g} L_res (tau {args.tau:g})" if args.lse_beta else "") +
+                                (f" + {args.mem_gamma:g} L_mem (tau {args.tau:g}; storage units and a sink op)"
+                                 if args.mem_gamma else "")},
         "ms_per_iteration_events": step_ms_events, "legalize_ms": legalize_ms,
         "poly_path": dict(poly_cfg, ops=census["ops"], edges=census["edges"]),
         "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_TFLOPS, "unit": "TFLOP/s",

@@ -62,7 +62,8 @@ typedef struct {
     int32_t n_ops;             /* N >= 1 */
     int32_t n_edges;           /* E >= 0 */
     const int32_t *row_ptr;    /* [N+1] CSR by producer: row_ptr[0]=0, nondecreasing, row_ptr[N]=E */
-    const int32_t *col_idx;    /* [E] consumer of each edge, in [0,N); the graph must be acyclic */
+    const int32_t *col_idx;    /* [E] consumer of each edge, in [0,N); the graph must be acyclic,
+                                  without duplicate edges */
     const int32_t *delay;      /* [N] Lat(v_i), 0 <= Lat <= 2^20 */
     const int32_t *rtype;      /* [N] resource type in [0,K); each op uses one unit of it */
     int32_t n_types;           /* K >= 1 */
@@ -73,13 +74,15 @@ typedef struct {
     const int32_t *back_src;   /* [n_back] producer v_j of each back edge */
     const int32_t *back_dst;   /* [n_back] consumer v_i (!= v_j) */
     const int32_t *back_dist;  /* [n_back] iteration distance k >= 1, k*II <= 2^30 */
+    const float *mem_units;    /* [N] storage units b_i of each op's output (Sec. 2.1 eq:mem),
+                                  finite, >= 0; NULL = 1 each.  Used by the storage term. */
 } gaus_problem;
 
 /* Hyper-parameters.  gaus_default_hparams() fills the paper's values
  * (App. C.1: Adam lr 1e-2, rho 1e-4, kappa 1/6, LogSumExp temperature 1e-2;
  * Sec. 3.3: lambda0 1e-6) and this library's choices for the unstated ones
  * (Adam betas/eps as in Kingma & Ba, alpha_com 0.01, sigma_min 0.05,
- * beta_res 0: the smooth peak term is off unless asked for). */
+ * beta_res 0 and gamma_mem 0: the smooth peak terms are off unless asked for). */
 typedef struct {
     float lr, beta1, beta2, eps;   /* Adam */
     float rho;                     /* ALM penalty */
@@ -95,6 +98,12 @@ typedef struct {
     float tau;                     /* its temperature (> 0): L_res = sum_k tau log sum_t
                                       exp(U_k(t)/tau), App. B.2 and eq:max; slots t < II
                                       when II > 0 (App. B.3) */
+    float gamma_mem;               /* weight of the smooth peak storage L_mem in L (>= 0;
+                                      1 gives Formulations B and C, Sec. 4.1):
+                                      L_mem = tau log sum_t exp(MReg(t)/tau) with MReg the
+                                      expected storage units of eq:active folded like the
+                                      usage (App. B.3).  When > 0 every op is evaluated step
+                                      by step (no chunk polynomials). */
 } gaus_hparams;
 
 void gaus_default_hparams(gaus_hparams *hp);
@@ -117,23 +126,24 @@ gaus_status gaus_bind_state(gaus_ctx *ctx, float *mu, float *sigma, float *adam_
 
 /* One forward + backward at (mu, sigma) with multipliers lambda, for all B
  * restarts.  Inputs DEVICE: mu, sigma [B][N], lambda [B][3].  Outputs DEVICE:
- * terms [B][6] = (L, V_dep, V_res, V_rec, L_com, L_res), grad_mu, grad_sigma
- * [B][N] (dL/dmu, dL/dsigma), where L = alpha_com L_com + beta_res L_res +
- * sum_c (lambda_c V_c + rho/2 V_c^2) (Sec. 3.3 eq. 11; L_res is 0 when
- * beta_res = 0).  Asynchronous.  Errors: INVALID_ARG (null pointer). */
+ * terms [B][7] = (L, V_dep, V_res, V_rec, L_com, L_res, L_mem), grad_mu,
+ * grad_sigma [B][N] (dL/dmu, dL/dsigma), where L = alpha_com L_com +
+ * beta_res L_res + gamma_mem L_mem + sum_c (lambda_c V_c + rho/2 V_c^2)
+ * (Sec. 3.3 eq. 11; L_res and L_mem are 0 when their weight is 0).
+ * Asynchronous.  Errors: INVALID_ARG (null pointer). */
 gaus_status gaus_loss_grad(gaus_ctx *ctx, const float *mu, const float *sigma, const float *lambda,
                            float *terms, float *grad_mu, float *grad_sigma);
 
 /* n_iters iterations of Alg. 1's update on the bound state: forward,
  * backward, Adam on mu and sigma, sigma <- max(sigma, sigma_min),
  * lambda_c <- lambda_c + rho * V_c (this iteration's V), adam_t += 1.
- * terms_last (DEVICE [B][6] or NULL) receives the last iteration's terms.
+ * terms_last (DEVICE [B][7] or NULL) receives the last iteration's terms.
  * Asynchronous.  Errors: INVALID_ARG (state not bound, n_iters < 0). */
 gaus_status gaus_step(gaus_ctx *ctx, int32_t n_iters, float *terms_last);
 
 /* The update half of gaus_step from a given gradient: Adam on the bound
  * (mu, sigma) with g_mu, g_sigma (DEVICE [B][N]), the sigma clamp, and
- * lambda_c += rho * terms[b][1+c] with terms DEVICE [B][6]; adam_t += 1.
+ * lambda_c += rho * terms[b][1+c] with terms DEVICE [B][7]; adam_t += 1.
  * Asynchronous.  Used to check the optimizer step on its own. */
 gaus_status gaus_adam_from_grad(gaus_ctx *ctx, const float *g_mu, const float *g_sigma,
                                 const float *terms);
@@ -160,6 +170,11 @@ gaus_status gaus_asap_alap(const gaus_ctx *ctx, int32_t *asap, int32_t *alap);
 /* Expected usage U [B][K][T] (T = II if II > 0 else D) of the last forward
  * pass, copied to DEVICE memory U.  Asynchronous. */
 gaus_status gaus_get_usage(gaus_ctx *ctx, float *U);
+
+/* Expected storage units MReg [B][T] of the last forward (Sec. 3.2 eq:active,
+ * folded like the usage, App. B.3), copied to DEVICE memory M.  Only when
+ * gamma_mem > 0 (else INVALID_ARG).  Asynchronous. */
+gaus_status gaus_get_storage(gaus_ctx *ctx, float *M);
 
 /* Profiling hook.  While enabled, every launch of the two kernels that carry
  * the per-step work of an iteration -- [0] the step-by-step op kernel and

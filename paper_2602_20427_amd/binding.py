@@ -21,7 +21,7 @@ OK, E_INVALID_ARG, E_CYCLE, E_HORIZON, E_NOT_CONVERGED, E_OVERFLOW, E_DEVICE, E_
 # symbols declared in include/gaus.h
 EXPORTS = ("gaus_default_hparams", "gaus_init", "gaus_bind_state", "gaus_loss_grad", "gaus_step",
            "gaus_adam_from_grad", "gaus_legalize", "gaus_init_state", "gaus_asap_alap",
-           "gaus_get_usage", "gaus_kernel_timing", "gaus_kernel_timing_read", "gaus_sync",
+           "gaus_get_usage", "gaus_get_storage", "gaus_kernel_timing", "gaus_kernel_timing_read", "gaus_sync",
            "gaus_get_dims", "gaus_get_poly_config", "gaus_poly_census", "gaus_last_error", "gaus_status_string",
            "gaus_destroy")
 
@@ -37,16 +37,16 @@ class _Problem(C.Structure):
                 ("col_idx", C.c_void_p), ("delay", C.c_void_p), ("rtype", C.c_void_p),
                 ("n_types", C.c_int32), ("capacity", C.c_void_p), ("D", C.c_int32), ("II", C.c_int32),
                 ("n_back", C.c_int32), ("back_src", C.c_void_p), ("back_dst", C.c_void_p),
-                ("back_dist", C.c_void_p)]
+                ("back_dist", C.c_void_p), ("mem_units", C.c_void_p)]
 
 
 class HParams(C.Structure):
     _fields_ = [("lr", C.c_float), ("beta1", C.c_float), ("beta2", C.c_float), ("eps", C.c_float),
                 ("rho", C.c_float), ("lambda0", C.c_float), ("alpha_com", C.c_float),
                 ("sigma_min", C.c_float), ("kappa", C.c_float), ("poly_chunk", C.c_int32),
-                ("beta_res", C.c_float), ("tau", C.c_float)]
+                ("beta_res", C.c_float), ("tau", C.c_float), ("gamma_mem", C.c_float)]
 
-N_TERMS = 6   # L, V_dep, V_res, V_rec, L_com, L_res
+N_TERMS = 7   # L, V_dep, V_res, V_rec, L_com, L_res, L_mem
 
 
 _lib = None
@@ -57,6 +57,7 @@ def load():
     global _lib
     if _lib is not None:
         return _lib
+    import torch  # noqa: F401  (HIP runtime and device memory come from torch)
     if not os.path.exists(LIB_PATH):
         raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
                            "(hipcc --offload-arch=gfx950); there is no CPU fallback")
@@ -73,6 +74,7 @@ def load():
         "gaus_init_state": ([vp] * 4, C.c_int),
         "gaus_asap_alap": ([vp] * 3, C.c_int),
         "gaus_get_usage": ([vp] * 2, C.c_int),
+        "gaus_get_storage": ([vp] * 2, C.c_int),
         "gaus_kernel_timing": ([vp, i32], C.c_int),
         "gaus_kernel_timing_read": ([vp, vp, vp], C.c_int),
         "gaus_sync": ([vp], C.c_int),
@@ -132,9 +134,14 @@ class Context:
                         np.ascontiguousarray(problem.back_dst, np.int32),
                         np.ascontiguousarray(problem.back_dist, np.int32)]
         rp, col, dl, rt, cap, bs, bd, bk = self._arrays
+        mem = getattr(problem, "mem_units", None)
+        if mem is not None:
+            mem = np.ascontiguousarray(mem, np.float32)
+            self._arrays.append(mem)
         self._p = _Problem(int(problem.n_ops), int(rp[-1]), _np_ptr(rp), _np_ptr(col), _np_ptr(dl),
                            _np_ptr(rt), int(cap.shape[0]), _np_ptr(cap), int(problem.D), int(problem.II),
-                           int(bs.shape[0]), _np_ptr(bs), _np_ptr(bd), _np_ptr(bk))
+                           int(bs.shape[0]), _np_ptr(bs), _np_ptr(bd), _np_ptr(bk),
+                           None if mem is None else _np_ptr(mem))
         self.hp = hparams if hparams is not None else default_hparams()
         self.B = int(B)
         if stream is None:
@@ -226,6 +233,10 @@ class Context:
     def get_usage(self, U):
         import torch
         self._check(load().gaus_get_usage(self._h, _dptr(U, torch.float32, (self.B, self.K, self.T), "U")))
+
+    def get_storage(self, M):
+        import torch
+        self._check(load().gaus_get_storage(self._h, _dptr(M, torch.float32, (self.B, self.T), "M")))
 
     def kernel_timing(self, enable: bool):
         self._check(load().gaus_kernel_timing(self._h, 1 if enable else 0))

@@ -148,12 +148,13 @@ gaus_status dupload(gaus_ctx *c, const T **out, const std::vector<T> &h) {
 struct HostGraph {
     int N = 0, E = 0, K = 0, D = 0, II = 0, nb = 0;
     std::vector<int> row_ptr, col, delay, rtype, bsrc, bdst, bdist;
-    std::vector<float> cap;
+    std::vector<float> cap, bmem;
     std::vector<int> pred_ptr, pred_eid, pred_src;
     std::vector<int> bin_ptr, bin, bout_ptr, bout;
     std::vector<int> level, lvl_ptr, lvl_ops;
     std::vector<int> asap, alap;
     std::vector<int> perm, grp_start, type_grp, grp_of;
+    std::vector<int> big_ops, big_of;
 };
 
 gaus_status validate(const gaus_problem *p, int32_t B) {
@@ -176,6 +177,19 @@ gaus_status validate(const gaus_problem *p, int32_t B) {
         if (p->row_ptr[i + 1] < p->row_ptr[i]) return fail(nullptr, GAUS_E_INVALID_ARG, "row_ptr decreases at %d", i);
     for (int e = 0; e < p->n_edges; ++e)
         if (p->col_idx[e] < 0 || p->col_idx[e] >= N) return fail(nullptr, GAUS_E_INVALID_ARG, "col_idx[%d] out of range", e);
+    {
+        std::vector<int> row;
+        for (int i = 0; i < N; ++i) {
+            row.assign(p->col_idx + p->row_ptr[i], p->col_idx + p->row_ptr[i + 1]);
+            std::sort(row.begin(), row.end());
+            if (std::adjacent_find(row.begin(), row.end()) != row.end())
+                return fail(nullptr, GAUS_E_INVALID_ARG, "duplicate edge from op %d", i);
+        }
+    }
+    if (p->mem_units)
+        for (int i = 0; i < N; ++i)
+            if (!std::isfinite(p->mem_units[i]) || p->mem_units[i] < 0.0f)
+                return fail(nullptr, GAUS_E_INVALID_ARG, "mem_units[%d] must be finite and >= 0", i);
     for (int i = 0; i < N; ++i) {
         if (p->delay[i] < 0 || p->delay[i] > (1 << 20)) return fail(nullptr, GAUS_E_INVALID_ARG, "delay[%d] out of [0, 2^20]", i);
         if (p->rtype[i] < 0 || p->rtype[i] >= p->n_types) return fail(nullptr, GAUS_E_INVALID_ARG, "rtype[%d] out of range", i);
@@ -200,6 +214,8 @@ gaus_status preprocess(const gaus_problem *p, HostGraph &h) {
     h.delay.assign(p->delay, p->delay + N);
     h.rtype.assign(p->rtype, p->rtype + N);
     h.cap.assign(p->capacity, p->capacity + h.K);
+    if (p->mem_units) h.bmem.assign(p->mem_units, p->mem_units + N);
+    else h.bmem.assign(N, 1.0f);
     h.bsrc.assign(p->back_src, p->back_src + h.nb);
     h.bdst.assign(p->back_dst, p->back_dst + h.nb);
     h.bdist.assign(p->back_dist, p->back_dist + h.nb);
@@ -308,6 +324,12 @@ void choose_config(HostGraph &h, int B, LaunchCfg &lc, int &tile, int &ntiles) {
     }
     h.type_grp[h.K] = (int)h.grp_start.size();
     h.grp_start.push_back(h.N);
+    h.big_of.assign(h.N, -1);
+    for (int i = 0; i < h.N; ++i)
+        if (h.pred_ptr[i + 1] - h.pred_ptr[i] > kBigIn) {
+            h.big_of[i] = (int)h.big_ops.size();
+            h.big_ops.push_back(i);
+        }
     h.grp_of.assign(h.N, 0);
     for (size_t gi = 0; gi + 1 < h.grp_start.size(); ++gi)
         for (int q = h.grp_start[gi]; q < h.grp_start[gi + 1]; ++q) h.grp_of[h.perm[q]] = (int)gi;
@@ -331,6 +353,7 @@ void gaus_default_hparams(gaus_hparams *hp) {
     hp->poly_chunk = 0;
     hp->beta_res = 0.0f;
     hp->tau = 1e-2f;
+    hp->gamma_mem = 0.0f;
 }
 
 const char *gaus_status_string(gaus_status s) {
@@ -365,8 +388,8 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     if (!c) return fail(nullptr, GAUS_E_NOMEM, "host allocation failed");
     gaus_hparams hp;
     if (hp_in) hp = *hp_in; else gaus_default_hparams(&hp);
-    c->hp = HP{hp.lr,        hp.beta1,     hp.beta2,     hp.eps,   hp.rho,     hp.lambda0,
-               hp.alpha_com, hp.sigma_min, hp.kappa,     hp.beta_res, hp.tau};
+    c->hp = HP{hp.lr,        hp.beta1,     hp.beta2,     hp.eps,      hp.rho, hp.lambda0,
+               hp.alpha_com, hp.sigma_min, hp.kappa,     hp.beta_res, hp.tau, hp.gamma_mem};
     c->stream = static_cast<hipStream_t>(hip_stream);
     (void)hipGetDevice(&c->device);
     int tile = 0, ntiles = 0;
@@ -375,11 +398,13 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
         delete c;
         return fail(nullptr, GAUS_E_INVALID_ARG, "poly_chunk must be 0 (auto), negative (off) or in [16, 256]");
     }
-    if (!(hp.beta_res >= 0.0f) || !std::isfinite(hp.beta_res) || !(hp.tau > 0.0f) || !std::isfinite(hp.tau)) {
+    if (!(hp.beta_res >= 0.0f) || !std::isfinite(hp.beta_res) || !(hp.tau > 0.0f) || !std::isfinite(hp.tau) ||
+        !(hp.gamma_mem >= 0.0f) || !std::isfinite(hp.gamma_mem)) {
         delete c;
-        return fail(nullptr, GAUS_E_INVALID_ARG, "beta_res must be finite and >= 0, tau finite and > 0");
+        return fail(nullptr, GAUS_E_INVALID_ARG, "beta_res and gamma_mem must be finite and >= 0, tau finite and > 0");
     }
-    setup_poly(h.D, hp.poly_chunk, c->pa);
+    // the storage term's successor products are evaluated step by step only
+    setup_poly(h.D, hp.gamma_mem > 0.0f ? -1 : hp.poly_chunk, c->pa);
 
     Graph &g = c->g;
     g.N = h.N; g.E = h.E; g.K = h.K; g.D = h.D; g.II = h.II; g.T = h.II > 0 ? h.II : h.D;
@@ -402,6 +427,10 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     UP(bout_ptr, h.bout_ptr); UP(bout, h.bout); UP(perm, h.perm); UP(grp_start, h.grp_start);
     UP(type_grp, h.type_grp); UP(lvl_ptr, h.lvl_ptr); UP(lvl_ops, h.lvl_ops); UP(asap, h.asap);
     UP(grp_of, h.grp_of);
+    UP(bmem, h.bmem);
+    UP(big_ops, h.big_ops);
+    UP(big_of, h.big_of);
+    g.nbig = (int)h.big_ops.size();
     UP(alap, h.alap);
 #undef UP
 #define AL(field, n) do { s = dalloc(c, &c->w.field, (n)); if (s != GAUS_OK) goto fail_alloc; } while (0)
@@ -419,6 +448,14 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     AL(lstrip, (size_t)B * h.K * kStripMax);
     AL(lpart, BN * ntiles * 2);
     AL(lpoly, BN * 2);
+    AL(Mpart, (size_t)B * g.ngroups * h.D);
+    AL(mreg, (size_t)B * g.T);
+    AL(mregd, (size_t)B * g.T);
+    AL(msoft, (size_t)B * g.T);
+    AL(lmem, (size_t)B);
+    AL(mown, BN * ntiles * 2);
+    AL(msucc, (size_t)B * h.E * ntiles * 2);
+    AL(bigsum, (size_t)B * std::max<size_t>(h.big_ops.size(), 1) * 6);
     AL(wts, (size_t)B * 4);
     AL(adamf, (size_t)B * 2);
     AL(cls, BN);
@@ -560,6 +597,16 @@ gaus_status gaus_get_usage(gaus_ctx *ctx, float *U) {
     const size_t bytes = sizeof(float) * (size_t)ctx->g.B * ctx->g.K * ctx->g.T;
     hipError_t e = hipMemcpyAsync(U, ctx->w.U, bytes, hipMemcpyDeviceToDevice, ctx->stream);
     if (e != hipSuccess) return hip_fail(ctx, e, "get_usage");
+    return GAUS_OK;
+}
+
+gaus_status gaus_get_storage(gaus_ctx *ctx, float *M) {
+    if (!ctx) return GAUS_E_INVALID_ARG;
+    if (!M) return fail(ctx, GAUS_E_INVALID_ARG, "get_storage: null pointer");
+    if (!(ctx->hp.gamma > 0.0f)) return fail(ctx, GAUS_E_INVALID_ARG, "get_storage: the storage term is off (gamma_mem = 0)");
+    const size_t bytes = sizeof(float) * (size_t)ctx->g.B * ctx->g.T;
+    hipError_t e = hipMemcpyAsync(M, ctx->w.mreg, bytes, hipMemcpyDeviceToDevice, ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "get_storage");
     return GAUS_OK;
 }
 

@@ -16,7 +16,8 @@ constexpr int kCP = 4;   // per (restart, edge, tile): dVdep/dmu_j, dVdep/dsigma
 constexpr int kBP = 5;   // per (restart, back edge, tile): V_rec, dVrec/dmu_j, dVrec/dsigma_j
                          //   (producer j), dVrec/dmu_i, dVrec/dsigma_i (consumer i)
 constexpr int kHalo = 256;  // largest producer delay handled from the LDS row window
-constexpr int kTerms = 6;   // per restart: L, V_dep, V_res, V_rec, L_com, L_res
+constexpr int kBigIn = 64;  // in-degree above which an op's in-edge records are reduced by a work-group
+constexpr int kTerms = 7;   // per restart: L, V_dep, V_res, V_rec, L_com, L_res, L_mem
 
 // Chunk-polynomial path (dense regime).  On a chunk of W consecutive steps
 // with rho = ((W-1)/2)/sigma <= kRhoMax the CDF row of an op is a degree-kDeg
@@ -58,6 +59,9 @@ struct Graph {
     const int *type_grp;                 // [K+1] groups of type k: [type_grp[k], type_grp[k+1])
     const int *lvl_ptr, *lvl_ops;        // ops by (topological level, id)
     const int *grp_of;                   // [N] group of each op
+    const float *bmem;                   // [N] storage units b_i
+    int nbig;                            // ops with more than kBigIn predecessors
+    const int *big_ops, *big_of;         // [nbig] those ops; [N] index into them or -1
     const int *asap, *alap;
 };
 
@@ -77,6 +81,14 @@ struct Work {
     float *lstrip;    // [B][K][kStripMax] the same differences at the strip positions
     float *lpart;     // [B][N][tiles][2]  smooth-peak gradient (mu, sigma) of step-by-step ops, per tile
     float *lpoly;     // [B][N][2]         the same for ops on the polynomial path
+    double *Mpart;    // [B][ngroups][D]   expected storage units of a group's ops per step
+    double *mregd;    // [B][T]            expected storage units per (modulo) slot
+    float *mreg;      // [B][T]            the same in float (gaus_get_storage)
+    float *msoft;     // [B][T]            gamma * dL_mem/dMReg (softmax over the slots)
+    float *lmem;      // [B]               smooth peak storage L_mem
+    float *mown;      // [B][N][tiles][2]  storage gradient of an op as the holder, per tile
+    float *msucc;     // [B][E][tiles][2]  storage gradient of an edge's consumer, per tile
+    double *bigsum;   // [B][nbig][6]      in-edge records of the high in-degree ops, reduced
     float *wts;       // [B][4]            w_dep, w_res, w_rec, unused
     float *adamf;     // [B][2]            Adam bias corrections 1-beta1^t, 1-beta2^t
     unsigned char *cls;  // [B][N]          1 = op on the chunk-polynomial path this iteration
@@ -98,6 +110,7 @@ struct Work {
 struct HP {
     float lr, b1, b2, eps, rho, lambda0, alpha, sigma_min, kappa;
     float beta, tau;   // weight and temperature of the smooth peak usage L_res
+    float gamma;       // weight of the smooth peak storage L_mem (same temperature)
 };
 
 // Kernel-side configuration chosen on the host from (N, D, B).
@@ -130,6 +143,10 @@ hipError_t launch_ops(const Graph &g, const Work &w, const LaunchCfg &lc, const 
 hipError_t launch_back(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu, const float *sigma,
                        hipStream_t st);
 hipError_t launch_lse_ops(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu,
+                          const float *sigma, hipStream_t st);
+hipError_t launch_mem_fwd(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu,
+                          const float *sigma, hipStream_t st);
+hipError_t launch_mem_bwd(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu,
                           const float *sigma, hipStream_t st);
 hipError_t launch_poly(const Graph &g, const Work &w, const PolyArgs &pa, const float *mu, const float *sigma,
                        hipStream_t st);

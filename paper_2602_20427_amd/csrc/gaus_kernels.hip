@@ -48,7 +48,6 @@ namespace gaus {
 __global__ void k_classify(Graph G, PolyArgs pa, const float *__restrict__ sigma, Work W) {
     const int b = blockIdx.y;
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < G.ngroups) W.gflag[(size_t)b * G.ngroups + i] = 0;
     if (i >= G.N) return;
     const float s = sigma[(size_t)b * G.N + i];
     W.cls[(size_t)b * G.N + i] = (pa.enabled && s >= pa.sig_thr && G.delay[i] <= kSmax) ? 1 : 0;
@@ -56,15 +55,20 @@ __global__ void k_classify(Graph G, PolyArgs pa, const float *__restrict__ sigma
 
 // Which ops (and groups) have step-by-step work this iteration: ops off the
 // polynomial path, and polynomial ops with an out-edge to such an op.
-__global__ void k_flags(Graph G, Work W) {
-    const int b = blockIdx.y;
-    const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= G.N) return;
+// Work-group = (op group, restart); groups hold at most 256 ops.
+__global__ __launch_bounds__(256) void k_flags(Graph G, Work W) {
+    const int grp = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+    const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
     const unsigned char *clsb = W.cls + (size_t)b * G.N;
-    int d = clsb[i] ? 0 : 1;
-    for (int e = G.row_ptr[i]; e < G.row_ptr[i + 1] && !d; ++e) d = clsb[G.col[e]] ? 0 : 1;
-    W.dflag[(size_t)b * G.N + i] = (unsigned char)d;
-    if (d) atomicOr(&W.gflag[(size_t)b * G.ngroups + G.grp_of[i]], 1);
+    int d = 0;
+    if (q0 + tid < q1) {
+        const int i = G.perm[q0 + tid];
+        d = clsb[i] ? 0 : 1;
+        for (int e = G.row_ptr[i]; e < G.row_ptr[i + 1] && !d; ++e) d = clsb[G.col[e]] ? 0 : 1;
+        W.dflag[(size_t)b * G.N + i] = (unsigned char)d;
+    }
+    d = __syncthreads_or(d);
+    if (tid == 0) W.gflag[(size_t)b * G.ngroups + grp] = d ? 1 : 0;
 }
 
 // ---------------------------------------------------------------------------
@@ -266,6 +270,45 @@ __global__ __launch_bounds__(kTermsBS) void k_vres(Graph G, Work W, HP hp) {
 }
 
 // ---------------------------------------------------------------------------
+// Expected storage units per (modulo) slot: the groups' partials summed and
+// folded (eq:active, App. B.3); then per restart the smooth peak
+// L_mem = M + tau log sum_t exp((MReg(t) - M)/tau) and gamma times its
+// derivative (a softmax) per slot.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_mreg(Graph G, Work W) {
+    const int slot = blockIdx.x * 256 + threadIdx.x, b = blockIdx.y;
+    if (slot >= G.T) return;
+    double acc = 0.0;
+    for (int t = slot; t < G.D; t += G.T)
+        for (int g = 0; g < G.ngroups; ++g) acc += W.Mpart[((size_t)b * G.ngroups + g) * G.D + t];
+    W.mregd[(size_t)b * G.T + slot] = acc;
+    W.mreg[(size_t)b * G.T + slot] = (float)acc;
+}
+
+__global__ __launch_bounds__(kTermsBS) void k_mem_lse(Graph G, Work W, HP hp) {
+    __shared__ float scratch[kTermsBS / 64];
+    const int b = blockIdx.x, tid = threadIdx.x, T = G.T;
+    const double *mr = W.mregd + (size_t)b * T;
+    // the maximum in fp64 (the profile's own precision), exponents in fp32
+    __shared__ double dmax[kTermsBS / 64];
+    double mx = -INFINITY;
+    for (int c = tid; c < T; c += kTermsBS) mx = fmax(mx, mr[c]);
+    for (int off = 32; off > 0; off >>= 1) mx = fmax(mx, __shfl_xor(mx, off, 64));
+    if ((tid & 63) == 0) dmax[tid >> 6] = mx;
+    __syncthreads();
+    mx = dmax[0];
+    for (int w = 1; w < kTermsBS / 64; ++w) mx = fmax(mx, dmax[w]);
+    const float itau = 1.0f / hp.tau;
+    float z = 0.0f;
+    for (int c = tid; c < T; c += kTermsBS) z += expf((float)(mr[c] - mx) * itau);
+    z = block_sum1024(z, scratch);
+    if (tid == 0) W.lmem[b] = (float)(mx + (double)hp.tau * log((double)z));
+    const float gz = hp.gamma / z;
+    float *ms = W.msoft + (size_t)b * T;
+    for (int c = tid; c < T; c += kTermsBS) ms[c] = gz * expf((float)(mr[c] - mx) * itau);
+}
+
+// ---------------------------------------------------------------------------
 // Per restart: V_res, V_dep, L_com, V_rec from the partials, the augmented
 // Lagrangian (eq. 11), the weights w_c = lambda_c + rho V_c, and in step mode
 // the multiplier update lambda_c += rho V_c and the Adam bias corrections.
@@ -316,14 +359,15 @@ __global__ __launch_bounds__(kCombineBS) void k_combine(Graph G, PolyArgs pa, Wo
     if (tid == 0) {
         const float V[3] = {vdep, vres, vrec};
         const float *lam = lambda_in + (size_t)b * 3;
-        float L = fmaf(hp.beta, lres, hp.alpha * lcom);
+        const float lmem = hp.gamma != 0.0f ? W.lmem[b] : 0.0f;
+        float L = fmaf(hp.gamma, lmem, fmaf(hp.beta, lres, hp.alpha * lcom));
         float w[3];
         for (int c = 0; c < 3; ++c) {
             L += lam[c] * V[c] + 0.5f * hp.rho * V[c] * V[c];
             w[c] = lam[c] + hp.rho * V[c];
         }
         float *tm = W.terms + (size_t)b * kTerms;
-        tm[0] = L; tm[1] = vdep; tm[2] = vres; tm[3] = vrec; tm[4] = lcom; tm[5] = lres;
+        tm[0] = L; tm[1] = vdep; tm[2] = vres; tm[3] = vrec; tm[4] = lcom; tm[5] = lres; tm[6] = lmem;
         if (terms_out) for (int c = 0; c < kTerms; ++c) terms_out[(size_t)b * kTerms + c] = tm[c];
         float *wt = W.wts + (size_t)b * 4;
         wt[0] = w[0]; wt[1] = w[1]; wt[2] = w[2]; wt[3] = 0.0f;
@@ -354,6 +398,45 @@ __device__ __forceinline__ float combine_grad(float w_res, float r, float w_dep,
 }
 
 // ---------------------------------------------------------------------------
+// In-edge records of the ops with more than kBigIn predecessors (a sink
+// joined to every leaf has thousands), reduced by one work-group each in
+// fp64 and a fixed order: consumer-side dependency / edge-length derivatives
+// and, with the storage term, the successor-side storage derivatives.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_gather_big(Graph G, Work W, HP hp) {
+    __shared__ double sRed[4][6];
+    const int x = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+    const int lane = tid & 63, wid = tid >> 6;
+    const int i = G.big_ops[x], N = G.N, nt = G.ntiles;
+    const bool poly_i = W.cls[(size_t)b * N + i] != 0;
+    double acc[6] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
+    for (int q = G.pred_ptr[i] + tid; q < G.pred_ptr[i + 1]; q += 256) {
+        const int e = G.pred_eid[q];
+        if (poly_i && W.cls[(size_t)b * N + G.pred_src[q]]) {
+            const float *cp = W.cpoly + ((size_t)b * G.E + e) * kCP;
+            for (int c = 0; c < 4; ++c) acc[c] += cp[c];
+        } else {
+            const float *cp = W.cpart + (((size_t)b * G.E + e) * nt) * kCP;
+            for (int tl = 0; tl < nt; ++tl)
+                for (int c = 0; c < 4; ++c) acc[c] += cp[tl * kCP + c];
+        }
+        if (hp.gamma != 0.0f) {
+            const float *sp = W.msucc + ((size_t)b * G.E + e) * nt * 2;
+            for (int tl = 0; tl < nt; ++tl) { acc[4] += sp[tl * 2 + 0]; acc[5] += sp[tl * 2 + 1]; }
+        }
+    }
+#pragma unroll
+    for (int c = 0; c < 6; ++c) {
+        double v = acc[c];
+        for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+        if (lane == 0) sRed[wid][c] = v;
+    }
+    __syncthreads();
+    if (tid < 6)
+        W.bigsum[((size_t)b * G.nbig + x) * 6 + tid] = (sRed[0][tid] + sRed[1][tid]) + (sRed[2][tid] + sRed[3][tid]);
+}
+
+// ---------------------------------------------------------------------------
 // Gradient assembly (+ Adam in step mode).  Thread per (restart, op):
 //   dL/dth_i = w_res dVres/dth_i + w_dep dVdep/dth_i + w_rec dVrec/dth_i + alpha dLcom/dth_i
 // dVres/dth_i = sum over bin edges t where the ReLU indicator of the op's type
@@ -378,7 +461,9 @@ __global__ __launch_bounds__(256) void k_final(Graph G, Work W, HP hp, const flo
     const int k = G.rtype[i];
     const int nt_k = W.ntrans[(size_t)b * G.K + k];
     const int *tr = W.trans + ((size_t)b * G.K + k) * G.D;
-    float rm = 0.0f, rsg = 0.0f;
+    // partial sums in fp64: an op can collect thousands of edge records
+    // (e.g. a sink joined to every leaf)
+    double rm = 0.0, rsg = 0.0;
     for (int q = 0; q < nt_k; ++q) {
         const int code = tr[q];
         const float sgn = code > 0 ? 1.0f : -1.0f;
@@ -386,11 +471,11 @@ __global__ __launch_bounds__(256) void k_final(Graph G, Work W, HP hp, const flo
         const float z = ((float)t + 0.5f - m_i) * rs;
         const float g = __builtin_amdgcn_exp2f(-(z * z) * kHalfLog2e);
         const float Fm = -g * cinv;
-        rm = fmaf(sgn, Fm, rm);
-        rsg = fmaf(sgn, Fm * z, rsg);
+        rm += (double)(sgn * Fm);
+        rsg += (double)(sgn * (Fm * z));
     }
 
-    float dm = 0.0f, ds = 0.0f, cm = 0.0f, cs = 0.0f;
+    double dm = 0.0, ds = 0.0, cm = 0.0, cs = 0.0;
     if (W.dflag[bi]) {
         const float *pp = W.ppart + bi * nt * kPP;
         for (int tl = 0; tl < nt; ++tl) {
@@ -401,7 +486,10 @@ __global__ __launch_bounds__(256) void k_final(Graph G, Work W, HP hp, const flo
     const float *ppy = W.ppoly + bi * kPP;
     dm += ppy[2]; ds += ppy[3]; cm += ppy[4]; cs += ppy[5];
     const bool poly_i = W.cls[bi] != 0;
-    for (int q = G.pred_ptr[i]; q < G.pred_ptr[i + 1]; ++q) {
+    const int big = G.big_of[i];
+    const double *bsum = big >= 0 ? W.bigsum + ((size_t)b * G.nbig + big) * 6 : nullptr;
+    if (bsum) { dm += bsum[0]; ds += bsum[1]; cm += bsum[2]; cs += bsum[3]; }
+    for (int q = bsum ? G.pred_ptr[i + 1] : G.pred_ptr[i]; q < G.pred_ptr[i + 1]; ++q) {
         const int e = G.pred_eid[q];
         if (poly_i && W.cls[(size_t)b * N + G.pred_src[q]]) {
             const float *cp = W.cpoly + ((size_t)b * G.E + e) * kCP;
@@ -414,7 +502,7 @@ __global__ __launch_bounds__(256) void k_final(Graph G, Work W, HP hp, const flo
             cm += cp[tl * kCP + 2]; cs += cp[tl * kCP + 3];
         }
     }
-    float qm = 0.0f, qs = 0.0f;
+    double qm = 0.0, qs = 0.0;
     for (int q = G.bout_ptr[i]; q < G.bout_ptr[i + 1]; ++q) {
         const float *bp = W.bpart + (((size_t)b * G.nb + G.bout[q]) * nt) * kBP;
         for (int tl = 0; tl < nt; ++tl) { qm += bp[tl * kBP + 1]; qs += bp[tl * kBP + 2]; }
@@ -423,18 +511,31 @@ __global__ __launch_bounds__(256) void k_final(Graph G, Work W, HP hp, const flo
         const float *bp = W.bpart + (((size_t)b * G.nb + G.bin[q]) * nt) * kBP;
         for (int tl = 0; tl < nt; ++tl) { qm += bp[tl * kBP + 3]; qs += bp[tl * kBP + 4]; }
     }
-    float g_mu = combine_grad(w_res, rm, w_dep, dm, w_rec, qm, hp.alpha, cm);
-    float g_sg = combine_grad(w_res, rsg, w_dep, ds, w_rec, qs, hp.alpha, cs);
+    float g_mu = combine_grad(w_res, (float)rm, w_dep, (float)dm, w_rec, (float)qm, hp.alpha, (float)cm);
+    float g_sg = combine_grad(w_res, (float)rsg, w_dep, (float)ds, w_rec, (float)qs, hp.alpha, (float)cs);
     if (hp.beta != 0.0f) {   // smooth peak usage, already weighted by beta
-        float lm = 0.0f, ls = 0.0f;
+        double lm = 0.0, ls = 0.0;
         if (poly_i) {
             lm = W.lpoly[bi * 2 + 0]; ls = W.lpoly[bi * 2 + 1];
         } else {
             const float *lp = W.lpart + bi * nt * 2;
             for (int tl = 0; tl < nt; ++tl) { lm += lp[tl * 2 + 0]; ls += lp[tl * 2 + 1]; }
         }
-        g_mu = __fadd_rn(g_mu, lm);
-        g_sg = __fadd_rn(g_sg, ls);
+        g_mu = __fadd_rn(g_mu, (float)lm);
+        g_sg = __fadd_rn(g_sg, (float)ls);
+    }
+    if (hp.gamma != 0.0f) {   // smooth peak storage, already weighted by gamma
+        double om = 0.0, os = 0.0;
+        const float *op = W.mown + bi * nt * 2;
+        if (G.row_ptr[i + 1] > G.row_ptr[i])
+            for (int tl = 0; tl < nt; ++tl) { om += op[tl * 2 + 0]; os += op[tl * 2 + 1]; }
+        if (bsum) { om += bsum[4]; os += bsum[5]; }
+        for (int q = bsum ? G.pred_ptr[i + 1] : G.pred_ptr[i]; q < G.pred_ptr[i + 1]; ++q) {
+            const float *sp = W.msucc + ((size_t)b * G.E + G.pred_eid[q]) * nt * 2;
+            for (int tl = 0; tl < nt; ++tl) { om += sp[tl * 2 + 0]; os += sp[tl * 2 + 1]; }
+        }
+        g_mu = __fadd_rn(g_mu, (float)om);
+        g_sg = __fadd_rn(g_sg, (float)os);
     }
 
     if (mode == 0) {
@@ -582,10 +683,9 @@ __global__ __launch_bounds__(kLegBS) void k_legalize(Graph G, Work W, const floa
 hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const LaunchCfg &lc,
                              const PolyArgs &pa, const IterArgs &a, hipStream_t st) {
     {
-        dim3 grid((std::max(g.N, g.ngroups) + 255) / 256, g.B);
+        dim3 grid((g.N + 255) / 256, g.B);
         hipLaunchKernelGGL(k_classify, grid, dim3(256), 0, st, g, pa, a.sigma, w);
-        dim3 grid2((g.N + 255) / 256, g.B);
-        hipLaunchKernelGGL(k_flags, grid2, dim3(256), 0, st, g, w);
+        hipLaunchKernelGGL(k_flags, dim3(g.ngroups, g.B), dim3(256), 0, st, g, w);
     }
     hipError_t e;
     if (a.ops_begin) (void)hipEventRecord(a.ops_begin, st);
@@ -601,6 +701,11 @@ hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const 
         hipLaunchKernelGGL(k_ucoef, dim3((pa.nc * kNC + pa.SP + 63) / 64, g.K, g.B), dim3(256), 0, st, g, pa, w);
     hipLaunchKernelGGL(k_usage, dim3((g.T + kUsageBS - 1) / kUsageBS, g.K, g.B), dim3(kUsageBS), 0, st, g, pa, w);
     hipLaunchKernelGGL(k_vres, dim3(g.K, g.B), dim3(kTermsBS), 0, st, g, w, hp);
+    if (hp.gamma != 0.0f) {   // expected storage units and their smooth peak
+        if ((e = launch_mem_fwd(g, w, lc, a.mu, a.sigma, st)) != hipSuccess) return e;
+        hipLaunchKernelGGL(k_mreg, dim3((g.T + 255) / 256, g.B), dim3(256), 0, st, g, w);
+        hipLaunchKernelGGL(k_mem_lse, dim3(g.B), dim3(kTermsBS), 0, st, g, w, hp);
+    }
     hipLaunchKernelGGL(k_combine, dim3(g.B), dim3(kCombineBS), 0, st, g, pa, w, hp, a.lambda_in,
                        a.mode == 1 ? a.lambda_out : nullptr, a.mode == 1 ? a.adam_t : nullptr,
                        a.terms_out);
@@ -608,6 +713,8 @@ hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const 
         if ((e = launch_lse_ops(g, w, lc, a.mu, a.sigma, st)) != hipSuccess) return e;
         if (pa.enabled && (e = launch_lse_poly(g, w, pa, a.mu, a.sigma, st)) != hipSuccess) return e;
     }
+    if (hp.gamma != 0.0f && (e = launch_mem_bwd(g, w, lc, a.mu, a.sigma, st)) != hipSuccess) return e;
+    if (g.nbig > 0) hipLaunchKernelGGL(k_gather_big, dim3(g.nbig, g.B), dim3(256), 0, st, g, w, hp);
     {
         dim3 grid((g.N + 255) / 256, g.B);
         hipLaunchKernelGGL(k_final, grid, dim3(256), 0, st, g, w, hp, a.mu, a.sigma, a.gmu, a.gsig,

@@ -340,6 +340,150 @@ __global__ __launch_bounds__(BS) void k_lse_ops(Graph G, const float *__restrict
 
 
 // ---------------------------------------------------------------------------
+// Expected storage units (eq:active): op h holds b_h units at step t with
+// probability F_h(t) (1 - Q_h(t)), Q_h(t) = prod over successors F_j(t).
+// Q and R = 1 - Q are carried together (R += Q (1 - F_j), Q *= F_j) with
+// 1 - F_j from the tail, so R keeps full precision when every F_j is near 1.
+// Work-group = (type-pure op group, tile of steps, restart); each thread
+// owns SPT steps and sums the group's ops into Mpart (no atomics).  The sums
+// are kept in fp64: the profile reaches 1e5 units and more, and its
+// LogSumExp weights amplify absolute errors by 1/tau.
+// ---------------------------------------------------------------------------
+template <int BS, int SPT>
+__global__ __launch_bounds__(BS) void k_mem_fwd(Graph G, const float *__restrict__ mu,
+                                                const float *__restrict__ sigma, Work W) {
+    constexpr int TILE = BS * SPT;
+    __shared__ int sI[BS];
+    __shared__ float sMu[BS], sRs[BS];
+    const int grp = blockIdx.x, tile = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
+    const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
+    const int N = G.N, D = G.D;
+    const int t0 = tile * TILE;
+    const float *mub = mu + (size_t)b * N, *sgb = sigma + (size_t)b * N;
+    sI[tid] = -1;
+    if (q0 + tid < q1) {
+        const int i = G.perm[q0 + tid];
+        if (G.row_ptr[i + 1] > G.row_ptr[i]) sI[tid] = i;   // an op without successors holds nothing
+        sMu[tid] = mub[i];
+        sRs[tid] = 1.0f / sgb[i];
+    }
+    __syncthreads();
+    double acc[SPT];
+#pragma unroll
+    for (int j = 0; j < SPT; ++j) acc[j] = 0.0;
+    for (int q = 0; q < q1 - q0; ++q) {
+        const int i = sI[q];
+        if (i < 0) continue;
+        const float m = sMu[q], rs = sRs[q], bi = G.bmem[i];
+        float Fi[SPT], Q[SPT], R[SPT];
+#pragma unroll
+        for (int j = 0; j < SPT; ++j) {
+            Fi[j] = st_F(st_at((long long)t0 + tid + j * BS, D, m, rs));
+            Q[j] = 1.0f; R[j] = 0.0f;
+        }
+        for (int e = G.row_ptr[i]; e < G.row_ptr[i + 1]; ++e) {
+            const int k = G.col[e];
+            const float mk = mub[k], rk = 1.0f / sgb[k];
+#pragma unroll
+            for (int j = 0; j < SPT; ++j) {
+                const float st = st_at((long long)t0 + tid + j * BS, D, mk, rk);
+                R[j] = fmaf(Q[j], st_1mF(st), R[j]);
+                Q[j] *= st_F(st);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < SPT; ++j) acc[j] += (double)(bi * Fi[j] * R[j]);
+    }
+    double *mp = W.Mpart + ((size_t)b * G.ngroups + grp) * D;
+#pragma unroll
+    for (int j = 0; j < SPT; ++j) {
+        const int t = t0 + tid + j * BS;
+        if (t < D) mp[t] = acc[j];
+    }
+}
+
+// Gradient of gamma L_mem with c(t) = gamma softmax(MReg / tau) at slot
+// t mod T, over the interior bin edges t = 0..D-2:
+//   as the holder:      c(t) b_h (1 - Q_h(t)) dF_h(t)/dth_h
+//   as a successor i:  -c(t) b_h F_h(t) prod_{j != i} F_j(t) dF_i(t)/dth_i
+// with prod_{j != i} F_j = Q_h / F_i (0 when F_i underflows: then so does
+// dF_i, and the term is below fp32 resolution).
+template <int BS, int SPT>
+__global__ __launch_bounds__(BS) void k_mem_bwd(Graph G, const float *__restrict__ mu,
+                                                const float *__restrict__ sigma, Work W) {
+    constexpr int TILE = BS * SPT;
+    __shared__ float sW[TILE];
+    __shared__ int sI[BS];
+    __shared__ float sMu[BS], sRs[BS];
+    __shared__ float sRed[2][BS / 64][8];
+    const int grp = blockIdx.x, tile = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
+    const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
+    const int N = G.N, D = G.D, T = G.T, nt = G.ntiles;
+    const int t0 = tile * TILE;
+    const float *mub = mu + (size_t)b * N, *sgb = sigma + (size_t)b * N;
+    sI[tid] = -1;
+    if (q0 + tid < q1) {
+        const int i = G.perm[q0 + tid];
+        if (G.row_ptr[i + 1] > G.row_ptr[i]) sI[tid] = i;
+        sMu[tid] = mub[i];
+        sRs[tid] = 1.0f / sgb[i];
+    }
+    const float *ms = W.msoft + (size_t)b * T;
+    for (int x = tid; x < TILE; x += BS) {
+        const int t = t0 + x;
+        sW[x] = t <= D - 2 ? ms[t % T] : 0.0f;
+    }
+    __syncthreads();
+    int par = 0;
+    for (int q = 0; q < q1 - q0; ++q) {
+        const int h = sI[q];
+        if (h < 0) continue;
+        const float m = sMu[q], rs = sRs[q], cinv = rs * kInvSqrt2Pi, bh = G.bmem[h];
+        const int e0 = G.row_ptr[h], e1 = G.row_ptr[h + 1];
+        float Fh[SPT], Q[SPT], R[SPT], own[2] = {0.0f, 0.0f};
+#pragma unroll
+        for (int j = 0; j < SPT; ++j) {
+            float st, Fm, Fs;
+            cdf_at((long long)t0 + tid + j * BS, D, m, rs, cinv, st, Fm, Fs);
+            Fh[j] = st_F(st);
+            Q[j] = 1.0f; R[j] = 0.0f;
+            for (int e = e0; e < e1; ++e) {
+                const int k = G.col[e];
+                const float sk = st_at((long long)t0 + tid + j * BS, D, mub[k], 1.0f / sgb[k]);
+                R[j] = fmaf(Q[j], st_1mF(sk), R[j]);
+                Q[j] *= st_F(sk);
+            }
+            const float wr = sW[tid + j * BS] * bh * R[j];
+            own[0] = fmaf(wr, Fm, own[0]);
+            own[1] = fmaf(wr, Fs, own[1]);
+        }
+        {
+            const float r = block_sum<2, BS>(own, sRed[par]);
+            par ^= 1;
+            if (tid < 2) W.mown[(((size_t)b * N + h) * nt + tile) * 2 + tid] = r;
+        }
+        for (int e = e0; e < e1; ++e) {
+            const int k = G.col[e];
+            const float mk = mub[k], rk = 1.0f / sgb[k], ck = rk * kInvSqrt2Pi;
+            float acc[2] = {0.0f, 0.0f};
+#pragma unroll
+            for (int j = 0; j < SPT; ++j) {
+                float st, Fm, Fs;
+                cdf_at((long long)t0 + tid + j * BS, D, mk, rk, ck, st, Fm, Fs);
+                const float Fk = st_F(st);
+                const float others = Fk > 0.0f ? Q[j] / Fk : 0.0f;
+                const float c = -sW[tid + j * BS] * bh * Fh[j] * others;
+                acc[0] = fmaf(c, Fm, acc[0]);
+                acc[1] = fmaf(c, Fs, acc[1]);
+            }
+            const float r = block_sum<2, BS>(acc, sRed[par]);
+            par ^= 1;
+            if (tid < 2) W.msucc[(((size_t)b * G.E + e) * nt + tile) * 2 + tid] = r;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
 hipError_t launch_ops(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu, const float *sigma,
@@ -368,6 +512,24 @@ hipError_t launch_lse_ops(const Graph &g, const Work &w, const LaunchCfg &lc, co
     if (lc.bs == 64) hipLaunchKernelGGL((k_lse_ops<64, 1>), grid, dim3(64), 0, st, g, mu, sigma, w);
     else if (lc.spt == 1) hipLaunchKernelGGL((k_lse_ops<256, 1>), grid, dim3(256), 0, st, g, mu, sigma, w);
     else hipLaunchKernelGGL((k_lse_ops<256, 4>), grid, dim3(256), 0, st, g, mu, sigma, w);
+    return hipSuccess;
+}
+
+hipError_t launch_mem_fwd(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu,
+                          const float *sigma, hipStream_t st) {
+    const dim3 grid(g.ngroups, g.ntiles, g.B);
+    if (lc.bs == 64) hipLaunchKernelGGL((k_mem_fwd<64, 1>), grid, dim3(64), 0, st, g, mu, sigma, w);
+    else if (lc.spt == 1) hipLaunchKernelGGL((k_mem_fwd<256, 1>), grid, dim3(256), 0, st, g, mu, sigma, w);
+    else hipLaunchKernelGGL((k_mem_fwd<256, 4>), grid, dim3(256), 0, st, g, mu, sigma, w);
+    return hipSuccess;
+}
+
+hipError_t launch_mem_bwd(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu,
+                          const float *sigma, hipStream_t st) {
+    const dim3 grid(g.ngroups, g.ntiles, g.B);
+    if (lc.bs == 64) hipLaunchKernelGGL((k_mem_bwd<64, 1>), grid, dim3(64), 0, st, g, mu, sigma, w);
+    else if (lc.spt == 1) hipLaunchKernelGGL((k_mem_bwd<256, 1>), grid, dim3(256), 0, st, g, mu, sigma, w);
+    else hipLaunchKernelGGL((k_mem_bwd<256, 4>), grid, dim3(256), 0, st, g, mu, sigma, w);
     return hipSuccess;
 }
 

@@ -206,3 +206,31 @@ def restart_uniforms(n_ops: int, B: int, seed: int) -> np.ndarray:
     [ASAP, ALAP] window (the library and the oracle both take these as input)."""
     rng = np.random.Generator(np.random.PCG64(seed + 15485863))
     return rng.random((B, n_ops))
+
+
+def with_storage(prob: Problem, seed: int, bits=(1, 8, 16, 32)) -> Problem:
+    """The same graph prepared for the storage (memory-footprint) objective of
+    Formulations B and C: every op's output gets a bit width drawn from `bits`
+    as its storage units, and one sink op is appended as a successor of every
+    op without successors, so that their outputs are held until the end
+    (the footnote to the memory-footprint definition, Sec. 2.1).  The sink has
+    storage 0, delay 0 and a resource type of its own that never binds."""
+    rng = np.random.default_rng(seed)
+    n = prob.n_ops
+    mem = rng.choice(np.asarray(bits, np.float32), size=n).astype(np.float32)
+    leaves = [i for i in range(n) if prob.row_ptr[i + 1] == prob.row_ptr[i]]
+    rows = [list(prob.col_idx[prob.row_ptr[i]:prob.row_ptr[i + 1]]) for i in range(n)]
+    for i in leaves:
+        rows[i].append(n)
+    rows.append([])
+    row_ptr = np.zeros(n + 2, np.int32)
+    row_ptr[1:] = np.cumsum([len(r) for r in rows])
+    col = np.array([j for r in rows for j in r], np.int32)
+    K = prob.n_types
+    return Problem(n_ops=n + 1, row_ptr=row_ptr, col_idx=col,
+                   delay=np.append(prob.delay, 0).astype(np.int32),
+                   rtype=np.append(prob.rtype, K).astype(np.int32),
+                   capacity=np.append(prob.capacity, np.float32(n + 1)).astype(np.float32),
+                   D=prob.D, II=prob.II, back_src=prob.back_src, back_dst=prob.back_dst,
+                   back_dist=prob.back_dist, layer=None, name=prob.name + "+sink",
+                   mem_units=np.append(mem, np.float32(0.0)).astype(np.float32))

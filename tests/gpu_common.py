@@ -58,7 +58,7 @@ def compare_restart(g, o_terms, o_U, o_gm, o_gs, b, what=""):
     """Assert the parity bar for restart b; returns the worst relative errors."""
     t, ot = g["terms"][b], o_terms
     err_t = np.abs(t - ot) / np.maximum(np.abs(ot), 1.0)
-    names = ["L", "V_dep", "V_res", "V_rec", "L_com", "L_res"]
+    names = ["L", "V_dep", "V_res", "V_rec", "L_com", "L_res", "L_mem"]
     assert err_t.max() <= TOL, f"{what} b={b} terms {dict(zip(names, t))} vs {dict(zip(names, ot))} err {err_t}"
     eu = np.abs(g["U"][b] - o_U).max() / max(np.abs(o_U).max(), 1.0)
     assert eu <= TOL, f"{what} b={b} usage err {eu}"

@@ -45,9 +45,11 @@ def _init(lib, p, B=1):
     arrs = [np.ascontiguousarray(x) for x in (p.row_ptr, p.col_idx, p.delay, p.rtype, p.capacity,
                                               p.back_src, p.back_dst, p.back_dist)]
     ptr = lambda a: a.ctypes.data_as(C.c_void_p)
+    mem = None if p.mem_units is None else np.ascontiguousarray(p.mem_units, np.float32)
     prob = bd._Problem(p.n_ops, int(p.row_ptr[-1]) if len(p.row_ptr) else 0, ptr(arrs[0]), ptr(arrs[1]),
                        ptr(arrs[2]), ptr(arrs[3]), len(p.capacity), ptr(arrs[4]), p.D, p.II,
-                       len(p.back_src), ptr(arrs[5]), ptr(arrs[6]), ptr(arrs[7]))
+                       len(p.back_src), ptr(arrs[5]), ptr(arrs[6]), ptr(arrs[7]),
+                       None if mem is None else ptr(mem))
     h = C.c_void_p(12345)
     st = lib.gaus_init(C.byref(prob), None, B, None, C.byref(h))
     return st, h.value, lib.gaus_last_error(None).decode()
@@ -68,6 +70,10 @@ def _chain(**kw):
     (dict(delay=np.array([1, -1, 1], np.int32)), bd.E_INVALID_ARG, "delay"),
     (dict(capacity=np.array([np.nan], np.float32)), bd.E_INVALID_ARG, "capacity"),
     (dict(D=0), bd.E_INVALID_ARG, "D must"),
+    (dict(row_ptr=np.array([0, 2, 3, 3], np.int32), col_idx=np.array([1, 1, 2], np.int32)),
+     bd.E_INVALID_ARG, "duplicate edge"),
+    (dict(mem_units=np.array([1.0, -1.0, 1.0], np.float32)), bd.E_INVALID_ARG, "mem_units"),
+    (dict(mem_units=np.array([1.0, np.inf, 1.0], np.float32)), bd.E_INVALID_ARG, "mem_units"),
     (dict(D=2), bd.E_HORIZON, "horizon"),
     (dict(row_ptr=np.array([0, 1, 2, 3], np.int32), col_idx=np.array([1, 2, 0], np.int32)), bd.E_CYCLE, "cycle"),
     (dict(II=0, back_src=np.array([2], np.int32), back_dst=np.array([0], np.int32),
