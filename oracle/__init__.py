@@ -59,6 +59,8 @@ def _load():
         lib.orc_edge_terms_double_sum.restype = None
         lib.orc_adam.argtypes = [i64, vp, vp, vp, vp, i32, dbl, dbl, dbl, dbl]
         lib.orc_adam.restype = None
+        lib.orc_schedule_cost.argtypes = [P, vp, dbl, dbl, dbl, vp]
+        lib.orc_schedule_cost.restype = C.c_int
         lib.orc_legalize.argtypes = [P, vp, vp]
         lib.orc_legalize.restype = C.c_int
         lib.orc_asap_alap.argtypes = [P, vp, vp]
@@ -178,6 +180,21 @@ def legalize(prob, mu):
         st[b] = lib.orc_legalize(C.byref(op.s), _ptr(m), _ptr(s))
         out[b] = s
     return out, st
+
+
+def schedule_cost(prob, sched, alpha=0.0, beta=0.0, gamma=0.0):
+    """Discrete cost of integer schedules sched [B,N]: [B,6] = (cost, L_com,
+    L_res, L_mem, V_res, legal)."""
+    lib, op = _load(), _op(prob)
+    sched = np.atleast_2d(np.asarray(sched, np.int64))
+    out = np.zeros((sched.shape[0], 6))
+    for b in range(sched.shape[0]):
+        sb = np.ascontiguousarray(sched[b]); o = np.zeros(6)
+        rc = lib.orc_schedule_cost(C.byref(op.s), _ptr(sb), float(alpha), float(beta), float(gamma), _ptr(o))
+        if rc != OK:
+            raise RuntimeError(f"oracle schedule_cost failed: {rc}")
+        out[b] = o
+    return out
 
 
 def asap_alap(prob):

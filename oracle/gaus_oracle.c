@@ -499,6 +499,65 @@ void orc_adam(int64_t n, double *theta, double *m, double *v, const double *g, i
     }
 }
 
+/* ------------------------------------------------- discrete schedule cost */
+
+/*
+ * Cost of one integer schedule s [n] (Sec. 2.1), the quantity a driver of
+ * Alg. 1 keeps the best of:
+ *   out[0] = alpha * L_com + beta * L_res + gamma * L_mem      (the cost)
+ *   out[1] = L_com = sum over edges (s_j - s_i)^+              (App. B.1)
+ *   out[2] = L_res = sum over types k of max_t U_k(t)          (eq. (3), usage
+ *            folded mod II when II > 0 as in eq. (5))
+ *   out[3] = L_mem = max_t Mem(t), Mem(d) = sum_i b_i [s_i <= d < max_succ s_j]
+ *            (eq:mem), folded like the usage
+ *   out[4] = V_res = sum_{k,t} (U_k(t) - C_k)^+                 (eq:relu at sigma -> 0)
+ *   out[5] = 1 if the schedule is legal: 0 <= s <= D-1, every edge has
+ *            s_j >= s_i + Lat_i and every back edge s_i + k II >= s_j + Lat_j
+ * Steps outside [0, D-1] count in neither usage nor storage.
+ */
+int orc_schedule_cost(const orc_problem *p, const int64_t *s, double alpha, double beta, double gamma,
+                      double *out) {
+    const int32_t n = p->n, D = p->D, K = p->K, II = p->II;
+    const int32_t T = (II > 0) ? II : D;
+    double *U = calloc((size_t)K * T + 1, sizeof(double));
+    double *M = calloc((size_t)T + 1, sizeof(double));
+    if (!U || !M) { free(U); free(M); return ORC_E_NOMEM; }
+    int legal = 1;
+    double lcom = 0.0;
+    for (int32_t i = 0; i < n; ++i) {
+        if (s[i] < 0 || s[i] > D - 1) legal = 0;
+        else U[(int64_t)p->rtype[i] * T + s[i] % T] += 1.0;
+        int64_t last = -1;
+        for (int32_t e = p->row_ptr[i]; e < p->row_ptr[i + 1]; ++e) {
+            int64_t sj = s[p->col[e]];
+            if (sj < s[i] + p->delay[i]) legal = 0;
+            if (sj > s[i]) lcom += (double)(sj - s[i]);
+            if (sj > last) last = sj;
+        }
+        for (int64_t d = s[i]; d < last; ++d)
+            if (d >= 0 && d <= D - 1) M[d % T] += p->bmem[i];
+    }
+    for (int32_t b = 0; b < p->nb; ++b) {
+        int32_t j = p->bsrc[b], i = p->bdst[b];
+        if (s[i] + (int64_t)p->bdist[b] * II < s[j] + p->delay[j]) legal = 0;
+    }
+    double lres = 0.0, vres = 0.0, lmem = 0.0;
+    for (int32_t k = 0; k < K; ++k) {
+        double mx = 0.0;
+        for (int32_t t = 0; t < T; ++t) {
+            double u = U[(int64_t)k * T + t];
+            if (u > mx) mx = u;
+            if (u > p->cap[k]) vres += u - p->cap[k];
+        }
+        lres += mx;
+    }
+    for (int32_t t = 0; t < T; ++t) if (M[t] > lmem) lmem = M[t];
+    out[0] = alpha * lcom + beta * lres + gamma * lmem;
+    out[1] = lcom; out[2] = lres; out[3] = lmem; out[4] = vres; out[5] = legal;
+    free(U); free(M);
+    return ORC_OK;
+}
+
 /* ------------------------------------------------------------ legalization */
 
 /* half-up rounding of a float32 value, after clamping it to [-1, D]; a NaN

@@ -604,3 +604,62 @@ def test_p16_storage_smooth_peak_bounds(orc):
             mr = np.zeros((1, T))
             terms, *_ = orc.loss_grad(p, mu, sg, [0, 0, 0], 0.0, 0.0, grad=False, gamma=1.0, tau=tau, mreg_out=mr)
             assert mr[0].max() - 1e-12 <= terms[0, 6] <= mr[0].max() + tau * np.log(T) + 1e-12
+
+
+# ------------------------------------------------------------------- P17
+
+def test_p17_schedule_cost_hand_counts(orc):
+    """The discrete cost of Sec. 2.1 on the hand-counted schedules of the
+    golden files: L_com = 6, usage [[1,2],[1,1]] (peaks 2 + 1), V_res = 1,
+    and the storage profile folded mod 4 (peak 5); the first schedule breaks
+    the dependency 0->1, so it is not legal."""
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "sigma0_hand_counts.json")))
+    p = Problem(n_ops=g["n"], row_ptr=np.array(g["row_ptr"], np.int32), col_idx=np.array(g["col_idx"], np.int32),
+                delay=np.array(g["delay"], np.int32), rtype=np.array(g["rtype"], np.int32),
+                capacity=np.array(g["capacity"], np.float32), D=g["D"], II=g["II"],
+                back_src=np.array(g["back_src"], np.int32), back_dst=np.array(g["back_dst"], np.int32),
+                back_dist=np.array(g["back_dist"], np.int32))
+    s = np.floor(np.array(g["mu"]) + 0.5).astype(np.int64)
+    out = orc.schedule_cost(p, s[None], alpha=0.5, beta=2.0)[0]
+    assert out[1] == g["expected"]["L_com"] and out[2] == 3.0 and out[4] == g["expected"]["V_res"]
+    assert out[5] == 0.0 and out[0] == 0.5 * 6.0 + 2.0 * 3.0
+    h = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "sigma0_storage_counts.json")))
+    n = h["n"]
+    q = Problem(n_ops=n, row_ptr=np.array(h["row_ptr"], np.int32), col_idx=np.array(h["col_idx"], np.int32),
+                delay=np.zeros(n, np.int32), rtype=np.zeros(n, np.int32), capacity=np.array([10.0], np.float32),
+                D=h["D"], II=h["II_fold"], mem_units=np.array(h["mem_units"], np.float64))
+    s = np.floor(np.array(h["mu"]) + 0.5).astype(np.int64)
+    out = orc.schedule_cost(q, s[None], gamma=1.0)[0]
+    assert out[3] == max(h["expected_folded"]) and out[5] == 1.0 and out[0] == out[3]
+
+
+def test_p17_schedule_cost_is_relaxed_cost_at_sigma_zero(orc):
+    """At sigma -> 0 the relaxed L_com and usage equal the discrete ones of
+    the rounded schedule, and a legal schedule has V_dep = V_rec = 0."""
+    rng = np.random.default_rng(170)
+    for II in (0, 4):
+        p = tiny_problem(rng, 8, 12, II=II, n_back=2 if II else 0)
+        p.mem_units = rng.integers(1, 5, size=8).astype(np.float64)
+        mu = rng.uniform(0, 11, size=8)
+        s = np.floor(mu + 0.5).astype(np.int64)
+        out = orc.schedule_cost(p, s[None], alpha=1.0)[0]
+        mr = np.zeros((1, II if II else 12))
+        terms, U, *_ = orc.loss_grad(p, mu, np.full(8, 1e-6), [0, 0, 0], 0.0, 0.0, grad=False, mreg_out=mr)
+        assert out[1] == terms[0, 4]
+        assert out[2] == U[0].max(axis=1).sum()
+        assert out[3] == mr[0].max()
+        assert (out[5] == 1.0) == (terms[0, 1] == 0.0 and terms[0, 3] == 0.0)
+        assert out[4] == terms[0, 2]
+
+
+def test_p17_legalized_schedules_are_legal(orc):
+    """Alg. 3 / Alg. 4 outputs (converged) are legal under the cost's check."""
+    rng = np.random.default_rng(171)
+    for II in (0, 5):
+        p = tiny_problem(rng, 9, 30, II=II, n_back=2 if II else 0)
+        mu = rng.uniform(-3, 33, size=(4, 9)).astype(np.float32)
+        sched, st = orc.legalize(p, mu)
+        out = orc.schedule_cost(p, sched)
+        for b in range(4):
+            if st[b] == 0:
+                assert out[b, 5] == 1.0
