@@ -160,6 +160,9 @@ def main():
     ap.add_argument("--mem-gamma", type=float, default=0.0,
                     help="weight of the smooth peak storage term (storage units of 1-32 bits per op and a "
                          "sink op are added to the workload); 0 = off")
+    ap.add_argument("--solve-check-every", type=int, default=0,
+                    help="time the Alg. 1 driver (gaus_solve) with a legalization check every this many "
+                         "iterations instead of plain steps + one legalization; 0 = off")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the run, copy this many MiB once (counter calibration)")
     args = ap.parse_args()
@@ -217,13 +220,24 @@ def main():
     ctx.kernel_timing(True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    ev[0].record(stream)
-    ctx.step(args.steps, terms)
-    ev[1].record(stream)
-    status = ctx.legalize(mu, sched)
-    ev[2].record(stream)
+    solve_stats = None
+    if args.solve_check_every:
+        best_cost = torch.zeros(B, bd.N_COST, dtype=torch.float64, device=dev)
+        ev[0].record(stream)
+        solve_stats = ctx.solve(sched, best_cost, max_iters=args.steps, check_every=args.solve_check_every)
+        ev[1].record(stream)
+        ev[2].record(stream)
+        status = None
+    else:
+        ev[0].record(stream)
+        ctx.step(args.steps, terms)
+        ev[1].record(stream)
+        status = ctx.legalize(mu, sched)
+        ev[2].record(stream)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    if status is None:   # driver: 0 where the best schedule is legal
+        status = (best_cost[:, 5] == 0).int().cpu().numpy()
     ktimes = ctx.kernel_timing_read()
     ctx.kernel_timing(False)
     census = ctx.poly_census()
@@ -278,6 +292,7 @@ def main():
                                  if args.mem_gamma else "")},
         "ms_per_iteration_events": step_ms_events, "legalize_ms": legalize_ms,
         "poly_path": dict(poly_cfg, ops=census["ops"], edges=census["edges"]),
+        "solve": solve_stats,
         "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_TFLOPS,
                      "traffic": pmc_traffic(dom, profile),

@@ -157,6 +157,51 @@ gaus_status gaus_adam_from_grad(gaus_ctx *ctx, const float *g_mu, const float *g
  * GAUS_E_NOT_CONVERGED or GAUS_E_OVERFLOW per restart.  Synchronizes. */
 gaus_status gaus_legalize(gaus_ctx *ctx, const float *mu, int32_t *sched, int32_t *status);
 
+/* Discrete cost of integer schedules (Sec. 2.1), the quantity the driver
+ * below keeps the best of.  sched DEVICE [B][N] int32; cost DEVICE [B][6]
+ * double = (alpha_com L_com + beta_res L_res + gamma_mem L_mem, L_com =
+ * sum over edges of (s_j - s_i)^+, L_res = sum over types of the peak usage
+ * (folded mod II, eq. (3)/(5)), L_mem = peak storage units (eq:mem, folded),
+ * V_res = sum over (type, slot) of usage above capacity, legal = 1 if
+ * 0 <= s <= D-1 and every edge and back edge holds, else 0).  Storage units
+ * are summed in steps of 2^-20.  Asynchronous. */
+gaus_status gaus_schedule_cost(gaus_ctx *ctx, const int32_t *sched, double *cost);
+
+/* Alg. 1 driver (Sec. 3.3) on the bound state. */
+typedef struct {
+    int32_t max_iters;     /* fused iterations in total, >= 1 */
+    int32_t check_every;   /* iterations between checks, >= 1 (App. A reports
+                              about two legalizations per run) */
+    double time_limit_s;   /* stop at the first check after this much wall
+                              time (Sec. 4.1 uses 900 s); <= 0: no limit */
+    int32_t reinit_sigma;  /* 1: a re-initialized restart also gets
+                              sigma = max(kappa (ALAP - ASAP), sigma_min) */
+} gaus_solve_params;
+
+typedef struct {
+    int32_t iters;         /* fused iterations run */
+    int32_t checks;        /* checks done */
+    int32_t reinits;       /* (restart, check) pairs re-initialized */
+    int32_t improvements;  /* (restart, check) pairs that improved that restart's best */
+    int32_t best_restart;  /* restart holding the best schedule (feasible first), -1 if none legal */
+    double seconds;        /* wall time */
+} gaus_solve_stats;
+
+/* Runs Alg. 1 on the bound state: blocks of check_every fused iterations
+ * (gaus_step); after each block, every restart's means are rounded and
+ * legalized (Alg. 3/4) and the result costed (gaus_schedule_cost); a
+ * restart keeps the best schedule it has produced (feasible = legal with
+ * V_res = 0 first, then lower cost).  A restart whose rounding was not legal
+ * is re-initialized (Sec. 3.3 Sampling): mu from the legalized schedule if it
+ * improved the restart's best, else from that best ("reset to the prior best",
+ * App. A); its Adam moments are cleared.  Stops after max_iters iterations or
+ * the time limit.  best_sched DEVICE [B][N] int32 and best_cost DEVICE
+ * [B][6] double (as gaus_schedule_cost) receive each restart's best;
+ * stats HOST.  Synchronizes.  Errors: INVALID_ARG (state not bound, bad
+ * parameters), DEVICE. */
+gaus_status gaus_solve(gaus_ctx *ctx, const gaus_solve_params *prm, int32_t *best_sched, double *best_cost,
+                       gaus_solve_stats *stats);
+
 /* Paper initialization (Sec. 3.3, Alg. 1): sigma = max(kappa*(ALAP-ASAP),
  * sigma_min); restart 0 gets mu = (ASAP+ALAP)/2, restart b >= 1 gets
  * mu = ASAP + u[b][i]*(ALAP-ASAP) with u HOST [B][N] double in [0,1) (may be

@@ -20,7 +20,8 @@ OK, E_INVALID_ARG, E_CYCLE, E_HORIZON, E_NOT_CONVERGED, E_OVERFLOW, E_DEVICE, E_
 
 # symbols declared in include/gaus.h
 EXPORTS = ("gaus_default_hparams", "gaus_init", "gaus_bind_state", "gaus_loss_grad", "gaus_step",
-           "gaus_adam_from_grad", "gaus_legalize", "gaus_init_state", "gaus_asap_alap",
+           "gaus_adam_from_grad", "gaus_legalize", "gaus_schedule_cost", "gaus_solve", "gaus_init_state",
+           "gaus_asap_alap",
            "gaus_get_usage", "gaus_get_storage", "gaus_kernel_timing", "gaus_kernel_timing_read", "gaus_sync",
            "gaus_get_dims", "gaus_get_poly_config", "gaus_poly_census", "gaus_last_error", "gaus_status_string",
            "gaus_destroy")
@@ -38,6 +39,19 @@ class _Problem(C.Structure):
                 ("n_types", C.c_int32), ("capacity", C.c_void_p), ("D", C.c_int32), ("II", C.c_int32),
                 ("n_back", C.c_int32), ("back_src", C.c_void_p), ("back_dst", C.c_void_p),
                 ("back_dist", C.c_void_p), ("mem_units", C.c_void_p)]
+
+
+class SolveParams(C.Structure):
+    _fields_ = [("max_iters", C.c_int32), ("check_every", C.c_int32), ("time_limit_s", C.c_double),
+                ("reinit_sigma", C.c_int32)]
+
+
+class SolveStats(C.Structure):
+    _fields_ = [("iters", C.c_int32), ("checks", C.c_int32), ("reinits", C.c_int32),
+                ("improvements", C.c_int32), ("best_restart", C.c_int32), ("seconds", C.c_double)]
+
+
+N_COST = 6    # cost, L_com, L_res, L_mem, V_res, legal
 
 
 class HParams(C.Structure):
@@ -71,6 +85,8 @@ def load():
         "gaus_step": ([vp, i32, vp], C.c_int),
         "gaus_adam_from_grad": ([vp] * 4, C.c_int),
         "gaus_legalize": ([vp] * 4, C.c_int),
+        "gaus_schedule_cost": ([vp] * 3, C.c_int),
+        "gaus_solve": ([vp] * 5, C.c_int),
         "gaus_init_state": ([vp] * 4, C.c_int),
         "gaus_asap_alap": ([vp] * 3, C.c_int),
         "gaus_get_usage": ([vp] * 2, C.c_int),
@@ -213,6 +229,24 @@ class Context:
                                          _dptr(sched, torch.int32, (self.B, self.N), "sched"),
                                          _np_ptr(status)))
         return status
+
+    def schedule_cost(self, sched, cost):
+        """Discrete cost of device schedules sched [B,N] int32 into cost [B,6] float64."""
+        import torch
+        self._check(load().gaus_schedule_cost(self._h, _dptr(sched, torch.int32, (self.B, self.N), "sched"),
+                                              _dptr(cost, torch.float64, (self.B, N_COST), "cost")))
+
+    def solve(self, best_sched, best_cost, max_iters: int, check_every: int, time_limit_s: float = 0.0,
+              reinit_sigma: bool = False) -> dict:
+        """Alg. 1 driver on the bound state; returns the stats as a dict."""
+        import torch
+        prm = SolveParams(int(max_iters), int(check_every), float(time_limit_s), 1 if reinit_sigma else 0)
+        st = SolveStats()
+        self._check(load().gaus_solve(self._h, C.byref(prm),
+                                      _dptr(best_sched, torch.int32, (self.B, self.N), "best_sched"),
+                                      _dptr(best_cost, torch.float64, (self.B, N_COST), "best_cost"),
+                                      C.byref(st)))
+        return {f: getattr(st, f) for f, _ in SolveStats._fields_}
 
     def init_state(self, mu, sigma, u=None):
         import torch

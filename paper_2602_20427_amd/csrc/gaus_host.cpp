@@ -4,6 +4,7 @@
 #include "gaus_internal.h"
 
 #include <algorithm>
+#include <chrono>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -456,6 +457,17 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     AL(mown, BN * ntiles * 2);
     AL(msucc, (size_t)B * h.E * ntiles * 2);
     AL(bigsum, (size_t)B * std::max<size_t>(h.big_ops.size(), 1) * 6);
+    AL(cand, BN);
+    AL(cand_cost, (size_t)B * kCost);
+    AL(hist, (size_t)B * h.K * g.T);
+    AL(mdiff, (size_t)B * (h.D + 1));
+    AL(mprof, (size_t)B * g.T);
+    AL(lcom_acc, (size_t)B);
+    AL(illegal, (size_t)B);
+    AL(round_bad, (size_t)B);
+    AL(mode, (size_t)B);
+    AL(n_reinit, (size_t)B);
+    AL(n_improve, (size_t)B);
     AL(wts, (size_t)B * 4);
     AL(adamf, (size_t)B * 2);
     AL(cls, BN);
@@ -559,6 +571,73 @@ gaus_status gaus_legalize(gaus_ctx *ctx, const float *mu, int32_t *sched, int32_
         e = hipMemcpyAsync(status, ctx->w.status, sizeof(int) * ctx->g.B, hipMemcpyDeviceToHost, ctx->stream);
     if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
     if (e != hipSuccess) return hip_fail(ctx, e, "legalize");
+    return GAUS_OK;
+}
+
+gaus_status gaus_schedule_cost(gaus_ctx *ctx, const int32_t *sched, double *cost) {
+    if (!ctx) return GAUS_E_INVALID_ARG;
+    if (!sched || !cost) return fail(ctx, GAUS_E_INVALID_ARG, "schedule_cost: null pointer");
+    hipError_t e = enqueue_schedule_cost(ctx->g, ctx->w, ctx->hp, sched, cost, ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "schedule_cost launch");
+    return GAUS_OK;
+}
+
+gaus_status gaus_solve(gaus_ctx *ctx, const gaus_solve_params *prm, int32_t *best_sched, double *best_cost,
+                       gaus_solve_stats *stats) {
+    if (!ctx) return GAUS_E_INVALID_ARG;
+    if (!ctx->bound) return fail(ctx, GAUS_E_INVALID_ARG, "solve: state not bound");
+    if (!prm || !best_sched || !best_cost || !stats) return fail(ctx, GAUS_E_INVALID_ARG, "solve: null pointer");
+    if (prm->max_iters < 1 || prm->check_every < 1)
+        return fail(ctx, GAUS_E_INVALID_ARG, "solve: need max_iters >= 1 and check_every >= 1");
+    const auto t0 = std::chrono::steady_clock::now();
+    auto elapsed = [&]() { return std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count(); };
+    hipError_t e = enqueue_best_init(ctx->g, ctx->w, best_cost, ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "solve init");
+    *stats = gaus_solve_stats{};
+    int it = 0, checks = 0;
+    while (it < prm->max_iters) {
+        const int n = std::min(prm->check_every, prm->max_iters - it);
+        gaus_status s = gaus_step(ctx, n, nullptr);
+        if (s != GAUS_OK) return s;
+        it += n;
+        e = enqueue_check(ctx->g, ctx->w, ctx->hp, ctx->mu, ctx->sigma, ctx->m, ctx->v, best_sched, best_cost,
+                          prm->reinit_sigma ? 1 : 0, ctx->stream);
+        if (e != hipSuccess) return hip_fail(ctx, e, "solve check");
+        ++checks;
+        if (prm->time_limit_s > 0.0) {
+            e = hipStreamSynchronize(ctx->stream);
+            if (e != hipSuccess) return hip_fail(ctx, e, "solve");
+            if (elapsed() >= prm->time_limit_s) break;
+        }
+    }
+    const int B = ctx->g.B;
+    std::vector<int> nre(B), nim(B);
+    std::vector<double> bc((size_t)B * kCost);
+    e = hipMemcpyAsync(nre.data(), ctx->w.n_reinit, sizeof(int) * B, hipMemcpyDeviceToHost, ctx->stream);
+    if (e == hipSuccess) e = hipMemcpyAsync(nim.data(), ctx->w.n_improve, sizeof(int) * B, hipMemcpyDeviceToHost, ctx->stream);
+    if (e == hipSuccess) e = hipMemcpyAsync(bc.data(), best_cost, sizeof(double) * bc.size(), hipMemcpyDeviceToHost, ctx->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "solve");
+    stats->iters = it;
+    stats->checks = checks;
+    for (int b = 0; b < B; ++b) { stats->reinits += nre[b]; stats->improvements += nim[b]; }
+    // best restart: the same order the device uses per restart
+    auto better = [](const double *a, const double *c) {
+        const bool fa = a[5] != 0.0 && a[4] == 0.0, fc = c[5] != 0.0 && c[4] == 0.0;
+        if (fa != fc) return fa;
+        if (fa) return a[0] < c[0];
+        if (a[5] != c[5]) return a[5] != 0.0;
+        if (a[4] != c[4]) return a[4] < c[4];
+        return a[0] < c[0];
+    };
+    int best = -1;
+    for (int b = 0; b < B; ++b) {
+        const double *cb = &bc[(size_t)b * kCost];
+        if (cb[5] == 0.0) continue;   // never legal
+        if (best < 0 || better(cb, &bc[(size_t)best * kCost])) best = b;
+    }
+    stats->best_restart = best;
+    stats->seconds = elapsed();
     return GAUS_OK;
 }
 

@@ -17,6 +17,7 @@ constexpr int kBP = 5;   // per (restart, back edge, tile): V_rec, dVrec/dmu_j, 
                          //   (producer j), dVrec/dmu_i, dVrec/dsigma_i (consumer i)
 constexpr int kHalo = 256;  // largest producer delay handled from the LDS row window
 constexpr int kBigIn = 64;  // in-degree above which an op's in-edge records are reduced by a work-group
+constexpr int kCost = 6;    // per schedule: cost, L_com, L_res, L_mem, V_res, legal
 constexpr int kTerms = 7;   // per restart: L, V_dep, V_res, V_rec, L_com, L_res, L_mem
 
 // Chunk-polynomial path (dense regime).  On a chunk of W consecutive steps
@@ -89,6 +90,17 @@ struct Work {
     float *mown;      // [B][N][tiles][2]  storage gradient of an op as the holder, per tile
     float *msucc;     // [B][E][tiles][2]  storage gradient of an edge's consumer, per tile
     double *bigsum;   // [B][nbig][6]      in-edge records of the high in-degree ops, reduced
+    // discrete schedules (cost of Sec. 2.1; the Alg. 1 driver)
+    int *cand;        // [B][N]            legalized rounding of the current means
+    double *cand_cost;// [B][kCost]        its cost
+    int *hist;        // [B][K][T]         usage counts of a schedule
+    long long *mdiff; // [B][D+1]          storage differences (fixed point)
+    long long *mprof; // [B][T]            storage profile (fixed point)
+    unsigned long long *lcom_acc;  // [B]  sum of (s_j - s_i)^+
+    int *illegal;     // [B]               1 if the schedule breaks an edge or the horizon
+    int *round_bad;   // [B]               1 if the rounding itself was not legal
+    int *mode;        // [B]               re-init: 0 none, 1 from the candidate, 2 from the best
+    int *n_reinit, *n_improve;     // [B]  driver counters
     float *wts;       // [B][4]            w_dep, w_res, w_rec, unused
     float *adamf;     // [B][2]            Adam bias corrections 1-beta1^t, 1-beta2^t
     unsigned char *cls;  // [B][N]          1 = op on the chunk-polynomial path this iteration
@@ -157,6 +169,17 @@ hipError_t launch_lse_poly(const Graph &g, const Work &w, const PolyArgs &pa, co
 hipError_t enqueue_adam_from_grad(const Graph &g, const Work &w, const HP &hp, const float *gmu,
                                   const float *gsig, const float *terms, float *mu, float *sigma,
                                   float *m, float *v, float *lambda, int *adam_t, hipStream_t st);
+
+// Discrete cost of schedules sched [B][N] (device) into cost [B][kCost] (device).
+hipError_t enqueue_schedule_cost(const Graph &g, const Work &w, const HP &hp, const int *sched, double *cost,
+                                 hipStream_t st);
+// One check of the Alg. 1 driver: legalize the rounded means, cost the
+// candidates, keep each restart's best, re-initialize restarts whose
+// rounding was not legal (from the candidate if it improved, else from the
+// best so far).
+hipError_t enqueue_best_init(const Graph &g, const Work &w, double *best_cost, hipStream_t st);
+hipError_t enqueue_check(const Graph &g, const Work &w, const HP &hp, float *mu, float *sigma, float *m,
+                         float *v, int *best_sched, double *best_cost, int reinit_sigma, hipStream_t st);
 
 // Round + legalize every restart; writes sched [B][N] and w.status [B].
 hipError_t enqueue_legalize(const Graph &g, const Work &w, const float *mu, int *sched,

@@ -678,6 +678,214 @@ __global__ __launch_bounds__(kLegBS) void k_legalize(Graph G, Work W, const floa
 }
 
 // ---------------------------------------------------------------------------
+// Discrete cost of integer schedules (Sec. 2.1): usage counts per (type,
+// slot), storage held from s_i until the last successor starts (eq:mem) as a
+// difference array in fixed point (integer sums are order-independent),
+// sum of edge lengths, legality.  Then per restart: peaks, V_res, the cost
+// alpha L_com + beta L_res + gamma L_mem.
+// ---------------------------------------------------------------------------
+constexpr double kMemFix = 1048576.0;   // storage units are counted in steps of 2^-20
+
+__global__ void k_cost_clear(Graph G, Work W) {
+    const int b = blockIdx.y;
+    const size_t x = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const size_t nh = (size_t)G.K * G.T, nd = (size_t)G.D + 1;
+    if (x < nh) W.hist[(size_t)b * nh + x] = 0;
+    if (x < nd) W.mdiff[(size_t)b * nd + x] = 0;
+    if (x < (size_t)G.T) W.mprof[(size_t)b * G.T + x] = 0;
+    if (x == 0) { W.lcom_acc[b] = 0; W.illegal[b] = 0; }
+}
+
+__global__ void k_cost_ops(Graph G, Work W, const int *__restrict__ sched) {
+    const int b = blockIdx.y;
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    const int N = G.N, D = G.D, T = G.T;
+    const int *s = sched + (size_t)b * N;
+    if (i < N) {
+        const int si = s[i];
+        bool bad = si < 0 || si > D - 1;
+        if (!bad) atomicAdd(&W.hist[((size_t)b * G.K + G.rtype[i]) * T + si % T], 1);
+        long long lc = 0;
+        int last = -1;
+        for (int e = G.row_ptr[i]; e < G.row_ptr[i + 1]; ++e) {
+            const int sj = s[G.col[e]];
+            if ((long long)sj < (long long)si + G.delay[i]) bad = true;
+            if (sj > si) lc += (long long)sj - si;
+            last = max(last, sj);
+        }
+        if (lc) atomicAdd(&W.lcom_acc[b], (unsigned long long)lc);
+        const int lo = max(si, 0), hi = min(last, D);   // held at steps [s_i, last) inside the horizon
+        if (lo < hi) {
+            const long long v = llrint((double)G.bmem[i] * kMemFix);
+            atomicAdd((unsigned long long *)&W.mdiff[(size_t)b * (D + 1) + lo], (unsigned long long)v);
+            atomicAdd((unsigned long long *)&W.mdiff[(size_t)b * (D + 1) + hi], (unsigned long long)(-v));
+        }
+        if (bad) W.illegal[b] = 1;
+    }
+    if (i < G.nb) {   // back edge (producer j, consumer c, k): s_c + k II >= s_j + Lat_j
+        const int j = G.bsrc[i], c = G.bdst[i];
+        if ((long long)s[c] + (long long)G.bdist[i] * G.II < (long long)s[j] + G.delay[j]) W.illegal[b] = 1;
+    }
+}
+
+constexpr int kCostBS = 1024;
+
+// per restart: prefix sum of the storage differences, fold, peaks, V_res, cost
+__global__ __launch_bounds__(kCostBS) void k_cost_final(Graph G, Work W, HP hp, double *cost) {
+    __shared__ long long sScan[kCostBS];
+    __shared__ double sRed[kCostBS / 64];
+    __shared__ long long carry;
+    const int b = blockIdx.x, tid = threadIdx.x;
+    const int D = G.D, T = G.T, K = G.K;
+    const long long *md = W.mdiff + (size_t)b * (D + 1);
+    long long *mp = W.mprof + (size_t)b * T;
+    if (tid == 0) carry = 0;
+    __syncthreads();
+    for (int d0 = 0; d0 < D; d0 += kCostBS) {
+        long long x = d0 + tid < D ? md[d0 + tid] : 0;
+        sScan[tid] = x;
+        __syncthreads();
+        for (int off = 1; off < kCostBS; off <<= 1) {     // inclusive scan (Hillis-Steele)
+            const long long y = tid >= off ? sScan[tid - off] : 0;
+            __syncthreads();
+            sScan[tid] += y;
+            __syncthreads();
+        }
+        const long long held = carry + sScan[tid];
+        if (d0 + tid < D) atomicAdd((unsigned long long *)&mp[(d0 + tid) % T], (unsigned long long)held);
+        __syncthreads();
+        if (tid == kCostBS - 1) carry = held;
+        __syncthreads();
+    }
+    __threadfence();
+    __syncthreads();
+    // peaks and V_res (the profile is read back from L2, where the atomics landed)
+    double lmem = 0.0, vres = 0.0, lres = 0.0;
+    for (int t = tid; t < T; t += kCostBS)
+        lmem = fmax(lmem, (double)__hip_atomic_load(&mp[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) / kMemFix);
+    for (int k = 0; k < K; ++k) {
+        double mx = 0.0;
+        for (int t = tid; t < T; t += kCostBS) {
+            const double u = (double)W.hist[((size_t)b * K + k) * T + t];
+            mx = fmax(mx, u);
+            if (u > (double)G.cap[k]) vres += u - (double)G.cap[k];
+        }
+        for (int off = 32; off > 0; off >>= 1) mx = fmax(mx, __shfl_xor(mx, off, 64));
+        if ((tid & 63) == 0) sRed[tid >> 6] = mx;
+        __syncthreads();
+        if (tid == 0) { double m2 = 0.0; for (int w = 0; w < kCostBS / 64; ++w) m2 = fmax(m2, sRed[w]); lres += m2; }
+        __syncthreads();
+    }
+    for (int off = 32; off > 0; off >>= 1) {
+        lmem = fmax(lmem, __shfl_xor(lmem, off, 64));
+        vres += __shfl_xor(vres, off, 64);
+    }
+    __shared__ double sM[kCostBS / 64], sV[kCostBS / 64];
+    if ((tid & 63) == 0) { sM[tid >> 6] = lmem; sV[tid >> 6] = vres; }
+    __syncthreads();
+    if (tid == 0) {
+        double m2 = 0.0, v2 = 0.0;
+        for (int w = 0; w < kCostBS / 64; ++w) { m2 = fmax(m2, sM[w]); v2 += sV[w]; }
+        const double lcom = (double)W.lcom_acc[b];
+        double *c = cost + (size_t)b * kCost;
+        c[0] = (double)hp.alpha * lcom + (double)hp.beta * lres + (double)hp.gamma * m2;
+        c[1] = lcom; c[2] = lres; c[3] = m2; c[4] = v2; c[5] = W.illegal[b] ? 0.0 : 1.0;
+    }
+}
+
+hipError_t enqueue_schedule_cost(const Graph &g, const Work &w, const HP &hp, const int *sched, double *cost,
+                                 hipStream_t st) {
+    const size_t cells = std::max({(size_t)g.K * g.T, (size_t)g.D + 1, (size_t)g.T});
+    hipLaunchKernelGGL(k_cost_clear, dim3((unsigned)((cells + 255) / 256), g.B), dim3(256), 0, st, g, w);
+    hipLaunchKernelGGL(k_cost_ops, dim3((std::max(g.N, g.nb) + 255) / 256, g.B), dim3(256), 0, st, g, w, sched);
+    hipLaunchKernelGGL(k_cost_final, dim3(g.B), dim3(kCostBS), 0, st, g, w, hp, cost);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Alg. 1 driver check.  A schedule is feasible if legal and within the
+// capacities (V_res = 0).  Order: feasible before infeasible; among feasible
+// the lower cost; among infeasible legal before illegal, then the lower V_res,
+// then the lower cost.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ bool cost_better(const double *a, const double *b) {
+    const bool fa = a[5] != 0.0 && a[4] == 0.0, fb = b[5] != 0.0 && b[4] == 0.0;
+    if (fa != fb) return fa;
+    if (fa) return a[0] < b[0];
+    if (a[5] != b[5]) return a[5] != 0.0;
+    if (a[4] != b[4]) return a[4] < b[4];
+    return a[0] < b[0];
+}
+
+__global__ void k_best_init(int B, double *best_cost, Work W) {
+    const int b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= B) return;
+    double *c = best_cost + (size_t)b * kCost;
+    c[0] = INFINITY; c[1] = INFINITY; c[2] = INFINITY; c[3] = INFINITY; c[4] = INFINITY; c[5] = 0.0;
+    W.n_reinit[b] = 0;
+    W.n_improve[b] = 0;
+}
+
+// was the rounding of mu already legal (legalization left it unchanged)?
+__global__ __launch_bounds__(256) void k_round_cmp(Graph G, Work W, const float *__restrict__ mu) {
+    const int b = blockIdx.x, tid = threadIdx.x;
+    int diff = 0;
+    for (int i = tid; i < G.N; i += 256)
+        if (round_half_up(mu[(size_t)b * G.N + i], G.D) != (long long)W.cand[(size_t)b * G.N + i]) diff = 1;
+    diff = __syncthreads_or(diff);
+    if (tid == 0) W.round_bad[b] = diff;
+}
+
+__global__ __launch_bounds__(256) void k_best_update(Graph G, Work W, int *best_sched, double *best_cost) {
+    __shared__ int improved;
+    const int b = blockIdx.x, tid = threadIdx.x;
+    if (tid == 0) {
+        improved = cost_better(W.cand_cost + (size_t)b * kCost, best_cost + (size_t)b * kCost) ? 1 : 0;
+        W.mode[b] = W.round_bad[b] ? (improved ? 1 : 2) : 0;
+        W.n_reinit[b] += W.round_bad[b] ? 1 : 0;
+        W.n_improve[b] += improved;
+    }
+    __syncthreads();
+    if (!improved) return;
+    for (int i = tid; i < G.N; i += 256) best_sched[(size_t)b * G.N + i] = W.cand[(size_t)b * G.N + i];
+    if (tid < kCost) best_cost[(size_t)b * kCost + tid] = W.cand_cost[(size_t)b * kCost + tid];
+}
+
+// re-initialize the restarts marked by k_best_update: mu from the candidate
+// (mode 1) or the best schedule so far (mode 2); Adam moments cleared;
+// optionally sigma back to the paper's initial width
+__global__ void k_reinit(Graph G, Work W, HP hp, const int *__restrict__ best_sched, float *mu, float *sigma,
+                         float *m, float *v, int reinit_sigma) {
+    const int b = blockIdx.y;
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= G.N) return;
+    const int md = W.mode[b];
+    if (md == 0) return;
+    const size_t bi = (size_t)b * G.N + i, half = (size_t)G.B * G.N;
+    mu[bi] = (float)(md == 1 ? W.cand[bi] : best_sched[bi]);
+    if (reinit_sigma) sigma[bi] = fmaxf(hp.kappa * (float)(G.alap[i] - G.asap[i]), hp.sigma_min);
+    m[bi] = 0.0f; m[half + bi] = 0.0f;
+    v[bi] = 0.0f; v[half + bi] = 0.0f;
+}
+
+hipError_t enqueue_best_init(const Graph &g, const Work &w, double *best_cost, hipStream_t st) {
+    hipLaunchKernelGGL(k_best_init, dim3((g.B + 255) / 256), dim3(256), 0, st, g.B, best_cost, w);
+    return hipGetLastError();
+}
+
+hipError_t enqueue_check(const Graph &g, const Work &w, const HP &hp, float *mu, float *sigma, float *m,
+                         float *v, int *best_sched, double *best_cost, int reinit_sigma, hipStream_t st) {
+    hipLaunchKernelGGL(k_legalize, dim3(g.B), dim3(kLegBS), 0, st, g, w, mu, w.cand);
+    hipLaunchKernelGGL(k_round_cmp, dim3(g.B), dim3(256), 0, st, g, w, mu);
+    hipError_t e = enqueue_schedule_cost(g, w, hp, w.cand, w.cand_cost, st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_best_update, dim3(g.B), dim3(256), 0, st, g, w, best_sched, best_cost);
+    hipLaunchKernelGGL(k_reinit, dim3((g.N + 255) / 256, g.B), dim3(256), 0, st, g, w, hp, best_sched, mu, sigma,
+                       m, v, reinit_sigma);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // Host-side enqueue helpers
 // ---------------------------------------------------------------------------
 hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const LaunchCfg &lc,

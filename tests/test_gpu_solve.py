@@ -1,0 +1,164 @@
+"""The discrete schedule cost (Sec. 2.1) and the Alg. 1 driver on the GPU,
+through the C ABI, against the oracle's cost, legality and legalization."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2602_20427_amd import binding as bd
+from paper_2602_20427_amd.workloads import CONFIGS, make_problem, random_state, restart_uniforms, with_storage
+from tests.gpu_common import hparams, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    oracle.build(force=False)
+    bd.load()
+    yield
+
+
+def _ctx(p, B, hp):
+    import torch
+    dev = torch.device("cuda")
+    ctx = bd.Context(p, B, hp)
+    st = dict(mu=torch.zeros(B, p.n_ops, device=dev), sigma=torch.zeros(B, p.n_ops, device=dev),
+              m=torch.zeros(2, B, p.n_ops, device=dev), v=torch.zeros(2, B, p.n_ops, device=dev),
+              lam=torch.full((B, 3), hp.lambda0, device=dev), t=torch.zeros(1, dtype=torch.int32, device=dev))
+    ctx.init_state(st["mu"], st["sigma"], restart_uniforms(p.n_ops, B, seed=0))
+    ctx.bind_state(st["mu"], st["sigma"], st["m"], st["v"], st["lam"], st["t"])
+    return ctx, st
+
+
+def _gpu_cost(ctx, sched):
+    import torch
+    s = torch.from_numpy(np.ascontiguousarray(sched, np.int32)).cuda()
+    c = torch.zeros(sched.shape[0], bd.N_COST, dtype=torch.float64, device="cuda")
+    ctx.schedule_cost(s, c)
+    ctx.sync()
+    return c.cpu().numpy()
+
+
+@pytest.mark.parametrize("cfg,storage", [("small", False), ("small", True), ("pipelined", False),
+                                         ("pipelined", True)])
+def test_schedule_cost_matches_oracle(cfg, storage):
+    p = make_problem(cfg, seed=0)
+    if storage:
+        p = with_storage(p, seed=2)
+    B = 6
+    hp = hparams(alpha=0.37)
+    hp.beta_res, hp.gamma_mem = 1.5, (0.25 if storage else 0.0)
+    ctx = bd.Context(p, B, hp)
+    rng = np.random.default_rng(11)
+    mu, _ = random_state(p.n_ops, p.D, B, seed=12)
+    legal, _ = oracle.legalize(p, mu)
+    sched = legal.copy()
+    sched[3] = rng.integers(0, p.D, size=p.n_ops)               # random, illegal
+    sched[4] = np.floor(mu[4] + 0.5).astype(np.int64)           # plain rounding
+    sched[5, :10] = -1                                          # outside the horizon
+    g = _gpu_cost(ctx, sched)
+    o = oracle.schedule_cost(p, sched, alpha=hp.alpha_com, beta=hp.beta_res, gamma=hp.gamma_mem)
+    say(f"[cost] {cfg} storage={storage}: legal {g[:, 5].tolist()} cost {g[:, 0].round(3).tolist()}")
+    assert np.array_equal(g[:, [1, 2, 5]], o[:, [1, 2, 5]])
+    assert np.allclose(g[:, [0, 3, 4]], o[:, [0, 3, 4]], rtol=1e-12, atol=0)
+    ctx.close()
+
+
+@pytest.mark.parametrize("cfg", ["small", "pipelined"])
+def test_solve_returns_legal_best_schedules(cfg):
+    import torch
+    p = make_problem(cfg, seed=0)
+    B = min(CONFIGS[cfg].B, 8)
+    hp = hparams(alpha=0.01, rho=1e-3, lr=0.05)
+    hp.beta_res = 1.0
+    ctx, st = _ctx(p, B, hp)
+    bs = torch.zeros(B, p.n_ops, dtype=torch.int32, device="cuda")
+    bc = torch.zeros(B, bd.N_COST, dtype=torch.float64, device="cuda")
+    stats = ctx.solve(bs, bc, max_iters=200, check_every=25)
+    say(f"[solve] {cfg}: {stats}")
+    assert stats["iters"] == 200 and stats["checks"] == 8
+    sched, cost = bs.cpu().numpy().astype(np.int64), bc.cpu().numpy()
+    o = oracle.schedule_cost(p, sched, alpha=hp.alpha_com, beta=hp.beta_res)
+    seen = cost[:, 0] < np.inf        # restarts that produced any legalized candidate
+    assert np.array_equal(cost[seen][:, [1, 2, 5]], o[seen][:, [1, 2, 5]])
+    assert np.allclose(cost[seen][:, [0, 4]], o[seen][:, [0, 4]], rtol=1e-12)
+    if p.II == 0:   # Alg. 3 always ends legal (clamp to [ASAP, ALAP], one pass)
+        assert np.all(cost[:, 5] == 1.0)
+    # documented order: feasible (legal, V_res = 0) first by cost; then legal
+    # by V_res and cost; restarts that never produced a legal schedule excluded
+    feas = (cost[:, 5] == 1.0) & (cost[:, 4] == 0.0)
+    key = [(0 if feas[b] else 1, 0.0 if feas[b] else cost[b, 4], cost[b, 0]) for b in range(B)]
+    legal = [b for b in range(B) if cost[b, 5] == 1.0]
+    assert stats["best_restart"] == (min(legal, key=lambda b: key[b]) if legal else -1)
+    ctx.close()
+
+
+def test_solve_first_check_reinitializes_from_the_legalized_rounding():
+    """One block of K iterations and one check: a restart whose rounding was
+    not legal restarts from its legalized rounding (which is its first best),
+    with cleared Adam moments; the others keep their means."""
+    import torch
+    p = make_problem("small", seed=0)
+    B, K = 8, 30
+    hp = hparams(alpha=0.01, rho=1e-3, lr=0.2)
+    a, sa = _ctx(p, B, hp)
+    a.step(K)
+    a.sync()
+    mu_k = sa["mu"].cpu().numpy()
+    cand, status = oracle.legalize(p, mu_k)
+    illegal = np.any(np.floor(mu_k + 0.5) != cand, axis=1)   # (mu stays inside [-1, D] here)
+    b_, sb = _ctx(p, B, hp)
+    bs = torch.zeros(B, p.n_ops, dtype=torch.int32, device="cuda")
+    bc = torch.zeros(B, bd.N_COST, dtype=torch.float64, device="cuda")
+    stats = b_.solve(bs, bc, max_iters=K, check_every=K)
+    say(f"[solve] one check: illegal roundings {int(illegal.sum())} of {B}; {stats}")
+    assert stats["reinits"] == int(illegal.sum()) and stats["improvements"] == B
+    assert np.array_equal(bs.cpu().numpy(), cand.astype(np.int32))
+    mu_after = sb["mu"].cpu().numpy()
+    for b in range(B):
+        if illegal[b]:
+            assert np.array_equal(mu_after[b], cand[b].astype(np.float32))
+            assert float(sb["m"][:, b].abs().max()) == 0.0 and float(sb["v"][:, b].abs().max()) == 0.0
+        else:
+            assert np.array_equal(mu_after[b], mu_k[b])
+    a.close(); b_.close()
+
+
+def test_solve_time_limit_and_determinism():
+    import torch
+    p = make_problem("small", seed=1)
+    B = 4
+    hp = hparams(alpha=0.01, rho=1e-3, lr=0.05)
+    out = []
+    for limit in (0.0, 0.0, 1e-9):
+        ctx, st = _ctx(p, B, hp)
+        bs = torch.zeros(B, p.n_ops, dtype=torch.int32, device="cuda")
+        bc = torch.zeros(B, bd.N_COST, dtype=torch.float64, device="cuda")
+        stats = ctx.solve(bs, bc, max_iters=120, check_every=20, time_limit_s=limit, reinit_sigma=True)
+        out.append((stats, bs.cpu().numpy(), bc.cpu().numpy(), st["mu"].cpu().numpy()))
+        ctx.close()
+    assert out[0][0]["iters"] == 120 and out[2][0]["iters"] == 20 and out[2][0]["checks"] == 1
+    assert np.array_equal(out[0][1], out[1][1]) and np.array_equal(out[0][2], out[1][2])
+    assert np.array_equal(out[0][3], out[1][3])
+
+
+def test_solve_legal_rounding_is_left_alone():
+    """After a re-initialization from a legal schedule, a tiny step keeps the
+    rounding legal, so later checks re-initialize nothing."""
+    import torch
+    p = make_problem("small", seed=2)
+    B = 4
+    hp = hparams(alpha=0.01, rho=1e-3, lr=1e-6)
+    runs = []
+    for iters in (1, 4):
+        ctx, st = _ctx(p, B, hp)
+        bs = torch.zeros(B, p.n_ops, dtype=torch.int32, device="cuda")
+        bc = torch.zeros(B, bd.N_COST, dtype=torch.float64, device="cuda")
+        runs.append((ctx.solve(bs, bc, max_iters=iters, check_every=1), st["mu"].cpu().numpy(), bs.cpu().numpy()))
+        ctx.close()
+    say(f"[solve] tiny steps: one check {runs[0][0]}; four checks {runs[1][0]}")
+    assert runs[1][0]["checks"] == 4
+    assert runs[1][0]["reinits"] == runs[0][0]["reinits"]   # only the first check re-initializes
+    assert np.array_equal(np.floor(runs[1][1] + 0.5).astype(np.int32), runs[1][2])
