@@ -69,6 +69,8 @@ def _load():
         lib.orc_topo.restype = C.c_int
         lib.orc_init_state.argtypes = [P, i32, vp, dbl, dbl, vp, vp]
         lib.orc_init_state.restype = C.c_int
+        lib.orc_set_family.argtypes = [i32]
+        lib.orc_set_family.restype = None
         lib.orc_mass.argtypes = [dbl, dbl, i32, i32]
         lib.orc_mass.restype = dbl
         lib.orc_num_threads.argtypes = []
@@ -115,6 +117,15 @@ def _op(prob):
 
 def num_threads() -> int:
     return int(_load().orc_num_threads())
+
+
+FAMILIES = {"gaussian": 0, "logistic": 1, "laplace": 2, "cauchy": 3}
+
+
+def set_family(family) -> None:
+    """Distribution family of the relaxed start times (App. D) for the calls
+    that follow: "gaussian", "logistic", "laplace", "cauchy" (or 0..3)."""
+    _load().orc_set_family(int(FAMILIES.get(family, family)))
 
 
 def loss_grad(prob, mu, sigma, lam, alpha, rho, grad=True, tie_tol=1e-4, beta=0.0, tau=1e-2, gamma=0.0,

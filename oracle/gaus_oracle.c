@@ -9,7 +9,8 @@
  * be checked against the paper by eye:
  *
  *   - masses P_i^d                : Sec. 3.2, eq:round and its footnote
- *                                   (bin 0 open to -inf, bin D-1 open to +inf)
+ *                                   (bin 0 open to -inf, bin D-1 open to +inf);
+ *                                   other CDF families of App. D
  *   - expected usage              : App. B.2 (Res^), App. B.3 (modulo fold, MRes^)
  *   - resource violation          : App. B.2, eq:relu
  *   - dependency violation        : Sec. 3.2, eq:dep (with producer delay)
@@ -89,12 +90,49 @@ int orc_num_threads(void) {
 #endif
 }
 
-/* ---------------------------------------------------------------- Gaussian */
+/* ------------------------------------------------------ distribution family */
 
-/* standard normal CDF and its upper tail, via the complementary error function */
-static double Phi(double z) { return 0.5 * erfc(-z / M_SQRT2); }
-static double Qtail(double z) { return 0.5 * erfc(z / M_SQRT2); }
-static double phi(double z) { return exp(-0.5 * z * z) / sqrt(2.0 * M_PI); }
+/* The relaxed start time is mu + sigma Z with Z of the chosen family
+ * (App. D): 0 Gaussian; 1 logistic with scale s = sigma sqrt(3)/pi and
+ * 2 Laplace with scale b = sigma/sqrt(2) (variance sigma^2); 3 Cauchy with
+ * scale gamma = sigma sqrt(2 ln 2) (the Gaussian's half-maximum width).
+ * Below, z is in sigma units and u = z / c the family's own variable. */
+static int g_family = 0;
+
+void orc_set_family(int32_t family) { g_family = family; }
+
+static double fam_c(void) {
+    switch (g_family) {
+    case 1: return sqrt(3.0) / M_PI;
+    case 2: return 1.0 / sqrt(2.0);
+    case 3: return sqrt(2.0 * log(2.0));
+    default: return 1.0;
+    }
+}
+
+/* P(Z > z) for z >= 0 (the upper tail; by symmetry P(Z <= -z) too) */
+static double tail_pos(double z) {
+    const double u = z / fam_c();
+    switch (g_family) {
+    case 1: return exp(-u) / (1.0 + exp(-u));
+    case 2: return 0.5 * exp(-u);
+    case 3: return u > 1.0 ? atan(1.0 / u) / M_PI : 0.5 - atan(u) / M_PI;
+    default: return 0.5 * erfc(z / M_SQRT2);
+    }
+}
+
+/* CDF, upper tail and density (with respect to z) of Z */
+static double Phi(double z) { return z >= 0.0 ? 1.0 - tail_pos(z) : tail_pos(-z); }
+static double Qtail(double z) { return z >= 0.0 ? tail_pos(z) : 1.0 - tail_pos(-z); }
+static double phi(double z) {
+    const double c = fam_c(), u = fabs(z) / c;
+    switch (g_family) {
+    case 1: return exp(-u) / ((1.0 + exp(-u)) * (1.0 + exp(-u))) / c;
+    case 2: return 0.5 * exp(-u) / c;
+    case 3: return 1.0 / (M_PI * c * (1.0 + u * u));
+    default: return exp(-0.5 * z * z) / sqrt(2.0 * M_PI);
+    }
+}
 
 /* eq:round: P_i^d = Phi((d+1/2-mu)/sigma) - Phi((d-1/2-mu)/sigma); the lower
  * limit of bin 0 is -inf and the upper limit of bin D-1 is +inf (footnote).

@@ -253,12 +253,30 @@ def test_p7_gradient_finite_differences(orc, II, n_back, beta, tau, gamma):
 torch = pytest.importorskip("torch")
 
 
-def _torch_total(p, mu, sg, lam, alpha, rho, beta=0.0, tau=1e-2, gamma=0.0):
+def _torch_cdf(family):
+    """CDF of the relaxation's family in sigma units, from torch's own
+    distributions (App. D's scale matching)."""
+    import math
+    if family == "logistic":
+        c = math.sqrt(3.0) / math.pi
+        return lambda z: torch.sigmoid(z / c)
+    if family == "laplace":
+        dist = torch.distributions.Laplace(torch.tensor(0.0, dtype=torch.float64),
+                                           torch.tensor(1.0 / math.sqrt(2.0), dtype=torch.float64))
+        return dist.cdf
+    if family == "cauchy":
+        dist = torch.distributions.Cauchy(torch.tensor(0.0, dtype=torch.float64),
+                                          torch.tensor(math.sqrt(2.0 * math.log(2.0)), dtype=torch.float64))
+        return dist.cdf
+    return torch.special.ndtr
+
+
+def _torch_total(p, mu, sg, lam, alpha, rho, beta=0.0, tau=1e-2, gamma=0.0, family="gaussian"):
     """The objective written with fp64 torch ops straight from the paper's
     printed double sums (a second, independent formulation)."""
     D = p.D
     d = torch.arange(D, dtype=torch.float64)
-    nd = torch.special.ndtr
+    nd = _torch_cdf(family)
     hi = nd((d[None, :] + 0.5 - mu[:, None]) / sg[:, None])
     lo = nd((d[None, :] - 0.5 - mu[:, None]) / sg[:, None])
     hi = torch.cat([hi[:, :-1], torch.ones_like(hi[:, :1])], 1)      # bin D-1 open to +inf
@@ -663,3 +681,82 @@ def test_p17_legalized_schedules_are_legal(orc):
         for b in range(4):
             if st[b] == 0:
                 assert out[b, 5] == 1.0
+
+
+# ------------------------------------------------------------------- P18
+
+FAMS = ["logistic", "laplace", "cauchy"]
+SCALE = {"logistic": np.sqrt(3.0) / np.pi, "laplace": 1.0 / np.sqrt(2.0), "cauchy": np.sqrt(2.0 * np.log(2.0))}
+QUARTILE = {"logistic": np.log(3.0), "laplace": np.log(2.0), "cauchy": 1.0}   # G(q) = 3/4 in the family's unit
+
+
+@pytest.fixture
+def family(orc, request):
+    orc.set_family(request.param)
+    yield request.param
+    orc.set_family("gaussian")
+
+
+@pytest.mark.parametrize("family", FAMS, indirect=True)
+def test_p18_masses_sum_to_one_and_quartile(orc, family):
+    """App. D families: masses telescope to 1; the CDF at the bin edge where
+    the family's variable equals its upper quartile (logistic ln 3, Laplace
+    ln 2, Cauchy 1, with the scale matching of App. D) is exactly 3/4."""
+    D, t = 400, 200
+    for sigma in (0.7, 13.0, 150.0):
+        mu = t + 0.5 - sigma * SCALE[family] * QUARTILE[family]
+        P = np.array([orc.mass(mu, sigma, d, D) for d in range(D)])
+        assert abs(P.sum() - 1.0) < 1e-13
+        assert abs(P[:t + 1].sum() - 0.75) < 1e-13
+
+
+@pytest.mark.parametrize("family", FAMS, indirect=True)
+def test_p18_symmetric_about_the_centre(orc, family):
+    """Centred in an odd horizon, the masses are symmetric, so the mean is
+    the centre exactly; the density is symmetric in the family's variable."""
+    D = 101
+    mu = 50.0
+    for sigma in (0.4, 5.0, 80.0):
+        P = np.array([orc.mass(mu, sigma, d, D) for d in range(D)])
+        assert np.abs(P - P[::-1]).max() < 1e-15
+        assert abs((P * np.arange(D)).sum() - mu) < 1e-11
+
+
+def test_p18_cauchy_half_width_matches_gaussian(orc):
+    """App. D's Cauchy scale matches the Gaussian's full width at half
+    maximum: far from the boundaries the masses of both fall to half their
+    peak at the same offset sigma sqrt(2 ln 2)."""
+    D, sigma = 40001, 3000.0
+    mu = 20000.0
+    off = int(round(sigma * np.sqrt(2 * np.log(2))))
+    for fam in ("gaussian", "cauchy"):
+        orc.set_family(fam)
+        r = orc.mass(mu, sigma, 20000 + off, D) / orc.mass(mu, sigma, 20000, D)
+        assert abs(r - 0.5) < 2e-4, (fam, r)
+    orc.set_family("gaussian")
+
+
+@pytest.mark.parametrize("family", FAMS, indirect=True)
+def test_p18_gradient_matches_autograd(orc, family):
+    """The hand-derived backward with each family's density equals fp64
+    autograd of the double-sum formulation built on torch's distributions."""
+    rng = np.random.default_rng(180 + FAMS.index(family))
+    done = 0
+    for _ in range(5):
+        p = tiny_problem(rng, 6, 10, II=3, n_back=2, max_delay=2, K=2)
+        p.mem_units = rng.uniform(0.5, 2.0, size=6)
+        mu = rng.uniform(-1, 10, size=6); sg = np.exp(rng.uniform(np.log(0.3), np.log(5.0), size=6))
+        lam = rng.uniform(0.05, 1.0, size=3).tolist()
+        terms, U, gm, gs, ties = orc.loss_grad(p, mu, sg, lam, 0.29, 0.13, tie_tol=1e-6, beta=0.5, tau=0.1,
+                                               gamma=0.4)
+        if ties[0]:
+            continue
+        tm = torch.tensor(mu, dtype=torch.float64, requires_grad=True)
+        ts = torch.tensor(sg, dtype=torch.float64, requires_grad=True)
+        L = _torch_total(p, tm, ts, lam, 0.29, 0.13, 0.5, 0.1, 0.4, family=family)
+        L.backward()
+        assert abs(L.item() - terms[0, 0]) < 1e-10
+        assert np.abs(tm.grad.numpy() - gm[0]).max() < 1e-9
+        assert np.abs(ts.grad.numpy() - gs[0]).max() < 1e-9
+        done += 1
+    assert done >= 3
