@@ -129,6 +129,7 @@ def cpu_baseline(prob, mu, sigma, lam, hp, n_restarts):
     import numpy as np
     import oracle
     oracle.build(force=False)
+    oracle.set_family(hp.family)
     t0 = time.perf_counter()
     for b in range(n_restarts):
         _, _, gm, gs, _ = oracle.loss_grad(prob, mu[b:b + 1].astype(np.float64), sigma[b:b + 1].astype(np.float64),
@@ -138,6 +139,7 @@ def cpu_baseline(prob, mu, sigma, lam, hp, n_restarts):
         oracle.adam(mu[b].astype(np.float64), z, z, gm[0], 1, hp.lr)
         oracle.adam(sigma[b].astype(np.float64), z, z, gs[0], 1, hp.lr)
     dt = time.perf_counter() - t0
+    oracle.set_family("gaussian")
     return {"value": n_restarts * prob.n_ops * prob.D / dt, "unit": "op-step evals/s",
             "cores": oracle.num_threads(), "kind": "oracle",
             "sample": f"{n_restarts} of {mu.shape[0]} restarts of the same workload and state, one fused "
@@ -160,6 +162,9 @@ def main():
     ap.add_argument("--mem-gamma", type=float, default=0.0,
                     help="weight of the smooth peak storage term (storage units of 1-32 bits per op and a "
                          "sink op are added to the workload); 0 = off")
+    ap.add_argument("--family", default="gaussian", choices=["gaussian", "logistic", "laplace", "cauchy"],
+                    help="distribution of the relaxed start times (App. D); non-Gaussian families run "
+                         "every op step by step")
     ap.add_argument("--solve-check-every", type=int, default=0,
                     help="time the Alg. 1 driver (gaus_solve) with a legalization check every this many "
                          "iterations instead of plain steps + one legalization; 0 = off")
@@ -190,6 +195,7 @@ def main():
     hp.beta_res = args.lse_beta
     hp.tau = args.tau
     hp.gamma_mem = args.mem_gamma
+    hp.family = bd.FAMILIES[args.family]
     dev = torch.device("cuda")
     ctx = bd.Context(prob, B, hp)
     mu = torch.zeros(B, N, device=dev)
@@ -278,6 +284,8 @@ def main():
         profile += "_lse"
     if args.mem_gamma:
         profile += "_mem"
+    if args.family != "gaussian":
+        profile += "_" + args.family
     whole = model_flops(B * N * (D - 1), B * (E + prob.n_back) * (D - 1))
     out = {
         "metric": METRIC, "value": value, "unit": "op-step evals/s", "n_gpus": 1,
@@ -289,7 +297,8 @@ def main():
                    "objective": "alpha L_com + ALM(V_dep, V_res, V_rec)" +
                                 (f" + {args.lse_beta:g} L_res (tau {args.tau:g})" if args.lse_beta else "") +
                                 (f" + {args.mem_gamma:g} L_mem (tau {args.tau:g}; storage units and a sink op)"
-                                 if args.mem_gamma else "")},
+                                 if args.mem_gamma else ""),
+                   "family": args.family},
         "ms_per_iteration_events": step_ms_events, "legalize_ms": legalize_ms,
         "poly_path": dict(poly_cfg, ops=census["ops"], edges=census["edges"]),
         "solve": solve_stats,

@@ -82,7 +82,8 @@ typedef struct {
  * (App. C.1: Adam lr 1e-2, rho 1e-4, kappa 1/6, LogSumExp temperature 1e-2;
  * Sec. 3.3: lambda0 1e-6) and this library's choices for the unstated ones
  * (Adam betas/eps as in Kingma & Ba, alpha_com 0.01, sigma_min 0.05,
- * beta_res 0 and gamma_mem 0: the smooth peak terms are off unless asked for). */
+ * beta_res 0 and gamma_mem 0: the smooth peak terms are off unless asked for;
+ * family 0, the Gaussian of Sec. 3.1). */
 typedef struct {
     float lr, beta1, beta2, eps;   /* Adam */
     float rho;                     /* ALM penalty */
@@ -104,6 +105,12 @@ typedef struct {
                                       expected storage units of eq:active folded like the
                                       usage (App. B.3).  When > 0 every op is evaluated step
                                       by step (no chunk polynomials). */
+    int32_t family;                /* distribution of the relaxed start times (App. D):
+                                      0 Gaussian, 1 logistic (scale sigma sqrt(3)/pi),
+                                      2 Laplace (scale sigma/sqrt(2)), 3 Cauchy (scale
+                                      sigma sqrt(2 ln 2)); sigma keeps its meaning as the
+                                      Gaussian-matched width.  Non-Gaussian families are
+                                      evaluated step by step (no chunk polynomials). */
 } gaus_hparams;
 
 void gaus_default_hparams(gaus_hparams *hp);

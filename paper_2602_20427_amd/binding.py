@@ -58,7 +58,11 @@ class HParams(C.Structure):
     _fields_ = [("lr", C.c_float), ("beta1", C.c_float), ("beta2", C.c_float), ("eps", C.c_float),
                 ("rho", C.c_float), ("lambda0", C.c_float), ("alpha_com", C.c_float),
                 ("sigma_min", C.c_float), ("kappa", C.c_float), ("poly_chunk", C.c_int32),
-                ("beta_res", C.c_float), ("tau", C.c_float), ("gamma_mem", C.c_float)]
+                ("beta_res", C.c_float), ("tau", C.c_float), ("gamma_mem", C.c_float),
+                ("family", C.c_int32)]
+
+# CDF family of the relaxed start times (App. D), the values of HParams.family
+FAMILIES = {"gaussian": 0, "logistic": 1, "laplace": 2, "cauchy": 3}
 
 N_TERMS = 7   # L, V_dep, V_res, V_rec, L_com, L_res, L_mem
 

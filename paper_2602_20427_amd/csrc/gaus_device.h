@@ -30,6 +30,86 @@ __device__ __forceinline__ void normal_tail_pdf(float z, float &tail, float &g) 
     tail = 0.5f * g * (t * q);
 }
 
+// Families of the relaxed start time (App. D).  Each is the CDF of a
+// symmetric law of z = (v + 1/2 - mu)/sigma; the non-Gaussian ones are taken
+// at u = z/c, with c matching them to the Gaussian: logistic c = sqrt(3)/pi and
+// Laplace c = 1/sqrt(2) (equal variance), Cauchy c = sqrt(2 ln 2) (equal
+// half-width at half maximum).  fam_tail_h<FAM>(z, tail, h) returns the tail
+// P(Z > |z|) and a density factor h with density(z) = fam_k<FAM>() * h;
+// fam_h<FAM>(z) returns h alone.
+constexpr float kLog2e = 1.44269504088896341f;
+constexpr float kInvPi = 0.31830988618379067f;
+
+template <int FAM>
+__host__ __device__ constexpr float fam_cinv() {   // 1/c
+    return FAM == 1 ? 1.81379936423421785f : FAM == 2 ? 1.41421356237309505f
+         : FAM == 3 ? 0.84932180028801904f : 1.0f;
+}
+template <int FAM>
+__host__ __device__ constexpr float fam_k() {
+    return FAM == 1 ? 1.81379936423421785f    // logistic: h = e/(1+e)^2, e = exp(-|u|); k = 1/c
+         : FAM == 2 ? 0.70710678118654752f    // Laplace:  h = exp(-|u|); k = 1/(2c)
+         : FAM == 3 ? 0.27034752558309155f    // Cauchy:   h = 1/(1+u^2); k = 1/(pi c)
+         : kInvSqrt2Pi;                       // Gaussian: h = exp(-z^2/2)
+}
+
+template <int FAM>
+__device__ __forceinline__ void fam_tail_h(float z, float &tail, float &h) {
+    if constexpr (FAM == 0) {
+        normal_tail_pdf(z, tail, h);
+    } else if constexpr (FAM == 1) {
+        const float e = __builtin_amdgcn_exp2f(-fabsf(z) * (fam_cinv<1>() * kLog2e));
+        const float r = __builtin_amdgcn_rcpf(1.0f + e);
+        tail = e * r;                 // e/(1+e) = 1/(1+exp|u|)
+        h = tail * r;
+    } else if constexpr (FAM == 2) {
+        const float e = __builtin_amdgcn_exp2f(-fabsf(z) * (fam_cinv<2>() * kLog2e));
+        tail = 0.5f * e;
+        h = e;
+    } else {
+        // P(U > u) = atan(1/u)/pi for u > 1 (no cancellation), 1/2 - atan(u)/pi below
+        const float u = fabsf(z) * fam_cinv<3>();
+        const bool far = u > 1.0f;
+        const float a = atanf(far ? __builtin_amdgcn_rcpf(u) : u);
+        tail = far ? a * kInvPi : fmaf(-a, kInvPi, 0.5f);
+        h = __builtin_amdgcn_rcpf(fmaf(u, u, 1.0f));
+    }
+}
+
+template <int FAM>
+__device__ __forceinline__ float fam_h(float z) {
+    if constexpr (FAM == 0) {
+        return __builtin_amdgcn_exp2f(-(z * z) * kHalfLog2e);
+    } else if constexpr (FAM == 1) {
+        const float e = __builtin_amdgcn_exp2f(-fabsf(z) * (fam_cinv<1>() * kLog2e));
+        const float r = __builtin_amdgcn_rcpf(1.0f + e);
+        return e * r * r;
+    } else if constexpr (FAM == 2) {
+        return __builtin_amdgcn_exp2f(-fabsf(z) * (fam_cinv<2>() * kLog2e));
+    } else {
+        const float u = z * fam_cinv<3>();
+        return __builtin_amdgcn_rcpf(fmaf(u, u, 1.0f));
+    }
+}
+
+// The same with the family chosen at run time (kernels outside the inner loops).
+__device__ __forceinline__ float fam_k_rt(int fam) {
+    switch (fam) {
+        case 1: return fam_k<1>();
+        case 2: return fam_k<2>();
+        case 3: return fam_k<3>();
+        default: return fam_k<0>();
+    }
+}
+__device__ __forceinline__ float fam_h_rt(int fam, float z) {
+    switch (fam) {
+        case 1: return fam_h<1>(z);
+        case 2: return fam_h<2>(z);
+        case 3: return fam_h<3>(z);
+        default: return fam_h<0>(z);
+    }
+}
+
 // A CDF value F is kept as a signed tail: +Phi(-|z|) below the median
 // (F = tail) and -Phi(-|z|) at or above it (F = 1 - tail; -0.0 for F = 1).
 // Differences of neighbouring CDF values (the masses P_i^d) are then formed
@@ -46,26 +126,29 @@ __device__ __forceinline__ float st_mass(float lo, float hi) {
 }
 
 // Signed-tail CDF and its derivatives at bin edge v of an op (mu, rs = 1/sigma,
-// cinv = 1/(sigma sqrt(2 pi))): dF/dmu = -phi(z)/sigma, dF/dsigma = -phi(z) z/sigma.
-// Outside the interior edges F is the constant 0 (v < 0) or 1 (v >= D-1).
+// cinv = fam_k<FAM>()/sigma, i.e. 1/(sigma sqrt(2 pi)) for the Gaussian):
+// dF/dmu = -phi(z)/sigma, dF/dsigma = -phi(z) z/sigma.  Outside the interior
+// edges F is the constant 0 (v < 0) or 1 (v >= D-1).
+template <int FAM = 0>
 __device__ __forceinline__ void cdf_at(long long v, int D, float mu, float rs, float cinv, float &st,
                                        float &Fm, float &Fs) {
     if (v < 0) { st = 0.0f; Fm = 0.0f; Fs = 0.0f; return; }
     if (v >= D - 1) { st = -0.0f; Fm = 0.0f; Fs = 0.0f; return; }
     const float z = ((float)v + 0.5f - mu) * rs;
     float tail, g;
-    normal_tail_pdf(z, tail, g);
+    fam_tail_h<FAM>(z, tail, g);
     st = (z >= 0.0f) ? -tail : tail;
     Fm = -g * cinv;
     Fs = Fm * z;
 }
 
+template <int FAM = 0>
 __device__ __forceinline__ float st_at(long long v, int D, float mu, float rs) {
     if (v < 0) return 0.0f;
     if (v >= D - 1) return -0.0f;
     const float z = ((float)v + 0.5f - mu) * rs;
     float tail, g;
-    normal_tail_pdf(z, tail, g);
+    fam_tail_h<FAM>(z, tail, g);
     return (z >= 0.0f) ? -tail : tail;
 }
 

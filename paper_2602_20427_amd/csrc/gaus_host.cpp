@@ -355,6 +355,7 @@ void gaus_default_hparams(gaus_hparams *hp) {
     hp->beta_res = 0.0f;
     hp->tau = 1e-2f;
     hp->gamma_mem = 0.0f;
+    hp->family = 0;
 }
 
 const char *gaus_status_string(gaus_status s) {
@@ -381,31 +382,32 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     *out = nullptr;
     gaus_status s = validate(prob, B);
     if (s != GAUS_OK) return s;
+    gaus_hparams hp;
+    if (hp_in) hp = *hp_in; else gaus_default_hparams(&hp);
+    if (hp.poly_chunk > 0 && (hp.poly_chunk < 16 || hp.poly_chunk > 256))
+        return fail(nullptr, GAUS_E_INVALID_ARG, "poly_chunk must be 0 (auto), negative (off) or in [16, 256]");
+    if (!(hp.beta_res >= 0.0f) || !std::isfinite(hp.beta_res) || !(hp.tau > 0.0f) || !std::isfinite(hp.tau) ||
+        !(hp.gamma_mem >= 0.0f) || !std::isfinite(hp.gamma_mem))
+        return fail(nullptr, GAUS_E_INVALID_ARG, "beta_res and gamma_mem must be finite and >= 0, tau finite and > 0");
+    if (hp.family < 0 || hp.family > 3)
+        return fail(nullptr, GAUS_E_INVALID_ARG, "family must be 0 (Gaussian), 1 (logistic), 2 (Laplace) or 3 (Cauchy)");
     HostGraph h;
     s = preprocess(prob, h);
     if (s != GAUS_OK) return s;
 
     gaus_ctx *c = new (std::nothrow) gaus_ctx();
     if (!c) return fail(nullptr, GAUS_E_NOMEM, "host allocation failed");
-    gaus_hparams hp;
-    if (hp_in) hp = *hp_in; else gaus_default_hparams(&hp);
     c->hp = HP{hp.lr,        hp.beta1,     hp.beta2,     hp.eps,      hp.rho, hp.lambda0,
-               hp.alpha_com, hp.sigma_min, hp.kappa,     hp.beta_res, hp.tau, hp.gamma_mem};
+               hp.alpha_com, hp.sigma_min, hp.kappa,     hp.beta_res, hp.tau, hp.gamma_mem,
+               hp.family};
     c->stream = static_cast<hipStream_t>(hip_stream);
     (void)hipGetDevice(&c->device);
     int tile = 0, ntiles = 0;
     choose_config(h, B, c->lc, tile, ntiles);
-    if (hp.poly_chunk > 0 && (hp.poly_chunk < 16 || hp.poly_chunk > 256)) {
-        delete c;
-        return fail(nullptr, GAUS_E_INVALID_ARG, "poly_chunk must be 0 (auto), negative (off) or in [16, 256]");
-    }
-    if (!(hp.beta_res >= 0.0f) || !std::isfinite(hp.beta_res) || !(hp.tau > 0.0f) || !std::isfinite(hp.tau) ||
-        !(hp.gamma_mem >= 0.0f) || !std::isfinite(hp.gamma_mem)) {
-        delete c;
-        return fail(nullptr, GAUS_E_INVALID_ARG, "beta_res and gamma_mem must be finite and >= 0, tau finite and > 0");
-    }
-    // the storage term's successor products are evaluated step by step only
-    setup_poly(h.D, hp.gamma_mem > 0.0f ? -1 : hp.poly_chunk, c->pa);
+    c->lc.fam = hp.family;
+    // the storage term's successor products and the non-Gaussian families are
+    // evaluated step by step only
+    setup_poly(h.D, (hp.gamma_mem > 0.0f || hp.family != 0) ? -1 : hp.poly_chunk, c->pa);
 
     Graph &g = c->g;
     g.N = h.N; g.E = h.E; g.K = h.K; g.D = h.D; g.II = h.II; g.T = h.II > 0 ? h.II : h.D;

@@ -123,12 +123,14 @@ struct HP {
     float lr, b1, b2, eps, rho, lambda0, alpha, sigma_min, kappa;
     float beta, tau;   // weight and temperature of the smooth peak usage L_res
     float gamma;       // weight of the smooth peak storage L_mem (same temperature)
+    int family;        // CDF family of the start times: 0 Gaussian, 1 logistic, 2 Laplace, 3 Cauchy
 };
 
 // Kernel-side configuration chosen on the host from (N, D, B).
 struct LaunchCfg {
     int bs;    // threads per work-group of the op kernel (64 or 256)
     int spt;   // steps per thread (1 or 4)
+    int fam;   // CDF family (HP::family), a template argument of the step-by-step kernels
 };
 
 // Enqueue one forward+backward.  mode 0: write terms/grad to the outputs;

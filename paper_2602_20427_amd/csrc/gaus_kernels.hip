@@ -146,9 +146,11 @@ __global__ __launch_bounds__(kUsageBS) void k_usage(Graph G, PolyArgs pa, Work W
     const int slot = blockIdx.x * kUsageBS + tid;
     if (slot >= T) return;
     const int ncoef = pa.nc * kNC;
-    float acc = 0.0f;
+    // fp64 sums: the softmax of the smooth peak terms amplifies a usage error
+    // dU by about dU/tau, so U is formed to well below fp32 rounding of its sum
+    double acc = 0.0;
     for (int t = slot; t < D; t += T) {
-        float ut = 0.0f;
+        double ut = 0.0;
         if (nact <= kMaxAct) {
             for (int q = 0; q < nact; ++q) ut += W.Upart[((size_t)b * G.ngroups + sAct[q]) * D + t];
         } else {
@@ -163,14 +165,14 @@ __global__ __launch_bounds__(kUsageBS) void k_usage(Graph G, PolyArgs pa, Work W
                 float v = cf[kNC - 1];
 #pragma unroll
                 for (int q = kNC - 2; q >= 0; --q) v = fmaf(v, x, cf[q]);
-                ut += v;
+                ut += (double)v;
             } else {
-                ut += sC[ncoef + (t < pa.L0 ? t : pa.L0 + (t - (D - 2)))];
+                ut += (double)sC[ncoef + (t < pa.L0 ? t : pa.L0 + (t - (D - 2)))];
             }
         }
         acc += ut;
     }
-    W.U[((size_t)b * G.K + k) * T + slot] = acc;
+    W.U[((size_t)b * G.K + k) * T + slot] = (float)acc;
 }
 
 // ---------------------------------------------------------------------------
@@ -453,7 +455,7 @@ __global__ __launch_bounds__(256) void k_final(Graph G, Work W, HP hp, const flo
     const int N = G.N, nt = G.ntiles;
     const size_t bi = (size_t)b * N + i;
     const float m_i = mu[bi], s_i = sigma[bi];
-    const float rs = 1.0f / s_i, cinv = rs * kInvSqrt2Pi;
+    const float rs = 1.0f / s_i, cinv = rs * fam_k_rt(hp.family);
     const float *wt = W.wts + (size_t)b * 4;
     const float w_dep = wt[0], w_res = wt[1], w_rec = wt[2];
 
@@ -469,8 +471,7 @@ __global__ __launch_bounds__(256) void k_final(Graph G, Work W, HP hp, const flo
         const float sgn = code > 0 ? 1.0f : -1.0f;
         const int t = (code > 0 ? code : -code) - 1;
         const float z = ((float)t + 0.5f - m_i) * rs;
-        const float g = __builtin_amdgcn_exp2f(-(z * z) * kHalfLog2e);
-        const float Fm = -g * cinv;
+        const float Fm = -fam_h_rt(hp.family, z) * cinv;
         rm += (double)(sgn * Fm);
         rsg += (double)(sgn * (Fm * z));
     }

@@ -2,6 +2,8 @@
 // evaluated directly (k_ops for the forward edges, k_back for back edges,
 // k_lse_ops for the gradient of the smooth peak usage).  See gaus_kernels.hip
 // for the notation.
+#include <type_traits>
+
 #include "gaus_device.h"
 
 namespace gaus {
@@ -12,7 +14,7 @@ namespace gaus {
 // resource type, out-degree m, delay s = Lat(v_i)):
 //   * its CDF row over the tile plus a left halo of s steps goes to LDS; the
 //     mass P_i^u is added to the group's usage;
-//   * for each out-edge (i -> j) the consumer's CDF and Gaussian factor are
+//   * for each out-edge (i -> j) the consumer's CDF and density factor are
 //     evaluated once per step.  The consumer-side derivatives of this edge are
 //       dVdep/dth_j = sum_u A(u) F_j'(u),   A(u) = P_i^{u-s+1}
 //       dLcom/dth_j = -sum_u F_i(u) F_j'(u)
@@ -27,7 +29,7 @@ namespace gaus {
 //     (u over the interior edges 0..D-2 except in dVdep/dth_i, which runs to
 //     u = D-1 with S_i(D-1) = m: the consumers' bin D-1 is open to +inf).
 // ---------------------------------------------------------------------------
-template <int BS, int SPT>
+template <int FAM, int BS, int SPT>
 __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ mu,
                                             const float *__restrict__ sigma, Work W) {
     constexpr int TILE = BS * SPT;
@@ -82,7 +84,7 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
         const int m = uniform(flag - 1);
         const float m_i = mub[i], s_i = sgb[i];
         const float rs = 1.0f / s_i;
-        const float cinv = rs * kInvSqrt2Pi;
+        const float cinv = rs * fam_k<FAM>();
         const int s = uniform(G.delay[i]);
         const bool win_shift = (m > 0) && (s <= kHalo);
         const int Lh = win_shift ? (s > 1 ? s : 1) : 1;
@@ -90,7 +92,7 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
         // row window: positions v = t0 - Lh + p, p in [0, TILE + Lh]
         for (int p = tid; p < TILE + Lh + 1; p += BS) {
             float st, Fm, Fs;
-            cdf_at(t0 - Lh + p, D, m_i, rs, cinv, st, Fm, Fs);
+            cdf_at<FAM>(t0 - Lh + p, D, m_i, rs, cinv, st, Fm, Fs);
             sT[p] = st; sFm[p] = Fm; sFs[p] = Fs;
         }
         __syncthreads();
@@ -111,8 +113,8 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
                     if (u == D - 1) tail1mF = st_1mF(sT[p - s]);
                 } else {
                     float st0, Fm0, Fs0, st1, Fm1, Fs1;
-                    cdf_at((long long)u - s, D, m_i, rs, cinv, st0, Fm0, Fs0);
-                    cdf_at((long long)u - s + 1, D, m_i, rs, cinv, st1, Fm1, Fs1);
+                    cdf_at<FAM>((long long)u - s, D, m_i, rs, cinv, st0, Fm0, Fs0);
+                    cdf_at<FAM>((long long)u - s + 1, D, m_i, rs, cinv, st1, Fm1, Fs1);
                     rA[k] = st_mass(st0, st1); rFms[k] = Fm0; rFss[k] = Fs0;
                     if (u == D - 1) tail1mF = st_1mF(st0);
                 }
@@ -137,7 +139,7 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
                 if (u < D - 1) {
                     const float z = ((float)u + 0.5f - m_j) * rsj;
                     float tl, gj;
-                    normal_tail_pdf(z, tl, gj);
+                    fam_tail_h<FAM>(z, tl, gj);
                     const bool up = z >= 0.0f;
                     SL[k] += up ? 0.0f : tl;
                     SU[k] += up ? tl : 0.0f;
@@ -152,14 +154,14 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
             if (tid == 0 && t0 > 0) {
                 const float z = ((float)(t0 - 1) + 0.5f - m_j) * rsj;
                 float tl, gj;
-                normal_tail_pdf(z, tl, gj);
+                fam_tail_h<FAM>(z, tl, gj);
                 if (z >= 0.0f) { pU += tl; pC += 1.0f; } else { pL += tl; }
             }
             const float r = block_sum<4, BS>(acc, sRed[par]);
             par ^= 1;
             if (tid < 4) {
-                // F_j'(u) = -g_j/(sigma_j sqrt(2 pi)) [* z for sigma]; L_com enters with a minus
-                const float cj = rsj * kInvSqrt2Pi;
+                // F_j'(u) = -k g_j/sigma_j (k = fam_k, g_j the density factor) [* z for sigma]; L_com enters with a minus
+                const float cj = rsj * fam_k<FAM>();
                 const float val = (tid < 2) ? -cj * r : cj * r;
                 W.cpart[(((size_t)b * G.E + e) * G.ntiles + tile) * kCP + tid] = val;
             }
@@ -231,7 +233,7 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
 //   dVrec/dth_i =  sum_t F_i'(t) P_j^{t+c+1}
 // with u, t over the interior edges 0..D-2.
 // ---------------------------------------------------------------------------
-template <int BS, int SPT>
+template <int FAM, int BS, int SPT>
 __global__ __launch_bounds__(BS) void k_back(Graph G, const float *__restrict__ mu,
                                              const float *__restrict__ sigma, Work W,
                                              int edges_per_block) {
@@ -249,17 +251,17 @@ __global__ __launch_bounds__(BS) void k_back(Graph G, const float *__restrict__ 
         const float mj = mu[(size_t)b * N + j], sj = sigma[(size_t)b * N + j];
         const float mi = mu[(size_t)b * N + i], si = sigma[(size_t)b * N + i];
         const float rsj = 1.0f / sj, rsi = 1.0f / si;
-        const float cj = rsj * kInvSqrt2Pi, ci = rsi * kInvSqrt2Pi;
+        const float cj = rsj * fam_k<FAM>(), ci = rsi * fam_k<FAM>();
         float acc[5] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int k = 0; k < SPT; ++k) {
             const int u = t0 + k * BS + tid;
             if (u < D - 1) {
                 float sj_, Fmj, Fsj, si_, Fmi, Fsi;
-                cdf_at(u, D, mj, rsj, cj, sj_, Fmj, Fsj);
-                cdf_at(u, D, mi, rsi, ci, si_, Fmi, Fsi);
-                const float Pi = st_mass(st_at((long long)u - c - 1, D, mi, rsi), st_at((long long)u - c, D, mi, rsi));
-                const float Pj = st_mass(st_at((long long)u + c, D, mj, rsj), st_at((long long)u + c + 1, D, mj, rsj));
+                cdf_at<FAM>(u, D, mj, rsj, cj, sj_, Fmj, Fsj);
+                cdf_at<FAM>(u, D, mi, rsi, ci, si_, Fmi, Fsi);
+                const float Pi = st_mass(st_at<FAM>((long long)u - c - 1, D, mi, rsi), st_at<FAM>((long long)u - c, D, mi, rsi));
+                const float Pj = st_mass(st_at<FAM>((long long)u + c, D, mj, rsj), st_at<FAM>((long long)u + c + 1, D, mj, rsj));
                 acc[0] = fmaf(Pi, st_1mF(sj_), acc[0]);
                 acc[1] = fmaf(-Fmj, Pi, acc[1]);
                 acc[2] = fmaf(-Fsj, Pi, acc[2]);
@@ -267,7 +269,7 @@ __global__ __launch_bounds__(BS) void k_back(Graph G, const float *__restrict__ 
                 acc[4] = fmaf(Fsi, Pj, acc[4]);
             }
         }
-        if (tile == 0 && tid == 0) acc[0] += st_F(st_at(-c - 1, D, mi, rsi));
+        if (tile == 0 && tid == 0) acc[0] += st_F(st_at<FAM>(-c - 1, D, mi, rsi));
         const float r = block_sum<5, BS>(acc, sRed[par]);
         par ^= 1;
         if (tid < kBP) W.bpart[(((size_t)b * G.nb + e) * G.ntiles + tile) * kBP + tid] = r;
@@ -285,7 +287,7 @@ __global__ __launch_bounds__(BS) void k_back(Graph G, const float *__restrict__ 
 // M_n = sum_y (c(t) - c(t+1)) y^n (k_lse_mom), dotted with the chunk
 // coefficients of dF/dmu and dF/dsigma (k_lse_poly).
 // ---------------------------------------------------------------------------
-template <int BS, int SPT>
+template <int FAM, int BS, int SPT>
 __global__ __launch_bounds__(BS) void k_lse_ops(Graph G, const float *__restrict__ mu,
                                                 const float *__restrict__ sigma, Work W) {
     constexpr int TILE = BS * SPT;
@@ -319,7 +321,7 @@ __global__ __launch_bounds__(BS) void k_lse_ops(Graph G, const float *__restrict
     for (int q = 0; q < q1 - q0; ++q) {
         const int i = sI[q];
         if (i < 0) continue;
-        const float m = sMu[q], rs = sRs[q], cinv = rs * kInvSqrt2Pi;
+        const float m = sMu[q], rs = sRs[q], cinv = rs * fam_k<FAM>();
         float acc[2] = {0.0f, 0.0f};
 #pragma unroll
         for (int j = 0; j < SPT; ++j) {
@@ -327,7 +329,7 @@ __global__ __launch_bounds__(BS) void k_lse_ops(Graph G, const float *__restrict
             const float w = sW[x];
             if (w != 0.0f) {
                 const float z = ((float)(t0 + x) + 0.5f - m) * rs;
-                const float Fm = -__builtin_amdgcn_exp2f(-(z * z) * kHalfLog2e) * cinv;
+                const float Fm = -fam_h<FAM>(z) * cinv;
                 acc[0] = fmaf(w, Fm, acc[0]);
                 acc[1] = fmaf(w, Fm * z, acc[1]);
             }
@@ -349,7 +351,7 @@ __global__ __launch_bounds__(BS) void k_lse_ops(Graph G, const float *__restrict
 // are kept in fp64: the profile reaches 1e5 units and more, and its
 // LogSumExp weights amplify absolute errors by 1/tau.
 // ---------------------------------------------------------------------------
-template <int BS, int SPT>
+template <int FAM, int BS, int SPT>
 __global__ __launch_bounds__(BS) void k_mem_fwd(Graph G, const float *__restrict__ mu,
                                                 const float *__restrict__ sigma, Work W) {
     constexpr int TILE = BS * SPT;
@@ -378,7 +380,7 @@ __global__ __launch_bounds__(BS) void k_mem_fwd(Graph G, const float *__restrict
         float Fi[SPT], Q[SPT], R[SPT];
 #pragma unroll
         for (int j = 0; j < SPT; ++j) {
-            Fi[j] = st_F(st_at((long long)t0 + tid + j * BS, D, m, rs));
+            Fi[j] = st_F(st_at<FAM>((long long)t0 + tid + j * BS, D, m, rs));
             Q[j] = 1.0f; R[j] = 0.0f;
         }
         for (int e = G.row_ptr[i]; e < G.row_ptr[i + 1]; ++e) {
@@ -386,7 +388,7 @@ __global__ __launch_bounds__(BS) void k_mem_fwd(Graph G, const float *__restrict
             const float mk = mub[k], rk = 1.0f / sgb[k];
 #pragma unroll
             for (int j = 0; j < SPT; ++j) {
-                const float st = st_at((long long)t0 + tid + j * BS, D, mk, rk);
+                const float st = st_at<FAM>((long long)t0 + tid + j * BS, D, mk, rk);
                 R[j] = fmaf(Q[j], st_1mF(st), R[j]);
                 Q[j] *= st_F(st);
             }
@@ -408,7 +410,7 @@ __global__ __launch_bounds__(BS) void k_mem_fwd(Graph G, const float *__restrict
 //   as a successor i:  -c(t) b_h F_h(t) prod_{j != i} F_j(t) dF_i(t)/dth_i
 // with prod_{j != i} F_j = Q_h / F_i (0 when F_i underflows: then so does
 // dF_i, and the term is below fp32 resolution).
-template <int BS, int SPT>
+template <int FAM, int BS, int SPT>
 __global__ __launch_bounds__(BS) void k_mem_bwd(Graph G, const float *__restrict__ mu,
                                                 const float *__restrict__ sigma, Work W) {
     constexpr int TILE = BS * SPT;
@@ -438,18 +440,18 @@ __global__ __launch_bounds__(BS) void k_mem_bwd(Graph G, const float *__restrict
     for (int q = 0; q < q1 - q0; ++q) {
         const int h = sI[q];
         if (h < 0) continue;
-        const float m = sMu[q], rs = sRs[q], cinv = rs * kInvSqrt2Pi, bh = G.bmem[h];
+        const float m = sMu[q], rs = sRs[q], cinv = rs * fam_k<FAM>(), bh = G.bmem[h];
         const int e0 = G.row_ptr[h], e1 = G.row_ptr[h + 1];
         float Fh[SPT], Q[SPT], R[SPT], own[2] = {0.0f, 0.0f};
 #pragma unroll
         for (int j = 0; j < SPT; ++j) {
             float st, Fm, Fs;
-            cdf_at((long long)t0 + tid + j * BS, D, m, rs, cinv, st, Fm, Fs);
+            cdf_at<FAM>((long long)t0 + tid + j * BS, D, m, rs, cinv, st, Fm, Fs);
             Fh[j] = st_F(st);
             Q[j] = 1.0f; R[j] = 0.0f;
             for (int e = e0; e < e1; ++e) {
                 const int k = G.col[e];
-                const float sk = st_at((long long)t0 + tid + j * BS, D, mub[k], 1.0f / sgb[k]);
+                const float sk = st_at<FAM>((long long)t0 + tid + j * BS, D, mub[k], 1.0f / sgb[k]);
                 R[j] = fmaf(Q[j], st_1mF(sk), R[j]);
                 Q[j] *= st_F(sk);
             }
@@ -464,12 +466,12 @@ __global__ __launch_bounds__(BS) void k_mem_bwd(Graph G, const float *__restrict
         }
         for (int e = e0; e < e1; ++e) {
             const int k = G.col[e];
-            const float mk = mub[k], rk = 1.0f / sgb[k], ck = rk * kInvSqrt2Pi;
+            const float mk = mub[k], rk = 1.0f / sgb[k], ck = rk * fam_k<FAM>();
             float acc[2] = {0.0f, 0.0f};
 #pragma unroll
             for (int j = 0; j < SPT; ++j) {
                 float st, Fm, Fs;
-                cdf_at((long long)t0 + tid + j * BS, D, mk, rk, ck, st, Fm, Fs);
+                cdf_at<FAM>((long long)t0 + tid + j * BS, D, mk, rk, ck, st, Fm, Fs);
                 const float Fk = st_F(st);
                 const float others = Fk > 0.0f ? Q[j] / Fk : 0.0f;
                 const float c = -sW[tid + j * BS] * bh * Fh[j] * others;
@@ -484,53 +486,75 @@ __global__ __launch_bounds__(BS) void k_mem_bwd(Graph G, const float *__restrict
 }
 
 // ---------------------------------------------------------------------------
-// Launchers
+// Launchers.  The CDF family and the work-group shape are template arguments;
+// dispatch() calls f(FAM, BS, SPT) with them as integral constants.
 // ---------------------------------------------------------------------------
+template <int V> using IC = std::integral_constant<int, V>;
+
+template <int FAM, class F>
+hipError_t dispatch_shape(const LaunchCfg &lc, F &&f) {
+    if (lc.bs == 64 && lc.spt == 1) f(IC<FAM>{}, IC<64>{}, IC<1>{});
+    else if (lc.bs == 256 && lc.spt == 1) f(IC<FAM>{}, IC<256>{}, IC<1>{});
+    else if (lc.bs == 256 && lc.spt == 4) f(IC<FAM>{}, IC<256>{}, IC<4>{});
+    else return hipErrorInvalidValue;
+    return hipSuccess;
+}
+
+template <class F>
+hipError_t dispatch(const LaunchCfg &lc, F &&f) {
+    switch (lc.fam) {
+        case 0: return dispatch_shape<0>(lc, f);
+        case 1: return dispatch_shape<1>(lc, f);
+        case 2: return dispatch_shape<2>(lc, f);
+        case 3: return dispatch_shape<3>(lc, f);
+    }
+    return hipErrorInvalidValue;
+}
+
 hipError_t launch_ops(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu, const float *sigma,
                       hipStream_t st) {
     const dim3 grid(g.ngroups, g.ntiles, g.B);
-    if (lc.bs == 64 && lc.spt == 1) hipLaunchKernelGGL((k_ops<64, 1>), grid, dim3(64), 0, st, g, mu, sigma, w);
-    else if (lc.bs == 256 && lc.spt == 1) hipLaunchKernelGGL((k_ops<256, 1>), grid, dim3(256), 0, st, g, mu, sigma, w);
-    else if (lc.bs == 256 && lc.spt == 4) hipLaunchKernelGGL((k_ops<256, 4>), grid, dim3(256), 0, st, g, mu, sigma, w);
-    else return hipErrorInvalidValue;
-    return hipSuccess;
+    return dispatch(lc, [&](auto fam, auto bs, auto spt) {
+        hipLaunchKernelGGL((k_ops<decltype(fam)::value, decltype(bs)::value, decltype(spt)::value>), grid,
+                           dim3(decltype(bs)::value), 0, st, g, mu, sigma, w);
+    });
 }
 
 hipError_t launch_back(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu, const float *sigma,
                        hipStream_t st) {
     const int epb = 4;
     const dim3 grid((g.nb + epb - 1) / epb, g.ntiles, g.B);
-    if (lc.bs == 64) hipLaunchKernelGGL((k_back<64, 1>), grid, dim3(64), 0, st, g, mu, sigma, w, epb);
-    else if (lc.spt == 1) hipLaunchKernelGGL((k_back<256, 1>), grid, dim3(256), 0, st, g, mu, sigma, w, epb);
-    else hipLaunchKernelGGL((k_back<256, 4>), grid, dim3(256), 0, st, g, mu, sigma, w, epb);
-    return hipSuccess;
+    return dispatch(lc, [&](auto fam, auto bs, auto spt) {
+        hipLaunchKernelGGL((k_back<decltype(fam)::value, decltype(bs)::value, decltype(spt)::value>), grid,
+                           dim3(decltype(bs)::value), 0, st, g, mu, sigma, w, epb);
+    });
 }
 
 hipError_t launch_lse_ops(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu,
                           const float *sigma, hipStream_t st) {
     const dim3 grid(g.ngroups, g.ntiles, g.B);
-    if (lc.bs == 64) hipLaunchKernelGGL((k_lse_ops<64, 1>), grid, dim3(64), 0, st, g, mu, sigma, w);
-    else if (lc.spt == 1) hipLaunchKernelGGL((k_lse_ops<256, 1>), grid, dim3(256), 0, st, g, mu, sigma, w);
-    else hipLaunchKernelGGL((k_lse_ops<256, 4>), grid, dim3(256), 0, st, g, mu, sigma, w);
-    return hipSuccess;
+    return dispatch(lc, [&](auto fam, auto bs, auto spt) {
+        hipLaunchKernelGGL((k_lse_ops<decltype(fam)::value, decltype(bs)::value, decltype(spt)::value>), grid,
+                           dim3(decltype(bs)::value), 0, st, g, mu, sigma, w);
+    });
 }
 
 hipError_t launch_mem_fwd(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu,
                           const float *sigma, hipStream_t st) {
     const dim3 grid(g.ngroups, g.ntiles, g.B);
-    if (lc.bs == 64) hipLaunchKernelGGL((k_mem_fwd<64, 1>), grid, dim3(64), 0, st, g, mu, sigma, w);
-    else if (lc.spt == 1) hipLaunchKernelGGL((k_mem_fwd<256, 1>), grid, dim3(256), 0, st, g, mu, sigma, w);
-    else hipLaunchKernelGGL((k_mem_fwd<256, 4>), grid, dim3(256), 0, st, g, mu, sigma, w);
-    return hipSuccess;
+    return dispatch(lc, [&](auto fam, auto bs, auto spt) {
+        hipLaunchKernelGGL((k_mem_fwd<decltype(fam)::value, decltype(bs)::value, decltype(spt)::value>), grid,
+                           dim3(decltype(bs)::value), 0, st, g, mu, sigma, w);
+    });
 }
 
 hipError_t launch_mem_bwd(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu,
                           const float *sigma, hipStream_t st) {
     const dim3 grid(g.ngroups, g.ntiles, g.B);
-    if (lc.bs == 64) hipLaunchKernelGGL((k_mem_bwd<64, 1>), grid, dim3(64), 0, st, g, mu, sigma, w);
-    else if (lc.spt == 1) hipLaunchKernelGGL((k_mem_bwd<256, 1>), grid, dim3(256), 0, st, g, mu, sigma, w);
-    else hipLaunchKernelGGL((k_mem_bwd<256, 4>), grid, dim3(256), 0, st, g, mu, sigma, w);
-    return hipSuccess;
+    return dispatch(lc, [&](auto fam, auto bs, auto spt) {
+        hipLaunchKernelGGL((k_mem_bwd<decltype(fam)::value, decltype(bs)::value, decltype(spt)::value>), grid,
+                           dim3(decltype(bs)::value), 0, st, g, mu, sigma, w);
+    });
 }
 
 }  // namespace gaus

@@ -41,7 +41,7 @@ def test_default_hparams_match_paper():
     assert (hp.beta1, hp.beta2) == (pytest.approx(0.9), pytest.approx(0.999))
 
 
-def _init(lib, p, B=1):
+def _init(lib, p, B=1, hp=None):
     arrs = [np.ascontiguousarray(x) for x in (p.row_ptr, p.col_idx, p.delay, p.rtype, p.capacity,
                                               p.back_src, p.back_dst, p.back_dist)]
     ptr = lambda a: a.ctypes.data_as(C.c_void_p)
@@ -51,7 +51,7 @@ def _init(lib, p, B=1):
                        len(p.back_src), ptr(arrs[5]), ptr(arrs[6]), ptr(arrs[7]),
                        None if mem is None else ptr(mem))
     h = C.c_void_p(12345)
-    st = lib.gaus_init(C.byref(prob), None, B, None, C.byref(h))
+    st = lib.gaus_init(C.byref(prob), None if hp is None else C.byref(hp), B, None, C.byref(h))
     return st, h.value, lib.gaus_last_error(None).decode()
 
 
@@ -87,6 +87,20 @@ def test_init_rejects_invalid_problems(lib, mutate, status, needle):
     st, h, msg = _init(lib, _chain(**mutate))
     assert st == status, msg
     assert h is None, "out must be NULL on failure"
+    assert needle in msg
+
+
+@pytest.mark.parametrize("field,value,needle", [
+    ("family", 4, "family"), ("family", -1, "family"),
+    ("tau", 0.0, "tau"), ("tau", float("nan"), "tau"),
+    ("beta_res", -1.0, "beta_res"), ("gamma_mem", float("inf"), "gamma_mem"),
+    ("poly_chunk", 8, "poly_chunk"), ("poly_chunk", 512, "poly_chunk"),
+])
+def test_init_rejects_invalid_hparams(lib, field, value, needle):
+    hp = bd.default_hparams()
+    setattr(hp, field, value)
+    st, h, msg = _init(lib, _chain(), hp=hp)
+    assert st == bd.E_INVALID_ARG and h is None, msg
     assert needle in msg
 
 

@@ -1,0 +1,147 @@
+"""Parity of the other start-time distributions (App. D: logistic, Laplace,
+Cauchy, each with its scale matched to the Gaussian sigma): loss terms,
+usage and gradients of the HIP path through the C ABI vs the fp64 oracle
+with the same family, alone and with the smooth peak usage and storage
+terms on."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2602_20427_amd import binding as bd
+from paper_2602_20427_amd.workloads import (CONFIGS, make_problem, random_state, restart_uniforms, uniform_state,
+                                            with_storage)
+from tests.gpu_common import TOL, compare_restart, gpu_loss_grad, hparams, say
+
+pytestmark = pytest.mark.gpu
+
+FAMS = ["logistic", "laplace", "cauchy"]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    oracle.build(force=False)
+    bd.load()
+    yield
+    oracle.set_family("gaussian")
+
+
+def _hp(family, **kw):
+    hp = hparams(**kw)
+    hp.family = bd.FAMILIES[family]
+    return hp
+
+
+def _init_state(cfg, p, B):
+    if CONFIGS[cfg].init == "uniform":
+        return uniform_state(p.n_ops, p.D, B, seed=0, sigma0=CONFIGS[cfg].sigma0)
+    mu, sg, rc = oracle.init_state(p, B, restart_uniforms(p.n_ops, B, seed=0))
+    assert rc == 0
+    return mu.astype(np.float32), sg.astype(np.float32)
+
+
+def _compare(p, mu, sg, lam, hp, family, what, beta=0.0, tau=1e-2, gamma=0.0):
+    g = gpu_loss_grad(p, mu, sg, lam, hp)
+    B = mu.shape[0]
+    oracle.set_family(family)
+    try:
+        for b in sorted({0, B - 1}):
+            ot, oU, ogm, ogs, ties = oracle.loss_grad(p, mu[b:b + 1].astype(np.float64),
+                                                      sg[b:b + 1].astype(np.float64), lam[b:b + 1],
+                                                      hp.alpha_com, hp.rho, tie_tol=1e-4, beta=beta, tau=tau,
+                                                      gamma=gamma)
+            if (beta > 0 or gamma > 0) and ties[0]:
+                say(f"  b={b}: {ties[0]} near-tie usage cells, comparing terms only")
+                err_t = np.abs(g["terms"][b] - ot[0]) / np.maximum(np.abs(ot[0]), 1.0)
+                assert err_t.max() <= TOL, (what, b, g["terms"][b], ot[0])
+                continue
+            dU = np.abs(g["U"][b] - oU[0]).max()
+            say(f"  b={b}: dU={dU:.2e} (max U {np.abs(oU[0]).max():.4g}, dU/tau {dU / tau:.1e})")
+            r = compare_restart(g, ot[0], oU[0], ogm[0], ogs[0], b, what)
+            say(f"  b={b}: L={g['terms'][b][0]:.6g} (oracle {ot[0][0]:.6g}) "
+                + " ".join(f"{k}={v:.2e}" for k, v in r.items()))
+    finally:
+        oracle.set_family("gaussian")
+
+
+@pytest.mark.parametrize("family", FAMS)
+@pytest.mark.parametrize("cfg", ["tiny", "small", "pipelined"])
+def test_family_loss_grad_random_state(family, cfg):
+    """Random means and widths from 0.3 to 8 steps: narrow and wide laws, mass
+    in the open end bins, heavy Cauchy tails across the whole horizon."""
+    p = make_problem(cfg, seed=1)
+    B = min(CONFIGS[cfg].B, 4)
+    mu, sg = random_state(p.n_ops, p.D, B, seed=3)
+    lam = np.random.default_rng(5).uniform(0.05, 1.0, size=(B, 3)).astype(np.float32)
+    hp = _hp(family, alpha=0.05, rho=1e-3)
+    say(f"[family] {family} {cfg} random: N={p.n_ops} D={p.D} II={p.II} B={B}")
+    _compare(p, mu, sg, lam, hp, family, f"{cfg}/{family}")
+
+
+@pytest.mark.parametrize("family", FAMS)
+@pytest.mark.parametrize("cfg", ["small", "medium"])
+def test_family_loss_grad_initial_state(family, cfg):
+    """The initial state of Alg. 1 (means inside [ASAP, ALAP], widths kappa
+    times the window), where the wide laws span most of the horizon."""
+    p = make_problem(cfg, seed=0)
+    B = min(CONFIGS[cfg].B, 4)
+    mu, sg = _init_state(cfg, p, B)
+    lam = np.full((B, 3), 0.2, np.float32)
+    hp = _hp(family, alpha=0.01, rho=1e-4)
+    say(f"[family] {family} {cfg} init: N={p.n_ops} D={p.D} B={B}")
+    _compare(p, mu, sg, lam, hp, family, f"{cfg}-init/{family}")
+
+
+@pytest.mark.parametrize("family", FAMS)
+def test_family_disables_polynomial_path(family):
+    p = make_problem("medium", seed=0)
+    ctx = bd.Context(p, 1, _hp(family))
+    try:
+        cfg = ctx.poly_config()
+    finally:
+        ctx.close()
+    assert not cfg["enabled"], cfg
+
+
+@pytest.mark.parametrize("family", ["gaussian"] + FAMS)
+@pytest.mark.parametrize("cfg", ["small", "pipelined"])
+def test_family_smooth_peak_usage(family, cfg):
+    """Random state: with the modulo fold the slot usages lie close together,
+    so the softmax weights are spread over many slots (the Gaussian runs on
+    the polynomial path here)."""
+    p = make_problem(cfg, seed=0)
+    B = min(CONFIGS[cfg].B, 4)
+    mu, sg = random_state(p.n_ops, p.D, B, seed=11)
+    lam = np.random.default_rng(2).uniform(0.05, 1.0, size=(B, 3)).astype(np.float32)
+    hp = _hp(family, alpha=0.01, rho=1e-3, beta=1.0, tau=0.1)
+    say(f"[family] {family} {cfg} smooth peak usage tau=0.1")
+    _compare(p, mu, sg, lam, hp, family, f"{cfg}-lse/{family}", beta=1.0, tau=0.1)
+
+
+@pytest.mark.parametrize("family", FAMS)
+@pytest.mark.parametrize("cfg", ["tiny", "small", "pipelined"])
+def test_family_storage(family, cfg):
+    p = with_storage(make_problem(cfg, seed=0), seed=4)
+    B = min(CONFIGS[cfg].B, 4)
+    mu, sg = random_state(p.n_ops, p.D, B, seed=13)
+    lam = np.random.default_rng(3).uniform(0.05, 1.0, size=(B, 3)).astype(np.float32)
+    hp = _hp(family, alpha=0.01, rho=1e-3, tau=1.0)
+    hp.gamma_mem = 1.0
+    say(f"[family] {family} {cfg} storage tau=1: N={p.n_ops} D={p.D} II={p.II}")
+    _compare(p, mu, sg, lam, hp, family, f"{cfg}-mem/{family}", tau=1.0, gamma=1.0)
+
+
+def test_family_large_full_size():
+    """Cauchy, the heaviest tails, on the 50k-op workload at full size
+    (B=8, D=4096) in bench.py's launch configuration."""
+    cfg = CONFIGS["large"]
+    p = make_problem(cfg, seed=0)
+    B = cfg.B
+    mu, sg = _init_state("large", p, B)
+    hp = bd.default_hparams()
+    hp.lr = cfg.lr
+    hp.family = bd.FAMILIES["cauchy"]
+    lam = np.full((B, 3), hp.lambda0, np.float32)
+    say(f"[family] cauchy large: N={p.n_ops} D={p.D} B={B}")
+    _compare(p, mu, sg, lam, hp, "cauchy", "large/cauchy")
