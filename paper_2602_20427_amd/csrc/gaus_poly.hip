@@ -13,10 +13,21 @@ namespace gaus {
 // step-by-step part, lanes = chunks for the polynomial part; per polynomial
 // out-edge the consumer-side derivatives of both parts are reduced together.
 // NP: strip passes of 64 lanes, ceil(SP / 64).
+//
+// Strip values are evaluated once per position and shared between lanes
+// through per-wave LDS rows: CDF values one step back (for the masses) and
+// Lat steps back (for the delay-shifted functions) are read from the lanes
+// that own those positions.  Position D-1 has the constant F = 1, so its lane
+// evaluates D-3 instead (the step before D-2, the first position of the upper
+// segment); the shifted values of the two upper positions and, for Lat = 0,
+// the value at L0 come from one more evaluation on four lanes.
+constexpr int kStripExtra = 8;   // row slots past SP: [SP] = D-3, [SP+1 .. SP+4] = helper values
+
 template <int NP>
 __global__ __launch_bounds__(64 * kPolyWaves) __attribute__((amdgpu_waves_per_eu(3)))
 void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__restrict__ sigma, Work W) {
-    // dynamic LDS: per wave 7 rows of SP strip values, then per wave SP strip usages
+    // dynamic LDS: per wave 7 rows of SP strip values and 3 rows of SP +
+    // kStripExtra raw CDF values, then per wave SP strip usages
     extern __shared__ float sDyn[];
     __shared__ float sUc[kPolyWaves][kMaxChunks][kNC];
     __shared__ float sGs[kPolyWaves][2];
@@ -37,8 +48,11 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
     float us[NP];
 #pragma unroll
     for (int ps = 0; ps < NP; ++ps) us[ps] = 0.0f;
-    float *own = sDyn + (size_t)wv * 7 * SP;
-    float *sUs = sDyn + (size_t)kPolyWaves * 7 * SP;
+    const int SPX = SP + kStripExtra;
+    float *own = sDyn + (size_t)wv * (7 * SP + 3 * SPX);
+    float *rSt = own + 7 * SP, *rFm = rSt + SPX, *rFs = rFm + SPX;
+    float *sUs = sDyn + (size_t)kPolyWaves * (7 * SP + 3 * SPX);
+    const int L0 = pa.L0;
 
     // the work-group's ops are q = q0 + sub + split*j; this wave's are
     // j = wv + kPolyWaves*l, parameters loaded by lane l
@@ -72,30 +86,59 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
         int x_j = 0, x_ok = 0;
         float x_mu = 0.0f, x_sg = 1.0f;
 
-        // (1) strip: own CDF values per position, kept in this wave's LDS rows
+        // (1) strip: own CDF values per position (raw rows), then the derived
+        // rows the out-edges read (F, dF, A = mass at u-s+1, dF(u-s), 1 - F(u-s))
 #pragma unroll
         for (int ps = 0; ps < NP; ++ps) {
             const int p = ps * 64 + lane;
             if (p < SP) {
-                const int u = p < pa.L0 ? p : D - 2 + (p - pa.L0);
-                float st, Fm, Fs, st0, Fm0, Fs0;
-                cdf_at(u, D, m_i, rs, cinv, st, Fm, Fs);
-                us[ps] += st_mass(st_at((long long)u - 1, D, m_i, rs), st);
-                cdf_at((long long)u - s, D, m_i, rs, cinv, st0, Fm0, Fs0);
-                const float st1 = st_at((long long)u - s + 1, D, m_i, rs);
+                const bool last = p == SP - 1;   // position D-1: evaluates D-3
+                const int u = p < L0 ? p : D - 2 + (p - L0);
+                float st, Fm, Fs;
+                cdf_at(last ? D - 3 : u, D, m_i, rs, cinv, st, Fm, Fs);
+                if (last) { rSt[SP] = st; st = -0.0f; Fm = 0.0f; Fs = 0.0f; }
+                rSt[p] = st; rFm[p] = Fm; rFs[p] = Fs;
+            }
+        }
+        if (lane < 4) {   // D-2-s, D-1-s, D-s (upper shifted positions) and L0
+            const int v = lane < 3 ? D - 2 - s + lane : L0;
+            float st, Fm, Fs;
+            cdf_at(v, D, m_i, rs, cinv, st, Fm, Fs);
+            rSt[SP + 1 + lane] = st; rFm[SP + 1 + lane] = Fm; rFs[SP + 1 + lane] = Fs;
+        }
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int ps = 0; ps < NP; ++ps) {
+            const int p = ps * 64 + lane;
+            if (p < SP) {
+                const float st = rSt[p];
+                const float stm1 = p == 0 ? 0.0f : rSt[p == L0 ? SP : p - 1];
+                us[ps] += st_mass(stm1, st);
+                // positions u-s and u-s+1: lanes p-s, p-s+1 below L0 (L0 itself
+                // from the helper slot), helper slots for the upper two
+                int i0, i1;
+                if (p < L0) { i0 = p - s; i1 = p - s + 1 == L0 ? SP + 4 : p - s + 1; }
+                else { i0 = SP + 1 + (p - L0); i1 = i0 + 1; }
+                const float st0 = i0 < 0 ? 0.0f : rSt[i0];
+                const float Fm0 = i0 < 0 ? 0.0f : rFm[i0];
+                const float Fs0 = i0 < 0 ? 0.0f : rFs[i0];
+                const float st1 = i1 < 0 ? 0.0f : rSt[i1];
                 own[0 * SP + p] = st_F(st);
-                own[1 * SP + p] = Fm;
-                own[2 * SP + p] = Fs;
+                own[1 * SP + p] = rFm[p];
+                own[2 * SP + p] = rFs[p];
                 own[3 * SP + p] = st_mass(st0, st1);
                 own[4 * SP + p] = Fm0;
                 own[5 * SP + p] = Fs0;
                 own[6 * SP + p] = st_1mF(st0);
             }
         }
+        __builtin_amdgcn_wave_barrier();
 
         // (2) chunk: producer vectors multiplied by the chunk moments
+        // (every lane: lanes past the last chunk compute finite values that the
+        // out-edges below and the usage readers never use)
         float HF[kNC], HFm[kNC], HFs[kNC], HA[kNC], HFm1[kNC], HFs1[kNC];
-        if (cact) {
+        {
             Expansion ea;
             expand(m_i, rs, tcen, ea);
             float v[kNC], w[kNC];
@@ -119,9 +162,6 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
             vec_moments(v, pa, HFm1);
             vec_times_z(v, ex.z0 - rs, ex.r, w);
             vec_moments(w, pa, HFs1);
-        } else {
-#pragma unroll
-            for (int k = 0; k < kNC; ++k) { HF[k] = HFm[k] = HFs[k] = HA[k] = HFm1[k] = HFs1[k] = 0.0f; }
         }
 
         // (3) polynomial out-edges
@@ -140,14 +180,27 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
             const float s_j = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x_sg), eb));
             const float rsj = 1.0f / s_j, cj = rsj * kInvSqrt2Pi;
             float cc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+            // the consumer's CDF per strip position (D-1's lane evaluates D-3)
+            float xst[NP], xFm[NP], xFs[NP];
 #pragma unroll
             for (int ps = 0; ps < NP; ++ps) {
                 const int p = ps * 64 + lane;
                 if (p < SP) {
-                    const int u = p < pa.L0 ? p : D - 2 + (p - pa.L0);
-                    float stj, Fmj, Fsj;
-                    cdf_at(u, D, m_j, rsj, cj, stj, Fmj, Fsj);
-                    const float Pj = st_mass(st_at((long long)u - 1, D, m_j, rsj), stj);
+                    const bool last = p == SP - 1;
+                    const int u = p < L0 ? p : D - 2 + (p - L0);
+                    cdf_at(last ? D - 3 : u, D, m_j, rsj, cj, xst[ps], xFm[ps], xFs[ps]);
+                    if (last) { rSt[SP] = xst[ps]; xst[ps] = -0.0f; xFm[ps] = 0.0f; xFs[ps] = 0.0f; }
+                    rSt[p] = xst[ps];
+                }
+            }
+            __builtin_amdgcn_wave_barrier();
+#pragma unroll
+            for (int ps = 0; ps < NP; ++ps) {
+                const int p = ps * 64 + lane;
+                if (p < SP) {
+                    const int u = p < L0 ? p : D - 2 + (p - L0);
+                    const float stj = xst[ps], Fmj = xFm[ps], Fsj = xFs[ps];
+                    const float Pj = st_mass(p == 0 ? 0.0f : rSt[p == L0 ? SP : p - 1], stj);
                     const float F = own[0 * SP + p], Fm = own[1 * SP + p];
                     const float Fs = own[2 * SP + p], A = own[3 * SP + p];
                     pr[2] = fmaf(-own[4 * SP + p], Pj, pr[2]);
@@ -349,7 +402,7 @@ __global__ __launch_bounds__(64 * kPolyWaves) void k_lse_poly(Graph G, PolyArgs 
 // ---------------------------------------------------------------------------
 hipError_t launch_poly(const Graph &g, const Work &w, const PolyArgs &pa, const float *mu, const float *sigma,
                        hipStream_t st) {
-    const size_t lds = sizeof(float) * (size_t)kPolyWaves * 8 * pa.SP;
+    const size_t lds = sizeof(float) * (size_t)kPolyWaves * (11 * pa.SP + 3 * kStripExtra);
     const dim3 grid(g.ngroups * pa.split, g.B), block(64 * kPolyWaves);
     switch ((pa.SP + 63) / 64) {
     case 1: hipLaunchKernelGGL(k_poly<1>, grid, block, lds, st, g, pa, mu, sigma, w); break;
