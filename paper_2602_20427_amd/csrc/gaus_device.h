@@ -142,6 +142,20 @@ __device__ __forceinline__ void cdf_at(long long v, int D, float mu, float rs, f
     Fs = Fm * z;
 }
 
+// the same for 32-bit positions (no 64-bit integer conversion)
+template <int FAM = 0>
+__device__ __forceinline__ void cdf_at(int v, int D, float mu, float rs, float cinv, float &st, float &Fm,
+                                       float &Fs) {
+    if (v < 0) { st = 0.0f; Fm = 0.0f; Fs = 0.0f; return; }
+    if (v >= D - 1) { st = -0.0f; Fm = 0.0f; Fs = 0.0f; return; }
+    const float z = ((float)v + 0.5f - mu) * rs;
+    float tail, g;
+    fam_tail_h<FAM>(z, tail, g);
+    st = (z >= 0.0f) ? -tail : tail;
+    Fm = -g * cinv;
+    Fs = Fm * z;
+}
+
 template <int FAM = 0>
 __device__ __forceinline__ float st_at(long long v, int D, float mu, float rs) {
     if (v < 0) return 0.0f;

@@ -22,11 +22,12 @@ namespace gaus {
 // segment); the shifted values of the two upper positions and, for Lat = 0,
 // the value at L0 come from one more evaluation on four lanes.
 constexpr int kStripExtra = 8;   // row slots past SP: [SP] = D-3, [SP+1 .. SP+4] = helper values
+constexpr int kStripPad = kSmax; // zero slots before position 0 (positions -kSmax .. -1, F = 0)
 
 template <int NP>
 __global__ __launch_bounds__(64 * kPolyWaves) __attribute__((amdgpu_waves_per_eu(3)))
 void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__restrict__ sigma, Work W) {
-    // dynamic LDS: per wave 7 rows of SP strip values and 3 rows of SP +
+    // dynamic LDS: per wave 6 rows of SP strip values and 3 rows of SP +
     // kStripExtra raw CDF values, then per wave SP strip usages
     extern __shared__ float sDyn[];
     __shared__ float sUc[kPolyWaves][kMaxChunks][kNC];
@@ -48,11 +49,14 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
     float us[NP];
 #pragma unroll
     for (int ps = 0; ps < NP; ++ps) us[ps] = 0.0f;
-    const int SPX = SP + kStripExtra;
-    float *own = sDyn + (size_t)wv * (7 * SP + 3 * SPX);
-    float *rSt = own + 7 * SP, *rFm = rSt + SPX, *rFs = rFm + SPX;
-    float *sUs = sDyn + (size_t)kPolyWaves * (7 * SP + 3 * SPX);
+    const int SPX = kStripPad + SP + kStripExtra;
+    float *own = sDyn + (size_t)wv * (6 * SP + 3 * SPX);
+    float *rSt = own + 6 * SP + kStripPad, *rFm = rSt + SPX, *rFs = rFm + SPX;
+    float *sUs = sDyn + (size_t)kPolyWaves * (6 * SP + 3 * SPX);
     const int L0 = pa.L0;
+    if (lane < kStripPad) {   // never overwritten: positions before 0 have F = 0, dF = 0
+        rSt[lane - kStripPad] = 0.0f; rFm[lane - kStripPad] = 0.0f; rFs[lane - kStripPad] = 0.0f;
+    }
 
     // the work-group's ops are q = q0 + sub + split*j; this wave's are
     // j = wv + kPolyWaves*l, parameters loaded by lane l
@@ -60,11 +64,11 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
     const int nj = (q1 - q0 - sub + split - 1) / split;
     const int nq = (nj - wv + kPolyWaves - 1) / kPolyWaves;
     int l_i = 0, l_cls = 0, l_s = 0, l_e0 = 0, l_e1 = 0;
-    float l_mu = 0.0f, l_sg = 1.0f;
+    float l_mu = 0.0f, l_sg = 1.0f;   // l_sg holds 1/sigma (divided once, on the loading lane)
     if (lane < nq) {
         l_i = G.perm[q0 + sub + split * (wv + kPolyWaves * lane)];
         l_cls = clsb[l_i];
-        l_mu = mub[l_i]; l_sg = sgb[l_i];
+        l_mu = mub[l_i]; l_sg = 1.0f / sgb[l_i];
         l_s = G.delay[l_i];
         l_e0 = G.row_ptr[l_i]; l_e1 = G.row_ptr[l_i + 1];
     }
@@ -77,17 +81,18 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
             continue;
         }
         const float m_i = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, l_mu), oq));
-        const float s_i = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, l_sg), oq));
-        const float rs = 1.0f / s_i, cinv = rs * kInvSqrt2Pi;
+        const float rs = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, l_sg), oq));
+        const float cinv = rs * kInvSqrt2Pi;
         const int s = __builtin_amdgcn_readlane(l_s, oq);
         const int e0 = __builtin_amdgcn_readlane(l_e0, oq), e1 = __builtin_amdgcn_readlane(l_e1, oq);
         float pr[kPP] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
         // the op's polynomial out-edges, loaded by lane (batches of 64)
         int x_j = 0, x_ok = 0;
-        float x_mu = 0.0f, x_sg = 1.0f;
+        float x_mu = 0.0f, x_sg = 1.0f;   // x_sg: 1/sigma of the consumer
 
         // (1) strip: own CDF values per position (raw rows), then the derived
-        // rows the out-edges read (F, dF, A = mass at u-s+1, dF(u-s), 1 - F(u-s))
+        // rows the out-edges read: F, dF(u), A(u) = mass at u-s+1 (at u = D-1
+        // instead 1 - F(u-s), the weight of the consumers' open last bin), dF(u-s)
 #pragma unroll
         for (int ps = 0; ps < NP; ++ps) {
             const int p = ps * 64 + lane;
@@ -112,24 +117,21 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
             const int p = ps * 64 + lane;
             if (p < SP) {
                 const float st = rSt[p];
-                const float stm1 = p == 0 ? 0.0f : rSt[p == L0 ? SP : p - 1];
+                const float stm1 = rSt[p == L0 ? SP : p - 1];
                 us[ps] += st_mass(stm1, st);
-                // positions u-s and u-s+1: lanes p-s, p-s+1 below L0 (L0 itself
-                // from the helper slot), helper slots for the upper two
+                // positions u-s and u-s+1: lanes p-s, p-s+1 below L0 (negative
+                // ones in the zero pad, L0 itself from the helper slot), helper
+                // slots for the upper two
                 int i0, i1;
                 if (p < L0) { i0 = p - s; i1 = p - s + 1 == L0 ? SP + 4 : p - s + 1; }
                 else { i0 = SP + 1 + (p - L0); i1 = i0 + 1; }
-                const float st0 = i0 < 0 ? 0.0f : rSt[i0];
-                const float Fm0 = i0 < 0 ? 0.0f : rFm[i0];
-                const float Fs0 = i0 < 0 ? 0.0f : rFs[i0];
-                const float st1 = i1 < 0 ? 0.0f : rSt[i1];
+                const float st0 = rSt[i0], Fm0 = rFm[i0], Fs0 = rFs[i0], st1 = rSt[i1];
                 own[0 * SP + p] = st_F(st);
                 own[1 * SP + p] = rFm[p];
                 own[2 * SP + p] = rFs[p];
-                own[3 * SP + p] = st_mass(st0, st1);
+                own[3 * SP + p] = p == SP - 1 ? st_1mF(st0) : st_mass(st0, st1);
                 own[4 * SP + p] = Fm0;
                 own[5 * SP + p] = Fs0;
-                own[6 * SP + p] = st_1mF(st0);
             }
         }
         __builtin_amdgcn_wave_barrier();
@@ -172,13 +174,13 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
                 if (e + lane < e1) {
                     x_j = G.col[e + lane];
                     x_ok = clsb[x_j];
-                    x_mu = mub[x_j]; x_sg = sgb[x_j];
+                    x_mu = mub[x_j]; x_sg = 1.0f / sgb[x_j];
                 }
             }
             if (!__builtin_amdgcn_readlane(x_ok, eb)) continue;  // step-by-step edge, done by k_ops
             const float m_j = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x_mu), eb));
-            const float s_j = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x_sg), eb));
-            const float rsj = 1.0f / s_j, cj = rsj * kInvSqrt2Pi;
+            const float rsj = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x_sg), eb));
+            const float cj = rsj * kInvSqrt2Pi;
             float cc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
             // the consumer's CDF per strip position (D-1's lane evaluates D-3)
             float xst[NP], xFm[NP], xFs[NP];
@@ -198,26 +200,23 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
             for (int ps = 0; ps < NP; ++ps) {
                 const int p = ps * 64 + lane;
                 if (p < SP) {
-                    const int u = p < L0 ? p : D - 2 + (p - L0);
+                    // at u = D-1 the consumer's F = 1 and dF = 0: only
+                    // pr[0] += 1 - F_i(D-1-s) remains, the rest adds zeros
                     const float stj = xst[ps], Fmj = xFm[ps], Fsj = xFs[ps];
-                    const float Pj = st_mass(p == 0 ? 0.0f : rSt[p == L0 ? SP : p - 1], stj);
+                    const float Pj = st_mass(rSt[p == L0 ? SP : p - 1], stj);
                     const float F = own[0 * SP + p], Fm = own[1 * SP + p];
                     const float Fs = own[2 * SP + p], A = own[3 * SP + p];
                     pr[2] = fmaf(-own[4 * SP + p], Pj, pr[2]);
                     pr[3] = fmaf(-own[5 * SP + p], Pj, pr[3]);
-                    if (u < D - 1) {
-                        const float omF = st_1mF(stj);
-                        pr[0] = fmaf(A, st_F(stj), pr[0]);
-                        pr[1] = fmaf(F, omF, pr[1]);
-                        pr[4] = fmaf(Fm, omF, pr[4]);
-                        pr[5] = fmaf(Fs, omF, pr[5]);
-                        cc[0] = fmaf(A, Fmj, cc[0]);
-                        cc[1] = fmaf(A, Fsj, cc[1]);
-                        cc[2] = fmaf(-F, Fmj, cc[2]);
-                        cc[3] = fmaf(-F, Fsj, cc[3]);
-                    } else {
-                        pr[0] += own[6 * SP + p];
-                    }
+                    const float omF = st_1mF(stj);
+                    pr[0] = fmaf(A, st_F(stj), pr[0]);
+                    pr[1] = fmaf(F, omF, pr[1]);
+                    pr[4] = fmaf(Fm, omF, pr[4]);
+                    pr[5] = fmaf(Fs, omF, pr[5]);
+                    cc[0] = fmaf(A, Fmj, cc[0]);
+                    cc[1] = fmaf(A, Fsj, cc[1]);
+                    cc[2] = fmaf(-F, Fmj, cc[2]);
+                    cc[3] = fmaf(-F, Fsj, cc[3]);
                 }
             }
             if (cact) {
@@ -402,7 +401,7 @@ __global__ __launch_bounds__(64 * kPolyWaves) void k_lse_poly(Graph G, PolyArgs 
 // ---------------------------------------------------------------------------
 hipError_t launch_poly(const Graph &g, const Work &w, const PolyArgs &pa, const float *mu, const float *sigma,
                        hipStream_t st) {
-    const size_t lds = sizeof(float) * (size_t)kPolyWaves * (11 * pa.SP + 3 * kStripExtra);
+    const size_t lds = sizeof(float) * (size_t)kPolyWaves * (10 * pa.SP + 3 * (kStripPad + kStripExtra));
     const dim3 grid(g.ngroups * pa.split, g.B), block(64 * kPolyWaves);
     switch ((pa.SP + 63) / 64) {
     case 1: hipLaunchKernelGGL(k_poly<1>, grid, block, lds, st, g, pa, mu, sigma, w); break;
