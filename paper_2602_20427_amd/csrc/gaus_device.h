@@ -259,9 +259,13 @@ __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirs
 
 
 
+// Expansion of an op's CDF around a chunk centre, NC coefficients per vector
+// (degree NC-1): T[n] = Phi^(n)(z0) r^n / n!, n < NC + kShiftTerms + 1, the
+// terms the one-step shift series reach.
+template <int NC = kNC>
 struct Expansion {
-    float T[kTN];   // Taylor coefficients in y, T[0] = F(z0)
-    float G0;       // 1 - F(z0), from the tail
+    float T[NC + kShiftTerms + 1];   // Taylor coefficients in y, T[0] = F(z0)
+    float G0;                        // 1 - F(z0), from the tail
     float z0, r;
 };
 
@@ -277,7 +281,9 @@ constexpr float back_coef(int k, int j) {
     return (float)(-(double)(k + j + 1) * binom_d(k + j, j) * ((j & 1) ? -1.0 : 1.0));
 }
 
-__device__ __forceinline__ void expand(float mu, float rs, float tcen, Expansion &e) {
+template <int NC>
+__device__ __forceinline__ void expand(float mu, float rs, float tcen, Expansion<NC> &e) {
+    constexpr int TN = NC + kShiftTerms + 1;
     e.r = rs;
     e.z0 = (tcen + 0.5f - mu) * rs;
     float tail, g;
@@ -289,27 +295,30 @@ __device__ __forceinline__ void expand(float mu, float rs, float tcen, Expansion
     const float zr = e.z0 * rs, r2 = rs * rs;
     e.T[2] = (zr * -0.5f) * e.T[1];
 #pragma unroll
-    for (int n = 2; n < kTN - 1; ++n) {
+    for (int n = 2; n < TN - 1; ++n) {
         const float c1 = -1.0f / (float)(n + 1);
         const float c2 = -(float)(n - 1) / (float)(n * (n + 1));
         e.T[n + 1] = fmaf(zr * c1, e.T[n], (r2 * c2) * e.T[n - 1]);
     }
 }
 
-__device__ __forceinline__ void vec_dFdmu(const Expansion &e, float (&a)[kNC]) {
+template <int NC>
+__device__ __forceinline__ void vec_dFdmu(const Expansion<NC> &e, float (&a)[NC]) {
 #pragma unroll
-    for (int k = 0; k < kNC; ++k) a[k] = -(float)(k + 1) * e.T[k + 1];
+    for (int k = 0; k < NC; ++k) a[k] = -(float)(k + 1) * e.T[k + 1];
 }
 
-__device__ __forceinline__ void vec_times_z(const float (&a)[kNC], float zc, float r, float (&o)[kNC]) {
+template <int NC>
+__device__ __forceinline__ void vec_times_z(const float (&a)[NC], float zc, float r, float (&o)[NC]) {
     o[0] = zc * a[0];
 #pragma unroll
-    for (int k = 1; k < kNC; ++k) o[k] = fmaf(zc, a[k], r * a[k - 1]);
+    for (int k = 1; k < NC; ++k) o[k] = fmaf(zc, a[k], r * a[k - 1]);
 }
 
-__device__ __forceinline__ void vec_mass(const Expansion &e, float (&m)[kNC]) {
+template <int NC>
+__device__ __forceinline__ void vec_mass(const Expansion<NC> &e, float (&m)[NC]) {
 #pragma unroll
-    for (int k = 0; k < kNC; ++k) {
+    for (int k = 0; k < NC; ++k) {
         float acc = 0.0f;
 #pragma unroll
         for (int j = kShiftTerms; j >= 1; --j) acc = fmaf(mass_coef(k, j), e.T[k + j], acc);
@@ -317,9 +326,10 @@ __device__ __forceinline__ void vec_mass(const Expansion &e, float (&m)[kNC]) {
     }
 }
 
-__device__ __forceinline__ void vec_dFdmu_back(const Expansion &e, float (&a)[kNC]) {
+template <int NC>
+__device__ __forceinline__ void vec_dFdmu_back(const Expansion<NC> &e, float (&a)[NC]) {
 #pragma unroll
-    for (int k = 0; k < kNC; ++k) {
+    for (int k = 0; k < NC; ++k) {
         float acc = 0.0f;
 #pragma unroll
         for (int j = kShiftTerms; j >= 0; --j) acc = fmaf(back_coef(k, j), e.T[k + 1 + j], acc);
@@ -328,36 +338,40 @@ __device__ __forceinline__ void vec_dFdmu_back(const Expansion &e, float (&a)[kN
 }
 
 // (H p)_k = sum_l H_{k+l} p_l; the chunk points are symmetric, odd moments vanish
-__device__ __forceinline__ void vec_moments(const float (&p)[kNC], const PolyArgs &pa, float (&o)[kNC]) {
+template <int NC>
+__device__ __forceinline__ void vec_moments(const float (&p)[NC], const PolyArgs &pa, float (&o)[NC]) {
 #pragma unroll
-    for (int k = 0; k < kNC; ++k) {
+    for (int k = 0; k < NC; ++k) {
         float acc = 0.0f;
 #pragma unroll
-        for (int l = 0; l < kNC; ++l)
+        for (int l = 0; l < NC; ++l)
             if (((k + l) & 1) == 0) acc = fmaf(pa.H[(k + l) / 2], p[l], acc);
         o[k] = acc;
     }
 }
 
-__device__ __forceinline__ float vdot(const float (&a)[kNC], const float (&b)[kNC]) {
+template <int NC>
+__device__ __forceinline__ float vdot(const float (&a)[NC], const float (&b)[NC]) {
     float acc = 0.0f;
 #pragma unroll
-    for (int k = 0; k < kNC; ++k) acc = fmaf(a[k], b[k], acc);
+    for (int k = 0; k < NC; ++k) acc = fmaf(a[k], b[k], acc);
     return acc;
 }
 
 // dot with 1 - F given F's coefficients and the precise 1 - F(z0)
-__device__ __forceinline__ float vdot_1mF(const float (&a)[kNC], const Expansion &e) {
+template <int NC>
+__device__ __forceinline__ float vdot_1mF(const float (&a)[NC], const Expansion<NC> &e) {
     float acc = a[0] * e.G0;
 #pragma unroll
-    for (int k = 1; k < kNC; ++k) acc = fmaf(-a[k], e.T[k], acc);
+    for (int k = 1; k < NC; ++k) acc = fmaf(-a[k], e.T[k], acc);
     return acc;
 }
 
-__device__ __forceinline__ float vdot_F(const float (&a)[kNC], const Expansion &e) {
+template <int NC>
+__device__ __forceinline__ float vdot_F(const float (&a)[NC], const Expansion<NC> &e) {
     float acc = 0.0f;
 #pragma unroll
-    for (int k = 0; k < kNC; ++k) acc = fmaf(a[k], e.T[k], acc);
+    for (int k = 0; k < NC; ++k) acc = fmaf(a[k], e.T[k], acc);
     return acc;
 }
 

@@ -113,7 +113,17 @@ void setup_poly(int D, int requested, PolyArgs &pa) {
     pa.SP = pa.L0 + 2;
     const double lam = (W - 1) / 2.0;
     pa.lam = (float)lam;
-    pa.sig_thr = (float)(lam / kRhoMax);
+    // Tier bounds: the truncated series of dF has relative error at most
+    // about rho^d / sqrt(d!) (Taylor remainder with Cramer's bound on the
+    // Hermite functions); each tier's rho bound matches the degree-8 error at
+    // rho = kRhoMax: rho_d = (kRhoMax^8 sqrt(d!) / sqrt(8!))^(1/d).
+    auto fact = [](int n) { double f = 1.0; for (int q = 2; q <= n; ++q) f *= q; return f; };
+    for (int t = 1; t <= kTiers; ++t) {
+        const int d = kTierDeg[t];
+        const double rho = std::pow(std::pow((double)kRhoMax, kDeg) * std::sqrt(fact(d) / fact(kDeg)), 1.0 / d);
+        pa.sig_thr[t] = (float)(lam / rho);
+    }
+    pa.sig_thr[0] = pa.sig_thr[1];
     for (int k = 0; k <= kDeg; ++k) {
         double acc = 0.0;
         for (int i = 0; i < W; ++i) acc += std::pow(i - lam, 2 * k);
@@ -474,6 +484,7 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     AL(adamf, (size_t)B * 2);
     AL(cls, BN);
     AL(dflag, BN);
+    AL(ptier, BN);
     AL(gflag, (size_t)B * g.ngroups);
     AL(gsum_ops, (size_t)B * g.ngroups * ntiles * 2);
     AL(gsum_poly, (size_t)B * g.ngroups * c->pa.split * 2);

@@ -23,7 +23,11 @@ constexpr int kTerms = 7;   // per restart: L, V_dep, V_res, V_rec, L_com, L_res
 // Chunk-polynomial path (dense regime).  On a chunk of W consecutive steps
 // with rho = ((W-1)/2)/sigma <= kRhoMax the CDF row of an op is a degree-kDeg
 // polynomial in the step offset to ~1e-10; sums over steps become dot products.
-constexpr int kDeg = 8;                       // polynomial degree
+// Wider ops need fewer terms for the same accuracy: tier t uses degree
+// kTierDeg[t] when rho is at most the tier's bound (set on the host).
+constexpr int kDeg = 8;                       // polynomial degree (tier 1, the largest)
+constexpr int kTiers = 3;
+constexpr int kTierDeg[kTiers + 1] = {0, 8, 6, 5};
 constexpr int kNC = kDeg + 1;                 // coefficients per vector
 constexpr int kShiftTerms = 4;                // terms of the one-step shift series
 constexpr int kTN = kDeg + kShiftTerms + 2;   // scaled derivatives T_0 .. T_{kTN-1}
@@ -37,7 +41,8 @@ struct PolyArgs {
     int W, nc, L0;        // chunk width, chunks, left strip [0, L0); chunks cover [L0, D-2)
     int SP;               // strip positions: [0, L0) and {D-2, D-1}
     int split;            // work-groups per op group in the polynomial kernel
-    float lam, sig_thr;   // chunk half-width (W-1)/2; ops with sigma >= sig_thr are polynomial
+    float lam;            // chunk half-width (W-1)/2
+    float sig_thr[kTiers + 1];   // sigma >= sig_thr[t]: tier t (decreasing degree); [1] = path threshold
     float H[kDeg + 1];    // even moments: H[k] = sum over a chunk's points y of y^(2k)
 };
 
@@ -105,6 +110,8 @@ struct Work {
     float *adamf;     // [B][2]            Adam bias corrections 1-beta1^t, 1-beta2^t
     unsigned char *cls;  // [B][N]          1 = op on the chunk-polynomial path this iteration
     unsigned char *dflag;  // [B][N]        1 = op has step-by-step work (own terms or out-edges)
+    unsigned char *ptier;  // [B][N]        polynomial op: tier of its vectors, the smallest over
+                           //               itself and its polynomial consumers (highest degree)
     int *gflag;       // [B][ngroups]      1 = some op of the group has step-by-step work
     float *gsum_ops;  // [B][ngroups][ntiles][2]  V_dep, L_com of a k_ops work-group
     float *gsum_poly; // [B][ngroups*split][2]  V_dep, L_com of a k_poly work-group

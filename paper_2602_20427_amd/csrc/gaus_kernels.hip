@@ -50,7 +50,10 @@ __global__ void k_classify(Graph G, PolyArgs pa, const float *__restrict__ sigma
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= G.N) return;
     const float s = sigma[(size_t)b * G.N + i];
-    W.cls[(size_t)b * G.N + i] = (pa.enabled && s >= pa.sig_thr && G.delay[i] <= kSmax) ? 1 : 0;
+    int t = 0;   // 0 = step by step, else the polynomial tier (wider sigma: higher tier, lower degree)
+    if (pa.enabled && G.delay[i] <= kSmax)
+        for (int q = 1; q <= kTiers; ++q) t = s >= pa.sig_thr[q] ? q : t;
+    W.cls[(size_t)b * G.N + i] = (unsigned char)t;
 }
 
 // Which ops (and groups) have step-by-step work this iteration: ops off the
@@ -63,9 +66,16 @@ __global__ __launch_bounds__(256) void k_flags(Graph G, Work W) {
     int d = 0;
     if (q0 + tid < q1) {
         const int i = G.perm[q0 + tid];
-        d = clsb[i] ? 0 : 1;
-        for (int e = G.row_ptr[i]; e < G.row_ptr[i + 1] && !d; ++e) d = clsb[G.col[e]] ? 0 : 1;
+        const int ci = clsb[i];
+        d = ci ? 0 : 1;
+        int t = ci;   // a polynomial producer's vectors: the highest degree its edges need
+        for (int e = G.row_ptr[i]; e < G.row_ptr[i + 1]; ++e) {
+            const int cj = clsb[G.col[e]];
+            d |= cj ? 0 : 1;
+            t = cj ? min(t, cj) : t;
+        }
         W.dflag[(size_t)b * G.N + i] = (unsigned char)d;
+        W.ptier[(size_t)b * G.N + i] = (unsigned char)t;
     }
     d = __syncthreads_or(d);
     if (tid == 0) W.gflag[(size_t)b * G.ngroups + grp] = d ? 1 : 0;

@@ -3,6 +3,8 @@
 // width allows it) and k_lse_mom / k_lse_poly (gradient of the smooth peak
 // usage for those ops).  The method is described at k_classify in
 // gaus_kernels.hip.
+#include <type_traits>
+
 #include "gaus_device.h"
 
 namespace gaus {
@@ -67,19 +69,25 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
     float l_mu = 0.0f, l_sg = 1.0f;   // l_sg holds 1/sigma (divided once, on the loading lane)
     if (lane < nq) {
         l_i = G.perm[q0 + sub + split * (wv + kPolyWaves * lane)];
-        l_cls = clsb[l_i];
+        l_cls = W.ptier[(size_t)b * N + l_i];   // 0: step by step, else the degree tier
         l_mu = mub[l_i]; l_sg = 1.0f / sgb[l_i];
         l_s = G.delay[l_i];
         l_e0 = G.row_ptr[l_i]; l_e1 = G.row_ptr[l_i + 1];
     }
     float gsum = 0.0f;  // V_dep, L_com of this wave's ops (lanes 0 and 2)
+    // step-by-step ops: no polynomial records
     for (int oq = 0; oq < nq; ++oq) {
+        if (__builtin_amdgcn_readlane(l_cls, oq)) continue;
+        const int i = __builtin_amdgcn_readlane(l_i, oq);
+        if (lane < kPP) W.ppoly[((size_t)b * N + i) * kPP + lane] = 0.0f;
+    }
+    // polynomial ops, one pass per degree tier (NC coefficients per vector)
+    auto tier_pass = [&](auto nc_tag, int tier) {
+    constexpr int NC = decltype(nc_tag)::value;
+    for (int oq = 0; oq < nq; ++oq) {
+        if (__builtin_amdgcn_readlane(l_cls, oq) != tier) continue;
         const int i = __builtin_amdgcn_readlane(l_i, oq);
         float *pp = W.ppoly + ((size_t)b * N + i) * kPP;
-        if (!__builtin_amdgcn_readlane(l_cls, oq)) {
-            if (lane < kPP) pp[lane] = 0.0f;
-            continue;
-        }
         const float m_i = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, l_mu), oq));
         const float rs = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, l_sg), oq));
         const float cinv = rs * kInvSqrt2Pi;
@@ -139,25 +147,25 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
         // (2) chunk: producer vectors multiplied by the chunk moments
         // (every lane: lanes past the last chunk compute finite values that the
         // out-edges below and the usage readers never use)
-        float HF[kNC], HFm[kNC], HFs[kNC], HA[kNC], HFm1[kNC], HFs1[kNC];
+        float HF[NC], HFm[NC], HFs[NC], HA[NC], HFm1[NC], HFs1[NC];
         {
-            Expansion ea;
+            Expansion<NC> ea;
             expand(m_i, rs, tcen, ea);
-            float v[kNC], w[kNC];
+            float v[NC], w[NC];
             vec_mass(ea, v);
 #pragma unroll
-            for (int k = 0; k < kNC; ++k) uc[k] += v[k];
+            for (int k = 0; k < NC; ++k) uc[k] += v[k];
 #pragma unroll
-            for (int k = 0; k < kNC; ++k) w[k] = ea.T[k];
+            for (int k = 0; k < NC; ++k) w[k] = ea.T[k];
             vec_moments(w, pa, HF);
             vec_dFdmu(ea, v);
             vec_moments(v, pa, HFm);
             vec_times_z(v, ea.z0, ea.r, w);
             vec_moments(w, pa, HFs);
             // shifted functions: A(u) = mass at u-s+1, dF(u-s)
-            Expansion es;
+            Expansion<NC> es;
             if (s != 1) expand(m_i, rs, tcen - (float)(s - 1), es);
-            const Expansion &ex = (s != 1) ? es : ea;
+            const Expansion<NC> &ex = (s != 1) ? es : ea;
             vec_mass(ex, v);
             vec_moments(v, pa, HA);
             vec_dFdmu_back(ex, v);
@@ -220,9 +228,9 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
                 }
             }
             if (cact) {
-                Expansion ej;
+                Expansion<NC> ej;
                 expand(m_j, rsj, tcen, ej);
-                float a[kNC], v[kNC];
+                float a[NC], v[NC];
                 pr[0] += vdot_F(HA, ej);
                 pr[1] += vdot_1mF(HF, ej);
                 pr[4] += vdot_1mF(HFm, ej);
@@ -246,6 +254,10 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
         if (lane < 2) pp[4 + lane] = pt2;
         gsum += pt4;   // lane 0: V_dep, lane 2: L_com
     }
+    };
+    tier_pass(std::integral_constant<int, kTierDeg[1] + 1>{}, 1);
+    tier_pass(std::integral_constant<int, kTierDeg[2] + 1>{}, 2);
+    tier_pass(std::integral_constant<int, kTierDeg[3] + 1>{}, 3);
     if (lane == 0) sGs[wv][0] = gsum;
     if (lane == 2) sGs[wv][1] = gsum;
 
@@ -383,7 +395,7 @@ __global__ __launch_bounds__(64 * kPolyWaves) void k_lse_poly(Graph G, PolyArgs 
             }
         }
         if (cact) {
-            Expansion e;
+            Expansion<> e;
             expand(m_i, rs, tcen, e);
             float a[kNC], v[kNC];
             vec_dFdmu(e, a);

@@ -1,5 +1,7 @@
 """Parity of the gfx950 HIP path (through the C ABI) with the fp64 CPU oracle
 on identical seeded inputs."""
+import math
+
 import numpy as np
 import pytest
 
@@ -177,6 +179,33 @@ def test_polynomial_path_chunk_widths(W):
     mu = rng.uniform(-200, p.D + 200, size=(B, p.n_ops)).astype(np.float32)
     sg = rng.uniform(2.0 * W, 1500.0, size=(B, p.n_ops)).astype(np.float32)
     _check(p, mu, sg, _lam(B, 42), hparams(alpha=0.2, rho=0.01, poly_chunk=W), range(B), f"chunk W={W}")
+
+
+def test_polynomial_degree_tiers():
+    """Wide ops take fewer series terms: degree 8 for rho = ((W-1)/2)/sigma up to
+    1/4, degree 6 and degree 5 above the sigmas where their truncation error
+    matches degree 8's at rho = 1/4.  Sigmas straddle every boundary, so edges
+    join ops of different degrees (the producer's vectors then take the
+    higher degree) and ops of both paths."""
+    p = _ragged_problem(77, N=1500, D=3000, big_delay=False)
+    p.delay[:] = np.random.default_rng(78).integers(0, 9, size=p.n_ops).astype(np.int32)
+    ctx = bd.Context(p, 1, hparams())
+    W = ctx.poly_config()["W"]
+    ctx.close()
+    lam_w = (W - 1) / 2.0
+    f = math.factorial
+    thr = {d: lam_w / (0.25 ** 8 * math.sqrt(f(d) / f(8))) ** (1.0 / d) for d in (8, 6, 5)}
+    B = 2
+    rng = np.random.default_rng(79)
+    centres = np.array([thr[8], thr[8], thr[6], thr[6], thr[5], thr[5], 3 * thr[5]])
+    pick = rng.integers(0, len(centres), size=(B, p.n_ops))
+    sg = (centres[pick] * rng.uniform(0.97, 1.03, size=(B, p.n_ops))).astype(np.float32)
+    mu = rng.uniform(-100, p.D + 100, size=(B, p.n_ops)).astype(np.float32)
+    for d, lo, hi in ((8, thr[8], thr[6]), (6, thr[6], thr[5]), (5, thr[5], np.inf)):
+        share = np.mean((sg >= lo) & (sg < hi))
+        say(f"  W={W}: degree {d} for sigma in [{lo:.1f}, {hi:.1f}): {share:.2f} of the ops")
+        assert share > 0.1
+    _check(p, mu, sg, _lam(B, 80), hparams(alpha=0.2, rho=0.01), range(B), "degree tiers")
 
 
 def test_small_edge_cases():
