@@ -123,27 +123,32 @@ def describe(cfg, prob):
             f"{cfg.name}: random layered DAG, {prob.n_ops} ops, D={prob.D}, B={cfg.B}, mu~U[0,D), sigma={cfg.sigma0}")
 
 
-def cpu_baseline(prob, mu, sigma, lam, hp, n_restarts):
-    """The oracle as it stands, on n_restarts of the workload: one fused
-    iteration (loss, gradient, Adam) each from the same state."""
+def cpu_baseline(prob, mu, sigma, lam, hp, min_seconds):
+    """The oracle as it stands: one fused iteration (loss, gradient, Adam) per
+    restart of the workload, cycling through the restarts from the same state
+    until at least min_seconds have passed (and at least one restart)."""
     import numpy as np
     import oracle
     oracle.build(force=False)
     oracle.set_family(hp.family)
+    B = mu.shape[0]
+    done = 0
     t0 = time.perf_counter()
-    for b in range(n_restarts):
+    while done == 0 or time.perf_counter() - t0 < min_seconds:
+        b = done % B
         _, _, gm, gs, _ = oracle.loss_grad(prob, mu[b:b + 1].astype(np.float64), sigma[b:b + 1].astype(np.float64),
                                            lam[b:b + 1].astype(np.float64), hp.alpha_com, hp.rho,
                                            beta=hp.beta_res, tau=hp.tau, gamma=hp.gamma_mem)
         z = np.zeros(prob.n_ops)
         oracle.adam(mu[b].astype(np.float64), z, z, gm[0], 1, hp.lr)
         oracle.adam(sigma[b].astype(np.float64), z, z, gs[0], 1, hp.lr)
+        done += 1
     dt = time.perf_counter() - t0
     oracle.set_family("gaussian")
-    return {"value": n_restarts * prob.n_ops * prob.D / dt, "unit": "op-step evals/s",
+    return {"value": done * prob.n_ops * prob.D / dt, "unit": "op-step evals/s",
             "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": f"{n_restarts} of {mu.shape[0]} restarts of the same workload and state, one fused "
-                      f"iteration (loss, gradient, Adam) each, fp64 C oracle with OpenMP; {dt:.2f} s"}
+            "sample": f"{done} restart-iterations (cycling over the {B} restarts of the same workload and state), "
+                      f"one fused iteration (loss, gradient, Adam) each, fp64 C oracle with OpenMP; {dt:.2f} s"}
 
 
 def main():
@@ -152,7 +157,8 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="large")
-    ap.add_argument("--cpu-restarts", type=int, default=2, help="restarts in the CPU-oracle sample")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="minimum CPU time of the oracle sample (whole restart-iterations)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--poly-chunk", type=int, default=0,
                     help="chunk width of the polynomial path: 0 = library's choice, -1 = off (every op step by step)")
@@ -317,8 +323,8 @@ def main():
         "iteration_model_tflops_per_s": whole / (step_ms_events * 1e-3) / 1e12,
     }
     if not args.no_cpu_baseline:
-        log(f"[bench] CPU oracle on {args.cpu_restarts} restarts")
-        out["cpu_baseline"] = cpu_baseline(prob, mu0, sg0, lam0, hp, min(args.cpu_restarts, B))
+        log(f"[bench] CPU oracle for at least {args.cpu_seconds:g} s")
+        out["cpu_baseline"] = cpu_baseline(prob, mu0, sg0, lam0, hp, args.cpu_seconds)
     if args.copy_probe_mib > 0:
         n = args.copy_probe_mib * (1 << 20) // 4
         a = torch.ones(n, device=dev)

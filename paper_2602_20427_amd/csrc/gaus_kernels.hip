@@ -89,8 +89,10 @@ __global__ __launch_bounds__(256) void k_flags(Graph G, Work W) {
 // work-group, combined in a fixed order).
 constexpr int kUcEntries = kMaxChunks * kNC + kStripMax;   // per (restart, type)
 
-__global__ __launch_bounds__(256) void k_ucoef(Graph G, PolyArgs pa, Work W) {
-    __shared__ float part[4][64];
+constexpr int kUcoefRows = 16;   // work-group = 64 entries x 16 strided partial sums
+
+__global__ __launch_bounds__(64 * kUcoefRows) void k_ucoef(Graph G, PolyArgs pa, Work W) {
+    __shared__ float part[kUcoefRows][64];
     const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
     const int x = blockIdx.x * 64 + tx, k = blockIdx.y, b = blockIdx.z;
     // the type's polynomial work-groups: slots [g0*split, g1*split) of restart b
@@ -99,14 +101,20 @@ __global__ __launch_bounds__(256) void k_ucoef(Graph G, PolyArgs pa, Work W) {
     const int ncoef = pa.nc * kNC;
     float acc = 0.0f;
     if (x < ncoef) {
-        for (int g = g0 + ty; g < g1; g += 4) acc += W.Ucoef[(rb + g) * kMaxChunks * kNC + x];
+#pragma unroll 4
+        for (int g = g0 + ty; g < g1; g += kUcoefRows) acc += W.Ucoef[(rb + g) * kMaxChunks * kNC + x];
     } else if (x < ncoef + pa.SP) {
-        for (int g = g0 + ty; g < g1; g += 4) acc += W.Ustrip[(rb + g) * kStripMax + (x - ncoef)];
+#pragma unroll 4
+        for (int g = g0 + ty; g < g1; g += kUcoefRows) acc += W.Ustrip[(rb + g) * kStripMax + (x - ncoef)];
     }
     part[ty][tx] = acc;
     __syncthreads();
-    if (ty == 0 && x < ncoef + pa.SP)
-        W.Ucoef_k[((size_t)b * G.K + k) * kUcEntries + x] = (part[0][tx] + part[1][tx]) + (part[2][tx] + part[3][tx]);
+    if (ty == 0 && x < ncoef + pa.SP) {
+        float t = 0.0f;
+#pragma unroll
+        for (int r = 0; r < kUcoefRows; ++r) t += part[r][tx];
+        W.Ucoef_k[((size_t)b * G.K + k) * kUcEntries + x] = t;
+    }
 }
 
 // Usage U(slot) per (slot block, type, restart): step-by-step partials of the
@@ -917,7 +925,8 @@ hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const 
     }
     if (g.nb > 0 && (e = launch_back(g, w, lc, a.mu, a.sigma, st)) != hipSuccess) return e;
     if (pa.enabled)
-        hipLaunchKernelGGL(k_ucoef, dim3((pa.nc * kNC + pa.SP + 63) / 64, g.K, g.B), dim3(256), 0, st, g, pa, w);
+        hipLaunchKernelGGL(k_ucoef, dim3((pa.nc * kNC + pa.SP + 63) / 64, g.K, g.B), dim3(64 * kUcoefRows), 0, st,
+                           g, pa, w);
     hipLaunchKernelGGL(k_usage, dim3((g.T + kUsageBS - 1) / kUsageBS, g.K, g.B), dim3(kUsageBS), 0, st, g, pa, w);
     hipLaunchKernelGGL(k_vres, dim3(g.K, g.B), dim3(kTermsBS), 0, st, g, w, hp);
     if (hp.gamma != 0.0f) {   // expected storage units and their smooth peak
