@@ -26,9 +26,18 @@ namespace gaus {
 constexpr int kStripExtra = 8;   // row slots past SP: [SP] = D-3, [SP+1 .. SP+4] = helper values
 constexpr int kStripPad = kSmax; // zero slots before position 0 (positions -kSmax .. -1, F = 0)
 
-template <int NP>
-__global__ __launch_bounds__(64 * kPolyWaves) __attribute__((amdgpu_waves_per_eu(3)))
+// The degree tiers run as two kernels so that each has its own register
+// budget: kPolyWide (tier 3, degree 5; 4 waves per SIMD with one strip pass)
+// is launched first; it writes the per-work-group usage and V_dep / L_com
+// outputs and clears the records of step-by-step ops.  kPolyNarrow (tiers 1
+// and 2) follows, adds to those outputs, and work-groups without such ops
+// exit at once.
+constexpr int kPolyWide = 3, kPolyNarrow = 12;
+
+template <int NP, int TIERS>
+__global__ __launch_bounds__(64 * kPolyWaves) __attribute__((amdgpu_waves_per_eu(TIERS == kPolyWide && NP == 1 ? 4 : 3)))
 void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__restrict__ sigma, Work W) {
+    constexpr bool kFirst = TIERS == kPolyWide;
     // dynamic LDS: per wave 6 rows of SP strip values and 3 rows of SP +
     // kStripExtra raw CDF values, then per wave SP strip usages
     extern __shared__ float sDyn[];
@@ -74,12 +83,16 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
         l_s = G.delay[l_i];
         l_e0 = G.row_ptr[l_i]; l_e1 = G.row_ptr[l_i + 1];
     }
+    if constexpr (!kFirst) {   // nothing to add unless the work-group has ops of these tiers
+        if (!__syncthreads_or(lane < nq && (l_cls == 1 || l_cls == 2))) return;
+    }
     float gsum = 0.0f;  // V_dep, L_com of this wave's ops (lanes 0 and 2)
-    // step-by-step ops: no polynomial records
-    for (int oq = 0; oq < nq; ++oq) {
-        if (__builtin_amdgcn_readlane(l_cls, oq)) continue;
-        const int i = __builtin_amdgcn_readlane(l_i, oq);
-        if (lane < kPP) W.ppoly[((size_t)b * N + i) * kPP + lane] = 0.0f;
+    if constexpr (kFirst) {   // step-by-step ops: no polynomial records
+        for (int oq = 0; oq < nq; ++oq) {
+            if (__builtin_amdgcn_readlane(l_cls, oq)) continue;
+            const int i = __builtin_amdgcn_readlane(l_i, oq);
+            if (lane < kPP) W.ppoly[((size_t)b * N + i) * kPP + lane] = 0.0f;
+        }
     }
     // polynomial ops, one pass per degree tier (NC coefficients per vector)
     auto tier_pass = [&](auto nc_tag, int tier) {
@@ -255,9 +268,12 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
         gsum += pt4;   // lane 0: V_dep, lane 2: L_com
     }
     };
-    tier_pass(std::integral_constant<int, kTierDeg[1] + 1>{}, 1);
-    tier_pass(std::integral_constant<int, kTierDeg[2] + 1>{}, 2);
-    tier_pass(std::integral_constant<int, kTierDeg[3] + 1>{}, 3);
+    if constexpr (kFirst) {
+        tier_pass(std::integral_constant<int, kTierDeg[3] + 1>{}, 3);
+    } else {
+        tier_pass(std::integral_constant<int, kTierDeg[1] + 1>{}, 1);
+        tier_pass(std::integral_constant<int, kTierDeg[2] + 1>{}, 2);
+    }
     if (lane == 0) sGs[wv][0] = gsum;
     if (lane == 2) sGs[wv][1] = gsum;
 
@@ -276,13 +292,14 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
         float acc = 0.0f;
 #pragma unroll
         for (int w = 0; w < kPolyWaves; ++w) acc += sUc[w][c][k];
-        ucg[x] = acc;
+        ucg[x] = kFirst ? acc : ucg[x] + acc;
     }
     if (threadIdx.x < 2) {
         float acc = 0.0f;
 #pragma unroll
         for (int w = 0; w < kPolyWaves; ++w) acc += sGs[w][threadIdx.x];
-        W.gsum_poly[slot_id * 2 + threadIdx.x] = acc;
+        float *gs = W.gsum_poly + slot_id * 2 + threadIdx.x;
+        *gs = kFirst ? acc : *gs + acc;
     }
     float *usg = W.Ustrip + slot_id * kStripMax;
     for (int p = threadIdx.x; p < kStripMax; p += 64 * kPolyWaves) {
@@ -291,7 +308,7 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
 #pragma unroll
             for (int w = 0; w < kPolyWaves; ++w) acc += sUs[w * SP + p];
         }
-        usg[p] = acc;
+        usg[p] = kFirst ? acc : usg[p] + acc;
     }
 }
 
@@ -415,14 +432,18 @@ hipError_t launch_poly(const Graph &g, const Work &w, const PolyArgs &pa, const 
                        hipStream_t st) {
     const size_t lds = sizeof(float) * (size_t)kPolyWaves * (10 * pa.SP + 3 * (kStripPad + kStripExtra));
     const dim3 grid(g.ngroups * pa.split, g.B), block(64 * kPolyWaves);
+#define GAUS_POLY_PAIR(NPV)                                                                       \
+    hipLaunchKernelGGL((k_poly<NPV, kPolyWide>), grid, block, lds, st, g, pa, mu, sigma, w);     \
+    hipLaunchKernelGGL((k_poly<NPV, kPolyNarrow>), grid, block, lds, st, g, pa, mu, sigma, w);
     switch ((pa.SP + 63) / 64) {
-    case 1: hipLaunchKernelGGL(k_poly<1>, grid, block, lds, st, g, pa, mu, sigma, w); break;
-    case 2: hipLaunchKernelGGL(k_poly<2>, grid, block, lds, st, g, pa, mu, sigma, w); break;
-    case 3: hipLaunchKernelGGL(k_poly<3>, grid, block, lds, st, g, pa, mu, sigma, w); break;
-    case 4: hipLaunchKernelGGL(k_poly<4>, grid, block, lds, st, g, pa, mu, sigma, w); break;
-    case kStripPassesMax: hipLaunchKernelGGL(k_poly<kStripPassesMax>, grid, block, lds, st, g, pa, mu, sigma, w); break;
+    case 1: GAUS_POLY_PAIR(1) break;
+    case 2: GAUS_POLY_PAIR(2) break;
+    case 3: GAUS_POLY_PAIR(3) break;
+    case 4: GAUS_POLY_PAIR(4) break;
+    case kStripPassesMax: GAUS_POLY_PAIR(kStripPassesMax) break;
     default: return hipErrorInvalidValue;
     }
+#undef GAUS_POLY_PAIR
     return hipSuccess;
 }
 
