@@ -103,8 +103,8 @@ typedef struct {
                                       1 gives Formulations B and C, Sec. 4.1):
                                       L_mem = tau log sum_t exp(MReg(t)/tau) with MReg the
                                       expected storage units of eq:active folded like the
-                                      usage (App. B.3).  When > 0 every op is evaluated step
-                                      by step (no chunk polynomials). */
+                                      usage (App. B.3), evaluated step by step for every op
+                                      (the other terms keep the chunk polynomials). */
     int32_t family;                /* distribution of the relaxed start times (App. D):
                                       0 Gaussian, 1 logistic (scale sigma sqrt(3)/pi),
                                       2 Laplace (scale sigma/sqrt(2)), 3 Cauchy (scale

@@ -415,9 +415,9 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     int tile = 0, ntiles = 0;
     choose_config(h, B, c->lc, tile, ntiles);
     c->lc.fam = hp.family;
-    // the storage term's successor products and the non-Gaussian families are
-    // evaluated step by step only
-    setup_poly(h.D, (hp.gamma_mem > 0.0f || hp.family != 0) ? -1 : hp.poly_chunk, c->pa);
+    // the chunk polynomials are the Gaussian's (the storage term's successor
+    // products are evaluated step by step by their own kernels in any case)
+    setup_poly(h.D, hp.family != 0 ? -1 : hp.poly_chunk, c->pa);
 
     Graph &g = c->g;
     g.N = h.N; g.E = h.E; g.K = h.K; g.D = h.D; g.II = h.II; g.T = h.II > 0 ? h.II : h.D;
