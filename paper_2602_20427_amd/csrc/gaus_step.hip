@@ -408,8 +408,8 @@ __global__ __launch_bounds__(BS) void k_mem_fwd(Graph G, const float *__restrict
 // t mod T, over the interior bin edges t = 0..D-2:
 //   as the holder:      c(t) b_h (1 - Q_h(t)) dF_h(t)/dth_h
 //   as a successor i:  -c(t) b_h F_h(t) prod_{j != i} F_j(t) dF_i(t)/dth_i
-// with prod_{j != i} F_j = Q_h / F_i (0 when F_i underflows: then so does
-// dF_i, and the term is below fp32 resolution).
+// with prod_{j != i} F_j = Q_h / F_i (taken as 0 when F_i < 2^-100: dF_i is
+// then as small up to a bounded factor, far below fp32 resolution).
 template <int FAM, int BS, int SPT>
 __global__ __launch_bounds__(BS) void k_mem_bwd(Graph G, const float *__restrict__ mu,
                                                 const float *__restrict__ sigma, Work W) {
@@ -442,22 +442,29 @@ __global__ __launch_bounds__(BS) void k_mem_bwd(Graph G, const float *__restrict
         if (h < 0) continue;
         const float m = sMu[q], rs = sRs[q], cinv = rs * fam_k<FAM>(), bh = G.bmem[h];
         const int e0 = G.row_ptr[h], e1 = G.row_ptr[h + 1];
-        float Fh[SPT], Q[SPT], R[SPT], own[2] = {0.0f, 0.0f};
+        float Fh[SPT], Fmh[SPT], Fsh[SPT], Q[SPT], R[SPT], own[2] = {0.0f, 0.0f};
 #pragma unroll
         for (int j = 0; j < SPT; ++j) {
-            float st, Fm, Fs;
-            cdf_at<FAM>((long long)t0 + tid + j * BS, D, m, rs, cinv, st, Fm, Fs);
+            float st;
+            cdf_at<FAM>((long long)t0 + tid + j * BS, D, m, rs, cinv, st, Fmh[j], Fsh[j]);
             Fh[j] = st_F(st);
             Q[j] = 1.0f; R[j] = 0.0f;
-            for (int e = e0; e < e1; ++e) {
-                const int k = G.col[e];
-                const float sk = st_at<FAM>((long long)t0 + tid + j * BS, D, mub[k], 1.0f / sgb[k]);
+        }
+        for (int e = e0; e < e1; ++e) {
+            const int k = uniform(G.col[e]);
+            const float mk = mub[k], rk = 1.0f / sgb[k];
+#pragma unroll
+            for (int j = 0; j < SPT; ++j) {
+                const float sk = st_at<FAM>((long long)t0 + tid + j * BS, D, mk, rk);
                 R[j] = fmaf(Q[j], st_1mF(sk), R[j]);
                 Q[j] *= st_F(sk);
             }
+        }
+#pragma unroll
+        for (int j = 0; j < SPT; ++j) {
             const float wr = sW[tid + j * BS] * bh * R[j];
-            own[0] = fmaf(wr, Fm, own[0]);
-            own[1] = fmaf(wr, Fs, own[1]);
+            own[0] = fmaf(wr, Fmh[j], own[0]);
+            own[1] = fmaf(wr, Fsh[j], own[1]);
         }
         {
             const float r = block_sum<2, BS>(own, sRed[par]);
@@ -465,7 +472,7 @@ __global__ __launch_bounds__(BS) void k_mem_bwd(Graph G, const float *__restrict
             if (tid < 2) W.mown[(((size_t)b * N + h) * nt + tile) * 2 + tid] = r;
         }
         for (int e = e0; e < e1; ++e) {
-            const int k = G.col[e];
+            const int k = uniform(G.col[e]);
             const float mk = mub[k], rk = 1.0f / sgb[k], ck = rk * fam_k<FAM>();
             float acc[2] = {0.0f, 0.0f};
 #pragma unroll
@@ -473,7 +480,9 @@ __global__ __launch_bounds__(BS) void k_mem_bwd(Graph G, const float *__restrict
                 float st, Fm, Fs;
                 cdf_at<FAM>((long long)t0 + tid + j * BS, D, mk, rk, ck, st, Fm, Fs);
                 const float Fk = st_F(st);
-                const float others = Fk > 0.0f ? Q[j] / Fk : 0.0f;
+                // prod over the other successors; below 2^-100 the term is far
+                // under fp32 resolution (dF_k vanishes with F_k)
+                const float others = Fk > 0x1p-100f ? Q[j] * __builtin_amdgcn_rcpf(Fk) : 0.0f;
                 const float c = -sW[tid + j * BS] * bh * Fh[j] * others;
                 acc[0] = fmaf(c, Fm, acc[0]);
                 acc[1] = fmaf(c, Fs, acc[1]);
