@@ -238,13 +238,23 @@ __device__ __forceinline__ float wave_sum2(float v0, float v1, int lane) {
 // one barrier per reduction is needed.
 template <int NV, int BS>
 __device__ __forceinline__ float block_sum(float (&v)[NV], float (*slot)[8]) {
+    static_assert(NV <= 8, "at most 8 values");
     constexpr int NW = BS / 64;
     const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    // wave totals four and two values at a time
 #pragma unroll
-    for (int c = 0; c < NV; ++c) v[c] = wave_sum(v[c]);
-    if (lane == 0) {
-#pragma unroll
-        for (int c = 0; c < NV; ++c) slot[wid][c] = v[c];
+    for (int c = 0; c + 4 <= NV; c += 4) {
+        const float r = wave_sum4(v[c], v[c + 1], v[c + 2], v[c + 3], lane);
+        if (lane < 4) slot[wid][c + wave4_comp(lane)] = r;
+    }
+    constexpr int c2 = NV / 4 * 4;
+    if constexpr (NV - c2 >= 2) {
+        const float r = wave_sum2(v[c2], v[c2 + 1], lane);
+        if (lane < 2) slot[wid][c2 + lane] = r;
+    }
+    if constexpr ((NV - c2) % 2 == 1) {
+        const float r = wave_sum(v[NV - 1]);
+        if (lane == 0) slot[wid][NV - 1] = r;
     }
     __syncthreads();
     float r = 0.0f;

@@ -483,6 +483,7 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     AL(wts, (size_t)B * 4);
     AL(adamf, (size_t)B * 2);
     AL(cls, BN);
+    AL(rsig, BN);
     AL(dflag, BN);
     AL(ptier, BN);
     AL(gflag, (size_t)B * g.ngroups);

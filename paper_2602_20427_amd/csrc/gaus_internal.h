@@ -109,6 +109,7 @@ struct Work {
     float *wts;       // [B][4]            w_dep, w_res, w_rec, unused
     float *adamf;     // [B][2]            Adam bias corrections 1-beta1^t, 1-beta2^t
     unsigned char *cls;  // [B][N]          1 = op on the chunk-polynomial path this iteration
+    float *rsig;           // [B][N]        1/sigma of this iteration (written by k_classify)
     unsigned char *dflag;  // [B][N]        1 = op has step-by-step work (own terms or out-edges)
     unsigned char *ptier;  // [B][N]        polynomial op: tier of its vectors, the smallest over
                            //               itself and its polynomial consumers (highest degree)

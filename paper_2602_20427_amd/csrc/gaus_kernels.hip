@@ -50,6 +50,7 @@ __global__ void k_classify(Graph G, PolyArgs pa, const float *__restrict__ sigma
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= G.N) return;
     const float s = sigma[(size_t)b * G.N + i];
+    W.rsig[(size_t)b * G.N + i] = 1.0f / s;
     int t = 0;   // 0 = step by step, else the polynomial tier (wider sigma: higher tier, lower degree)
     if (pa.enabled && G.delay[i] <= kSmax)
         for (int q = 1; q <= kTiers; ++q) t = s >= pa.sig_thr[q] ? q : t;
@@ -473,7 +474,7 @@ __global__ __launch_bounds__(256) void k_final(Graph G, Work W, HP hp, const flo
     const int N = G.N, nt = G.ntiles;
     const size_t bi = (size_t)b * N + i;
     const float m_i = mu[bi], s_i = sigma[bi];
-    const float rs = 1.0f / s_i, cinv = rs * fam_k_rt(hp.family);
+    const float rs = W.rsig[bi], cinv = rs * fam_k_rt(hp.family);
     const float *wt = W.wts + (size_t)b * 4;
     const float w_dep = wt[0], w_res = wt[1], w_rec = wt[2];
 

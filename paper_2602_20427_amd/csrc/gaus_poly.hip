@@ -49,7 +49,7 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     const int N = G.N, D = G.D;
     const float *mub = mu + (size_t)b * N;
-    const float *sgb = sigma + (size_t)b * N;
+    const float *rsb = W.rsig + (size_t)b * N;   // 1/sigma
     const unsigned char *clsb = W.cls + (size_t)b * N;
     const bool cact = lane < pa.nc;
     const float tcen = (float)(pa.L0 + lane * pa.W) + pa.lam;
@@ -75,11 +75,11 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
     const int nj = (q1 - q0 - sub + split - 1) / split;
     const int nq = (nj - wv + kPolyWaves - 1) / kPolyWaves;
     int l_i = 0, l_cls = 0, l_s = 0, l_e0 = 0, l_e1 = 0;
-    float l_mu = 0.0f, l_sg = 1.0f;   // l_sg holds 1/sigma (divided once, on the loading lane)
+    float l_mu = 0.0f, l_sg = 1.0f;   // l_sg holds 1/sigma
     if (lane < nq) {
         l_i = G.perm[q0 + sub + split * (wv + kPolyWaves * lane)];
         l_cls = W.ptier[(size_t)b * N + l_i];   // 0: step by step, else the degree tier
-        l_mu = mub[l_i]; l_sg = 1.0f / sgb[l_i];
+        l_mu = mub[l_i]; l_sg = rsb[l_i];
         l_s = G.delay[l_i];
         l_e0 = G.row_ptr[l_i]; l_e1 = G.row_ptr[l_i + 1];
     }
@@ -195,7 +195,7 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
                 if (e + lane < e1) {
                     x_j = G.col[e + lane];
                     x_ok = clsb[x_j];
-                    x_mu = mub[x_j]; x_sg = 1.0f / sgb[x_j];
+                    x_mu = mub[x_j]; x_sg = rsb[x_j];
                 }
             }
             if (!__builtin_amdgcn_readlane(x_ok, eb)) continue;  // step-by-step edge, done by k_ops
@@ -376,7 +376,7 @@ __global__ __launch_bounds__(64 * kPolyWaves) void k_lse_poly(Graph G, PolyArgs 
         l_i = G.perm[q0 + sub + split * (wv + kPolyWaves * lane)];
         const size_t bi = (size_t)b * N + l_i;
         l_cls = W.cls[bi];
-        l_mu = mu[bi]; l_sg = sigma[bi];
+        l_mu = mu[bi]; l_sg = W.rsig[bi];   // 1/sigma
     }
     // this lane's chunk moments and strip weights of the group's type
     const int k = G.rtype[G.perm[q0]];
@@ -397,8 +397,8 @@ __global__ __launch_bounds__(64 * kPolyWaves) void k_lse_poly(Graph G, PolyArgs 
         if (!__builtin_amdgcn_readlane(l_cls, oq)) continue;
         const int i = __builtin_amdgcn_readlane(l_i, oq);
         const float m_i = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, l_mu), oq));
-        const float s_i = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, l_sg), oq));
-        const float rs = 1.0f / s_i, cinv = rs * kInvSqrt2Pi;
+        const float rs = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, l_sg), oq));
+        const float cinv = rs * kInvSqrt2Pi;
         float gm = 0.0f, gs = 0.0f;
 #pragma unroll
         for (int ps = 0; ps < NP; ++ps) {

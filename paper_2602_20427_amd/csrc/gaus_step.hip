@@ -43,7 +43,7 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
     const int D = G.D, N = G.N;
     const int t0 = tile * TILE;
     const float *mub = mu + (size_t)b * N;
-    const float *sgb = sigma + (size_t)b * N;
+    const float *rsb = W.rsig + (size_t)b * N;   // 1/sigma
 
     const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
     float accU[SPT];
@@ -82,8 +82,7 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
         const int e0 = uniform(G.row_ptr[i]), e1 = uniform(G.row_ptr[i + 1]);
         const bool poly_i = clsb[i] != 0;
         const int m = uniform(flag - 1);
-        const float m_i = mub[i], s_i = sgb[i];
-        const float rs = 1.0f / s_i;
+        const float m_i = mub[i], rs = rsb[i];
         const float cinv = rs * fam_k<FAM>();
         const int s = uniform(G.delay[i]);
         const bool win_shift = (m > 0) && (s <= kHalo);
@@ -130,8 +129,7 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
         for (int e = e0; e < e1; ++e) {
             const int j = uniform(G.col[e]);
             if (poly_i && clsb[j]) continue;  // polynomial edge
-            const float m_j = mub[j], s_j = sgb[j];
-            const float rsj = 1.0f / s_j;
+            const float m_j = mub[j], rsj = rsb[j];
             float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
             for (int k = 0; k < SPT; ++k) {
@@ -248,9 +246,8 @@ __global__ __launch_bounds__(BS) void k_back(Graph G, const float *__restrict__ 
     for (int e = be0; e < be1; ++e) {
         const int j = uniform(G.bsrc[e]), i = uniform(G.bdst[e]);
         const long long c = (long long)G.bdist[e] * G.II - G.delay[j];
-        const float mj = mu[(size_t)b * N + j], sj = sigma[(size_t)b * N + j];
-        const float mi = mu[(size_t)b * N + i], si = sigma[(size_t)b * N + i];
-        const float rsj = 1.0f / sj, rsi = 1.0f / si;
+        const float mj = mu[(size_t)b * N + j], rsj = W.rsig[(size_t)b * N + j];
+        const float mi = mu[(size_t)b * N + i], rsi = W.rsig[(size_t)b * N + i];
         const float cj = rsj * fam_k<FAM>(), ci = rsi * fam_k<FAM>();
         float acc[5] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
@@ -306,7 +303,7 @@ __global__ __launch_bounds__(BS) void k_lse_ops(Graph G, const float *__restrict
         direct = W.cls[bi] ? 0 : 1;
         sI[tid] = direct ? i : -1;
         sMu[tid] = mu[bi];
-        sRs[tid] = 1.0f / sigma[bi];
+        sRs[tid] = W.rsig[bi];
     } else if (tid < BS) {
         sI[tid] = -1;
     }
@@ -361,13 +358,13 @@ __global__ __launch_bounds__(BS) void k_mem_fwd(Graph G, const float *__restrict
     const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
     const int N = G.N, D = G.D;
     const int t0 = tile * TILE;
-    const float *mub = mu + (size_t)b * N, *sgb = sigma + (size_t)b * N;
+    const float *mub = mu + (size_t)b * N, *rsb = W.rsig + (size_t)b * N;
     sI[tid] = -1;
     if (q0 + tid < q1) {
         const int i = G.perm[q0 + tid];
         if (G.row_ptr[i + 1] > G.row_ptr[i]) sI[tid] = i;   // an op without successors holds nothing
         sMu[tid] = mub[i];
-        sRs[tid] = 1.0f / sgb[i];
+        sRs[tid] = rsb[i];
     }
     __syncthreads();
     double acc[SPT];
@@ -385,7 +382,7 @@ __global__ __launch_bounds__(BS) void k_mem_fwd(Graph G, const float *__restrict
         }
         for (int e = G.row_ptr[i]; e < G.row_ptr[i + 1]; ++e) {
             const int k = G.col[e];
-            const float mk = mub[k], rk = 1.0f / sgb[k];
+            const float mk = mub[k], rk = rsb[k];
 #pragma unroll
             for (int j = 0; j < SPT; ++j) {
                 const float st = st_at<FAM>((long long)t0 + tid + j * BS, D, mk, rk);
@@ -422,13 +419,13 @@ __global__ __launch_bounds__(BS) void k_mem_bwd(Graph G, const float *__restrict
     const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
     const int N = G.N, D = G.D, T = G.T, nt = G.ntiles;
     const int t0 = tile * TILE;
-    const float *mub = mu + (size_t)b * N, *sgb = sigma + (size_t)b * N;
+    const float *mub = mu + (size_t)b * N, *rsb = W.rsig + (size_t)b * N;
     sI[tid] = -1;
     if (q0 + tid < q1) {
         const int i = G.perm[q0 + tid];
         if (G.row_ptr[i + 1] > G.row_ptr[i]) sI[tid] = i;
         sMu[tid] = mub[i];
-        sRs[tid] = 1.0f / sgb[i];
+        sRs[tid] = rsb[i];
     }
     const float *ms = W.msoft + (size_t)b * T;
     for (int x = tid; x < TILE; x += BS) {
@@ -452,7 +449,7 @@ __global__ __launch_bounds__(BS) void k_mem_bwd(Graph G, const float *__restrict
         }
         for (int e = e0; e < e1; ++e) {
             const int k = uniform(G.col[e]);
-            const float mk = mub[k], rk = 1.0f / sgb[k];
+            const float mk = mub[k], rk = rsb[k];
 #pragma unroll
             for (int j = 0; j < SPT; ++j) {
                 const float sk = st_at<FAM>((long long)t0 + tid + j * BS, D, mk, rk);
@@ -473,7 +470,7 @@ __global__ __launch_bounds__(BS) void k_mem_bwd(Graph G, const float *__restrict
         }
         for (int e = e0; e < e1; ++e) {
             const int k = uniform(G.col[e]);
-            const float mk = mub[k], rk = 1.0f / sgb[k], ck = rk * fam_k<FAM>();
+            const float mk = mub[k], rk = rsb[k], ck = rk * fam_k<FAM>();
             float acc[2] = {0.0f, 0.0f};
 #pragma unroll
             for (int j = 0; j < SPT; ++j) {
