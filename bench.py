@@ -171,6 +171,9 @@ def main():
     ap.add_argument("--family", default="gaussian", choices=["gaussian", "logistic", "laplace", "cauchy"],
                     help="distribution of the relaxed start times (App. D); non-Gaussian families run "
                          "every op step by step")
+    ap.add_argument("--sigma", type=float, default=0.0,
+                    help="replace the initial widths by this sigma (a sharpened state like late iterations: "
+                         "ops narrower than the polynomial threshold run step by step); 0 = paper init")
     ap.add_argument("--solve-check-every", type=int, default=0,
                     help="time the Alg. 1 driver (gaus_solve) with a legalization check every this many "
                          "iterations instead of plain steps + one legalization; 0 = off")
@@ -211,6 +214,8 @@ def main():
         mu.copy_(torch.from_numpy(m0)); sigma.copy_(torch.from_numpy(s0))
     else:
         ctx.init_state(mu, sigma, restart_uniforms(N, B, seed=0))
+    if args.sigma > 0:
+        sigma.fill_(args.sigma)
     lam = torch.full((B, 3), hp.lambda0, device=dev)
     m = torch.zeros(2, B, N, device=dev)
     v = torch.zeros(2, B, N, device=dev)
@@ -292,6 +297,8 @@ def main():
         profile += "_mem"
     if args.family != "gaussian":
         profile += "_" + args.family
+    if args.sigma > 0:
+        profile += f"_sigma{args.sigma:g}"
     whole = model_flops(B * N * (D - 1), B * (E + prob.n_back) * (D - 1))
     out = {
         "metric": METRIC, "value": value, "unit": "op-step evals/s", "n_gpus": 1,
@@ -304,7 +311,9 @@ def main():
                                 (f" + {args.lse_beta:g} L_res (tau {args.tau:g})" if args.lse_beta else "") +
                                 (f" + {args.mem_gamma:g} L_mem (tau {args.tau:g}; storage units and a sink op)"
                                  if args.mem_gamma else ""),
-                   "family": args.family},
+                   "family": args.family,
+                   "state": "paper initialization" if args.sigma <= 0 else
+                            f"paper initialization means, sigma = {args.sigma:g}"},
         "ms_per_iteration_events": step_ms_events, "legalize_ms": legalize_ms,
         "poly_path": dict(poly_cfg, ops=census["ops"], edges=census["edges"]),
         "solve": solve_stats,

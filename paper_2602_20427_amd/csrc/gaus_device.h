@@ -92,6 +92,18 @@ __device__ __forceinline__ float fam_h(float z) {
     }
 }
 
+// |z| beyond which the density factor and the tail are exactly 0 in fp32
+// (the exponential underflows past the smallest subnormal, 2^-149): then a
+// CDF value is exactly 0 or 1 and its derivatives exactly 0.  The Cauchy
+// tails never vanish.
+template <int FAM>
+__host__ __device__ constexpr float fam_zflush() {
+    return FAM == 0 ? 15.0f      // exp2(-z^2 log2(e)/2) = 0 for |z| > 14.4
+         : FAM == 1 ? 60.0f      // exp2(-|z| pi/sqrt(3) log2(e)) = 0 for |z| > 57.4
+         : FAM == 2 ? 75.0f      // exp2(-|z| sqrt(2) log2(e)) = 0 for |z| > 73.6
+         : 3.0e38f;
+}
+
 // The same with the family chosen at run time (kernels outside the inner loops).
 __device__ __forceinline__ float fam_k_rt(int fam) {
     switch (fam) {

@@ -88,10 +88,21 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
         const bool win_shift = (m > 0) && (s <= kHalo);
         const int Lh = win_shift ? (s > 1 ? s : 1) : 1;
 
-        // row window: positions v = t0 - Lh + p, p in [0, TILE + Lh]
+        // row window: positions v = t0 - Lh + p, p in [0, TILE + Lh].  When
+        // all of it lies past fam_zflush on one side of the mean, its values
+        // are the exact constants (F = 0 or 1, zero derivatives).
+        constexpr float kZF = fam_zflush<FAM>();
+        const int wside = uniform(((float)(t0 + TILE) + 0.5f - m_i) * rs < -kZF ? -1
+                                  : ((float)(t0 - Lh) + 0.5f - m_i) * rs > kZF ? 1 : 0);
         for (int p = tid; p < TILE + Lh + 1; p += BS) {
             float st, Fm, Fs;
-            cdf_at<FAM>(t0 - Lh + p, D, m_i, rs, cinv, st, Fm, Fs);
+            const int v = t0 - Lh + p;
+            if (wside == 0) {
+                cdf_at<FAM>(v, D, m_i, rs, cinv, st, Fm, Fs);
+            } else {
+                st = v < 0 ? 0.0f : (v >= D - 1 || wside > 0) ? -0.0f : 0.0f;
+                Fm = 0.0f; Fs = 0.0f;
+            }
             sT[p] = st; sFm[p] = Fm; sFs[p] = Fs;
         }
         __syncthreads();
@@ -130,6 +141,21 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
             const int j = uniform(G.col[e]);
             if (poly_i && clsb[j]) continue;  // polynomial edge
             const float m_j = mub[j], rsj = rsb[j];
+            // steps t0-1 .. t0+TILE-1 all past fam_zflush on one side of the
+            // consumer's mean: its tail and density are exactly 0 there, so
+            // the edge adds only the count of consumers past their median
+            const int side = uniform(((float)(t0 + TILE - 1) + 0.5f - m_j) * rsj < -kZF ? -1
+                                     : ((float)(t0 - 1) + 0.5f - m_j) * rsj > kZF ? 1 : 0);
+            if (side != 0) {
+                if (side > 0) {
+#pragma unroll
+                    for (int k = 0; k < SPT; ++k)
+                        if (t0 + k * BS + tid < D - 1) SC[k] += 1.0f;
+                    if (tid == 0 && t0 > 0) pC += 1.0f;
+                }
+                if (tid < 4) W.cpart[(((size_t)b * G.E + e) * G.ntiles + tile) * kCP + tid] = 0.0f;
+                continue;
+            }
             float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
             for (int k = 0; k < SPT; ++k) {
