@@ -487,6 +487,7 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     AL(dflag, BN);
     AL(ptier, BN);
     AL(gflag, (size_t)B * g.ngroups);
+    AL(gnarrow, (size_t)B * g.ngroups);
     AL(gsum_ops, (size_t)B * g.ngroups * ntiles * 2);
     AL(gsum_poly, (size_t)B * g.ngroups * c->pa.split * 2);
     AL(vres_part, (size_t)B * h.K);

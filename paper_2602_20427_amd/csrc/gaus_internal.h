@@ -109,11 +109,12 @@ struct Work {
     float *wts;       // [B][4]            w_dep, w_res, w_rec, unused
     float *adamf;     // [B][2]            Adam bias corrections 1-beta1^t, 1-beta2^t
     unsigned char *cls;  // [B][N]          1 = op on the chunk-polynomial path this iteration
-    float *rsig;           // [B][N]        1/sigma of this iteration (written by k_classify)
+    float *rsig;           // [B][N]        1/sigma of this iteration (written by k_flags)
     unsigned char *dflag;  // [B][N]        1 = op has step-by-step work (own terms or out-edges)
     unsigned char *ptier;  // [B][N]        polynomial op: tier of its vectors, the smallest over
                            //               itself and its polynomial consumers (highest degree)
     int *gflag;       // [B][ngroups]      1 = some op of the group has step-by-step work
+    int *gnarrow;     // [B][ngroups]      1 = some op of the group takes polynomial degree 8 or 6
     float *gsum_ops;  // [B][ngroups][ntiles][2]  V_dep, L_com of a k_ops work-group
     float *gsum_poly; // [B][ngroups*split][2]  V_dep, L_com of a k_poly work-group
     float *vres_part; // [B][K]            V_res of one resource type

@@ -45,41 +45,54 @@ namespace gaus {
 // The strip [0, L0) u {D-2, D-1} (boundary conventions of the open end bins,
 // zero derivatives outside the interior edges) is evaluated step by step.
 // ---------------------------------------------------------------------------
-__global__ void k_classify(Graph G, PolyArgs pa, const float *__restrict__ sigma, Work W) {
-    const int b = blockIdx.y;
-    const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= G.N) return;
-    const float s = sigma[(size_t)b * G.N + i];
-    W.rsig[(size_t)b * G.N + i] = 1.0f / s;
-    int t = 0;   // 0 = step by step, else the polynomial tier (wider sigma: higher tier, lower degree)
-    if (pa.enabled && G.delay[i] <= kSmax)
+// Path of an op this iteration: 0 = step by step, else the polynomial tier
+// (wider sigma: higher tier, lower degree).
+__device__ __forceinline__ int poly_tier(const PolyArgs &pa, float s, int delay) {
+    int t = 0;
+    if (pa.enabled && delay <= kSmax)
         for (int q = 1; q <= kTiers; ++q) t = s >= pa.sig_thr[q] ? q : t;
-    W.cls[(size_t)b * G.N + i] = (unsigned char)t;
+    return t;
 }
 
-// Which ops (and groups) have step-by-step work this iteration: ops off the
-// polynomial path, and polynomial ops with an out-edge to such an op.
-// Work-group = (op group, restart); groups hold at most 256 ops.
-__global__ __launch_bounds__(256) void k_flags(Graph G, Work W) {
+// Classification and work flags.  Work-group = (op group, restart), thread
+// per op (groups hold at most 256 ops, and together every op):
+//   * 1/sigma and the op's path (tier) for the other kernels;
+//   * step-by-step work of the op: its own path, or an out-edge to an op off
+//     the polynomial path; of the group: any such op;
+//   * a polynomial producer's tier: the highest degree among itself and its
+//     polynomial consumers; of the group: whether the degree-8/6 kernel has
+//     work in it.
+// The consumers' tiers are recomputed here from their sigmas.
+__global__ __launch_bounds__(256) void k_flags(Graph G, PolyArgs pa, const float *__restrict__ sigma, Work W) {
     const int grp = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
     const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
-    const unsigned char *clsb = W.cls + (size_t)b * G.N;
-    int d = 0;
+    const float *sgb = sigma + (size_t)b * G.N;
+    int d = 0, narrow = 0;
     if (q0 + tid < q1) {
         const int i = G.perm[q0 + tid];
-        const int ci = clsb[i];
+        const size_t bi = (size_t)b * G.N + i;
+        const float s = sgb[i];
+        W.rsig[bi] = 1.0f / s;
+        const int ci = poly_tier(pa, s, G.delay[i]);
+        W.cls[bi] = (unsigned char)ci;
         d = ci ? 0 : 1;
-        int t = ci;   // a polynomial producer's vectors: the highest degree its edges need
+        int t = ci;
         for (int e = G.row_ptr[i]; e < G.row_ptr[i + 1]; ++e) {
-            const int cj = clsb[G.col[e]];
+            const int j = G.col[e];
+            const int cj = poly_tier(pa, sgb[j], G.delay[j]);
             d |= cj ? 0 : 1;
             t = cj ? min(t, cj) : t;
         }
-        W.dflag[(size_t)b * G.N + i] = (unsigned char)d;
-        W.ptier[(size_t)b * G.N + i] = (unsigned char)t;
+        W.dflag[bi] = (unsigned char)d;
+        W.ptier[bi] = (unsigned char)t;
+        narrow = (t == 1 || t == 2) ? 1 : 0;
     }
     d = __syncthreads_or(d);
-    if (tid == 0) W.gflag[(size_t)b * G.ngroups + grp] = d ? 1 : 0;
+    narrow = __syncthreads_or(narrow);
+    if (tid == 0) {
+        W.gflag[(size_t)b * G.ngroups + grp] = d ? 1 : 0;
+        W.gnarrow[(size_t)b * G.ngroups + grp] = narrow ? 1 : 0;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -910,11 +923,7 @@ hipError_t enqueue_check(const Graph &g, const Work &w, const HP &hp, float *mu,
 // ---------------------------------------------------------------------------
 hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const LaunchCfg &lc,
                              const PolyArgs &pa, const IterArgs &a, hipStream_t st) {
-    {
-        dim3 grid((g.N + 255) / 256, g.B);
-        hipLaunchKernelGGL(k_classify, grid, dim3(256), 0, st, g, pa, a.sigma, w);
-        hipLaunchKernelGGL(k_flags, dim3(g.ngroups, g.B), dim3(256), 0, st, g, w);
-    }
+    hipLaunchKernelGGL(k_flags, dim3(g.ngroups, g.B), dim3(256), 0, st, g, pa, a.sigma, w);
     hipError_t e;
     if (a.ops_begin) (void)hipEventRecord(a.ops_begin, st);
     if ((e = launch_ops(g, w, lc, a.mu, a.sigma, st)) != hipSuccess) return e;

@@ -1,7 +1,7 @@
 // gfx950 kernels of the chunk-polynomial evaluation (dense regime): k_poly
 // (forward terms, usage coefficients and the edge derivatives of ops whose
 // width allows it) and k_lse_mom / k_lse_poly (gradient of the smooth peak
-// usage for those ops).  The method is described at k_classify in
+// usage for those ops).  The method is described before poly_tier in
 // gaus_kernels.hip.
 #include <type_traits>
 
@@ -38,6 +38,9 @@ template <int NP, int TIERS>
 __global__ __launch_bounds__(64 * kPolyWaves) __attribute__((amdgpu_waves_per_eu(TIERS == kPolyWide && NP == 1 ? 4 : 3)))
 void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__restrict__ sigma, Work W) {
     constexpr bool kFirst = TIERS == kPolyWide;
+    if constexpr (!kFirst) {   // no op of the group takes degree 8 or 6
+        if (!W.gnarrow[(size_t)blockIdx.y * G.ngroups + blockIdx.x / pa.split]) return;
+    }
     // dynamic LDS: per wave 6 rows of SP strip values and 3 rows of SP +
     // kStripExtra raw CDF values, then per wave SP strip usages
     extern __shared__ float sDyn[];
