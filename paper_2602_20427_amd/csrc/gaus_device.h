@@ -284,9 +284,11 @@ __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirs
 // Expansion of an op's CDF around a chunk centre, NC coefficients per vector
 // (degree NC-1): T[n] = Phi^(n)(z0) r^n / n!, n < NC + kShiftTerms + 1, the
 // terms the one-step shift series reach.
-template <int NC = kNC>
+// NT: coefficients kept (the shift series need NC + kShiftTerms + 1; dF/dmu
+// alone needs NC + 1).
+template <int NC = kNC, int NT = NC + kShiftTerms + 1>
 struct Expansion {
-    float T[NC + kShiftTerms + 1];   // Taylor coefficients in y, T[0] = F(z0)
+    float T[NT];                     // Taylor coefficients in y, T[0] = F(z0)
     float G0;                        // 1 - F(z0), from the tail
     float z0, r;
 };
@@ -303,9 +305,9 @@ constexpr float back_coef(int k, int j) {
     return (float)(-(double)(k + j + 1) * binom_d(k + j, j) * ((j & 1) ? -1.0 : 1.0));
 }
 
-template <int NC>
-__device__ __forceinline__ void expand(float mu, float rs, float tcen, Expansion<NC> &e) {
-    constexpr int TN = NC + kShiftTerms + 1;
+template <int NC, int NT>
+__device__ __forceinline__ void expand(float mu, float rs, float tcen, Expansion<NC, NT> &e) {
+    constexpr int TN = NT;
     e.r = rs;
     e.z0 = (tcen + 0.5f - mu) * rs;
     float tail, g;
@@ -324,8 +326,9 @@ __device__ __forceinline__ void expand(float mu, float rs, float tcen, Expansion
     }
 }
 
-template <int NC>
-__device__ __forceinline__ void vec_dFdmu(const Expansion<NC> &e, float (&a)[NC]) {
+template <int NC, int NT>
+__device__ __forceinline__ void vec_dFdmu(const Expansion<NC, NT> &e, float (&a)[NC]) {
+    static_assert(NT >= NC + 1, "dF/dmu needs NC + 1 coefficients");
 #pragma unroll
     for (int k = 0; k < NC; ++k) a[k] = -(float)(k + 1) * e.T[k + 1];
 }

@@ -414,14 +414,24 @@ __global__ __launch_bounds__(64 * kPolyWaves) void k_lse_poly(Graph G, PolyArgs 
                 gs = fmaf(sw[ps], Fm * z, gs);
             }
         }
-        if (cact) {
-            Expansion<> e;
+        // the op's own degree tier (its chunk expansion meets no consumer here)
+        auto chunk = [&](auto nc_tag) {
+            constexpr int NC = decltype(nc_tag)::value;
+            Expansion<NC, NC + 1> e;
             expand(m_i, rs, tcen, e);
-            float a[kNC], v[kNC];
+            float a[NC], v[NC], mm[NC];
             vec_dFdmu(e, a);
             vec_times_z(a, e.z0, e.r, v);
-            gm += vdot(a, mom);
-            gs += vdot(v, mom);
+#pragma unroll
+            for (int n = 0; n < NC; ++n) mm[n] = mom[n];
+            gm += vdot(a, mm);
+            gs += vdot(v, mm);
+        };
+        if (cact) {
+            const int tier = __builtin_amdgcn_readlane(l_cls, oq);
+            if (tier == 3) chunk(std::integral_constant<int, kTierDeg[3] + 1>{});
+            else if (tier == 2) chunk(std::integral_constant<int, kTierDeg[2] + 1>{});
+            else chunk(std::integral_constant<int, kTierDeg[1] + 1>{});
         }
         const float r = wave_sum2(gm, gs, lane);
         if (lane < 2) W.lpoly[((size_t)b * N + i) * 2 + lane] = r;

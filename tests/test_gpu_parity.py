@@ -181,12 +181,14 @@ def test_polynomial_path_chunk_widths(W):
     _check(p, mu, sg, _lam(B, 42), hparams(alpha=0.2, rho=0.01, poly_chunk=W), range(B), f"chunk W={W}")
 
 
-def test_polynomial_degree_tiers():
+@pytest.mark.parametrize("beta", [0.0, 1.0])
+def test_polynomial_degree_tiers(beta):
     """Wide ops take fewer series terms: degree 8 for rho = ((W-1)/2)/sigma up to
     1/4, degree 6 and degree 5 above the sigmas where their truncation error
     matches degree 8's at rho = 1/4.  Sigmas straddle every boundary, so edges
     join ops of different degrees (the producer's vectors then take the
-    higher degree) and ops of both paths."""
+    higher degree) and ops of both paths; with the smooth peak usage on, its
+    gradient takes each op's own degree."""
     p = _ragged_problem(77, N=1500, D=3000, big_delay=False)
     p.delay[:] = np.random.default_rng(78).integers(0, 9, size=p.n_ops).astype(np.int32)
     ctx = bd.Context(p, 1, hparams())
@@ -205,7 +207,8 @@ def test_polynomial_degree_tiers():
         share = np.mean((sg >= lo) & (sg < hi))
         say(f"  W={W}: degree {d} for sigma in [{lo:.1f}, {hi:.1f}): {share:.2f} of the ops")
         assert share > 0.1
-    _check(p, mu, sg, _lam(B, 80), hparams(alpha=0.2, rho=0.01), range(B), "degree tiers")
+    _check(p, mu, sg, _lam(B, 80), hparams(alpha=0.2, rho=0.01, beta=beta, tau=0.1), range(B),
+           f"degree tiers, smooth peak weight {beta:g}")
 
 
 def test_small_edge_cases():
