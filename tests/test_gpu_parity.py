@@ -211,6 +211,22 @@ def test_polynomial_degree_tiers(beta):
            f"degree tiers, smooth peak weight {beta:g}")
 
 
+@pytest.mark.parametrize("II,n_back", [(0, 0), (3001, 3)])
+def test_maximum_horizon(II, n_back):
+    """D = 2^22, the largest horizon the library takes: 4096 tiles of the
+    step-by-step kernel, no polynomial path (no chunk width leaves a strip of
+    at most 320 steps), sigmas from 0.5 to 2e5 (sharp ops leave most tiles
+    to the exact far-tail shortcut, wide ones span the horizon), delays up
+    to 70000 steps."""
+    p = _ragged_problem(91 + II, N=40, D=1 << 22, II=II, n_back=n_back, big_delay=False)
+    p.delay[[5, 17]] = [300, 70000]
+    B = 2
+    rng = np.random.default_rng(92)
+    mu = rng.uniform(-100, p.D + 100, size=(B, p.n_ops)).astype(np.float32)
+    sg = np.exp(rng.uniform(np.log(0.5), np.log(2e5), size=(B, p.n_ops))).astype(np.float32)
+    _check(p, mu, sg, _lam(B, 93), hparams(alpha=0.2, rho=0.01), range(B), f"D=2^22 II={II}")
+
+
 def test_small_edge_cases():
     """D = 1 (one bin holds all mass), a single op, no edges."""
     for D, N, with_edges in ((1, 5, True), (2, 1, False), (3, 4, False), (64, 1, False)):
