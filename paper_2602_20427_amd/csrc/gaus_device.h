@@ -400,6 +400,18 @@ __device__ __forceinline__ float vdot_F(const float (&a)[NC], const Expansion<NC
     return acc;
 }
 
+// c = a b truncated to NC coefficients (the Cauchy product of two series)
+template <int NC>
+__device__ __forceinline__ void poly_mul(const float (&a)[NC], const float (&b)[NC], float (&c)[NC]) {
+#pragma unroll
+    for (int k = 0; k < NC; ++k) {
+        float acc = 0.0f;
+#pragma unroll
+        for (int i = 0; i <= k; ++i) acc = fmaf(a[i], b[k - i], acc);
+        c[k] = acc;
+    }
+}
+
 // weight difference c(t) - c(t+1) of a per-slot table folded mod T
 __device__ __forceinline__ float soft_diff(const float *sk, int t, int T) {
     return sk[t % T] - sk[(t + 1) % T];

@@ -462,6 +462,13 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     AL(lpart, BN * ntiles * 2);
     AL(lpoly, BN * 2);
     AL(Mpart, (size_t)B * g.ngroups * h.D);
+    AL(mpoly, BN);
+    {
+        const size_t slots = (size_t)B * g.ngroups * std::max(1, c->pa.split);
+        AL(mcoef, slots * kMaxChunks * kNC);
+        AL(mstrip, slots * kStripMax);
+        AL(mcoef_r, (size_t)B * (kMaxChunks * kNC + kStripMax));
+    }
     AL(mreg, (size_t)B * g.T);
     AL(mregd, (size_t)B * g.T);
     AL(msoft, (size_t)B * g.T);

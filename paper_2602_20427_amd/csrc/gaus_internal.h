@@ -35,6 +35,12 @@ constexpr int kSmax = 8;                      // largest producer delay on that 
 constexpr float kRhoMax = 0.25f;
 constexpr int kMaxChunks = 64;                // one chunk per lane of a wave
 constexpr int kStripMax = 320;                 // step-by-step strip positions per op, at most
+// Storage term on the chunk polynomials: a holder whose successors are all
+// polynomial, at most kMemPolyDeg of them, with rho summed over the holder
+// and its successors at most kMemRhoMax (the product of their series keeps
+// the degree-8 accuracy); every other holder is evaluated step by step.
+constexpr int kMemPolyDeg = 4;
+constexpr float kMemRhoMax = 0.25f;
 
 struct PolyArgs {
     int enabled;          // 0: every op takes the per-step path
@@ -88,6 +94,10 @@ struct Work {
     float *lpart;     // [B][N][tiles][2]  smooth-peak gradient (mu, sigma) of step-by-step ops, per tile
     float *lpoly;     // [B][N][2]         the same for ops on the polynomial path
     double *Mpart;    // [B][ngroups][D]   expected storage units of a group's ops per step
+    unsigned char *mpoly;  // [B][N]       1 = the op's storage term is taken on the chunk polynomials
+    double *mcoef;    // [B][ngroups*split][kMaxChunks][kNC]  storage profile coefficients per chunk
+    double *mstrip;   // [B][ngroups*split][kStripMax]        storage profile at the strip positions
+    double *mcoef_r;  // [B][kMaxChunks*kNC + kStripMax]     the same summed over the work-groups
     double *mregd;    // [B][T]            expected storage units per (modulo) slot
     float *mreg;      // [B][T]            the same in float (gaus_get_storage)
     float *msoft;     // [B][T]            gamma * dL_mem/dMReg (softmax over the slots)
@@ -173,6 +183,8 @@ hipError_t launch_mem_bwd(const Graph &g, const Work &w, const LaunchCfg &lc, co
                           const float *sigma, hipStream_t st);
 hipError_t launch_poly(const Graph &g, const Work &w, const PolyArgs &pa, const float *mu, const float *sigma,
                        hipStream_t st);
+hipError_t launch_mem_poly_fwd(const Graph &g, const Work &w, const PolyArgs &pa, const float *mu,
+                               hipStream_t st);
 hipError_t launch_lse_poly(const Graph &g, const Work &w, const PolyArgs &pa, const float *mu,
                            const float *sigma, hipStream_t st);
 

@@ -62,8 +62,11 @@ __device__ __forceinline__ int poly_tier(const PolyArgs &pa, float s, int delay)
 //   * a polynomial producer's tier: the highest degree among itself and its
 //     polynomial consumers; of the group: whether the degree-8/6 kernel has
 //     work in it.
-// The consumers' tiers are recomputed here from their sigmas.
-__global__ __launch_bounds__(256) void k_flags(Graph G, PolyArgs pa, const float *__restrict__ sigma, Work W) {
+// The consumers' tiers are recomputed here from their sigmas.  With the
+// storage term on, also whether a holder's storage term is taken on the
+// chunk polynomials (kMemPolyDeg, kMemRhoMax).
+__global__ __launch_bounds__(256) void k_flags(Graph G, PolyArgs pa, const float *__restrict__ sigma, Work W,
+                                               int mem_on) {
     const int grp = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
     const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
     const float *sgb = sigma + (size_t)b * G.N;
@@ -77,13 +80,19 @@ __global__ __launch_bounds__(256) void k_flags(Graph G, PolyArgs pa, const float
         W.cls[bi] = (unsigned char)ci;
         d = ci ? 0 : 1;
         int t = ci;
-        for (int e = G.row_ptr[i]; e < G.row_ptr[i + 1]; ++e) {
+        const int e0 = G.row_ptr[i], e1 = G.row_ptr[i + 1];
+        float rsum = 1.0f / s;   // sum of 1/sigma over the holder and its successors
+        for (int e = e0; e < e1; ++e) {
             const int j = G.col[e];
-            const int cj = poly_tier(pa, sgb[j], G.delay[j]);
+            const float sj = sgb[j];
+            const int cj = poly_tier(pa, sj, G.delay[j]);
             d |= cj ? 0 : 1;
             t = cj ? min(t, cj) : t;
+            if (mem_on) rsum += 1.0f / sj;
         }
         W.dflag[bi] = (unsigned char)d;
+        W.mpoly[bi] = (unsigned char)(mem_on && ci != 0 && d == 0 && e1 > e0 && e1 - e0 <= kMemPolyDeg &&
+                                      pa.lam * rsum <= kMemRhoMax);
         W.ptier[bi] = (unsigned char)t;
         narrow = (t == 1 || t == 2) ? 1 : 0;
     }
@@ -309,12 +318,54 @@ __global__ __launch_bounds__(kTermsBS) void k_vres(Graph G, Work W, HP hp) {
 // L_mem = M + tau log sum_t exp((MReg(t) - M)/tau) and gamma times its
 // derivative (a softmax) per slot.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_mreg(Graph G, Work W) {
+// Storage profile coefficients of the polynomial holders summed over the
+// work-groups of a restart (16 strided partial sums per entry, fp64).
+__global__ __launch_bounds__(64 * kUcoefRows) void k_mcoef(Graph G, PolyArgs pa, Work W) {
+    __shared__ double part[kUcoefRows][64];
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    const int x = blockIdx.x * 64 + tx, b = blockIdx.y;
+    const int nslot = G.ngroups * pa.split;
+    const size_t rb = (size_t)b * nslot;
+    const int ncoef = pa.nc * kNC;
+    double acc = 0.0;
+    if (x < ncoef) {
+        for (int g = ty; g < nslot; g += kUcoefRows) acc += W.mcoef[(rb + g) * kMaxChunks * kNC + x];
+    } else if (x < ncoef + pa.SP) {
+        for (int g = ty; g < nslot; g += kUcoefRows) acc += W.mstrip[(rb + g) * kStripMax + (x - ncoef)];
+    }
+    part[ty][tx] = acc;
+    __syncthreads();
+    if (ty == 0 && x < ncoef + pa.SP) {
+        double t = 0.0;
+#pragma unroll
+        for (int r = 0; r < kUcoefRows; ++r) t += part[r][tx];
+        W.mcoef_r[(size_t)b * (kMaxChunks * kNC + kStripMax) + x] = t;
+    }
+}
+
+// Storage profile per (modulo) slot: the step-by-step holders' group partials
+// plus, with the polynomial path on, the polynomial holders' chunk
+// polynomial at t (or their strip value), in fp64.
+__global__ __launch_bounds__(256) void k_mreg(Graph G, PolyArgs pa, Work W) {
     const int slot = blockIdx.x * 256 + threadIdx.x, b = blockIdx.y;
     if (slot >= G.T) return;
+    const double *mc = W.mcoef_r + (size_t)b * (kMaxChunks * kNC + kStripMax);
+    const int D = G.D, ncoef = pa.nc * kNC;
     double acc = 0.0;
-    for (int t = slot; t < G.D; t += G.T)
-        for (int g = 0; g < G.ngroups; ++g) acc += W.Mpart[((size_t)b * G.ngroups + g) * G.D + t];
+    for (int t = slot; t < D; t += G.T) {
+        for (int g = 0; g < G.ngroups; ++g) acc += W.Mpart[((size_t)b * G.ngroups + g) * D + t];
+        if (pa.enabled) {
+            if (t >= pa.L0 && t < D - 2) {
+                const int c = (t - pa.L0) / pa.W;
+                const double y = (double)(t - pa.L0 - c * pa.W) - (double)pa.lam;
+                double v = mc[c * kNC + kNC - 1];
+                for (int k = kNC - 2; k >= 0; --k) v = fma(v, y, mc[c * kNC + k]);
+                acc += v;
+            } else {
+                acc += mc[ncoef + (t < pa.L0 ? t : pa.L0 + (t - (D - 2)))];
+            }
+        }
+    }
     W.mregd[(size_t)b * G.T + slot] = acc;
     W.mreg[(size_t)b * G.T + slot] = (float)acc;
 }
@@ -923,7 +974,8 @@ hipError_t enqueue_check(const Graph &g, const Work &w, const HP &hp, float *mu,
 // ---------------------------------------------------------------------------
 hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const LaunchCfg &lc,
                              const PolyArgs &pa, const IterArgs &a, hipStream_t st) {
-    hipLaunchKernelGGL(k_flags, dim3(g.ngroups, g.B), dim3(256), 0, st, g, pa, a.sigma, w);
+    hipLaunchKernelGGL(k_flags, dim3(g.ngroups, g.B), dim3(256), 0, st, g, pa, a.sigma, w,
+                       (hp.gamma != 0.0f && pa.enabled) ? 1 : 0);
     hipError_t e;
     if (a.ops_begin) (void)hipEventRecord(a.ops_begin, st);
     if ((e = launch_ops(g, w, lc, a.mu, a.sigma, st)) != hipSuccess) return e;
@@ -941,7 +993,12 @@ hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const 
     hipLaunchKernelGGL(k_vres, dim3(g.K, g.B), dim3(kTermsBS), 0, st, g, w, hp);
     if (hp.gamma != 0.0f) {   // expected storage units and their smooth peak
         if ((e = launch_mem_fwd(g, w, lc, a.mu, a.sigma, st)) != hipSuccess) return e;
-        hipLaunchKernelGGL(k_mreg, dim3((g.T + 255) / 256, g.B), dim3(256), 0, st, g, w);
+        if (pa.enabled) {
+            if ((e = launch_mem_poly_fwd(g, w, pa, a.mu, st)) != hipSuccess) return e;
+            hipLaunchKernelGGL(k_mcoef, dim3((pa.nc * kNC + pa.SP + 63) / 64, g.B), dim3(64 * kUcoefRows), 0, st,
+                               g, pa, w);
+        }
+        hipLaunchKernelGGL(k_mreg, dim3((g.T + 255) / 256, g.B), dim3(256), 0, st, g, pa, w);
         hipLaunchKernelGGL(k_mem_lse, dim3(g.B), dim3(kTermsBS), 0, st, g, w, hp);
     }
     hipLaunchKernelGGL(k_combine, dim3(g.B), dim3(kCombineBS), 0, st, g, pa, w, hp, a.lambda_in,

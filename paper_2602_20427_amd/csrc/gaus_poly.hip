@@ -439,6 +439,120 @@ __global__ __launch_bounds__(64 * kPolyWaves) void k_lse_poly(Graph G, PolyArgs 
 }
 
 // ---------------------------------------------------------------------------
+// Storage term of the polynomial holders (eq:active): on a chunk the holder's
+// CDF F_h and its successors' F_j are degree-8 series in the step offset, and
+//   R = 1 - prod_j F_j = sum_j (prod_{k<j} F_k) (1 - F_j),   Reg_h = b_h F_h R
+// are formed as truncated series products, 1 - F_j from the precise tail at
+// the chunk centre, so R keeps full precision where every F_j is near 1.
+// The strip positions are evaluated step by step.  Work-group = (op group,
+// restart, split slot) as in k_poly; per work-group the chunk coefficients and
+// strip values of its holders are summed in fp64.
+// ---------------------------------------------------------------------------
+template <int NP>
+__global__ __launch_bounds__(64 * kPolyWaves) void k_mem_poly_fwd(Graph G, PolyArgs pa, const float *__restrict__ mu,
+                                                                  Work W) {
+    __shared__ double sMc[kPolyWaves][kNC][kMaxChunks];
+    __shared__ double sMs[kPolyWaves][NP * 64];
+    const int SP = pa.SP, split = pa.split, L0 = pa.L0;
+    const int grp = blockIdx.x / split, sub = blockIdx.x - grp * split, b = blockIdx.y;
+    const size_t slot_id = ((size_t)b * G.ngroups + grp) * split + sub;
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int N = G.N, D = G.D;
+    const float *mub = mu + (size_t)b * N;
+    const float *rsb = W.rsig + (size_t)b * N;
+    const float tcen = (float)(L0 + lane * pa.W) + pa.lam;
+
+    double mc[kNC], ms[NP];
+#pragma unroll
+    for (int k = 0; k < kNC; ++k) mc[k] = 0.0;
+#pragma unroll
+    for (int ps = 0; ps < NP; ++ps) ms[ps] = 0.0;
+
+    const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
+    const int nj = (q1 - q0 - sub + split - 1) / split;
+    const int nq = (nj - wv + kPolyWaves - 1) / kPolyWaves;
+    int l_i = 0, l_ok = 0;
+    if (lane < nq) {
+        l_i = G.perm[q0 + sub + split * (wv + kPolyWaves * lane)];
+        l_ok = W.mpoly[(size_t)b * N + l_i];
+    }
+    for (int oq = 0; oq < nq; ++oq) {
+        if (!__builtin_amdgcn_readlane(l_ok, oq)) continue;
+        const int i = __builtin_amdgcn_readlane(l_i, oq);
+        const float m_i = mub[i], rs = rsb[i], bh = G.bmem[i];
+        const int e0 = G.row_ptr[i], e1 = G.row_ptr[i + 1];
+        // strip: Reg_h(u) step by step
+#pragma unroll
+        for (int ps = 0; ps < NP; ++ps) {
+            const int p = ps * 64 + lane;
+            if (p < SP) {
+                const int u = p < L0 ? p : D - 2 + (p - L0);
+                const float Fh = st_F(st_at(u, D, m_i, rs));
+                float Q = 1.0f, R = 0.0f;
+                for (int e = e0; e < e1; ++e) {
+                    const int j = G.col[e];
+                    const float st = st_at(u, D, mub[j], rsb[j]);
+                    R = fmaf(Q, st_1mF(st), R);
+                    Q *= st_F(st);
+                }
+                ms[ps] += (double)(bh * Fh * R);
+            }
+        }
+        // chunks: truncated series products
+        Expansion<kNC, kNC> eh;
+        expand(m_i, rs, tcen, eh);
+        float Q[kNC], R[kNC];
+#pragma unroll
+        for (int k = 0; k < kNC; ++k) { Q[k] = k == 0 ? 1.0f : 0.0f; R[k] = 0.0f; }
+        for (int e = e0; e < e1; ++e) {
+            const int j = G.col[e];
+            Expansion<kNC, kNC> ej;
+            expand(mub[j], rsb[j], tcen, ej);
+            float omF[kNC], Fj[kNC], t[kNC];
+#pragma unroll
+            for (int k = 0; k < kNC; ++k) { omF[k] = k == 0 ? ej.G0 : -ej.T[k]; Fj[k] = ej.T[k]; }
+            poly_mul(Q, omF, t);
+#pragma unroll
+            for (int k = 0; k < kNC; ++k) R[k] += t[k];
+            poly_mul(Q, Fj, t);
+#pragma unroll
+            for (int k = 0; k < kNC; ++k) Q[k] = t[k];
+        }
+        float Fh[kNC], reg[kNC];
+#pragma unroll
+        for (int k = 0; k < kNC; ++k) Fh[k] = eh.T[k];
+        poly_mul(Fh, R, reg);
+#pragma unroll
+        for (int k = 0; k < kNC; ++k) mc[k] += (double)(bh * reg[k]);
+    }
+    // combine the waves in a fixed order; every slot is written (zeros if the
+    // work-group holds no polynomial holder)
+#pragma unroll
+    for (int k = 0; k < kNC; ++k) sMc[wv][k][lane] = mc[k];
+#pragma unroll
+    for (int ps = 0; ps < NP; ++ps) sMs[wv][ps * 64 + lane] = ms[ps];
+    __syncthreads();
+    double *mcg = W.mcoef + slot_id * kMaxChunks * kNC;
+    for (int x = threadIdx.x; x < kMaxChunks * kNC; x += 64 * kPolyWaves) {
+        const int c = x / kNC, k = x % kNC;
+        double acc = 0.0;
+#pragma unroll
+        for (int w = 0; w < kPolyWaves; ++w) acc += sMc[w][k][c];
+        mcg[x] = acc;
+    }
+    double *msg = W.mstrip + slot_id * kStripMax;
+    for (int p = threadIdx.x; p < kStripMax; p += 64 * kPolyWaves) {
+        double acc = 0.0;
+        if (p < SP) {
+#pragma unroll
+            for (int w = 0; w < kPolyWaves; ++w) acc += sMs[w][p];
+        }
+        msg[p] = acc;
+    }
+}
+
+
+// ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
 hipError_t launch_poly(const Graph &g, const Work &w, const PolyArgs &pa, const float *mu, const float *sigma,
@@ -457,6 +571,20 @@ hipError_t launch_poly(const Graph &g, const Work &w, const PolyArgs &pa, const 
     default: return hipErrorInvalidValue;
     }
 #undef GAUS_POLY_PAIR
+    return hipSuccess;
+}
+
+hipError_t launch_mem_poly_fwd(const Graph &g, const Work &w, const PolyArgs &pa, const float *mu,
+                               hipStream_t st) {
+    const dim3 grid(g.ngroups * pa.split, g.B), block(64 * kPolyWaves);
+    switch ((pa.SP + 63) / 64) {
+    case 1: hipLaunchKernelGGL(k_mem_poly_fwd<1>, grid, block, 0, st, g, pa, mu, w); break;
+    case 2: hipLaunchKernelGGL(k_mem_poly_fwd<2>, grid, block, 0, st, g, pa, mu, w); break;
+    case 3: hipLaunchKernelGGL(k_mem_poly_fwd<3>, grid, block, 0, st, g, pa, mu, w); break;
+    case 4: hipLaunchKernelGGL(k_mem_poly_fwd<4>, grid, block, 0, st, g, pa, mu, w); break;
+    case kStripPassesMax: hipLaunchKernelGGL(k_mem_poly_fwd<kStripPassesMax>, grid, block, 0, st, g, pa, mu, w); break;
+    default: return hipErrorInvalidValue;
+    }
     return hipSuccess;
 }
 
