@@ -468,6 +468,9 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
         AL(mcoef, slots * kMaxChunks * kNC);
         AL(mstrip, slots * kStripMax);
         AL(mcoef_r, (size_t)B * (kMaxChunks * kNC + kStripMax));
+        AL(mmom, (size_t)B * kMaxChunks * kNC);
+        AL(mopoly, BN * 2);
+        AL(mspoly, (size_t)B * h.E * 2);
     }
     AL(mreg, (size_t)B * g.T);
     AL(mregd, (size_t)B * g.T);

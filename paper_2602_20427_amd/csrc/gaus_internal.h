@@ -98,6 +98,9 @@ struct Work {
     double *mcoef;    // [B][ngroups*split][kMaxChunks][kNC]  storage profile coefficients per chunk
     double *mstrip;   // [B][ngroups*split][kStripMax]        storage profile at the strip positions
     double *mcoef_r;  // [B][kMaxChunks*kNC + kStripMax]     the same summed over the work-groups
+    float *mmom;      // [B][kMaxChunks][kNC]  chunk moments sum_y c(t) y^n of the storage softmax
+    float *mopoly;    // [B][N][2]         storage gradient of a polynomial holder as the holder
+    float *mspoly;    // [B][E][2]         storage gradient of the consumer of an edge out of one
     double *mregd;    // [B][T]            expected storage units per (modulo) slot
     float *mreg;      // [B][T]            the same in float (gaus_get_storage)
     float *msoft;     // [B][T]            gamma * dL_mem/dMReg (softmax over the slots)
@@ -184,6 +187,8 @@ hipError_t launch_mem_bwd(const Graph &g, const Work &w, const LaunchCfg &lc, co
 hipError_t launch_poly(const Graph &g, const Work &w, const PolyArgs &pa, const float *mu, const float *sigma,
                        hipStream_t st);
 hipError_t launch_mem_poly_fwd(const Graph &g, const Work &w, const PolyArgs &pa, const float *mu,
+                               hipStream_t st);
+hipError_t launch_mem_poly_bwd(const Graph &g, const Work &w, const PolyArgs &pa, const float *mu,
                                hipStream_t st);
 hipError_t launch_lse_poly(const Graph &g, const Work &w, const PolyArgs &pa, const float *mu,
                            const float *sigma, hipStream_t st);

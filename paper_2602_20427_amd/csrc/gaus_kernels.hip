@@ -506,8 +506,13 @@ __global__ __launch_bounds__(256) void k_gather_big(Graph G, Work W, HP hp) {
                 for (int c = 0; c < 4; ++c) acc[c] += cp[tl * kCP + c];
         }
         if (hp.gamma != 0.0f) {
-            const float *sp = W.msucc + ((size_t)b * G.E + e) * nt * 2;
-            for (int tl = 0; tl < nt; ++tl) { acc[4] += sp[tl * 2 + 0]; acc[5] += sp[tl * 2 + 1]; }
+            if (W.mpoly[(size_t)b * N + G.pred_src[q]]) {   // producer's storage term on the polynomials
+                acc[4] += W.mspoly[((size_t)b * G.E + e) * 2 + 0];
+                acc[5] += W.mspoly[((size_t)b * G.E + e) * 2 + 1];
+            } else {
+                const float *sp = W.msucc + ((size_t)b * G.E + e) * nt * 2;
+                for (int tl = 0; tl < nt; ++tl) { acc[4] += sp[tl * 2 + 0]; acc[5] += sp[tl * 2 + 1]; }
+            }
         }
     }
 #pragma unroll
@@ -610,13 +615,22 @@ __global__ __launch_bounds__(256) void k_final(Graph G, Work W, HP hp, const flo
     }
     if (hp.gamma != 0.0f) {   // smooth peak storage, already weighted by gamma
         double om = 0.0, os = 0.0;
-        const float *op = W.mown + bi * nt * 2;
-        if (G.row_ptr[i + 1] > G.row_ptr[i])
+        if (W.mpoly[bi]) {   // holder on the polynomials
+            om += W.mopoly[bi * 2 + 0]; os += W.mopoly[bi * 2 + 1];
+        } else if (G.row_ptr[i + 1] > G.row_ptr[i]) {
+            const float *op = W.mown + bi * nt * 2;
             for (int tl = 0; tl < nt; ++tl) { om += op[tl * 2 + 0]; os += op[tl * 2 + 1]; }
+        }
         if (bsum) { om += bsum[4]; os += bsum[5]; }
         for (int q = bsum ? G.pred_ptr[i + 1] : G.pred_ptr[i]; q < G.pred_ptr[i + 1]; ++q) {
-            const float *sp = W.msucc + ((size_t)b * G.E + G.pred_eid[q]) * nt * 2;
-            for (int tl = 0; tl < nt; ++tl) { om += sp[tl * 2 + 0]; os += sp[tl * 2 + 1]; }
+            const int e = G.pred_eid[q];
+            if (W.mpoly[(size_t)b * N + G.pred_src[q]]) {
+                om += W.mspoly[((size_t)b * G.E + e) * 2 + 0];
+                os += W.mspoly[((size_t)b * G.E + e) * 2 + 1];
+            } else {
+                const float *sp = W.msucc + ((size_t)b * G.E + e) * nt * 2;
+                for (int tl = 0; tl < nt; ++tl) { om += sp[tl * 2 + 0]; os += sp[tl * 2 + 1]; }
+            }
         }
         g_mu = __fadd_rn(g_mu, (float)om);
         g_sg = __fadd_rn(g_sg, (float)os);
@@ -1008,7 +1022,10 @@ hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const 
         if ((e = launch_lse_ops(g, w, lc, a.mu, a.sigma, st)) != hipSuccess) return e;
         if (pa.enabled && (e = launch_lse_poly(g, w, pa, a.mu, a.sigma, st)) != hipSuccess) return e;
     }
-    if (hp.gamma != 0.0f && (e = launch_mem_bwd(g, w, lc, a.mu, a.sigma, st)) != hipSuccess) return e;
+    if (hp.gamma != 0.0f) {
+        if ((e = launch_mem_bwd(g, w, lc, a.mu, a.sigma, st)) != hipSuccess) return e;
+        if (pa.enabled && (e = launch_mem_poly_bwd(g, w, pa, a.mu, st)) != hipSuccess) return e;
+    }
     if (g.nbig > 0) hipLaunchKernelGGL(k_gather_big, dim3(g.nbig, g.B), dim3(256), 0, st, g, w, hp);
     {
         dim3 grid((g.N + 255) / 256, g.B);

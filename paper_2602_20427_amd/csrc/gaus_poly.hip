@@ -552,6 +552,200 @@ __global__ __launch_bounds__(64 * kPolyWaves) void k_mem_poly_fwd(Graph G, PolyA
 }
 
 
+// Chunk moments of the storage softmax c(t) = gamma dL_mem/dMReg(t mod T) at
+// the bin edges: mmom[c][n] = sum_y c(t_mid + y) y^n.  Work-group per (chunk,
+// restart).
+__global__ __launch_bounds__(256) void k_mem_mom(Graph G, PolyArgs pa, Work W) {
+    __shared__ float sRed[4][kNC];
+    const int c = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+    const int lane = tid & 63, wid = tid >> 6;
+    const float *ms = W.msoft + (size_t)b * G.T;
+    float mom[kNC];
+#pragma unroll
+    for (int n = 0; n < kNC; ++n) mom[n] = 0.0f;
+    if (tid < pa.W) {
+        const int t = pa.L0 + c * pa.W + tid;
+        const float y = (float)tid - pa.lam;
+        float yp = ms[t % G.T];
+#pragma unroll
+        for (int n = 0; n < kNC; ++n) { mom[n] = yp; yp *= y; }
+    }
+#pragma unroll
+    for (int n = 0; n < kNC; ++n) {
+        const float r = wave_sum(mom[n]);
+        if (lane == 0) sRed[wid][n] = r;
+    }
+    __syncthreads();
+    if (tid < kNC)
+        W.mmom[((size_t)b * kMaxChunks + c) * kNC + tid] = (sRed[0][tid] + sRed[1][tid]) + (sRed[2][tid] + sRed[3][tid]);
+}
+
+// Gradient of gamma L_mem for the polynomial holders, c(t) as above:
+//   holder h:      sum_t c(t) b_h R_h(t) dF_h(t)
+//   successor j:  -sum_t c(t) b_h F_h(t) prod_{k != j} F_k(t) dF_j(t)
+// (dF = dF/dmu or dF/dsigma).  Chunks: the products as truncated series,
+// dotted with the chunk moments; strip: step by step.  DEG successors.
+template <int DEG, int NP>
+__device__ __forceinline__ void mem_poly_holder(const Graph &G, const PolyArgs &pa, const Work &W, int b, int h,
+                                                int e0, const float *mub, const float *rsb, const float *ms,
+                                                const float (&cm)[kNC], bool cact, float tcen, int lane) {
+    const int SP = pa.SP, L0 = pa.L0, D = G.D, T = G.T;
+    const float m_h = mub[h], rs_h = rsb[h], bh = G.bmem[h];
+    const float cinv_h = rs_h * kInvSqrt2Pi;
+    float mj[DEG], rj[DEG];
+#pragma unroll
+    for (int q = 0; q < DEG; ++q) {
+        const int j = G.col[e0 + q];
+        mj[q] = mub[j]; rj[q] = rsb[j];
+    }
+    float own[2] = {0.0f, 0.0f}, sc[DEG][2];
+#pragma unroll
+    for (int q = 0; q < DEG; ++q) { sc[q][0] = 0.0f; sc[q][1] = 0.0f; }
+    // strip, step by step
+#pragma unroll
+    for (int ps = 0; ps < NP; ++ps) {
+        const int p = ps * 64 + lane;
+        if (p < SP) {
+            const int u = p < L0 ? p : D - 2 + (p - L0);
+            const float c = u <= D - 2 ? ms[u % T] : 0.0f;
+            float st, Fm, Fs;
+            cdf_at(u, D, m_h, rs_h, cinv_h, st, Fm, Fs);
+            const float Fh = st_F(st);
+            float F[DEG], Fmj[DEG], Fsj[DEG];
+            float Q = 1.0f, R = 0.0f;
+#pragma unroll
+            for (int q = 0; q < DEG; ++q) {
+                float sj;
+                cdf_at(u, D, mj[q], rj[q], rj[q] * kInvSqrt2Pi, sj, Fmj[q], Fsj[q]);
+                F[q] = st_F(sj);
+                R = fmaf(Q, st_1mF(sj), R);
+                Q *= F[q];
+            }
+            const float wr = c * bh * R;
+            own[0] = fmaf(wr, Fm, own[0]);
+            own[1] = fmaf(wr, Fs, own[1]);
+            const float wf = -c * bh * Fh;
+#pragma unroll
+            for (int q = 0; q < DEG; ++q) {
+                float others = 1.0f;
+#pragma unroll
+                for (int k = 0; k < DEG; ++k) others *= (k == q) ? 1.0f : F[k];
+                sc[q][0] = fmaf(wf * others, Fmj[q], sc[q][0]);
+                sc[q][1] = fmaf(wf * others, Fsj[q], sc[q][1]);
+            }
+        }
+    }
+    // chunks
+    if (cact) {
+        Expansion<kNC, kNC + 1> eh;
+        expand(m_h, rs_h, tcen, eh);
+        float T_[DEG][kNC + 1], G0[DEG], Z0[DEG];
+#pragma unroll
+        for (int q = 0; q < DEG; ++q) {
+            Expansion<kNC, kNC + 1> ej;
+            expand(mj[q], rj[q], tcen, ej);
+#pragma unroll
+            for (int k = 0; k <= kNC; ++k) T_[q][k] = ej.T[k];
+            G0[q] = ej.G0; Z0[q] = ej.z0;
+        }
+        // R = 1 - prod F_j (from the precise tails), own gradient
+        float Q[kNC], R[kNC], t[kNC];
+#pragma unroll
+        for (int k = 0; k < kNC; ++k) { Q[k] = k == 0 ? 1.0f : 0.0f; R[k] = 0.0f; }
+#pragma unroll
+        for (int q = 0; q < DEG; ++q) {
+            float omF[kNC], Fq[kNC];
+#pragma unroll
+            for (int k = 0; k < kNC; ++k) { omF[k] = k == 0 ? G0[q] : -T_[q][k]; Fq[k] = T_[q][k]; }
+            poly_mul(Q, omF, t);
+#pragma unroll
+            for (int k = 0; k < kNC; ++k) R[k] += t[k];
+            poly_mul(Q, Fq, t);
+#pragma unroll
+            for (int k = 0; k < kNC; ++k) Q[k] = t[k];
+        }
+        float a[kNC], v[kNC];
+        vec_dFdmu(eh, a);
+        vec_times_z(a, eh.z0, eh.r, v);
+        poly_mul(R, a, t);
+        own[0] += bh * vdot(t, cm);
+        poly_mul(R, v, t);
+        own[1] += bh * vdot(t, cm);
+        // successors: W_q = b_h F_h prod_{k != q} F_k, times dF_q
+        float Fh[kNC];
+#pragma unroll
+        for (int k = 0; k < kNC; ++k) Fh[k] = eh.T[k];
+#pragma unroll
+        for (int q = 0; q < DEG; ++q) {
+            float Wq[kNC];
+#pragma unroll
+            for (int k = 0; k < kNC; ++k) Wq[k] = Fh[k];
+#pragma unroll
+            for (int k = 0; k < DEG; ++k) {
+                if (k == q) continue;
+                float Fk[kNC];
+#pragma unroll
+                for (int n = 0; n < kNC; ++n) Fk[n] = T_[k][n];
+                poly_mul(Wq, Fk, t);
+#pragma unroll
+                for (int n = 0; n < kNC; ++n) Wq[n] = t[n];
+            }
+#pragma unroll
+            for (int k = 0; k < kNC; ++k) a[k] = -(float)(k + 1) * T_[q][k + 1];
+            vec_times_z(a, Z0[q], rj[q], v);
+            poly_mul(Wq, a, t);
+            sc[q][0] -= bh * vdot(t, cm);
+            poly_mul(Wq, v, t);
+            sc[q][1] -= bh * vdot(t, cm);
+        }
+    }
+    const float r = wave_sum2(own[0], own[1], lane);
+    if (lane < 2) W.mopoly[((size_t)b * G.N + h) * 2 + lane] = r;
+#pragma unroll
+    for (int q = 0; q < DEG; ++q) {
+        const float rq = wave_sum2(sc[q][0], sc[q][1], lane);
+        if (lane < 2) W.mspoly[((size_t)b * G.E + e0 + q) * 2 + lane] = rq;
+    }
+}
+
+template <int NP>
+__global__ __launch_bounds__(64 * kPolyWaves) void k_mem_poly_bwd(Graph G, PolyArgs pa, const float *__restrict__ mu,
+                                                                  Work W) {
+    const int split = pa.split;
+    const int grp = blockIdx.x / split, sub = blockIdx.x - grp * split, b = blockIdx.y;
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int N = G.N;
+    const float *mub = mu + (size_t)b * N;
+    const float *rsb = W.rsig + (size_t)b * N;
+    const float *ms = W.msoft + (size_t)b * G.T;
+    const bool cact = lane < pa.nc;
+    const float tcen = (float)(pa.L0 + lane * pa.W) + pa.lam;
+    float cm[kNC];
+    const float *msrc = W.mmom + ((size_t)b * kMaxChunks + lane) * kNC;
+#pragma unroll
+    for (int n = 0; n < kNC; ++n) cm[n] = cact ? msrc[n] : 0.0f;
+    const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
+    const int nj = (q1 - q0 - sub + split - 1) / split;
+    const int nq = (nj - wv + kPolyWaves - 1) / kPolyWaves;
+    int l_i = 0, l_ok = 0;
+    if (lane < nq) {
+        l_i = G.perm[q0 + sub + split * (wv + kPolyWaves * lane)];
+        l_ok = W.mpoly[(size_t)b * N + l_i];
+    }
+    for (int oq = 0; oq < nq; ++oq) {
+        if (!__builtin_amdgcn_readlane(l_ok, oq)) continue;
+        const int h = __builtin_amdgcn_readlane(l_i, oq);
+        const int e0 = G.row_ptr[h], deg = G.row_ptr[h + 1] - e0;   // 1 .. kMemPolyDeg
+        switch (deg) {
+            case 1: mem_poly_holder<1, NP>(G, pa, W, b, h, e0, mub, rsb, ms, cm, cact, tcen, lane); break;
+            case 2: mem_poly_holder<2, NP>(G, pa, W, b, h, e0, mub, rsb, ms, cm, cact, tcen, lane); break;
+            case 3: mem_poly_holder<3, NP>(G, pa, W, b, h, e0, mub, rsb, ms, cm, cact, tcen, lane); break;
+            default: mem_poly_holder<kMemPolyDeg, NP>(G, pa, W, b, h, e0, mub, rsb, ms, cm, cact, tcen, lane); break;
+        }
+    }
+}
+
+
 // ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
@@ -583,6 +777,21 @@ hipError_t launch_mem_poly_fwd(const Graph &g, const Work &w, const PolyArgs &pa
     case 3: hipLaunchKernelGGL(k_mem_poly_fwd<3>, grid, block, 0, st, g, pa, mu, w); break;
     case 4: hipLaunchKernelGGL(k_mem_poly_fwd<4>, grid, block, 0, st, g, pa, mu, w); break;
     case kStripPassesMax: hipLaunchKernelGGL(k_mem_poly_fwd<kStripPassesMax>, grid, block, 0, st, g, pa, mu, w); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipSuccess;
+}
+
+hipError_t launch_mem_poly_bwd(const Graph &g, const Work &w, const PolyArgs &pa, const float *mu,
+                               hipStream_t st) {
+    hipLaunchKernelGGL(k_mem_mom, dim3(pa.nc, g.B), dim3(256), 0, st, g, pa, w);
+    const dim3 grid(g.ngroups * pa.split, g.B), block(64 * kPolyWaves);
+    switch ((pa.SP + 63) / 64) {
+    case 1: hipLaunchKernelGGL(k_mem_poly_bwd<1>, grid, block, 0, st, g, pa, mu, w); break;
+    case 2: hipLaunchKernelGGL(k_mem_poly_bwd<2>, grid, block, 0, st, g, pa, mu, w); break;
+    case 3: hipLaunchKernelGGL(k_mem_poly_bwd<3>, grid, block, 0, st, g, pa, mu, w); break;
+    case 4: hipLaunchKernelGGL(k_mem_poly_bwd<4>, grid, block, 0, st, g, pa, mu, w); break;
+    case kStripPassesMax: hipLaunchKernelGGL(k_mem_poly_bwd<kStripPassesMax>, grid, block, 0, st, g, pa, mu, w); break;
     default: return hipErrorInvalidValue;
     }
     return hipSuccess;

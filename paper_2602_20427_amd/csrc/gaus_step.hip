@@ -450,7 +450,7 @@ __global__ __launch_bounds__(BS) void k_mem_bwd(Graph G, const float *__restrict
     sI[tid] = -1;
     if (q0 + tid < q1) {
         const int i = G.perm[q0 + tid];
-        if (G.row_ptr[i + 1] > G.row_ptr[i]) sI[tid] = i;
+        if (G.row_ptr[i + 1] > G.row_ptr[i] && !W.mpoly[(size_t)b * N + i]) sI[tid] = i;
         sMu[tid] = mub[i];
         sRs[tid] = rsb[i];
     }

@@ -118,6 +118,45 @@ def test_storage_loss_grad(cfg, tau):
     _check_storage(p, mu, sg, lam, hp, cfg)
 
 
+@pytest.mark.parametrize("tau", [1.0, 0.01])
+def test_storage_polynomial_holders(tau):
+    """Holders whose storage term is taken on the chunk polynomials (every
+    successor polynomial, at most 4 of them, rho = ((W-1)/2)/sigma summed over
+    the holder and its successors at most 1/4) beside holders evaluated step
+    by step (more successors, a narrow successor, too large a summed rho):
+    sigmas are drawn around those bounds on a 1024-step horizon."""
+    p = with_storage(make_problem("medium", seed=2), seed=3)
+    B = 2
+    ctx = bd.Context(p, 1, hparams())
+    W = ctx.poly_config()["W"]
+    ctx.close()
+    lam_w = (W - 1) / 2.0
+    rng = np.random.default_rng(21)
+    rho = np.exp(rng.uniform(np.log(0.02), np.log(0.3), size=(B, p.n_ops)))
+    sg = (lam_w / rho).astype(np.float32)
+    mu = rng.uniform(-50, p.D + 50, size=(B, p.n_ops)).astype(np.float32)
+    # the holders the rule puts on the polynomials (a coverage check only)
+    deg = np.diff(p.row_ptr)
+    thr = lam_w / 0.25   # the degree-8 bound rho <= 1/4
+    n_poly = []
+    for b in range(B):
+        poly = (sg[b] >= thr) & (p.delay <= 8)
+        cnt = 0
+        for i in range(p.n_ops):
+            succ = p.col_idx[p.row_ptr[i]:p.row_ptr[i + 1]]
+            if poly[i] and 1 <= deg[i] <= 4 and poly[succ].all() and \
+                    lam_w * (1.0 / sg[b, i] + (1.0 / sg[b, succ]).sum()) <= 0.25:
+                cnt += 1
+        n_poly.append(cnt)
+    holders = int((deg > 0).sum())
+    say(f"  W={W}: polynomial holders {n_poly} of {holders}")
+    assert min(n_poly) > 0.15 * holders and max(n_poly) < 0.85 * holders
+    lam = np.random.default_rng(22).uniform(0.05, 1.0, size=(B, 3)).astype(np.float32)
+    hp = hparams(alpha=0.01, rho=1e-3, tau=tau)
+    hp.gamma_mem = 1.0
+    _check_storage(p, mu, sg, lam, hp, f"polynomial holders tau={tau}")
+
+
 def test_storage_large_full_size():
     """The 50k-op workload with storage units and a sink at full size (B=8,
     D=4096) in bench.py's launch configuration, from the paper's
