@@ -169,8 +169,8 @@ def main():
                     help="weight of the smooth peak storage term (storage units of 1-32 bits per op and a "
                          "sink op are added to the workload); 0 = off")
     ap.add_argument("--family", default="gaussian", choices=["gaussian", "logistic", "laplace", "cauchy"],
-                    help="distribution of the relaxed start times (App. D); non-Gaussian families run "
-                         "every op step by step")
+                    help="distribution of the relaxed start times (App. D); the Laplace law runs every "
+                         "op step by step")
     ap.add_argument("--sigma", type=float, default=0.0,
                     help="replace the initial widths by this sigma (a sharpened state like late iterations: "
                          "ops narrower than the polynomial threshold run step by step); 0 = paper init")

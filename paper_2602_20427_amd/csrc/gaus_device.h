@@ -305,24 +305,62 @@ constexpr float back_coef(int k, int j) {
     return (float)(-(double)(k + j + 1) * binom_d(k + j, j) * ((j & 1) ? -1.0 : 1.0));
 }
 
-template <int NC, int NT>
+// Taylor coefficients in y of F(z0 + r y) for each family (App. D), from one
+// tail/density evaluation at the chunk centre:
+//   Gaussian: the Hermite recursion above;
+//   logistic: F = S(q y + u0), q = r/c, S' = S (1 - S), so with the
+//     coefficients of 1 - F being 1 - T_0 and -T_n,
+//     (n+1) T_{n+1} = q (T_n (1 - 2 T_0) - sum_{k=1}^{n-1} T_k T_{n-k});
+//   Cauchy: F' = 1/(pi (1 + u^2)) = Im(1/(u - i))/pi, whose expansion about
+//     u0 is a geometric series, so T_n = -Im((-w)^n)/(pi n) with
+//     w = q/(u0 - i) = q (u0 + i)/(1 + u0^2).
+// 1 - T_0 is taken from the precise tail (G0), never as 1 - F.
+template <int FAM = 0, int NC, int NT>
 __device__ __forceinline__ void expand(float mu, float rs, float tcen, Expansion<NC, NT> &e) {
+    static_assert(FAM == 0 || FAM == 1 || FAM == 3, "no chunk expansion for this family");
     constexpr int TN = NT;
     e.r = rs;
     e.z0 = (tcen + 0.5f - mu) * rs;
     float tail, g;
-    normal_tail_pdf(e.z0, tail, g);
+    fam_tail_h<FAM>(e.z0, tail, g);
     const bool up = e.z0 >= 0.0f;
     e.T[0] = up ? 1.0f - tail : tail;
     e.G0 = up ? tail : 1.0f - tail;
-    e.T[1] = g * (kInvSqrt2Pi * rs);
-    const float zr = e.z0 * rs, r2 = rs * rs;
-    e.T[2] = (zr * -0.5f) * e.T[1];
+    e.T[1] = g * (fam_k<FAM>() * rs);
+    if constexpr (FAM == 0) {
+        const float zr = e.z0 * rs, r2 = rs * rs;
+        e.T[2] = (zr * -0.5f) * e.T[1];
 #pragma unroll
-    for (int n = 2; n < TN - 1; ++n) {
-        const float c1 = -1.0f / (float)(n + 1);
-        const float c2 = -(float)(n - 1) / (float)(n * (n + 1));
-        e.T[n + 1] = fmaf(zr * c1, e.T[n], (r2 * c2) * e.T[n - 1]);
+        for (int n = 2; n < TN - 1; ++n) {
+            const float c1 = -1.0f / (float)(n + 1);
+            const float c2 = -(float)(n - 1) / (float)(n * (n + 1));
+            e.T[n + 1] = fmaf(zr * c1, e.T[n], (r2 * c2) * e.T[n - 1]);
+        }
+    } else if constexpr (FAM == 1) {
+        const float q = rs * fam_cinv<1>();
+        const float d0 = e.G0 - e.T[0];   // 1 - 2 F(z0)
+#pragma unroll
+        for (int n = 1; n < TN - 1; ++n) {
+            // sum_{k=1}^{n-1} T_k T_{n-k}, each pair once
+            float acc = 0.0f;
+#pragma unroll
+            for (int k = 1; 2 * k < n; ++k) acc = fmaf(e.T[k], e.T[n - k], acc);
+            acc += acc;
+            if (n % 2 == 0) acc = fmaf(e.T[n / 2], e.T[n / 2], acc);
+            e.T[n + 1] = fmaf(e.T[n], d0, -acc) * (q * (1.0f / (float)(n + 1)));
+        }
+    } else {
+        const float q = rs * fam_cinv<3>();
+        const float qh = q * g;                          // g = 1/(1 + u0^2)
+        const float wr = -qh * (e.z0 * fam_cinv<3>()), wi = -qh;   // -w
+        float pr = wr, pim = wi;
+#pragma unroll
+        for (int n = 2; n < TN; ++n) {
+            const float nr = fmaf(pr, wr, -pim * wi);
+            const float ni = fmaf(pr, wi, pim * wr);
+            pr = nr; pim = ni;
+            e.T[n] = -pim * (kInvPi / (float)n);
+        }
     }
 }
 

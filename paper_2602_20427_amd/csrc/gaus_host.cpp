@@ -88,10 +88,34 @@ hipError_t next_events(gaus_ctx *c, IterArgs &a) {
     return hipSuccess;
 }
 
-// Chunk width, strip and constant tables of the polynomial path.
-void setup_poly(int D, int requested, PolyArgs &pa) {
+// Truncation bound of an op's chunk series at degree d and rho = lam/sigma:
+// the error of the density series (degree d-1) over the chunk, relative to
+// the family's peak density.
+//   Gaussian: Taylor remainder with Cramer's bound |He_n(x)| e^(-x^2/4) <=
+//     1.09 sqrt(n!): 1.09 rho^d / sqrt(d!);
+//   logistic: the density 1/(4 cosh^2(u/2)) has double poles at u = +-i pi,
+//     so its n-th coefficient is at most 2 (n+1)/pi^(n+2); with x = rho/sqrt(3)
+//     (rho in u units over pi): 8 (d+1)/pi^2 x^d/(1 - x);
+//   Cauchy: the coefficients of 1/(1 + u^2) are at most 1 in modulus (poles
+//     at +-i), x = rho/sqrt(2 ln 2): x^d/(1 - x).
+double poly_bound(int fam, int d, double rho) {
+    auto fact = [](int n) { double f = 1.0; for (int q = 2; q <= n; ++q) f *= q; return f; };
+    if (fam == 1) {
+        const double x = rho / std::sqrt(3.0);
+        return 8.0 * (d + 1) / (M_PI * M_PI) * std::pow(x, d) / (1.0 - x);
+    }
+    if (fam == 3) {
+        const double x = rho / std::sqrt(2.0 * std::log(2.0));
+        return std::pow(x, d) / (1.0 - x);
+    }
+    return 1.09 * std::pow(rho, d) / std::sqrt(fact(d));
+}
+
+// Chunk width, strip, tier bounds and constant tables of the polynomial path
+// (families with an analytic CDF: Gaussian, logistic, Cauchy).
+void setup_poly(int D, int requested, int fam, PolyArgs &pa) {
     pa = PolyArgs{};
-    if (requested < 0) return;
+    if (requested < 0 || !(fam == 0 || fam == 1 || fam == 3)) return;
     // Chunks tile [L0, D-2) with nc <= 64 chunks (one per lane); the strip
     // [0, L0) u {D-2, D-1} is evaluated step by step in passes of 64 lanes.
     // Take the fewest strip passes, then the smallest W (the lowest sigma
@@ -108,19 +132,31 @@ void setup_poly(int D, int requested, PolyArgs &pa) {
     }
     if (W == 0) return;
     pa.enabled = 1;
+    pa.fam = fam;
     pa.W = W; pa.nc = nc;
     pa.L0 = D - 2 - nc * W;
     pa.SP = pa.L0 + 2;
     const double lam = (W - 1) / 2.0;
     pa.lam = (float)lam;
-    // Tier bounds: the truncated series of dF has relative error at most
-    // about rho^d / sqrt(d!) (Taylor remainder with Cramer's bound on the
-    // Hermite functions); each tier's rho bound matches the degree-8 error at
-    // rho = kRhoMax: rho_d = (kRhoMax^8 sqrt(d!) / sqrt(8!))^(1/d).
+    // Tier bounds: each tier's rho bound gives the family's truncation bound
+    // the value of the Gaussian degree-8 bound at rho = kRhoMax (the Gaussian
+    // in closed form, rho_d = (kRhoMax^8 sqrt(d!) / sqrt(8!))^(1/d); the other
+    // families by bisection of their increasing bounds).
     auto fact = [](int n) { double f = 1.0; for (int q = 2; q <= n; ++q) f *= q; return f; };
+    const double target = poly_bound(0, kDeg, kRhoMax);
     for (int t = 1; t <= kTiers; ++t) {
         const int d = kTierDeg[t];
-        const double rho = std::pow(std::pow((double)kRhoMax, kDeg) * std::sqrt(fact(d) / fact(kDeg)), 1.0 / d);
+        double rho;
+        if (fam == 0) {
+            rho = std::pow(std::pow((double)kRhoMax, kDeg) * std::sqrt(fact(d) / fact(kDeg)), 1.0 / d);
+        } else {
+            double lo = 0.0, hi = kRhoMax;
+            for (int it = 0; it < 200; ++it) {
+                const double m = 0.5 * (lo + hi);
+                (poly_bound(fam, d, m) <= target ? lo : hi) = m;
+            }
+            rho = lo;
+        }
         pa.sig_thr[t] = (float)(lam / rho);
     }
     pa.sig_thr[0] = pa.sig_thr[1];
@@ -415,9 +451,9 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     int tile = 0, ntiles = 0;
     choose_config(h, B, c->lc, tile, ntiles);
     c->lc.fam = hp.family;
-    // the chunk polynomials are the Gaussian's (the storage term's successor
-    // products are evaluated step by step by their own kernels in any case)
-    setup_poly(h.D, hp.family != 0 ? -1 : hp.poly_chunk, c->pa);
+    // the chunk polynomials take the Gaussian, logistic and Cauchy laws; the
+    // Laplace CDF has a kink at the median (no series over a chunk there)
+    setup_poly(h.D, hp.poly_chunk, hp.family, c->pa);
 
     Graph &g = c->g;
     g.N = h.N; g.E = h.E; g.K = h.K; g.D = h.D; g.II = h.II; g.T = h.II > 0 ? h.II : h.D;

@@ -44,6 +44,7 @@ constexpr float kMemRhoMax = 0.25f;
 
 struct PolyArgs {
     int enabled;          // 0: every op takes the per-step path
+    int fam;              // CDF family (HP::family): 0 Gaussian, 1 logistic, 3 Cauchy on this path
     int W, nc, L0;        // chunk width, chunks, left strip [0, L0); chunks cover [L0, D-2)
     int SP;               // strip positions: [0, L0) and {D-2, D-1}
     int split;            // work-groups per op group in the polynomial kernel

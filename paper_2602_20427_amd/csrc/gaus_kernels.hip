@@ -31,15 +31,19 @@ namespace gaus {
 // T_n = Phi^(n)(z0) r^n / n!, which obey
 //   T_1 = phi(z0) r,
 //   T_{n+1} = -(z0 r/(n+1)) T_n - ((n-1) r^2/(n(n+1))) T_{n-1}
-// (the Hermite recursion of the derivatives of phi, scaled).  From one set of
-// T's follow, with constant integer coefficients (one step = 1 in y):
+// (the Hermite recursion of the derivatives of phi, scaled).  The logistic
+// and Cauchy laws of App. D have recursions of their own (expand in the
+// device header); everything below uses only the T's and holds for any
+// location-scale family.  From one set of T's follow, with constant integer
+// coefficients (one step = 1 in y):
 //   F:         f_k = T_k
 //   dF/dmu:    a_k = -(k+1) T_{k+1}
 //   dF/dsigma: e_k = z0 a_k + r a_{k-1}           (dF/dsigma = z dF/dmu)
 //   mass F(v) - F(v-1):  m_k = -sum_{j>=1} C(k+j,j) (-1)^j T_{k+j}
 //   dF/dmu at v-1:       a1_k = -sum_{j>=0} (k+j+1) C(k+j,j) (-1)^j T_{k+1+j}
-// The series converge like powers of rho = lam r; with rho <= kRhoMax the
-// truncation error is ~1e-10.  Every sum over the chunk's steps of a product
+// The series converge like powers of rho = lam r; each family's tier bounds
+// (set on the host) keep the truncation error of the density series below
+// ~8e-8 of the peak density.  Every sum over the chunk's steps of a product
 // p(u) q(u) equals sum_k (H p)_k q_k with the chunk moments H_n = sum_y y^n,
 // so an edge costs 10 dot products of length kNC.
 // The strip [0, L0) u {D-2, D-1} (boundary conventions of the open end bins,
@@ -64,7 +68,7 @@ __device__ __forceinline__ int poly_tier(const PolyArgs &pa, float s, int delay)
 //     work in it.
 // The consumers' tiers are recomputed here from their sigmas.  With the
 // storage term on, also whether a holder's storage term is taken on the
-// chunk polynomials (kMemPolyDeg, kMemRhoMax).
+// chunk polynomials (Gaussian start times only; kMemPolyDeg, kMemRhoMax).
 __global__ __launch_bounds__(256) void k_flags(Graph G, PolyArgs pa, const float *__restrict__ sigma, Work W,
                                                int mem_on) {
     const int grp = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
@@ -91,8 +95,8 @@ __global__ __launch_bounds__(256) void k_flags(Graph G, PolyArgs pa, const float
             if (mem_on) rsum += 1.0f / sj;
         }
         W.dflag[bi] = (unsigned char)d;
-        W.mpoly[bi] = (unsigned char)(mem_on && ci != 0 && d == 0 && e1 > e0 && e1 - e0 <= kMemPolyDeg &&
-                                      pa.lam * rsum <= kMemRhoMax);
+        W.mpoly[bi] = (unsigned char)(mem_on && pa.fam == 0 && ci != 0 && d == 0 && e1 > e0 &&
+                                      e1 - e0 <= kMemPolyDeg && pa.lam * rsum <= kMemRhoMax);
         W.ptier[bi] = (unsigned char)t;
         narrow = (t == 1 || t == 2) ? 1 : 0;
     }

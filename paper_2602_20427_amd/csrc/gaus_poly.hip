@@ -34,7 +34,7 @@ constexpr int kStripPad = kSmax; // zero slots before position 0 (positions -kSm
 // exit at once.
 constexpr int kPolyWide = 3, kPolyNarrow = 12;
 
-template <int NP, int TIERS>
+template <int NP, int TIERS, int FAM>
 __global__ __launch_bounds__(64 * kPolyWaves) __attribute__((amdgpu_waves_per_eu(TIERS == kPolyWide && NP == 1 ? 4 : 3)))
 void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__restrict__ sigma, Work W) {
     constexpr bool kFirst = TIERS == kPolyWide;
@@ -106,7 +106,7 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
         float *pp = W.ppoly + ((size_t)b * N + i) * kPP;
         const float m_i = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, l_mu), oq));
         const float rs = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, l_sg), oq));
-        const float cinv = rs * kInvSqrt2Pi;
+        const float cinv = rs * fam_k<FAM>();
         const int s = __builtin_amdgcn_readlane(l_s, oq);
         const int e0 = __builtin_amdgcn_readlane(l_e0, oq), e1 = __builtin_amdgcn_readlane(l_e1, oq);
         float pr[kPP] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
@@ -124,7 +124,7 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
                 const bool last = p == SP - 1;   // position D-1: evaluates D-3
                 const int u = p < L0 ? p : D - 2 + (p - L0);
                 float st, Fm, Fs;
-                cdf_at(last ? D - 3 : u, D, m_i, rs, cinv, st, Fm, Fs);
+                cdf_at<FAM>(last ? D - 3 : u, D, m_i, rs, cinv, st, Fm, Fs);
                 if (last) { rSt[SP] = st; st = -0.0f; Fm = 0.0f; Fs = 0.0f; }
                 rSt[p] = st; rFm[p] = Fm; rFs[p] = Fs;
             }
@@ -132,7 +132,7 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
         if (lane < 4) {   // D-2-s, D-1-s, D-s (upper shifted positions) and L0
             const int v = lane < 3 ? D - 2 - s + lane : L0;
             float st, Fm, Fs;
-            cdf_at(v, D, m_i, rs, cinv, st, Fm, Fs);
+            cdf_at<FAM>(v, D, m_i, rs, cinv, st, Fm, Fs);
             rSt[SP + 1 + lane] = st; rFm[SP + 1 + lane] = Fm; rFs[SP + 1 + lane] = Fs;
         }
         __builtin_amdgcn_wave_barrier();
@@ -166,7 +166,7 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
         float HF[NC], HFm[NC], HFs[NC], HA[NC], HFm1[NC], HFs1[NC];
         {
             Expansion<NC> ea;
-            expand(m_i, rs, tcen, ea);
+            expand<FAM>(m_i, rs, tcen, ea);
             float v[NC], w[NC];
             vec_mass(ea, v);
 #pragma unroll
@@ -180,7 +180,7 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
             vec_moments(w, pa, HFs);
             // shifted functions: A(u) = mass at u-s+1, dF(u-s)
             Expansion<NC> es;
-            if (s != 1) expand(m_i, rs, tcen - (float)(s - 1), es);
+            if (s != 1) expand<FAM>(m_i, rs, tcen - (float)(s - 1), es);
             const Expansion<NC> &ex = (s != 1) ? es : ea;
             vec_mass(ex, v);
             vec_moments(v, pa, HA);
@@ -204,7 +204,7 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
             if (!__builtin_amdgcn_readlane(x_ok, eb)) continue;  // step-by-step edge, done by k_ops
             const float m_j = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x_mu), eb));
             const float rsj = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x_sg), eb));
-            const float cj = rsj * kInvSqrt2Pi;
+            const float cj = rsj * fam_k<FAM>();
             float cc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
             // the consumer's CDF per strip position (D-1's lane evaluates D-3)
             float xst[NP], xFm[NP], xFs[NP];
@@ -214,7 +214,7 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
                 if (p < SP) {
                     const bool last = p == SP - 1;
                     const int u = p < L0 ? p : D - 2 + (p - L0);
-                    cdf_at(last ? D - 3 : u, D, m_j, rsj, cj, xst[ps], xFm[ps], xFs[ps]);
+                    cdf_at<FAM>(last ? D - 3 : u, D, m_j, rsj, cj, xst[ps], xFm[ps], xFs[ps]);
                     if (last) { rSt[SP] = xst[ps]; xst[ps] = -0.0f; xFm[ps] = 0.0f; xFs[ps] = 0.0f; }
                     rSt[p] = xst[ps];
                 }
@@ -245,7 +245,7 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
             }
             if (cact) {
                 Expansion<NC> ej;
-                expand(m_j, rsj, tcen, ej);
+                expand<FAM>(m_j, rsj, tcen, ej);
                 float a[NC], v[NC];
                 pr[0] += vdot_F(HA, ej);
                 pr[1] += vdot_1mF(HF, ej);
@@ -362,7 +362,7 @@ __global__ __launch_bounds__(256) void k_lse_mom(Graph G, PolyArgs pa, Work W) {
 }
 
 
-template <int NP>
+template <int NP, int FAM>
 __global__ __launch_bounds__(64 * kPolyWaves) void k_lse_poly(Graph G, PolyArgs pa, const float *__restrict__ mu,
                                                               const float *__restrict__ sigma, Work W) {
     const int SP = pa.SP, split = pa.split;
@@ -401,7 +401,7 @@ __global__ __launch_bounds__(64 * kPolyWaves) void k_lse_poly(Graph G, PolyArgs 
         const int i = __builtin_amdgcn_readlane(l_i, oq);
         const float m_i = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, l_mu), oq));
         const float rs = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, l_sg), oq));
-        const float cinv = rs * kInvSqrt2Pi;
+        const float cinv = rs * fam_k<FAM>();
         float gm = 0.0f, gs = 0.0f;
 #pragma unroll
         for (int ps = 0; ps < NP; ++ps) {
@@ -409,7 +409,7 @@ __global__ __launch_bounds__(64 * kPolyWaves) void k_lse_poly(Graph G, PolyArgs 
             if (p < SP) {
                 const int u = p < pa.L0 ? p : D - 2 + (p - pa.L0);
                 const float z = ((float)u + 0.5f - m_i) * rs;
-                const float Fm = -__builtin_amdgcn_exp2f(-(z * z) * kHalfLog2e) * cinv;
+                const float Fm = -fam_h<FAM>(z) * cinv;
                 gm = fmaf(sw[ps], Fm, gm);
                 gs = fmaf(sw[ps], Fm * z, gs);
             }
@@ -418,7 +418,7 @@ __global__ __launch_bounds__(64 * kPolyWaves) void k_lse_poly(Graph G, PolyArgs 
         auto chunk = [&](auto nc_tag) {
             constexpr int NC = decltype(nc_tag)::value;
             Expansion<NC, NC + 1> e;
-            expand(m_i, rs, tcen, e);
+            expand<FAM>(m_i, rs, tcen, e);
             float a[NC], v[NC], mm[NC];
             vec_dFdmu(e, a);
             vec_times_z(a, e.z0, e.r, v);
@@ -753,19 +753,28 @@ hipError_t launch_poly(const Graph &g, const Work &w, const PolyArgs &pa, const 
                        hipStream_t st) {
     const size_t lds = sizeof(float) * (size_t)kPolyWaves * (10 * pa.SP + 3 * (kStripPad + kStripExtra));
     const dim3 grid(g.ngroups * pa.split, g.B), block(64 * kPolyWaves);
-#define GAUS_POLY_PAIR(NPV)                                                                       \
-    hipLaunchKernelGGL((k_poly<NPV, kPolyWide>), grid, block, lds, st, g, pa, mu, sigma, w);     \
-    hipLaunchKernelGGL((k_poly<NPV, kPolyNarrow>), grid, block, lds, st, g, pa, mu, sigma, w);
-    switch ((pa.SP + 63) / 64) {
-    case 1: GAUS_POLY_PAIR(1) break;
-    case 2: GAUS_POLY_PAIR(2) break;
-    case 3: GAUS_POLY_PAIR(3) break;
-    case 4: GAUS_POLY_PAIR(4) break;
-    case kStripPassesMax: GAUS_POLY_PAIR(kStripPassesMax) break;
+    auto pair = [&](auto fam_tag) -> hipError_t {
+        constexpr int FAM = decltype(fam_tag)::value;
+#define GAUS_POLY_PAIR(NPV)                                                                            \
+        hipLaunchKernelGGL((k_poly<NPV, kPolyWide, FAM>), grid, block, lds, st, g, pa, mu, sigma, w);   \
+        hipLaunchKernelGGL((k_poly<NPV, kPolyNarrow, FAM>), grid, block, lds, st, g, pa, mu, sigma, w);
+        switch ((pa.SP + 63) / 64) {
+        case 1: GAUS_POLY_PAIR(1) break;
+        case 2: GAUS_POLY_PAIR(2) break;
+        case 3: GAUS_POLY_PAIR(3) break;
+        case 4: GAUS_POLY_PAIR(4) break;
+        case kStripPassesMax: GAUS_POLY_PAIR(kStripPassesMax) break;
+        default: return hipErrorInvalidValue;
+        }
+#undef GAUS_POLY_PAIR
+        return hipSuccess;
+    };
+    switch (pa.fam) {
+    case 0: return pair(std::integral_constant<int, 0>{});
+    case 1: return pair(std::integral_constant<int, 1>{});
+    case 3: return pair(std::integral_constant<int, 3>{});
     default: return hipErrorInvalidValue;
     }
-#undef GAUS_POLY_PAIR
-    return hipSuccess;
 }
 
 hipError_t launch_mem_poly_fwd(const Graph &g, const Work &w, const PolyArgs &pa, const float *mu,
@@ -801,15 +810,25 @@ hipError_t launch_lse_poly(const Graph &g, const Work &w, const PolyArgs &pa, co
                            const float *sigma, hipStream_t st) {
     hipLaunchKernelGGL(k_lse_mom, dim3(pa.nc + 1, g.K, g.B), dim3(256), 0, st, g, pa, w);
     const dim3 grid(g.ngroups * pa.split, g.B), block(64 * kPolyWaves);
-    switch ((pa.SP + 63) / 64) {
-    case 1: hipLaunchKernelGGL(k_lse_poly<1>, grid, block, 0, st, g, pa, mu, sigma, w); break;
-    case 2: hipLaunchKernelGGL(k_lse_poly<2>, grid, block, 0, st, g, pa, mu, sigma, w); break;
-    case 3: hipLaunchKernelGGL(k_lse_poly<3>, grid, block, 0, st, g, pa, mu, sigma, w); break;
-    case 4: hipLaunchKernelGGL(k_lse_poly<4>, grid, block, 0, st, g, pa, mu, sigma, w); break;
-    case kStripPassesMax: hipLaunchKernelGGL(k_lse_poly<kStripPassesMax>, grid, block, 0, st, g, pa, mu, sigma, w); break;
+    auto run = [&](auto fam_tag) -> hipError_t {
+        constexpr int FAM = decltype(fam_tag)::value;
+        switch ((pa.SP + 63) / 64) {
+        case 1: hipLaunchKernelGGL((k_lse_poly<1, FAM>), grid, block, 0, st, g, pa, mu, sigma, w); break;
+        case 2: hipLaunchKernelGGL((k_lse_poly<2, FAM>), grid, block, 0, st, g, pa, mu, sigma, w); break;
+        case 3: hipLaunchKernelGGL((k_lse_poly<3, FAM>), grid, block, 0, st, g, pa, mu, sigma, w); break;
+        case 4: hipLaunchKernelGGL((k_lse_poly<4, FAM>), grid, block, 0, st, g, pa, mu, sigma, w); break;
+        case kStripPassesMax:
+            hipLaunchKernelGGL((k_lse_poly<kStripPassesMax, FAM>), grid, block, 0, st, g, pa, mu, sigma, w); break;
+        default: return hipErrorInvalidValue;
+        }
+        return hipSuccess;
+    };
+    switch (pa.fam) {
+    case 0: return run(std::integral_constant<int, 0>{});
+    case 1: return run(std::integral_constant<int, 1>{});
+    case 3: return run(std::integral_constant<int, 3>{});
     default: return hipErrorInvalidValue;
     }
-    return hipSuccess;
 }
 
 }  // namespace gaus

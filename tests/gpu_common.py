@@ -69,3 +69,36 @@ def compare_restart(g, o_terms, o_U, o_gm, o_gs, b, what=""):
         assert e <= TOL, f"{what} b={b} {name} normwise err {e} (scale {scale})"
         res[name] = float(e)
     return res
+
+
+# Tier bounds of the chunk-polynomial path (restated from the library's
+# rule): the truncation bound of an op's series at degree d and
+# rho = ((W-1)/2)/sigma, per family, and the sigma at which each degree
+# starts (the bound equals the Gaussian degree-8 bound at rho = 1/4).
+POLY_DEGREES = (8, 6, 5)
+
+
+def poly_bound(family, d, rho):
+    import math
+    if family == "logistic":
+        x = rho / math.sqrt(3.0)
+        return 8.0 * (d + 1) / math.pi ** 2 * x ** d / (1.0 - x)
+    if family == "cauchy":
+        x = rho / math.sqrt(2.0 * math.log(2.0))
+        return x ** d / (1.0 - x)
+    return 1.09 * rho ** d / math.sqrt(math.factorial(d))
+
+
+def poly_rho(family, d):
+    target = poly_bound("gaussian", 8, 0.25)
+    lo, hi = 0.0, 0.25
+    for _ in range(200):
+        m = 0.5 * (lo + hi)
+        lo, hi = (m, hi) if poly_bound(family, d, m) <= target else (lo, m)
+    return lo
+
+
+def poly_sigma_thresholds(family, W):
+    """{degree: smallest sigma that takes it} for chunk width W."""
+    lam = (W - 1) / 2.0
+    return {d: lam / poly_rho(family, d) for d in POLY_DEGREES}

@@ -10,7 +10,7 @@ import oracle
 from paper_2602_20427_amd import binding as bd
 from paper_2602_20427_amd.workloads import (CONFIGS, make_problem, random_state, restart_uniforms, uniform_state,
                                             with_storage)
-from tests.gpu_common import TOL, compare_restart, gpu_loss_grad, hparams, say
+from tests.gpu_common import TOL, compare_restart, gpu_loss_grad, hparams, poly_sigma_thresholds, say
 
 pytestmark = pytest.mark.gpu
 
@@ -94,14 +94,46 @@ def test_family_loss_grad_initial_state(family, cfg):
 
 
 @pytest.mark.parametrize("family", FAMS)
-def test_family_disables_polynomial_path(family):
+def test_family_polynomial_path_switch(family):
+    """The logistic and Cauchy CDFs are analytic and take the chunk
+    polynomials; the Laplace CDF has a kink at the median and runs step by
+    step."""
     p = make_problem("medium", seed=0)
     ctx = bd.Context(p, 1, _hp(family))
     try:
         cfg = ctx.poly_config()
     finally:
         ctx.close()
-    assert not cfg["enabled"], cfg
+    assert cfg["enabled"] == (family != "laplace"), cfg
+
+
+@pytest.mark.parametrize("beta", [0.0, 1.0])
+@pytest.mark.parametrize("family", ["logistic", "cauchy"])
+def test_family_polynomial_degree_tiers(family, beta):
+    """Sigmas straddle the family's tier bounds (degree 8, 6, 5 and the
+    step-by-step path below degree 8's), so edges join ops of different
+    degrees and of both paths; delays 0..8; with the smooth peak usage on,
+    its gradient takes each op's own degree."""
+    from tests.test_gpu_parity import _ragged_problem
+    p = _ragged_problem(177, N=1500, D=3000, big_delay=False)
+    p.delay[:] = np.random.default_rng(178).integers(0, 9, size=p.n_ops).astype(np.int32)
+    ctx = bd.Context(p, 1, _hp(family))
+    W = ctx.poly_config()["W"]
+    ctx.close()
+    thr = poly_sigma_thresholds(family, W)
+    B = 2
+    rng = np.random.default_rng(179)
+    centres = np.array([thr[8], thr[8], thr[6], thr[6], thr[5], thr[5], 3 * thr[5]])
+    pick = rng.integers(0, len(centres), size=(B, p.n_ops))
+    sg = (centres[pick] * rng.uniform(0.97, 1.03, size=(B, p.n_ops))).astype(np.float32)
+    mu = rng.uniform(-100, p.D + 100, size=(B, p.n_ops)).astype(np.float32)
+    for d, lo, hi in ((0, 0, thr[8]), (8, thr[8], thr[6]), (6, thr[6], thr[5]), (5, thr[5], np.inf)):
+        share = np.mean((sg >= lo) & (sg < hi))
+        say(f"  {family} W={W}: degree {d} for sigma in [{lo:.1f}, {hi:.1f}): {share:.2f} of the ops")
+        assert share > 0.05
+    lam = np.random.default_rng(180).uniform(0.05, 1.0, size=(B, 3)).astype(np.float32)
+    hp = _hp(family, alpha=0.2, rho=0.01, beta=beta, tau=0.1)
+    _compare(p, mu, sg, lam, hp, family, f"tiers/{family} beta={beta:g}", beta=beta, tau=0.1)
 
 
 @pytest.mark.parametrize("family", ["gaussian"] + FAMS)
@@ -130,6 +162,21 @@ def test_family_storage(family, cfg):
     hp.gamma_mem = 1.0
     say(f"[family] {family} {cfg} storage tau=1: N={p.n_ops} D={p.D} II={p.II}")
     _compare(p, mu, sg, lam, hp, family, f"{cfg}-mem/{family}", tau=1.0, gamma=1.0)
+
+
+@pytest.mark.parametrize("family", ["logistic", "cauchy"])
+def test_family_storage_initial_state(family):
+    """Initial state of the 1k-op workload with storage units and a sink: the
+    usage and edge terms of the wide ops run on the chunk polynomials, the
+    storage term of every holder step by step."""
+    p = with_storage(make_problem("small", seed=0), seed=4)
+    B = 4
+    mu, sg = _init_state("small", p, B)
+    lam = np.full((B, 3), 0.2, np.float32)
+    hp = _hp(family, alpha=0.01, rho=1e-3, tau=1.0)
+    hp.gamma_mem = 1.0
+    say(f"[family] {family} small-init storage tau=1: N={p.n_ops} D={p.D}")
+    _compare(p, mu, sg, lam, hp, family, f"small-init-mem/{family}", tau=1.0, gamma=1.0)
 
 
 def test_family_large_full_size():
