@@ -259,6 +259,9 @@ def main():
     ctx.kernel_timing(False)
     census = ctx.poly_census()
     poly_cfg = ctx.poly_config()
+    grids = ctx.poly_grids()
+    for gr, n in zip(grids, ctx.poly_grid_census()):
+        gr["ops"] = n
     step_ms_events = ev[0].elapsed_time(ev[1]) / args.steps
     legalize_ms = ev[1].elapsed_time(ev[2])
     ms_per_step = (t1 - t0) * 1e3 / args.steps
@@ -282,7 +285,8 @@ def main():
         f"legalize {legalize_ms:.3f} ms; " +
         "; ".join(f"{k} {v['ms']:.3f} ms x {v['launches']}" for k, v in kern.items()))
     log(f"[bench] polynomial path: {census['ops']} of {B * N} (restart, op) pairs, "
-        f"{census['edges']} of {B * E} (restart, edge) pairs")
+        f"{census['edges']} of {B * E} (restart, edge) pairs; per grid (P, W, ops): " +
+        ", ".join(f"({g['P']}, {g['W']}, {g['ops']})" for g in grids if g["on"]))
     log(f"[bench] last terms restart 0: L={tt[0, 0]:.6g} V_dep={tt[0, 1]:.6g} V_res={tt[0, 2]:.6g} "
         f"V_rec={tt[0, 3]:.6g} L_com={tt[0, 4]:.6g}; legalize status {status.tolist()}")
 
@@ -315,7 +319,7 @@ def main():
                    "state": "paper initialization" if args.sigma <= 0 else
                             f"paper initialization means, sigma = {args.sigma:g}"},
         "ms_per_iteration_events": step_ms_events, "legalize_ms": legalize_ms,
-        "poly_path": dict(poly_cfg, ops=census["ops"], edges=census["edges"]),
+        "poly_path": dict(poly_cfg, ops=census["ops"], edges=census["edges"], grids=grids),
         "solve": solve_stats,
         "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_TFLOPS,

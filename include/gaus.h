@@ -92,8 +92,9 @@ typedef struct {
     float sigma_min;               /* sigma is clamped to >= sigma_min after each update */
     float kappa;                   /* initial sigma = kappa * (ALAP - ASAP) */
     int32_t poly_chunk;            /* chunk width W of the polynomial evaluation of wide
-                                      Gaussians: 0 = chosen from D, < 0 = off (every op
-                                      evaluated step by step), else W in [16, 256] */
+                                      start-time laws (one restart per wave): 0 = chosen
+                                      from D, < 0 = off (every op evaluated step by step),
+                                      else W in [16, 256] */
     float beta_res;                /* weight of the smooth peak usage L_res in L (>= 0;
                                       1 with alpha_com gives Formulation A, Sec. 4.1) */
     float tau;                     /* its temperature (> 0): L_res = sum_k tau log sum_t
@@ -103,14 +104,22 @@ typedef struct {
                                       1 gives Formulations B and C, Sec. 4.1):
                                       L_mem = tau log sum_t exp(MReg(t)/tau) with MReg the
                                       expected storage units of eq:active folded like the
-                                      usage (App. B.3), evaluated step by step for every op
-                                      (the other terms keep the chunk polynomials). */
+                                      usage (App. B.3).  Holders with at most 4 successors,
+                                      all wide Gaussians, take it on the chunk polynomials,
+                                      the others step by step. */
     int32_t family;                /* distribution of the relaxed start times (App. D):
                                       0 Gaussian, 1 logistic (scale sigma sqrt(3)/pi),
                                       2 Laplace (scale sigma/sqrt(2)), 3 Cauchy (scale
                                       sigma sqrt(2 ln 2)); sigma keeps its meaning as the
-                                      Gaussian-matched width.  Non-Gaussian families are
-                                      evaluated step by step (no chunk polynomials). */
+                                      Gaussian-matched width.  Laplace is evaluated step
+                                      by step (its CDF has a kink at the median); the others
+                                      take the chunk polynomials when wide enough. */
+    int32_t poly_pack;             /* restart packing of the polynomial evaluation: the ops
+                                      of 2 or 4 restarts share a wave on wider chunks when
+                                      all of them (and their consumers) are wide enough.
+                                      0 = on when poly_chunk is 0, > 0 = on, < 0 = off.
+                                      Results agree with the unpacked evaluation to fp32
+                                      rounding; B < 2 leaves it off. */
 } gaus_hparams;
 
 void gaus_default_hparams(gaus_hparams *hp);
@@ -246,8 +255,9 @@ gaus_status gaus_sync(gaus_ctx *ctx);
 /* Problem sizes after preprocessing: N, E, K, D, II, T, n_back, B. */
 gaus_status gaus_get_dims(const gaus_ctx *ctx, int32_t dims[8]);
 
-/* Chunk-polynomial configuration: enabled (0/1), chunk width W, number of
- * chunks, left strip width.  Ops whose sigma >= 2(W-1) and Lat <= 8 use it. */
+/* Chunk-polynomial configuration of grid 0: enabled (0/1), chunk width W,
+ * number of chunks, left strip width.  Ops with Lat <= 8 whose width reaches
+ * the degree-8 bound (sigma >= 2(W-1) for the Gaussian) use the path. */
 gaus_status gaus_get_poly_config(const gaus_ctx *ctx, int32_t cfg[4]);
 
 /* Census of the last iteration's classification (HOST output, [2]):
@@ -256,6 +266,18 @@ gaus_status gaus_get_poly_config(const gaus_ctx *ctx, int32_t cfg[4]);
  * evaluates).  The rest are evaluated step by step.  Synchronizes the stream;
  * zeros before the first iteration. */
 gaus_status gaus_poly_census(gaus_ctx *ctx, int64_t counts[2]);
+
+/* Chunk grids of the polynomial path (HOST output, [3][5]): per grid g
+ * (0: one restart per wave, 1 and 2: packs of 2 and 4 restarts sharing a
+ * wave) its state (0/1), restarts per wave P, chunk width W, number of chunks
+ * and left strip width.  A packed grid takes an op for a whole restart pack
+ * when every restart's width, and that of each consumer, reaches the grid's
+ * degree-8 bound; the coarsest such grid is used. */
+gaus_status gaus_get_poly_grids(const gaus_ctx *ctx, int32_t cfg[15]);
+
+/* Census of the last iteration's grid assignment (HOST output, [3]):
+ * (restart, op) pairs evaluated on grid 0, 1, 2.  Synchronizes the stream. */
+gaus_status gaus_poly_grid_census(gaus_ctx *ctx, int64_t counts[3]);
 
 /* Message of the last failed call on ctx (or of the last failed gaus_init
  * when ctx is NULL).  Never NULL. */

@@ -23,7 +23,8 @@ EXPORTS = ("gaus_default_hparams", "gaus_init", "gaus_bind_state", "gaus_loss_gr
            "gaus_adam_from_grad", "gaus_legalize", "gaus_schedule_cost", "gaus_solve", "gaus_init_state",
            "gaus_asap_alap",
            "gaus_get_usage", "gaus_get_storage", "gaus_kernel_timing", "gaus_kernel_timing_read", "gaus_sync",
-           "gaus_get_dims", "gaus_get_poly_config", "gaus_poly_census", "gaus_last_error", "gaus_status_string",
+           "gaus_get_dims", "gaus_get_poly_config", "gaus_poly_census", "gaus_get_poly_grids",
+           "gaus_poly_grid_census", "gaus_last_error", "gaus_status_string",
            "gaus_destroy")
 
 
@@ -59,7 +60,7 @@ class HParams(C.Structure):
                 ("rho", C.c_float), ("lambda0", C.c_float), ("alpha_com", C.c_float),
                 ("sigma_min", C.c_float), ("kappa", C.c_float), ("poly_chunk", C.c_int32),
                 ("beta_res", C.c_float), ("tau", C.c_float), ("gamma_mem", C.c_float),
-                ("family", C.c_int32)]
+                ("family", C.c_int32), ("poly_pack", C.c_int32)]
 
 # CDF family of the relaxed start times (App. D), the values of HParams.family
 FAMILIES = {"gaussian": 0, "logistic": 1, "laplace": 2, "cauchy": 3}
@@ -101,6 +102,8 @@ def load():
         "gaus_get_dims": ([vp, vp], C.c_int),
         "gaus_get_poly_config": ([vp, vp], C.c_int),
         "gaus_poly_census": ([vp, vp], C.c_int),
+        "gaus_get_poly_grids": ([vp, vp], C.c_int),
+        "gaus_poly_grid_census": ([vp, vp], C.c_int),
         "gaus_last_error": ([vp], C.c_char_p),
         "gaus_status_string": ([C.c_int], C.c_char_p),
         "gaus_destroy": ([vp], None),
@@ -298,6 +301,19 @@ class Context:
         c = np.zeros(2, np.int64)
         self._check(load().gaus_poly_census(self._h, _np_ptr(c)))
         return {"ops": int(c[0]), "edges": int(c[1])}
+
+    def poly_grids(self):
+        """Chunk grids: [{on, P (restarts per wave), W, chunks, L0}] for grids 0, 1, 2."""
+        cfg = np.zeros(15, np.int32)
+        self._check(load().gaus_get_poly_grids(self._h, _np_ptr(cfg)))
+        return [{"on": bool(cfg[5 * g]), "P": int(cfg[5 * g + 1]), "W": int(cfg[5 * g + 2]),
+                 "chunks": int(cfg[5 * g + 3]), "L0": int(cfg[5 * g + 4])} for g in range(3)]
+
+    def poly_grid_census(self):
+        """(restart, op) pairs evaluated on each chunk grid in the last iteration."""
+        c = np.zeros(3, np.int64)
+        self._check(load().gaus_poly_grid_census(self._h, _np_ptr(c)))
+        return [int(x) for x in c]
 
     def sync(self):
         self._check(load().gaus_sync(self._h))

@@ -223,6 +223,46 @@ __device__ __forceinline__ float wave_sum4(float v0, float v1, float v2, float v
     return cross_rows_sum(x);
 }
 
+// Sums over groups of 64/P consecutive lanes (P = 1, 2, 4 restarts per wave):
+// rows of 16 lanes are summed by the DPP steps, then across rows inside the
+// group (ds_swizzle within 32 lanes, ds_bpermute across the halves).
+template <int P>
+__device__ __forceinline__ float group_rows_sum(float x) {
+    if constexpr (P == 1) {
+        return cross_rows_sum(x);
+    } else if constexpr (P == 2) {
+        constexpr int kSwizzleXor16 = 0x1F | (0x10 << 10);
+        return x + __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), kSwizzleXor16));
+    } else {
+        static_assert(P == 4, "groups of 64, 32 or 16 lanes");
+        return x;
+    }
+}
+
+// wave_sum4 per lane group: lane l of a group (l < 4) receives the group's
+// total of value wave4_comp(l).  P = 1 is wave_sum4.
+template <int P>
+__device__ __forceinline__ float group_sum4(float v0, float v1, float v2, float v3, int lane) {
+    const bool b0 = lane & 1, b1 = lane & 2;
+    const float a = (b0 ? v2 : v0) + dpp_mov<kDppXor1>(b0 ? v0 : v2);
+    const float c = (b0 ? v3 : v1) + dpp_mov<kDppXor1>(b0 ? v1 : v3);
+    float x = (b1 ? c : a) + dpp_mov<kDppXor2>(b1 ? a : c);
+    x += dpp_mov<kDppRor4>(x);
+    x += dpp_mov<kDppRor8>(x);
+    return group_rows_sum<P>(x);
+}
+
+// wave_sum2 per lane group: lane l < 2 of a group receives total l.
+template <int P>
+__device__ __forceinline__ float group_sum2(float v0, float v1, int lane) {
+    const bool b0 = lane & 1;
+    float x = (b0 ? v1 : v0) + dpp_mov<kDppXor1>(b0 ? v0 : v1);
+    x += dpp_mov<kDppXor2>(x);
+    x += dpp_mov<kDppRor4>(x);
+    x += dpp_mov<kDppRor8>(x);
+    return group_rows_sum<P>(x);
+}
+
 // Maximum over the 64 lanes; every lane receives it.
 __device__ __forceinline__ float wave_max(float x) {
     x = fmaxf(x, dpp_mov<kDppXor1>(x));
@@ -402,13 +442,13 @@ __device__ __forceinline__ void vec_dFdmu_back(const Expansion<NC> &e, float (&a
 
 // (H p)_k = sum_l H_{k+l} p_l; the chunk points are symmetric, odd moments vanish
 template <int NC>
-__device__ __forceinline__ void vec_moments(const float (&p)[NC], const PolyArgs &pa, float (&o)[NC]) {
+__device__ __forceinline__ void vec_moments(const float (&p)[NC], const float (&H)[kDeg + 1], float (&o)[NC]) {
 #pragma unroll
     for (int k = 0; k < NC; ++k) {
         float acc = 0.0f;
 #pragma unroll
         for (int l = 0; l < NC; ++l)
-            if (((k + l) & 1) == 0) acc = fmaf(pa.H[(k + l) / 2], p[l], acc);
+            if (((k + l) & 1) == 0) acc = fmaf(H[(k + l) / 2], p[l], acc);
         o[k] = acc;
     }
 }

@@ -111,37 +111,19 @@ double poly_bound(int fam, int d, double rho) {
     return 1.09 * std::pow(rho, d) / std::sqrt(fact(d));
 }
 
-// Chunk width, strip, tier bounds and constant tables of the polynomial path
-// (families with an analytic CDF: Gaussian, logistic, Cauchy).
-void setup_poly(int D, int requested, int fam, PolyArgs &pa) {
-    pa = PolyArgs{};
-    if (requested < 0 || !(fam == 0 || fam == 1 || fam == 3)) return;
-    // Chunks tile [L0, D-2) with nc <= 64 chunks (one per lane); the strip
-    // [0, L0) u {D-2, D-1} is evaluated step by step in passes of 64 lanes.
-    // Take the fewest strip passes, then the smallest W (the lowest sigma
-    // threshold 2(W-1) for the polynomial path).
-    int W = 0, nc = 0, best_passes = 1 << 30;
-    for (int w = 16; w <= 256; ++w) {
-        if (requested > 0 && w != requested) continue;
-        const int n = std::min(kMaxChunks, (D - 2 - kSmax) / w);
-        if (n < 4) continue;
-        const int sp = D - 2 - n * w + 2;
-        if (sp > kStripMax) continue;
-        const int passes = (sp + 63) / 64;
-        if (passes < best_passes) { best_passes = passes; W = w; nc = n; }
-    }
-    if (W == 0) return;
-    pa.enabled = 1;
-    pa.fam = fam;
-    pa.W = W; pa.nc = nc;
-    pa.L0 = D - 2 - nc * W;
-    pa.SP = pa.L0 + 2;
+// Tier bounds and moment table of a grid with chunk width W: each tier's rho
+// bound gives the family's truncation bound the value of the Gaussian
+// degree-8 bound at rho = kRhoMax (the Gaussian in closed form,
+// rho_d = (kRhoMax^8 sqrt(d!) / sqrt(8!))^(1/d); the other families by
+// bisection of their increasing bounds).
+void setup_grid(int D, int W, int nc, int fam, GridArgs &gr) {
+    gr = GridArgs{};
+    gr.on = 1;
+    gr.W = W; gr.nc = nc;
+    gr.L0 = D - 2 - nc * W;
+    gr.SP = gr.L0 + 2;
     const double lam = (W - 1) / 2.0;
-    pa.lam = (float)lam;
-    // Tier bounds: each tier's rho bound gives the family's truncation bound
-    // the value of the Gaussian degree-8 bound at rho = kRhoMax (the Gaussian
-    // in closed form, rho_d = (kRhoMax^8 sqrt(d!) / sqrt(8!))^(1/d); the other
-    // families by bisection of their increasing bounds).
+    gr.lam = (float)lam;
     auto fact = [](int n) { double f = 1.0; for (int q = 2; q <= n; ++q) f *= q; return f; };
     const double target = poly_bound(0, kDeg, kRhoMax);
     for (int t = 1; t <= kTiers; ++t) {
@@ -157,13 +139,59 @@ void setup_poly(int D, int requested, int fam, PolyArgs &pa) {
             }
             rho = lo;
         }
-        pa.sig_thr[t] = (float)(lam / rho);
+        gr.sig_thr[t] = (float)(lam / rho);
     }
-    pa.sig_thr[0] = pa.sig_thr[1];
+    gr.sig_thr[0] = gr.sig_thr[1];
     for (int k = 0; k <= kDeg; ++k) {
         double acc = 0.0;
         for (int i = 0; i < W; ++i) acc += std::pow(i - lam, 2 * k);
-        pa.H[k] = (float)acc;   // symmetric points: odd moments vanish
+        gr.H[k] = (float)acc;   // symmetric points: odd moments vanish
+    }
+}
+
+// Chunk grids, strips, tier bounds and constant tables of the polynomial
+// path (families with an analytic CDF: Gaussian, logistic, Cauchy).
+// requested: grid-0 chunk width (0 = chosen here, < 0 = path off);
+// pack: packed grids (0 = when the width is chosen here, > 0 = on, < 0 = off),
+// used only for grids whose restart pack fits B.
+void setup_poly(int D, int requested, int pack, int fam, int B, PolyArgs &pa) {
+    pa = PolyArgs{};
+    if (requested < 0 || !(fam == 0 || fam == 1 || fam == 3)) return;
+    // Grid 0: chunks tile [L0, D-2) with nc <= 64 chunks (one per lane); the
+    // strip [0, L0) u {D-2, D-1} is evaluated step by step in passes of 64
+    // lanes.  Take the fewest strip passes, then the smallest W (the lowest
+    // sigma threshold 2(W-1) for the polynomial path).
+    int W = 0, nc = 0, best_passes = 1 << 30;
+    for (int w = 16; w <= 256; ++w) {
+        if (requested > 0 && w != requested) continue;
+        const int n = std::min(kMaxChunks, (D - 2 - kSmax) / w);
+        if (n < 4) continue;
+        const int sp = D - 2 - n * w + 2;
+        if (sp > kStripMax) continue;
+        const int passes = (sp + 63) / 64;
+        if (passes < best_passes) { best_passes = passes; W = w; nc = n; }
+    }
+    if (W == 0) return;
+    pa.enabled = 1;
+    pa.fam = fam;
+    setup_grid(D, W, nc, fam, pa.gr[0]);
+    pa.W = W; pa.nc = nc; pa.L0 = pa.gr[0].L0; pa.SP = pa.gr[0].SP; pa.lam = pa.gr[0].lam;
+    for (int t = 0; t <= kTiers; ++t) pa.sig_thr[t] = pa.gr[0].sig_thr[t];
+    for (int k = 0; k <= kDeg; ++k) pa.H[k] = pa.gr[0].H[k];
+    // Packed grids: 64/P lanes per restart, at most that many chunks and a
+    // strip of at most that many positions (one pass); the smallest such W
+    // (W <= 256 keeps the degree-16 moments within fp32 range).
+    const bool packing = pack > 0 || (pack == 0 && requested == 0);
+    for (int g = 1; g < kGrids && packing; ++g) {
+        const int P = kGridP[g], L = 64 / P;
+        if (B < P) continue;
+        for (int w = 16; w <= 256; ++w) {
+            const int n = std::min(L, (D - 2 - kSmax) / w);
+            if (n < 4) continue;
+            if (D - 2 - n * w + 2 > L) continue;
+            setup_grid(D, w, n, fam, pa.gr[g]);
+            break;
+        }
     }
 }
 
@@ -402,6 +430,7 @@ void gaus_default_hparams(gaus_hparams *hp) {
     hp->tau = 1e-2f;
     hp->gamma_mem = 0.0f;
     hp->family = 0;
+    hp->poly_pack = 0;
 }
 
 const char *gaus_status_string(gaus_status s) {
@@ -453,7 +482,7 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     c->lc.fam = hp.family;
     // the chunk polynomials take the Gaussian, logistic and Cauchy laws; the
     // Laplace CDF has a kink at the median (no series over a chunk there)
-    setup_poly(h.D, hp.poly_chunk, hp.family, c->pa);
+    setup_poly(h.D, hp.poly_chunk, hp.poly_pack, hp.family, B, c->pa);
 
     Graph &g = c->g;
     g.N = h.N; g.E = h.E; g.K = h.K; g.D = h.D; g.II = h.II; g.T = h.II > 0 ? h.II : h.D;
@@ -465,6 +494,9 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
         int gmax = 1;
         for (int q = 0; q < g.ngroups; ++q) gmax = std::max(gmax, h.grp_start[q + 1] - h.grp_start[q]);
         c->pa.split = std::max(1, std::min(kPolySplitMax, (gmax + 63) / 64));
+        // the packed kernels load each wave's ops on 64/P >= 16 lanes per restart
+        if ((gmax + c->pa.split - 1) / c->pa.split > 64)
+            for (int gi = 1; gi < kGrids; ++gi) c->pa.gr[gi].on = 0;
     }
     g.nlevels = (int)h.lvl_ptr.size() - 1;
     std::vector<float> cap(h.cap);
@@ -532,16 +564,17 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     AL(rsig, BN);
     AL(dflag, BN);
     AL(ptier, BN);
+    AL(ptpk, (size_t)(kGrids - 1) * BN);
     AL(gflag, (size_t)B * g.ngroups);
     AL(gnarrow, (size_t)B * g.ngroups);
     AL(gsum_ops, (size_t)B * g.ngroups * ntiles * 2);
-    AL(gsum_poly, (size_t)B * g.ngroups * c->pa.split * 2);
+    AL(gsum_poly, (size_t)kGrids * B * g.ngroups * c->pa.split * 2);
     AL(vres_part, (size_t)B * h.K);
-    AL(Ucoef_k, (size_t)B * h.K * (kMaxChunks * kNC + kStripMax));
+    AL(Ucoef_k, (size_t)B * h.K * kGrids * (kMaxChunks * kNC + kStripMax));
     AL(ppoly, BN * kPP);
     AL(cpoly, (size_t)B * h.E * kCP);
-    AL(Ucoef, (size_t)B * g.ngroups * c->pa.split * kMaxChunks * kNC);
-    AL(Ustrip, (size_t)B * g.ngroups * c->pa.split * kStripMax);
+    AL(Ucoef, (size_t)kGrids * B * g.ngroups * c->pa.split * kMaxChunks * kNC);
+    AL(Ustrip, (size_t)kGrids * B * g.ngroups * c->pa.split * kStripMax);
     AL(s64, BN);
     AL(s64b, BN);
     AL(status, (size_t)B);
@@ -550,7 +583,8 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
         hipError_t e = hipMemset(c->w.U, 0, sizeof(float) * (size_t)B * h.K * g.T);
         if (e == hipSuccess) e = hipMemset(c->w.ppoly, 0, sizeof(float) * BN * kPP);
         if (e == hipSuccess) e = hipMemset(c->w.cls, 0, BN);
-        if (e == hipSuccess) e = hipMemset(c->w.gsum_poly, 0, sizeof(float) * (size_t)B * g.ngroups * c->pa.split * 2);
+        if (e == hipSuccess) e = hipMemset(c->w.gsum_poly, 0, sizeof(float) * (size_t)kGrids * B * g.ngroups * c->pa.split * 2);
+        if (e == hipSuccess) e = hipMemset(c->w.ptpk, 0, (size_t)(kGrids - 1) * BN);
         if (e == hipSuccess) e = hipDeviceSynchronize();
         if (e != hipSuccess) { s = fail(nullptr, GAUS_E_DEVICE, "init: %s", hipGetErrorString(e)); goto fail_alloc; }
     }
@@ -823,6 +857,46 @@ gaus_status gaus_poly_census(gaus_ctx *ctx, int64_t counts[2]) {
     }
     counts[0] = nop;
     counts[1] = ned;
+    return GAUS_OK;
+}
+
+gaus_status gaus_get_poly_grids(const gaus_ctx *ctx, int32_t cfg[15]) {
+    if (!ctx || !cfg) return GAUS_E_INVALID_ARG;
+    for (int gi = 0; gi < kGrids; ++gi) {
+        const GridArgs &gr = ctx->pa.gr[gi];
+        int32_t *q = cfg + 5 * gi;
+        q[0] = gr.on; q[1] = kGridP[gi]; q[2] = gr.W; q[3] = gr.nc; q[4] = gr.L0;
+    }
+    return GAUS_OK;
+}
+
+gaus_status gaus_poly_grid_census(gaus_ctx *ctx, int64_t counts[3]) {
+    if (!ctx) return GAUS_E_INVALID_ARG;
+    if (!counts) return fail(ctx, GAUS_E_INVALID_ARG, "poly_grid_census: null pointer");
+    const Graph &g = ctx->g;
+    const size_t BN = (size_t)g.B * g.N;
+    hipError_t e = hipStreamSynchronize(ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "poly_grid_census");
+    std::vector<unsigned char> cls(BN), pk((kGrids - 1) * BN);
+    e = hipMemcpy(cls.data(), ctx->w.cls, BN, hipMemcpyDeviceToHost);
+    if (e == hipSuccess) e = hipMemcpy(pk.data(), ctx->w.ptpk, pk.size(), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(ctx, e, "poly_grid_census");
+    for (int gi = 0; gi < kGrids; ++gi) counts[gi] = 0;
+    for (int b = 0; b < g.B; ++b) {
+        for (int i = 0; i < g.N; ++i) {
+            if (!cls[(size_t)b * g.N + i]) continue;
+            int grid = 0;   // the coarsest packed grid whose whole pack qualifies
+            for (int gi = kGrids - 1; gi >= 1 && grid == 0; --gi) {
+                if (!ctx->pa.gr[gi].on) continue;
+                const int P = kGridP[gi], b0 = b - b % P;
+                bool ok = true;
+                for (int q = 0; q < P && b0 + q < g.B; ++q)
+                    ok = ok && pk[((size_t)(gi - 1) * g.B + b0 + q) * g.N + i] != 0;
+                if (ok) grid = gi;
+            }
+            ++counts[grid];
+        }
+    }
     return GAUS_OK;
 }
 

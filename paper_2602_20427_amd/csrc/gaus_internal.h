@@ -42,15 +42,33 @@ constexpr int kStripMax = 320;                 // step-by-step strip positions p
 constexpr int kMemPolyDeg = 4;
 constexpr float kMemRhoMax = 0.25f;
 
+// Chunk grids: grid g gives each restart 64/P_g lanes of a wave, so P_g
+// restarts of one op share a wave (P = 1, 2, 4).  Grid 0 is the per-restart
+// layout every polynomial op can take; the packed grids use wider chunks (at
+// most 64/P each, a strip of at most 64/P positions) and take an op when
+// every restart of its pack, the op and all its consumers are wide enough
+// for the grid's degree-8 bound.
+constexpr int kGrids = 3;
+constexpr int kGridP[kGrids] = {1, 2, 4};
+
+struct GridArgs {
+    int on;               // grid in use
+    int W, nc, L0, SP;    // chunk width, chunks, left strip [0, L0), strip positions [0, L0) u {D-2, D-1}
+    float lam;            // chunk half-width (W-1)/2
+    float sig_thr[kTiers + 1];   // sigma >= sig_thr[t]: tier t on this grid
+    float H[kDeg + 1];    // even moments of a chunk's points
+};
+
 struct PolyArgs {
     int enabled;          // 0: every op takes the per-step path
     int fam;              // CDF family (HP::family): 0 Gaussian, 1 logistic, 3 Cauchy on this path
-    int W, nc, L0;        // chunk width, chunks, left strip [0, L0); chunks cover [L0, D-2)
+    int W, nc, L0;        // grid 0: chunk width, chunks, left strip [0, L0); chunks cover [L0, D-2)
     int SP;               // strip positions: [0, L0) and {D-2, D-1}
     int split;            // work-groups per op group in the polynomial kernel
     float lam;            // chunk half-width (W-1)/2
     float sig_thr[kTiers + 1];   // sigma >= sig_thr[t]: tier t (decreasing degree); [1] = path threshold
     float H[kDeg + 1];    // even moments: H[k] = sum over a chunk's points y of y^(2k)
+    GridArgs gr[kGrids];  // [0] = the fields above; [1], [2] = packed grids
 };
 
 // Device copy of the preprocessed problem (all pointers are device memory).
@@ -127,16 +145,19 @@ struct Work {
     unsigned char *dflag;  // [B][N]        1 = op has step-by-step work (own terms or out-edges)
     unsigned char *ptier;  // [B][N]        polynomial op: tier of its vectors, the smallest over
                            //               itself and its polynomial consumers (highest degree)
+    unsigned char *ptpk;   // [kGrids-1][B][N]  tier of the op's vectors on packed grid 1, 2 if the
+                           //               op and all its consumers meet that grid's degree-8
+                           //               bound, else 0
     int *gflag;       // [B][ngroups]      1 = some op of the group has step-by-step work
     int *gnarrow;     // [B][ngroups]      1 = some op of the group takes polynomial degree 8 or 6
     float *gsum_ops;  // [B][ngroups][ntiles][2]  V_dep, L_com of a k_ops work-group
-    float *gsum_poly; // [B][ngroups*split][2]  V_dep, L_com of a k_poly work-group
+    float *gsum_poly; // [kGrids][B][ngroups*split][2]  V_dep, L_com of a k_poly work-group
     float *vres_part; // [B][K]            V_res of one resource type
-    float *Ucoef_k;   // [B][K][64*kNC + 320]  polynomial usage coefficients and strip values per type
+    float *Ucoef_k;   // [B][K][kGrids][64*kNC + 320]  polynomial usage coefficients and strip values per type
     float *ppoly;     // [B][N][kPP]       producer partials of the polynomial path
     float *cpoly;     // [B][E][kCP]       consumer partials of polynomial edges
-    float *Ucoef;     // [B][ngroups*split][kMaxChunks][kNC]  usage coefficients per chunk
-    float *Ustrip;    // [B][ngroups][SP]  usage at the strip positions
+    float *Ucoef;     // [kGrids][B][ngroups*split][kMaxChunks][kNC]  usage coefficients per chunk
+    float *Ustrip;    // [kGrids][B][ngroups*split][kStripMax]  usage at the strip positions
     long long *s64;   // [B][N]            legalization workspace
     long long *s64b;  // [B][N]            legalization snapshot (back edges)
     int *status;      // [B]               legalization status

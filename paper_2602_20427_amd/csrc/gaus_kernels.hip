@@ -58,6 +58,14 @@ __device__ __forceinline__ int poly_tier(const PolyArgs &pa, float s, int delay)
     return t;
 }
 
+// The same on packed grid g (0 when the grid is off).
+__device__ __forceinline__ int grid_tier(const GridArgs &gr, float s, int delay) {
+    int t = 0;
+    if (gr.on && delay <= kSmax)
+        for (int q = 1; q <= kTiers; ++q) t = s >= gr.sig_thr[q] ? q : t;
+    return t;
+}
+
 // Classification and work flags.  Work-group = (op group, restart), thread
 // per op (groups hold at most 256 ops, and together every op):
 //   * 1/sigma and the op's path (tier) for the other kernels;
@@ -65,7 +73,10 @@ __device__ __forceinline__ int poly_tier(const PolyArgs &pa, float s, int delay)
 //     the polynomial path; of the group: any such op;
 //   * a polynomial producer's tier: the highest degree among itself and its
 //     polynomial consumers; of the group: whether the degree-8/6 kernel has
-//     work in it.
+//     work in it;
+//   * on each packed grid: the same tier if the op and all its consumers
+//     meet the grid's degree-8 bound, else 0 (the kernels then combine the
+//     restarts of a pack).
 // The consumers' tiers are recomputed here from their sigmas.  With the
 // storage term on, also whether a holder's storage term is taken on the
 // chunk polynomials (Gaussian start times only; kMemPolyDeg, kMemRhoMax).
@@ -84,16 +95,28 @@ __global__ __launch_bounds__(256) void k_flags(Graph G, PolyArgs pa, const float
         W.cls[bi] = (unsigned char)ci;
         d = ci ? 0 : 1;
         int t = ci;
+        int tp[kGrids - 1];
+#pragma unroll
+        for (int g = 1; g < kGrids; ++g) tp[g - 1] = grid_tier(pa.gr[g], s, G.delay[i]);
         const int e0 = G.row_ptr[i], e1 = G.row_ptr[i + 1];
         float rsum = 1.0f / s;   // sum of 1/sigma over the holder and its successors
         for (int e = e0; e < e1; ++e) {
             const int j = G.col[e];
             const float sj = sgb[j];
-            const int cj = poly_tier(pa, sj, G.delay[j]);
+            const int dj = G.delay[j];
+            const int cj = poly_tier(pa, sj, dj);
             d |= cj ? 0 : 1;
             t = cj ? min(t, cj) : t;
+#pragma unroll
+            for (int g = 1; g < kGrids; ++g) {
+                const int c = grid_tier(pa.gr[g], sj, dj);
+                tp[g - 1] = c ? min(tp[g - 1], c) : 0;
+            }
             if (mem_on) rsum += 1.0f / sj;
         }
+#pragma unroll
+        for (int g = 1; g < kGrids; ++g)
+            W.ptpk[((size_t)(g - 1) * G.B + b) * G.N + i] = (unsigned char)tp[g - 1];
         W.dflag[bi] = (unsigned char)d;
         W.mpoly[bi] = (unsigned char)(mem_on && pa.fam == 0 && ci != 0 && d == 0 && e1 > e0 &&
                                       e1 - e0 <= kMemPolyDeg && pa.lam * rsum <= kMemRhoMax);
@@ -111,36 +134,38 @@ __global__ __launch_bounds__(256) void k_flags(Graph G, PolyArgs pa, const float
 // ---------------------------------------------------------------------------
 // Usage: U[b][k][slot] = sum over type-k groups and steps t = slot (mod T).
 // ---------------------------------------------------------------------------
-// Polynomial usage per (type, restart): the groups' chunk coefficients and
-// strip values summed over the type's groups (64 entries x 4 group slices per
-// work-group, combined in a fixed order).
-constexpr int kUcEntries = kMaxChunks * kNC + kStripMax;   // per (restart, type)
+// Polynomial usage per (type, restart, grid): the groups' chunk coefficients
+// and strip values summed over the type's groups (64 entries x 16 group
+// slices per work-group, combined in a fixed order).
+constexpr int kUcEntries = kMaxChunks * kNC + kStripMax;   // per (restart, type, grid)
 
 constexpr int kUcoefRows = 16;   // work-group = 64 entries x 16 strided partial sums
 
 __global__ __launch_bounds__(64 * kUcoefRows) void k_ucoef(Graph G, PolyArgs pa, Work W) {
     __shared__ float part[kUcoefRows][64];
     const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-    const int x = blockIdx.x * 64 + tx, k = blockIdx.y, b = blockIdx.z;
+    const int x = blockIdx.x * 64 + tx, k = blockIdx.y, b = blockIdx.z / kGrids, gi = blockIdx.z % kGrids;
+    const GridArgs &gd = pa.gr[gi];
+    if (!gd.on) return;
     // the type's polynomial work-groups: slots [g0*split, g1*split) of restart b
     const int g0 = G.type_grp[k] * pa.split, g1 = G.type_grp[k + 1] * pa.split;
-    const size_t rb = (size_t)b * G.ngroups * pa.split;
-    const int ncoef = pa.nc * kNC;
+    const size_t rb = ((size_t)gi * G.B + b) * G.ngroups * pa.split;
+    const int ncoef = gd.nc * kNC;
     float acc = 0.0f;
     if (x < ncoef) {
 #pragma unroll 4
         for (int g = g0 + ty; g < g1; g += kUcoefRows) acc += W.Ucoef[(rb + g) * kMaxChunks * kNC + x];
-    } else if (x < ncoef + pa.SP) {
+    } else if (x < ncoef + gd.SP) {
 #pragma unroll 4
         for (int g = g0 + ty; g < g1; g += kUcoefRows) acc += W.Ustrip[(rb + g) * kStripMax + (x - ncoef)];
     }
     part[ty][tx] = acc;
     __syncthreads();
-    if (ty == 0 && x < ncoef + pa.SP) {
+    if (ty == 0 && x < ncoef + gd.SP) {
         float t = 0.0f;
 #pragma unroll
         for (int r = 0; r < kUcoefRows; ++r) t += part[r][tx];
-        W.Ucoef_k[((size_t)b * G.K + k) * kUcEntries + x] = t;
+        W.Ucoef_k[(((size_t)b * G.K + k) * kGrids + gi) * kUcEntries + x] = t;
     }
 }
 
@@ -151,7 +176,7 @@ constexpr int kUsageBS = 256;
 
 __global__ __launch_bounds__(kUsageBS) void k_usage(Graph G, PolyArgs pa, Work W) {
     constexpr int kMaxAct = 1024;
-    __shared__ float sC[kUcEntries];
+    __shared__ float sC[kGrids][kUcEntries];
     __shared__ int sAct[kMaxAct];
     __shared__ int wcount[kUsageBS / 64];
     __shared__ int base;
@@ -182,15 +207,16 @@ __global__ __launch_bounds__(kUsageBS) void k_usage(Graph G, PolyArgs pa, Work W
         __syncthreads();
     }
     const int nact = base;   // > kMaxAct: scan the flags instead of the list
-    if (pa.enabled) {
-        const float *src = W.Ucoef_k + ((size_t)b * G.K + k) * kUcEntries;
-        const int n = pa.nc * kNC + pa.SP;
-        for (int x = tid; x < n; x += kUsageBS) sC[x] = src[x];
+    for (int gi = 0; gi < kGrids; ++gi) {
+        const GridArgs &gd = pa.gr[gi];
+        if (!gd.on) continue;
+        const float *src = W.Ucoef_k + (((size_t)b * G.K + k) * kGrids + gi) * kUcEntries;
+        const int n = gd.nc * kNC + gd.SP;
+        for (int x = tid; x < n; x += kUsageBS) sC[gi][x] = src[x];
     }
     __syncthreads();
     const int slot = blockIdx.x * kUsageBS + tid;
     if (slot >= T) return;
-    const int ncoef = pa.nc * kNC;
     // fp64 sums: the softmax of the smooth peak terms amplifies a usage error
     // dU by about dU/tau, so U is formed to well below fp32 rounding of its sum
     double acc = 0.0;
@@ -202,17 +228,19 @@ __global__ __launch_bounds__(kUsageBS) void k_usage(Graph G, PolyArgs pa, Work W
             for (int g = g0; g < g1; ++g)
                 if (W.gflag[(size_t)b * G.ngroups + g]) ut += W.Upart[((size_t)b * G.ngroups + g) * D + t];
         }
-        if (pa.enabled) {
-            if (t >= pa.L0 && t < D - 2) {
-                const int c = (t - pa.L0) / pa.W;
-                const float x = (float)(t - pa.L0 - c * pa.W) - pa.lam;
-                const float *cf = sC + c * kNC;
+        for (int gi = 0; gi < kGrids; ++gi) {
+            const GridArgs &gd = pa.gr[gi];
+            if (!gd.on) continue;
+            if (t >= gd.L0 && t < D - 2) {
+                const int c = (t - gd.L0) / gd.W;
+                const float x = (float)(t - gd.L0 - c * gd.W) - gd.lam;
+                const float *cf = sC[gi] + c * kNC;
                 float v = cf[kNC - 1];
 #pragma unroll
                 for (int q = kNC - 2; q >= 0; --q) v = fmaf(v, x, cf[q]);
                 ut += (double)v;
             } else {
-                ut += (double)sC[ncoef + (t < pa.L0 ? t : pa.L0 + (t - (D - 2)))];
+                ut += (double)sC[gi][gd.nc * kNC + (t < gd.L0 ? t : gd.L0 + (t - (D - 2)))];
             }
         }
         acc += ut;
@@ -426,9 +454,12 @@ __global__ __launch_bounds__(kCombineBS) void k_combine(Graph G, PolyArgs pa, Wo
         lres += W.lres_part[(size_t)b * G.K + k];
     }
     const int npoly = G.ngroups * pa.split;
-    for (int g = tid; g < npoly; g += kCombineBS) {
-        const float *gp = W.gsum_poly + ((size_t)b * npoly + g) * 2;
-        vdep += gp[0]; lcom += gp[1];
+    for (int gi = 0; gi < kGrids; ++gi) {
+        if (!pa.gr[gi].on) continue;
+        for (int g = tid; g < npoly; g += kCombineBS) {
+            const float *gp = W.gsum_poly + (((size_t)gi * G.B + b) * npoly + g) * 2;
+            vdep += gp[0]; lcom += gp[1];
+        }
     }
     for (int g = tid; g < G.ngroups; g += kCombineBS) {
         if (W.gflag[(size_t)b * G.ngroups + g]) {
@@ -1004,9 +1035,13 @@ hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const 
         if (a.poly_end) (void)hipEventRecord(a.poly_end, st);
     }
     if (g.nb > 0 && (e = launch_back(g, w, lc, a.mu, a.sigma, st)) != hipSuccess) return e;
-    if (pa.enabled)
-        hipLaunchKernelGGL(k_ucoef, dim3((pa.nc * kNC + pa.SP + 63) / 64, g.K, g.B), dim3(64 * kUcoefRows), 0, st,
+    if (pa.enabled) {
+        int nent = 0;
+        for (int gi = 0; gi < kGrids; ++gi)
+            if (pa.gr[gi].on) nent = std::max(nent, pa.gr[gi].nc * kNC + pa.gr[gi].SP);
+        hipLaunchKernelGGL(k_ucoef, dim3((nent + 63) / 64, g.K, g.B * kGrids), dim3(64 * kUcoefRows), 0, st,
                            g, pa, w);
+    }
     hipLaunchKernelGGL(k_usage, dim3((g.T + kUsageBS - 1) / kUsageBS, g.K, g.B), dim3(kUsageBS), 0, st, g, pa, w);
     hipLaunchKernelGGL(k_vres, dim3(g.K, g.B), dim3(kTermsBS), 0, st, g, w, hp);
     if (hp.gamma != 0.0f) {   // expected storage units and their smooth peak

@@ -10,52 +10,97 @@
 namespace gaus {
 
 
-// Work-group = (op group, restart), kPolyWaves waves; each wave takes the
-// group's ops in turn.  For a polynomial op: lanes = strip positions for the
-// step-by-step part, lanes = chunks for the polynomial part; per polynomial
-// out-edge the consumer-side derivatives of both parts are reduced together.
-// NP: strip passes of 64 lanes, ceil(SP / 64).
-//
-// Strip values are evaluated once per position and shared between lanes
-// through per-wave LDS rows: CDF values one step back (for the masses) and
-// Lat steps back (for the delay-shifted functions) are read from the lanes
-// that own those positions.  Position D-1 has the constant F = 1, so its lane
-// evaluates D-3 instead (the step before D-2, the first position of the upper
-// segment); the shifted values of the two upper positions and, for Lat = 0,
-// the value at L0 come from one more evaluation on four lanes.
 constexpr int kStripExtra = 8;   // row slots past SP: [SP] = D-3, [SP+1 .. SP+4] = helper values
 constexpr int kStripPad = kSmax; // zero slots before position 0 (positions -kSmax .. -1, F = 0)
 
-// The degree tiers run as two kernels so that each has its own register
-// budget: kPolyWide (tier 3, degree 5; 4 waves per SIMD with one strip pass)
-// is launched first; it writes the per-work-group usage and V_dep / L_com
-// outputs and clears the records of step-by-step ops.  kPolyNarrow (tiers 1
-// and 2) follows, adds to those outputs, and work-groups without such ops
-// exit at once.
-constexpr int kPolyWide = 3, kPolyNarrow = 12;
+// The degree tiers of grid 0 run as two kernels so that each has its own
+// register budget: kPolyWide (tier 3, degree 5; 4 waves per SIMD with one
+// strip pass) is launched first; it writes the per-work-group usage and
+// V_dep / L_com outputs and clears the records of step-by-step ops.
+// kPolyNarrow (tiers 1 and 2) follows, adds to those outputs, and
+// work-groups without such ops exit at once.  The packed grids run every
+// tier in one kernel (kPolyAll), which writes its grid's outputs.
+constexpr int kPolyWide = 3, kPolyNarrow = 12, kPolyAll = 15;
 
-template <int NP, int TIERS, int FAM>
+// Grid that evaluates op i of restart b, and the tier of its vectors there:
+// the coarsest packed grid whose whole restart pack (the restarts < B of
+// [P floor(b/P), P floor(b/P) + P)) qualifies, the pack's tier being the
+// smallest (highest degree) of its members'; else grid 0 with the op's own
+// tier (ptier).
+__device__ __forceinline__ int op_grid(const Work &W, const PolyArgs &pa, int B, int N, int b, int i, int &tier) {
+#pragma unroll
+    for (int g = kGrids - 1; g >= 1; --g) {
+        if (!pa.gr[g].on) continue;
+        const int P = kGridP[g], b0 = b - b % P;
+        int t = kTiers;
+        bool ok = true;
+        for (int q = 0; q < P && b0 + q < B; ++q) {
+            const int v = W.ptpk[((size_t)(g - 1) * B + b0 + q) * N + i];
+            ok = ok && v != 0;
+            t = min(t, v);
+        }
+        if (ok) { tier = t; return g; }
+    }
+    tier = W.ptier[(size_t)b * N + i];
+    return 0;
+}
+
+// Value of lane h*(64/P) + src (the lane holding item src of this lane's
+// restart h), for P > 1; P = 1 reads lane src.
+template <int P>
+__device__ __forceinline__ float from_lane(float v, int src, int h) {
+    if constexpr (P == 1) {
+        return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), src));
+    } else {
+        const int addr = (h * (64 / P) + src) << 2;
+        return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(addr, __builtin_bit_cast(int, v)));
+    }
+}
+
+// Work-group = (op group slice, restart pack), kPolyWaves waves; each wave
+// takes the slice's ops in turn.  P restarts of the op share the wave: lane
+// = (restart h of the pack, index c < 64/P); for each restart, lanes = strip
+// positions for the step-by-step part and lanes = chunks of grid GI for the
+// polynomial part; per polynomial out-edge the consumer-side derivatives of
+// both parts are reduced together over the restart's lanes.
+// NP: strip passes of 64/P lanes, ceil(SP / (64/P)).
+//
+// Strip values are evaluated once per position and shared between lanes
+// through per-(wave, restart) LDS rows: CDF values one step back (for the
+// masses) and Lat steps back (for the delay-shifted functions) are read from
+// the lanes that own those positions.  Position D-1 has the constant F = 1,
+// so its lane evaluates D-3 instead (the step before D-2, the first position
+// of the upper segment); the shifted values of the two upper positions and,
+// for Lat = 0, the value at L0 come from one more evaluation on four lanes.
+template <int NP, int TIERS, int FAM, int P>
 __global__ __launch_bounds__(64 * kPolyWaves) __attribute__((amdgpu_waves_per_eu(TIERS == kPolyWide && NP == 1 ? 4 : 3)))
 void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__restrict__ sigma, Work W) {
-    constexpr bool kFirst = TIERS == kPolyWide;
-    if constexpr (!kFirst) {   // no op of the group takes degree 8 or 6
-        if (!W.gnarrow[(size_t)blockIdx.y * G.ngroups + blockIdx.x / pa.split]) return;
+    static_assert(P == 1 || (NP == 1 && TIERS == kPolyAll), "packed grids: one strip pass, one kernel");
+    constexpr int GI = P == 1 ? 0 : P == 2 ? 1 : 2;   // grid
+    constexpr int L = 64 / P;                          // lanes per restart
+    constexpr bool kWrite = TIERS != kPolyNarrow;      // write (not add) the work-group outputs
+    constexpr bool kClear = P == 1 && TIERS == kPolyWide;   // clear records of step-by-step ops
+    const int split = pa.split;
+    const int grp = blockIdx.x / split, sub = blockIdx.x - grp * split;
+    const int N = G.N, D = G.D, B = G.B;
+    if constexpr (TIERS == kPolyNarrow) {   // no op of the group takes degree 8 or 6
+        if (!W.gnarrow[(size_t)blockIdx.y * G.ngroups + grp]) return;
     }
-    // dynamic LDS: per wave 6 rows of SP strip values and 3 rows of SP +
-    // kStripExtra raw CDF values, then per wave SP strip usages
+    // dynamic LDS: per (wave, restart) 6 rows of SP strip values and 3 rows of
+    // SP + kStripExtra raw CDF values, then per (wave, restart) SP strip usages
     extern __shared__ float sDyn[];
-    __shared__ float sUc[kPolyWaves][kMaxChunks][kNC];
-    __shared__ float sGs[kPolyWaves][2];
-    const int SP = pa.SP, split = pa.split;
-    const int grp = blockIdx.x / split, sub = blockIdx.x - grp * split, b = blockIdx.y;
-    const size_t slot_id = ((size_t)b * G.ngroups + grp) * split + sub;   // per-work-group outputs
+    __shared__ float sUc[kPolyWaves][64][kNC];
+    __shared__ float sGs[kPolyWaves][P][2];
+    const GridArgs &gd = pa.gr[GI];
+    const int SP = gd.SP, L0 = gd.L0;
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    const int N = G.N, D = G.D;
-    const float *mub = mu + (size_t)b * N;
-    const float *rsb = W.rsig + (size_t)b * N;   // 1/sigma
-    const unsigned char *clsb = W.cls + (size_t)b * N;
-    const bool cact = lane < pa.nc;
-    const float tcen = (float)(pa.L0 + lane * pa.W) + pa.lam;
+    const int h = P == 1 ? 0 : lane / L, c = P == 1 ? lane : lane % L;
+    const int b0 = blockIdx.y * P, bh = b0 + h;    // this lane's restart
+    const bool hact = P == 1 || bh < B;
+    const bool cact = hact && c < gd.nc;
+    const float tcen = (float)(L0 + c * gd.W) + gd.lam;
+    // per-work-group output slot of restart b
+    auto slot_of = [&](int b) { return (((size_t)GI * B + b) * G.ngroups + grp) * split + sub; };
 
     float uc[kNC];
 #pragma unroll
@@ -64,54 +109,67 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
 #pragma unroll
     for (int ps = 0; ps < NP; ++ps) us[ps] = 0.0f;
     const int SPX = kStripPad + SP + kStripExtra;
-    float *own = sDyn + (size_t)wv * (6 * SP + 3 * SPX);
+    float *own = sDyn + (size_t)(wv * P + h) * (6 * SP + 3 * SPX);
     float *rSt = own + 6 * SP + kStripPad, *rFm = rSt + SPX, *rFs = rFm + SPX;
-    float *sUs = sDyn + (size_t)kPolyWaves * (6 * SP + 3 * SPX);
-    const int L0 = pa.L0;
-    if (lane < kStripPad) {   // never overwritten: positions before 0 have F = 0, dF = 0
-        rSt[lane - kStripPad] = 0.0f; rFm[lane - kStripPad] = 0.0f; rFs[lane - kStripPad] = 0.0f;
+    float *sUs = sDyn + (size_t)kPolyWaves * P * (6 * SP + 3 * SPX);
+    if (c < kStripPad) {   // never overwritten: positions before 0 have F = 0, dF = 0
+        rSt[c - kStripPad] = 0.0f; rFm[c - kStripPad] = 0.0f; rFs[c - kStripPad] = 0.0f;
     }
 
     // the work-group's ops are q = q0 + sub + split*j; this wave's are
-    // j = wv + kPolyWaves*l, parameters loaded by lane l
+    // j = wv + kPolyWaves*l (at most 16, as split keeps 64 ops per work-group):
+    // lane l < nq loads op l's restart-independent data, lane h*(64/P) + l its
+    // mean and 1/sigma in restart h of the pack
     const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
     const int nj = (q1 - q0 - sub + split - 1) / split;
     const int nq = (nj - wv + kPolyWaves - 1) / kPolyWaves;
-    int l_i = 0, l_cls = 0, l_s = 0, l_e0 = 0, l_e1 = 0;
+    int l_i = 0, l_cls = 0, l_mine = 0, l_s = 0, l_e0 = 0, l_e1 = 0;
     float l_mu = 0.0f, l_sg = 1.0f;   // l_sg holds 1/sigma
-    if (lane < nq) {
-        l_i = G.perm[q0 + sub + split * (wv + kPolyWaves * lane)];
-        l_cls = W.ptier[(size_t)b * N + l_i];   // 0: step by step, else the degree tier
-        l_mu = mub[l_i]; l_sg = rsb[l_i];
-        l_s = G.delay[l_i];
-        l_e0 = G.row_ptr[l_i]; l_e1 = G.row_ptr[l_i + 1];
+    if (c < nq) {
+        const int i = G.perm[q0 + sub + split * (wv + kPolyWaves * c)];
+        if (hact) { l_mu = mu[(size_t)bh * N + i]; l_sg = W.rsig[(size_t)bh * N + i]; }
+        if (lane < nq) {
+            l_i = i;
+            int tier = 0;
+            const int g = op_grid(W, pa, B, N, b0, i, tier);
+            if constexpr (P == 1) {
+                l_cls = W.ptier[(size_t)b0 * N + i];   // 0: step by step, else the degree tier
+                l_mine = g == 0;
+            } else {
+                l_cls = g == GI ? tier : 0;
+                l_mine = g == GI;
+            }
+            l_s = G.delay[i];
+            l_e0 = G.row_ptr[i]; l_e1 = G.row_ptr[i + 1];
+        }
     }
-    if constexpr (!kFirst) {   // nothing to add unless the work-group has ops of these tiers
-        if (!__syncthreads_or(lane < nq && (l_cls == 1 || l_cls == 2))) return;
+    if constexpr (TIERS == kPolyNarrow) {   // nothing to add unless the work-group has ops of these tiers
+        if (!__syncthreads_or(lane < nq && l_mine && (l_cls == 1 || l_cls == 2))) return;
     }
-    float gsum = 0.0f;  // V_dep, L_com of this wave's ops (lanes 0 and 2)
-    if constexpr (kFirst) {   // step-by-step ops: no polynomial records
+    float gsum = 0.0f;  // V_dep, L_com of this wave's ops (lanes c = 0 and 2)
+    if constexpr (kClear) {   // step-by-step ops: no polynomial records
         for (int oq = 0; oq < nq; ++oq) {
             if (__builtin_amdgcn_readlane(l_cls, oq)) continue;
             const int i = __builtin_amdgcn_readlane(l_i, oq);
-            if (lane < kPP) W.ppoly[((size_t)b * N + i) * kPP + lane] = 0.0f;
+            if (lane < kPP) W.ppoly[((size_t)b0 * N + i) * kPP + lane] = 0.0f;
         }
     }
     // polynomial ops, one pass per degree tier (NC coefficients per vector)
     auto tier_pass = [&](auto nc_tag, int tier) {
     constexpr int NC = decltype(nc_tag)::value;
     for (int oq = 0; oq < nq; ++oq) {
-        if (__builtin_amdgcn_readlane(l_cls, oq) != tier) continue;
+        if (!__builtin_amdgcn_readlane(l_mine, oq) || __builtin_amdgcn_readlane(l_cls, oq) != tier) continue;
         const int i = __builtin_amdgcn_readlane(l_i, oq);
-        float *pp = W.ppoly + ((size_t)b * N + i) * kPP;
-        const float m_i = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, l_mu), oq));
-        const float rs = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, l_sg), oq));
+        float *pp = W.ppoly + ((size_t)bh * N + i) * kPP;
+        const float m_i = from_lane<P>(l_mu, oq, h);
+        const float rs = from_lane<P>(l_sg, oq, h);
         const float cinv = rs * fam_k<FAM>();
         const int s = __builtin_amdgcn_readlane(l_s, oq);
         const int e0 = __builtin_amdgcn_readlane(l_e0, oq), e1 = __builtin_amdgcn_readlane(l_e1, oq);
         float pr[kPP] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
-        // the op's polynomial out-edges, loaded by lane (batches of 64)
-        int x_j = 0, x_ok = 0;
+        // the op's polynomial out-edges in batches of 64/P: lane h*(64/P) + l
+        // loads edge l's consumer in restart h
+        int x_ok = 0;
         float x_mu = 0.0f, x_sg = 1.0f;   // x_sg: 1/sigma of the consumer
 
         // (1) strip: own CDF values per position (raw rows), then the derived
@@ -119,7 +177,7 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
         // instead 1 - F(u-s), the weight of the consumers' open last bin), dF(u-s)
 #pragma unroll
         for (int ps = 0; ps < NP; ++ps) {
-            const int p = ps * 64 + lane;
+            const int p = ps * L + c;
             if (p < SP) {
                 const bool last = p == SP - 1;   // position D-1: evaluates D-3
                 const int u = p < L0 ? p : D - 2 + (p - L0);
@@ -129,16 +187,16 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
                 rSt[p] = st; rFm[p] = Fm; rFs[p] = Fs;
             }
         }
-        if (lane < 4) {   // D-2-s, D-1-s, D-s (upper shifted positions) and L0
-            const int v = lane < 3 ? D - 2 - s + lane : L0;
+        if (c < 4) {   // D-2-s, D-1-s, D-s (upper shifted positions) and L0
+            const int v = c < 3 ? D - 2 - s + c : L0;
             float st, Fm, Fs;
             cdf_at<FAM>(v, D, m_i, rs, cinv, st, Fm, Fs);
-            rSt[SP + 1 + lane] = st; rFm[SP + 1 + lane] = Fm; rFs[SP + 1 + lane] = Fs;
+            rSt[SP + 1 + c] = st; rFm[SP + 1 + c] = Fm; rFs[SP + 1 + c] = Fs;
         }
         __builtin_amdgcn_wave_barrier();
 #pragma unroll
         for (int ps = 0; ps < NP; ++ps) {
-            const int p = ps * 64 + lane;
+            const int p = ps * L + c;
             if (p < SP) {
                 const float st = rSt[p];
                 const float stm1 = rSt[p == L0 ? SP : p - 1];
@@ -173,44 +231,45 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
             for (int k = 0; k < NC; ++k) uc[k] += v[k];
 #pragma unroll
             for (int k = 0; k < NC; ++k) w[k] = ea.T[k];
-            vec_moments(w, pa, HF);
+            vec_moments(w, gd.H, HF);
             vec_dFdmu(ea, v);
-            vec_moments(v, pa, HFm);
+            vec_moments(v, gd.H, HFm);
             vec_times_z(v, ea.z0, ea.r, w);
-            vec_moments(w, pa, HFs);
+            vec_moments(w, gd.H, HFs);
             // shifted functions: A(u) = mass at u-s+1, dF(u-s)
             Expansion<NC> es;
             if (s != 1) expand<FAM>(m_i, rs, tcen - (float)(s - 1), es);
             const Expansion<NC> &ex = (s != 1) ? es : ea;
             vec_mass(ex, v);
-            vec_moments(v, pa, HA);
+            vec_moments(v, gd.H, HA);
             vec_dFdmu_back(ex, v);
-            vec_moments(v, pa, HFm1);
+            vec_moments(v, gd.H, HFm1);
             vec_times_z(v, ex.z0 - rs, ex.r, w);
-            vec_moments(w, pa, HFs1);
+            vec_moments(w, gd.H, HFs1);
         }
 
         // (3) polynomial out-edges
         for (int e = e0; e < e1; ++e) {
-            const int eb = (e - e0) & 63;
+            const int eb = (e - e0) % L;
             if (eb == 0) {
                 x_ok = 0;
-                if (e + lane < e1) {
-                    x_j = G.col[e + lane];
-                    x_ok = clsb[x_j];
-                    x_mu = mub[x_j]; x_sg = rsb[x_j];
+                if (e + c < e1) {
+                    const int x_j = G.col[e + c];
+                    // packed ops have only polynomial consumers (every restart)
+                    x_ok = P == 1 ? W.cls[(size_t)b0 * N + x_j] : 1;
+                    if (hact) { x_mu = mu[(size_t)bh * N + x_j]; x_sg = W.rsig[(size_t)bh * N + x_j]; }
                 }
             }
             if (!__builtin_amdgcn_readlane(x_ok, eb)) continue;  // step-by-step edge, done by k_ops
-            const float m_j = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x_mu), eb));
-            const float rsj = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x_sg), eb));
+            const float m_j = from_lane<P>(x_mu, eb, h);
+            const float rsj = from_lane<P>(x_sg, eb, h);
             const float cj = rsj * fam_k<FAM>();
             float cc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
             // the consumer's CDF per strip position (D-1's lane evaluates D-3)
             float xst[NP], xFm[NP], xFs[NP];
 #pragma unroll
             for (int ps = 0; ps < NP; ++ps) {
-                const int p = ps * 64 + lane;
+                const int p = ps * L + c;
                 if (p < SP) {
                     const bool last = p == SP - 1;
                     const int u = p < L0 ? p : D - 2 + (p - L0);
@@ -222,7 +281,7 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
             __builtin_amdgcn_wave_barrier();
 #pragma unroll
             for (int ps = 0; ps < NP; ++ps) {
-                const int p = ps * 64 + lane;
+                const int p = ps * L + c;
                 if (p < SP) {
                     // at u = D-1 the consumer's F = 1 and dF = 0: only
                     // pr[0] += 1 - F_i(D-1-s) remains, the rest adds zeros
@@ -261,57 +320,71 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
                 pr[2] -= vdot(HFm1, v);
                 pr[3] -= vdot(HFs1, v);
             }
-            const float ct = wave_sum4(cc[0], cc[1], cc[2], cc[3], lane);
-            if (lane < kCP) W.cpoly[((size_t)b * G.E + e) * kCP + wave4_comp(lane)] = ct;
+            const float ct = group_sum4<P>(cc[0], cc[1], cc[2], cc[3], lane);
+            if (c < kCP && hact) W.cpoly[((size_t)bh * G.E + e) * kCP + wave4_comp(c)] = ct;
         }
-        const float pt4 = wave_sum4(pr[0], pr[1], pr[2], pr[3], lane);
-        const float pt2 = wave_sum2(pr[4], pr[5], lane);
-        if (lane < 4) pp[wave4_comp(lane)] = pt4;
-        if (lane < 2) pp[4 + lane] = pt2;
-        gsum += pt4;   // lane 0: V_dep, lane 2: L_com
+        const float pt4 = group_sum4<P>(pr[0], pr[1], pr[2], pr[3], lane);
+        const float pt2 = group_sum2<P>(pr[4], pr[5], lane);
+        if (hact) {
+            if (c < 4) pp[wave4_comp(c)] = pt4;
+            if (c < 2) pp[4 + c] = pt2;
+        }
+        gsum += pt4;   // lane c = 0: V_dep, c = 2: L_com
     }
     };
-    if constexpr (kFirst) {
+    if constexpr (TIERS == kPolyWide) {
         tier_pass(std::integral_constant<int, kTierDeg[3] + 1>{}, 3);
-    } else {
+    } else if constexpr (TIERS == kPolyNarrow) {
         tier_pass(std::integral_constant<int, kTierDeg[1] + 1>{}, 1);
         tier_pass(std::integral_constant<int, kTierDeg[2] + 1>{}, 2);
+    } else {
+        tier_pass(std::integral_constant<int, kTierDeg[3] + 1>{}, 3);
+        tier_pass(std::integral_constant<int, kTierDeg[2] + 1>{}, 2);
+        tier_pass(std::integral_constant<int, kTierDeg[1] + 1>{}, 1);
     }
-    if (lane == 0) sGs[wv][0] = gsum;
-    if (lane == 2) sGs[wv][1] = gsum;
+    if (c == 0) sGs[wv][h][0] = gsum;
+    if (c == 2) sGs[wv][h][1] = gsum;
 
     // usage of the group: combine the waves' chunk coefficients and strip values
 #pragma unroll
     for (int k = 0; k < kNC; ++k) sUc[wv][lane][k] = uc[k];
 #pragma unroll
     for (int ps = 0; ps < NP; ++ps) {
-        const int p = ps * 64 + lane;
-        if (p < SP) sUs[wv * SP + p] = us[ps];
+        const int p = ps * L + c;
+        if (p < SP) sUs[(wv * P + h) * SP + p] = us[ps];
     }
     __syncthreads();
-    float *ucg = W.Ucoef + slot_id * kMaxChunks * kNC;
-    for (int x = threadIdx.x; x < kMaxChunks * kNC; x += 64 * kPolyWaves) {
-        const int c = x / kNC, k = x % kNC;
+    // entries (restart hh of the pack, chunk cc < 64/P, coefficient k)
+    for (int x = threadIdx.x; x < 64 * kNC; x += 64 * kPolyWaves) {
+        const int ln = x / kNC, k = x % kNC;
+        const int hh = ln / L, cx = ln % L;
+        if (b0 + hh >= B) continue;
         float acc = 0.0f;
 #pragma unroll
-        for (int w = 0; w < kPolyWaves; ++w) acc += sUc[w][c][k];
-        ucg[x] = kFirst ? acc : ucg[x] + acc;
+        for (int w = 0; w < kPolyWaves; ++w) acc += sUc[w][ln][k];
+        float *dst = W.Ucoef + slot_of(b0 + hh) * kMaxChunks * kNC + cx * kNC + k;
+        *dst = kWrite ? acc : *dst + acc;
     }
-    if (threadIdx.x < 2) {
-        float acc = 0.0f;
+    if (threadIdx.x < 2 * P) {
+        const int hh = threadIdx.x >> 1, v = threadIdx.x & 1;
+        if (b0 + hh < B) {
+            float acc = 0.0f;
 #pragma unroll
-        for (int w = 0; w < kPolyWaves; ++w) acc += sGs[w][threadIdx.x];
-        float *gs = W.gsum_poly + slot_id * 2 + threadIdx.x;
-        *gs = kFirst ? acc : *gs + acc;
+            for (int w = 0; w < kPolyWaves; ++w) acc += sGs[w][hh][v];
+            float *gs = W.gsum_poly + slot_of(b0 + hh) * 2 + v;
+            *gs = kWrite ? acc : *gs + acc;
+        }
     }
-    float *usg = W.Ustrip + slot_id * kStripMax;
-    for (int p = threadIdx.x; p < kStripMax; p += 64 * kPolyWaves) {
+    for (int x = threadIdx.x; x < P * kStripMax; x += 64 * kPolyWaves) {
+        const int hh = x / kStripMax, p = x % kStripMax;
+        if (b0 + hh >= B) continue;
         float acc = 0.0f;
         if (p < SP) {
 #pragma unroll
-            for (int w = 0; w < kPolyWaves; ++w) acc += sUs[w * SP + p];
+            for (int w = 0; w < kPolyWaves; ++w) acc += sUs[(w * P + hh) * SP + p];
         }
-        usg[p] = kFirst ? acc : usg[p] + acc;
+        float *usg = W.Ustrip + slot_of(b0 + hh) * kStripMax + p;
+        *usg = kWrite ? acc : *usg + acc;
     }
 }
 
@@ -753,11 +826,21 @@ hipError_t launch_poly(const Graph &g, const Work &w, const PolyArgs &pa, const 
                        hipStream_t st) {
     const size_t lds = sizeof(float) * (size_t)kPolyWaves * (10 * pa.SP + 3 * (kStripPad + kStripExtra));
     const dim3 grid(g.ngroups * pa.split, g.B), block(64 * kPolyWaves);
-    auto pair = [&](auto fam_tag) -> hipError_t {
+    // packed grid G_: restart packs of P_ on the y axis, per-(wave, restart) LDS rows
+    auto packed = [&](auto fam_tag, auto p_tag) {
+        constexpr int FAM = decltype(fam_tag)::value, P_ = decltype(p_tag)::value;
+        constexpr int G_ = P_ == 2 ? 1 : 2;
+        const GridArgs &gd = pa.gr[G_];
+        if (!gd.on) return;
+        const size_t ldsp = sizeof(float) * (size_t)kPolyWaves * P_ * (10 * gd.SP + 3 * (kStripPad + kStripExtra));
+        const dim3 gridp(g.ngroups * pa.split, (g.B + P_ - 1) / P_);
+        hipLaunchKernelGGL((k_poly<1, kPolyAll, FAM, P_>), gridp, block, ldsp, st, g, pa, mu, sigma, w);
+    };
+    auto run = [&](auto fam_tag) -> hipError_t {
         constexpr int FAM = decltype(fam_tag)::value;
-#define GAUS_POLY_PAIR(NPV)                                                                            \
-        hipLaunchKernelGGL((k_poly<NPV, kPolyWide, FAM>), grid, block, lds, st, g, pa, mu, sigma, w);   \
-        hipLaunchKernelGGL((k_poly<NPV, kPolyNarrow, FAM>), grid, block, lds, st, g, pa, mu, sigma, w);
+#define GAUS_POLY_PAIR(NPV)                                                                              \
+        hipLaunchKernelGGL((k_poly<NPV, kPolyWide, FAM, 1>), grid, block, lds, st, g, pa, mu, sigma, w);   \
+        hipLaunchKernelGGL((k_poly<NPV, kPolyNarrow, FAM, 1>), grid, block, lds, st, g, pa, mu, sigma, w);
         switch ((pa.SP + 63) / 64) {
         case 1: GAUS_POLY_PAIR(1) break;
         case 2: GAUS_POLY_PAIR(2) break;
@@ -767,12 +850,14 @@ hipError_t launch_poly(const Graph &g, const Work &w, const PolyArgs &pa, const 
         default: return hipErrorInvalidValue;
         }
 #undef GAUS_POLY_PAIR
+        packed(fam_tag, std::integral_constant<int, 2>{});
+        packed(fam_tag, std::integral_constant<int, 4>{});
         return hipSuccess;
     };
     switch (pa.fam) {
-    case 0: return pair(std::integral_constant<int, 0>{});
-    case 1: return pair(std::integral_constant<int, 1>{});
-    case 3: return pair(std::integral_constant<int, 3>{});
+    case 0: return run(std::integral_constant<int, 0>{});
+    case 1: return run(std::integral_constant<int, 1>{});
+    case 3: return run(std::integral_constant<int, 3>{});
     default: return hipErrorInvalidValue;
     }
 }

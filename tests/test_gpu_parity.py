@@ -211,6 +211,69 @@ def test_polynomial_degree_tiers(beta):
            f"degree tiers, smooth peak weight {beta:g}")
 
 
+def _grid_census(p, mu, sg, hp):
+    """Grid census of one loss+gradient evaluation (and the grids' layout)."""
+    import torch
+    B = mu.shape[0]
+    ctx = bd.Context(p, B, hp)
+    dev = torch.device("cuda")
+    m = torch.from_numpy(mu).to(dev)
+    s = torch.from_numpy(sg).to(dev)
+    l = torch.full((B, 3), 0.1, device=dev)
+    terms = torch.zeros(B, bd.N_TERMS, device=dev)
+    gm = torch.zeros(B, p.n_ops, device=dev)
+    gs = torch.zeros(B, p.n_ops, device=dev)
+    ctx.loss_grad(m, s, l, terms, gm, gs)
+    out = ctx.poly_grid_census(), ctx.poly_grids()
+    ctx.close()
+    return out
+
+
+@pytest.mark.parametrize("beta", [0.0, 1.0])
+def test_packed_grids(beta):
+    """Restart packing: ops whose pack (2 or 4 restarts sharing a wave) and
+    consumers all reach a packed grid's degree-8 bound take it; mixed packs,
+    narrower consumers and delays above 8 fall back to grid 0 or to the
+    step-by-step path.  B = 7 leaves partial packs (4 + 3, 2+2+2+1).  Every
+    restart matches the oracle; the packed evaluation matches the unpacked
+    one (poly_pack = -1) to fp32 rounding."""
+    p = _ragged_problem(301, N=1500, D=3000, big_delay=False)
+    rng = np.random.default_rng(302)
+    p.delay[:] = rng.integers(0, 11, size=p.n_ops).astype(np.int32)
+    B = 7
+    hp0 = hparams(alpha=0.2, rho=0.01, beta=beta, tau=0.1)
+    ctx = bd.Context(p, B, hp0)
+    grids = ctx.poly_grids()
+    ctx.close()
+    say(f"  grids {grids}")
+    assert all(g["on"] for g in grids)
+    lam = [(g["W"] - 1) / 2.0 for g in grids]
+    # width classes: step by step, grid 0, grid 1, grid 2 (degree 8), grid 2 (low degree)
+    cls_sigma = np.array([0.5 * lam[0] / 0.25, 1.3 * lam[0] / 0.25, 1.3 * lam[1] / 0.25,
+                          1.3 * lam[2] / 0.25, 6.0 * lam[2] / 0.25])
+    prob = np.array([0.1, 0.15, 0.15, 0.3, 0.3])
+    base = rng.choice(len(cls_sigma), size=p.n_ops, p=prob)
+    pick = np.repeat(base[None, :], B, axis=0)
+    flip = rng.random((B, p.n_ops)) < 0.08
+    pick[flip] = rng.choice(len(cls_sigma), size=int(flip.sum()), p=prob)
+    sg = (cls_sigma[pick] * rng.uniform(0.97, 1.03, size=(B, p.n_ops))).astype(np.float32)
+    mu = rng.uniform(-100, p.D + 100, size=(B, p.n_ops)).astype(np.float32)
+    census, _ = _grid_census(p, mu, sg, hp0)
+    say(f"  (restart, op) pairs per grid: {census}")
+    assert min(census) > 0.03 * B * p.n_ops, census
+    lamb = _lam(B, 303)
+    g = _check(p, mu, sg, lamb, hp0, range(B), f"packed grids beta={beta:g}")
+    hp1 = hparams(alpha=0.2, rho=0.01, beta=beta, tau=0.1)
+    hp1.poly_pack = -1
+    g1 = gpu_loss_grad(p, mu, sg, lamb, hp1)
+    for b in range(B):
+        dt = np.abs(g["terms"][b] - g1["terms"][b]) / np.maximum(np.abs(g1["terms"][b]), 1.0)
+        assert dt.max() <= 1e-6, (b, g["terms"][b], g1["terms"][b])
+        for k in ("gm", "gs"):
+            e = np.abs(g[k][b] - g1[k][b]).max() / np.abs(g1[k][b]).max()
+            assert e <= 1e-6, (b, k, e)
+
+
 @pytest.mark.parametrize("II,n_back", [(0, 0), (3001, 3)])
 def test_maximum_horizon(II, n_back):
     """D = 2^22, the largest horizon the library takes: 4096 tiles of the
