@@ -37,6 +37,7 @@ struct gaus_ctx {
     int *adam_t = nullptr;
     bool bound = false;
     PolyArgs pa{};
+    int poly_slots = 0;                 // per-work-group output slots of the polynomial kernels
     // kernel timing (gaus_kernel_timing): per iteration two pairs of events,
     // [4k, 4k+1] around the op kernel and [4k+2, 4k+3] around the polynomial kernel
     bool timing = false;
@@ -45,6 +46,8 @@ struct gaus_ctx {
 };
 
 constexpr int kPolySplitMax = 4;   // polynomial work-groups per op group, at most
+constexpr int kPackOpsPerWave = 16;// packed grids: ops per wave, at most (when the split allows)
+constexpr int kPackSplitMax = 16;  // packed grids: work-groups per op group, at most
 
 namespace {
 
@@ -494,9 +497,20 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
         int gmax = 1;
         for (int q = 0; q < g.ngroups; ++q) gmax = std::max(gmax, h.grp_start[q + 1] - h.grp_start[q]);
         c->pa.split = std::max(1, std::min(kPolySplitMax, (gmax + 63) / 64));
-        // the packed kernels load each wave's ops on 64/P >= 16 lanes per restart
-        if ((gmax + c->pa.split - 1) / c->pa.split > 64)
-            for (int gi = 1; gi < kGrids; ++gi) c->pa.gr[gi].on = 0;
+        c->pa.gr[0].split = c->pa.split;
+        // packed grids: at most kPackOpsPerWave ops per wave (each wave-op
+        // carries P restarts, so fewer ops per wave keep the last waves short)
+        int base = 0;
+        for (int gi = 0; gi < kGrids; ++gi) {
+            GridArgs &gr = c->pa.gr[gi];
+            if (gi > 0)
+                gr.split = std::max(1, std::min(kPackSplitMax, (gmax + 4 * kPackOpsPerWave - 1) / (4 * kPackOpsPerWave)));
+            // the packed kernels load each wave's ops on 64/P >= 16 lanes per restart
+            if (gi > 0 && (gmax + gr.split - 1) / gr.split > 64) gr.on = 0;
+            gr.slot_base = base;
+            if (gr.on) base += B * g.ngroups * gr.split;
+        }
+        c->poly_slots = base;
     }
     g.nlevels = (int)h.lvl_ptr.size() - 1;
     std::vector<float> cap(h.cap);
@@ -568,13 +582,16 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     AL(gflag, (size_t)B * g.ngroups);
     AL(gnarrow, (size_t)B * g.ngroups);
     AL(gsum_ops, (size_t)B * g.ngroups * ntiles * 2);
-    AL(gsum_poly, (size_t)kGrids * B * g.ngroups * c->pa.split * 2);
+    AL(gsum_poly, (size_t)std::max(c->poly_slots, 1) * 2);
+    AL(gsel, BN);
+    AL(gtier, BN);
+    AL(gwork, (size_t)kGrids * B * g.ngroups);
     AL(vres_part, (size_t)B * h.K);
     AL(Ucoef_k, (size_t)B * h.K * kGrids * (kMaxChunks * kNC + kStripMax));
     AL(ppoly, BN * kPP);
     AL(cpoly, (size_t)B * h.E * kCP);
-    AL(Ucoef, (size_t)kGrids * B * g.ngroups * c->pa.split * kMaxChunks * kNC);
-    AL(Ustrip, (size_t)kGrids * B * g.ngroups * c->pa.split * kStripMax);
+    AL(Ucoef, (size_t)std::max(c->poly_slots, 1) * kMaxChunks * kNC);
+    AL(Ustrip, (size_t)std::max(c->poly_slots, 1) * kStripMax);
     AL(s64, BN);
     AL(s64b, BN);
     AL(status, (size_t)B);
@@ -583,7 +600,9 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
         hipError_t e = hipMemset(c->w.U, 0, sizeof(float) * (size_t)B * h.K * g.T);
         if (e == hipSuccess) e = hipMemset(c->w.ppoly, 0, sizeof(float) * BN * kPP);
         if (e == hipSuccess) e = hipMemset(c->w.cls, 0, BN);
-        if (e == hipSuccess) e = hipMemset(c->w.gsum_poly, 0, sizeof(float) * (size_t)kGrids * B * g.ngroups * c->pa.split * 2);
+        if (e == hipSuccess) e = hipMemset(c->w.gsum_poly, 0, sizeof(float) * (size_t)std::max(c->poly_slots, 1) * 2);
+        if (e == hipSuccess) e = hipMemset(c->w.gsel, kNoGrid, BN);
+        if (e == hipSuccess) e = hipMemset(c->w.gwork, 0, (size_t)kGrids * B * g.ngroups);
         if (e == hipSuccess) e = hipMemset(c->w.ptpk, 0, (size_t)(kGrids - 1) * BN);
         if (e == hipSuccess) e = hipDeviceSynchronize();
         if (e != hipSuccess) { s = fail(nullptr, GAUS_E_DEVICE, "init: %s", hipGetErrorString(e)); goto fail_alloc; }
@@ -873,30 +892,15 @@ gaus_status gaus_get_poly_grids(const gaus_ctx *ctx, int32_t cfg[15]) {
 gaus_status gaus_poly_grid_census(gaus_ctx *ctx, int64_t counts[3]) {
     if (!ctx) return GAUS_E_INVALID_ARG;
     if (!counts) return fail(ctx, GAUS_E_INVALID_ARG, "poly_grid_census: null pointer");
-    const Graph &g = ctx->g;
-    const size_t BN = (size_t)g.B * g.N;
+    const size_t BN = (size_t)ctx->g.B * ctx->g.N;
     hipError_t e = hipStreamSynchronize(ctx->stream);
     if (e != hipSuccess) return hip_fail(ctx, e, "poly_grid_census");
-    std::vector<unsigned char> cls(BN), pk((kGrids - 1) * BN);
-    e = hipMemcpy(cls.data(), ctx->w.cls, BN, hipMemcpyDeviceToHost);
-    if (e == hipSuccess) e = hipMemcpy(pk.data(), ctx->w.ptpk, pk.size(), hipMemcpyDeviceToHost);
+    std::vector<unsigned char> sel(BN);
+    e = hipMemcpy(sel.data(), ctx->w.gsel, BN, hipMemcpyDeviceToHost);
     if (e != hipSuccess) return hip_fail(ctx, e, "poly_grid_census");
     for (int gi = 0; gi < kGrids; ++gi) counts[gi] = 0;
-    for (int b = 0; b < g.B; ++b) {
-        for (int i = 0; i < g.N; ++i) {
-            if (!cls[(size_t)b * g.N + i]) continue;
-            int grid = 0;   // the coarsest packed grid whose whole pack qualifies
-            for (int gi = kGrids - 1; gi >= 1 && grid == 0; --gi) {
-                if (!ctx->pa.gr[gi].on) continue;
-                const int P = kGridP[gi], b0 = b - b % P;
-                bool ok = true;
-                for (int q = 0; q < P && b0 + q < g.B; ++q)
-                    ok = ok && pk[((size_t)(gi - 1) * g.B + b0 + q) * g.N + i] != 0;
-                if (ok) grid = gi;
-            }
-            ++counts[grid];
-        }
-    }
+    for (size_t q = 0; q < BN; ++q)
+        if (sel[q] < kGrids) ++counts[sel[q]];
     return GAUS_OK;
 }
 

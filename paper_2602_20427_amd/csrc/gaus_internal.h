@@ -50,10 +50,14 @@ constexpr float kMemRhoMax = 0.25f;
 // for the grid's degree-8 bound.
 constexpr int kGrids = 3;
 constexpr int kGridP[kGrids] = {1, 2, 4};
+constexpr unsigned char kNoGrid = 255;
 
 struct GridArgs {
     int on;               // grid in use
     int W, nc, L0, SP;    // chunk width, chunks, left strip [0, L0), strip positions [0, L0) u {D-2, D-1}
+    int split;            // work-groups per op group
+    int slot_base;        // first per-work-group output slot of the grid: slot of (restart b, group,
+                          // part) = slot_base + (b * ngroups + group) * split + part
     float lam;            // chunk half-width (W-1)/2
     float sig_thr[kTiers + 1];   // sigma >= sig_thr[t]: tier t on this grid
     float H[kDeg + 1];    // even moments of a chunk's points
@@ -151,13 +155,19 @@ struct Work {
     int *gflag;       // [B][ngroups]      1 = some op of the group has step-by-step work
     int *gnarrow;     // [B][ngroups]      1 = some op of the group takes polynomial degree 8 or 6
     float *gsum_ops;  // [B][ngroups][ntiles][2]  V_dep, L_com of a k_ops work-group
-    float *gsum_poly; // [kGrids][B][ngroups*split][2]  V_dep, L_com of a k_poly work-group
+    float *gsum_poly; // [slots][2]        V_dep, L_com of a k_poly work-group (GridArgs::slot_base)
+    unsigned char *gsel;   // [B][N]        grid that evaluates the (restart, op) this iteration (0..2),
+                           //               kNoGrid on the step-by-step path
+    unsigned char *gtier;  // [B][N]        tier of its vectors on that grid (0 off the polynomial path)
+    unsigned char *gwork;  // [kGrids][B][ngroups]  1 = the group has ops on the grid (grid 0 also:
+                           //               step-by-step ops, whose polynomial records are cleared);
+                           //               only such groups' polynomial work-groups write outputs
     float *vres_part; // [B][K]            V_res of one resource type
     float *Ucoef_k;   // [B][K][kGrids][64*kNC + 320]  polynomial usage coefficients and strip values per type
     float *ppoly;     // [B][N][kPP]       producer partials of the polynomial path
     float *cpoly;     // [B][E][kCP]       consumer partials of polynomial edges
-    float *Ucoef;     // [kGrids][B][ngroups*split][kMaxChunks][kNC]  usage coefficients per chunk
-    float *Ustrip;    // [kGrids][B][ngroups*split][kStripMax]  usage at the strip positions
+    float *Ucoef;     // [slots][kMaxChunks][kNC]  usage coefficients per chunk of a k_poly work-group
+    float *Ustrip;    // [slots][kStripMax]  usage at the strip positions
     long long *s64;   // [B][N]            legalization workspace
     long long *s64b;  // [B][N]            legalization snapshot (back edges)
     int *status;      // [B]               legalization status

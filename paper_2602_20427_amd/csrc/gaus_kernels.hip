@@ -131,6 +131,45 @@ __global__ __launch_bounds__(256) void k_flags(Graph G, PolyArgs pa, const float
     }
 }
 
+// Grid of every (restart, op) this iteration: the coarsest packed grid whose
+// whole restart pack (the restarts < B of [P floor(b/P), P floor(b/P) + P))
+// has the op qualify (ptpk != 0), with the pack's tier (the smallest, i.e.
+// highest degree, of its members'); else grid 0 with the op's own tier
+// (ptier), or kNoGrid on the step-by-step path.  Per (grid, restart, group)
+// whether any op is there.  Work-group = (op group, restart), thread per op.
+__global__ __launch_bounds__(256) void k_grid(Graph G, PolyArgs pa, Work W) {
+    const int grp = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+    const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
+    const int N = G.N, B = G.B;
+    int sel = -1;
+    if (q0 + tid < q1) {
+        const int i = G.perm[q0 + tid];
+        const size_t bi = (size_t)b * N + i;
+        int tier = W.ptier[bi];
+        sel = W.cls[bi] ? 0 : kNoGrid;
+        for (int g = kGrids - 1; g >= 1 && sel == 0; --g) {
+            if (!pa.gr[g].on) continue;
+            const int P = kGridP[g], b0 = b - b % P;
+            int t = kTiers;
+            bool ok = true;
+            for (int q = 0; q < P && b0 + q < B; ++q) {
+                const int v = W.ptpk[((size_t)(g - 1) * B + b0 + q) * N + i];
+                ok = ok && v != 0;
+                t = min(t, v);
+            }
+            if (ok) { sel = g; tier = t; }
+        }
+        W.gsel[bi] = (unsigned char)sel;
+        W.gtier[bi] = (unsigned char)(sel == kNoGrid ? 0 : tier);
+    }
+#pragma unroll
+    for (int g = 0; g < kGrids; ++g) {
+        // grid 0 also runs for groups with step-by-step ops (it clears their records)
+        const int any = __syncthreads_or(sel == g || (g == 0 && sel == kNoGrid));
+        if (tid == 0) W.gwork[((size_t)g * B + b) * G.ngroups + grp] = (unsigned char)any;
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Usage: U[b][k][slot] = sum over type-k groups and steps t = slot (mod T).
 // ---------------------------------------------------------------------------
@@ -148,16 +187,50 @@ __global__ __launch_bounds__(64 * kUcoefRows) void k_ucoef(Graph G, PolyArgs pa,
     const GridArgs &gd = pa.gr[gi];
     if (!gd.on) return;
     // the type's polynomial work-groups: slots [g0*split, g1*split) of restart b
-    const int g0 = G.type_grp[k] * pa.split, g1 = G.type_grp[k + 1] * pa.split;
-    const size_t rb = ((size_t)gi * G.B + b) * G.ngroups * pa.split;
+    const int g0 = G.type_grp[k] * gd.split, g1 = G.type_grp[k + 1] * gd.split;
+    const size_t rb = (size_t)gd.slot_base + (size_t)b * G.ngroups * gd.split;
     const int ncoef = gd.nc * kNC;
     float acc = 0.0f;
-    if (x < ncoef) {
+    // the type's groups with ops on the grid, compacted in order (their
+    // work-groups wrote every slot; the others wrote nothing)
+    __shared__ int sGrp[64 * kUcoefRows];
+    __shared__ int wcnt[kUcoefRows];
+    const unsigned char *work = W.gwork + ((size_t)gi * G.B + b) * G.ngroups;
+    const int t0 = G.type_grp[k], t1 = G.type_grp[k + 1];
+    int ng = -1;   // -1: more groups than one pass of the work-group lists
+    if (t1 - t0 <= 64 * kUcoefRows) {
+        const int q = t0 + (int)threadIdx.x;
+        const bool f = q < t1 && work[q];
+        const unsigned long long bal = __ballot(f);
+        if (tx == 0) wcnt[ty] = __popcll(bal);
+        __syncthreads();
+        int off = 0;
+        ng = 0;
+#pragma unroll
+        for (int w = 0; w < kUcoefRows; ++w) { off += w < ty ? wcnt[w] : 0; ng += wcnt[w]; }
+        if (f) sGrp[off + __popcll(bal & ((1ull << tx) - 1ull))] = q;
+        __syncthreads();
+    }
+    const int split = gd.split;
+    if (ng >= 0) {
+        const int nsl = ng * split;
+        if (x < ncoef) {
 #pragma unroll 4
-        for (int g = g0 + ty; g < g1; g += kUcoefRows) acc += W.Ucoef[(rb + g) * kMaxChunks * kNC + x];
-    } else if (x < ncoef + gd.SP) {
+            for (int q = ty; q < nsl; q += kUcoefRows)
+                acc += W.Ucoef[(rb + (size_t)sGrp[q / split] * split + q % split) * kMaxChunks * kNC + x];
+        } else if (x < ncoef + gd.SP) {
 #pragma unroll 4
-        for (int g = g0 + ty; g < g1; g += kUcoefRows) acc += W.Ustrip[(rb + g) * kStripMax + (x - ncoef)];
+            for (int q = ty; q < nsl; q += kUcoefRows)
+                acc += W.Ustrip[(rb + (size_t)sGrp[q / split] * split + q % split) * kStripMax + (x - ncoef)];
+        }
+    } else {   // more groups than the list holds: test each
+        if (x < ncoef) {
+            for (int g = g0 + ty; g < g1; g += kUcoefRows)
+                if (work[g / split]) acc += W.Ucoef[(rb + g) * kMaxChunks * kNC + x];
+        } else if (x < ncoef + gd.SP) {
+            for (int g = g0 + ty; g < g1; g += kUcoefRows)
+                if (work[g / split]) acc += W.Ustrip[(rb + g) * kStripMax + (x - ncoef)];
+        }
     }
     part[ty][tx] = acc;
     __syncthreads();
@@ -453,12 +526,15 @@ __global__ __launch_bounds__(kCombineBS) void k_combine(Graph G, PolyArgs pa, Wo
         vres += W.vres_part[(size_t)b * G.K + k];
         lres += W.lres_part[(size_t)b * G.K + k];
     }
-    const int npoly = G.ngroups * pa.split;
     for (int gi = 0; gi < kGrids; ++gi) {
-        if (!pa.gr[gi].on) continue;
+        const GridArgs &gd = pa.gr[gi];
+        if (!gd.on) continue;
+        const int npoly = G.ngroups * gd.split;
+        const unsigned char *work = W.gwork + ((size_t)gi * G.B + b) * G.ngroups;
         for (int g = tid; g < npoly; g += kCombineBS) {
-            const float *gp = W.gsum_poly + (((size_t)gi * G.B + b) * npoly + g) * 2;
-            vdep += gp[0]; lcom += gp[1];
+            if (!work[g / gd.split]) continue;
+            const size_t sl = (size_t)gd.slot_base + (size_t)b * npoly + g;
+            vdep += W.gsum_poly[sl * 2]; lcom += W.gsum_poly[sl * 2 + 1];
         }
     }
     for (int g = tid; g < G.ngroups; g += kCombineBS) {
@@ -1025,6 +1101,7 @@ hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const 
                              const PolyArgs &pa, const IterArgs &a, hipStream_t st) {
     hipLaunchKernelGGL(k_flags, dim3(g.ngroups, g.B), dim3(256), 0, st, g, pa, a.sigma, w,
                        (hp.gamma != 0.0f && pa.enabled) ? 1 : 0);
+    if (pa.enabled) hipLaunchKernelGGL(k_grid, dim3(g.ngroups, g.B), dim3(256), 0, st, g, pa, w);
     hipError_t e;
     if (a.ops_begin) (void)hipEventRecord(a.ops_begin, st);
     if ((e = launch_ops(g, w, lc, a.mu, a.sigma, st)) != hipSuccess) return e;

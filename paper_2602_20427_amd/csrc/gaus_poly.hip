@@ -22,27 +22,14 @@ constexpr int kStripPad = kSmax; // zero slots before position 0 (positions -kSm
 // tier in one kernel (kPolyAll), which writes its grid's outputs.
 constexpr int kPolyWide = 3, kPolyNarrow = 12, kPolyAll = 15;
 
-// Grid that evaluates op i of restart b, and the tier of its vectors there:
-// the coarsest packed grid whose whole restart pack (the restarts < B of
-// [P floor(b/P), P floor(b/P) + P)) qualifies, the pack's tier being the
-// smallest (highest degree) of its members'; else grid 0 with the op's own
-// tier (ptier).
-__device__ __forceinline__ int op_grid(const Work &W, const PolyArgs &pa, int B, int N, int b, int i, int &tier) {
-#pragma unroll
-    for (int g = kGrids - 1; g >= 1; --g) {
-        if (!pa.gr[g].on) continue;
-        const int P = kGridP[g], b0 = b - b % P;
-        int t = kTiers;
-        bool ok = true;
-        for (int q = 0; q < P && b0 + q < B; ++q) {
-            const int v = W.ptpk[((size_t)(g - 1) * B + b0 + q) * N + i];
-            ok = ok && v != 0;
-            t = min(t, v);
-        }
-        if (ok) { tier = t; return g; }
-    }
-    tier = W.ptier[(size_t)b * N + i];
-    return 0;
+// LDS floats per (wave, restart) of k_poly: 6 rows of SP strip values and 3
+// rows of SP + kStripExtra raw CDF values after kStripPad zeros; with P > 1
+// rounded so that the restarts' rows start 64/P banks apart (lane c of every
+// restart then reads and writes a bank of its own).
+template <int P>
+__host__ __device__ constexpr int row_stride(int SP) {
+    const int n = 6 * SP + 3 * (kStripPad + SP + kStripExtra);
+    return P == 1 ? n : n + ((64 / P - n % 64) % 64 + 64) % 64;
 }
 
 // Value of lane h*(64/P) + src (the lane holding item src of this lane's
@@ -80,18 +67,21 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
     constexpr int L = 64 / P;                          // lanes per restart
     constexpr bool kWrite = TIERS != kPolyNarrow;      // write (not add) the work-group outputs
     constexpr bool kClear = P == 1 && TIERS == kPolyWide;   // clear records of step-by-step ops
-    const int split = pa.split;
+    const GridArgs &gd = pa.gr[GI];
+    const int split = gd.split;
     const int grp = blockIdx.x / split, sub = blockIdx.x - grp * split;
     const int N = G.N, D = G.D, B = G.B;
     if constexpr (TIERS == kPolyNarrow) {   // no op of the group takes degree 8 or 6
         if (!W.gnarrow[(size_t)blockIdx.y * G.ngroups + grp]) return;
     }
+    // no op of the group on this grid (in every restart of the pack): nothing
+    // to write, the readers skip the group
+    if (!W.gwork[((size_t)GI * B + blockIdx.y * P) * G.ngroups + grp]) return;
     // dynamic LDS: per (wave, restart) 6 rows of SP strip values and 3 rows of
     // SP + kStripExtra raw CDF values, then per (wave, restart) SP strip usages
     extern __shared__ float sDyn[];
     __shared__ float sUc[kPolyWaves][64][kNC];
     __shared__ float sGs[kPolyWaves][P][2];
-    const GridArgs &gd = pa.gr[GI];
     const int SP = gd.SP, L0 = gd.L0;
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     const int h = P == 1 ? 0 : lane / L, c = P == 1 ? lane : lane % L;
@@ -100,7 +90,7 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
     const bool cact = hact && c < gd.nc;
     const float tcen = (float)(L0 + c * gd.W) + gd.lam;
     // per-work-group output slot of restart b
-    auto slot_of = [&](int b) { return (((size_t)GI * B + b) * G.ngroups + grp) * split + sub; };
+    auto slot_of = [&](int b) { return (size_t)gd.slot_base + ((size_t)b * G.ngroups + grp) * split + sub; };
 
     float uc[kNC];
 #pragma unroll
@@ -109,9 +99,10 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
 #pragma unroll
     for (int ps = 0; ps < NP; ++ps) us[ps] = 0.0f;
     const int SPX = kStripPad + SP + kStripExtra;
-    float *own = sDyn + (size_t)(wv * P + h) * (6 * SP + 3 * SPX);
+    const int RS = row_stride<P>(SP);
+    float *own = sDyn + (size_t)(wv * P + h) * RS;
     float *rSt = own + 6 * SP + kStripPad, *rFm = rSt + SPX, *rFs = rFm + SPX;
-    float *sUs = sDyn + (size_t)kPolyWaves * P * (6 * SP + 3 * SPX);
+    float *sUs = sDyn + (size_t)kPolyWaves * P * RS;
     if (c < kStripPad) {   // never overwritten: positions before 0 have F = 0, dF = 0
         rSt[c - kStripPad] = 0.0f; rFm[c - kStripPad] = 0.0f; rFs[c - kStripPad] = 0.0f;
     }
@@ -130,15 +121,9 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
         if (hact) { l_mu = mu[(size_t)bh * N + i]; l_sg = W.rsig[(size_t)bh * N + i]; }
         if (lane < nq) {
             l_i = i;
-            int tier = 0;
-            const int g = op_grid(W, pa, B, N, b0, i, tier);
-            if constexpr (P == 1) {
-                l_cls = W.ptier[(size_t)b0 * N + i];   // 0: step by step, else the degree tier
-                l_mine = g == 0;
-            } else {
-                l_cls = g == GI ? tier : 0;
-                l_mine = g == GI;
-            }
+            // tier on its grid (0: step by step); every restart of a pack has the same
+            l_cls = W.gtier[(size_t)b0 * N + i];
+            l_mine = W.gsel[(size_t)b0 * N + i] == GI;
             l_s = G.delay[i];
             l_e0 = G.row_ptr[i]; l_e1 = G.row_ptr[i + 1];
         }
@@ -375,14 +360,12 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
             *gs = kWrite ? acc : *gs + acc;
         }
     }
-    for (int x = threadIdx.x; x < P * kStripMax; x += 64 * kPolyWaves) {
-        const int hh = x / kStripMax, p = x % kStripMax;
+    for (int x = threadIdx.x; x < P * SP; x += 64 * kPolyWaves) {
+        const int hh = x / SP, p = x % SP;
         if (b0 + hh >= B) continue;
         float acc = 0.0f;
-        if (p < SP) {
 #pragma unroll
-            for (int w = 0; w < kPolyWaves; ++w) acc += sUs[(w * P + hh) * SP + p];
-        }
+        for (int w = 0; w < kPolyWaves; ++w) acc += sUs[(w * P + hh) * SP + p];
         float *usg = W.Ustrip + slot_of(b0 + hh) * kStripMax + p;
         *usg = kWrite ? acc : *usg + acc;
     }
@@ -824,7 +807,7 @@ __global__ __launch_bounds__(64 * kPolyWaves) void k_mem_poly_bwd(Graph G, PolyA
 // ---------------------------------------------------------------------------
 hipError_t launch_poly(const Graph &g, const Work &w, const PolyArgs &pa, const float *mu, const float *sigma,
                        hipStream_t st) {
-    const size_t lds = sizeof(float) * (size_t)kPolyWaves * (10 * pa.SP + 3 * (kStripPad + kStripExtra));
+    const size_t lds = sizeof(float) * (size_t)kPolyWaves * (row_stride<1>(pa.SP) + pa.SP);
     const dim3 grid(g.ngroups * pa.split, g.B), block(64 * kPolyWaves);
     // packed grid G_: restart packs of P_ on the y axis, per-(wave, restart) LDS rows
     auto packed = [&](auto fam_tag, auto p_tag) {
@@ -832,8 +815,8 @@ hipError_t launch_poly(const Graph &g, const Work &w, const PolyArgs &pa, const 
         constexpr int G_ = P_ == 2 ? 1 : 2;
         const GridArgs &gd = pa.gr[G_];
         if (!gd.on) return;
-        const size_t ldsp = sizeof(float) * (size_t)kPolyWaves * P_ * (10 * gd.SP + 3 * (kStripPad + kStripExtra));
-        const dim3 gridp(g.ngroups * pa.split, (g.B + P_ - 1) / P_);
+        const size_t ldsp = sizeof(float) * (size_t)kPolyWaves * P_ * (row_stride<P_>(gd.SP) + gd.SP);
+        const dim3 gridp(g.ngroups * gd.split, (g.B + P_ - 1) / P_);
         hipLaunchKernelGGL((k_poly<1, kPolyAll, FAM, P_>), gridp, block, ldsp, st, g, pa, mu, sigma, w);
     };
     auto run = [&](auto fam_tag) -> hipError_t {
