@@ -179,62 +179,73 @@ __global__ __launch_bounds__(256) void k_grid(Graph G, PolyArgs pa, Work W) {
 constexpr int kUcEntries = kMaxChunks * kNC + kStripMax;   // per (restart, type, grid)
 
 constexpr int kUcoefRows = 16;   // work-group = 64 entries x 16 strided partial sums
+constexpr int kUcoefMaxSlots = 4096;   // slots of one type listed in LDS
 
 __global__ __launch_bounds__(64 * kUcoefRows) void k_ucoef(Graph G, PolyArgs pa, Work W) {
     __shared__ float part[kUcoefRows][64];
+    __shared__ int sGrp[64 * kUcoefRows];
+    __shared__ int sSlot[kUcoefMaxSlots];
+    __shared__ int wcnt[kUcoefRows];
     const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
     const int x = blockIdx.x * 64 + tx, k = blockIdx.y, b = blockIdx.z / kGrids, gi = blockIdx.z % kGrids;
     const GridArgs &gd = pa.gr[gi];
-    if (!gd.on) return;
-    // the type's polynomial work-groups: slots [g0*split, g1*split) of restart b
-    const int g0 = G.type_grp[k] * gd.split, g1 = G.type_grp[k + 1] * gd.split;
-    const size_t rb = (size_t)gd.slot_base + (size_t)b * G.ngroups * gd.split;
-    const int ncoef = gd.nc * kNC;
-    float acc = 0.0f;
+    const int ncoef = gd.nc * kNC, nent = ncoef + gd.SP;
+    if (!gd.on || blockIdx.x * 64 >= nent) return;
+    const int split = gd.split;
+    const size_t rb = (size_t)gd.slot_base + (size_t)b * G.ngroups * split;
     // the type's groups with ops on the grid, compacted in order (their
     // work-groups wrote every slot; the others wrote nothing)
-    __shared__ int sGrp[64 * kUcoefRows];
-    __shared__ int wcnt[kUcoefRows];
     const unsigned char *work = W.gwork + ((size_t)gi * G.B + b) * G.ngroups;
     const int t0 = G.type_grp[k], t1 = G.type_grp[k + 1];
-    int ng = -1;   // -1: more groups than one pass of the work-group lists
+    float acc = 0.0f;
     if (t1 - t0 <= 64 * kUcoefRows) {
         const int q = t0 + (int)threadIdx.x;
         const bool f = q < t1 && work[q];
         const unsigned long long bal = __ballot(f);
         if (tx == 0) wcnt[ty] = __popcll(bal);
         __syncthreads();
-        int off = 0;
-        ng = 0;
+        int off = 0, ng = 0;
 #pragma unroll
         for (int w = 0; w < kUcoefRows; ++w) { off += w < ty ? wcnt[w] : 0; ng += wcnt[w]; }
         if (f) sGrp[off + __popcll(bal & ((1ull << tx) - 1ull))] = q;
         __syncthreads();
-    }
-    const int split = gd.split;
-    if (ng >= 0) {
         const int nsl = ng * split;
-        if (x < ncoef) {
+        if (nsl <= kUcoefMaxSlots) {
+            // the listed groups' slots, then row ty sums slots ty, ty + 16, ...
+            for (int q2 = threadIdx.x; q2 < nsl; q2 += 64 * kUcoefRows)
+                sSlot[q2] = sGrp[q2 / split] * split + q2 % split;
+            __syncthreads();
+            if (x < ncoef) {
 #pragma unroll 4
-            for (int q = ty; q < nsl; q += kUcoefRows)
-                acc += W.Ucoef[(rb + (size_t)sGrp[q / split] * split + q % split) * kMaxChunks * kNC + x];
-        } else if (x < ncoef + gd.SP) {
+                for (int q2 = ty; q2 < nsl; q2 += kUcoefRows) acc += W.Ucoef[(rb + sSlot[q2]) * kMaxChunks * kNC + x];
+            } else if (x < nent) {
 #pragma unroll 4
-            for (int q = ty; q < nsl; q += kUcoefRows)
-                acc += W.Ustrip[(rb + (size_t)sGrp[q / split] * split + q % split) * kStripMax + (x - ncoef)];
+                for (int q2 = ty; q2 < nsl; q2 += kUcoefRows) acc += W.Ustrip[(rb + sSlot[q2]) * kStripMax + (x - ncoef)];
+            }
+        } else {
+            for (int j = ty; j < ng; j += kUcoefRows) {
+                const size_t s0 = rb + (size_t)sGrp[j] * split;
+                if (x < ncoef) {
+                    for (int u = 0; u < split; ++u) acc += W.Ucoef[(s0 + u) * kMaxChunks * kNC + x];
+                } else if (x < nent) {
+                    for (int u = 0; u < split; ++u) acc += W.Ustrip[(s0 + u) * kStripMax + (x - ncoef)];
+                }
+            }
         }
-    } else {   // more groups than the list holds: test each
-        if (x < ncoef) {
-            for (int g = g0 + ty; g < g1; g += kUcoefRows)
-                if (work[g / split]) acc += W.Ucoef[(rb + g) * kMaxChunks * kNC + x];
-        } else if (x < ncoef + gd.SP) {
-            for (int g = g0 + ty; g < g1; g += kUcoefRows)
-                if (work[g / split]) acc += W.Ustrip[(rb + g) * kStripMax + (x - ncoef)];
+    } else {   // more groups than one pass lists: test each
+        for (int g = t0 + ty; g < t1; g += kUcoefRows) {
+            if (!work[g]) continue;
+            const size_t s0 = rb + (size_t)g * split;
+            if (x < ncoef) {
+                for (int u = 0; u < split; ++u) acc += W.Ucoef[(s0 + u) * kMaxChunks * kNC + x];
+            } else if (x < nent) {
+                for (int u = 0; u < split; ++u) acc += W.Ustrip[(s0 + u) * kStripMax + (x - ncoef)];
+            }
         }
     }
     part[ty][tx] = acc;
     __syncthreads();
-    if (ty == 0 && x < ncoef + gd.SP) {
+    if (ty == 0 && x < nent) {
         float t = 0.0f;
 #pragma unroll
         for (int r = 0; r < kUcoefRows; ++r) t += part[r][tx];
