@@ -578,7 +578,6 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     AL(rsig, BN);
     AL(dflag, BN);
     AL(ptier, BN);
-    AL(ptpk, (size_t)(kGrids - 1) * BN);
     AL(gflag, (size_t)B * g.ngroups);
     AL(gnarrow, (size_t)B * g.ngroups);
     AL(gsum_ops, (size_t)B * g.ngroups * ntiles * 2);
@@ -603,7 +602,6 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
         if (e == hipSuccess) e = hipMemset(c->w.gsum_poly, 0, sizeof(float) * (size_t)std::max(c->poly_slots, 1) * 2);
         if (e == hipSuccess) e = hipMemset(c->w.gsel, kNoGrid, BN);
         if (e == hipSuccess) e = hipMemset(c->w.gwork, 0, (size_t)kGrids * B * g.ngroups);
-        if (e == hipSuccess) e = hipMemset(c->w.ptpk, 0, (size_t)(kGrids - 1) * BN);
         if (e == hipSuccess) e = hipDeviceSynchronize();
         if (e != hipSuccess) { s = fail(nullptr, GAUS_E_DEVICE, "init: %s", hipGetErrorString(e)); goto fail_alloc; }
     }

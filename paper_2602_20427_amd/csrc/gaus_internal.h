@@ -149,9 +149,6 @@ struct Work {
     unsigned char *dflag;  // [B][N]        1 = op has step-by-step work (own terms or out-edges)
     unsigned char *ptier;  // [B][N]        polynomial op: tier of its vectors, the smallest over
                            //               itself and its polynomial consumers (highest degree)
-    unsigned char *ptpk;   // [kGrids-1][B][N]  tier of the op's vectors on packed grid 1, 2 if the
-                           //               op and all its consumers meet that grid's degree-8
-                           //               bound, else 0
     int *gflag;       // [B][ngroups]      1 = some op of the group has step-by-step work
     int *gnarrow;     // [B][ngroups]      1 = some op of the group takes polynomial degree 8 or 6
     float *gsum_ops;  // [B][ngroups][ntiles][2]  V_dep, L_com of a k_ops work-group

@@ -66,38 +66,53 @@ __device__ __forceinline__ int grid_tier(const GridArgs &gr, float s, int delay)
     return t;
 }
 
-// Classification and work flags.  Work-group = (op group, restart), thread
-// per op (groups hold at most 256 ops, and together every op):
+// Classification and work flags.  Work-group = (op group, pack of kFlagPack
+// restarts), thread per (restart of the pack, op) (groups hold at most 256
+// ops, and together every op):
 //   * 1/sigma and the op's path (tier) for the other kernels;
 //   * step-by-step work of the op: its own path, or an out-edge to an op off
 //     the polynomial path; of the group: any such op;
 //   * a polynomial producer's tier: the highest degree among itself and its
 //     polynomial consumers; of the group: whether the degree-8/6 kernel has
 //     work in it;
-//   * on each packed grid: the same tier if the op and all its consumers
-//     meet the grid's degree-8 bound, else 0 (the kernels then combine the
-//     restarts of a pack).
+//   * its grid: the coarsest packed grid whose whole restart pack (the
+//     restarts < B of [P floor(b/P), P floor(b/P) + P)) has the op and all
+//     its consumers reach the grid's degree-8 bound, with the pack's tier
+//     (the highest degree of its members'); else grid 0 with the op's own
+//     tier, or kNoGrid on the step-by-step path; per (grid, restart, group)
+//     whether any op is there (grid 0 also: step-by-step ops, whose
+//     polynomial records it clears).
 // The consumers' tiers are recomputed here from their sigmas.  With the
 // storage term on, also whether a holder's storage term is taken on the
 // chunk polynomials (Gaussian start times only; kMemPolyDeg, kMemRhoMax).
-__global__ __launch_bounds__(256) void k_flags(Graph G, PolyArgs pa, const float *__restrict__ sigma, Work W,
-                                               int mem_on) {
-    const int grp = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+constexpr int kFlagPack = 4;   // the largest restart pack of a grid
+static_assert(kGridP[kGrids - 1] == kFlagPack, "packs nest in the flag kernel's restarts");
+
+__global__ __launch_bounds__(256 * kFlagPack) void k_flags(Graph G, PolyArgs pa, const float *__restrict__ sigma,
+                                                           Work W, int mem_on) {
+    __shared__ unsigned char sTp[kFlagPack][kGrids][256];   // tier on each packed grid, 0 if not eligible
+    __shared__ int wor[256 * kFlagPack / 64];
+    const int grp = blockIdx.x, q = threadIdx.x >> 8, op = threadIdx.x & 255;
+    const int b = blockIdx.y * kFlagPack + q, lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
     const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
-    const float *sgb = sigma + (size_t)b * G.N;
-    int d = 0, narrow = 0;
-    if (q0 + tid < q1) {
-        const int i = G.perm[q0 + tid];
-        const size_t bi = (size_t)b * G.N + i;
+    const int N = G.N, nb = min(kFlagPack, G.B - (int)blockIdx.y * kFlagPack);
+    const bool act = q < nb && q0 + op < q1;
+    int d = 0, narrow = 0, sel = -1, t = 0, ci = 0;
+    size_t bi = 0;
+    if (act) {
+        const int i = G.perm[q0 + op];
+        bi = (size_t)b * N + i;
+        const float *sgb = sigma + (size_t)b * N;
         const float s = sgb[i];
         W.rsig[bi] = 1.0f / s;
-        const int ci = poly_tier(pa, s, G.delay[i]);
+        const int di = G.delay[i];
+        ci = poly_tier(pa, s, di);
         W.cls[bi] = (unsigned char)ci;
         d = ci ? 0 : 1;
-        int t = ci;
-        int tp[kGrids - 1];
+        t = ci;
+        int tp[kGrids];   // [0] unused
 #pragma unroll
-        for (int g = 1; g < kGrids; ++g) tp[g - 1] = grid_tier(pa.gr[g], s, G.delay[i]);
+        for (int g = 1; g < kGrids; ++g) tp[g] = grid_tier(pa.gr[g], s, di);
         const int e0 = G.row_ptr[i], e1 = G.row_ptr[i + 1];
         float rsum = 1.0f / s;   // sum of 1/sigma over the holder and its successors
         for (int e = e0; e < e1; ++e) {
@@ -110,63 +125,58 @@ __global__ __launch_bounds__(256) void k_flags(Graph G, PolyArgs pa, const float
 #pragma unroll
             for (int g = 1; g < kGrids; ++g) {
                 const int c = grid_tier(pa.gr[g], sj, dj);
-                tp[g - 1] = c ? min(tp[g - 1], c) : 0;
+                tp[g] = c ? min(tp[g], c) : 0;
             }
             if (mem_on) rsum += 1.0f / sj;
         }
 #pragma unroll
-        for (int g = 1; g < kGrids; ++g)
-            W.ptpk[((size_t)(g - 1) * G.B + b) * G.N + i] = (unsigned char)tp[g - 1];
+        for (int g = 1; g < kGrids; ++g) sTp[q][g][op] = (unsigned char)tp[g];
         W.dflag[bi] = (unsigned char)d;
         W.mpoly[bi] = (unsigned char)(mem_on && pa.fam == 0 && ci != 0 && d == 0 && e1 > e0 &&
                                       e1 - e0 <= kMemPolyDeg && pa.lam * rsum <= kMemRhoMax);
         W.ptier[bi] = (unsigned char)t;
         narrow = (t == 1 || t == 2) ? 1 : 0;
     }
-    d = __syncthreads_or(d);
-    narrow = __syncthreads_or(narrow);
-    if (tid == 0) {
-        W.gflag[(size_t)b * G.ngroups + grp] = d ? 1 : 0;
-        W.gnarrow[(size_t)b * G.ngroups + grp] = narrow ? 1 : 0;
-    }
-}
-
-// Grid of every (restart, op) this iteration: the coarsest packed grid whose
-// whole restart pack (the restarts < B of [P floor(b/P), P floor(b/P) + P))
-// has the op qualify (ptpk != 0), with the pack's tier (the smallest, i.e.
-// highest degree, of its members'); else grid 0 with the op's own tier
-// (ptier), or kNoGrid on the step-by-step path.  Per (grid, restart, group)
-// whether any op is there.  Work-group = (op group, restart), thread per op.
-__global__ __launch_bounds__(256) void k_grid(Graph G, PolyArgs pa, Work W) {
-    const int grp = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
-    const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
-    const int N = G.N, B = G.B;
-    int sel = -1;
-    if (q0 + tid < q1) {
-        const int i = G.perm[q0 + tid];
-        const size_t bi = (size_t)b * N + i;
-        int tier = W.ptier[bi];
-        sel = W.cls[bi] ? 0 : kNoGrid;
-        for (int g = kGrids - 1; g >= 1 && sel == 0; --g) {
-            if (!pa.gr[g].on) continue;
-            const int P = kGridP[g], b0 = b - b % P;
-            int t = kTiers;
-            bool ok = true;
-            for (int q = 0; q < P && b0 + q < B; ++q) {
-                const int v = W.ptpk[((size_t)(g - 1) * B + b0 + q) * N + i];
-                ok = ok && v != 0;
-                t = min(t, v);
-            }
-            if (ok) { sel = g; tier = t; }
-        }
-        W.gsel[bi] = (unsigned char)sel;
-        W.gtier[bi] = (unsigned char)(sel == kNoGrid ? 0 : tier);
-    }
+    __syncthreads();
+    if (act) {   // grid: the coarsest packed grid whose pack qualifies
+        int g_sel = ci ? 0 : kNoGrid, tier = t;
 #pragma unroll
-    for (int g = 0; g < kGrids; ++g) {
-        // grid 0 also runs for groups with step-by-step ops (it clears their records)
-        const int any = __syncthreads_or(sel == g || (g == 0 && sel == kNoGrid));
-        if (tid == 0) W.gwork[((size_t)g * B + b) * G.ngroups + grp] = (unsigned char)any;
+        for (int g = kGrids - 1; g >= 1; --g) {
+            if (!pa.gr[g].on || g_sel != 0) continue;
+            const int P = kGridP[g], p0 = q - q % P;
+            int tt = kTiers;
+            bool ok = true;
+            for (int r = p0; r < p0 + P && r < nb; ++r) {
+                const int v = sTp[r][g][op];
+                ok = ok && v != 0;
+                tt = min(tt, v);
+            }
+            if (ok) { g_sel = g; tier = tt; }
+        }
+        sel = g_sel;
+        W.gsel[bi] = (unsigned char)g_sel;
+        W.gtier[bi] = (unsigned char)(g_sel == kNoGrid ? 0 : tier);
+    }
+    // per restart of the pack (256 threads = 4 waves each): OR of the flags
+    auto group_or = [&](int v) {
+        const int w = __any(v) ? 1 : 0;
+        if (lane == 0) wor[wid] = w;
+        __syncthreads();
+        const int r = wor[q * 4] | wor[q * 4 + 1] | wor[q * 4 + 2] | wor[q * 4 + 3];
+        __syncthreads();
+        return r;
+    };
+    const int dq = group_or(d), nq = group_or(narrow);
+    int wk[kGrids];
+#pragma unroll
+    for (int g = 0; g < kGrids; ++g)   // grid 0 also for step-by-step ops (it clears their records)
+        wk[g] = group_or(sel == g || (g == 0 && sel == kNoGrid));
+    if (op == 0 && q < nb) {
+        const size_t bg = (size_t)b * G.ngroups + grp;
+        W.gflag[bg] = dq ? 1 : 0;
+        W.gnarrow[bg] = nq ? 1 : 0;
+#pragma unroll
+        for (int g = 0; g < kGrids; ++g) W.gwork[((size_t)g * G.B + b) * G.ngroups + grp] = (unsigned char)wk[g];
     }
 }
 
@@ -1110,9 +1120,8 @@ hipError_t enqueue_check(const Graph &g, const Work &w, const HP &hp, float *mu,
 // ---------------------------------------------------------------------------
 hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const LaunchCfg &lc,
                              const PolyArgs &pa, const IterArgs &a, hipStream_t st) {
-    hipLaunchKernelGGL(k_flags, dim3(g.ngroups, g.B), dim3(256), 0, st, g, pa, a.sigma, w,
-                       (hp.gamma != 0.0f && pa.enabled) ? 1 : 0);
-    if (pa.enabled) hipLaunchKernelGGL(k_grid, dim3(g.ngroups, g.B), dim3(256), 0, st, g, pa, w);
+    hipLaunchKernelGGL(k_flags, dim3(g.ngroups, (g.B + kFlagPack - 1) / kFlagPack), dim3(256 * kFlagPack), 0, st,
+                       g, pa, a.sigma, w, (hp.gamma != 0.0f && pa.enabled) ? 1 : 0);
     hipError_t e;
     if (a.ops_begin) (void)hipEventRecord(a.ops_begin, st);
     if ((e = launch_ops(g, w, lc, a.mu, a.sigma, st)) != hipSuccess) return e;
