@@ -440,7 +440,12 @@ __device__ __forceinline__ void vec_dFdmu_back(const Expansion<NC> &e, float (&a
     }
 }
 
-// (H p)_k = sum_l H_{k+l} p_l; the chunk points are symmetric, odd moments vanish
+// (H p)_k = sum_l H_{k+l} p_l; the chunk points are symmetric, odd moments
+// vanish.  Only terms with k + l <= NC - 1 are kept: the dot product with a
+// consumer vector q then sums p_l q_k H_{k+l} over total degree k + l <= d
+// (the series degree), i.e. the product p q truncated at degree d like p and
+// q themselves; the dropped terms are O(rho^(d+2)) against O(rho^(d+1)) for
+// the truncation of either series.
 template <int NC>
 __device__ __forceinline__ void vec_moments(const float (&p)[NC], const float (&H)[kDeg + 1], float (&o)[NC]) {
 #pragma unroll
@@ -448,7 +453,7 @@ __device__ __forceinline__ void vec_moments(const float (&p)[NC], const float (&
         float acc = 0.0f;
 #pragma unroll
         for (int l = 0; l < NC; ++l)
-            if (((k + l) & 1) == 0) acc = fmaf(H[(k + l) / 2], p[l], acc);
+            if (((k + l) & 1) == 0 && k + l <= NC - 1) acc = fmaf(H[(k + l) / 2], p[l], acc);
         o[k] = acc;
     }
 }
