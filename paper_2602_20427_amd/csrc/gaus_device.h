@@ -418,24 +418,29 @@ __device__ __forceinline__ void vec_times_z(const float (&a)[NC], float zc, floa
     for (int k = 1; k < NC; ++k) o[k] = fmaf(zc, a[k], r * a[k - 1]);
 }
 
-template <int NC>
-__device__ __forceinline__ void vec_mass(const Expansion<NC> &e, float (&m)[NC]) {
+// The shift series take the coefficients the expansion holds (T_n, n < NT):
+// with NT = NC + 1 a coefficient of degree k gets min(kShiftTerms, NC - k)
+// terms, the rest being of the order of the series' own truncation.
+template <int NC, int NT>
+__device__ __forceinline__ void vec_mass(const Expansion<NC, NT> &e, float (&m)[NC]) {
 #pragma unroll
     for (int k = 0; k < NC; ++k) {
         float acc = 0.0f;
 #pragma unroll
-        for (int j = kShiftTerms; j >= 1; --j) acc = fmaf(mass_coef(k, j), e.T[k + j], acc);
+        for (int j = kShiftTerms; j >= 1; --j)
+            if (k + j < NT) acc = fmaf(mass_coef(k, j), e.T[k + j], acc);
         m[k] = acc;
     }
 }
 
-template <int NC>
-__device__ __forceinline__ void vec_dFdmu_back(const Expansion<NC> &e, float (&a)[NC]) {
+template <int NC, int NT>
+__device__ __forceinline__ void vec_dFdmu_back(const Expansion<NC, NT> &e, float (&a)[NC]) {
 #pragma unroll
     for (int k = 0; k < NC; ++k) {
         float acc = 0.0f;
 #pragma unroll
-        for (int j = kShiftTerms; j >= 0; --j) acc = fmaf(back_coef(k, j), e.T[k + 1 + j], acc);
+        for (int j = kShiftTerms; j >= 0; --j)
+            if (k + 1 + j < NT) acc = fmaf(back_coef(k, j), e.T[k + 1 + j], acc);
         a[k] = acc;
     }
 }
@@ -467,16 +472,16 @@ __device__ __forceinline__ float vdot(const float (&a)[NC], const float (&b)[NC]
 }
 
 // dot with 1 - F given F's coefficients and the precise 1 - F(z0)
-template <int NC>
-__device__ __forceinline__ float vdot_1mF(const float (&a)[NC], const Expansion<NC> &e) {
+template <int NC, int NT>
+__device__ __forceinline__ float vdot_1mF(const float (&a)[NC], const Expansion<NC, NT> &e) {
     float acc = a[0] * e.G0;
 #pragma unroll
     for (int k = 1; k < NC; ++k) acc = fmaf(-a[k], e.T[k], acc);
     return acc;
 }
 
-template <int NC>
-__device__ __forceinline__ float vdot_F(const float (&a)[NC], const Expansion<NC> &e) {
+template <int NC, int NT>
+__device__ __forceinline__ float vdot_F(const float (&a)[NC], const Expansion<NC, NT> &e) {
     float acc = 0.0f;
 #pragma unroll
     for (int k = 0; k < NC; ++k) acc = fmaf(a[k], e.T[k], acc);

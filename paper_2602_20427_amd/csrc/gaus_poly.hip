@@ -21,6 +21,8 @@ constexpr int kStripPad = kSmax; // zero slots before position 0 (positions -kSm
 // work-groups without such ops exit at once.  The packed grids run every
 // tier in one kernel (kPolyAll), which writes its grid's outputs.
 constexpr int kPolyWide = 3, kPolyNarrow = 12, kPolyAll = 15;
+// Taylor coefficients kept past the degree (the shift series' extra terms)
+constexpr int kPolyExtraT = 2;
 
 // LDS floats per (wave, restart) of k_poly: 6 rows of SP strip values and 3
 // rows of SP + kStripExtra raw CDF values after kStripPad zeros; with P > 1
@@ -208,7 +210,7 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
         // out-edges below and the usage readers never use)
         float HF[NC], HFm[NC], HFs[NC], HA[NC], HFm1[NC], HFs1[NC];
         {
-            Expansion<NC> ea;
+            Expansion<NC, NC + kPolyExtraT> ea;
             expand<FAM>(m_i, rs, tcen, ea);
             float v[NC], w[NC];
             vec_mass(ea, v);
@@ -222,9 +224,9 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
             vec_times_z(v, ea.z0, ea.r, w);
             vec_moments(w, gd.H, HFs);
             // shifted functions: A(u) = mass at u-s+1, dF(u-s)
-            Expansion<NC> es;
+            Expansion<NC, NC + kPolyExtraT> es;
             if (s != 1) expand<FAM>(m_i, rs, tcen - (float)(s - 1), es);
-            const Expansion<NC> &ex = (s != 1) ? es : ea;
+            const Expansion<NC, NC + kPolyExtraT> &ex = (s != 1) ? es : ea;
             vec_mass(ex, v);
             vec_moments(v, gd.H, HA);
             vec_dFdmu_back(ex, v);
@@ -288,7 +290,7 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
                 }
             }
             if (cact) {
-                Expansion<NC> ej;
+                Expansion<NC, NC + kPolyExtraT> ej;
                 expand<FAM>(m_j, rsj, tcen, ej);
                 float a[NC], v[NC];
                 pr[0] += vdot_F(HA, ej);
