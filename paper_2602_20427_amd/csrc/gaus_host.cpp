@@ -230,6 +230,7 @@ struct HostGraph {
     std::vector<int> pred_ptr, pred_eid, pred_src;
     std::vector<int> bin_ptr, bin, bout_ptr, bout;
     std::vector<int> level, lvl_ptr, lvl_ops;
+    std::vector<int> leg_items, leg_over;   // legalization items in level order (see Graph::leg_items)
     std::vector<int> asap, alap;
     std::vector<int> perm, grp_start, type_grp, grp_of;
     std::vector<int> big_ops, big_of;
@@ -513,6 +514,41 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
         c->poly_slots = base;
     }
     g.nlevels = (int)h.lvl_ptr.size() - 1;
+    {
+        // one 32-byte item per op in level order: op, delay, predecessor
+        // count, start of the ones past kLegPre in leg_over, first kLegPre
+        h.leg_items.assign((size_t)8 * std::max(h.N, 1), 0);
+        h.leg_over.clear();
+        for (int q = 0; q < h.N; ++q) {
+            const int v = h.lvl_ops[q], p0 = h.pred_ptr[v], n = h.pred_ptr[v + 1] - p0;
+            int *it = &h.leg_items[(size_t)8 * q];
+            it[0] = v; it[1] = h.delay[v]; it[2] = n; it[3] = (int)h.leg_over.size();
+            for (int k = 0; k < n; ++k) {
+                if (k < kLegPre) it[4 + k] = h.pred_src[p0 + k];
+                else h.leg_over.push_back(h.pred_src[p0 + k]);
+            }
+        }
+        if (h.leg_over.empty()) h.leg_over.push_back(0);
+    }
+    {
+        // legalization schedule in LDS when it fits: 16-bit ready times for
+        // II = 0 (every s stays in [ASAP, ALAP] within [0, D-1]); 32-bit ones
+        // and their pass snapshot for II > 0 while D + dmax + N^2 dmax (a
+        // bound on what N passes can reach) stays below 2^31
+        int lds = 0;
+        if (hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerBlock, c->device) != hipSuccess)
+            lds = 65536;
+        const long long budget = std::min(lds, 160 * 1024) - 2048;
+        long long dmax = 0;
+        for (int d : h.delay) dmax = std::max<long long>(dmax, d);
+        const long long N = h.N;
+        const long long room = budget - 4LL * ((g.nlevels + 1 + 3) & ~3);   // after the level bounds
+        g.leg_mode = 0;
+        if (h.II == 0 && (long long)h.D + dmax < 32767 && 2 * N <= room) g.leg_mode = 1;
+        else if (h.II == 0 && (long long)h.D + dmax < (1LL << 31) - 1 && 4 * N <= room) g.leg_mode = 2;
+        else if (h.II > 0 && (long long)h.D + dmax + N * N * (dmax + 1) < (1LL << 31) - 1 && 8 * N <= room)
+            g.leg_mode = 2;
+    }
     std::vector<float> cap(h.cap);
     const size_t BN = (size_t)B * h.N;
 #define UP(field, vec) do { s = dupload(c, &g.field, vec); if (s != GAUS_OK) goto fail_alloc; } while (0)
@@ -521,6 +557,7 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     UP(bsrc, h.bsrc); UP(bdst, h.bdst); UP(bdist, h.bdist); UP(bin_ptr, h.bin_ptr); UP(bin, h.bin);
     UP(bout_ptr, h.bout_ptr); UP(bout, h.bout); UP(perm, h.perm); UP(grp_start, h.grp_start);
     UP(type_grp, h.type_grp); UP(lvl_ptr, h.lvl_ptr); UP(lvl_ops, h.lvl_ops); UP(asap, h.asap);
+    UP(leg_items, h.leg_items); UP(leg_over, h.leg_over);
     UP(grp_of, h.grp_of);
     UP(bmem, h.bmem);
     UP(big_ops, h.big_ops);

@@ -17,6 +17,7 @@ constexpr int kBP = 5;   // per (restart, back edge, tile): V_rec, dVrec/dmu_j, 
                          //   (producer j), dVrec/dmu_i, dVrec/dsigma_i (consumer i)
 constexpr int kHalo = 256;  // largest producer delay handled from the LDS row window
 constexpr int kBigIn = 64;  // in-degree above which an op's in-edge records are reduced by a work-group
+constexpr int kLegPre = 4;  // predecessors held in a legalization item
 constexpr int kCost = 6;    // per schedule: cost, L_com, L_res, L_mem, V_res, legal
 constexpr int kTerms = 7;   // per restart: L, V_dep, V_res, V_rec, L_com, L_res, L_mem
 
@@ -81,6 +82,7 @@ struct Graph {
     int tile, ntiles;          // steps per tile of the op kernel, tiles per restart
     int ngroups;               // type-pure op groups (one work-group each per tile)
     int nlevels;               // topological levels (legalization)
+    int leg_mode;              // legalization schedule: 0 global int64, 1 LDS int16, 2 LDS int32
     const int *row_ptr, *col;            // CSR by producer
     const int *pred_ptr, *pred_eid;      // CSC: CSR edge id of each in-edge
     const int *pred_src;                 // CSC: producer of each in-edge
@@ -93,6 +95,10 @@ struct Graph {
     const int *grp_start;                // [ngroups+1] ranges of perm
     const int *type_grp;                 // [K+1] groups of type k: [type_grp[k], type_grp[k+1])
     const int *lvl_ptr, *lvl_ops;        // ops by (topological level, id)
+    const int *leg_items;                // [N][8] per op in level order: op, delay, predecessor count,
+                                         // start of the predecessors past kLegPre in leg_over, the first
+                                         // kLegPre predecessors (32-byte aligned)
+    const int *leg_over;                 // predecessors past the first kLegPre, in level order
     const int *grp_of;                   // [N] group of each op
     const float *bmem;                   // [N] storage units b_i
     int nbig;                            // ops with more than kBigIn predecessors

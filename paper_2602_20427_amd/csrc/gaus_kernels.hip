@@ -907,6 +907,166 @@ __global__ __launch_bounds__(kLegBS) void k_legalize(Graph G, Work W, const floa
     if (tid == 0) W.status[b] = st;
 }
 
+// The same with the schedule in LDS (chosen on the host when it fits:
+// 16-bit entries for II = 0 with D < 2^15, where every value stays in
+// [ASAP, ALAP]; 32-bit entries, with the pass snapshot beside them, for
+// II > 0 when no value can leave the 32-bit range).  LDS holds the ready
+// time r_v = s_v + Lat_v, so a predecessor costs one LDS read; each thread's
+// op of the next level is loaded during the current level as one 32-byte
+// item (op, delay, predecessor count, the first kLegPre predecessors), so the
+// per-level barrier does not wait on dependent global loads.
+constexpr int kLegLdsBS = 1024;
+constexpr int kLegInitU = 4;    // ops per thread and round of the initial rounding (loads in flight)
+
+// Work-group barrier for LDS-only communication: waits for this wave's LDS
+// accesses (lgkmcnt 0), not for its global loads, so loads issued for later
+// levels stay in flight across it (__syncthreads would also wait for them).
+__device__ __forceinline__ void lds_barrier() {
+    __asm__ volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // vmcnt 63, expcnt 7, lgkmcnt 0
+    __builtin_amdgcn_s_barrier();
+    __asm__ volatile("" ::: "memory");
+}
+
+struct LegItem {
+    int v, dv, n, p0;
+    int u[kLegPre];
+};
+
+// Item q, clamped into [0, N) (the caller tests q against its level's end):
+// the load is issued on every path, which keeps its wait count predictable.
+__device__ __forceinline__ void leg_load(const Graph &G, int q, int q1, LegItem &it) {
+    (void)q1;
+    const size_t qc = (size_t)min(q, G.N - 1);
+    const int4 a = reinterpret_cast<const int4 *>(G.leg_items)[2 * qc];
+    const int4 c = reinterpret_cast<const int4 *>(G.leg_items)[2 * qc + 1];
+    it.v = a.x; it.dv = a.y; it.n = a.z; it.p0 = a.w;
+    it.u[0] = c.x; it.u[1] = c.y; it.u[2] = c.z; it.u[3] = c.w;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kLegLdsBS) void k_legalize_lds(Graph G, Work W, const float *__restrict__ mu,
+                                                         int *sched) {
+    extern __shared__ __align__(16) unsigned char sDynLeg[];
+    const int nl = G.nlevels, nlp = (nl + 1 + 3) & ~3;
+    int *lp = reinterpret_cast<int *>(sDynLeg);         // level bounds (lvl_ptr)
+    T *rd = reinterpret_cast<T *>(lp + nlp);            // ready times s_v + Lat_v
+    T *rp = rd + G.N;                                  // II > 0: their snapshot at the start of a pass
+    __shared__ int changed, over;
+    const int b = blockIdx.x, tid = threadIdx.x;
+    const int N = G.N, D = G.D;
+    for (int l = tid; l <= nl; l += kLegLdsBS) lp[l] = G.lvl_ptr[l];
+    for (int v0 = tid; v0 < N; v0 += kLegInitU * kLegLdsBS) {
+        float m[kLegInitU];
+        int lo[kLegInitU], hi[kLegInitU], dl[kLegInitU];
+#pragma unroll
+        for (int k = 0; k < kLegInitU; ++k) {
+            const int v = v0 + k * kLegLdsBS;
+            if (v < N) {
+                m[k] = mu[(size_t)b * N + v];
+                lo[k] = G.II == 0 ? G.asap[v] : 0;
+                hi[k] = G.II == 0 ? G.alap[v] : D - 1;
+                dl[k] = G.delay[v];
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < kLegInitU; ++k) {
+            const int v = v0 + k * kLegLdsBS;
+            if (v < N) {
+                long long r = round_half_up(m[k], D);
+                r = r < lo[k] ? lo[k] : (r > hi[k] ? hi[k] : r);
+                rd[v] = (T)(r + dl[k]);
+            }
+        }
+    }
+    __syncthreads();
+    int st = 0;
+    // levels l0.. of one sweep; each thread's first item of a level is loaded
+    // two levels ahead into one of two buffers (A: levels l0, l0+2, ...; B:
+    // l0+1, ...), reloaded right after its level is done, so no register
+    // rotation makes the next level wait for the newest loads
+    auto process = [&](const LegItem it, bool modulo) {
+        const int v = it.v;
+        long long req = modulo ? 0 : (long long)rd[v] - it.dv;
+#pragma unroll
+        for (int k = 0; k < kLegPre; ++k)
+            if (k < it.n) req = max(req, (long long)rd[it.u[k]]);
+        for (int k = kLegPre; k < it.n; ++k) req = max(req, (long long)rd[G.leg_over[it.p0 + k - kLegPre]]);
+        if (modulo) {
+            for (int r = G.bin_ptr[v]; r < G.bin_ptr[v + 1]; ++r) {
+                const int e = G.bin[r], j = G.bsrc[e];
+                req = max(req, (long long)rp[j] - (long long)G.bdist[e] * G.II);
+            }
+            if (req > (long long)rd[v] - it.dv) { rd[v] = (T)(req + it.dv); changed = 1; }
+        } else {
+            rd[v] = (T)(req + it.dv);
+        }
+    };
+    auto level = [&](int l, LegItem cur, bool modulo) -> LegItem {
+        const int qa = lp[l], qb = lp[l + 1];
+        if (qa + tid < qb) process(cur, modulo);
+        for (int q = qa + tid + kLegLdsBS; q < qb; q += kLegLdsBS) {   // levels wider than the work-group
+            LegItem it;
+            leg_load(G, q, qb, it);
+            process(it, modulo);
+        }
+        const int l2 = min(l + 2, nl - 1);   // past the last level: a valid, unused item
+        leg_load(G, lp[l2] + tid, lp[l2 + 1], cur);
+        lds_barrier();
+        return cur;
+    };
+    auto sweep = [&](int l0, bool modulo) {
+        LegItem A{}, B{};
+        leg_load(G, lp[l0] + tid, lp[l0 + 1], A);
+        const int l1 = min(l0 + 1, nl - 1);
+        leg_load(G, lp[l1] + tid, lp[l1 + 1], B);
+        for (int l = l0; l < nl; l += 2) {
+            A = level(l, A, modulo);
+            if (l + 1 < nl) B = level(l + 1, B, modulo);
+        }
+    };
+    if (G.II == 0) {
+        if (G.nlevels > 1) sweep(1, false);
+    } else {
+        int converged = 0;
+        for (int pass = 0; pass < (N > 0 ? N : 1); ++pass) {
+            for (int v = tid; v < N; v += kLegLdsBS) rp[v] = rd[v];
+            if (tid == 0) changed = 0;
+            __syncthreads();
+            if (G.nlevels > 0) sweep(0, true);
+            const int ch = changed;
+            __syncthreads();
+            if (!ch) { converged = 1; break; }
+        }
+        if (!converged) {
+            st = 4;  // GAUS_E_NOT_CONVERGED
+        } else {
+            if (tid == 0) over = 0;
+            __syncthreads();
+            for (int v = tid; v < N; v += kLegLdsBS)
+                if ((long long)rd[v] - G.delay[v] > D - 1) over = 1;
+            __syncthreads();
+            st = over ? 5 : 0;  // GAUS_E_OVERFLOW
+        }
+    }
+    for (int v = tid; v < N; v += kLegLdsBS) sched[(size_t)b * N + v] = (int)((long long)rd[v] - G.delay[v]);
+    if (tid == 0) W.status[b] = st;
+}
+
+// Legalization of every restart with the variant the host chose (Graph::leg_mode).
+hipError_t launch_legalize(const Graph &g, const Work &w, const float *mu, int *sched, hipStream_t st) {
+    const size_t lvl = sizeof(int) * (size_t)((g.nlevels + 1 + 3) & ~3);
+    if (g.leg_mode == 1)
+        hipLaunchKernelGGL(k_legalize_lds<short>, dim3(g.B), dim3(kLegLdsBS), lvl + sizeof(short) * (size_t)g.N, st,
+                           g, w, mu, sched);
+    else if (g.leg_mode == 2)
+        hipLaunchKernelGGL(k_legalize_lds<int>, dim3(g.B), dim3(kLegLdsBS),
+                           lvl + sizeof(int) * (size_t)g.N * (g.II > 0 ? 2 : 1), st, g, w, mu, sched);
+    else
+        hipLaunchKernelGGL(k_legalize, dim3(g.B), dim3(kLegBS), 0, st, g, w, mu, sched);
+    return hipGetLastError();
+}
+
 // ---------------------------------------------------------------------------
 // Discrete cost of integer schedules (Sec. 2.1): usage counts per (type,
 // slot), storage held from s_i until the last successor starts (eq:mem) as a
@@ -1105,9 +1265,10 @@ hipError_t enqueue_best_init(const Graph &g, const Work &w, double *best_cost, h
 
 hipError_t enqueue_check(const Graph &g, const Work &w, const HP &hp, float *mu, float *sigma, float *m,
                          float *v, int *best_sched, double *best_cost, int reinit_sigma, hipStream_t st) {
-    hipLaunchKernelGGL(k_legalize, dim3(g.B), dim3(kLegBS), 0, st, g, w, mu, w.cand);
+    hipError_t e = launch_legalize(g, w, mu, w.cand, st);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_round_cmp, dim3(g.B), dim3(256), 0, st, g, w, mu);
-    hipError_t e = enqueue_schedule_cost(g, w, hp, w.cand, w.cand_cost, st);
+    e = enqueue_schedule_cost(g, w, hp, w.cand, w.cand_cost, st);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_best_update, dim3(g.B), dim3(256), 0, st, g, w, best_sched, best_cost);
     hipLaunchKernelGGL(k_reinit, dim3((g.N + 255) / 256, g.B), dim3(256), 0, st, g, w, hp, best_sched, mu, sigma,
@@ -1184,8 +1345,7 @@ hipError_t enqueue_adam_from_grad(const Graph &g, const Work &w, const HP &hp, c
 
 hipError_t enqueue_legalize(const Graph &g, const Work &w, const float *mu, int *sched,
                             hipStream_t st) {
-    hipLaunchKernelGGL(k_legalize, dim3(g.B), dim3(kLegBS), 0, st, g, w, mu, sched);
-    return hipGetLastError();
+    return launch_legalize(g, w, mu, sched, st);
 }
 
 }  // namespace gaus

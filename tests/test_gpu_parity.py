@@ -409,10 +409,17 @@ def test_step_equals_loss_grad_plus_adam_bitwise():
     ca.close(); cb.close()
 
 
-@pytest.mark.parametrize("cfg,II", [("small", 0), ("medium", 0), ("pipelined", 64)])
-def test_legalize_bit_exact(cfg, II):
+@pytest.mark.parametrize("cfg,II,D", [("small", 0, 0), ("medium", 0, 0), ("pipelined", 64, 0), ("large", 0, 0),
+                                      ("large", 0, 40000)])
+def test_legalize_bit_exact(cfg, II, D):
+    """Alg. 3 / Alg. 4 bit for bit against the oracle, with the schedule in
+    LDS as 16-bit ready times (II = 0, D < 2^15), as 32-bit ones with the
+    pass snapshot (modulo), and in HBM (50k ops at D = 40000: neither fits)."""
+    import dataclasses
     import torch
     p = make_problem(cfg, seed=2)
+    if D:
+        p = dataclasses.replace(p, D=D)
     B = 4
     rng = np.random.default_rng(30)
     mu = rng.uniform(-3, p.D + 3, size=(B, p.n_ops)).astype(np.float32)
