@@ -45,6 +45,7 @@ class WorkloadConfig:
     lr: float = 1e-2
     init: str = "asap_alap"     # "asap_alap" (paper init) or "uniform" (mu~U[0,D), sigma=sigma0)
     sigma0: float = 1.0
+    tight_slack: int = 0        # > 0: D = (longest delay-weighted path to a start) + tight_slack
 
 
 def _zipf_probs(k: int, s: float) -> tuple:
@@ -64,6 +65,10 @@ CONFIGS = {
     "pipelined": WorkloadConfig("pipelined", 5000, 100, 2.0, HLS_TYPE_PROBS, HLS_TYPE_DELAYS,
                                 (16.0, 8.0, 4.0, 1.0), D=2048, II=64, back_edge_frac=0.02,
                                 B=32, iters=2000),
+    # the 50k-op graph with the horizon cut to its critical path + 8 steps (the
+    # paper sizes horizons by graph depth): narrow start-time laws
+    "large-tight": WorkloadConfig("large-tight", 50000, 500, 2.0, _zipf_probs(8, 1.2), ("uniform", 1, 4),
+                                  (64.0,) * 8, D=0, B=8, iters=2000, tight_slack=8),
 }
 
 
@@ -173,9 +178,17 @@ def make_problem(cfg: WorkloadConfig | str, seed: int = 0, n_ops: int | None = N
             if dist[j] >= 0 and dist[j] + delay[j] > k * cfg.II:
                 continue  # recurrence i ~> j -> i could not fit k*II
             bsrc.append(j); bdst.append(i); bdist.append(k)
+    D = cfg.D
+    if cfg.tight_slack > 0:   # longest delay-weighted path to any op's start (ids are topological)
+        start = np.zeros(N, dtype=np.int64)
+        for u in range(N):
+            for e in range(row_ptr[u], row_ptr[u + 1]):
+                v = col_idx[e]
+                start[v] = max(start[v], start[u] + delay[u])
+        D = int(start.max()) + cfg.tight_slack
     return Problem(
         n_ops=N, row_ptr=row_ptr, col_idx=col_idx, delay=delay, rtype=rtype,
-        capacity=np.asarray(cfg.capacities, dtype=np.float32), D=cfg.D, II=cfg.II,
+        capacity=np.asarray(cfg.capacities, dtype=np.float32), D=D, II=cfg.II,
         back_src=np.asarray(bsrc, np.int32), back_dst=np.asarray(bdst, np.int32),
         back_dist=np.asarray(bdist, np.int32), layer=layer.astype(np.int32), name=cfg.name)
 
