@@ -29,6 +29,34 @@ namespace gaus {
 //     (u over the interior edges 0..D-2 except in dVdep/dth_i, which runs to
 //     u = D-1 with S_i(D-1) = m: the consumers' bin D-1 is open to +inf).
 // ---------------------------------------------------------------------------
+// Narrow ops.  An op's CDF is the exact constant 0 below and 1 above the
+// bin edges where |z| <= fam_zflush, so an edge i -> j varies over a tile only
+// near the two ops' spreads and the horizon's ends; elsewhere each summand
+// above is 0, except F_i(u)(1 - F_j(u)) = 1 between the spreads (i done, j
+// not started).  When these spreads are short, one wave takes the op: it
+// evaluates every summand on the steps where one may vary (the spread of
+// F_i(u), that of A(u) and F_i'(u-s), that of F_j(u), and the steps 0, s-1,
+// D-2, D-1) and counts the steps between the spreads, with no work-group
+// barrier; the other ops of the group follow the row path above.  When no
+// spread meets the tile at all, every term is an integer (counts and the unit
+// masses at the horizon's ends) and the op's own thread finishes it while the
+// group is sorted.
+constexpr int kNarrowSpan = 128;   // widest spread (in steps) on the narrow path
+
+// Bin edges [lo, hi] (clamped into [a - 1 .. b + 1]) outside which an op's CDF
+// is the exact constant: 0 below lo, 1 above hi.  Widened by one step for the
+// rounding of the float bounds; a NaN mean gives [a, b].
+template <int FAM>
+__device__ __forceinline__ void spread(float mu, float rs, int a, int b, int &lo, int &hi) {
+    constexpr float kZF = fam_zflush<FAM>();
+    const float w = kZF / rs, c = mu - 0.5f;
+    float l = floorf(c - w) - 1.0f, h = ceilf(c + w) + 1.0f;
+    l = fminf(fmaxf(l, (float)a), (float)b + 1.0f);
+    h = fmaxf(fminf(h, (float)b), (float)a - 1.0f);
+    lo = (int)l;
+    hi = (int)h;
+}
+
 template <int FAM, int BS, int SPT>
 __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ mu,
                                             const float *__restrict__ sigma, Work W) {
@@ -56,28 +84,208 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
     // hold at most as many ops as the work-group has threads); ops and edges
     // on the chunk-polynomial path are left to k_poly.
     if (!W.gflag[(size_t)b * G.ngroups + grp]) return;
-    __shared__ int sDirect[BS];   // 0: nothing; else 1 + number of step-by-step out-edges
+    // Each op of the group is sorted for this tile by thread q-q0: nothing to
+    // do (no step-by-step work), constant (every spread misses the tile: its
+    // terms are integer counts, finished here), narrow (one wave each, below)
+    // or wide (the row path).
+    enum : unsigned char { kNone = 0, kConst = 1, kNarrow = 2, kWide = 3 };
+    __shared__ int sDirect[BS];   // 1 + number of step-by-step out-edges
+    __shared__ unsigned char sCls[BS];
+    __shared__ int sConst[4];     // constant ops: V_dep, L_com, P^0, P^{D-1}
     const unsigned char *clsb = W.cls + (size_t)b * N;
+    const int tb = min(t0 + TILE, D);   // the tile's steps are [t0, tb)
+    if (tid < 4) sConst[tid] = 0;
+    __syncthreads();
     {
+        unsigned char c = kNone;
         int flag = 0;
         if (q0 + tid < q1) {
             const int i = G.perm[q0 + tid];
             if (W.dflag[(size_t)b * N + i]) {
                 const int e0 = G.row_ptr[i], e1 = G.row_ptr[i + 1];
                 const bool poly_i = clsb[i] != 0;
-                int m = 0;
-                for (int e = e0; e < e1; ++e) m += (poly_i && clsb[G.col[e]]) ? 0 : 1;
+                const int s = G.delay[i];
+                int pl, ph;   // F_i is read at the bin edges u - s .. u (u in the tile)
+                spread<FAM>(mub[i], rsb[i], t0 - s - 1, tb, pl, ph);
+                // the tile's steps where F_i(u), F_i'(u) or P_i^u may vary, and
+                // where A(u) or F_i'(u-s) may
+                const int n1 = min(ph + 1, tb - 1) - max(pl, t0) + 1;
+                const int n2 = min(ph + s, tb - 1) - max(pl + s - 1, t0) + 1;
+                int span = max(max(n1, n2), 0);
+                bool act = n1 > 0 || n2 > 0;
+                // F_i off its spread, and A(u) at the steps 0, s-1, D-2 (where
+                // the bins open to -inf and +inf meet it)
+                auto Fc = [&](int v) { return v < 0 ? 0 : (v >= D - 1 || v > ph) ? 1 : 0; };
+                const int us[3] = {0, s - 1, D - 2};
+                int ua[3];
+#pragma unroll
+                for (int k = 0; k < 3; ++k) {
+                    const int u = us[k];
+                    const bool fresh = (k < 1 || u != us[0]) && (k < 2 || u != us[1]);
+                    ua[k] = (fresh && u >= t0 && u < tb && u < D - 1) ? Fc(u - s + 1) - Fc(u - s) : 0;
+                }
+                int m = 0, cnt = 0, dep = 0;
+                for (int e = e0; e < e1; ++e) {
+                    const int j = G.col[e];
+                    if (poly_i && clsb[j]) continue;
+                    ++m;
+                    int cl, ch;
+                    spread<FAM>(mub[j], rsb[j], t0 - 1, tb, cl, ch);
+                    const int n3 = min(ch + 1, tb - 1) - max(cl, t0) + 1;
+                    span = max(span, n3);
+                    act = act || n3 > 0;
+                    // F_i(u) (1 - F_j(u)) = 1 for ph < u < cl
+                    cnt += max(min(min(tb, D - 1), cl) - max(t0, ph + 1), 0);
+#pragma unroll
+                    for (int k = 0; k < 3; ++k) dep += ua[k] * (us[k] > ch ? 1 : 0);
+                }
                 flag = 1 + m;
+                c = act ? (span <= kNarrowSpan ? kNarrow : kWide) : kConst;
+                if (c == kConst) {
+                    if (D - 1 >= t0 && D - 1 < tb) dep += m * (1 - Fc(D - 1 - s));
+                    if (m == 0) dep = cnt = 0;
+                    float *pp = W.ppart + (((size_t)b * N + i) * G.ntiles + tile) * kPP;
+                    pp[0] = (float)dep; pp[1] = (float)cnt;
+                    pp[2] = 0.0f; pp[3] = 0.0f; pp[4] = 0.0f; pp[5] = 0.0f;
+                    for (int e = e0; e < e1; ++e) {
+                        if (poly_i && clsb[G.col[e]]) continue;
+                        *reinterpret_cast<float4 *>(W.cpart + (((size_t)b * G.E + e) * G.ntiles + tile) * kCP) =
+                            make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+                    }
+                    if (dep) atomicAdd(&sConst[0], dep);
+                    if (cnt) atomicAdd(&sConst[1], cnt);
+                    // P_i^0 = F_i(0), P_i^{D-1} = 1 - F_i(D-2): integers off the spread
+                    if (!poly_i && t0 == 0 && Fc(0)) atomicAdd(&sConst[2], 1);
+                    if (!poly_i && D - 1 >= t0 && D - 1 < tb && D > 1 && !Fc(D - 2)) atomicAdd(&sConst[3], 1);
+                }
             }
         }
         sDirect[tid] = flag;
+        sCls[tid] = c;
     }
     float gsum0 = 0.0f, gsum1 = 0.0f;  // V_dep, L_com of the work-group (threads 0, 1)
     __syncthreads();
 
+    // Narrow ops, one wave each, taken from the group's list in turn.
+    constexpr int NW = BS / 64;
+    __shared__ float sUw[NW][TILE];       // usage of each wave's narrow ops
+    __shared__ float sGw[NW][2];          // their V_dep and L_com
+    {
+        const int lane = tid & 63, w = tid >> 6;
+        for (int p = lane; p < TILE; p += 64) sUw[w][p] = 0.0f;
+        float g0 = 0.0f, g1 = 0.0f;
+        for (int base = 0; base < q1 - q0; base += 64 * NW) {
+            const int x = base + lane * NW + w;
+            unsigned long long todo = __ballot(x < q1 - q0 && sCls[x] == kNarrow);
+            while (todo) {
+                const int l = __builtin_ctzll(todo);
+                todo &= todo - 1;
+                const int q = q0 + base + l * NW + w;
+                const int i = uniform(G.perm[q]);
+                const int e0 = uniform(G.row_ptr[i]), e1 = uniform(G.row_ptr[i + 1]);
+                const bool poly_i = clsb[i] != 0;
+                const int m = uniform(sDirect[q - q0] - 1);
+                const float m_i = mub[i], rs = rsb[i];
+                const float cinv = rs * fam_k<FAM>();
+                const int s = uniform(G.delay[i]);
+                int pl, ph;
+                spread<FAM>(m_i, rs, t0 - s - 1, tb, pl, ph);
+                const int x1l = max(pl, t0), x1h = min(ph + 1, tb - 1);
+                const int x2l = max(pl + s - 1, t0), x2h = min(ph + s, tb - 1);
+                const int n1 = max(x1h - x1l + 1, 0), n2 = max(x2h - x2l + 1, 0);
+                {
+                    // usage: P_i^u = F_i(u) - F_i(u-1) is 0 off X1 but at u = 0 and D-1
+                    if (!poly_i) {
+                        for (int x = lane; x < n1 + 2; x += 64) {
+                            int u = x1l + x;
+                            if (x >= n1) {
+                                u = x == n1 ? 0 : D - 1;
+                                if (u < t0 || u >= tb || (u >= x1l && u <= x1h) || (x > n1 && u == 0)) continue;
+                            }
+                            sUw[w][u - t0] += st_mass(st_at<FAM>(u - 1, D, m_i, rs), st_at<FAM>(u, D, m_i, rs));
+                        }
+                    }
+                    float pr[6] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+                    int cnt = 0;   // steps between the spreads, summed over the edges
+                    for (int e = e0; e < e1; ++e) {
+                        const int j = uniform(G.col[e]);
+                        if (poly_i && clsb[j]) continue;
+                        const float m_j = mub[j], rsj = rsb[j];
+                        const float cj = rsj * fam_k<FAM>();
+                        int cl, ch;
+                        spread<FAM>(m_j, rsj, t0 - 1, tb, cl, ch);
+                        const int x3l = max(cl, t0), x3h = min(ch + 1, tb - 1);
+                        const int n3 = max(x3h - x3l + 1, 0);
+                        // F_i(u) (1 - F_j(u)) = 1 on [r0, r1) off the evaluated steps
+                        const int r0 = max(t0, ph + 1), r1 = min(min(tb, D - 1), cl);
+                        cnt += max(r1 - r0, 0);
+                        float c4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+                        const int n12 = n1 + n2, n123 = n12 + n3;
+                        for (int x = lane; x < n123 + 4; x += 64) {
+                            // the x-th step of X1, X2 \ X1, X3 \ (X1 u X2), then 0, s-1, D-2, D-1
+                            int u;
+                            bool skip;
+                            if (x < n1) {
+                                u = x1l + x;
+                                skip = false;
+                            } else if (x < n12) {
+                                u = x2l + (x - n1);
+                                skip = u >= x1l && u <= x1h;
+                            } else if (x < n123) {
+                                u = x3l + (x - n12);
+                                skip = (u >= x1l && u <= x1h) || (u >= x2l && u <= x2h);
+                            } else {
+                                const int k = x - n123;
+                                u = k == 0 ? 0 : k == 1 ? s - 1 : k == 2 ? D - 2 : D - 1;
+                                skip = u < t0 || u >= tb || (u >= x1l && u <= x1h) || (u >= x2l && u <= x2h) ||
+                                       (u >= x3l && u <= x3h) || (k >= 1 && u == 0) || (k >= 2 && u == s - 1) ||
+                                       (k == 3 && u == D - 2);
+                            }
+                            if (skip) continue;
+                            float st_i, Fm_i, Fs_i, st0, Fms, Fss, st_j, Fmj, Fsj;
+                            cdf_at<FAM>(u, D, m_i, rs, cinv, st_i, Fm_i, Fs_i);
+                            cdf_at<FAM>(u - s, D, m_i, rs, cinv, st0, Fms, Fss);
+                            cdf_at<FAM>(u, D, m_j, rsj, cj, st_j, Fmj, Fsj);
+                            const float dS = st_mass(st_at<FAM>(u - 1, D, m_j, rsj), st_j);
+                            pr[2] = fmaf(-Fms, dS, pr[2]);
+                            pr[3] = fmaf(-Fss, dS, pr[3]);
+                            if (u < D - 1) {
+                                const float A = st_mass(st0, st_at<FAM>(u - s + 1, D, m_i, rs));
+                                const float Fi = st_F(st_i), Rj = st_1mF(st_j);
+                                pr[0] = fmaf(A, st_F(st_j), pr[0]);
+                                pr[1] += fmaf(Fi, Rj, (u >= r0 && u < r1) ? -1.0f : 0.0f);
+                                pr[4] = fmaf(Fm_i, Rj, pr[4]);
+                                pr[5] = fmaf(Fs_i, Rj, pr[5]);
+                                c4[0] = fmaf(A, Fmj, c4[0]);
+                                c4[1] = fmaf(A, Fsj, c4[1]);
+                                c4[2] = fmaf(-Fi, Fmj, c4[2]);
+                                c4[3] = fmaf(-Fi, Fsj, c4[3]);
+                            } else {
+                                pr[0] += st_1mF(st0);   // 1 - F_i(D-1-s)
+                            }
+                        }
+                        const float r = wave_sum4(c4[0], c4[1], c4[2], c4[3], lane);
+                        if (lane < 4) W.cpart[(((size_t)b * G.E + e) * G.ntiles + tile) * kCP + wave4_comp(lane)] = r;
+                    }
+                    if (lane == 0) pr[1] += (float)cnt;
+                    const float ra = wave_sum4(pr[0], pr[1], pr[2], pr[3], lane);
+                    const float rb = wave_sum2(pr[4], pr[5], lane);
+                    float *pp = W.ppart + (((size_t)b * N + i) * G.ntiles + tile) * kPP;
+                    if (lane < 4) pp[wave4_comp(lane)] = m > 0 ? ra : 0.0f;
+                    if (lane < 2) pp[4 + lane] = m > 0 ? rb : 0.0f;
+                    if (m > 0 && lane == 0) g0 += ra;   // V_dep (component 0 at lane 0)
+                    if (m > 0 && lane == 2) g1 += ra;   // L_com (component 1 at lane 2)
+                }
+            }
+        }
+        if (lane == 0) sGw[w][0] = g0;
+        if (lane == 2) sGw[w][1] = g1;
+    }
+    __syncthreads();
+
     for (int q = q0; q < q1; ++q) {
+        if (sCls[q - q0] != kWide) continue;
         const int flag = sDirect[q - q0];
-        if (flag == 0) continue;
         const int i = uniform(G.perm[q]);
         const int e0 = uniform(G.row_ptr[i]), e1 = uniform(G.row_ptr[i + 1]);
         const bool poly_i = clsb[i] != 0;
@@ -233,6 +441,25 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
         } else if (tid < kPP) {
             W.ppart[(((size_t)b * N + i) * G.ntiles + tile) * kPP + tid] = 0.0f;
         }
+    }
+    // the narrow and constant ops' usage and sums (published by the barrier
+    // after the narrow ops)
+#pragma unroll
+    for (int k = 0; k < SPT; ++k) {
+        const int u = t0 + k * BS + tid;
+        float v = sUw[0][k * BS + tid];
+#pragma unroll
+        for (int w = 1; w < NW; ++w) v += sUw[w][k * BS + tid];
+        if (u == 0) v += (float)sConst[2];
+        if (u == D - 1) v += (float)sConst[3];
+        accU[k] += v;
+    }
+    if (tid < 2) {
+        float v = sGw[0][tid];
+#pragma unroll
+        for (int w = 1; w < NW; ++w) v += sGw[w][tid];
+        v += (float)sConst[tid];
+        if (tid == 0) gsum0 += v; else gsum1 += v;
     }
     {
         float *gs = W.gsum_ops + (((size_t)b * G.ngroups + grp) * G.ntiles + tile) * 2;

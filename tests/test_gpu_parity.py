@@ -168,6 +168,26 @@ def test_loss_grad_ragged_tiles_and_big_delays(II, n_back, poly):
            f"ragged II={II} poly={poly}")
 
 
+@pytest.mark.parametrize("poly", [0, -1])
+@pytest.mark.parametrize("D,II", [(50, 0), (300, 0), (1500, 0), (1500, 37)])
+def test_loss_grad_narrow_ops(D, II, poly):
+    """Sharpened states (sigma from 0.03 to 8: most ops and edges on the
+    narrow-op path of the step-by-step kernel), with means gathered at the
+    horizon's ends and at the step-tile boundaries, mixed with uniform ones,
+    and producer delays far beyond the ops' spreads."""
+    p = _ragged_problem(31 + D + II, N=700 if D > 100 else 200, D=D, II=II, n_back=6 if II else 0,
+                        big_delay=D > 1000)
+    B = 3
+    rng = np.random.default_rng(32 + D)
+    centers = np.array([0.0, D - 1.0] + [t for t in (64.0, 256.0, 1024.0) if t < D], np.float64)
+    near = centers[rng.integers(0, len(centers), size=(B, p.n_ops))] + rng.normal(0.0, 3.0, size=(B, p.n_ops))
+    far = rng.uniform(-25, p.D + 25, size=(B, p.n_ops))
+    mu = np.where(rng.random((B, p.n_ops)) < 0.5, near, far).astype(np.float32)
+    sg = np.exp(rng.uniform(np.log(0.03), np.log(8.0), size=(B, p.n_ops))).astype(np.float32)
+    _check(p, mu, sg, _lam(B, 33), hparams(alpha=0.3, rho=0.02, poly_chunk=poly), range(B),
+           f"narrow D={D} II={II} poly={poly}")
+
+
 @pytest.mark.parametrize("W", [16, 32, 64, 128, 256])
 def test_polynomial_path_chunk_widths(W):
     """Every chunk width on a wide-sigma state (all ops polynomial where the
