@@ -33,15 +33,17 @@ namespace gaus {
 // bin edges where |z| <= fam_zflush, so an edge i -> j varies over a tile only
 // near the two ops' spreads and the horizon's ends; elsewhere each summand
 // above is 0, except F_i(u)(1 - F_j(u)) = 1 between the spreads (i done, j
-// not started).  When these spreads are short, one wave takes the op: it
-// evaluates every summand on the steps where one may vary (the spread of
-// F_i(u), that of A(u) and F_i'(u-s), that of F_j(u), and the steps 0, s-1,
-// D-2, D-1) and counts the steps between the spreads, with no work-group
-// barrier; the other ops of the group follow the row path above.  When no
-// spread meets the tile at all, every term is an integer (counts and the unit
-// masses at the horizon's ends) and the op's own thread finishes it while the
-// group is sorted.
+// not started).  When these spreads are short, a lane group takes the op (a
+// quarter of a wave when every spread has at most kTinySpan steps, else the
+// whole wave): it evaluates every summand on the steps where one may vary
+// (the spread of F_i(u), that of A(u) and F_i'(u-s), that of F_j(u), and the
+// steps 0, s-1, D-2, D-1) and counts the steps between the spreads, with no
+// work-group barrier; the other ops of the group follow the row path above.
+// When no spread meets the tile at all, every term is an integer (counts and
+// the unit masses at the horizon's ends) and the op's own thread finishes it
+// while the group is sorted.
 constexpr int kNarrowSpan = 128;   // widest spread (in steps) on the narrow path
+constexpr int kTinySpan = 32;      // widest spread of the ops taken four per wave
 
 // Bin edges [lo, hi] (clamped into [a - 1 .. b + 1]) outside which an op's CDF
 // is the exact constant: 0 below lo, 1 above hi.  Widened by one step for the
@@ -55,6 +57,163 @@ __device__ __forceinline__ void spread(float mu, float rs, int a, int b, int &lo
     h = fmaxf(fminf(h, (float)b), (float)a - 1.0f);
     lo = (int)l;
     hi = (int)h;
+}
+
+// classes of an op in a step tile
+enum : unsigned char { kNone = 0, kConst = 1, kTiny = 2, kNarrow = 3, kWide = 4 };
+
+// Narrow ops of class `want` from the group's list, NP at a time by each wave,
+// one op per lane group of 64/NP lanes (the loads of the ops and their
+// consumers overlap; loops run to the lane groups' maximum).  The wave's
+// usage goes to sU (its own LDS row), its V_dep and L_com to g0 and g1 of the
+// lanes 0 and 2 of each lane group.
+template <int FAM, int NP, int BS>
+__device__ __forceinline__ void narrow_ops(const Graph &G, const Work &W, const float *__restrict__ mub,
+                                           const float *__restrict__ rsb, const unsigned char *__restrict__ clsb,
+                                           const unsigned char *sCls, const int *sDirect, float *sU,
+                                           unsigned char want, int q0, int q1, int t0, int tb, int tile, int b,
+                                           float &g0, float &g1) {
+    constexpr int NW = BS / 64, GL = 64 / NP;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int grl = lane / GL, gl = lane % GL;   // lane group, lane in the group
+    const int D = G.D, N = G.N;
+    for (int base = 0; base < q1 - q0; base += 64 * NW) {
+        const int x = base + lane * NW + w;
+        unsigned long long todo = __ballot(x < q1 - q0 && sCls[x] == want);
+        while (todo) {
+            int myl = -1;
+            for (int k = 0; k < NP && todo; ++k) {
+                const int l = __builtin_ctzll(todo);
+                todo &= todo - 1;
+                if (grl == k) myl = l;
+            }
+            const bool ok = myl >= 0;
+            const int q = q0 + base + myl * NW + w;
+            int i = 0, e0 = 0, e1 = 0, m = 0, s = 0;
+            float m_i = 0.0f, rs = 1.0f;
+            bool poly_i = false;
+            if (ok) {
+                i = G.perm[q];
+                e0 = G.row_ptr[i]; e1 = G.row_ptr[i + 1];
+                poly_i = clsb[i] != 0;
+                m = sDirect[q - q0] - 1;
+                m_i = mub[i]; rs = rsb[i];
+                s = G.delay[i];
+            }
+            const float cinv = rs * fam_k<FAM>();
+            int pl, ph;   // F_i is read at the bin edges u - s .. u (u in the tile)
+            spread<FAM>(m_i, rs, t0 - s - 1, tb, pl, ph);
+            // steps where F_i(u), F_i'(u) or P_i^u may vary (X1), and where
+            // A(u) or F_i'(u-s) may (X2)
+            const int x1l = max(pl, t0), x1h = min(ph + 1, tb - 1);
+            const int x2l = max(pl + s - 1, t0), x2h = min(ph + s, tb - 1);
+            const int n1 = ok ? max(x1h - x1l + 1, 0) : 0, n2 = ok ? max(x2h - x2l + 1, 0) : 0;
+
+            // usage: P_i^u = F_i(u) - F_i(u-1) is 0 off X1 but at u = 0 and D-1
+            const int nu = (ok && !poly_i) ? n1 + 2 : 0;
+            const int nu_max = (int)wave_max((float)nu);
+            for (int x0 = 0; x0 < nu_max; x0 += GL) {
+                const int xx = x0 + gl;
+                int u = x1l + xx;
+                bool take = xx < nu;
+                if (take && xx >= n1) {
+                    u = xx == n1 ? 0 : D - 1;
+                    take = u >= t0 && u < tb && !(u >= x1l && u <= x1h) && !(xx > n1 && u == 0);
+                }
+                const float P = take ? st_mass(st_at<FAM>(u - 1, D, m_i, rs), st_at<FAM>(u, D, m_i, rs)) : 0.0f;
+                // lane groups may share a step: their additions go one group
+                // at a time (kept apart by the compiler barriers)
+#pragma unroll
+                for (int k = 0; k < NP; ++k) {
+                    if (take && grl == k) sU[u - t0] += P;
+                    asm volatile("" ::: "memory");
+                }
+            }
+
+            float pr[6] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+            int cnt = 0;   // steps between the spreads, summed over the edges
+            const int deg = ok ? e1 - e0 : 0;
+            const int deg_max = (int)wave_max((float)deg);
+            for (int t = 0; t < deg_max; ++t) {
+                const int e = e0 + t;
+                bool ev = t < deg;
+                int j = 0;
+                if (ev) {
+                    j = G.col[e];
+                    ev = !(poly_i && clsb[j]);
+                }
+                float m_j = 0.0f, rsj = 1.0f;
+                if (ev) { m_j = mub[j]; rsj = rsb[j]; }
+                const float cj = rsj * fam_k<FAM>();
+                int cl, ch;
+                spread<FAM>(m_j, rsj, t0 - 1, tb, cl, ch);
+                const int x3l = max(cl, t0), x3h = min(ch + 1, tb - 1);
+                const int n3 = max(x3h - x3l + 1, 0);
+                // F_i(u) (1 - F_j(u)) = 1 on [r0, r1) off the evaluated steps
+                const int r0 = max(t0, ph + 1), r1 = min(min(tb, D - 1), cl);
+                if (ev) cnt += max(r1 - r0, 0);
+                float c4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+                const int n12 = n1 + n2, n123 = n12 + n3;
+                const int ntot = ev ? n123 + 4 : 0;
+                const int ntot_max = (int)wave_max((float)ntot);
+                for (int x0 = 0; x0 < ntot_max; x0 += GL) {
+                    // the xx-th step of X1, X2 \ X1, X3 \ (X1 u X2), then 0, s-1, D-2, D-1
+                    const int xx = x0 + gl;
+                    int u;
+                    bool take = xx < ntot;
+                    if (xx < n1) {
+                        u = x1l + xx;
+                    } else if (xx < n12) {
+                        u = x2l + (xx - n1);
+                        take = take && !(u >= x1l && u <= x1h);
+                    } else if (xx < n123) {
+                        u = x3l + (xx - n12);
+                        take = take && !(u >= x1l && u <= x1h) && !(u >= x2l && u <= x2h);
+                    } else {
+                        const int k = xx - n123;
+                        u = k == 0 ? 0 : k == 1 ? s - 1 : k == 2 ? D - 2 : D - 1;
+                        take = take && u >= t0 && u < tb && !(u >= x1l && u <= x1h) && !(u >= x2l && u <= x2h) &&
+                               !(u >= x3l && u <= x3h) && !(k >= 1 && u == 0) && !(k >= 2 && u == s - 1) &&
+                               !(k == 3 && u == D - 2);
+                    }
+                    if (!take) continue;
+                    float st_i, Fm_i, Fs_i, st0, Fms, Fss, st_j, Fmj, Fsj;
+                    cdf_at<FAM>(u, D, m_i, rs, cinv, st_i, Fm_i, Fs_i);
+                    cdf_at<FAM>(u - s, D, m_i, rs, cinv, st0, Fms, Fss);
+                    cdf_at<FAM>(u, D, m_j, rsj, cj, st_j, Fmj, Fsj);
+                    const float dS = st_mass(st_at<FAM>(u - 1, D, m_j, rsj), st_j);
+                    pr[2] = fmaf(-Fms, dS, pr[2]);
+                    pr[3] = fmaf(-Fss, dS, pr[3]);
+                    if (u < D - 1) {
+                        const float A = st_mass(st0, st_at<FAM>(u - s + 1, D, m_i, rs));
+                        const float Fi = st_F(st_i), Rj = st_1mF(st_j);
+                        pr[0] = fmaf(A, st_F(st_j), pr[0]);
+                        pr[1] += fmaf(Fi, Rj, (u >= r0 && u < r1) ? -1.0f : 0.0f);
+                        pr[4] = fmaf(Fm_i, Rj, pr[4]);
+                        pr[5] = fmaf(Fs_i, Rj, pr[5]);
+                        c4[0] = fmaf(A, Fmj, c4[0]);
+                        c4[1] = fmaf(A, Fsj, c4[1]);
+                        c4[2] = fmaf(-Fi, Fmj, c4[2]);
+                        c4[3] = fmaf(-Fi, Fsj, c4[3]);
+                    } else {
+                        pr[0] += st_1mF(st0);   // 1 - F_i(D-1-s)
+                    }
+                }
+                const float r = group_sum4<NP>(c4[0], c4[1], c4[2], c4[3], lane);
+                if (ev && gl < 4) W.cpart[(((size_t)b * G.E + e) * G.ntiles + tile) * kCP + wave4_comp(gl)] = r;
+            }
+            if (gl == 0) pr[1] += (float)cnt;
+            const float ra = group_sum4<NP>(pr[0], pr[1], pr[2], pr[3], lane);
+            const float rb = group_sum2<NP>(pr[4], pr[5], lane);
+            if (ok) {
+                float *pp = W.ppart + (((size_t)b * N + i) * G.ntiles + tile) * kPP;
+                if (gl < 4) pp[wave4_comp(gl)] = m > 0 ? ra : 0.0f;
+                if (gl < 2) pp[4 + gl] = m > 0 ? rb : 0.0f;
+                if (m > 0 && gl == 0) g0 += ra;   // V_dep (component 0 at lane 0 of the group)
+                if (m > 0 && gl == 2) g1 += ra;   // L_com (component 1 at lane 2)
+            }
+        }
+    }
 }
 
 template <int FAM, int BS, int SPT>
@@ -88,7 +247,6 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
     // do (no step-by-step work), constant (every spread misses the tile: its
     // terms are integer counts, finished here), narrow (one wave each, below)
     // or wide (the row path).
-    enum : unsigned char { kNone = 0, kConst = 1, kNarrow = 2, kWide = 3 };
     __shared__ int sDirect[BS];   // 1 + number of step-by-step out-edges
     __shared__ unsigned char sCls[BS];
     __shared__ int sConst[4];     // constant ops: V_dep, L_com, P^0, P^{D-1}
@@ -140,7 +298,7 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
                     for (int k = 0; k < 3; ++k) dep += ua[k] * (us[k] > ch ? 1 : 0);
                 }
                 flag = 1 + m;
-                c = act ? (span <= kNarrowSpan ? kNarrow : kWide) : kConst;
+                c = !act ? kConst : span <= kTinySpan ? kTiny : span <= kNarrowSpan ? kNarrow : kWide;
                 if (c == kConst) {
                     if (D - 1 >= t0 && D - 1 < tb) dep += m * (1 - Fc(D - 1 - s));
                     if (m == 0) dep = cnt = 0;
@@ -166,7 +324,8 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
     float gsum0 = 0.0f, gsum1 = 0.0f;  // V_dep, L_com of the work-group (threads 0, 1)
     __syncthreads();
 
-    // Narrow ops, one wave each, taken from the group's list in turn.
+    // Narrow ops: the shortest spreads four at a time per wave, the others one
+    // at a time.
     constexpr int NW = BS / 64;
     __shared__ float sUw[NW][TILE];       // usage of each wave's narrow ops
     __shared__ float sGw[NW][2];          // their V_dep and L_com
@@ -174,112 +333,10 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
         const int lane = tid & 63, w = tid >> 6;
         for (int p = lane; p < TILE; p += 64) sUw[w][p] = 0.0f;
         float g0 = 0.0f, g1 = 0.0f;
-        for (int base = 0; base < q1 - q0; base += 64 * NW) {
-            const int x = base + lane * NW + w;
-            unsigned long long todo = __ballot(x < q1 - q0 && sCls[x] == kNarrow);
-            while (todo) {
-                const int l = __builtin_ctzll(todo);
-                todo &= todo - 1;
-                const int q = q0 + base + l * NW + w;
-                const int i = uniform(G.perm[q]);
-                const int e0 = uniform(G.row_ptr[i]), e1 = uniform(G.row_ptr[i + 1]);
-                const bool poly_i = clsb[i] != 0;
-                const int m = uniform(sDirect[q - q0] - 1);
-                const float m_i = mub[i], rs = rsb[i];
-                const float cinv = rs * fam_k<FAM>();
-                const int s = uniform(G.delay[i]);
-                int pl, ph;
-                spread<FAM>(m_i, rs, t0 - s - 1, tb, pl, ph);
-                const int x1l = max(pl, t0), x1h = min(ph + 1, tb - 1);
-                const int x2l = max(pl + s - 1, t0), x2h = min(ph + s, tb - 1);
-                const int n1 = max(x1h - x1l + 1, 0), n2 = max(x2h - x2l + 1, 0);
-                {
-                    // usage: P_i^u = F_i(u) - F_i(u-1) is 0 off X1 but at u = 0 and D-1
-                    if (!poly_i) {
-                        for (int x = lane; x < n1 + 2; x += 64) {
-                            int u = x1l + x;
-                            if (x >= n1) {
-                                u = x == n1 ? 0 : D - 1;
-                                if (u < t0 || u >= tb || (u >= x1l && u <= x1h) || (x > n1 && u == 0)) continue;
-                            }
-                            sUw[w][u - t0] += st_mass(st_at<FAM>(u - 1, D, m_i, rs), st_at<FAM>(u, D, m_i, rs));
-                        }
-                    }
-                    float pr[6] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
-                    int cnt = 0;   // steps between the spreads, summed over the edges
-                    for (int e = e0; e < e1; ++e) {
-                        const int j = uniform(G.col[e]);
-                        if (poly_i && clsb[j]) continue;
-                        const float m_j = mub[j], rsj = rsb[j];
-                        const float cj = rsj * fam_k<FAM>();
-                        int cl, ch;
-                        spread<FAM>(m_j, rsj, t0 - 1, tb, cl, ch);
-                        const int x3l = max(cl, t0), x3h = min(ch + 1, tb - 1);
-                        const int n3 = max(x3h - x3l + 1, 0);
-                        // F_i(u) (1 - F_j(u)) = 1 on [r0, r1) off the evaluated steps
-                        const int r0 = max(t0, ph + 1), r1 = min(min(tb, D - 1), cl);
-                        cnt += max(r1 - r0, 0);
-                        float c4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-                        const int n12 = n1 + n2, n123 = n12 + n3;
-                        for (int x = lane; x < n123 + 4; x += 64) {
-                            // the x-th step of X1, X2 \ X1, X3 \ (X1 u X2), then 0, s-1, D-2, D-1
-                            int u;
-                            bool skip;
-                            if (x < n1) {
-                                u = x1l + x;
-                                skip = false;
-                            } else if (x < n12) {
-                                u = x2l + (x - n1);
-                                skip = u >= x1l && u <= x1h;
-                            } else if (x < n123) {
-                                u = x3l + (x - n12);
-                                skip = (u >= x1l && u <= x1h) || (u >= x2l && u <= x2h);
-                            } else {
-                                const int k = x - n123;
-                                u = k == 0 ? 0 : k == 1 ? s - 1 : k == 2 ? D - 2 : D - 1;
-                                skip = u < t0 || u >= tb || (u >= x1l && u <= x1h) || (u >= x2l && u <= x2h) ||
-                                       (u >= x3l && u <= x3h) || (k >= 1 && u == 0) || (k >= 2 && u == s - 1) ||
-                                       (k == 3 && u == D - 2);
-                            }
-                            if (skip) continue;
-                            float st_i, Fm_i, Fs_i, st0, Fms, Fss, st_j, Fmj, Fsj;
-                            cdf_at<FAM>(u, D, m_i, rs, cinv, st_i, Fm_i, Fs_i);
-                            cdf_at<FAM>(u - s, D, m_i, rs, cinv, st0, Fms, Fss);
-                            cdf_at<FAM>(u, D, m_j, rsj, cj, st_j, Fmj, Fsj);
-                            const float dS = st_mass(st_at<FAM>(u - 1, D, m_j, rsj), st_j);
-                            pr[2] = fmaf(-Fms, dS, pr[2]);
-                            pr[3] = fmaf(-Fss, dS, pr[3]);
-                            if (u < D - 1) {
-                                const float A = st_mass(st0, st_at<FAM>(u - s + 1, D, m_i, rs));
-                                const float Fi = st_F(st_i), Rj = st_1mF(st_j);
-                                pr[0] = fmaf(A, st_F(st_j), pr[0]);
-                                pr[1] += fmaf(Fi, Rj, (u >= r0 && u < r1) ? -1.0f : 0.0f);
-                                pr[4] = fmaf(Fm_i, Rj, pr[4]);
-                                pr[5] = fmaf(Fs_i, Rj, pr[5]);
-                                c4[0] = fmaf(A, Fmj, c4[0]);
-                                c4[1] = fmaf(A, Fsj, c4[1]);
-                                c4[2] = fmaf(-Fi, Fmj, c4[2]);
-                                c4[3] = fmaf(-Fi, Fsj, c4[3]);
-                            } else {
-                                pr[0] += st_1mF(st0);   // 1 - F_i(D-1-s)
-                            }
-                        }
-                        const float r = wave_sum4(c4[0], c4[1], c4[2], c4[3], lane);
-                        if (lane < 4) W.cpart[(((size_t)b * G.E + e) * G.ntiles + tile) * kCP + wave4_comp(lane)] = r;
-                    }
-                    if (lane == 0) pr[1] += (float)cnt;
-                    const float ra = wave_sum4(pr[0], pr[1], pr[2], pr[3], lane);
-                    const float rb = wave_sum2(pr[4], pr[5], lane);
-                    float *pp = W.ppart + (((size_t)b * N + i) * G.ntiles + tile) * kPP;
-                    if (lane < 4) pp[wave4_comp(lane)] = m > 0 ? ra : 0.0f;
-                    if (lane < 2) pp[4 + lane] = m > 0 ? rb : 0.0f;
-                    if (m > 0 && lane == 0) g0 += ra;   // V_dep (component 0 at lane 0)
-                    if (m > 0 && lane == 2) g1 += ra;   // L_com (component 1 at lane 2)
-                }
-            }
-        }
-        if (lane == 0) sGw[w][0] = g0;
-        if (lane == 2) sGw[w][1] = g1;
+        narrow_ops<FAM, 4, BS>(G, W, mub, rsb, clsb, sCls, sDirect, sUw[w], kTiny, q0, q1, t0, tb, tile, b, g0, g1);
+        narrow_ops<FAM, 1, BS>(G, W, mub, rsb, clsb, sCls, sDirect, sUw[w], kNarrow, q0, q1, t0, tb, tile, b, g0, g1);
+        const float s0 = wave_sum((lane & 15) == 0 ? g0 : 0.0f), s1 = wave_sum((lane & 15) == 2 ? g1 : 0.0f);
+        if (lane == 0) { sGw[w][0] = s0; sGw[w][1] = s1; }
     }
     __syncthreads();
 
