@@ -492,6 +492,14 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     g.N = h.N; g.E = h.E; g.K = h.K; g.D = h.D; g.II = h.II; g.T = h.II > 0 ? h.II : h.D;
     g.nb = h.nb; g.B = B; g.tile = tile; g.ntiles = ntiles;
     g.ngroups = (int)h.grp_start.size() - 1;
+    {
+        // a small op-kernel grid (few tiles) over many ops leaves the last round
+        // of work-groups mostly idle: split each (group, tile) over up to 4
+        // work-groups (small problems keep one: their op kernel is short)
+        const long long wgs = (long long)g.ngroups * ntiles * B;
+        g.parts = (wgs >= 4096 || (long long)h.N * B < (1 << 18))
+                      ? 1 : (int)std::min<long long>(4, (8192 + wgs - 1) / wgs);
+    }
     if (c->pa.enabled) {
         // polynomial work-groups per op group: at most 16 ops per wave, so that
         // every SIMD receives many short waves and the last ones end together
@@ -566,7 +574,7 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     UP(alap, h.alap);
 #undef UP
 #define AL(field, n) do { s = dalloc(c, &c->w.field, (n)); if (s != GAUS_OK) goto fail_alloc; } while (0)
-    AL(Upart, (size_t)B * g.ngroups * h.D);
+    AL(Upart, (size_t)B * g.ngroups * g.parts * h.D);
     AL(ppart, BN * ntiles * kPP);
     AL(cpart, (size_t)B * h.E * ntiles * kCP);
     AL(bpart, (size_t)B * h.nb * ntiles * kBP);
@@ -617,7 +625,7 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     AL(ptier, BN);
     AL(gflag, (size_t)B * g.ngroups);
     AL(gnarrow, (size_t)B * g.ngroups);
-    AL(gsum_ops, (size_t)B * g.ngroups * ntiles * 2);
+    AL(gsum_ops, (size_t)B * g.ngroups * g.parts * ntiles * 2);
     AL(gsum_poly, (size_t)std::max(c->poly_slots, 1) * 2);
     AL(gsel, BN);
     AL(gtier, BN);

@@ -80,7 +80,8 @@ struct PolyArgs {
 struct Graph {
     int N, E, K, D, II, T, nb, B;
     int tile, ntiles;          // steps per tile of the op kernel, tiles per restart
-    int ngroups;               // type-pure op groups (one work-group each per tile)
+    int ngroups;               // type-pure op groups
+    int parts;                 // op-kernel work-groups per (op group, tile): each takes every parts-th op
     int nlevels;               // topological levels (legalization)
     int leg_mode;              // legalization schedule: 0 global int64, 1 LDS int16, 2 LDS int32
     const int *row_ptr, *col;            // CSR by producer
@@ -108,7 +109,7 @@ struct Graph {
 
 // Library-owned device workspace.
 struct Work {
-    float *Upart;     // [B][ngroups][D]   per-group unfolded usage partials
+    float *Upart;     // [B][ngroups][parts][D]   unfolded usage partials of the op kernel
     float *ppart;     // [B][N][ntiles][kPP]
     float *cpart;     // [B][E][ntiles][kCP]
     float *bpart;     // [B][nb][ntiles][kBP]
@@ -157,7 +158,7 @@ struct Work {
                            //               itself and its polynomial consumers (highest degree)
     int *gflag;       // [B][ngroups]      1 = some op of the group has step-by-step work
     int *gnarrow;     // [B][ngroups]      1 = some op of the group takes polynomial degree 8 or 6
-    float *gsum_ops;  // [B][ngroups][ntiles][2]  V_dep, L_com of a k_ops work-group
+    float *gsum_ops;  // [B][ngroups][parts][ntiles][2]  V_dep, L_com of a k_ops work-group
     float *gsum_poly; // [slots][2]        V_dep, L_com of a k_poly work-group (GridArgs::slot_base)
     unsigned char *gsel;   // [B][N]        grid that evaluates the (restart, op) this iteration (0..2),
                            //               kNoGrid on the step-by-step path

@@ -316,11 +316,14 @@ __global__ __launch_bounds__(kUsageBS) void k_usage(Graph G, PolyArgs pa, Work W
     double acc = 0.0;
     for (int t = slot; t < D; t += T) {
         double ut = 0.0;
+        const int P = G.parts;
         if (nact <= kMaxAct) {
-            for (int q = 0; q < nact; ++q) ut += W.Upart[((size_t)b * G.ngroups + sAct[q]) * D + t];
+            for (int q = 0; q < nact; ++q)
+                for (int pt = 0; pt < P; ++pt) ut += W.Upart[(((size_t)b * G.ngroups + sAct[q]) * P + pt) * D + t];
         } else {
             for (int g = g0; g < g1; ++g)
-                if (W.gflag[(size_t)b * G.ngroups + g]) ut += W.Upart[((size_t)b * G.ngroups + g) * D + t];
+                if (W.gflag[(size_t)b * G.ngroups + g])
+                    for (int pt = 0; pt < P; ++pt) ut += W.Upart[(((size_t)b * G.ngroups + g) * P + pt) * D + t];
         }
         for (int gi = 0; gi < kGrids; ++gi) {
             const GridArgs &gd = pa.gr[gi];
@@ -560,8 +563,8 @@ __global__ __launch_bounds__(kCombineBS) void k_combine(Graph G, PolyArgs pa, Wo
     }
     for (int g = tid; g < G.ngroups; g += kCombineBS) {
         if (W.gflag[(size_t)b * G.ngroups + g]) {
-            const float *go = W.gsum_ops + ((size_t)b * G.ngroups + g) * G.ntiles * 2;
-            for (int tl = 0; tl < G.ntiles; ++tl) { vdep += go[2 * tl]; lcom += go[2 * tl + 1]; }
+            const float *go = W.gsum_ops + ((size_t)b * G.ngroups + g) * G.parts * G.ntiles * 2;
+            for (int tl = 0; tl < G.parts * G.ntiles; ++tl) { vdep += go[2 * tl]; lcom += go[2 * tl + 1]; }
         }
     }
     const size_t nbp = (size_t)G.nb * G.ntiles;

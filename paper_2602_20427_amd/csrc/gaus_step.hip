@@ -62,6 +62,22 @@ __device__ __forceinline__ void spread(float mu, float rs, int a, int b, int &lo
 // classes of an op in a step tile
 enum : unsigned char { kNone = 0, kConst = 1, kTiny = 2, kNarrow = 3, kWide = 4 };
 
+// A group's ops and their consumers as the op kernel reads them, staged in
+// LDS once per work-group (the consumers of at most kStage edges; an op whose
+// edges do not fit reads them from global memory).
+constexpr int kStage = 1024;
+struct OpStage {
+    int *i, *e0, *deg, *s, *off;   // op id, first edge, out-degree, delay, first staged edge (-1: none)
+    float *mu, *rs;                // mean and 1/sigma
+    unsigned char *poly;           // op on the chunk-polynomial path
+    float *emu, *ers;              // consumer mean and 1/sigma, per staged edge
+    unsigned char *eon;            // edge on the step-by-step path
+};
+
+__device__ __forceinline__ float uniformf(float x) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, x)));
+}
+
 // Narrow ops of class `want` from the group's list, NP at a time by each wave,
 // one op per lane group of 64/NP lanes (the loads of the ops and their
 // consumers overlap; loops run to the lane groups' maximum).  The wave's
@@ -70,16 +86,16 @@ enum : unsigned char { kNone = 0, kConst = 1, kTiny = 2, kNarrow = 3, kWide = 4 
 template <int FAM, int NP, int BS>
 __device__ __forceinline__ void narrow_ops(const Graph &G, const Work &W, const float *__restrict__ mub,
                                            const float *__restrict__ rsb, const unsigned char *__restrict__ clsb,
-                                           const unsigned char *sCls, const int *sDirect, float *sU,
-                                           unsigned char want, int q0, int q1, int t0, int tb, int tile, int b,
+                                           const OpStage &st, const unsigned char *sCls, const int *sDirect,
+                                           float *sU, unsigned char want, int nq, int t0, int tb, int tile, int b,
                                            float &g0, float &g1) {
     constexpr int NW = BS / 64, GL = 64 / NP;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int grl = lane / GL, gl = lane % GL;   // lane group, lane in the group
     const int D = G.D, N = G.N;
-    for (int base = 0; base < q1 - q0; base += 64 * NW) {
-        const int x = base + lane * NW + w;
-        unsigned long long todo = __ballot(x < q1 - q0 && sCls[x] == want);
+    for (int base = 0; base < nq; base += 64 * NW) {
+        const int xl = base + lane * NW + w;
+        unsigned long long todo = __ballot(xl < nq && sCls[xl] == want);
         while (todo) {
             int myl = -1;
             for (int k = 0; k < NP && todo; ++k) {
@@ -88,17 +104,16 @@ __device__ __forceinline__ void narrow_ops(const Graph &G, const Work &W, const 
                 if (grl == k) myl = l;
             }
             const bool ok = myl >= 0;
-            const int q = q0 + base + myl * NW + w;
-            int i = 0, e0 = 0, e1 = 0, m = 0, s = 0;
+            const int x = base + myl * NW + w;   // the op's index in the work-group's list
+            int i = 0, e0 = 0, e1 = 0, m = 0, s = 0, off = -1;
             float m_i = 0.0f, rs = 1.0f;
             bool poly_i = false;
             if (ok) {
-                i = G.perm[q];
-                e0 = G.row_ptr[i]; e1 = G.row_ptr[i + 1];
-                poly_i = clsb[i] != 0;
-                m = sDirect[q - q0] - 1;
-                m_i = mub[i]; rs = rsb[i];
-                s = G.delay[i];
+                i = st.i[x]; e0 = st.e0[x]; e1 = e0 + st.deg[x];
+                poly_i = st.poly[x] != 0;
+                m = sDirect[x] - 1;
+                m_i = st.mu[x]; rs = st.rs[x];
+                s = st.s[x]; off = st.off[x];
             }
             const float cinv = rs * fam_k<FAM>();
             int pl, ph;   // F_i is read at the bin edges u - s .. u (u in the tile)
@@ -137,13 +152,15 @@ __device__ __forceinline__ void narrow_ops(const Graph &G, const Work &W, const 
             for (int t = 0; t < deg_max; ++t) {
                 const int e = e0 + t;
                 bool ev = t < deg;
-                int j = 0;
-                if (ev) {
-                    j = G.col[e];
-                    ev = !(poly_i && clsb[j]);
-                }
                 float m_j = 0.0f, rsj = 1.0f;
-                if (ev) { m_j = mub[j]; rsj = rsb[j]; }
+                if (ev && off >= 0) {
+                    ev = st.eon[off + t] != 0;
+                    m_j = st.emu[off + t]; rsj = st.ers[off + t];
+                } else if (ev) {
+                    const int j = G.col[e];
+                    ev = !(poly_i && clsb[j]);
+                    if (ev) { m_j = mub[j]; rsj = rsb[j]; }
+                }
                 const float cj = rsj * fam_k<FAM>();
                 int cl, ch;
                 spread<FAM>(m_j, rsj, t0 - 1, tb, cl, ch);
@@ -221,101 +238,147 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
                                             const float *__restrict__ sigma, Work W) {
     constexpr int TILE = BS * SPT;
     constexpr int WIN = TILE + kHalo + 1;
-    __shared__ float sT[WIN], sFm[WIN], sFs[WIN];
+    constexpr int NW = BS / 64;
+    // the narrow ops' usage rows (one per wave), then the row path's window
+    constexpr int kBuf = NW * TILE > 3 * WIN ? NW * TILE : 3 * WIN;
+    __shared__ float sBuf[kBuf];
+    float *sT = sBuf, *sFm = sBuf + WIN, *sFs = sBuf + 2 * WIN;
     __shared__ float sRed[2][BS / 64][8];
     __shared__ float sPrev[3];
+    constexpr int kEdgeBatch = 16;
+    __shared__ float sCp[2][kEdgeBatch][NW][4];   // wave partials of the out-edges' derivatives
+    __shared__ int sCpE[2][kEdgeBatch];           // their edges
+    __shared__ float sCpC[2][kEdgeBatch];         // and fam_k/sigma_j
+    __shared__ float sLast[NW][SPT][3];           // each wave's last S_i(u) terms (lower, upper, count)
+    int cpar = 0;
 
-    const int grp = blockIdx.x, tile = blockIdx.y, b = blockIdx.z;
+    const int grp = blockIdx.x / G.parts, part = blockIdx.x % G.parts, tile = blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x;
+    const int lane = tid & 63, wid = tid >> 6;
     const int D = G.D, N = G.N;
     const int t0 = tile * TILE;
     const float *mub = mu + (size_t)b * N;
     const float *rsb = W.rsig + (size_t)b * N;   // 1/sigma
 
-    const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
+    // this work-group's ops: every parts-th op of the group, from op q0 + part
+    const int q0 = G.grp_start[grp] + part, q1 = G.grp_start[grp + 1];
+    const int nq = q1 > q0 ? (q1 - q0 + G.parts - 1) / G.parts : 0;
     float accU[SPT];
 #pragma unroll
     for (int k = 0; k < SPT; ++k) accU[k] = 0.0f;
     int par = 0;
 
     // Groups without step-by-step work leave nothing here: their readers skip
-    // them (group and op flags).  Otherwise thread t looks at op q0+t (groups
-    // hold at most as many ops as the work-group has threads); ops and edges
-    // on the chunk-polynomial path are left to k_poly.
+    // them (group and op flags).  Otherwise thread t looks at op q0 + t*parts
+    // (groups hold at most as many ops as the work-group has threads); ops and
+    // edges on the chunk-polynomial path are left to k_poly.
     if (!W.gflag[(size_t)b * G.ngroups + grp]) return;
-    // Each op of the group is sorted for this tile by thread q-q0: nothing to
-    // do (no step-by-step work), constant (every spread misses the tile: its
-    // terms are integer counts, finished here), narrow (one wave each, below)
+    // Each op is sorted for this tile by its thread: nothing to do (no
+    // step-by-step work), constant (every spread misses the tile: its terms
+    // are integer counts, finished here), tiny or narrow (lane groups, below)
     // or wide (the row path).
     __shared__ int sDirect[BS];   // 1 + number of step-by-step out-edges
     __shared__ unsigned char sCls[BS];
     __shared__ int sConst[4];     // constant ops: V_dep, L_com, P^0, P^{D-1}
+    __shared__ int sOpI[BS], sOpE0[BS], sOpDeg[BS], sOpS[BS], sOpOff[BS], sWsum[NW];
+    __shared__ float sOpMu[BS], sOpRs[BS], sEmu[kStage], sErs[kStage];
+    __shared__ unsigned char sOpPoly[BS], sEon[kStage];
+    const OpStage st{sOpI, sOpE0, sOpDeg, sOpS, sOpOff, sOpMu, sOpRs, sOpPoly, sEmu, sErs, sEon};
     const unsigned char *clsb = W.cls + (size_t)b * N;
     const int tb = min(t0 + TILE, D);   // the tile's steps are [t0, tb)
     if (tid < 4) sConst[tid] = 0;
-    __syncthreads();
     {
+        const int lane = tid & 63, w = tid >> 6;
+        int i = 0, e0 = 0, deg = 0, s = 0;
+        float m_i = 0.0f, rs = 1.0f;
+        bool poly_i = false, on = false;
+        if (tid < nq) {
+            i = G.perm[q0 + tid * G.parts];
+            on = W.dflag[(size_t)b * N + i] != 0;
+            if (on) {
+                e0 = G.row_ptr[i]; deg = G.row_ptr[i + 1] - e0;
+                poly_i = clsb[i] != 0;
+                s = G.delay[i];
+                m_i = mub[i]; rs = rsb[i];
+            }
+        }
+        // LDS offsets of the ops' edges: exclusive scan of the out-degrees
+        int x = deg;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int y = __shfl_up(x, o, 64);
+            if (lane >= o) x += y;
+        }
+        if (lane == 63) sWsum[w] = x;
+        __syncthreads();
+        int off = x - deg;
+        for (int k = 0; k < w; ++k) off += sWsum[k];
+        if (!on || off + deg > kStage) off = -1;
+        sOpI[tid] = i; sOpE0[tid] = e0; sOpDeg[tid] = deg; sOpS[tid] = s; sOpOff[tid] = off;
+        sOpMu[tid] = m_i; sOpRs[tid] = rs; sOpPoly[tid] = poly_i ? 1 : 0;
+
         unsigned char c = kNone;
         int flag = 0;
-        if (q0 + tid < q1) {
-            const int i = G.perm[q0 + tid];
-            if (W.dflag[(size_t)b * N + i]) {
-                const int e0 = G.row_ptr[i], e1 = G.row_ptr[i + 1];
-                const bool poly_i = clsb[i] != 0;
-                const int s = G.delay[i];
-                int pl, ph;   // F_i is read at the bin edges u - s .. u (u in the tile)
-                spread<FAM>(mub[i], rsb[i], t0 - s - 1, tb, pl, ph);
-                // the tile's steps where F_i(u), F_i'(u) or P_i^u may vary, and
-                // where A(u) or F_i'(u-s) may
-                const int n1 = min(ph + 1, tb - 1) - max(pl, t0) + 1;
-                const int n2 = min(ph + s, tb - 1) - max(pl + s - 1, t0) + 1;
-                int span = max(max(n1, n2), 0);
-                bool act = n1 > 0 || n2 > 0;
-                // F_i off its spread, and A(u) at the steps 0, s-1, D-2 (where
-                // the bins open to -inf and +inf meet it)
-                auto Fc = [&](int v) { return v < 0 ? 0 : (v >= D - 1 || v > ph) ? 1 : 0; };
-                const int us[3] = {0, s - 1, D - 2};
-                int ua[3];
+        if (on) {
+            const int e1 = e0 + deg;
+            int pl, ph;   // F_i is read at the bin edges u - s .. u (u in the tile)
+            spread<FAM>(m_i, rs, t0 - s - 1, tb, pl, ph);
+            // the tile's steps where F_i(u), F_i'(u) or P_i^u may vary, and
+            // where A(u) or F_i'(u-s) may
+            const int n1 = min(ph + 1, tb - 1) - max(pl, t0) + 1;
+            const int n2 = min(ph + s, tb - 1) - max(pl + s - 1, t0) + 1;
+            int span = max(max(n1, n2), 0);
+            bool act = n1 > 0 || n2 > 0;
+            // F_i off its spread, and A(u) at the steps 0, s-1, D-2 (where
+            // the bins open to -inf and +inf meet it)
+            auto Fc = [&](int v) { return v < 0 ? 0 : (v >= D - 1 || v > ph) ? 1 : 0; };
+            const int us[3] = {0, s - 1, D - 2};
+            int ua[3];
 #pragma unroll
-                for (int k = 0; k < 3; ++k) {
-                    const int u = us[k];
-                    const bool fresh = (k < 1 || u != us[0]) && (k < 2 || u != us[1]);
-                    ua[k] = (fresh && u >= t0 && u < tb && u < D - 1) ? Fc(u - s + 1) - Fc(u - s) : 0;
+            for (int k = 0; k < 3; ++k) {
+                const int u = us[k];
+                const bool fresh = (k < 1 || u != us[0]) && (k < 2 || u != us[1]);
+                ua[k] = (fresh && u >= t0 && u < tb && u < D - 1) ? Fc(u - s + 1) - Fc(u - s) : 0;
+            }
+            int m = 0, cnt = 0, dep = 0;
+            for (int e = e0; e < e1; ++e) {
+                const int j = G.col[e];
+                const bool sbs = !(poly_i && clsb[j]);
+                float m_j = 0.0f, rsj = 1.0f;
+                if (sbs) { m_j = mub[j]; rsj = rsb[j]; }
+                if (off >= 0) {
+                    sEmu[off + e - e0] = m_j; sErs[off + e - e0] = rsj; sEon[off + e - e0] = sbs ? 1 : 0;
                 }
-                int m = 0, cnt = 0, dep = 0;
+                if (!sbs) continue;
+                ++m;
+                int cl, ch;
+                spread<FAM>(m_j, rsj, t0 - 1, tb, cl, ch);
+                const int n3 = min(ch + 1, tb - 1) - max(cl, t0) + 1;
+                span = max(span, n3);
+                act = act || n3 > 0;
+                // F_i(u) (1 - F_j(u)) = 1 for ph < u < cl
+                cnt += max(min(min(tb, D - 1), cl) - max(t0, ph + 1), 0);
+#pragma unroll
+                for (int k = 0; k < 3; ++k) dep += ua[k] * (us[k] > ch ? 1 : 0);
+            }
+            flag = 1 + m;
+            c = !act ? kConst : span <= kTinySpan ? kTiny : span <= kNarrowSpan ? kNarrow : kWide;
+            if (c == kConst) {
+                if (D - 1 >= t0 && D - 1 < tb) dep += m * (1 - Fc(D - 1 - s));
+                if (m == 0) dep = cnt = 0;
+                float *pp = W.ppart + (((size_t)b * N + i) * G.ntiles + tile) * kPP;
+                pp[0] = (float)dep; pp[1] = (float)cnt;
+                pp[2] = 0.0f; pp[3] = 0.0f; pp[4] = 0.0f; pp[5] = 0.0f;
                 for (int e = e0; e < e1; ++e) {
-                    const int j = G.col[e];
-                    if (poly_i && clsb[j]) continue;
-                    ++m;
-                    int cl, ch;
-                    spread<FAM>(mub[j], rsb[j], t0 - 1, tb, cl, ch);
-                    const int n3 = min(ch + 1, tb - 1) - max(cl, t0) + 1;
-                    span = max(span, n3);
-                    act = act || n3 > 0;
-                    // F_i(u) (1 - F_j(u)) = 1 for ph < u < cl
-                    cnt += max(min(min(tb, D - 1), cl) - max(t0, ph + 1), 0);
-#pragma unroll
-                    for (int k = 0; k < 3; ++k) dep += ua[k] * (us[k] > ch ? 1 : 0);
+                    if (poly_i && clsb[G.col[e]]) continue;
+                    *reinterpret_cast<float4 *>(W.cpart + (((size_t)b * G.E + e) * G.ntiles + tile) * kCP) =
+                        make_float4(0.0f, 0.0f, 0.0f, 0.0f);
                 }
-                flag = 1 + m;
-                c = !act ? kConst : span <= kTinySpan ? kTiny : span <= kNarrowSpan ? kNarrow : kWide;
-                if (c == kConst) {
-                    if (D - 1 >= t0 && D - 1 < tb) dep += m * (1 - Fc(D - 1 - s));
-                    if (m == 0) dep = cnt = 0;
-                    float *pp = W.ppart + (((size_t)b * N + i) * G.ntiles + tile) * kPP;
-                    pp[0] = (float)dep; pp[1] = (float)cnt;
-                    pp[2] = 0.0f; pp[3] = 0.0f; pp[4] = 0.0f; pp[5] = 0.0f;
-                    for (int e = e0; e < e1; ++e) {
-                        if (poly_i && clsb[G.col[e]]) continue;
-                        *reinterpret_cast<float4 *>(W.cpart + (((size_t)b * G.E + e) * G.ntiles + tile) * kCP) =
-                            make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-                    }
-                    if (dep) atomicAdd(&sConst[0], dep);
-                    if (cnt) atomicAdd(&sConst[1], cnt);
-                    // P_i^0 = F_i(0), P_i^{D-1} = 1 - F_i(D-2): integers off the spread
-                    if (!poly_i && t0 == 0 && Fc(0)) atomicAdd(&sConst[2], 1);
-                    if (!poly_i && D - 1 >= t0 && D - 1 < tb && D > 1 && !Fc(D - 2)) atomicAdd(&sConst[3], 1);
-                }
+                if (dep) atomicAdd(&sConst[0], dep);
+                if (cnt) atomicAdd(&sConst[1], cnt);
+                // P_i^0 = F_i(0), P_i^{D-1} = 1 - F_i(D-2): integers off the spread
+                if (!poly_i && t0 == 0 && Fc(0)) atomicAdd(&sConst[2], 1);
+                if (!poly_i && D - 1 >= t0 && D - 1 < tb && D > 1 && !Fc(D - 2)) atomicAdd(&sConst[3], 1);
             }
         }
         sDirect[tid] = flag;
@@ -325,31 +388,39 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
     __syncthreads();
 
     // Narrow ops: the shortest spreads four at a time per wave, the others one
-    // at a time.
-    constexpr int NW = BS / 64;
-    __shared__ float sUw[NW][TILE];       // usage of each wave's narrow ops
-    __shared__ float sGw[NW][2];          // their V_dep and L_com
+    // at a time.  Each wave's usage row is folded into the step owners' sums
+    // before the row path takes the buffer.
+    __shared__ float sGw[NW][2];          // the narrow ops' V_dep and L_com
     {
         const int lane = tid & 63, w = tid >> 6;
-        for (int p = lane; p < TILE; p += 64) sUw[w][p] = 0.0f;
+        float *sU = sBuf + w * TILE;
+        for (int p = lane; p < TILE; p += 64) sU[p] = 0.0f;
         float g0 = 0.0f, g1 = 0.0f;
-        narrow_ops<FAM, 4, BS>(G, W, mub, rsb, clsb, sCls, sDirect, sUw[w], kTiny, q0, q1, t0, tb, tile, b, g0, g1);
-        narrow_ops<FAM, 1, BS>(G, W, mub, rsb, clsb, sCls, sDirect, sUw[w], kNarrow, q0, q1, t0, tb, tile, b, g0, g1);
+        narrow_ops<FAM, 4, BS>(G, W, mub, rsb, clsb, st, sCls, sDirect, sU, kTiny, nq, t0, tb, tile, b, g0, g1);
+        narrow_ops<FAM, 1, BS>(G, W, mub, rsb, clsb, st, sCls, sDirect, sU, kNarrow, nq, t0, tb, tile, b, g0, g1);
         const float s0 = wave_sum((lane & 15) == 0 ? g0 : 0.0f), s1 = wave_sum((lane & 15) == 2 ? g1 : 0.0f);
         if (lane == 0) { sGw[w][0] = s0; sGw[w][1] = s1; }
     }
     __syncthreads();
+#pragma unroll
+    for (int k = 0; k < SPT; ++k) {
+        float v = sBuf[k * BS + tid];
+#pragma unroll
+        for (int w = 1; w < NW; ++w) v += sBuf[w * TILE + k * BS + tid];
+        accU[k] += v;
+    }
+    __syncthreads();
 
-    for (int q = q0; q < q1; ++q) {
-        if (sCls[q - q0] != kWide) continue;
-        const int flag = sDirect[q - q0];
-        const int i = uniform(G.perm[q]);
-        const int e0 = uniform(G.row_ptr[i]), e1 = uniform(G.row_ptr[i + 1]);
-        const bool poly_i = clsb[i] != 0;
-        const int m = uniform(flag - 1);
-        const float m_i = mub[i], rs = rsb[i];
+    for (int x = 0; x < nq; ++x) {
+        if (sCls[x] != kWide) continue;
+        const int i = uniform(sOpI[x]);
+        const int e0 = uniform(sOpE0[x]), e1 = e0 + uniform(sOpDeg[x]);
+        const int off = uniform(sOpOff[x]);
+        const bool poly_i = uniform(sOpPoly[x]) != 0;
+        const int m = uniform(sDirect[x] - 1);
+        const float m_i = uniformf(sOpMu[x]), rs = uniformf(sOpRs[x]);
         const float cinv = rs * fam_k<FAM>();
-        const int s = uniform(G.delay[i]);
+        const int s = uniform(sOpS[x]);
         const bool win_shift = (m > 0) && (s <= kHalo);
         const int Lh = win_shift ? (s > 1 ? s : 1) : 1;
 
@@ -395,17 +466,38 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
                 }
             }
         }
-        __syncthreads();  // the window may be overwritten from here on
 
+        // Out-edges.  Each wave sums its part of an edge's consumer-side
+        // derivatives at once; the work-group totals of a batch of kEdgeBatch
+        // edges are formed after one barrier.
         float SL[SPT], SU[SPT], SC[SPT];
 #pragma unroll
         for (int k = 0; k < SPT; ++k) { SL[k] = 0.0f; SU[k] = 0.0f; SC[k] = 0.0f; }
         float pL = 0.0f, pU = 0.0f, pC = 0.0f;   // S_i(t0-1), thread 0 only
+        int ne = 0;                              // edges of the open batch
+        auto flush = [&](int n) {   // after a barrier: the batch's totals to cpart
+            if (tid < 4 * n) {
+                const int slot = tid >> 2, c = tid & 3;
+                float r = sCp[cpar][slot][0][c];
+#pragma unroll
+                for (int w2 = 1; w2 < NW; ++w2) r += sCp[cpar][slot][w2][c];
+                // F_j'(u) = -k g_j/sigma_j (k = fam_k, g_j the density factor) [* z for sigma]; L_com enters with a minus
+                const float cj = sCpC[cpar][slot];
+                W.cpart[(((size_t)b * G.E + sCpE[cpar][slot]) * G.ntiles + tile) * kCP + c] = c < 2 ? -cj * r : cj * r;
+            }
+            cpar ^= 1;
+        };
 
         for (int e = e0; e < e1; ++e) {
-            const int j = uniform(G.col[e]);
-            if (poly_i && clsb[j]) continue;  // polynomial edge
-            const float m_j = mub[j], rsj = rsb[j];
+            float m_j, rsj;
+            if (off >= 0) {
+                if (!uniform(sEon[off + e - e0])) continue;   // polynomial edge
+                m_j = uniformf(sEmu[off + e - e0]); rsj = uniformf(sErs[off + e - e0]);
+            } else {
+                const int j = uniform(G.col[e]);
+                if (poly_i && clsb[j]) continue;
+                m_j = mub[j]; rsj = rsb[j];
+            }
             // steps t0-1 .. t0+TILE-1 all past fam_zflush on one side of the
             // consumer's mean: its tail and density are exactly 0 there, so
             // the edge adds only the count of consumers past their median
@@ -446,13 +538,13 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
                 fam_tail_h<FAM>(z, tl, gj);
                 if (z >= 0.0f) { pU += tl; pC += 1.0f; } else { pL += tl; }
             }
-            const float r = block_sum<4, BS>(acc, sRed[par]);
-            par ^= 1;
-            if (tid < 4) {
-                // F_j'(u) = -k g_j/sigma_j (k = fam_k, g_j the density factor) [* z for sigma]; L_com enters with a minus
-                const float cj = rsj * fam_k<FAM>();
-                const float val = (tid < 2) ? -cj * r : cj * r;
-                W.cpart[(((size_t)b * G.E + e) * G.ntiles + tile) * kCP + tid] = val;
+            const float r = wave_sum4(acc[0], acc[1], acc[2], acc[3], lane);
+            if (lane < 4) sCp[cpar][ne][wid][wave4_comp(lane)] = r;
+            if (tid == 0) { sCpE[cpar][ne] = e; sCpC[cpar][ne] = rsj * fam_k<FAM>(); }
+            if (++ne == kEdgeBatch) {
+                __syncthreads();
+                flush(ne);
+                ne = 0;
             }
         }
 
@@ -464,18 +556,28 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
             for (int k = 0; k < SPT; ++k) {
                 const int u = t0 + k * BS + tid;
                 if (u == D - 1) { SL[k] = 0.0f; SU[k] = 0.0f; SC[k] = mf; }
-                if (u < D) { sT[u - t0] = SL[k]; sFm[u - t0] = SU[k]; sFs[u - t0] = SC[k]; }
+            }
+            // S_i(u-1) of each step: from the lane below, across waves and
+            // steps-per-thread blocks through LDS (each wave's last lane)
+            if (lane == 63) {
+#pragma unroll
+                for (int k = 0; k < SPT; ++k) { sLast[wid][k][0] = SL[k]; sLast[wid][k][1] = SU[k]; sLast[wid][k][2] = SC[k]; }
             }
             if (tid == 0) { sPrev[0] = pL; sPrev[1] = pU; sPrev[2] = pC; }
             __syncthreads();
+            flush(ne);
+            ne = 0;
 #pragma unroll
             for (int k = 0; k < SPT; ++k) {
                 const int u = t0 + k * BS + tid;
+                float L1 = __shfl_up(SL[k], 1, 64), U1 = __shfl_up(SU[k], 1, 64), C1 = __shfl_up(SC[k], 1, 64);
+                if (lane == 0) {
+                    const int w2 = wid > 0 ? wid - 1 : NW - 1, k2 = wid > 0 ? k : k - 1;
+                    L1 = k2 >= 0 ? sLast[w2][k2 < 0 ? 0 : k2][0] : sPrev[0];
+                    U1 = k2 >= 0 ? sLast[w2][k2 < 0 ? 0 : k2][1] : sPrev[1];
+                    C1 = k2 >= 0 ? sLast[w2][k2 < 0 ? 0 : k2][2] : sPrev[2];
+                }
                 if (u >= D) continue;
-                const int ix = u - t0;
-                const float L1 = ix ? sT[ix - 1] : sPrev[0];
-                const float U1 = ix ? sFm[ix - 1] : sPrev[1];
-                const float C1 = ix ? sFs[ix - 1] : sPrev[2];
                 const float dS = ((SL[k] - L1) + (SC[k] - C1)) - (SU[k] - U1);
                 pr[2] = fmaf(-rFms[k], dS, pr[2]);
                 pr[3] = fmaf(-rFss[k], dS, pr[3]);
@@ -495,21 +597,17 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
             if (tid < kPP) W.ppart[(((size_t)b * N + i) * G.ntiles + tile) * kPP + tid] = r;
             if (tid == 0) gsum0 += r;
             if (tid == 1) gsum1 += r;
-        } else if (tid < kPP) {
-            W.ppart[(((size_t)b * N + i) * G.ntiles + tile) * kPP + tid] = 0.0f;
+        } else {
+            __syncthreads();   // every wave is done with the window
+            if (tid < kPP) W.ppart[(((size_t)b * N + i) * G.ntiles + tile) * kPP + tid] = 0.0f;
         }
     }
-    // the narrow and constant ops' usage and sums (published by the barrier
-    // after the narrow ops)
+    // the constant ops' usage, and the narrow and constant ops' sums
 #pragma unroll
     for (int k = 0; k < SPT; ++k) {
         const int u = t0 + k * BS + tid;
-        float v = sUw[0][k * BS + tid];
-#pragma unroll
-        for (int w = 1; w < NW; ++w) v += sUw[w][k * BS + tid];
-        if (u == 0) v += (float)sConst[2];
-        if (u == D - 1) v += (float)sConst[3];
-        accU[k] += v;
+        if (u == 0) accU[k] += (float)sConst[2];
+        if (u == D - 1) accU[k] += (float)sConst[3];
     }
     if (tid < 2) {
         float v = sGw[0][tid];
@@ -519,12 +617,12 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
         if (tid == 0) gsum0 += v; else gsum1 += v;
     }
     {
-        float *gs = W.gsum_ops + (((size_t)b * G.ngroups + grp) * G.ntiles + tile) * 2;
+        float *gs = W.gsum_ops + ((((size_t)b * G.ngroups + grp) * G.parts + part) * G.ntiles + tile) * 2;
         if (tid == 0) gs[0] = gsum0;
         if (tid == 1) gs[1] = gsum1;
     }
 
-    float *up = W.Upart + ((size_t)b * G.ngroups + grp) * D;
+    float *up = W.Upart + (((size_t)b * G.ngroups + grp) * G.parts + part) * D;
 #pragma unroll
     for (int k = 0; k < SPT; ++k) {
         const int u = t0 + k * BS + tid;
@@ -830,7 +928,7 @@ hipError_t dispatch(const LaunchCfg &lc, F &&f) {
 
 hipError_t launch_ops(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu, const float *sigma,
                       hipStream_t st) {
-    const dim3 grid(g.ngroups, g.ntiles, g.B);
+    const dim3 grid(g.ngroups * g.parts, g.ntiles, g.B);
     return dispatch(lc, [&](auto fam, auto bs, auto spt) {
         hipLaunchKernelGGL((k_ops<decltype(fam)::value, decltype(bs)::value, decltype(spt)::value>), grid,
                            dim3(decltype(bs)::value), 0, st, g, mu, sigma, w);
