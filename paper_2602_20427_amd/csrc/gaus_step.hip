@@ -44,6 +44,7 @@ namespace gaus {
 // while the group is sorted.
 constexpr int kNarrowSpan = 128;   // widest spread (in steps) on the narrow path
 constexpr int kTinySpan = 32;      // widest spread of the ops taken four per wave
+constexpr int kNarrowPass = 4;     // passes of a lane group over the producer's steps
 
 // Bin edges [lo, hi] (clamped into [a - 1 .. b + 1]) outside which an op's CDF
 // is the exact constant: 0 below lo, 1 above hi.  Widened by one step for the
@@ -145,6 +146,40 @@ __device__ __forceinline__ void narrow_ops(const Graph &G, const Work &W, const 
                 }
             }
 
+            // F_i off its spread (every step of the tile outside X1 u X2 sees
+            // F_i(u), A(u) and the tail 1 - F_i(D-1-s) only through it)
+            auto Fc = [&](int v) { return v < 0 ? 0 : (v >= D - 1 || v > ph) ? 1 : 0; };
+            // Producer values on X1 and X2 \ X1, the same steps for every
+            // out-edge: kNarrowPass passes of GL lanes (x < n1: X1; then X2,
+            // less the steps of X1).  At u = D-1 the A slot holds 1 - F_i(D-1-s).
+            constexpr int R = kNarrowPass;
+            static_assert(R * GL >= 2 * (NP == 1 ? kNarrowSpan : kTinySpan), "passes cover X1 and X2");
+            const int n12 = n1 + n2;
+            const int n12_max = (int)wave_max((float)n12);
+            float cSt[R], cFm[R], cFs[R], cA[R], cFms[R], cFss[R];
+            int cu[R];
+            bool cin2[R];
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const int xx = r * GL + gl;
+                int u = xx < n1 ? x1l + xx : x2l + (xx - n1);
+                const bool in1 = u >= x1l && u <= x1h, in2 = u >= x2l && u <= x2h;
+                const bool take = xx < n12 && (xx < n1 || !in1);
+                cu[r] = take ? u : -1;
+                cin2[r] = take && in2;
+                cSt[r] = 0.0f; cFm[r] = 0.0f; cFs[r] = 0.0f; cA[r] = 0.0f; cFms[r] = 0.0f; cFss[r] = 0.0f;
+                if (r * GL >= n12_max || !take) continue;
+                if (in1) cdf_at<FAM>(u, D, m_i, rs, cinv, cSt[r], cFm[r], cFs[r]);
+                else cSt[r] = Fc(u) ? -0.0f : 0.0f;
+                if (in2) {
+                    float st0;
+                    cdf_at<FAM>(u - s, D, m_i, rs, cinv, st0, cFms[r], cFss[r]);
+                    cA[r] = u < D - 1 ? st_mass(st0, st_at<FAM>(u - s + 1, D, m_i, rs)) : st_1mF(st0);
+                } else {
+                    cA[r] = (float)(u < D - 1 ? Fc(u - s + 1) - Fc(u - s) : 1 - Fc(D - 1 - s));
+                }
+            }
+
             float pr[6] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
             int cnt = 0;   // steps between the spreads, summed over the edges
             const int deg = ok ? e1 - e0 : 0;
@@ -170,50 +205,65 @@ __device__ __forceinline__ void narrow_ops(const Graph &G, const Work &W, const 
                 const int r0 = max(t0, ph + 1), r1 = min(min(tb, D - 1), cl);
                 if (ev) cnt += max(r1 - r0, 0);
                 float c4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-                const int n12 = n1 + n2, n123 = n12 + n3;
-                const int ntot = ev ? n123 + 4 : 0;
+                // X1 u X2 with the cached producer values
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    if (r * GL >= n12_max) break;
+                    const int u = cu[r];
+                    if (!ev || u < 0) continue;
+                    float st_j, Fmj, Fsj;
+                    cdf_at<FAM>(u, D, m_j, rsj, cj, st_j, Fmj, Fsj);
+                    if (cin2[r]) {
+                        const float dS = st_mass(st_at<FAM>(u - 1, D, m_j, rsj), st_j);
+                        pr[2] = fmaf(-cFms[r], dS, pr[2]);
+                        pr[3] = fmaf(-cFss[r], dS, pr[3]);
+                    }
+                    if (u < D - 1) {
+                        const float Fi = st_F(cSt[r]), Rj = st_1mF(st_j);
+                        pr[0] = fmaf(cA[r], st_F(st_j), pr[0]);
+                        pr[1] += fmaf(Fi, Rj, (u >= r0 && u < r1) ? -1.0f : 0.0f);
+                        pr[4] = fmaf(cFm[r], Rj, pr[4]);
+                        pr[5] = fmaf(cFs[r], Rj, pr[5]);
+                        c4[0] = fmaf(cA[r], Fmj, c4[0]);
+                        c4[1] = fmaf(cA[r], Fsj, c4[1]);
+                        c4[2] = fmaf(-Fi, Fmj, c4[2]);
+                        c4[3] = fmaf(-Fi, Fsj, c4[3]);
+                    } else {
+                        pr[0] += cA[r];   // 1 - F_i(D-1-s)
+                    }
+                }
+                // X3 \ (X1 u X2), then the steps 0, s-1, D-2, D-1 off all three:
+                // F_i is constant there (no producer derivatives)
+                const int ntot = ev ? n3 + 4 : 0;
                 const int ntot_max = (int)wave_max((float)ntot);
                 for (int x0 = 0; x0 < ntot_max; x0 += GL) {
-                    // the xx-th step of X1, X2 \ X1, X3 \ (X1 u X2), then 0, s-1, D-2, D-1
                     const int xx = x0 + gl;
                     int u;
                     bool take = xx < ntot;
-                    if (xx < n1) {
-                        u = x1l + xx;
-                    } else if (xx < n12) {
-                        u = x2l + (xx - n1);
-                        take = take && !(u >= x1l && u <= x1h);
-                    } else if (xx < n123) {
-                        u = x3l + (xx - n12);
+                    if (xx < n3) {
+                        u = x3l + xx;
                         take = take && !(u >= x1l && u <= x1h) && !(u >= x2l && u <= x2h);
                     } else {
-                        const int k = xx - n123;
+                        const int k = xx - n3;
                         u = k == 0 ? 0 : k == 1 ? s - 1 : k == 2 ? D - 2 : D - 1;
                         take = take && u >= t0 && u < tb && !(u >= x1l && u <= x1h) && !(u >= x2l && u <= x2h) &&
                                !(u >= x3l && u <= x3h) && !(k >= 1 && u == 0) && !(k >= 2 && u == s - 1) &&
                                !(k == 3 && u == D - 2);
                     }
                     if (!take) continue;
-                    float st_i, Fm_i, Fs_i, st0, Fms, Fss, st_j, Fmj, Fsj;
-                    cdf_at<FAM>(u, D, m_i, rs, cinv, st_i, Fm_i, Fs_i);
-                    cdf_at<FAM>(u - s, D, m_i, rs, cinv, st0, Fms, Fss);
+                    float st_j, Fmj, Fsj;
                     cdf_at<FAM>(u, D, m_j, rsj, cj, st_j, Fmj, Fsj);
-                    const float dS = st_mass(st_at<FAM>(u - 1, D, m_j, rsj), st_j);
-                    pr[2] = fmaf(-Fms, dS, pr[2]);
-                    pr[3] = fmaf(-Fss, dS, pr[3]);
                     if (u < D - 1) {
-                        const float A = st_mass(st0, st_at<FAM>(u - s + 1, D, m_i, rs));
-                        const float Fi = st_F(st_i), Rj = st_1mF(st_j);
+                        const float Fi = (float)Fc(u), A = (float)(Fc(u - s + 1) - Fc(u - s));
+                        const float Rj = st_1mF(st_j);
                         pr[0] = fmaf(A, st_F(st_j), pr[0]);
                         pr[1] += fmaf(Fi, Rj, (u >= r0 && u < r1) ? -1.0f : 0.0f);
-                        pr[4] = fmaf(Fm_i, Rj, pr[4]);
-                        pr[5] = fmaf(Fs_i, Rj, pr[5]);
                         c4[0] = fmaf(A, Fmj, c4[0]);
                         c4[1] = fmaf(A, Fsj, c4[1]);
                         c4[2] = fmaf(-Fi, Fmj, c4[2]);
                         c4[3] = fmaf(-Fi, Fsj, c4[3]);
                     } else {
-                        pr[0] += st_1mF(st0);   // 1 - F_i(D-1-s)
+                        pr[0] += (float)(1 - Fc(D - 1 - s));   // 1 - F_i(D-1-s)
                     }
                 }
                 const float r = group_sum4<NP>(c4[0], c4[1], c4[2], c4[3], lane);
