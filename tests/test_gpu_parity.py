@@ -188,6 +188,18 @@ def test_loss_grad_narrow_ops(D, II, poly):
            f"narrow D={D} II={II} poly={poly}")
 
 
+def test_loss_grad_split_op_work_groups():
+    """The 10k-op workload with 32 restarts has a single 1024-step tile and
+    fewer than 4096 op-kernel work-groups over 320k (restart, op) pairs, so
+    each (group, tile) is split over several work-groups; a mixed state
+    (sigma 0.2 .. 40) puts ops on the constant, narrow, wide and polynomial
+    paths of every split."""
+    p = make_problem("medium", seed=1)
+    B = CONFIGS["medium"].B
+    mu, sg = random_state(p.n_ops, p.D, B, seed=41, sigma_range=(0.2, 40.0), mu_margin=10.0)
+    _check(p, mu, sg, _lam(B, 42), hparams(alpha=0.25, rho=0.02), [0, 13, B - 1], "medium/split work-groups")
+
+
 @pytest.mark.parametrize("W", [16, 32, 64, 128, 256])
 def test_polynomial_path_chunk_widths(W):
     """Every chunk width on a wide-sigma state (all ops polynomial where the
