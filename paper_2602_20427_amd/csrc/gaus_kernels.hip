@@ -309,22 +309,34 @@ __global__ __launch_bounds__(kUsageBS) void k_usage(Graph G, PolyArgs pa, Work W
         for (int x = tid; x < n; x += kUsageBS) sC[gi][x] = src[x];
     }
     __syncthreads();
-    const int slot = blockIdx.x * kUsageBS + tid;
-    if (slot >= T) return;
+    // thread (row part ry, slot): the step-by-step rows ry, ry + 4, ... of
+    // the slot's steps, then the row parts are added in order by ry = 0
+    const int ry = tid >> 6, slot = blockIdx.x * 64 + lane;
+    __shared__ double sPart[kUsageBS / 64][64];
     // fp64 sums: the softmax of the smooth peak terms amplifies a usage error
     // dU by about dU/tau, so U is formed to well below fp32 rounding of its sum
+    double rows = 0.0;
+    const int P = G.parts;
+    if (slot < T) {
+        for (int t = slot; t < D; t += T) {
+            if (nact <= kMaxAct) {
+                for (int r = ry; r < nact * P; r += kUsageBS / 64)
+                    rows += W.Upart[(((size_t)b * G.ngroups + sAct[r / P]) * P + r % P) * D + t];
+            } else if (ry == 0) {
+                for (int g = g0; g < g1; ++g)
+                    if (W.gflag[(size_t)b * G.ngroups + g])
+                        for (int pt = 0; pt < P; ++pt) rows += W.Upart[(((size_t)b * G.ngroups + g) * P + pt) * D + t];
+            }
+        }
+    }
+    sPart[ry][lane] = rows;
+    __syncthreads();
+    if (ry != 0 || slot >= T) return;
     double acc = 0.0;
+#pragma unroll
+    for (int y = 0; y < kUsageBS / 64; ++y) acc += sPart[y][lane];
     for (int t = slot; t < D; t += T) {
         double ut = 0.0;
-        const int P = G.parts;
-        if (nact <= kMaxAct) {
-            for (int q = 0; q < nact; ++q)
-                for (int pt = 0; pt < P; ++pt) ut += W.Upart[(((size_t)b * G.ngroups + sAct[q]) * P + pt) * D + t];
-        } else {
-            for (int g = g0; g < g1; ++g)
-                if (W.gflag[(size_t)b * G.ngroups + g])
-                    for (int pt = 0; pt < P; ++pt) ut += W.Upart[(((size_t)b * G.ngroups + g) * P + pt) * D + t];
-        }
         for (int gi = 0; gi < kGrids; ++gi) {
             const GridArgs &gd = pa.gr[gi];
             if (!gd.on) continue;
@@ -1303,7 +1315,7 @@ hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const 
         hipLaunchKernelGGL(k_ucoef, dim3((nent + 63) / 64, g.K, g.B * kGrids), dim3(64 * kUcoefRows), 0, st,
                            g, pa, w);
     }
-    hipLaunchKernelGGL(k_usage, dim3((g.T + kUsageBS - 1) / kUsageBS, g.K, g.B), dim3(kUsageBS), 0, st, g, pa, w);
+    hipLaunchKernelGGL(k_usage, dim3((g.T + 63) / 64, g.K, g.B), dim3(kUsageBS), 0, st, g, pa, w);
     hipLaunchKernelGGL(k_vres, dim3(g.K, g.B), dim3(kTermsBS), 0, st, g, w, hp);
     if (hp.gamma != 0.0f) {   // expected storage units and their smooth peak
         if ((e = launch_mem_fwd(g, w, lc, a.mu, a.sigma, st)) != hipSuccess) return e;
