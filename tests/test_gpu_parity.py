@@ -200,6 +200,22 @@ def test_loss_grad_split_op_work_groups():
     _check(p, mu, sg, _lam(B, 42), hparams(alpha=0.25, rho=0.02), [0, 13, B - 1], "medium/split work-groups")
 
 
+def test_usage_over_a_thousand_groups_of_one_type():
+    """5000 ops of one resource type with one restart are cut into groups of
+    4 ops: more than the 1024 groups the usage kernel lists in LDS, so it
+    scans the group flags instead."""
+    rng = np.random.default_rng(51)
+    N, D = 5000, 300
+    rows = [np.unique(rng.integers(i + 1, min(N, i + 40), size=rng.poisson(1.5))) if i < N - 1
+            else np.zeros(0, int) for i in range(N)]
+    row_ptr = np.zeros(N + 1, np.int32); row_ptr[1:] = np.cumsum([len(r) for r in rows])
+    col = np.concatenate(rows).astype(np.int32)
+    p = Problem(n_ops=N, row_ptr=row_ptr, col_idx=col, delay=rng.integers(0, 2, size=N).astype(np.int32),
+                rtype=np.zeros(N, np.int32), capacity=np.array([40.0], np.float32), D=D)
+    mu, sg = random_state(N, D, 1, seed=52, sigma_range=(0.3, 30.0))
+    _check(p, mu, sg, _lam(1, 53), hparams(alpha=0.2, rho=0.01), [0], "one type, 1250 groups")
+
+
 @pytest.mark.parametrize("W", [16, 32, 64, 128, 256])
 def test_polynomial_path_chunk_widths(W):
     """Every chunk width on a wide-sigma state (all ops polynomial where the
