@@ -157,26 +157,25 @@ __global__ __launch_bounds__(256 * kFlagPack) void k_flags(Graph G, PolyArgs pa,
         W.gsel[bi] = (unsigned char)g_sel;
         W.gtier[bi] = (unsigned char)(g_sel == kNoGrid ? 0 : tier);
     }
-    // per restart of the pack (256 threads = 4 waves each): OR of the flags
-    auto group_or = [&](int v) {
-        const int w = __any(v) ? 1 : 0;
-        if (lane == 0) wor[wid] = w;
-        __syncthreads();
-        const int r = wor[q * 4] | wor[q * 4 + 1] | wor[q * 4 + 2] | wor[q * 4 + 3];
-        __syncthreads();
-        return r;
-    };
-    const int dq = group_or(d), nq = group_or(narrow);
-    int wk[kGrids];
+    // per restart of the pack (256 threads = 4 waves each): OR of the flags,
+    // bit 0 step-by-step work, bit 1 degree 8/6, bit 2+g ops on grid g (grid 0
+    // also for step-by-step ops: it clears their records)
+    int bits = (d ? 1 : 0) | (narrow ? 2 : 0);
 #pragma unroll
-    for (int g = 0; g < kGrids; ++g)   // grid 0 also for step-by-step ops (it clears their records)
-        wk[g] = group_or(sel == g || (g == 0 && sel == kNoGrid));
+    for (int g = 0; g < kGrids; ++g) bits |= (sel == g || (g == 0 && sel == kNoGrid)) ? 4 << g : 0;
+    int wbits = 0;
+#pragma unroll
+    for (int k = 0; k < 2 + kGrids; ++k) wbits |= __any((bits >> k) & 1) ? 1 << k : 0;
+    if (lane == 0) wor[wid] = wbits;
+    __syncthreads();
+    const int r = wor[q * 4] | wor[q * 4 + 1] | wor[q * 4 + 2] | wor[q * 4 + 3];
     if (op == 0 && q < nb) {
         const size_t bg = (size_t)b * G.ngroups + grp;
-        W.gflag[bg] = dq ? 1 : 0;
-        W.gnarrow[bg] = nq ? 1 : 0;
+        W.gflag[bg] = (r & 1) ? 1 : 0;
+        W.gnarrow[bg] = (r & 2) ? 1 : 0;
 #pragma unroll
-        for (int g = 0; g < kGrids; ++g) W.gwork[((size_t)g * G.B + b) * G.ngroups + grp] = (unsigned char)wk[g];
+        for (int g = 0; g < kGrids; ++g)
+            W.gwork[((size_t)g * G.B + b) * G.ngroups + grp] = (unsigned char)((r >> (2 + g)) & 1);
     }
 }
 
@@ -268,6 +267,7 @@ __global__ __launch_bounds__(64 * kUcoefRows) void k_ucoef(Graph G, PolyArgs pa,
 // the strip value), summed over t = slot mod T.
 constexpr int kUsageBS = 256;
 
+template <int RP>   // threads per slot, each summing every RP-th step-by-step row
 __global__ __launch_bounds__(kUsageBS) void k_usage(Graph G, PolyArgs pa, Work W) {
     constexpr int kMaxAct = 1024;
     __shared__ float sC[kGrids][kUcEntries];
@@ -309,10 +309,11 @@ __global__ __launch_bounds__(kUsageBS) void k_usage(Graph G, PolyArgs pa, Work W
         for (int x = tid; x < n; x += kUsageBS) sC[gi][x] = src[x];
     }
     __syncthreads();
-    // thread (row part ry, slot): the step-by-step rows ry, ry + 4, ... of
+    // thread (row part ry, slot): the step-by-step rows ry, ry + RP, ... of
     // the slot's steps, then the row parts are added in order by ry = 0
-    const int ry = tid >> 6, slot = blockIdx.x * 64 + lane;
-    __shared__ double sPart[kUsageBS / 64][64];
+    constexpr int NS = kUsageBS / RP;   // slots per work-group
+    const int ry = tid / NS, sl = tid % NS, slot = blockIdx.x * NS + sl;
+    __shared__ double sPart[RP][NS];
     // fp64 sums: the softmax of the smooth peak terms amplifies a usage error
     // dU by about dU/tau, so U is formed to well below fp32 rounding of its sum
     double rows = 0.0;
@@ -320,7 +321,7 @@ __global__ __launch_bounds__(kUsageBS) void k_usage(Graph G, PolyArgs pa, Work W
     if (slot < T) {
         for (int t = slot; t < D; t += T) {
             if (nact <= kMaxAct) {
-                for (int r = ry; r < nact * P; r += kUsageBS / 64)
+                for (int r = ry; r < nact * P; r += RP)
                     rows += W.Upart[(((size_t)b * G.ngroups + sAct[r / P]) * P + r % P) * D + t];
             } else if (ry == 0) {
                 for (int g = g0; g < g1; ++g)
@@ -329,12 +330,12 @@ __global__ __launch_bounds__(kUsageBS) void k_usage(Graph G, PolyArgs pa, Work W
             }
         }
     }
-    sPart[ry][lane] = rows;
+    sPart[ry][sl] = rows;
     __syncthreads();
     if (ry != 0 || slot >= T) return;
     double acc = 0.0;
 #pragma unroll
-    for (int y = 0; y < kUsageBS / 64; ++y) acc += sPart[y][lane];
+    for (int y = 0; y < RP; ++y) acc += sPart[y][sl];
     for (int t = slot; t < D; t += T) {
         double ut = 0.0;
         for (int gi = 0; gi < kGrids; ++gi) {
@@ -1315,7 +1316,13 @@ hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const 
         hipLaunchKernelGGL(k_ucoef, dim3((nent + 63) / 64, g.K, g.B * kGrids), dim3(64 * kUcoefRows), 0, st,
                            g, pa, w);
     }
-    hipLaunchKernelGGL(k_usage, dim3((g.T + 63) / 64, g.K, g.B), dim3(kUsageBS), 0, st, g, pa, w);
+    // split work-groups of the op kernel: many step-by-step rows per slot
+    if (g.parts > 1)
+        hipLaunchKernelGGL(k_usage<4>, dim3((g.T + kUsageBS / 4 - 1) / (kUsageBS / 4), g.K, g.B), dim3(kUsageBS), 0,
+                           st, g, pa, w);
+    else
+        hipLaunchKernelGGL(k_usage<1>, dim3((g.T + kUsageBS - 1) / kUsageBS, g.K, g.B), dim3(kUsageBS), 0, st, g,
+                           pa, w);
     hipLaunchKernelGGL(k_vres, dim3(g.K, g.B), dim3(kTermsBS), 0, st, g, w, hp);
     if (hp.gamma != 0.0f) {   // expected storage units and their smooth peak
         if ((e = launch_mem_fwd(g, w, lc, a.mu, a.sigma, st)) != hipSuccess) return e;
