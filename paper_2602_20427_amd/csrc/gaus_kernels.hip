@@ -540,23 +540,13 @@ __global__ __launch_bounds__(kTermsBS) void k_mem_lse(Graph G, Work W, HP hp) {
 // Lagrangian (eq. 11), the weights w_c = lambda_c + rho V_c, and in step mode
 // the multiplier update lambda_c += rho V_c and the Adam bias corrections.
 // ---------------------------------------------------------------------------
-constexpr int kCombineBS = 256;
-
-__device__ float block_sum256(float x, float *scratch /*[4]*/) {
-    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-    x = wave_sum(x);
-    if (lane == 0) scratch[wid] = x;
-    __syncthreads();
-    const float r = (scratch[0] + scratch[1]) + (scratch[2] + scratch[3]);
-    __syncthreads();
-    return r;
-}
+constexpr int kCombineBS = 1024;
 
 __global__ __launch_bounds__(kCombineBS) void k_combine(Graph G, PolyArgs pa, Work W, HP hp,
                                                         const float *__restrict__ lambda_in,
                                                         float *lambda_out, const int *adam_t,
                                                         float *terms_out) {
-    __shared__ float scratch[kCombineBS / 64];
+    __shared__ float scratch[5][kCombineBS / 64];
     const int b = blockIdx.x, tid = threadIdx.x;
     float vres = 0.0f, vdep = 0.0f, lcom = 0.0f, vrec = 0.0f, lres = 0.0f;
     for (int k = tid; k < G.K; k += kCombineBS) {
@@ -583,13 +573,27 @@ __global__ __launch_bounds__(kCombineBS) void k_combine(Graph G, PolyArgs pa, Wo
     const size_t nbp = (size_t)G.nb * G.ntiles;
     const float *bp = W.bpart + (size_t)b * nbp * kBP;
     for (size_t r = tid; r < nbp; r += kCombineBS) vrec += bp[r * kBP + 0];
-    vres = block_sum256(vres, scratch);
-    vdep = block_sum256(vdep, scratch);
-    lcom = block_sum256(lcom, scratch);
-    vrec = block_sum256(vrec, scratch);
-    lres = block_sum256(lres, scratch);
-
+    // the five sums: per wave, then over the waves in order (one barrier)
+    {
+        const int lane = tid & 63, wid = tid >> 6;
+        const float v5[5] = {vres, vdep, lcom, vrec, lres};
+#pragma unroll
+        for (int c = 0; c < 5; ++c) {
+            const float r = wave_sum(v5[c]);
+            if (lane == 0) scratch[c][wid] = r;
+        }
+    }
+    __syncthreads();
     if (tid == 0) {
+        float t5[5];
+#pragma unroll
+        for (int c = 0; c < 5; ++c) {
+            float r = 0.0f;
+            for (int w = 0; w < kCombineBS / 64; ++w) r += scratch[c][w];
+            t5[c] = r;
+        }
+        vres = t5[0]; vdep = t5[1]; lcom = t5[2]; vrec = t5[3]; lres = t5[4];
+
         const float V[3] = {vdep, vres, vrec};
         const float *lam = lambda_in + (size_t)b * 3;
         const float lmem = hp.gamma != 0.0f ? W.lmem[b] : 0.0f;
