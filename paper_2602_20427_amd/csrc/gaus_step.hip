@@ -94,9 +94,18 @@ __device__ __forceinline__ void narrow_ops(const Graph &G, const Work &W, const 
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int grl = lane / GL, gl = lane % GL;   // lane group, lane in the group
     const int D = G.D, N = G.N;
-    for (int base = 0; base < nq; base += 64 * NW) {
+    // lane groups run their edge loops to the longest: ops are taken in
+    // bins of similar step-by-step out-degree (NP > 1)
+    constexpr int NBIN = NP > 1 ? 3 : 1;
+    for (int pass = 0; pass < (nq + 64 * NW - 1) / (64 * NW) * NBIN; ++pass) {
+        const int base = pass / NBIN * 64 * NW, bin = pass % NBIN;
         const int xl = base + lane * NW + w;
-        unsigned long long todo = __ballot(xl < nq && sCls[xl] == want);
+        bool sel = xl < nq && sCls[xl] == want;
+        if (NBIN > 1 && sel) {
+            const int md = sDirect[xl] - 1;
+            sel = (md <= 1 ? 0 : md <= 3 ? 1 : 2) == bin;
+        }
+        unsigned long long todo = __ballot(sel);
         while (todo) {
             int myl = -1;
             for (int k = 0; k < NP && todo; ++k) {
