@@ -200,6 +200,16 @@ def test_loss_grad_split_op_work_groups():
     _check(p, mu, sg, _lam(B, 42), hparams(alpha=0.25, rho=0.02), [0, 13, B - 1], "medium/split work-groups")
 
 
+def test_loss_grad_split_op_work_groups_pipelined():
+    """The pipelined workload (II > 0, back edges) with 80 restarts: two
+    tiles and 3360 op-kernel work-groups, split three ways (a split that
+    does not divide the group sizes)."""
+    p = make_problem("pipelined", seed=2)
+    B = 80
+    mu, sg = random_state(p.n_ops, p.D, B, seed=43, sigma_range=(0.2, 40.0), mu_margin=10.0)
+    _check(p, mu, sg, _lam(B, 44), hparams(alpha=0.25, rho=0.02), [0, 41, B - 1], "pipelined/split work-groups")
+
+
 def test_usage_over_a_thousand_groups_of_one_type():
     """5000 ops of one resource type with one restart are cut into groups of
     4 ops: more than the 1024 groups the usage kernel lists in LDS, so it
