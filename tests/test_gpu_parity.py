@@ -392,6 +392,22 @@ def test_deterministic_bitwise():
         assert np.array_equal(a[k], b[k]), k
 
 
+@pytest.mark.parametrize("cfg,sig", [("medium", (0.05, 6.0)), ("large", (0.2, 4.0))])
+def test_deterministic_bitwise_narrow_and_split(cfg, sig):
+    """Repeat runs agree bit for bit where ops of a wave share LDS usage rows
+    (four-op lane groups), constant ops add integer counts with LDS atomics
+    and the op kernel's work-groups are split (the 10k-op workload with 32
+    restarts)."""
+    p = make_problem(cfg, seed=5)
+    B = CONFIGS[cfg].B
+    mu, sg = random_state(p.n_ops, p.D, B, seed=5, sigma_range=sig)
+    lam = _lam(B, 5)
+    a = gpu_loss_grad(p, mu, sg, lam, hparams())
+    b = gpu_loss_grad(p, mu, sg, lam, hparams())
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
+
+
 def _state(ctx, mu, sg, lam):
     import torch
     dev = torch.device("cuda")
