@@ -158,11 +158,10 @@ __global__ __launch_bounds__(256 * kFlagPack) void k_flags(Graph G, PolyArgs pa,
         W.gtier[bi] = (unsigned char)(g_sel == kNoGrid ? 0 : tier);
     }
     // per restart of the pack (256 threads = 4 waves each): OR of the flags,
-    // bit 0 step-by-step work, bit 1 degree 8/6, bit 2+g ops on grid g (grid 0
-    // also for step-by-step ops: it clears their records)
+    // bit 0 step-by-step work, bit 1 degree 8/6, bit 2+g ops on grid g
     int bits = (d ? 1 : 0) | (narrow ? 2 : 0);
 #pragma unroll
-    for (int g = 0; g < kGrids; ++g) bits |= (sel == g || (g == 0 && sel == kNoGrid)) ? 4 << g : 0;
+    for (int g = 0; g < kGrids; ++g) bits |= sel == g ? 4 << g : 0;
     int wbits = 0;
 #pragma unroll
     for (int k = 0; k < 2 + kGrids; ++k) wbits |= __any((bits >> k) & 1) ? 1 << k : 0;
@@ -724,9 +723,11 @@ __global__ __launch_bounds__(256) void k_final(Graph G, Work W, HP hp, const flo
             cm += pp[tl * kPP + 4]; cs += pp[tl * kPP + 5];
         }
     }
-    const float *ppy = W.ppoly + bi * kPP;
-    dm += ppy[2]; ds += ppy[3]; cm += ppy[4]; cs += ppy[5];
     const bool poly_i = W.cls[bi] != 0;
+    if (poly_i) {   // producer records of the polynomial path (written for its ops only)
+        const float *ppy = W.ppoly + bi * kPP;
+        dm += ppy[2]; ds += ppy[3]; cm += ppy[4]; cs += ppy[5];
+    }
     const int big = G.big_of[i];
     const double *bsum = big >= 0 ? W.bigsum + ((size_t)b * G.nbig + big) * 6 : nullptr;
     if (bsum) { dm += bsum[0]; ds += bsum[1]; cm += bsum[2]; cs += bsum[3]; }
