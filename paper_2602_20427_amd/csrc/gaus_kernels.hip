@@ -319,7 +319,17 @@ __global__ __launch_bounds__(kUsageBS) void k_usage(Graph G, PolyArgs pa, Work W
     const int P = G.parts;
     if (slot < T) {
         for (int t = slot; t < D; t += T) {
-            if (nact <= kMaxAct) {
+            if (nact <= kMaxAct && P == 1) {
+                // four rows in flight at a time (the sum order stays the row order)
+                const float *ub = W.Upart + (size_t)b * G.ngroups * D + t;
+                int r = ry;
+                for (; r + 3 * RP < nact; r += 4 * RP) {
+                    const float u0 = ub[(size_t)sAct[r] * D], u1 = ub[(size_t)sAct[r + RP] * D];
+                    const float u2 = ub[(size_t)sAct[r + 2 * RP] * D], u3 = ub[(size_t)sAct[r + 3 * RP] * D];
+                    rows += u0; rows += u1; rows += u2; rows += u3;
+                }
+                for (; r < nact; r += RP) rows += ub[(size_t)sAct[r] * D];
+            } else if (nact <= kMaxAct) {
                 for (int r = ry; r < nact * P; r += RP)
                     rows += W.Upart[(((size_t)b * G.ngroups + sAct[r / P]) * P + r % P) * D + t];
             } else if (ry == 0) {
