@@ -29,35 +29,98 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 METRIC = "op-step evals/sec (fwd+bwd+Adam), ms/iteration, % roofline at 50k ops"
 
-# VALU cost model of one iteration (per-unit algorithmic work):
-#   per op-bin-edge (B*N*(D-1) units): 20 FMA-class instructions plus 2
-#     transcendental evaluations (the CDF needs an exp and a reciprocal; the
-#     Gaussian factor of the gradient shares the exp);
-#   per edge-step (B*(E+E_B)*(D-1) units): 10 FMA-class instructions (the
-#     products and sums of the edge terms and their derivatives, with both
-#     end points' rows available).
-# A transcendental occupies TRANS_WEIGHT FMA issue slots: the measured ratio of
-# the v_fma_f32 to the v_exp_f32 rate on gfx950 (gaus_microbench:
-# 101.7 vs 21.2 per clock per CU).  One slot = one fp32 FMA = 2 flops; the
-# peak is MI355X's 157.3 TFLOP/s fp32 vector rate.
-#
-# The units of one launch of a kernel are the op-bin-edges and edge-steps it
-# is responsible for: the chunk-polynomial kernel (k_poly) owns the (restart,
-# op) pairs classified onto its path and the edges with both ends there
-# (gaus_poly_census); the step-by-step kernel (k_ops) owns the rest of the
-# forward edges and ops.  k_poly reaches its units through per-chunk
-# polynomial expansions, so its figure is an effective rate of this per-unit
-# model, not an instruction-issue rate.
+# Roofline of the dominant kernel.  Peaks are MI355X's published figures:
+# fp32 vector 157.3 TFLOP/s = 256 CU x 128 FMA lanes per clock x 2.4 GHz x 2
+# flops (7.86e13 FMA lane-operations/s), a transcendental (v_exp_f32,
+# v_rcp_f32) issuing at a quarter of that rate (4 FMA slots), HBM 8 TB/s.
+PEAK_TFLOPS = 157.3
+N_CU = 256
+CLOCK_HZ = 2.4e9
+FMA_LANES_PER_CLK_CU = 128
+PEAK_FMA_LANE_OPS = FMA_LANES_PER_CLK_CU * N_CU * CLOCK_HZ
+TRANS_SLOTS = 4.0
+PEAK_HBM_GBS = 8000.0
+
+# (1) Chunk-polynomial kernel (k_poly): the work the method's sums require on
+# a chunk of W steps at series degree d (NC = d + 1 coefficients per vector,
+# the expansion carrying T_0 .. T_{d+2}), counted in FMA-class operations:
+#   one CDF evaluation (tail and density of one z): the z value, |z|/sqrt(2),
+#     z^2, the degree-8 rational form of erfc (8 FMA) and its products:
+#     EVAL_FMA, plus 2 transcendentals (exp, reciprocal);
+#   expansion at a chunk centre: one evaluation + 2 per Taylor coefficient
+#     T_2 .. T_{d+2} (the three-term recursion with folded constants);
+#   per (restart, op, chunk): the expansion at the centre, and for ops with
+#     Lat != 1 a second one at the centre shifted by Lat - 1; the one-step mass
+#     series (4 terms per coefficient) of both; dF/dmu one step back (5 terms
+#     per coefficient); dF/dmu and dF/dsigma = z dF/dmu (3 per coefficient)
+#     of both; the usage coefficients (1 per coefficient); six moment vectors
+#     (H p)_k truncated at degree d (moments_fma(d) each);
+#   per (restart, edge, chunk): the consumer's expansion, its dF/dmu,
+#     dF/dsigma and mass (1 + 2 + 4 per coefficient) and ten dot products;
+#   strip positions (per restart, SP = L0 + 2 of them): one evaluation per
+#     op and position plus STRIP_OP_FMA for the derived rows, one evaluation
+#     per edge and position plus STRIP_EDGE_FMA for its products.
+EVAL_FMA = 14
+STRIP_OP_FMA = 8
+STRIP_EDGE_FMA = 12
+TIER_DEGREE = {1: 8, 2: 6, 3: 5}
+
+
+def moments_fma(d):
+    """FMAs of one moment vector (H p)_k = sum_l H_{k+l} p_l over k + l <= d, k + l even."""
+    return sum(t + 1 for t in range(0, d + 1, 2))
+
+
+def expansion_fma(d):
+    return EVAL_FMA + 2 * (d + 1)
+
+
+def poly_op_chunk_fma(d, shifted):
+    nc = d + 1
+    per_expansion = expansion_fma(d) + 4 * nc + 3 * nc          # expansion, mass series, dF/dmu and dF/dsigma
+    return (1 + shifted) * per_expansion + 5 * nc + nc + 6 * moments_fma(d)
+
+
+def poly_edge_chunk_fma(d):
+    nc = d + 1
+    return expansion_fma(d) + 7 * nc + 10 * nc
+
+
+def poly_model(tier_census, grids, shifted):
+    """FMA-class operations and transcendentals of one k_poly launch from the
+    census of (restart, op) pairs and polynomial edges per grid and tier;
+    shifted = share of the ops whose delay is not 1."""
+    fma = trans = 0.0
+    for g, gr in enumerate(grids):
+        if not gr["on"]:
+            continue
+        nc, sp = gr["chunks"], gr["L0"] + 2
+        for t, d in TIER_DEGREE.items():
+            ops, edges = float(tier_census[g][t][0]), float(tier_census[g][t][1])
+            fma += ops * (nc * poly_op_chunk_fma(d, shifted) + sp * (EVAL_FMA + STRIP_OP_FMA))
+            fma += edges * (nc * poly_edge_chunk_fma(d) + sp * (EVAL_FMA + STRIP_EDGE_FMA))
+            trans += ops * (nc * 2 * (1 + shifted) + sp * 2) + edges * (nc * 2 + sp * 2)
+    return fma, trans
+
+
+# (2) Step-by-step op kernel (k_ops; the narrow regime, where each op's CDF
+# differs from exactly 0 or 1 on a few steps only): bound by memory traffic
+# and latency, priced against HBM with the bytes any split of the method
+# must move across this kernel's boundary: per (restart, op) its mean and
+# width in and four producer-side derivative pieces out (24 B); per
+# (restart, edge) the consumer's mean and width in and four consumer-side
+# pieces out (24 B); per (restart, type, step) one usage value out (4 B); the
+# graph once (delay, type, row start per op, consumer per edge: 12 B + 4 B).
+OPS_BYTES_PER_OP, OPS_BYTES_PER_EDGE, OPS_BYTES_PER_USAGE = 24, 24, 4
+
+# (3) The per-step model of the whole iteration, kept as an effective rate
+# (not a roofline): per op-bin-edge 20 FMA-class instructions and 2
+# transcendentals, per edge-step 10; the chunk polynomials reach these units
+# with far fewer operations, so this rate can exceed the fp32 peak.
 FMA_PER_OP_STEP = 20.0
 TRANS_PER_OP_STEP = 2.0
 FMA_PER_EDGE_STEP = 10.0
-FMA_LANES_PER_CLK_CU = 101.7
-EXP_LANES_PER_CLK_CU = 21.2
-TRANS_WEIGHT = FMA_LANES_PER_CLK_CU / EXP_LANES_PER_CLK_CU
-PEAK_TFLOPS = 157.3
-# issue-rate reference: the measured v_fma_f32 rate above
-N_CU = 256
-CLOCK_HZ = 2.4e9
+
 CSRC = os.path.join(ROOT, "paper_2602_20427_amd", "csrc")
 # the sources a kernel is built from (its file and the shared device headers)
 KERNEL_SOURCES = {"k_poly": "gaus_poly.hip", "k_ops": "gaus_step.hip"}
@@ -77,8 +140,8 @@ def kernel_source_hash(kernel: str) -> str:
     return h.hexdigest()[:16]
 
 
-def model_flops(units_op, units_edge):
-    slots = units_op * (FMA_PER_OP_STEP + TRANS_PER_OP_STEP * TRANS_WEIGHT) + units_edge * FMA_PER_EDGE_STEP
+def per_step_model_flops(units_op, units_edge):
+    slots = units_op * (FMA_PER_OP_STEP + TRANS_PER_OP_STEP * TRANS_SLOTS) + units_edge * FMA_PER_EDGE_STEP
     return 2.0 * slots
 
 
@@ -103,16 +166,16 @@ def pmc_traffic(kernel, profile):
 
 
 def pmc_issue(kernel, profile, kernel_ms):
-    """VALU issue rate from the committed SQ-counter summary, against the
-    measured v_fma_f32 issue rate of the chip; else None."""
+    """VALU issue rate (wave instructions x 64 lanes) from the committed
+    SQ-counter summary, against the fp32 FMA lane rate of the spec
+    (128 lanes per clock per CU); else None."""
     valu = pmc_value(kernel, profile, "valu_instructions_per_launch")
     if valu is None:
         return None
     lane_ops = valu * 64
     rate = lane_ops / (kernel_ms * 1e-3)
-    peak = FMA_LANES_PER_CLK_CU * N_CU * CLOCK_HZ
     return {"valu_lane_ops_per_launch": lane_ops, "achieved_lane_ops_per_s": rate,
-            "peak_lane_ops_per_s": peak, "frac": rate / peak}
+            "peak_lane_ops_per_s": PEAK_FMA_LANE_OPS, "frac": rate / PEAK_FMA_LANE_OPS}
 
 
 def describe(cfg, prob):
@@ -123,32 +186,81 @@ def describe(cfg, prob):
             f"{cfg.name}: random layered DAG, {prob.n_ops} ops, D={prob.D}, B={cfg.B}, mu~U[0,D), sigma={cfg.sigma0}")
 
 
-def cpu_baseline(prob, mu, sigma, lam, hp, min_seconds):
-    """The oracle as it stands: one fused iteration (loss, gradient, Adam) per
-    restart of the workload, cycling through the restarts from the same state
-    until at least min_seconds have passed (and at least one restart)."""
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _oracle_iterations(prob, mu, sigma, lam, hp, min_seconds, max_iters=None):
+    """Whole restart-iterations of the oracle (loss, gradient, Adam on mu and
+    sigma) cycling over the restarts from the same state, until min_seconds
+    have passed (at least one); returns (count, seconds)."""
     import numpy as np
     import oracle
-    oracle.build(force=False)
-    oracle.set_family(hp.family)
     B = mu.shape[0]
     done = 0
     t0 = time.perf_counter()
-    while done == 0 or time.perf_counter() - t0 < min_seconds:
+    while done == 0 or (time.perf_counter() - t0 < min_seconds and (max_iters is None or done < max_iters)):
         b = done % B
         _, _, gm, gs, _ = oracle.loss_grad(prob, mu[b:b + 1].astype(np.float64), sigma[b:b + 1].astype(np.float64),
                                            lam[b:b + 1].astype(np.float64), hp.alpha_com, hp.rho,
                                            beta=hp.beta_res, tau=hp.tau, gamma=hp.gamma_mem)
-        z = np.zeros(prob.n_ops)
+        z = np.zeros(mu.shape[1])
         oracle.adam(mu[b].astype(np.float64), z, z, gm[0], 1, hp.lr)
         oracle.adam(sigma[b].astype(np.float64), z, z, gs[0], 1, hp.lr)
         done += 1
-    dt = time.perf_counter() - t0
+    return done, time.perf_counter() - t0
+
+
+def cpu_baseline(prob, mu, sigma, lam, hp, min_seconds, single_ops, cfg=None):
+    """The oracle as it stands, timed on the host's cores:
+    * all threads: whole restart-iterations of the full workload from the
+      benchmark's state, cycling over the B restarts, for at least
+      min_seconds; value = op-step evals/s, plus ms per B-restart iteration;
+    * one thread: one restart-iteration of the same generator and
+      parameters at single_ops ops (same horizon, out-degree, delays, types,
+      capacities), the bounded single-core sample."""
+    import numpy as np
+    import oracle
+    oracle.build(force=False)
+    oracle.set_family(hp.family)
+    B, D = mu.shape[0], prob.D
+    threads = oracle.num_threads()
+    done, dt = _oracle_iterations(prob, mu, sigma, lam, hp, min_seconds)
+    out = {"value": done * prob.n_ops * D / dt, "unit": "op-step evals/s", "cores": threads, "kind": "oracle",
+           "cpu_model": cpu_model(),
+           "ms_per_iteration": dt / done * B * 1e3,
+           "sample": f"{done} restart-iterations of the full workload (cycling over its {B} restarts from the "
+                     f"benchmark's state), each one fused iteration (loss, gradient, Adam), fp64 C oracle, "
+                     f"OpenMP on {threads} threads; {dt:.2f} s; ms_per_iteration = the {B} restarts of one "
+                     f"iteration"}
+    if single_ops > 0 and cfg is not None:
+        from paper_2602_20427_amd.workloads import make_problem, restart_uniforms
+        n = min(single_ops, prob.n_ops)
+        sub = make_problem(cfg, seed=0, n_ops=n)
+        u = restart_uniforms(n, 1, seed=0)
+        m1, s1, rc = oracle.init_state(sub, 1, u, kappa=float(hp.kappa), sigma_min=float(hp.sigma_min))
+        oracle.set_num_threads(1)
+        try:
+            d1, t1 = _oracle_iterations(sub, m1.astype(np.float32), s1.astype(np.float32), lam[:1], hp, 0.0,
+                                        max_iters=1)
+        finally:
+            oracle.set_num_threads(threads)
+        rate1 = d1 * n * D / t1
+        out["single_thread"] = {
+            "value": rate1, "unit": "op-step evals/s", "cores": 1,
+            "ms_per_iteration_scaled": B * prob.n_ops * D / rate1 * 1e3,
+            "sample": f"{d1} restart-iteration (loss, gradient, Adam) of the same generator and parameters at "
+                      f"{n} ops ({sub.n_edges} edges, D={D}, paper initialization), 1 thread; {t1:.2f} s; "
+                      f"ms_per_iteration_scaled = B*N*D of the full workload at that rate"}
     oracle.set_family("gaussian")
-    return {"value": done * prob.n_ops * prob.D / dt, "unit": "op-step evals/s",
-            "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": f"{done} restart-iterations (cycling over the {B} restarts of the same workload and state), "
-                      f"one fused iteration (loss, gradient, Adam) each, fp64 C oracle with OpenMP; {dt:.2f} s"}
+    return out
 
 
 def main():
@@ -160,6 +272,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum CPU time of the oracle sample (whole restart-iterations)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-single-ops", type=int, default=5000,
+                    help="ops of the one-thread oracle sample (the same generator at this size); 0 = skip")
     ap.add_argument("--poly-chunk", type=int, default=0,
                     help="chunk width of the polynomial path: 0 = library's choice, -1 = off (every op step by step)")
     ap.add_argument("--lse-beta", type=float, default=0.0,
@@ -169,7 +283,7 @@ def main():
                     help="weight of the smooth peak storage term (storage units of 1-32 bits per op and a "
                          "sink op are added to the workload); 0 = off")
     ap.add_argument("--family", default="gaussian", choices=["gaussian", "logistic", "laplace", "cauchy"],
-                    help="distribution of the relaxed start times (App. D); the Laplace law runs every "
+                    help="distribution of the relaxed start times (App. E); the Laplace law runs every "
                          "op step by step")
     ap.add_argument("--sigma", type=float, default=0.0,
                     help="replace the initial widths by this sigma (a sharpened state like late iterations: "
@@ -258,6 +372,7 @@ def main():
     ktimes = ctx.kernel_timing_read()
     ctx.kernel_timing(False)
     census = ctx.poly_census()
+    tier_census = ctx.poly_tier_census()
     poly_cfg = ctx.poly_config()
     grids = ctx.poly_grids()
     for gr, n in zip(grids, ctx.poly_grid_census()):
@@ -267,7 +382,7 @@ def main():
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     tt = terms.cpu().numpy()
 
-    # units of each per-step kernel (see the cost model above)
+    # per-step model units of each kernel (effective rates only)
     E = prob.n_edges
     units = {"poly": (census["ops"] * (D - 1), census["edges"] * (D - 1)),
              "ops": ((B * N - census["ops"]) * (D - 1), (B * E - census["edges"]) * (D - 1))}
@@ -276,10 +391,10 @@ def main():
         if n == 0:
             continue
         kms = tot_ms / n
-        fl = model_flops(*units[k])
+        fl = per_step_model_flops(*units[k])
         kern[KERNEL_NAMES[k]] = {"ms": kms, "launches": n, "op_bin_edges": units[k][0],
-                                 "edge_steps": units[k][1], "model_tflops": fl / 1e12,
-                                 "achieved_tflops": fl / (kms * 1e-3) / 1e12}
+                                 "edge_steps": units[k][1],
+                                 "per_step_model_tflops_per_s": fl / (kms * 1e-3) / 1e12}
     dom = max(kern, key=lambda k: kern[k]["ms"])
     log(f"[bench] {ms_per_step:.3f} ms/step wall; gaus_step {step_ms_events:.3f} ms/iter (events); "
         f"legalize {legalize_ms:.3f} ms; " +
@@ -291,7 +406,6 @@ def main():
         f"V_rec={tt[0, 3]:.6g} L_com={tt[0, 4]:.6g}; legalize status {status.tolist()}")
 
     value = B * N * D / (ms_per_step * 1e-3)
-    achieved = kern[dom]["achieved_tflops"]
     # committed counter summary of this kernel and launch configuration
     profile = f"{dom}_{args.workload}" + ("" if args.poly_chunk == 0 else
                                           "_direct" if args.poly_chunk < 0 else f"_w{args.poly_chunk}")
@@ -303,7 +417,32 @@ def main():
         profile += "_" + args.family
     if args.sigma > 0:
         profile += f"_sigma{args.sigma:g}"
-    whole = model_flops(B * N * (D - 1), B * (E + prob.n_back) * (D - 1))
+    kms = kern[dom]["ms"]
+    if dom == "k_poly":
+        shifted = float(np.mean(np.asarray(prob.delay) != 1))
+        fma, trans = poly_model(tier_census, grids, shifted)
+        flops = 2.0 * (fma + TRANS_SLOTS * trans)
+        achieved = flops / (kms * 1e-3) / 1e12
+        roofline = {"bound": "alu", "achieved": achieved, "peak": PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": achieved / PEAK_TFLOPS, "traffic": pmc_traffic(dom, profile),
+                    "kernel": dom, "kernel_ms": kms,
+                    "work_per_launch": {"fma": fma, "transcendental": trans, "flops": flops,
+                                        "ops_by_grid_tier": tier_census.tolist()},
+                    "model": "chunk-polynomial work of the method's sums per (restart, op, chunk) and "
+                             "(restart, edge, chunk) at each op's series degree, plus the strip steps; "
+                             "a transcendental = 4 FMA slots, 2 flops per slot"}
+    else:
+        n_ops_k = B * N - census["ops"]
+        n_edges_k = B * E - census["edges"]
+        alg = (n_ops_k * OPS_BYTES_PER_OP + n_edges_k * OPS_BYTES_PER_EDGE + B * prob.n_types * D *
+               OPS_BYTES_PER_USAGE + 16 * N + 4 * E)
+        achieved = alg / (kms * 1e-3) / 1e9
+        roofline = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                    "frac": achieved / PEAK_HBM_GBS, "traffic": pmc_traffic(dom, profile),
+                    "kernel": dom, "kernel_ms": kms, "algorithmic_bytes_per_launch": alg,
+                    "model": "per (restart, op) 24 B, per (restart, edge) 24 B, per (restart, type, step) 4 B, "
+                             "graph 16 B per op + 4 B per edge"}
+    whole = per_step_model_flops(B * N * (D - 1), B * (E + prob.n_back) * (D - 1))
     out = {
         "metric": METRIC, "value": value, "unit": "op-step evals/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
@@ -321,23 +460,17 @@ def main():
         "ms_per_iteration_events": step_ms_events, "legalize_ms": legalize_ms,
         "poly_path": dict(poly_cfg, ops=census["ops"], edges=census["edges"], grids=grids),
         "solve": solve_stats,
-        "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_TFLOPS,
-                     "traffic": pmc_traffic(dom, profile),
-                     "kernel": dom, "kernel_ms": kern[dom]["ms"],
-                     "model": f"{FMA_PER_OP_STEP:g} FMA + {TRANS_PER_OP_STEP:g} transcendental "
-                              f"(x{TRANS_WEIGHT:.2f} FMA slots) per op-bin-edge, {FMA_PER_EDGE_STEP:g} FMA per "
-                              f"edge-step, 2 flops per FMA slot; units = those the kernel owns",
-                     "note": "k_poly reaches its op-bin-edges through per-chunk polynomial expansions and "
-                             "needs fewer operations than this per-step model charges, so frac can exceed 1; "
-                             "'issue' gives its measured VALU issue rate"},
-        "issue": pmc_issue(dom, profile, kern[dom]["ms"]),
+        "roofline": roofline,
+        "issue": pmc_issue(dom, profile, kms),
         "kernels": kern,
-        "iteration_model_tflops_per_s": whole / (step_ms_events * 1e-3) / 1e12,
+        "per_step_model_tflops_per_s": {
+            "iteration": whole / (step_ms_events * 1e-3) / 1e12,
+            "note": "20 FMA + 2 transcendentals per op-bin-edge and 10 FMA per edge-step over B*N*(D-1) and "
+                    "B*(E+E_B)*(D-1) units: an effective rate of the per-step formulation, not a roofline"},
     }
     if not args.no_cpu_baseline:
         log(f"[bench] CPU oracle for at least {args.cpu_seconds:g} s")
-        out["cpu_baseline"] = cpu_baseline(prob, mu0, sg0, lam0, hp, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(prob, mu0, sg0, lam0, hp, args.cpu_seconds, args.cpu_single_ops, cfg)
     if args.copy_probe_mib > 0:
         n = args.copy_probe_mib * (1 << 20) // 4
         a = torch.ones(n, device=dev)

@@ -107,7 +107,7 @@ typedef struct {
                                       usage (App. B.3).  Holders with at most 4 successors,
                                       all wide Gaussians, take it on the chunk polynomials,
                                       the others step by step. */
-    int32_t family;                /* distribution of the relaxed start times (App. D):
+    int32_t family;                /* distribution of the relaxed start times (App. E):
                                       0 Gaussian, 1 logistic (scale sigma sqrt(3)/pi),
                                       2 Laplace (scale sigma/sqrt(2)), 3 Cauchy (scale
                                       sigma sqrt(2 ln 2)); sigma keeps its meaning as the
@@ -218,6 +218,26 @@ typedef struct {
 gaus_status gaus_solve(gaus_ctx *ctx, const gaus_solve_params *prm, int32_t *best_sched, double *best_cost,
                        gaus_solve_stats *stats);
 
+/* One check of the Alg. 1 driver on the bound state, the step gaus_solve
+ * takes after each block of iterations (Sec. 3.3 "Sampling"; App. A,
+ * "Empirical Behavior", reset to the prior best).  For every restart, in
+ * order: the means are rounded half-up and legalized (Alg. 3 / Alg. 4) into a
+ * candidate; the candidate is costed (gaus_schedule_cost); it replaces the
+ * restart's best (best_sched DEVICE [B][N] int32, best_cost DEVICE [B][6]
+ * double, as gaus_schedule_cost writes) when it is better in the order
+ * gaus_solve documents (equal ones do not replace); if the rounding was not
+ * already legal, mu is re-initialized from the candidate when it improved the
+ * best, else from the best held before this check, the restart's Adam
+ * moments (both halves) are cleared and, with reinit_sigma = 1, sigma is set
+ * to max(kappa (ALAP - ASAP), sigma_min).  A best_cost row (+inf, +inf,
+ * +inf, +inf, +inf, 0) holds no schedule yet (every candidate replaces it).
+ * mode HOST [B] (or NULL) receives per restart 0 (rounding legal, state
+ * kept), 1 (re-initialized from the candidate) or 2 (reset to the prior
+ * best); when it is given the call synchronizes, else it is asynchronous.
+ * Errors: INVALID_ARG (state not bound, null pointer), DEVICE. */
+gaus_status gaus_solve_check(gaus_ctx *ctx, int32_t *best_sched, double *best_cost, int32_t reinit_sigma,
+                             int32_t *mode);
+
 /* Paper initialization (Sec. 3.3, Alg. 1): sigma = max(kappa*(ALAP-ASAP),
  * sigma_min); restart 0 gets mu = (ASAP+ALAP)/2, restart b >= 1 gets
  * mu = ASAP + u[b][i]*(ALAP-ASAP) with u HOST [B][N] double in [0,1) (may be
@@ -278,6 +298,15 @@ gaus_status gaus_get_poly_grids(const gaus_ctx *ctx, int32_t cfg[15]);
 /* Census of the last iteration's grid assignment (HOST output, [3]):
  * (restart, op) pairs evaluated on grid 0, 1, 2.  Synchronizes the stream. */
 gaus_status gaus_poly_grid_census(gaus_ctx *ctx, int64_t counts[3]);
+
+/* Census of the last iteration's chunk-polynomial work by grid and series
+ * degree tier (HOST output, [3][4][2]): counts[g][t][0] = (restart, op)
+ * pairs evaluated on grid g at tier t (1: degree 8, 2: degree 6, 3: degree 5;
+ * t = 0 unused), counts[g][t][1] = their out-edges evaluated there (both
+ * ends on the polynomial path).  The per-unit work of the polynomial kernel
+ * follows from these counts and each grid's chunk and strip sizes
+ * (gaus_get_poly_grids).  Synchronizes the stream. */
+gaus_status gaus_poly_tier_census(gaus_ctx *ctx, int64_t counts[24]);
 
 /* Message of the last failed call on ctx (or of the last failed gaus_init
  * when ctx is NULL).  Never NULL. */

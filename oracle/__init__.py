@@ -73,6 +73,13 @@ def _load():
         lib.orc_set_family.restype = None
         lib.orc_mass.argtypes = [dbl, dbl, i32, i32]
         lib.orc_mass.restype = dbl
+        lib.orc_check.argtypes = [P, vp, vp, vp, vp, vp, vp, dbl, dbl, dbl, i32, C.c_float, C.c_float,
+                                  vp, vp, vp, vp]
+        lib.orc_check.restype = C.c_int
+        lib.orc_usage_cell_grad.argtypes = [P, vp, vp, i32, i32, dbl, vp, vp]
+        lib.orc_usage_cell_grad.restype = C.c_int
+        lib.orc_set_num_threads.argtypes = [i32]
+        lib.orc_set_num_threads.restype = None
         lib.orc_num_threads.argtypes = []
         lib.orc_num_threads.restype = C.c_int
         _lib = lib
@@ -119,11 +126,16 @@ def num_threads() -> int:
     return int(_load().orc_num_threads())
 
 
+def set_num_threads(n: int) -> None:
+    """OpenMP threads of the oracle's loops from now on."""
+    _load().orc_set_num_threads(int(n))
+
+
 FAMILIES = {"gaussian": 0, "logistic": 1, "laplace": 2, "cauchy": 3}
 
 
 def set_family(family) -> None:
-    """Distribution family of the relaxed start times (App. D) for the calls
+    """Distribution family of the relaxed start times (App. E) for the calls
     that follow: "gaussian", "logistic", "laplace", "cauchy" (or 0..3)."""
     _load().orc_set_family(int(FAMILIES.get(family, family)))
 
@@ -160,6 +172,19 @@ def loss_grad(prob, mu, sigma, lam, alpha, rho, grad=True, tie_tol=1e-4, beta=0.
     return terms, U, gm, gs, ties
 
 
+def usage_cell_grad(prob, mu, sigma, k, s, w=1.0):
+    """w * dU_k(s)/dmu_i and w * dU_k(s)/dsigma_i for every op i (fp64 [N]
+    each) of one restart: the gradient the ReLU indicator of cell (k, s) adds
+    when it is 1 (App. B.2 eq:relu, folded as in App. B.3)."""
+    lib, op = _load(), _op(prob)
+    m = np.ascontiguousarray(mu, np.float64); sg = np.ascontiguousarray(sigma, np.float64)
+    gm = np.zeros(op.n); gs = np.zeros(op.n)
+    rc = lib.orc_usage_cell_grad(C.byref(op.s), _ptr(m), _ptr(sg), int(k), int(s), float(w), _ptr(gm), _ptr(gs))
+    if rc != OK:
+        raise RuntimeError(f"oracle usage_cell_grad failed: {rc}")
+    return gm, gs
+
+
 def edge_terms_double_sum(prob, mu, sigma):
     """(V_dep, L_com, V_rec) from the paper's literal double sums (tiny only)."""
     lib, op = _load(), _op(prob)
@@ -191,6 +216,38 @@ def legalize(prob, mu):
         st[b] = lib.orc_legalize(C.byref(op.s), _ptr(m), _ptr(s))
         out[b] = s
     return out, st
+
+
+NO_BEST = (np.inf, np.inf, np.inf, np.inf, np.inf, 0.0)   # a best-cost row holding no schedule yet
+
+
+def check(prob, mu, sigma, m, v, best_s, best_c, alpha=0.0, beta=0.0, gamma=0.0, reinit_sigma=0,
+          kappa=1.0 / 6.0, sigma_min=0.05):
+    """One check of the Alg. 1 driver for every restart (orc_check): mu,
+    sigma [B,N] float32, m, v [2,B,N] float32 (moments of mu, then sigma),
+    best_s [B,N] int64, best_c [B,6]; returns new copies of all six and
+    (cand [B,N] int64, cand_c [B,6], mode [B], improved [B])."""
+    lib, op = _load(), _op(prob)
+    mu = np.array(mu, np.float32, copy=True); sigma = np.array(sigma, np.float32, copy=True)
+    m = np.array(m, np.float32, copy=True); v = np.array(v, np.float32, copy=True)
+    best_s = np.array(best_s, np.int64, copy=True); best_c = np.array(best_c, np.float64, copy=True)
+    B = mu.shape[0]
+    cand = np.zeros((B, op.n), np.int64); cand_c = np.zeros((B, 6))
+    mode = np.zeros(B, np.int32); imp = np.zeros(B, np.int32)
+    for b in range(B):
+        mb, sb = np.ascontiguousarray(mu[b]), np.ascontiguousarray(sigma[b])
+        m2, v2 = np.ascontiguousarray(m[:, b]), np.ascontiguousarray(v[:, b])
+        bs, bc = np.ascontiguousarray(best_s[b]), np.ascontiguousarray(best_c[b])
+        cs, cc = np.zeros(op.n, np.int64), np.zeros(6)
+        md, im = np.zeros(1, np.int32), np.zeros(1, np.int32)
+        rc = lib.orc_check(C.byref(op.s), _ptr(mb), _ptr(sb), _ptr(m2), _ptr(v2), _ptr(bs), _ptr(bc),
+                           float(alpha), float(beta), float(gamma), int(reinit_sigma), float(kappa),
+                           float(sigma_min), _ptr(cs), _ptr(cc), _ptr(md), _ptr(im))
+        if rc != OK:
+            raise RuntimeError(f"oracle check failed: {rc}")
+        mu[b], sigma[b], m[:, b], v[:, b], best_s[b], best_c[b] = mb, sb, m2, v2, bs, bc
+        cand[b], cand_c[b], mode[b], imp[b] = cs, cc, md[0], im[0]
+    return mu, sigma, m, v, best_s, best_c, cand, cand_c, mode, imp
 
 
 def schedule_cost(prob, sched, alpha=0.0, beta=0.0, gamma=0.0):

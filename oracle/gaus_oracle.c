@@ -10,7 +10,7 @@
  *
  *   - masses P_i^d                : Sec. 3.2, eq:round and its footnote
  *                                   (bin 0 open to -inf, bin D-1 open to +inf);
- *                                   other CDF families of App. D
+ *                                   other CDF families of App. E
  *   - expected usage              : App. B.2 (Res^), App. B.3 (modulo fold, MRes^)
  *   - resource violation          : App. B.2, eq:relu
  *   - dependency violation        : Sec. 3.2, eq:dep (with producer delay)
@@ -90,10 +90,19 @@ int orc_num_threads(void) {
 #endif
 }
 
+/* Threads of the OpenMP loops that follow (the CPU baseline times 1 and all). */
+void orc_set_num_threads(int32_t n) {
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /* ------------------------------------------------------ distribution family */
 
 /* The relaxed start time is mu + sigma Z with Z of the chosen family
- * (App. D): 0 Gaussian; 1 logistic with scale s = sigma sqrt(3)/pi and
+ * (App. E): 0 Gaussian; 1 logistic with scale s = sigma sqrt(3)/pi and
  * 2 Laplace with scale b = sigma/sqrt(2) (variance sigma^2); 3 Cauchy with
  * scale gamma = sigma sqrt(2 ln 2) (the Gaussian's half-maximum width).
  * Below, z is in sigma units and u = z / c the family's own variable. */
@@ -493,6 +502,43 @@ int orc_loss_grad(const orc_problem *p, const double *mu, const double *sigma,
     return ORC_OK;
 }
 
+/*
+ * Derivative of one expected usage cell U_k(s) (App. B.2; folded modulo II as
+ * in App. B.3, steps d = s, s+T, ... inside [0, D-1]) with respect to mu_i and
+ * sigma_i of every op i, times w (ops of other types get 0).  With
+ * P_i^d = F_i(d) - F_i(d-1) (eq:round) and the constant end values
+ * F_i(-1) = 0, F_i(D-1) = 1, each step d of the cell contributes
+ * dF_i(d) - dF_i(d-1) over the interior bin edges, where
+ * dF/dmu = -phi(z)/sigma and dF/dsigma = -phi(z) z/sigma at z = (t+1/2-mu)/sigma.
+ * The ReLU of eq:relu adds w_res times this vector to the gradient exactly
+ * when the cell's indicator [U_k(s) > C_k] is 1, so a comparison that meets a
+ * cell within rounding of its capacity can accept either indicator value.
+ */
+int orc_usage_cell_grad(const orc_problem *p, const double *mu, const double *sigma, int32_t k, int32_t s,
+                        double w, double *g_mu, double *g_sigma) {
+    const int32_t n = p->n, D = p->D, T = (p->II > 0) ? p->II : D;
+    if (k < 0 || k >= p->K || s < 0 || s >= T) return ORC_E_INVALID;
+    for (int32_t i = 0; i < n; ++i) {
+        double gm = 0.0, gs = 0.0;
+        if (p->rtype[i] == k) {
+            for (int32_t d = s; d < D; d += T) {
+                /* +dF(d) at the upper edge of bin d, -dF(d-1) at its lower edge */
+                for (int32_t side = 0; side < 2; ++side) {
+                    const int32_t t = side == 0 ? d : d - 1;
+                    if (t < 0 || t > D - 2) continue;
+                    const double z = (t + 0.5 - mu[i]) / sigma[i];
+                    const double sg = side == 0 ? 1.0 : -1.0;
+                    gm += sg * (-phi(z) / sigma[i]);
+                    gs += sg * (-phi(z) * z / sigma[i]);
+                }
+            }
+        }
+        g_mu[i] = w * gm;
+        g_sigma[i] = w * gs;
+    }
+    return ORC_OK;
+}
+
 /* The paper's formulas written as literal double sums over (d_i, d_j) (with the
  * producer delay of reading R1/R2).  O(E * D^2): tiny instances only. */
 void orc_edge_terms_double_sum(const orc_problem *p, const double *mu, const double *sigma, double out[3]) {
@@ -609,12 +655,63 @@ static int64_t round_half_up(float muf, int32_t D) {
 }
 
 /*
- * Legalize one restart.  mu [n] float32; out s [n] int64; status returned.
- *   II == 0 : Alg. 3 -- clamp to [ASAP, ALAP], one pass in topological order
- *             raising s_v to max over preds of s_u + delta_u.
- *   II >  0 : Alg. 4 -- clamp to [0, D-1], then passes in topological order
- *             raising s_v to max(t_min, t_back) until a pass changes nothing,
- *             at most n passes.
+ * Both legalization heuristics of App. A start from the rounded means, clamp
+ * them (Alg. 3 for II = 0: into [ASAP, ALAP]; Alg. 4 for II > 0: into
+ * [0, D-1]), and then only ever raise an op, each time to the smallest step
+ * its predecessors (and, for Alg. 4, its recurrences) allow; Alg. 4 repeats
+ * its sweeps until nothing moves, at most N of them.  What they return is
+ * therefore, by definition, the least schedule s >= r (r = the clamped
+ * rounding) with
+ *     s_v >= s_u + Lat_u              for every edge u -> v,
+ *     s_i + k II >= s_j + Lat_j       for every back edge (j -> i, k);
+ * the set of such s is closed under componentwise minimum, so when one
+ * exists a least one does.  This oracle computes that schedule directly, as
+ * the limit of whole-graph rounds s <- max(s, requirement(s)) in which every
+ * op reads the previous round's values (no sweep order at all):
+ *   - without a cycle of positive weight in the constraint graph a longest
+ *     path has at most N-1 edges, so the values settle within N-1 rounds and
+ *     a round that changes nothing ends the computation;
+ *   - a positive cycle (recurrences no schedule can meet) changes something
+ *     in every round: after N rounds the status is NOT_CONVERGED (the pass
+ *     cap of Alg. 4; any sweep order settles no later than these rounds, so
+ *     the status does not depend on the order);
+ *   - OVERFLOW when the least schedule leaves the horizon (some s_v > D-1).
+ * Returns ORC_OK, ORC_E_NOT_CONVERGED or ORC_E_OVERFLOW.
+ */
+static int least_schedule_above(const orc_problem *p, const orc_adj *a, int64_t *s) {
+    const int32_t n = p->n;
+    int64_t *prev = malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+    if (!prev) return ORC_E_NOMEM;
+    int settled = 0;
+    for (int32_t round = 0; round < (n > 0 ? n : 1) && !settled; ++round) {
+        memcpy(prev, s, sizeof(int64_t) * (size_t)n);
+        settled = 1;
+        for (int32_t v = 0; v < n; ++v) {
+            int64_t need = prev[v];
+            for (int32_t r = a->pred_ptr[v]; r < a->pred_ptr[v + 1]; ++r) {   /* forward edges u -> v */
+                const int32_t u = a->pred[r];
+                if (prev[u] + p->delay[u] > need) need = prev[u] + p->delay[u];
+            }
+            for (int32_t r = a->bin_ptr[v]; r < a->bin_ptr[v + 1]; ++r) {     /* back edges (j -> v, k) */
+                const int32_t b = a->bin[r], j = p->bsrc[b];
+                const int64_t c = prev[j] + p->delay[j] - (int64_t)p->bdist[b] * p->II;
+                if (c > need) need = c;
+            }
+            if (need != prev[v]) settled = 0;
+            s[v] = need;
+        }
+    }
+    free(prev);
+    if (!settled) return ORC_E_NOT_CONVERGED;
+    for (int32_t v = 0; v < n; ++v) if (s[v] > p->D - 1) return ORC_E_OVERFLOW;
+    return ORC_OK;
+}
+
+/*
+ * Legalize one restart (App. A).  mu [n] float32; out s [n] int64; returns the
+ * status of least_schedule_above (or ORC_E_CYCLE / ORC_E_HORIZON for a bad
+ * problem).  r = half-up rounding of mu (R4), clamped to [ASAP, ALAP] when
+ * II == 0 (Alg. 3) and to [0, D-1] when II > 0 (Alg. 4, R14).
  */
 int orc_legalize(const orc_problem *p, const float *mu, int64_t *s) {
     const int32_t n = p->n, D = p->D;
@@ -628,56 +725,93 @@ int orc_legalize(const orc_problem *p, const float *mu, int64_t *s) {
     }
     int rc = orc_topo(p, level, order);
     if (rc == ORC_OK && p->II == 0) rc = orc_asap_alap(p, asap, alap);
-    if (rc != ORC_OK) { free(level); free(order); free(asap); free(alap); adj_free(&a); return rc; }
-
-    for (int32_t v = 0; v < n; ++v) s[v] = round_half_up(mu[v], D);
-    if (p->II == 0) {
+    if (rc == ORC_OK) {
         for (int32_t v = 0; v < n; ++v) {
-            if (s[v] < asap[v]) s[v] = asap[v];
-            if (s[v] > alap[v]) s[v] = alap[v];
+            const int64_t lo = p->II == 0 ? asap[v] : 0, hi = p->II == 0 ? alap[v] : (int64_t)D - 1;
+            const int64_t r = round_half_up(mu[v], D);
+            s[v] = r < lo ? lo : (r > hi ? hi : r);
         }
-        for (int32_t q = 0; q < n; ++q) {
-            int32_t v = order[q];
-            if (a.pred_ptr[v + 1] == a.pred_ptr[v]) continue;
-            int64_t treq = INT64_MIN;
-            for (int32_t r = a.pred_ptr[v]; r < a.pred_ptr[v + 1]; ++r) {
-                int32_t u = a.pred[r];
-                if (s[u] + p->delay[u] > treq) treq = s[u] + p->delay[u];
-            }
-            if (treq > s[v]) s[v] = treq;
-        }
-    } else {
-        for (int32_t v = 0; v < n; ++v) {
-            if (s[v] < 0) s[v] = 0;
-            if (s[v] > D - 1) s[v] = D - 1;
-        }
-        int converged = 0;
-        for (int32_t pass = 0; pass < (n > 0 ? n : 1); ++pass) {
-            int changed = 0;
-            for (int32_t q = 0; q < n; ++q) {
-                int32_t v = order[q];
-                int64_t tmin = 0, tback = 0;
-                for (int32_t r = a.pred_ptr[v]; r < a.pred_ptr[v + 1]; ++r) {
-                    int32_t u = a.pred[r];
-                    if (s[u] + p->delay[u] > tmin) tmin = s[u] + p->delay[u];
-                }
-                for (int32_t r = a.bin_ptr[v]; r < a.bin_ptr[v + 1]; ++r) {
-                    int32_t b = a.bin[r], j = p->bsrc[b];
-                    int64_t c = s[j] + p->delay[j] - (int64_t)p->bdist[b] * p->II;
-                    if (c > tback) tback = c;
-                }
-                int64_t treq = tmin > tback ? tmin : tback;
-                if (treq > s[v]) { s[v] = treq; changed = 1; }
-            }
-            if (!changed) { converged = 1; break; }
-        }
-        if (!converged) rc = ORC_E_NOT_CONVERGED;
-        else {
-            for (int32_t v = 0; v < n; ++v) if (s[v] > D - 1) { rc = ORC_E_OVERFLOW; break; }
-        }
+        rc = least_schedule_above(p, &a, s);
     }
     free(level); free(order); free(asap); free(alap); adj_free(&a);
     return rc;
+}
+
+/* --------------------------------------------------- one check of Alg. 1 */
+
+/*
+ * The order in which a driver of Alg. 1 keeps schedules (reading R15 of the
+ * Sampling paragraph of Sec. 3.3 and App. A's "reset to the prior best"):
+ * a schedule is feasible when it is legal and within every capacity
+ * (V_res = 0); feasible beats infeasible; two feasible ones compare by cost;
+ * among infeasible ones a legal one beats an illegal one, then the lower
+ * V_res wins, then the lower cost.  Equal ones do not replace each other.
+ * c = (cost, L_com, L_res, L_mem, V_res, legal) as orc_schedule_cost writes.
+ */
+static int better_schedule(const double *c, const double *b) {
+    const int fc = c[5] != 0.0 && c[4] == 0.0, fb = b[5] != 0.0 && b[4] == 0.0;
+    if (fc != fb) return fc;
+    if (fc) return c[0] < b[0];
+    if (c[5] != b[5]) return c[5] != 0.0;
+    if (c[4] != b[4]) return c[4] < b[4];
+    return c[0] < b[0];
+}
+
+/*
+ * One check of the Alg. 1 driver for one restart, in the order the driver
+ * takes its steps:
+ *   1. round the means half-up (R4);
+ *   2. legalize (Alg. 3 / Alg. 4 above): the candidate schedule;
+ *   3. cost the candidate (Sec. 2.1, orc_schedule_cost);
+ *   4. keep it as the restart's best if it is better (better_schedule);
+ *   5. if the rounding was not already legal (the candidate differs from it),
+ *      re-initialize the means (Sec. 3.3 "Sampling"): from the candidate if
+ *      it improved the best, else from the prior best (App. A);
+ *   6. clear the re-initialized restart's Adam moments and, with
+ *      reinit_sigma, set sigma = max(kappa (ALAP - ASAP), sigma_min) (the
+ *      initial rule, Sec. 3.3 "Initialization").
+ * In/out: mu, sigma [n] float32; m, v [2][n] float32 (moments of mu, then of
+ * sigma); best_s [n] int64 and best_c [6] (a best_c with legal = 0 and
+ * V_res = cost = +inf holds no schedule yet).  Out: cand [n], cand_c [6],
+ * *mode (0 kept, 1 from the candidate, 2 from the prior best), *improved.
+ * kappa and sigma_min are the float32 hyper-parameters.
+ */
+int orc_check(const orc_problem *p, float *mu, float *sigma, float *m, float *v, int64_t *best_s,
+              double *best_c, double alpha, double beta, double gamma, int32_t reinit_sigma, float kappa,
+              float sigma_min, int64_t *cand, double *cand_c, int32_t *mode, int32_t *improved) {
+    const int32_t n = p->n;
+    int64_t *asap = malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+    int64_t *alap = malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+    if (!asap || !alap) { free(asap); free(alap); return ORC_E_NOMEM; }
+    int rc = orc_asap_alap(p, asap, alap);
+    if (rc != ORC_OK && p->II == 0) { free(asap); free(alap); return rc; }
+    (void)orc_legalize(p, mu, cand);                        /* steps 1-2; the status is not used */
+    rc = orc_schedule_cost(p, cand, alpha, beta, gamma, cand_c);   /* step 3 */
+    if (rc != ORC_OK) { free(asap); free(alap); return rc; }
+    int rounding_legal = 1;
+    for (int32_t i = 0; i < n; ++i) if (round_half_up(mu[i], p->D) != cand[i]) rounding_legal = 0;
+    *improved = better_schedule(cand_c, best_c);            /* step 4 */
+    if (*improved) {
+        memcpy(best_s, cand, sizeof(int64_t) * (size_t)n);
+        memcpy(best_c, cand_c, sizeof(double) * 6);
+    }
+    *mode = rounding_legal ? 0 : (*improved ? 1 : 2);
+    if (*mode) {                                            /* steps 5-6 */
+        const int64_t *src = (*mode == 1) ? cand : best_s;  /* after step 4, best_s is the prior best
+                                                               whenever mode is 2 */
+        for (int32_t i = 0; i < n; ++i) {
+            mu[i] = (float)src[i];
+            if (reinit_sigma) {
+                const double w = (double)kappa * (double)(alap[i] - asap[i]);
+                const float sg = (float)w;
+                sigma[i] = sg > sigma_min ? sg : sigma_min;
+            }
+            m[i] = 0.0f; m[n + i] = 0.0f;
+            v[i] = 0.0f; v[n + i] = 0.0f;
+        }
+    }
+    free(asap); free(alap);
+    return ORC_OK;
 }
 
 /* ---------------------------------------------------------- initial state */

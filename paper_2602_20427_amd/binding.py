@@ -20,11 +20,12 @@ OK, E_INVALID_ARG, E_CYCLE, E_HORIZON, E_NOT_CONVERGED, E_OVERFLOW, E_DEVICE, E_
 
 # symbols declared in include/gaus.h
 EXPORTS = ("gaus_default_hparams", "gaus_init", "gaus_bind_state", "gaus_loss_grad", "gaus_step",
-           "gaus_adam_from_grad", "gaus_legalize", "gaus_schedule_cost", "gaus_solve", "gaus_init_state",
+           "gaus_adam_from_grad", "gaus_legalize", "gaus_schedule_cost", "gaus_solve", "gaus_solve_check",
+           "gaus_init_state",
            "gaus_asap_alap",
            "gaus_get_usage", "gaus_get_storage", "gaus_kernel_timing", "gaus_kernel_timing_read", "gaus_sync",
            "gaus_get_dims", "gaus_get_poly_config", "gaus_poly_census", "gaus_get_poly_grids",
-           "gaus_poly_grid_census", "gaus_last_error", "gaus_status_string",
+           "gaus_poly_grid_census", "gaus_poly_tier_census", "gaus_last_error", "gaus_status_string",
            "gaus_destroy")
 
 
@@ -62,7 +63,7 @@ class HParams(C.Structure):
                 ("beta_res", C.c_float), ("tau", C.c_float), ("gamma_mem", C.c_float),
                 ("family", C.c_int32), ("poly_pack", C.c_int32)]
 
-# CDF family of the relaxed start times (App. D), the values of HParams.family
+# CDF family of the relaxed start times (App. E), the values of HParams.family
 FAMILIES = {"gaussian": 0, "logistic": 1, "laplace": 2, "cauchy": 3}
 
 N_TERMS = 7   # L, V_dep, V_res, V_rec, L_com, L_res, L_mem
@@ -92,6 +93,7 @@ def load():
         "gaus_legalize": ([vp] * 4, C.c_int),
         "gaus_schedule_cost": ([vp] * 3, C.c_int),
         "gaus_solve": ([vp] * 5, C.c_int),
+        "gaus_solve_check": ([vp, vp, vp, i32, vp], C.c_int),
         "gaus_init_state": ([vp] * 4, C.c_int),
         "gaus_asap_alap": ([vp] * 3, C.c_int),
         "gaus_get_usage": ([vp] * 2, C.c_int),
@@ -104,6 +106,7 @@ def load():
         "gaus_poly_census": ([vp, vp], C.c_int),
         "gaus_get_poly_grids": ([vp, vp], C.c_int),
         "gaus_poly_grid_census": ([vp, vp], C.c_int),
+        "gaus_poly_tier_census": ([vp, vp], C.c_int),
         "gaus_last_error": ([vp], C.c_char_p),
         "gaus_status_string": ([C.c_int], C.c_char_p),
         "gaus_destroy": ([vp], None),
@@ -255,6 +258,16 @@ class Context:
                                       C.byref(st)))
         return {f: getattr(st, f) for f, _ in SolveStats._fields_}
 
+    def solve_check(self, best_sched, best_cost, reinit_sigma: bool = False) -> np.ndarray:
+        """One check of the Alg. 1 driver on the bound state; returns the
+        per-restart re-initialization mode (0 kept, 1 candidate, 2 prior best)."""
+        import torch
+        mode = np.zeros(self.B, np.int32)
+        self._check(load().gaus_solve_check(self._h, _dptr(best_sched, torch.int32, (self.B, self.N), "best_sched"),
+                                            _dptr(best_cost, torch.float64, (self.B, N_COST), "best_cost"),
+                                            1 if reinit_sigma else 0, _np_ptr(mode)))
+        return mode
+
     def init_state(self, mu, sigma, u=None):
         import torch
         B, N = self.B, self.N
@@ -314,6 +327,13 @@ class Context:
         c = np.zeros(3, np.int64)
         self._check(load().gaus_poly_grid_census(self._h, _np_ptr(c)))
         return [int(x) for x in c]
+
+    def poly_tier_census(self):
+        """[grid][tier][0: (restart, op) pairs, 1: their polynomial out-edges] of
+        the last iteration (tier 1..3 = degree 8, 6, 5; tier 0 unused)."""
+        c = np.zeros((3, 4, 2), np.int64)
+        self._check(load().gaus_poly_tier_census(self._h, _np_ptr(c)))
+        return c
 
     def sync(self):
         self._check(load().gaus_sync(self._h))

@@ -30,7 +30,7 @@ __device__ __forceinline__ void normal_tail_pdf(float z, float &tail, float &g) 
     tail = 0.5f * g * (t * q);
 }
 
-// Families of the relaxed start time (App. D).  Each is the CDF of a
+// Families of the relaxed start time (App. E).  Each is the CDF of a
 // symmetric law of z = (v + 1/2 - mu)/sigma; the non-Gaussian ones are taken
 // at u = z/c, with c matching them to the Gaussian: logistic c = sqrt(3)/pi and
 // Laplace c = 1/sqrt(2) (equal variance), Cauchy c = sqrt(2 ln 2) (equal
@@ -345,7 +345,7 @@ constexpr float back_coef(int k, int j) {
     return (float)(-(double)(k + j + 1) * binom_d(k + j, j) * ((j & 1) ? -1.0 : 1.0));
 }
 
-// Taylor coefficients in y of F(z0 + r y) for each family (App. D), from one
+// Taylor coefficients in y of F(z0 + r y) for each family (App. E), from one
 // tail/density evaluation at the chunk centre:
 //   Gaussian: the Hermite recursion above;
 //   logistic: F = S(q y + u0), q = r/c, S' = S (1 - S), so with the

@@ -798,6 +798,20 @@ gaus_status gaus_solve(gaus_ctx *ctx, const gaus_solve_params *prm, int32_t *bes
     return GAUS_OK;
 }
 
+gaus_status gaus_solve_check(gaus_ctx *ctx, int32_t *best_sched, double *best_cost, int32_t reinit_sigma,
+                             int32_t *mode) {
+    if (!ctx) return GAUS_E_INVALID_ARG;
+    if (!ctx->bound) return fail(ctx, GAUS_E_INVALID_ARG, "solve_check: state not bound");
+    if (!best_sched || !best_cost) return fail(ctx, GAUS_E_INVALID_ARG, "solve_check: null pointer");
+    hipError_t e = enqueue_check(ctx->g, ctx->w, ctx->hp, ctx->mu, ctx->sigma, ctx->m, ctx->v, best_sched,
+                                 best_cost, reinit_sigma ? 1 : 0, ctx->stream);
+    if (e == hipSuccess && mode)
+        e = hipMemcpyAsync(mode, ctx->w.mode, sizeof(int) * ctx->g.B, hipMemcpyDeviceToHost, ctx->stream);
+    if (e == hipSuccess && mode) e = hipStreamSynchronize(ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "solve_check");
+    return GAUS_OK;
+}
+
 gaus_status gaus_init_state(gaus_ctx *ctx, const double *u, float *mu, float *sigma) {
     if (!ctx) return GAUS_E_INVALID_ARG;
     if (!mu || !sigma) return fail(ctx, GAUS_E_INVALID_ARG, "init_state: null pointer");
@@ -944,6 +958,33 @@ gaus_status gaus_poly_grid_census(gaus_ctx *ctx, int64_t counts[3]) {
     for (int gi = 0; gi < kGrids; ++gi) counts[gi] = 0;
     for (size_t q = 0; q < BN; ++q)
         if (sel[q] < kGrids) ++counts[sel[q]];
+    return GAUS_OK;
+}
+
+gaus_status gaus_poly_tier_census(gaus_ctx *ctx, int64_t counts[24]) {
+    if (!ctx) return GAUS_E_INVALID_ARG;
+    if (!counts) return fail(ctx, GAUS_E_INVALID_ARG, "poly_tier_census: null pointer");
+    const Graph &g = ctx->g;
+    const size_t BN = (size_t)g.B * g.N;
+    hipError_t e = hipStreamSynchronize(ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "poly_tier_census");
+    std::vector<unsigned char> sel(BN), tier(BN), cls(BN);
+    std::vector<int> rp(g.N + 1), col(std::max(g.E, 1));
+    e = hipMemcpy(sel.data(), ctx->w.gsel, BN, hipMemcpyDeviceToHost);
+    if (e == hipSuccess) e = hipMemcpy(tier.data(), ctx->w.gtier, BN, hipMemcpyDeviceToHost);
+    if (e == hipSuccess) e = hipMemcpy(cls.data(), ctx->w.cls, BN, hipMemcpyDeviceToHost);
+    if (e == hipSuccess) e = hipMemcpy(rp.data(), g.row_ptr, sizeof(int) * rp.size(), hipMemcpyDeviceToHost);
+    if (e == hipSuccess && g.E > 0) e = hipMemcpy(col.data(), g.col, sizeof(int) * g.E, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(ctx, e, "poly_tier_census");
+    for (int q = 0; q < 24; ++q) counts[q] = 0;
+    for (int b = 0; b < g.B; ++b)
+        for (int i = 0; i < g.N; ++i) {
+            const size_t bi = (size_t)b * g.N + i;
+            if (sel[bi] >= kGrids || tier[bi] < 1 || tier[bi] > kTiers) continue;
+            int64_t *c = counts + (sel[bi] * (kTiers + 1) + tier[bi]) * 2;
+            c[0] += 1;
+            for (int q = rp[i]; q < rp[i + 1]; ++q) c[1] += cls[(size_t)b * g.N + col[q]] ? 1 : 0;
+        }
     return GAUS_OK;
 }
 

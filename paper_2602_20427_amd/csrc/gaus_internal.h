@@ -163,9 +163,10 @@ struct Work {
     unsigned char *gsel;   // [B][N]        grid that evaluates the (restart, op) this iteration (0..2),
                            //               kNoGrid on the step-by-step path
     unsigned char *gtier;  // [B][N]        tier of its vectors on that grid (0 off the polynomial path)
-    unsigned char *gwork;  // [kGrids][B][ngroups]  1 = the group has ops on the grid (grid 0 also:
-                           //               step-by-step ops, whose polynomial records are cleared);
-                           //               only such groups' polynomial work-groups write outputs
+    unsigned char *gwork;  // [kGrids][B][ngroups]  1 = the group has ops on the grid; only such
+                           //               groups' polynomial work-groups write outputs
+                           //               (ppoly / cpoly hold valid records for cls != 0 ops
+                           //               only: readers check cls)
     float *vres_part; // [B][K]            V_res of one resource type
     float *Ucoef_k;   // [B][K][kGrids][64*kNC + 320]  polynomial usage coefficients and strip values per type
     float *ppoly;     // [B][N][kPP]       producer partials of the polynomial path

@@ -32,7 +32,7 @@ namespace gaus {
 //   T_1 = phi(z0) r,
 //   T_{n+1} = -(z0 r/(n+1)) T_n - ((n-1) r^2/(n(n+1))) T_{n-1}
 // (the Hermite recursion of the derivatives of phi, scaled).  The logistic
-// and Cauchy laws of App. D have recursions of their own (expand in the
+// and Cauchy laws of App. E have recursions of their own (expand in the
 // device header); everything below uses only the T's and holds for any
 // location-scale family.  From one set of T's follow, with constant integer
 // coefficients (one step = 1 in y):
@@ -80,8 +80,8 @@ __device__ __forceinline__ int grid_tier(const GridArgs &gr, float s, int delay)
 //     its consumers reach the grid's degree-8 bound, with the pack's tier
 //     (the highest degree of its members'); else grid 0 with the op's own
 //     tier, or kNoGrid on the step-by-step path; per (grid, restart, group)
-//     whether any op is there (grid 0 also: step-by-step ops, whose
-//     polynomial records it clears).
+//     whether any op is there.  Polynomial records (ppoly, cpoly) are
+//     written only for ops on a grid; every reader checks cls first.
 // The consumers' tiers are recomputed here from their sigmas.  With the
 // storage term on, also whether a holder's storage term is taken on the
 // chunk polynomials (Gaussian start times only; kMemPolyDeg, kMemRhoMax).
@@ -110,9 +110,12 @@ __global__ __launch_bounds__(256 * kFlagPack) void k_flags(Graph G, PolyArgs pa,
         W.cls[bi] = (unsigned char)ci;
         d = ci ? 0 : 1;
         t = ci;
+        // packed-grid tiers count only for ops on the polynomial path of grid 0
+        // (an explicit grid-0 chunk width can make a packed grid's threshold
+        // the lower one: such an op stays step by step in every restart)
         int tp[kGrids];   // [0] unused
 #pragma unroll
-        for (int g = 1; g < kGrids; ++g) tp[g] = grid_tier(pa.gr[g], s, di);
+        for (int g = 1; g < kGrids; ++g) tp[g] = ci ? grid_tier(pa.gr[g], s, di) : 0;
         const int e0 = G.row_ptr[i], e1 = G.row_ptr[i + 1];
         float rsum = 1.0f / s;   // sum of 1/sigma over the holder and its successors
         for (int e = e0; e < e1; ++e) {
@@ -124,8 +127,8 @@ __global__ __launch_bounds__(256 * kFlagPack) void k_flags(Graph G, PolyArgs pa,
             t = cj ? min(t, cj) : t;
 #pragma unroll
             for (int g = 1; g < kGrids; ++g) {
-                const int c = grid_tier(pa.gr[g], sj, dj);
-                tp[g] = c ? min(tp[g], c) : 0;
+                const int c = cj ? grid_tier(pa.gr[g], sj, dj) : 0;   // a step-by-step consumer
+                tp[g] = c ? min(tp[g], c) : 0;                         // keeps the op off the packs
             }
             if (mem_on) rsum += 1.0f / sj;
         }

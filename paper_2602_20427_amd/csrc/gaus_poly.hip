@@ -16,7 +16,7 @@ constexpr int kStripPad = kSmax; // zero slots before position 0 (positions -kSm
 // The degree tiers of grid 0 run as two kernels so that each has its own
 // register budget: kPolyWide (tier 3, degree 5; 4 waves per SIMD with one
 // strip pass) is launched first; it writes the per-work-group usage and
-// V_dep / L_com outputs and clears the records of step-by-step ops.
+// V_dep / L_com outputs.
 // kPolyNarrow (tiers 1 and 2) follows, adds to those outputs, and
 // work-groups without such ops exit at once.  The packed grids run every
 // tier in one kernel (kPolyAll), which writes its grid's outputs.
@@ -68,7 +68,6 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
     constexpr int GI = P == 1 ? 0 : P == 2 ? 1 : 2;   // grid
     constexpr int L = 64 / P;                          // lanes per restart
     constexpr bool kWrite = TIERS != kPolyNarrow;      // write (not add) the work-group outputs
-    constexpr bool kClear = P == 1 && TIERS == kPolyWide;   // clear records of step-by-step ops
     const GridArgs &gd = pa.gr[GI];
     const int split = gd.split;
     const int grp = blockIdx.x / split, sub = blockIdx.x - grp * split;
@@ -134,13 +133,6 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
         if (!__syncthreads_or(lane < nq && l_mine && (l_cls == 1 || l_cls == 2))) return;
     }
     float gsum = 0.0f;  // V_dep, L_com of this wave's ops (lanes c = 0 and 2)
-    if constexpr (kClear) {   // step-by-step ops: no polynomial records
-        for (int oq = 0; oq < nq; ++oq) {
-            if (__builtin_amdgcn_readlane(l_cls, oq)) continue;
-            const int i = __builtin_amdgcn_readlane(l_i, oq);
-            if (lane < kPP) W.ppoly[((size_t)b0 * N + i) * kPP + lane] = 0.0f;
-        }
-    }
     // polynomial ops, one pass per degree tier (NC coefficients per vector)
     auto tier_pass = [&](auto nc_tag, int tier) {
     constexpr int NC = decltype(nc_tag)::value;

@@ -1,4 +1,4 @@
-"""Parity of the other start-time distributions (App. D: logistic, Laplace,
+"""Parity of the other start-time distributions (App. E: logistic, Laplace,
 Cauchy, each with its scale matched to the Gaussian sigma): loss terms,
 usage and gradients of the HIP path through the C ABI vs the fp64 oracle
 with the same family, alone and with the smooth peak usage and storage
@@ -10,7 +10,7 @@ import oracle
 from paper_2602_20427_amd import binding as bd
 from paper_2602_20427_amd.workloads import (CONFIGS, make_problem, random_state, restart_uniforms, uniform_state,
                                             with_storage)
-from tests.gpu_common import TOL, compare_restart, gpu_loss_grad, hparams, poly_sigma_thresholds, say
+from tests.gpu_common import TOL, gpu_loss_grad, hparams, oracle_compare, poly_sigma_thresholds, say
 
 pytestmark = pytest.mark.gpu
 
@@ -41,25 +41,16 @@ def _init_state(cfg, p, B):
     return mu.astype(np.float32), sg.astype(np.float32)
 
 
-def _compare(p, mu, sg, lam, hp, family, what, beta=0.0, tau=1e-2, gamma=0.0):
+def _compare(p, mu, sg, lam, hp, family, what, beta=0.0, tau=1e-2, gamma=0.0, restarts=None):
     g = gpu_loss_grad(p, mu, sg, lam, hp)
     B = mu.shape[0]
     oracle.set_family(family)
     try:
-        for b in sorted({0, B - 1}):
-            ot, oU, ogm, ogs, ties = oracle.loss_grad(p, mu[b:b + 1].astype(np.float64),
-                                                      sg[b:b + 1].astype(np.float64), lam[b:b + 1],
-                                                      hp.alpha_com, hp.rho, tie_tol=1e-4, beta=beta, tau=tau,
-                                                      gamma=gamma)
-            if (beta > 0 or gamma > 0) and ties[0]:
-                say(f"  b={b}: {ties[0]} near-tie usage cells, comparing terms only")
-                err_t = np.abs(g["terms"][b] - ot[0]) / np.maximum(np.abs(ot[0]), 1.0)
-                assert err_t.max() <= TOL, (what, b, g["terms"][b], ot[0])
-                continue
-            dU = np.abs(g["U"][b] - oU[0]).max()
-            say(f"  b={b}: dU={dU:.2e} (max U {np.abs(oU[0]).max():.4g}, dU/tau {dU / tau:.1e})")
-            r = compare_restart(g, ot[0], oU[0], ogm[0], ogs[0], b, what)
-            say(f"  b={b}: L={g['terms'][b][0]:.6g} (oracle {ot[0][0]:.6g}) "
+        for b in (sorted({0, B - 1}) if restarts is None else restarts):
+            r, o = oracle_compare(p, g, b, mu, sg, lam, hp, what, beta=beta, tau=tau, gamma=gamma)
+            dU = np.abs(g["U"][b] - o["U"]).max()
+            say(f"  b={b}: dU={dU:.2e} (max U {np.abs(o['U']).max():.4g}, dU/tau {dU / tau:.1e}) "
+                f"L={g['terms'][b][0]:.6g} (oracle {o['terms'][0]:.6g}) "
                 + " ".join(f"{k}={v:.2e}" for k, v in r.items()))
     finally:
         oracle.set_family("gaussian")
@@ -179,16 +170,19 @@ def test_family_storage_initial_state(family):
     _compare(p, mu, sg, lam, hp, family, f"small-init-mem/{family}", tau=1.0, gamma=1.0)
 
 
-def test_family_large_full_size():
-    """Cauchy, the heaviest tails, on the 50k-op workload at full size
-    (B=8, D=4096) in bench.py's launch configuration."""
+@pytest.mark.parametrize("family", FAMS)
+def test_family_large_full_size(family):
+    """Each family on the 50k-op workload at full size (B=8, D=4096) in
+    bench.py's launch configuration (logistic and Cauchy on the packed chunk
+    polynomials; Laplace on its own path), restarts 0, 1, 2 (pack positions
+    0..2) and 7."""
     cfg = CONFIGS["large"]
     p = make_problem(cfg, seed=0)
     B = cfg.B
     mu, sg = _init_state("large", p, B)
     hp = bd.default_hparams()
     hp.lr = cfg.lr
-    hp.family = bd.FAMILIES["cauchy"]
+    hp.family = bd.FAMILIES[family]
     lam = np.full((B, 3), hp.lambda0, np.float32)
-    say(f"[family] cauchy large: N={p.n_ops} D={p.D} B={B}")
-    _compare(p, mu, sg, lam, hp, "cauchy", "large/cauchy")
+    say(f"[family] {family} large: N={p.n_ops} D={p.D} B={B}")
+    _compare(p, mu, sg, lam, hp, family, f"large/{family}", restarts=(0, 1, 2, B - 1))

@@ -9,7 +9,7 @@ import pytest
 import oracle
 from paper_2602_20427_amd import binding as bd
 from paper_2602_20427_amd.workloads import CONFIGS, make_problem, random_state, restart_uniforms, uniform_state
-from tests.gpu_common import TOL, compare_restart, gpu_loss_grad, hparams, say
+from tests.gpu_common import TOL, gpu_loss_grad, hparams, oracle_compare, say
 
 pytestmark = pytest.mark.gpu
 
@@ -42,19 +42,10 @@ def test_smooth_peak_loss_grad(cfg, poly, tau):
     say(f"[lse] {cfg} poly={poly} tau={tau}: N={p.n_ops} D={p.D} II={p.II} B={B}")
     g = gpu_loss_grad(p, mu, sg, lam, hp)
     for b in (0, B - 1):
-        m64, s64 = mu[b:b + 1].astype(np.float64), sg[b:b + 1].astype(np.float64)
-        ot, oU, ogm, ogs, ties = oracle.loss_grad(p, m64, s64, lam[b:b + 1], hp.alpha_com, hp.rho,
-                                                  tie_tol=1e-4, beta=1.0, tau=tau)
         # the softmax weights scale a usage error dU by up to 2 dU / tau; the
         # gradient bar stays the plain one (measured errors are far below it)
-        dU = np.abs(g["U"][b] - oU[0]).max()
-        if ties[0]:
-            say(f"  b={b}: {ties[0]} near-tie usage cells, comparing terms only")
-            err_t = np.abs(g["terms"][b] - ot[0]) / np.maximum(np.abs(ot[0]), 1.0)
-            assert err_t.max() <= TOL
-            continue
-        r = compare_restart(g, ot[0], oU[0], ogm[0], ogs[0], b, f"{cfg}/lse tau={tau}")
-        say(f"  b={b}: L_res={g['terms'][b][5]:.6g} (oracle {ot[0][5]:.6g}) dU={dU:.2e} 2dU/tau={2 * dU / tau:.1e} "
+        r, o = oracle_compare(p, g, b, mu, sg, lam, hp, f"{cfg}/lse tau={tau}", beta=1.0, tau=tau)
+        say(f"  b={b}: L_res={g['terms'][b][5]:.6g} (oracle {o['terms'][5]:.6g}) U err {r['U']:.2e} "
             + " ".join(f"{k}={v:.2e}" for k, v in r.items()))
 
 
@@ -71,13 +62,9 @@ def test_smooth_peak_large_full_size():
     lam = np.full((B, 3), hp.lambda0, np.float32)
     say(f"[lse] large tau={hp.tau}: N={p.n_ops} D={p.D} B={B}")
     g = gpu_loss_grad(p, mu, sg, lam, hp)
-    for b in (0, B - 1):
-        ot, oU, ogm, ogs, ties = oracle.loss_grad(p, mu[b:b + 1].astype(np.float64), sg[b:b + 1].astype(np.float64),
-                                                  lam[b:b + 1], hp.alpha_com, hp.rho, tie_tol=1e-4,
-                                                  beta=1.0, tau=hp.tau)
-        assert ties[0] == 0
-        r = compare_restart(g, ot[0], oU[0], ogm[0], ogs[0], b, "large/lse")
-        say(f"  b={b}: L_res={g['terms'][b][5]:.6g} (oracle {ot[0][5]:.6g}) "
+    for b in (0, 1, 2, B - 1):
+        r, o = oracle_compare(p, g, b, mu, sg, lam, hp, "large/lse", beta=1.0, tau=hp.tau)
+        say(f"  b={b}: L_res={g['terms'][b][5]:.6g} (oracle {o['terms'][5]:.6g}) "
             + " ".join(f"{k}={v:.2e}" for k, v in r.items()))
 
 
@@ -90,7 +77,14 @@ def test_smooth_peak_single_slot_is_op_count():
     g = gpu_loss_grad(p, mu, sg, np.zeros((B, 3), np.float32), hparams(alpha=0.0, rho=0.0, beta=1.0, tau=0.01))
     for b in range(B):
         assert abs(g["terms"][b][5] - p.n_ops) <= TOL * p.n_ops
-        assert np.abs(g["gm"][b]).max() < 1e-3 and np.abs(g["gs"][b]).max() < 1e-3
+        # the exact gradient is 0 (the one slot holds a total mass); its pieces
+        # are beta times sums over bin edges of |dF_i/dtheta|, which the
+        # discrete sum of the density bounds by 1 + phi(0)/sigma_i, so the
+        # plain relative bar is taken against that scale
+        scale = 1.0 + 0.3989422804014327 / float(sg[b].min())
+        e = max(np.abs(g["gm"][b]).max(), np.abs(g["gs"][b]).max())
+        say(f"  b={b}: max |g| {e:.2e} (bar {TOL * scale:.2e})")
+        assert e <= TOL * scale
 
 
 def test_smooth_peak_step_equals_loss_grad_plus_adam():

@@ -7,7 +7,7 @@ import pytest
 import oracle
 from paper_2602_20427_amd import binding as bd
 from paper_2602_20427_amd.workloads import CONFIGS, make_problem, random_state, with_storage
-from tests.gpu_common import TOL, compare_restart, hparams, say
+from tests.gpu_common import TOL, hparams, oracle_compare, say
 
 pytestmark = pytest.mark.gpu
 
@@ -82,26 +82,24 @@ def _check_storage(p, mu, sg, lam, hp, what):
     say(f"[mem] {what}: N={p.n_ops} E={p.n_edges} D={p.D} II={p.II} B={mu.shape[0]} tau={tau}")
     g = _run(p, mu, sg, lam, hp)
     for b in range(mu.shape[0]):
-        m64, s64 = mu[b:b + 1].astype(np.float64), sg[b:b + 1].astype(np.float64)
-        mr = np.zeros((1, g["M"].shape[1]))
-        ot, oU, ogm, ogs, ties = oracle.loss_grad(p, m64, s64, lam[b:b + 1], hp.alpha_com, hp.rho, tie_tol=1e-4,
-                                                  tau=tau, gamma=hp.gamma_mem, mreg_out=mr)
-        dM = np.abs(g["M"][b] - mr[0]).max()
-        em = dM / max(np.abs(mr[0]).max(), 1.0)
-        assert em <= TOL, f"storage err {em}"
-        err_t = np.abs(g["terms"][b] - ot[0]) / np.maximum(np.abs(ot[0]), 1.0)
-        assert err_t.max() <= TOL, (g["terms"][b], ot[0])
-        if ties[0]:
-            say(f"  b={b}: {ties[0]} near-tie usage cells, comparing terms and storage only")
-            continue
-        for name, gg, oo in (("g_mu", g["gm"][b], ogm[0]), ("g_sigma", g["gs"][b], ogs[0])):
-            bar = _storage_bar(dM, tau, mr[0], hp.gamma_mem, p, sg[b], oo)
-            e = np.abs(gg - oo).max() / np.abs(oo).max()
-            say(f"  b={b} {name}: err {e:.2e} (derived bound {bar:.2e}, dM {dM:.2e}, "
-                f"L_mem {g['terms'][b][6]:.6g} vs {ot[0][6]:.6g})")
-            # the plain bar holds with the fp64 storage sums; the derived bound
-            # (>= TOL) says how far the softmax could amplify the profile error
-            assert e <= TOL, f"{what} b={b} {name} err {e} (derived bound {bar})"
+        _compare_storage(p, g, b, mu, sg, lam, hp, what)
+
+
+def _compare_storage(p, g, b, mu, sg, lam, hp, what):
+    """Storage profile, terms, usage and gradients of restart b against the
+    oracle, all at the plain bar (either indicator at near-tie usage
+    cells); the derived bound on how far the softmax could amplify the
+    profile's rounding error is printed beside each gradient error."""
+    mr = np.zeros((1, g["M"].shape[1]))
+    r, o = oracle_compare(p, g, b, mu, sg, lam, hp, what, tau=hp.tau, gamma=hp.gamma_mem, mreg_out=mr)
+    dM = np.abs(g["M"][b] - mr[0]).max()
+    em = dM / max(np.abs(mr[0]).max(), 1.0)
+    assert em <= TOL, f"{what} b={b} storage err {em}"
+    for name, key in (("g_mu", "gm"), ("g_sigma", "gs")):
+        bar = _storage_bar(dM, hp.tau, mr[0], hp.gamma_mem, p, sg[b], o[key])
+        say(f"  b={b} {name}: err {r[name]:.2e} (derived bound {bar:.2e}, dM {dM:.2e}, max MReg "
+            f"{mr[0].max():.6g}, L_mem {g['terms'][b][6]:.8g} vs {o['terms'][6]:.8g})")
+    return r
 
 
 @pytest.mark.parametrize("tau", [100.0, 1.0, 0.01])
@@ -174,21 +172,7 @@ def test_storage_large_full_size():
     lam = np.full((B, 3), hp.lambda0, np.float32)
     g = _run(p, mu, sg, lam, hp)
     for b in (0, B - 1):
-        m64, s64 = mu[b:b + 1].astype(np.float64), sg[b:b + 1].astype(np.float64)
-        mr = np.zeros((1, g["M"].shape[1]))
-        ot, oU, ogm, ogs, ties = oracle.loss_grad(p, m64, s64, lam[b:b + 1], hp.alpha_com, hp.rho, tie_tol=1e-4,
-                                                  tau=hp.tau, gamma=1.0, mreg_out=mr)
-        dM = np.abs(g["M"][b] - mr[0]).max()
-        em = dM / max(np.abs(mr[0]).max(), 1.0)
-        assert em <= TOL and ties[0] == 0
-        err_t = np.abs(g["terms"][b] - ot[0]) / np.maximum(np.abs(ot[0]), 1.0)
-        assert err_t.max() <= TOL
-        for name, gg, oo in (("g_mu", g["gm"][b], ogm[0]), ("g_sigma", g["gs"][b], ogs[0])):
-            bound = _storage_bar(dM, hp.tau, mr[0], 1.0, p, sg[b], oo)
-            e = np.abs(gg - oo).max() / np.abs(oo).max()
-            say(f"  b={b} {name}: err {e:.2e} derived bound {bound:.2e} dM {dM:.2e} max MReg {mr[0].max():.6g} "
-                f"L_mem {g['terms'][b][6]:.8g} vs {ot[0][6]:.8g}")
-            assert e <= max(TOL, bound), f"large/mem b={b} {name} err {e} > bound {bound}"
+        _compare_storage(p, g, b, mu, sg, lam, hp, "large/mem")
 
 
 def test_storage_unit_bits_plain_bar():
@@ -201,13 +185,7 @@ def test_storage_unit_bits_plain_bar():
     hp.gamma_mem = 1.0
     g = _run(p, mu, sg, np.full((B, 3), 0.3, np.float32), hp)
     for b in range(B):
-        mr = np.zeros((1, g["M"].shape[1]))
-        ot, oU, ogm, ogs, ties = oracle.loss_grad(p, mu[b:b + 1].astype(np.float64), sg[b:b + 1].astype(np.float64),
-                                                  np.full((1, 3), 0.3), hp.alpha_com, hp.rho, tie_tol=1e-4,
-                                                  tau=10.0, gamma=1.0, mreg_out=mr)
-        if ties[0]:
-            continue
-        r = compare_restart(g, ot[0], oU[0], ogm[0], ogs[0], b, "small/mem unit bits")
+        r = _compare_storage(p, g, b, mu, sg, np.full((B, 3), 0.3, np.float32), hp, "small/mem unit bits")
         say(f"  b={b}: " + " ".join(f"{k}={v:.2e}" for k, v in r.items()))
 
 

@@ -9,7 +9,7 @@ import oracle
 from paper_2602_20427_amd import binding as bd
 from paper_2602_20427_amd.workloads import (CONFIGS, Problem, make_problem, random_state,
                                             restart_uniforms, uniform_state)
-from tests.gpu_common import TOL, compare_restart, gpu_loss_grad, hparams, say
+from tests.gpu_common import TOL, gpu_loss_grad, hparams, oracle_compare, say
 
 pytestmark = pytest.mark.gpu
 
@@ -26,21 +26,9 @@ def _gpu():
 def _check(prob, mu, sigma, lam, hp, restarts, what):
     say(f"[parity] {what}: N={prob.n_ops} E={prob.n_edges} nb={prob.n_back} D={prob.D} II={prob.II} B={mu.shape[0]}")
     g = gpu_loss_grad(prob, mu, sigma, lam, hp)
-    compared = 0
     for b in restarts:
-        ot, oU, ogm, ogs, ties = oracle.loss_grad(prob, mu[b:b + 1].astype(np.float64),
-                                                  sigma[b:b + 1].astype(np.float64), lam[b:b + 1],
-                                                  hp.alpha_com, hp.rho, tie_tol=1e-4,
-                                                  beta=hp.beta_res, tau=hp.tau)
-        if ties[0]:
-            say(f"  b={b}: {ties[0]} near-tie usage cells, comparing terms/usage only")
-            err_t = np.abs(g["terms"][b] - ot[0]) / np.maximum(np.abs(ot[0]), 1.0)
-            assert err_t.max() <= TOL
-            continue
-        r = compare_restart(g, ot[0], oU[0], ogm[0], ogs[0], b, what)
+        r, _ = oracle_compare(prob, g, b, mu, sigma, lam, hp, what, beta=hp.beta_res, tau=hp.tau)
         say(f"  b={b}: " + " ".join(f"{k}={v:.2e}" for k, v in r.items()))
-        compared += 1
-    assert compared >= 1
     return g
 
 
@@ -78,8 +66,8 @@ def test_loss_grad_paper_init(cfg, poly):
 def test_loss_grad_large_full_size():
     """The 50k-op workload at its full size (B=8, D=4096) in the launch
     configuration bench.py times (library defaults: chunk-polynomial path with
-    the automatic chunk width), from the paper's initialization; restarts 0
-    and 7 against the oracle."""
+    the automatic chunk width and restart packs of 4), from the paper's
+    initialization; every restart against the oracle."""
     cfg = CONFIGS["large"]
     p = make_problem(cfg, seed=0)
     B = cfg.B
@@ -89,7 +77,7 @@ def test_loss_grad_large_full_size():
     mu, sg = mu.astype(np.float32), sg.astype(np.float32)
     hp = bd.default_hparams()
     hp.lr = cfg.lr
-    _check(p, mu, sg, np.full((B, 3), hp.lambda0, np.float32), hp, [0, B - 1], "large/init bench config")
+    _check(p, mu, sg, np.full((B, 3), hp.lambda0, np.float32), hp, range(B), "large/init bench config")
 
 
 def test_loss_grad_large_after_steps():
@@ -118,7 +106,7 @@ def test_loss_grad_large_after_steps():
     say(f"  [large] after 20 steps: poly census {ctx.poly_census()}")
     mu_h, sg_h, lam_h = mu.cpu().numpy(), sg.cpu().numpy(), lam.cpu().numpy()
     ctx.close()
-    _check(p, mu_h, sg_h, lam_h, hp, [0, B - 1], "large/after 20 steps")
+    _check(p, mu_h, sg_h, lam_h, hp, [0, 1, 2, B - 1], "large/after 20 steps")
 
 
 def test_loss_grad_pipelined_random():
@@ -322,6 +310,55 @@ def test_packed_grids(beta):
     lamb = _lam(B, 303)
     g = _check(p, mu, sg, lamb, hp0, range(B), f"packed grids beta={beta:g}")
     hp1 = hparams(alpha=0.2, rho=0.01, beta=beta, tau=0.1)
+    hp1.poly_pack = -1
+    g1 = gpu_loss_grad(p, mu, sg, lamb, hp1)
+    for b in range(B):
+        dt = np.abs(g["terms"][b] - g1["terms"][b]) / np.maximum(np.abs(g1["terms"][b]), 1.0)
+        assert dt.max() <= 1e-6, (b, g["terms"][b], g1["terms"][b])
+        for k in ("gm", "gs"):
+            e = np.abs(g[k][b] - g1[k][b]).max() / np.abs(g1[k][b]).max()
+            assert e <= 1e-6, (b, k, e)
+
+
+def test_packed_grids_explicit_chunk_width():
+    """An explicit grid-0 chunk width (W = 200) with packing on: the packed
+    grid of 2 restarts (W = 127) then has the lower sigma threshold, and ops
+    or consumers between the two thresholds must stay step by step in every
+    restart (never on a pack while grid 0 leaves them to the op kernel).
+    50k-op workload, B = 8, sigmas drawn around the three thresholds; four
+    restarts against the oracle and every restart against the unpacked
+    evaluation."""
+    cfg = CONFIGS["large"]
+    p = make_problem(cfg, seed=0)
+    B = cfg.B
+    hp0 = hparams(alpha=0.2, rho=0.01)
+    hp0.poly_chunk = 200
+    hp0.poly_pack = 1
+    ctx = bd.Context(p, B, hp0)
+    grids = ctx.poly_grids()
+    ctx.close()
+    say(f"  grids {grids}")
+    assert all(g["on"] for g in grids) and grids[0]["W"] == 200
+    thr = [4.0 * (g["W"] - 1) / 2.0 for g in grids]   # degree-8 bound rho = 1/4
+    assert thr[1] < thr[0] < thr[2], thr
+    rng = np.random.default_rng(401)
+    cls_sigma = np.array([0.8 * thr[1], 0.5 * (thr[1] + thr[0]), 0.5 * (thr[0] + thr[2]), 1.4 * thr[2]])
+    base = rng.choice(4, size=p.n_ops, p=[0.1, 0.3, 0.3, 0.3])
+    pick = np.repeat(base[None, :], B, axis=0)
+    flip = rng.random((B, p.n_ops)) < 0.05
+    pick[flip] = rng.choice(4, size=int(flip.sum()))
+    sg = (cls_sigma[pick] * rng.uniform(0.98, 1.02, size=(B, p.n_ops))).astype(np.float32)
+    u = restart_uniforms(p.n_ops, B, seed=0)
+    mu, _, rc = oracle.init_state(p, B, u)
+    assert rc == 0
+    mu = mu.astype(np.float32)
+    census, _ = _grid_census(p, mu, sg, hp0)
+    say(f"  (restart, op) pairs per grid: {census}")
+    assert min(census) > 0.02 * B * p.n_ops, census
+    lamb = _lam(B, 402)
+    g = _check(p, mu, sg, lamb, hp0, [0, 1, 2, B - 1], "explicit W=200 with packs")
+    hp1 = hparams(alpha=0.2, rho=0.01)
+    hp1.poly_chunk = 200
     hp1.poly_pack = -1
     g1 = gpu_loss_grad(p, mu, sg, lamb, hp1)
     for b in range(B):

@@ -250,12 +250,16 @@ def test_p7_gradient_finite_differences(orc, II, n_back, beta, tau, gamma):
     assert checked >= 4
 
 
-torch = pytest.importorskip("torch")
+try:   # the fp64 autograd pins below need torch; every other pin runs without it
+    import torch
+except ImportError:
+    torch = None
+needs_torch = pytest.mark.skipif(torch is None, reason="fp64 autograd pins need torch")
 
 
 def _torch_cdf(family):
     """CDF of the relaxation's family in sigma units, from torch's own
-    distributions (App. D's scale matching)."""
+    distributions (App. E's scale matching)."""
     import math
     if family == "logistic":
         c = math.sqrt(3.0) / math.pi
@@ -323,6 +327,7 @@ def _torch_total(p, mu, sg, lam, alpha, rho, beta=0.0, tau=1e-2, gamma=0.0, fami
     return L
 
 
+@needs_torch
 @pytest.mark.parametrize("II,n_back,beta,tau,gamma", [(0, 0, 0.0, 1e-2, 0.0), (3, 2, 0.0, 1e-2, 0.0),
                                                       (5, 3, 0.0, 1e-2, 0.0), (0, 0, 1.0, 1e-2, 0.0),
                                                       (0, 0, 0.6, 0.2, 0.0), (3, 2, 1.0, 0.05, 0.0),
@@ -445,6 +450,46 @@ def test_p14_isolated_op_below_capacity_has_zero_gradient(orc):
 def _round_half_up(mu, D):
     m = np.clip(np.where(np.isnan(mu), -1.0, mu.astype(np.float64)), -1.0, D)
     return np.floor(m).astype(np.int64) + ((m - np.floor(m)) >= 0.5)
+
+
+@pytest.mark.parametrize("II", [0, 4])
+def test_p19_usage_cell_derivative(orc, II):
+    """dU_k(s)/dmu_i and dU_k(s)/dsigma_i of each usage cell (App. B.2, folded
+    as in App. B.3) equal central differences of the oracle's forward usage;
+    summed over the cells above capacity they give the whole ReLU part of the
+    gradient (eq:relu with lambda_res = 1 and every other weight 0).  The GPU
+    parity tests accept either indicator value of a near-tie cell through
+    these vectors."""
+    rng = np.random.default_rng(19 + II)
+    p = tiny_problem(rng, 6, 10, II=II)
+    T = II if II else p.D
+    mu = rng.uniform(-1.0, p.D, size=p.n_ops)
+    sg = rng.uniform(0.4, 3.0, size=p.n_ops)
+    h = 1e-6
+
+    def usage(m, s):
+        return orc.loss_grad(p, m[None], s[None], [0, 0, 0], 0.0, 0.0, grad=False)[1][0]
+
+    for k in range(p.n_types):
+        for slot in range(T):
+            gm, gs = orc.usage_cell_grad(p, mu, sg, k, slot, w=1.0)
+            for i in range(p.n_ops):
+                e = np.zeros(p.n_ops); e[i] = h
+                fd_m = (usage(mu + e, sg)[k, slot] - usage(mu - e, sg)[k, slot]) / (2 * h)
+                fd_s = (usage(mu, sg + e)[k, slot] - usage(mu, sg - e)[k, slot]) / (2 * h)
+                assert abs(gm[i] - fd_m) < 1e-7 and abs(gs[i] - fd_s) < 1e-7, (k, slot, i)
+                if p.rtype[i] != k:
+                    assert gm[i] == 0.0 and gs[i] == 0.0
+    _, U, gm_all, gs_all, _ = orc.loss_grad(p, mu[None], sg[None], [0.0, 1.0, 0.0], 0.0, 0.0)
+    sm = np.zeros(p.n_ops); ss = np.zeros(p.n_ops)
+    active = 0
+    for k in range(p.n_types):
+        for slot in range(T):
+            if U[0, k, slot] > p.capacity[k]:
+                gm, gs = orc.usage_cell_grad(p, mu, sg, k, slot, w=1.0)
+                sm += gm; ss += gs; active += 1
+    assert active > 0
+    assert np.abs(sm - gm_all[0]).max() < 1e-12 and np.abs(ss - gs_all[0]).max() < 1e-12
 
 
 def test_rounding_half_up_edges(orc):
@@ -670,6 +715,81 @@ def test_p17_schedule_cost_is_relaxed_cost_at_sigma_zero(orc):
         assert out[4] == terms[0, 2]
 
 
+def _check_golden():
+    with open(os.path.join(GOLDEN, "driver_check_hand_counts.json")) as f:
+        return json.load(f)
+
+
+@pytest.mark.parametrize("case", range(len(_check_golden()["cases"])))
+def test_p20_driver_check_hand_counts(orc, case):
+    """One check of the Alg. 1 driver (Sec. 3.3 Sampling, App. A's reset to
+    the prior best) on hand-counted cases: the legalized candidate, its
+    cost, every rule of the best order, the three re-initialization modes,
+    cleared moments and the initial-width rule."""
+    gd = _check_golden()
+    c = gd["cases"][case]
+    g, pr, w, st = gd["graph"], gd["problems"][c["problem"]], gd["weights"], gd["start"]
+    n = g["n"]
+    p = Problem(n_ops=n, row_ptr=np.array(g["row_ptr"], np.int32), col_idx=np.array(g["col_idx"], np.int32),
+                delay=np.array(g["delay"], np.int32), rtype=np.array(pr["rtype"], np.int32),
+                capacity=np.array(pr["capacity"], np.float32), D=g["D"])
+    mu = np.array([c["mu"]], np.float32)
+    sg = np.array([st["sigma"]], np.float32)
+    m = np.full((2, 1, n), st["m"], np.float32)
+    v = np.full((2, 1, n), st["v"], np.float32)
+    best_c = np.array([orc.NO_BEST if c["best_c"] == "NO" else c["best_c"]], np.float64)
+    out = orc.check(p, mu, sg, m, v, np.array([c["best_s"]]), best_c, w["alpha"], w["beta"], w["gamma"],
+                    reinit_sigma=c["reinit_sigma"], kappa=float(np.float32(1.0 / 6.0)),
+                    sigma_min=float(np.float32(0.05)))
+    mu2, sg2, m2, v2, bs2, bc2, cand, cand_c, mode, imp = out
+    assert cand[0].tolist() == c["cand"], c["name"]
+    assert cand_c[0].tolist() == [float(x) for x in c["cand_c"]], c["name"]
+    assert (int(imp[0]), int(mode[0])) == (c["improved"], c["mode"]), c["name"]
+    assert mu2[0].tolist() == np.array(c["mu_out"], np.float32).tolist(), c["name"]
+    assert sg2[0].tolist() == np.array(c["sigma_out"], np.float32).tolist(), c["name"]
+    want_m, want_v = (0.0, 0.0) if c["moments_cleared"] else (st["m"], st["v"])
+    assert np.all(m2 == want_m) and np.all(v2 == want_v), c["name"]
+    assert bs2[0].tolist() == c["best_s_out"], c["name"]
+    assert bc2[0].tolist() == [float(x) for x in c["best_c_out"]], c["name"]
+
+
+def test_p20_driver_check_mode_follows_definitions(orc):
+    """On random states of a pipelined graph (II > 0, back edges): the
+    candidate is the legalized rounding, its cost the discrete cost, and the
+    mode is 0 exactly when the rounding was already legal, else 1 when the
+    candidate improved the best and 2 when it did not; a re-initialized
+    restart's means are the candidate (1) or the prior best (2)."""
+    rng = np.random.default_rng(120)
+    p = tiny_problem(rng, 9, 24, II=5, n_back=3, max_delay=2, K=2)
+    B = 6
+    mu = rng.uniform(-2, p.D + 2, size=(B, p.n_ops)).astype(np.float32)
+    sg = rng.uniform(0.5, 3, size=(B, p.n_ops)).astype(np.float32)
+    m = rng.uniform(-1, 1, size=(2, B, p.n_ops)).astype(np.float32)
+    v = rng.uniform(0, 1, size=(2, B, p.n_ops)).astype(np.float32)
+    prior_s, _ = orc.legalize(p, rng.uniform(0, p.D, size=(B, p.n_ops)).astype(np.float32))
+    prior_c = orc.schedule_cost(p, prior_s, 0.3, 0.2, 0.1)
+    out = orc.check(p, mu, sg, m, v, prior_s, prior_c, 0.3, 0.2, 0.1)
+    mu2, sg2, m2, v2, bs2, bc2, cand, cand_c, mode, imp = out
+    s_leg, _ = orc.legalize(p, mu)
+    assert np.array_equal(cand, s_leg)
+    assert np.array_equal(cand_c, orc.schedule_cost(p, cand, 0.3, 0.2, 0.1))
+    seen = set()
+    for b in range(B):
+        r = np.floor(mu[b].astype(np.float64) + 0.5).astype(np.int64)
+        legal_rounding = np.array_equal(r, cand[b])
+        want = 0 if legal_rounding else (1 if imp[b] else 2)
+        assert mode[b] == want
+        seen.add(int(mode[b]))
+        if mode[b] == 0:
+            assert np.array_equal(mu2[b], mu[b]) and np.array_equal(m2[:, b], m[:, b])
+        else:
+            src = cand[b] if mode[b] == 1 else prior_s[b]
+            assert np.array_equal(mu2[b], src.astype(np.float32))
+            assert np.all(m2[:, b] == 0) and np.all(v2[:, b] == 0)
+        assert np.array_equal(bs2[b], cand[b] if imp[b] else prior_s[b])
+    assert seen >= {1, 2}, seen
+
+
 def test_p17_legalized_schedules_are_legal(orc):
     """Alg. 3 / Alg. 4 outputs (converged) are legal under the cost's check."""
     rng = np.random.default_rng(171)
@@ -699,9 +819,9 @@ def family(orc, request):
 
 @pytest.mark.parametrize("family", FAMS, indirect=True)
 def test_p18_masses_sum_to_one_and_quartile(orc, family):
-    """App. D families: masses telescope to 1; the CDF at the bin edge where
+    """App. E families: masses telescope to 1; the CDF at the bin edge where
     the family's variable equals its upper quartile (logistic ln 3, Laplace
-    ln 2, Cauchy 1, with the scale matching of App. D) is exactly 3/4."""
+    ln 2, Cauchy 1, with the scale matching of App. E) is exactly 3/4."""
     D, t = 400, 200
     for sigma in (0.7, 13.0, 150.0):
         mu = t + 0.5 - sigma * SCALE[family] * QUARTILE[family]
@@ -723,7 +843,7 @@ def test_p18_symmetric_about_the_centre(orc, family):
 
 
 def test_p18_cauchy_half_width_matches_gaussian(orc):
-    """App. D's Cauchy scale matches the Gaussian's full width at half
+    """App. E's Cauchy scale matches the Gaussian's full width at half
     maximum: far from the boundaries the masses of both fall to half their
     peak at the same offset sigma sqrt(2 ln 2)."""
     D, sigma = 40001, 3000.0
@@ -736,6 +856,7 @@ def test_p18_cauchy_half_width_matches_gaussian(orc):
     orc.set_family("gaussian")
 
 
+@needs_torch
 @pytest.mark.parametrize("family", FAMS, indirect=True)
 def test_p18_gradient_matches_autograd(orc, family):
     """The hand-derived backward with each family's density equals fp64
