@@ -183,6 +183,21 @@ gaus_status gaus_legalize(gaus_ctx *ctx, const float *mu, int32_t *sched, int32_
  * are summed in steps of 2^-20.  Asynchronous. */
 gaus_status gaus_schedule_cost(gaus_ctx *ctx, const int32_t *sched, double *cost);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * discrete cost as gaus_schedule_cost (same kernels, bitwise equal results),
+ * with its scratch -- usage counts, storage differences and profile,
+ * edge-length sums and legality flags -- in a fixed 8 MiB device array of
+ * the library instead of its allocations; the call allocates and frees
+ * nothing.  It needs B*(4*K*T + 8*(D+1) + 8*T) + 12*B bytes (each part
+ * rounded up to 256): INVALID_ARG with a message when that exceeds 8 MiB.
+ * Every context on one device shares that device's array and the kernels
+ * clear it on each call, so calls that overlap on one device (other
+ * streams, other threads) race; calls in stream order do not.  sched DEVICE
+ * [B][N] int32, cost DEVICE [B][6] double as gaus_schedule_cost.
+ * Asynchronous.  Errors: INVALID_ARG, DEVICE. */
+gaus_status gaus_schedule_cost_noalloc(gaus_ctx *ctx, const int32_t *sched, double *cost);
+
 /* Alg. 1 driver (Sec. 3.3) on the bound state. */
 typedef struct {
     int32_t max_iters;     /* fused iterations in total, >= 1 */

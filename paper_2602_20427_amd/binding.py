@@ -20,7 +20,8 @@ OK, E_INVALID_ARG, E_CYCLE, E_HORIZON, E_NOT_CONVERGED, E_OVERFLOW, E_DEVICE, E_
 
 # symbols declared in include/gaus.h
 EXPORTS = ("gaus_default_hparams", "gaus_init", "gaus_bind_state", "gaus_loss_grad", "gaus_step",
-           "gaus_adam_from_grad", "gaus_legalize", "gaus_schedule_cost", "gaus_solve", "gaus_solve_check",
+           "gaus_adam_from_grad", "gaus_legalize", "gaus_schedule_cost", "gaus_schedule_cost_noalloc",
+           "gaus_solve", "gaus_solve_check",
            "gaus_init_state",
            "gaus_asap_alap",
            "gaus_get_usage", "gaus_get_storage", "gaus_kernel_timing", "gaus_kernel_timing_read", "gaus_sync",
@@ -92,6 +93,7 @@ def load():
         "gaus_adam_from_grad": ([vp] * 4, C.c_int),
         "gaus_legalize": ([vp] * 4, C.c_int),
         "gaus_schedule_cost": ([vp] * 3, C.c_int),
+        "gaus_schedule_cost_noalloc": ([vp] * 3, C.c_int),
         "gaus_solve": ([vp] * 5, C.c_int),
         "gaus_solve_check": ([vp, vp, vp, i32, vp], C.c_int),
         "gaus_init_state": ([vp] * 4, C.c_int),
@@ -245,6 +247,14 @@ class Context:
         import torch
         self._check(load().gaus_schedule_cost(self._h, _dptr(sched, torch.int32, (self.B, self.N), "sched"),
                                               _dptr(cost, torch.float64, (self.B, N_COST), "cost")))
+
+    def schedule_cost_noalloc(self, sched, cost):
+        """gaus_schedule_cost with its scratch in the library's fixed device
+        array (the call allocates nothing)."""
+        import torch
+        self._check(load().gaus_schedule_cost_noalloc(
+            self._h, _dptr(sched, torch.int32, (self.B, self.N), "sched"),
+            _dptr(cost, torch.float64, (self.B, N_COST), "cost")))
 
     def solve(self, best_sched, best_cost, max_iters: int, check_every: int, time_limit_s: float = 0.0,
               reinit_sigma: bool = False) -> dict:

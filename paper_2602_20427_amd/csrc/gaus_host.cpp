@@ -29,6 +29,7 @@ struct gaus_ctx {
     LaunchCfg lc{};
     hipStream_t stream = nullptr;
     int device = 0;
+    void *scratch = nullptr;            // this device's copy of the library's scratch array
     std::vector<void *> allocs;
     std::vector<int> asap, alap;
     std::string err = "no error";
@@ -481,6 +482,15 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
                hp.family};
     c->stream = static_cast<hipStream_t>(hip_stream);
     (void)hipGetDevice(&c->device);
+    {
+        // address of the scratch array on this device (the allocation-free
+        // entry point's workspace), taken once per device with it current
+        const hipError_t e = scratch_address(c->device, &c->scratch);
+        if (e != hipSuccess) {
+            delete c;
+            return fail(nullptr, GAUS_E_DEVICE, "scratch address: %s", hipGetErrorString(e));
+        }
+    }
     int tile = 0, ntiles = 0;
     choose_config(h, B, c->lc, tile, ntiles);
     c->lc.fam = hp.family;
@@ -736,6 +746,20 @@ gaus_status gaus_schedule_cost(gaus_ctx *ctx, const int32_t *sched, double *cost
     if (!sched || !cost) return fail(ctx, GAUS_E_INVALID_ARG, "schedule_cost: null pointer");
     hipError_t e = enqueue_schedule_cost(ctx->g, ctx->w, ctx->hp, sched, cost, ctx->stream);
     if (e != hipSuccess) return hip_fail(ctx, e, "schedule_cost launch");
+    return GAUS_OK;
+}
+
+gaus_status gaus_schedule_cost_noalloc(gaus_ctx *ctx, const int32_t *sched, double *cost) {
+    if (!ctx) return GAUS_E_INVALID_ARG;
+    if (!sched || !cost) return fail(ctx, GAUS_E_INVALID_ARG, "schedule_cost_noalloc: null pointer");
+    const size_t need = cost_scratch_bytes(ctx->g);
+    if (need > kScratchBytes)
+        return fail(ctx, GAUS_E_INVALID_ARG,
+                    "schedule_cost_noalloc: needs %zu bytes of scratch (B*(4*K*T + 8*(D+1) + 8*T) + 12*B, "
+                    "each part rounded up to 256), more than the library's %zu",
+                    need, kScratchBytes);
+    hipError_t e = enqueue_schedule_cost_scratch(ctx->g, ctx->w, ctx->hp, ctx->scratch, sched, cost, ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "schedule_cost_noalloc launch");
     return GAUS_OK;
 }
 

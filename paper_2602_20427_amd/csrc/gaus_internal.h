@@ -238,6 +238,16 @@ hipError_t enqueue_adam_from_grad(const Graph &g, const Work &w, const HP &hp, c
 // Discrete cost of schedules sched [B][N] (device) into cost [B][kCost] (device).
 hipError_t enqueue_schedule_cost(const Graph &g, const Work &w, const HP &hp, const int *sched, double *cost,
                                  hipStream_t st);
+// The same with its scratch (usage counts, storage differences and profile,
+// edge-length sums, legality flags) in the library's file-scope device array
+// of kScratchBytes: cost_scratch_bytes(g) must not exceed it.  scratch_ptr is
+// that array's address on the current device (scratch_address, cached per
+// device).  Calls that overlap on one device share the array and race.
+constexpr size_t kScratchBytes = size_t(8) << 20;
+size_t cost_scratch_bytes(const Graph &g);
+hipError_t scratch_address(int device, void **out);
+hipError_t enqueue_schedule_cost_scratch(const Graph &g, const Work &w, const HP &hp, void *scratch_ptr,
+                                         const int *sched, double *cost, hipStream_t st);
 // One check of the Alg. 1 driver: legalize the rounded means, cost the
 // candidates, keep each restart's best, re-initialize restarts whose
 // rounding was not legal (from the candidate if it improved, else from the

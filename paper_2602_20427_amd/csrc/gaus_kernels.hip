@@ -19,6 +19,8 @@
 #include "gaus_device.h"
 
 #include <algorithm>
+#include <map>
+#include <mutex>
 
 namespace gaus {
 
@@ -1224,6 +1226,62 @@ hipError_t enqueue_schedule_cost(const Graph &g, const Work &w, const HP &hp, co
     hipLaunchKernelGGL(k_cost_ops, dim3((std::max(g.N, g.nb) + 255) / 256, g.B), dim3(256), 0, st, g, w, sched);
     hipLaunchKernelGGL(k_cost_final, dim3(g.B), dim3(kCostBS), 0, st, g, w, hp, cost);
     return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Scratch of the allocation-free schedule cost: the usage counts, storage
+// differences and profile, edge-length sums and legality flags of every
+// restart (the buffers k_cost_* clear and fill) are carved from one
+// file-scope device array instead of library allocations.  Each device holds
+// its own copy until the process ends; host code takes its address on that
+// device from hipGetSymbolAddress (cached per device) and never uses the
+// array's name, which in host code is only a stand-in.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+}  // namespace
+
+size_t cost_scratch_bytes(const Graph &g) {
+    const size_t B = (size_t)g.B;
+    return align256(sizeof(int) * B * g.K * g.T) + align256(sizeof(long long) * B * ((size_t)g.D + 1)) +
+           align256(sizeof(long long) * B * g.T) + align256(sizeof(unsigned long long) * B) +
+           align256(sizeof(int) * B);
+}
+
+hipError_t scratch_address(int device, void **out) {
+    static std::mutex mu;
+    static std::map<int, void *> by_device;
+    std::lock_guard<std::mutex> lock(mu);
+    auto it = by_device.find(device);
+    if (it != by_device.end()) {
+        *out = it->second;
+        return hipSuccess;
+    }
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));   // the current device's copy
+    if (e != hipSuccess) return e;
+    by_device[device] = p;
+    *out = p;
+    return hipSuccess;
+}
+
+hipError_t enqueue_schedule_cost_scratch(const Graph &g, const Work &w, const HP &hp, void *scratch_ptr,
+                                         const int *sched, double *cost, hipStream_t st) {
+    Work ws = w;   // the same kernels on buffers inside the scratch array
+    unsigned char *q = static_cast<unsigned char *>(scratch_ptr);
+    const size_t B = (size_t)g.B;
+    ws.hist = reinterpret_cast<int *>(q);
+    q += align256(sizeof(int) * B * g.K * g.T);
+    ws.mdiff = reinterpret_cast<long long *>(q);
+    q += align256(sizeof(long long) * B * ((size_t)g.D + 1));
+    ws.mprof = reinterpret_cast<long long *>(q);
+    q += align256(sizeof(long long) * B * g.T);
+    ws.lcom_acc = reinterpret_cast<unsigned long long *>(q);
+    q += align256(sizeof(unsigned long long) * B);
+    ws.illegal = reinterpret_cast<int *>(q);
+    return enqueue_schedule_cost(g, ws, hp, sched, cost, st);
 }
 
 // ---------------------------------------------------------------------------
