@@ -232,6 +232,8 @@ struct HostGraph {
     std::vector<int> bin_ptr, bin, bout_ptr, bout;
     std::vector<int> level, lvl_ptr, lvl_ops;
     std::vector<int> leg_items, leg_over;   // legalization items in level order (see Graph::leg_items)
+    int leg_nover = 0;                       // predecessors in leg_over (before padding)
+    std::vector<int> leg_batch;              // ring batches (see Graph::leg_batch)
     std::vector<int> asap, alap;
     std::vector<int> perm, grp_start, type_grp, grp_of;
     std::vector<int> big_ops, big_of;
@@ -546,6 +548,7 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
                 else h.leg_over.push_back(h.pred_src[p0 + k]);
             }
         }
+        h.leg_nover = (int)h.leg_over.size();
         if (h.leg_over.empty()) h.leg_over.push_back(0);
     }
     {
@@ -566,6 +569,51 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
         else if (h.II == 0 && (long long)h.D + dmax < (1LL << 31) - 1 && 4 * N <= room) g.leg_mode = 2;
         else if (h.II > 0 && (long long)h.D + dmax + N * N * (dmax + 1) < (1LL << 31) - 1 && 8 * N <= room)
             g.leg_mode = 2;
+        // II = 0 with the schedule in LDS: the level items through a double
+        // ring in the LDS left over (two halves of RI items of 32 bytes and
+        // RO = RI overflow predecessors), unless one op's predecessors exceed
+        // a half
+        g.leg_ring = 0;
+        if (h.II == 0 && (g.leg_mode == 1 || g.leg_mode == 2) && g.nlevels > 1) {
+            const long long rdb = (long long)(g.leg_mode == 1 ? 2 : 4) * N;
+            const long long left = room - ((rdb + 15) & ~15LL);
+            // ring halves of RI items; the batch table needs 12 bytes per
+            // batch (at most N / RI + 2 batches unless one op's predecessors
+            // fill a half) and is checked after the cut
+            long long ri = std::min<long long>({left / 2 / 36, kLegRingItemsMax, kLegRingOverMax});
+            for (; ri >= 64 && !g.leg_ring; ri = ri * 7 / 8) {
+                const int RI = (int)ri, RO = (int)ri;
+                // batches: contiguous item ranges from the first item of level 1
+                // (a wide level spans several), each within RI items and RO
+                // overflow predecessors; row = (level of the first item, first
+                // item, first overflow predecessor)
+                auto over_at = [&](int q) { return q < h.N ? h.leg_items[(size_t)8 * q + 3] : h.leg_nover; };
+                std::vector<int> bt;
+                bool fits = true;
+                int q = h.lvl_ptr[1], l = 1;
+                while (q < h.N && fits) {
+                    while (h.lvl_ptr[l + 1] <= q) ++l;
+                    const int o0 = over_at(q);
+                    int q1 = std::min(h.N, q + RI);
+                    while (q1 > q && over_at(q1) - o0 > RO) --q1;
+                    if (q1 == q) fits = false;   // one item's predecessors exceed a half
+                    bt.insert(bt.end(), {l, q, o0});
+                    q = q1;
+                }
+                if (!fits) break;
+                bt.insert(bt.end(), {g.nlevels, h.N, over_at(h.N)});
+                const long long nbatch = (long long)bt.size() / 3 - 1;
+                const long long need = ((rdb + 15) & ~15LL) + 4LL * ((3 * (nbatch + 1) + 3) & ~3LL) +
+                                       2LL * 16 * (2 * RI + (RO + 3) / 4);
+                if (need > room) continue;   // smaller halves, more batches
+                h.leg_batch = bt;
+                g.leg_nbatch = (int)nbatch;
+                g.leg_ring_items = RI;
+                g.leg_ring_over = RO;
+                g.leg_ring = 1;
+            }
+        }
+        if (h.leg_batch.empty()) h.leg_batch.assign(3, 0);
     }
     std::vector<float> cap(h.cap);
     const size_t BN = (size_t)B * h.N;
@@ -575,7 +623,7 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     UP(bsrc, h.bsrc); UP(bdst, h.bdst); UP(bdist, h.bdist); UP(bin_ptr, h.bin_ptr); UP(bin, h.bin);
     UP(bout_ptr, h.bout_ptr); UP(bout, h.bout); UP(perm, h.perm); UP(grp_start, h.grp_start);
     UP(type_grp, h.type_grp); UP(lvl_ptr, h.lvl_ptr); UP(lvl_ops, h.lvl_ops); UP(asap, h.asap);
-    UP(leg_items, h.leg_items); UP(leg_over, h.leg_over);
+    UP(leg_items, h.leg_items); UP(leg_over, h.leg_over); UP(leg_batch, h.leg_batch);
     UP(grp_of, h.grp_of);
     UP(bmem, h.bmem);
     UP(big_ops, h.big_ops);

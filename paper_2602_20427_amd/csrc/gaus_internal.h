@@ -100,6 +100,11 @@ struct Graph {
                                          // start of the predecessors past kLegPre in leg_over, the first
                                          // kLegPre predecessors (32-byte aligned)
     const int *leg_over;                 // predecessors past the first kLegPre, in level order
+    int leg_ring;                        // 1: II = 0 legalization through the LDS ring (k_legalize_ring)
+    int leg_ring_items, leg_ring_over;   // items and overflow predecessors one ring half holds
+    int leg_nbatch;                      // ring batches: contiguous ranges of the items of levels >= 1
+    const int *leg_batch;                // [nbatch+1][3] level of the first item, first item, first
+                                         // overflow predecessor of each batch (last row: the ends)
     const int *grp_of;                   // [N] group of each op
     const float *bmem;                   // [N] storage units b_i
     int nbig;                            // ops with more than kBigIn predecessors
@@ -255,6 +260,12 @@ hipError_t enqueue_schedule_cost_scratch(const Graph &g, const Work &w, const HP
 hipError_t enqueue_best_init(const Graph &g, const Work &w, double *best_cost, hipStream_t st);
 hipError_t enqueue_check(const Graph &g, const Work &w, const HP &hp, float *mu, float *sigma, float *m,
                          float *v, int *best_sched, double *best_cost, int reinit_sigma, hipStream_t st);
+
+// Dynamic LDS of the ring legalization with ready times of ready_bytes each.
+size_t legalize_ring_lds(const Graph &g, int ready_bytes);
+// Ring batch limits (kernel staging: two 16-byte loads per item, kLegRingV4 of
+// them per thread; kLegRingOv overflow predecessors per thread; 512 threads).
+constexpr int kLegRingItemsMax = 2048, kLegRingOverMax = 2048;
 
 // Round + legalize every restart; writes sched [B][N] and w.status [B].
 hipError_t enqueue_legalize(const Graph &g, const Work &w, const float *mu, int *sched,

@@ -1089,10 +1089,207 @@ __global__ __launch_bounds__(kLegLdsBS) void k_legalize_lds(Graph G, Work W, con
     if (tid == 0) W.status[b] = st;
 }
 
-// Legalization of every restart with the variant the host chose (Graph::leg_mode).
+// Alg. 3 (II = 0) with the level items in a double-buffered LDS ring: the
+// host cuts the items of levels 1 .. nlevels-1 (in level order) into batches
+// whose items and predecessors past the first kLegPre fit one half of the
+// ring (a wide level spans batches; its items are independent, and batches
+// run in order); while batch k is processed from one half, the global loads
+// of batch k+1 are in flight into registers and are written to the other
+// half afterwards, so a level costs LDS reads and an LDS-only barrier.  Same
+// arithmetic as k_legalize_lds, so the same schedules.
+constexpr int kLegRingBS = 512;
+constexpr int kLegRingV4 = 8;   // 16-byte loads staged per thread and batch (two per item)
+constexpr int kLegRingOv = 4;   // overflow predecessors staged per thread and batch
+constexpr int kLegRingU = 16;   // ops per thread and round of the rounding and the output (loads in flight)
+
+template <typename T>
+__global__ __launch_bounds__(kLegRingBS) void k_legalize_ring(Graph G, Work W, const float *__restrict__ mu,
+                                                           int *sched) {
+    extern __shared__ __align__(16) unsigned char sDynLeg[];
+    const int nl = G.nlevels, nlp = (nl + 1 + 3) & ~3, nb = G.leg_nbatch, nbt = (3 * (nb + 1) + 3) & ~3;
+    const int b = blockIdx.x, tid = threadIdx.x;
+    const int N = G.N, D = G.D;
+    // LDS: level bounds, the batch table, ready times s_v + Lat_v, the ring.
+    // Everything the level loop reads is in LDS, so its waits are LDS waits
+    // and the staged global loads of the next batch stay in flight.
+    int *lp = reinterpret_cast<int *>(sDynLeg);
+    int *bt = lp + nlp;
+    T *rd = reinterpret_cast<T *>(bt + nbt);
+    const size_t rd_bytes = (sizeof(T) * (size_t)N + 15) & ~size_t(15);
+    int4 *ring = reinterpret_cast<int4 *>(reinterpret_cast<unsigned char *>(rd) + rd_bytes);
+    const int RI = G.leg_ring_items, RO = G.leg_ring_over;
+    const int HS = 2 * RI + (RO + 3) / 4;               // int4 per ring half: items, then overflow
+    for (int l = tid; l <= nl; l += kLegRingBS) lp[l] = G.lvl_ptr[l];
+    for (int q = tid; q < 3 * (nb + 1); q += kLegRingBS) bt[q] = G.leg_batch[q];
+    for (int v0 = tid; v0 < N; v0 += kLegRingU * kLegRingBS) {
+        float m[kLegRingU];
+        int lo[kLegRingU], hi[kLegRingU], dl[kLegRingU];
+#pragma unroll
+        for (int k = 0; k < kLegRingU; ++k) {
+            const int v = v0 + k * kLegRingBS;
+            if (v < N) { m[k] = mu[(size_t)b * N + v]; lo[k] = G.asap[v]; hi[k] = G.alap[v]; dl[k] = G.delay[v]; }
+        }
+#pragma unroll
+        for (int k = 0; k < kLegRingU; ++k) {
+            const int v = v0 + k * kLegRingBS;
+            if (v < N) {
+                long long r = round_half_up(m[k], D);
+                r = r < lo[k] ? lo[k] : (r > hi[k] ? hi[k] : r);
+                rd[v] = (T)(r + dl[k]);
+            }
+        }
+    }
+    __syncthreads();
+    // staged data in native 4-vectors (plain registers)
+    typedef int vi4 __attribute__((ext_vector_type(4)));
+    const vi4 *items = reinterpret_cast<const vi4 *>(G.leg_items);
+    vi4 *vring = reinterpret_cast<vi4 *>(ring);
+    vi4 sv[kLegRingV4];
+    int so[kLegRingOv];
+    // batch 0 straight into half 0
+    if (nb > 0) {
+        const int q0 = bt[1], q1 = bt[4], o0 = bt[2], o1 = bt[5];
+#pragma unroll
+        for (int m = 0; m < kLegRingV4; ++m) {
+            const int j = tid + m * kLegRingBS;
+            sv[m] = items[j < 2 * (q1 - q0) ? 2 * (size_t)q0 + j : 0];
+        }
+#pragma unroll
+        for (int m = 0; m < kLegRingOv; ++m) {
+            const int j = tid + m * kLegRingBS;
+            so[m] = G.leg_over[j < o1 - o0 ? o0 + j : 0];
+        }
+        int *ov = reinterpret_cast<int *>(ring + 2 * RI);
+#pragma unroll
+        for (int m = 0; m < kLegRingV4; ++m) {
+            const int j = tid + m * kLegRingBS;
+            if (j < 2 * (q1 - q0)) vring[j] = sv[m];
+        }
+#pragma unroll
+        for (int m = 0; m < kLegRingOv; ++m) {
+            const int j = tid + m * kLegRingBS;
+            if (j < o1 - o0) ov[j] = so[m];
+        }
+    }
+    __syncthreads();
+    for (int k = 0; k < nb; ++k) {
+        const int qb = bt[3 * k + 1], ob = bt[3 * k + 2], qe = bt[3 * k + 4], lb = bt[3 * k];
+        const bool more = k + 1 < nb;
+        const int nq0 = more ? bt[3 * k + 4] : 0, nq1 = more ? bt[3 * k + 7] : 0;
+        const int no0 = more ? bt[3 * k + 5] : 0, no1 = more ? bt[3 * k + 8] : 0;
+        // batch k+1 into registers: in flight while batch k is processed
+        // (straight-line loads, each index clamped into its array, so that
+        // no branch makes the compiler wait for the earlier ones)
+#pragma unroll
+        for (int m = 0; m < kLegRingV4; ++m) {
+            const int j = tid + m * kLegRingBS;
+            sv[m] = items[j < 2 * (nq1 - nq0) ? 2 * (size_t)nq0 + j : 0];
+        }
+#pragma unroll
+        for (int m = 0; m < kLegRingOv; ++m) {
+            const int j = tid + m * kLegRingBS;
+            so[m] = G.leg_over[j < no1 - no0 ? no0 + j : 0];
+        }
+        const vi4 *base = vring + (size_t)(k & 1) * HS;
+        const int *ov = reinterpret_cast<const int *>(base + 2 * RI);
+        // one item: its ready time from its predecessors' (Alg. 3's raise)
+        auto process = [&](const vi4 a, const vi4 c) __attribute__((always_inline)) {
+            const int v = a.x, dv = a.y, n = a.z, p0 = a.w;
+            // the first kLegPre predecessors read at once (absent ones read
+            // v's own slot and count as 0: ready times are >= 0); values stay
+            // below 2^31 (D + Lat < 2^31 for the LDS schedules)
+            const int u[kLegPre] = {c.x, c.y, c.z, c.w};
+            int x[kLegPre];
+#pragma unroll
+            for (int kk = 0; kk < kLegPre; ++kk) x[kk] = (int)rd[kk < n ? u[kk] : v];
+            int req = (int)rd[v] - dv;
+#pragma unroll
+            for (int kk = 0; kk < kLegPre; ++kk) req = max(req, kk < n ? x[kk] : 0);
+            // the rest four at a time: four independent index reads, then four
+            // ready times (indices clamped into the overflow area; the values
+            // past n are discarded)
+            for (int kk = kLegPre; kk < n; kk += 4) {
+                int w[4], y[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) w[j] = ov[min(p0 - ob + kk + j - kLegPre, RO - 1)];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) y[j] = (int)rd[kk + j < n ? w[j] : v];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) req = max(req, kk + j < n ? y[j] : 0);
+            }
+            rd[v] = (T)(req + dv);
+        };
+        // the levels this batch's items meet, one item per thread and level
+        // (wider levels loop); the bounds and the item of the next level are
+        // read before the barrier (they do not change during the batch), so
+        // after it only the predecessors' ready times are waited for
+        int l = lb;
+        int qz = min(lp[l + 1], qe);
+        int q = max(lp[l], qb) + tid;
+        vi4 ia = {0, 0, 0, 0}, ic = {0, 0, 0, 0};
+        if (q < qz) { ia = base[2 * (q - qb)]; ic = base[2 * (q - qb) + 1]; }
+        while (true) {
+            if (q < qz) process(ia, ic);
+            for (int q2 = q + kLegRingBS; q2 < qz; q2 += kLegRingBS) process(base[2 * (q2 - qb)], base[2 * (q2 - qb) + 1]);
+            const bool next = l + 1 < nl && lp[l + 1] < qe;
+            if (next) {
+                q = lp[l + 1] + tid;
+                qz = min(lp[l + 2], qe);
+                if (q < qz) { ia = base[2 * (q - qb)]; ic = base[2 * (q - qb) + 1]; }
+            }
+            lds_barrier();
+            if (!next) break;
+            ++l;
+        }
+        if (more) {   // the staged batch into the other half (its last readers finished batch k-1)
+            vi4 *nbase = vring + (size_t)((k + 1) & 1) * HS;
+            int *nov = reinterpret_cast<int *>(nbase + 2 * RI);
+#pragma unroll
+            for (int m = 0; m < kLegRingV4; ++m) {
+                const int j = tid + m * kLegRingBS;
+                if (j < 2 * (nq1 - nq0)) nbase[j] = sv[m];
+            }
+#pragma unroll
+            for (int m = 0; m < kLegRingOv; ++m) {
+                const int j = tid + m * kLegRingBS;
+                if (j < no1 - no0) nov[j] = so[m];
+            }
+        }
+        __syncthreads();
+    }
+    for (int v0 = tid; v0 < N; v0 += kLegRingU * kLegRingBS) {
+        int dl[kLegRingU];
+#pragma unroll
+        for (int k = 0; k < kLegRingU; ++k) {
+            const int v = v0 + k * kLegRingBS;
+            dl[k] = v < N ? G.delay[v] : 0;
+        }
+#pragma unroll
+        for (int k = 0; k < kLegRingU; ++k) {
+            const int v = v0 + k * kLegRingBS;
+            if (v < N) sched[(size_t)b * N + v] = (int)((long long)rd[v] - dl[k]);
+        }
+    }
+    if (tid == 0) W.status[b] = 0;
+}
+
+size_t legalize_ring_lds(const Graph &g, int ready_bytes) {
+    const size_t lvl = sizeof(int) * (size_t)((g.nlevels + 1 + 3) & ~3);
+    const size_t bt = sizeof(int) * (size_t)((3 * (g.leg_nbatch + 1) + 3) & ~3);
+    const size_t rd = ((size_t)ready_bytes * g.N + 15) & ~size_t(15);
+    const size_t half = 16 * (2 * (size_t)g.leg_ring_items + (size_t)(g.leg_ring_over + 3) / 4);
+    return lvl + bt + rd + 2 * half;
+}
+
 hipError_t launch_legalize(const Graph &g, const Work &w, const float *mu, int *sched, hipStream_t st) {
     const size_t lvl = sizeof(int) * (size_t)((g.nlevels + 1 + 3) & ~3);
-    if (g.leg_mode == 1)
+    if (g.leg_ring && g.leg_mode == 1)
+        hipLaunchKernelGGL(k_legalize_ring<short>, dim3(g.B), dim3(kLegRingBS), legalize_ring_lds(g, 2), st, g, w, mu,
+                           sched);
+    else if (g.leg_ring && g.leg_mode == 2)
+        hipLaunchKernelGGL(k_legalize_ring<int>, dim3(g.B), dim3(kLegRingBS), legalize_ring_lds(g, 4), st, g, w, mu,
+                           sched);
+    else if (g.leg_mode == 1)
         hipLaunchKernelGGL(k_legalize_lds<short>, dim3(g.B), dim3(kLegLdsBS), lvl + sizeof(short) * (size_t)g.N, st,
                            g, w, mu, sched);
     else if (g.leg_mode == 2)
