@@ -104,6 +104,39 @@ __host__ __device__ constexpr float fam_zflush() {
          : 3.0e38f;
 }
 
+// Bin edges [lo, hi] (clamped into [a - 1 .. b + 1]) outside which an op's CDF
+// is the exact constant: 0 below lo, 1 above hi (kZF = fam_zflush of its
+// family).  Widened by one step for the rounding of the float bounds; a NaN
+// mean gives [a, b].
+__device__ __forceinline__ void spread_z(float kZF, float mu, float rs, int a, int b, int &lo, int &hi) {
+    const float w = kZF / rs, c = mu - 0.5f;
+    float l = floorf(c - w) - 1.0f, h = ceilf(c + w) + 1.0f;
+    l = fminf(fmaxf(l, (float)a), (float)b + 1.0f);
+    h = fmaxf(fminf(h, (float)b), (float)a - 1.0f);
+    lo = (int)l;
+    hi = (int)h;
+}
+
+// Tiles [t0, tb) of the step-by-step op kernel that hold records: an op's
+// producer-side derivatives (of F_i at u and of A(u) and F_i' at u - s) can
+// be nonzero only where its spread, or the spread shifted by its delay s,
+// meets the tile; the consumer-side derivatives of an edge into an op only
+// where the consumer's spread does.  Elsewhere they are exactly 0: the op
+// kernel writes no record there and its readers skip the tile.  (These are
+// the op kernel's own spread tests, so writer and readers agree.)
+__device__ __forceinline__ bool tile_prod_rec(float kZF, float mu, float rs, int s, int t0, int tb) {
+    int pl, ph;
+    spread_z(kZF, mu, rs, t0 - s - 1, tb, pl, ph);
+    const int n1 = min(ph + 1, tb - 1) - max(pl, t0) + 1;
+    const int n2 = min(ph + s, tb - 1) - max(pl + s - 1, t0) + 1;
+    return n1 > 0 || n2 > 0;
+}
+__device__ __forceinline__ bool tile_cons_rec(float kZF, float mu, float rs, int t0, int tb) {
+    int cl, ch;
+    spread_z(kZF, mu, rs, t0 - 1, tb, cl, ch);
+    return min(ch + 1, tb - 1) - max(cl, t0) + 1 > 0;
+}
+
 // The same with the family chosen at run time (kernels outside the inner loops).
 __device__ __forceinline__ float fam_k_rt(int fam) {
     switch (fam) {
@@ -111,6 +144,14 @@ __device__ __forceinline__ float fam_k_rt(int fam) {
         case 2: return fam_k<2>();
         case 3: return fam_k<3>();
         default: return fam_k<0>();
+    }
+}
+__device__ __forceinline__ float fam_zflush_rt(int fam) {
+    switch (fam) {
+        case 1: return fam_zflush<1>();
+        case 2: return fam_zflush<2>();
+        case 3: return fam_zflush<3>();
+        default: return fam_zflush<0>();
     }
 }
 __device__ __forceinline__ float fam_h_rt(int fam, float z) {

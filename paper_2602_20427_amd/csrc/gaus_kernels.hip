@@ -654,12 +654,15 @@ __device__ __forceinline__ float combine_grad(float w_res, float r, float w_dep,
 // fp64 and a fixed order: consumer-side dependency / edge-length derivatives
 // and, with the storage term, the successor-side storage derivatives.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_gather_big(Graph G, Work W, HP hp) {
+__global__ __launch_bounds__(256) void k_gather_big(Graph G, Work W, HP hp, const float *__restrict__ mu) {
     __shared__ double sRed[4][6];
     const int x = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
     const int lane = tid & 63, wid = tid >> 6;
     const int i = G.big_ops[x], N = G.N, nt = G.ntiles;
     const bool poly_i = W.cls[(size_t)b * N + i] != 0;
+    // step-by-step in-edge records exist only in the tiles the op's spread
+    // meets (tile_cons_rec, the op kernel's own test)
+    const float kZF = fam_zflush_rt(hp.family), m_i = mu[(size_t)b * N + i], rs = W.rsig[(size_t)b * N + i];
     double acc[6] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
     for (int q = G.pred_ptr[i] + tid; q < G.pred_ptr[i + 1]; q += 256) {
         const int e = G.pred_eid[q];
@@ -668,8 +671,11 @@ __global__ __launch_bounds__(256) void k_gather_big(Graph G, Work W, HP hp) {
             for (int c = 0; c < 4; ++c) acc[c] += cp[c];
         } else {
             const float *cp = W.cpart + (((size_t)b * G.E + e) * nt) * kCP;
-            for (int tl = 0; tl < nt; ++tl)
+            for (int tl = 0; tl < nt; ++tl) {
+                const int t0 = tl * G.tile;
+                if (!tile_cons_rec(kZF, m_i, rs, t0, min(t0 + G.tile, G.D))) continue;
                 for (int c = 0; c < 4; ++c) acc[c] += cp[tl * kCP + c];
+            }
         }
         if (hp.gamma != 0.0f) {
             if (W.mpoly[(size_t)b * N + G.pred_src[q]]) {   // producer's storage term on the polynomials
@@ -730,10 +736,27 @@ __global__ __launch_bounds__(256) void k_final(Graph G, Work W, HP hp, const flo
         rsg += (double)(sgn * (Fm * z));
     }
 
+    // step-by-step records exist only in the tiles the op's spreads meet
+    // (tile_prod_rec / tile_cons_rec, the op kernel's own tests)
+    const float kZF = fam_zflush_rt(hp.family);
+    unsigned cons_tiles = 0;   // bit t: tile t holds records of edges into this op (nt <= 32)
+    if (nt <= 32)
+        for (int tl = 0; tl < nt; ++tl) {
+            const int t0 = tl * G.tile;
+            cons_tiles |= tile_cons_rec(kZF, m_i, rs, t0, min(t0 + G.tile, G.D)) ? 1u << tl : 0u;
+        }
+    auto cons_tile = [&](int tl) {
+        if (nt <= 32) return ((cons_tiles >> tl) & 1u) != 0;
+        const int t0 = tl * G.tile;
+        return tile_cons_rec(kZF, m_i, rs, t0, min(t0 + G.tile, G.D));
+    };
     double dm = 0.0, ds = 0.0, cm = 0.0, cs = 0.0;
     if (W.dflag[bi]) {
         const float *pp = W.ppart + bi * nt * kPP;
+        const int lat_i = G.delay[i];
         for (int tl = 0; tl < nt; ++tl) {
+            const int t0 = tl * G.tile;
+            if (!tile_prod_rec(kZF, m_i, rs, lat_i, t0, min(t0 + G.tile, G.D))) continue;
             dm += pp[tl * kPP + 2]; ds += pp[tl * kPP + 3];
             cm += pp[tl * kPP + 4]; cs += pp[tl * kPP + 5];
         }
@@ -755,6 +778,7 @@ __global__ __launch_bounds__(256) void k_final(Graph G, Work W, HP hp, const flo
         }
         const float *cp = W.cpart + (((size_t)b * G.E + e) * nt) * kCP;
         for (int tl = 0; tl < nt; ++tl) {
+            if (!cons_tile(tl)) continue;
             dm += cp[tl * kCP + 0]; ds += cp[tl * kCP + 1];
             cm += cp[tl * kCP + 2]; cs += cp[tl * kCP + 3];
         }
@@ -1618,7 +1642,7 @@ hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const 
         if ((e = launch_mem_bwd(g, w, lc, a.mu, a.sigma, st)) != hipSuccess) return e;
         if (pa.enabled && (e = launch_mem_poly_bwd(g, w, pa, a.mu, st)) != hipSuccess) return e;
     }
-    if (g.nbig > 0) hipLaunchKernelGGL(k_gather_big, dim3(g.nbig, g.B), dim3(256), 0, st, g, w, hp);
+    if (g.nbig > 0) hipLaunchKernelGGL(k_gather_big, dim3(g.nbig, g.B), dim3(256), 0, st, g, w, hp, a.mu);
     {
         dim3 grid((g.N + 255) / 256, g.B);
         hipLaunchKernelGGL(k_final, grid, dim3(256), 0, st, g, w, hp, a.mu, a.sigma, a.gmu, a.gsig,

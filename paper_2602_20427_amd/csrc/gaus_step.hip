@@ -46,18 +46,9 @@ constexpr int kNarrowSpan = 128;   // widest spread (in steps) on the narrow pat
 constexpr int kTinySpan = 32;      // widest spread of the ops taken four per wave
 constexpr int kNarrowPass = 4;     // passes of a lane group over the producer's steps
 
-// Bin edges [lo, hi] (clamped into [a - 1 .. b + 1]) outside which an op's CDF
-// is the exact constant: 0 below lo, 1 above hi.  Widened by one step for the
-// rounding of the float bounds; a NaN mean gives [a, b].
 template <int FAM>
 __device__ __forceinline__ void spread(float mu, float rs, int a, int b, int &lo, int &hi) {
-    constexpr float kZF = fam_zflush<FAM>();
-    const float w = kZF / rs, c = mu - 0.5f;
-    float l = floorf(c - w) - 1.0f, h = ceilf(c + w) + 1.0f;
-    l = fminf(fmaxf(l, (float)a), (float)b + 1.0f);
-    h = fmaxf(fminf(h, (float)b), (float)a - 1.0f);
-    lo = (int)l;
-    hi = (int)h;
+    spread_z(fam_zflush<FAM>(), mu, rs, a, b, lo, hi);
 }
 
 // classes of an op in a step tile
@@ -423,16 +414,10 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
             flag = 1 + m;
             c = !act ? kConst : span <= kTinySpan ? kTiny : span <= kNarrowSpan ? kNarrow : kWide;
             if (c == kConst) {
+                // no records: every derivative is 0 here, and the readers skip
+                // this tile (tile_prod_rec / tile_cons_rec are false for it)
                 if (D - 1 >= t0 && D - 1 < tb) dep += m * (1 - Fc(D - 1 - s));
                 if (m == 0) dep = cnt = 0;
-                float *pp = W.ppart + (((size_t)b * N + i) * G.ntiles + tile) * kPP;
-                pp[0] = (float)dep; pp[1] = (float)cnt;
-                pp[2] = 0.0f; pp[3] = 0.0f; pp[4] = 0.0f; pp[5] = 0.0f;
-                for (int e = e0; e < e1; ++e) {
-                    if (poly_i && clsb[G.col[e]]) continue;
-                    *reinterpret_cast<float4 *>(W.cpart + (((size_t)b * G.E + e) * G.ntiles + tile) * kCP) =
-                        make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-                }
                 if (dep) atomicAdd(&sConst[0], dep);
                 if (cnt) atomicAdd(&sConst[1], cnt);
                 // P_i^0 = F_i(0), P_i^{D-1} = 1 - F_i(D-2): integers off the spread
