@@ -291,6 +291,9 @@ def main():
     ap.add_argument("--solve-check-every", type=int, default=0,
                     help="time the Alg. 1 driver (gaus_solve) with a legalization check every this many "
                          "iterations instead of plain steps + one legalization; 0 = off")
+    ap.add_argument("--kernel-timing-every", type=int, default=10,
+                    help="bracket the op and polynomial kernels of every n-th timed iteration with HIP events "
+                         "(each event adds a few microseconds between launches; 1 = every iteration)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the run, copy this many MiB once (counter calibration)")
     args = ap.parse_args()
@@ -348,7 +351,7 @@ def main():
     log(f"[bench] timing {args.steps} steps + 1 legalization")
     stream = torch.cuda.current_stream()
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-    ctx.kernel_timing(True)
+    ctx.kernel_timing(max(1, args.kernel_timing_every))
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     solve_stats = None
@@ -458,6 +461,7 @@ def main():
                    "state": "paper initialization" if args.sigma <= 0 else
                             f"paper initialization means, sigma = {args.sigma:g}"},
         "ms_per_iteration_events": step_ms_events, "legalize_ms": legalize_ms,
+        "kernel_timing_every": max(1, args.kernel_timing_every),
         "poly_path": dict(poly_cfg, ops=census["ops"], edges=census["edges"], grids=grids),
         "solve": solve_stats,
         "roofline": roofline,

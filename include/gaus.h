@@ -272,16 +272,20 @@ gaus_status gaus_get_usage(gaus_ctx *ctx, float *U);
  * gamma_mem > 0 (else INVALID_ARG).  Asynchronous. */
 gaus_status gaus_get_storage(gaus_ctx *ctx, float *M);
 
-/* Profiling hook.  While enabled, every launch of the two kernels that carry
- * the per-step work of an iteration -- [0] the step-by-step op kernel and
- * [1] the chunk-polynomial kernel (CDFs, masses, usage, edge terms and their
- * derivatives) -- is bracketed by a pair of HIP events recorded on the
- * context's stream.  Enabling or disabling discards pending events. */
+/* Profiling hook.  enable = n > 0: in every n-th iteration enqueued from now
+ * on (the first, the (n+1)-th, ...), the launches of the two kernels that
+ * carry the per-step work -- [0] the step-by-step op kernel and [1] the
+ * chunk-polynomial kernel (CDFs, masses, usage, edge terms and their
+ * derivatives) -- are bracketed by a pair of HIP events recorded on the
+ * context's stream (each recorded event adds a few microseconds between
+ * launches, so sampling keeps them out of the iterations' time); 0 = off;
+ * negative: INVALID_ARG.  Changing it discards pending events. */
 gaus_status gaus_kernel_timing(gaus_ctx *ctx, int32_t enable);
 
 /* Total duration in milliseconds of the bracketed launches of each of the two
  * kernels since timing was enabled or last read, and their numbers (HOST
- * outputs, [2] each).  Synchronizes the stream, then resets. */
+ * outputs, [2] each; only the sampled iterations count).  Synchronizes the
+ * stream, then resets. */
 gaus_status gaus_kernel_timing_read(gaus_ctx *ctx, double *total_ms, int32_t *launches);
 
 /* Wait for all work enqueued by this context; reports device errors. */

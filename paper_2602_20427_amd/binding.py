@@ -302,8 +302,10 @@ class Context:
         import torch
         self._check(load().gaus_get_storage(self._h, _dptr(M, torch.float32, (self.B, self.T), "M")))
 
-    def kernel_timing(self, enable: bool):
-        self._check(load().gaus_kernel_timing(self._h, 1 if enable else 0))
+    def kernel_timing(self, enable):
+        """False/0: off; True/1: bracket the op and polynomial kernels of every
+        iteration with HIP events; n > 1: of every n-th iteration."""
+        self._check(load().gaus_kernel_timing(self._h, int(enable)))
 
     def kernel_timing_read(self):
         """{kernel: (total milliseconds, launches)} for the step-by-step op

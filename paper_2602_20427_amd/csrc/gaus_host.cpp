@@ -39,15 +39,18 @@ struct gaus_ctx {
     bool bound = false;
     PolyArgs pa{};
     int poly_slots = 0;                 // per-work-group output slots of the polynomial kernels
-    // kernel timing (gaus_kernel_timing): per iteration two pairs of events,
-    // [4k, 4k+1] around the op kernel and [4k+2, 4k+3] around the polynomial kernel
+    // kernel timing (gaus_kernel_timing): per sampled iteration two pairs of
+    // events, [4k, 4k+1] around the op kernel and [4k+2, 4k+3] around the
+    // polynomial kernel; every timing_every-th iteration is sampled
     bool timing = false;
+    int timing_every = 1;
+    long long timing_iter = 0;          // iterations enqueued since timing was enabled
     std::vector<hipEvent_t> ev_pool;
     size_t ev_used = 0;                 // iterations recorded since the last read
 };
 
 constexpr int kPolySplitMax = 4;   // polynomial work-groups per op group, at most
-constexpr int kPackOpsPerWave = 16;// packed grids: ops per wave, at most (when the split allows)
+constexpr int kPackOpsPerWave = 8; // packed grids: ops per wave, at most (when the split allows)
 constexpr int kPackSplitMax = 16;  // packed grids: work-groups per op group, at most
 
 namespace {
@@ -78,7 +81,7 @@ void free_all(gaus_ctx *c) {
 // Timing events of the next iteration (nulls when timing is off).
 hipError_t next_events(gaus_ctx *c, IterArgs &a) {
     a.ops_begin = a.ops_end = a.poly_begin = a.poly_end = nullptr;
-    if (!c->timing) return hipSuccess;
+    if (!c->timing || c->timing_iter++ % c->timing_every != 0) return hipSuccess;
     while (4 * c->ev_used + 4 > c->ev_pool.size()) {
         hipEvent_t ev;
         hipError_t r = hipEventCreate(&ev);
@@ -316,6 +319,7 @@ gaus_status preprocess(const gaus_problem *p, HostGraph &h) {
                 h.pred_eid[q] = e; h.pred_src[q] = i;
             }
     }
+
     // back edges by consumer and by producer
     h.bin_ptr.assign(N + 1, 0); h.bout_ptr.assign(N + 1, 0);
     for (int e = 0; e < h.nb; ++e) { h.bin_ptr[h.bdst[e] + 1]++; h.bout_ptr[h.bsrc[e] + 1]++; }
@@ -681,13 +685,11 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     AL(rsig, BN);
     AL(dflag, BN);
     AL(ptier, BN);
-    AL(gflag, (size_t)B * g.ngroups);
-    AL(gnarrow, (size_t)B * g.ngroups);
+    AL(gbits, (size_t)B * g.ngroups);
     AL(gsum_ops, (size_t)B * g.ngroups * g.parts * ntiles * 2);
     AL(gsum_poly, (size_t)std::max(c->poly_slots, 1) * 2);
     AL(gsel, BN);
     AL(gtier, BN);
-    AL(gwork, (size_t)kGrids * B * g.ngroups);
     AL(vres_part, (size_t)B * h.K);
     AL(Ucoef_k, (size_t)B * h.K * kGrids * (kMaxChunks * kNC + kStripMax));
     AL(ppoly, BN * kPP);
@@ -704,7 +706,7 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
         if (e == hipSuccess) e = hipMemset(c->w.cls, 0, BN);
         if (e == hipSuccess) e = hipMemset(c->w.gsum_poly, 0, sizeof(float) * (size_t)std::max(c->poly_slots, 1) * 2);
         if (e == hipSuccess) e = hipMemset(c->w.gsel, kNoGrid, BN);
-        if (e == hipSuccess) e = hipMemset(c->w.gwork, 0, (size_t)kGrids * B * g.ngroups);
+        if (e == hipSuccess) e = hipMemset(c->w.gbits, 0, sizeof(unsigned) * (size_t)B * g.ngroups);
         if (e == hipSuccess) e = hipDeviceSynchronize();
         if (e != hipSuccess) { s = fail(nullptr, GAUS_E_DEVICE, "init: %s", hipGetErrorString(e)); goto fail_alloc; }
     }
@@ -936,7 +938,10 @@ gaus_status gaus_kernel_timing(gaus_ctx *ctx, int32_t enable) {
     if (!ctx) return GAUS_E_INVALID_ARG;
     hipError_t e = hipStreamSynchronize(ctx->stream);
     if (e != hipSuccess) return hip_fail(ctx, e, "kernel_timing");
+    if (enable < 0) return fail(ctx, GAUS_E_INVALID_ARG, "kernel_timing: enable < 0");
     ctx->timing = enable != 0;
+    ctx->timing_every = enable > 0 ? enable : 1;
+    ctx->timing_iter = 0;
     ctx->ev_used = 0;
     return GAUS_OK;
 }

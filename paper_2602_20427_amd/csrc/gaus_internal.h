@@ -52,6 +52,8 @@ constexpr float kMemRhoMax = 0.25f;
 constexpr int kGrids = 3;
 constexpr int kGridP[kGrids] = {1, 2, 4};
 constexpr unsigned char kNoGrid = 255;
+// bits of Work::gbits
+constexpr unsigned kGbStep = 1u, kGbNarrow = 2u, kGbGrid = 4u;
 
 struct GridArgs {
     int on;               // grid in use
@@ -161,17 +163,18 @@ struct Work {
     unsigned char *dflag;  // [B][N]        1 = op has step-by-step work (own terms or out-edges)
     unsigned char *ptier;  // [B][N]        polynomial op: tier of its vectors, the smallest over
                            //               itself and its polynomial consumers (highest degree)
-    int *gflag;       // [B][ngroups]      1 = some op of the group has step-by-step work
-    int *gnarrow;     // [B][ngroups]      1 = some op of the group takes polynomial degree 8 or 6
+    unsigned *gbits;  // [B][ngroups]      work of the group this iteration (k_gbits):
+                      //                   kGbStep = some op has step-by-step work,
+                      //                   kGbNarrow = some op takes polynomial degree 8 or 6,
+                      //                   kGbGrid << g = ops on grid g; only such groups'
+                      //                   polynomial work-groups write outputs (ppoly / cpoly
+                      //                   hold valid records for cls != 0 ops only: readers
+                      //                   check cls)
     float *gsum_ops;  // [B][ngroups][parts][ntiles][2]  V_dep, L_com of a k_ops work-group
     float *gsum_poly; // [slots][2]        V_dep, L_com of a k_poly work-group (GridArgs::slot_base)
     unsigned char *gsel;   // [B][N]        grid that evaluates the (restart, op) this iteration (0..2),
                            //               kNoGrid on the step-by-step path
     unsigned char *gtier;  // [B][N]        tier of its vectors on that grid (0 off the polynomial path)
-    unsigned char *gwork;  // [kGrids][B][ngroups]  1 = the group has ops on the grid; only such
-                           //               groups' polynomial work-groups write outputs
-                           //               (ppoly / cpoly hold valid records for cls != 0 ops
-                           //               only: readers check cls)
     float *vres_part; // [B][K]            V_res of one resource type
     float *Ucoef_k;   // [B][K][kGrids][64*kNC + 320]  polynomial usage coefficients and strip values per type
     float *ppoly;     // [B][N][kPP]       producer partials of the polynomial path

@@ -68,41 +68,38 @@ __device__ __forceinline__ int grid_tier(const GridArgs &gr, float s, int delay)
     return t;
 }
 
-// Classification and work flags.  Work-group = (op group, pack of kFlagPack
-// restarts), thread per (restart of the pack, op) (groups hold at most 256
-// ops, and together every op):
+// Classification and work flags.  Work-group = (64 consecutive ops, pack of
+// kFlagPack restarts), one wave per restart of the pack and thread per
+// (restart, op), so every per-op array is read and written in op order:
 //   * 1/sigma and the op's path (tier) for the other kernels;
 //   * step-by-step work of the op: its own path, or an out-edge to an op off
-//     the polynomial path; of the group: any such op;
+//     the polynomial path;
 //   * a polynomial producer's tier: the highest degree among itself and its
-//     polynomial consumers; of the group: whether the degree-8/6 kernel has
-//     work in it;
+//     polynomial consumers;
 //   * its grid: the coarsest packed grid whose whole restart pack (the
 //     restarts < B of [P floor(b/P), P floor(b/P) + P)) has the op and all
 //     its consumers reach the grid's degree-8 bound, with the pack's tier
 //     (the highest degree of its members'); else grid 0 with the op's own
-//     tier, or kNoGrid on the step-by-step path; per (grid, restart, group)
-//     whether any op is there.  Polynomial records (ppoly, cpoly) are
-//     written only for ops on a grid; every reader checks cls first.
+//     tier, or kNoGrid on the step-by-step path.  Polynomial records (ppoly,
+//     cpoly) are written only for ops on a grid; every reader checks cls.
+// The per-(restart, group) OR of these flags (gbits) follows in k_gbits.
 // The consumers' tiers are recomputed here from their sigmas.  With the
 // storage term on, also whether a holder's storage term is taken on the
 // chunk polynomials (Gaussian start times only; kMemPolyDeg, kMemRhoMax).
 constexpr int kFlagPack = 4;   // the largest restart pack of a grid
 static_assert(kGridP[kGrids - 1] == kFlagPack, "packs nest in the flag kernel's restarts");
 
-__global__ __launch_bounds__(256 * kFlagPack) void k_flags(Graph G, PolyArgs pa, const float *__restrict__ sigma,
-                                                           Work W, int mem_on) {
-    __shared__ unsigned char sTp[kFlagPack][kGrids][256];   // tier on each packed grid, 0 if not eligible
-    __shared__ int wor[256 * kFlagPack / 64];
-    const int grp = blockIdx.x, q = threadIdx.x >> 8, op = threadIdx.x & 255;
-    const int b = blockIdx.y * kFlagPack + q, lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-    const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
+__global__ __launch_bounds__(64 * kFlagPack) void k_flags(Graph G, PolyArgs pa, const float *__restrict__ sigma,
+                                                          Work W, int mem_on) {
+    __shared__ unsigned char sTp[kFlagPack][kGrids][64];   // tier on each packed grid, 0 if not eligible
+    const int q = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int i = blockIdx.x * 64 + lane;
+    const int b = blockIdx.y * kFlagPack + q;
     const int N = G.N, nb = min(kFlagPack, G.B - (int)blockIdx.y * kFlagPack);
-    const bool act = q < nb && q0 + op < q1;
-    int d = 0, narrow = 0, sel = -1, t = 0, ci = 0;
+    const bool act = q < nb && i < N;
+    int d = 0, t = 0, ci = 0;
     size_t bi = 0;
     if (act) {
-        const int i = G.perm[q0 + op];
         bi = (size_t)b * N + i;
         const float *sgb = sigma + (size_t)b * N;
         const float s = sgb[i];
@@ -135,12 +132,11 @@ __global__ __launch_bounds__(256 * kFlagPack) void k_flags(Graph G, PolyArgs pa,
             if (mem_on) rsum += 1.0f / sj;
         }
 #pragma unroll
-        for (int g = 1; g < kGrids; ++g) sTp[q][g][op] = (unsigned char)tp[g];
+        for (int g = 1; g < kGrids; ++g) sTp[q][g][lane] = (unsigned char)tp[g];
         W.dflag[bi] = (unsigned char)d;
         W.mpoly[bi] = (unsigned char)(mem_on && pa.fam == 0 && ci != 0 && d == 0 && e1 > e0 &&
                                       e1 - e0 <= kMemPolyDeg && pa.lam * rsum <= kMemRhoMax);
         W.ptier[bi] = (unsigned char)t;
-        narrow = (t == 1 || t == 2) ? 1 : 0;
     }
     __syncthreads();
     if (act) {   // grid: the coarsest packed grid whose pack qualifies
@@ -152,35 +148,38 @@ __global__ __launch_bounds__(256 * kFlagPack) void k_flags(Graph G, PolyArgs pa,
             int tt = kTiers;
             bool ok = true;
             for (int r = p0; r < p0 + P && r < nb; ++r) {
-                const int v = sTp[r][g][op];
+                const int v = sTp[r][g][lane];
                 ok = ok && v != 0;
                 tt = min(tt, v);
             }
             if (ok) { g_sel = g; tier = tt; }
         }
-        sel = g_sel;
         W.gsel[bi] = (unsigned char)g_sel;
         W.gtier[bi] = (unsigned char)(g_sel == kNoGrid ? 0 : tier);
     }
-    // per restart of the pack (256 threads = 4 waves each): OR of the flags,
-    // bit 0 step-by-step work, bit 1 degree 8/6, bit 2+g ops on grid g
-    int bits = (d ? 1 : 0) | (narrow ? 2 : 0);
-#pragma unroll
-    for (int g = 0; g < kGrids; ++g) bits |= sel == g ? 4 << g : 0;
-    int wbits = 0;
-#pragma unroll
-    for (int k = 0; k < 2 + kGrids; ++k) wbits |= __any((bits >> k) & 1) ? 1 << k : 0;
-    if (lane == 0) wor[wid] = wbits;
-    __syncthreads();
-    const int r = wor[q * 4] | wor[q * 4 + 1] | wor[q * 4 + 2] | wor[q * 4 + 3];
-    if (op == 0 && q < nb) {
-        const size_t bg = (size_t)b * G.ngroups + grp;
-        W.gflag[bg] = (r & 1) ? 1 : 0;
-        W.gnarrow[bg] = (r & 2) ? 1 : 0;
-#pragma unroll
-        for (int g = 0; g < kGrids; ++g)
-            W.gwork[((size_t)g * G.B + b) * G.ngroups + grp] = (unsigned char)((r >> (2 + g)) & 1);
+}
+
+// Work bits of each (restart, group): the OR over its ops of kGbStep (step-by-
+// step work), kGbNarrow (degree 8 or 6) and kGbGrid << grid.  Work-group =
+// (group, restart), thread per op; one plain store per (restart, group).
+__global__ __launch_bounds__(256) void k_gbits(Graph G, Work W) {
+    __shared__ unsigned sW[4];
+    const int grp = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid & 63;
+    const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
+    unsigned bits = 0u;
+    for (int q = q0 + tid; q < q1; q += 256) {
+        const size_t bi = (size_t)b * G.N + G.perm[q];
+        const int t = W.ptier[bi], gs = W.gsel[bi];
+        bits |= W.dflag[bi] ? kGbStep : 0u;
+        bits |= (t == 1 || t == 2) ? kGbNarrow : 0u;
+        bits |= gs < kGrids ? kGbGrid << gs : 0u;
     }
+    unsigned v = 0u;
+#pragma unroll
+    for (int k = 0; k < 2 + kGrids; ++k) v |= __ballot((bits >> k) & 1u) ? 1u << k : 0u;
+    if (lane == 0) sW[tid >> 6] = v;
+    __syncthreads();
+    if (tid == 0) W.gbits[(size_t)b * G.ngroups + grp] = (sW[0] | sW[1]) | (sW[2] | sW[3]);
 }
 
 // ---------------------------------------------------------------------------
@@ -208,12 +207,14 @@ __global__ __launch_bounds__(64 * kUcoefRows) void k_ucoef(Graph G, PolyArgs pa,
     const size_t rb = (size_t)gd.slot_base + (size_t)b * G.ngroups * split;
     // the type's groups with ops on the grid, compacted in order (their
     // work-groups wrote every slot; the others wrote nothing)
-    const unsigned char *work = W.gwork + ((size_t)gi * G.B + b) * G.ngroups;
+    const unsigned *gb = W.gbits + (size_t)b * G.ngroups;
+    const unsigned gmask = kGbGrid << gi;
+    auto work = [&](int q) { return (gb[q] & gmask) != 0u; };
     const int t0 = G.type_grp[k], t1 = G.type_grp[k + 1];
     float acc = 0.0f;
     if (t1 - t0 <= 64 * kUcoefRows) {
         const int q = t0 + (int)threadIdx.x;
-        const bool f = q < t1 && work[q];
+        const bool f = q < t1 && work(q);
         const unsigned long long bal = __ballot(f);
         if (tx == 0) wcnt[ty] = __popcll(bal);
         __syncthreads();
@@ -229,10 +230,10 @@ __global__ __launch_bounds__(64 * kUcoefRows) void k_ucoef(Graph G, PolyArgs pa,
                 sSlot[q2] = sGrp[q2 / split] * split + q2 % split;
             __syncthreads();
             if (x < ncoef) {
-#pragma unroll 4
+#pragma unroll 8
                 for (int q2 = ty; q2 < nsl; q2 += kUcoefRows) acc += W.Ucoef[(rb + sSlot[q2]) * kMaxChunks * kNC + x];
             } else if (x < nent) {
-#pragma unroll 4
+#pragma unroll 8
                 for (int q2 = ty; q2 < nsl; q2 += kUcoefRows) acc += W.Ustrip[(rb + sSlot[q2]) * kStripMax + (x - ncoef)];
             }
         } else {
@@ -247,7 +248,7 @@ __global__ __launch_bounds__(64 * kUcoefRows) void k_ucoef(Graph G, PolyArgs pa,
         }
     } else {   // more groups than one pass lists: test each
         for (int g = t0 + ty; g < t1; g += kUcoefRows) {
-            if (!work[g]) continue;
+            if (!work(g)) continue;
             const size_t s0 = rb + (size_t)g * split;
             if (x < ncoef) {
                 for (int u = 0; u < split; ++u) acc += W.Ucoef[(s0 + u) * kMaxChunks * kNC + x];
@@ -288,7 +289,7 @@ __global__ __launch_bounds__(kUsageBS) void k_usage(Graph G, PolyArgs pa, Work W
     __syncthreads();
     for (int c0 = g0; c0 < g1; c0 += kUsageBS) {
         const int g = c0 + tid;
-        const bool f = g < g1 && W.gflag[(size_t)b * G.ngroups + g] != 0;
+        const bool f = g < g1 && (W.gbits[(size_t)b * G.ngroups + g] & kGbStep) != 0u;
         const unsigned long long bal = __ballot(f);
         const int before = __popcll(bal & ((1ull << lane) - 1ull));
         if (lane == 0) wcount[wid] = __popcll(bal);
@@ -339,7 +340,7 @@ __global__ __launch_bounds__(kUsageBS) void k_usage(Graph G, PolyArgs pa, Work W
                     rows += W.Upart[(((size_t)b * G.ngroups + sAct[r / P]) * P + r % P) * D + t];
             } else if (ry == 0) {
                 for (int g = g0; g < g1; ++g)
-                    if (W.gflag[(size_t)b * G.ngroups + g])
+                    if (W.gbits[(size_t)b * G.ngroups + g] & kGbStep)
                         for (int pt = 0; pt < P; ++pt) rows += W.Upart[(((size_t)b * G.ngroups + g) * P + pt) * D + t];
             }
         }
@@ -571,15 +572,15 @@ __global__ __launch_bounds__(kCombineBS) void k_combine(Graph G, PolyArgs pa, Wo
         const GridArgs &gd = pa.gr[gi];
         if (!gd.on) continue;
         const int npoly = G.ngroups * gd.split;
-        const unsigned char *work = W.gwork + ((size_t)gi * G.B + b) * G.ngroups;
+        const unsigned *gb = W.gbits + (size_t)b * G.ngroups;
         for (int g = tid; g < npoly; g += kCombineBS) {
-            if (!work[g / gd.split]) continue;
+            if (!(gb[g / gd.split] & (kGbGrid << gi))) continue;
             const size_t sl = (size_t)gd.slot_base + (size_t)b * npoly + g;
             vdep += W.gsum_poly[sl * 2]; lcom += W.gsum_poly[sl * 2 + 1];
         }
     }
     for (int g = tid; g < G.ngroups; g += kCombineBS) {
-        if (W.gflag[(size_t)b * G.ngroups + g]) {
+        if (W.gbits[(size_t)b * G.ngroups + g] & kGbStep) {
             const float *go = W.gsum_ops + ((size_t)b * G.ngroups + g) * G.parts * G.ntiles * 2;
             for (int tl = 0; tl < G.parts * G.ntiles; ++tl) { vdep += go[2 * tl]; lcom += go[2 * tl + 1]; }
         }
@@ -709,8 +710,11 @@ __global__ __launch_bounds__(256) void k_final(Graph G, Work W, HP hp, const flo
                                                const float *sigma, float *gmu,
                                                float *gsig, float *mu_io, float *sig_io, float *am,
                                                float *av, int *adam_t, int mode) {
-    const int b = blockIdx.y;
-    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    // work-group x serves restart x mod B: work-groups are dealt to the 8 XCDs
+    // in turn, so with B a multiple of 8 each restart's records (gathered at
+    // random through the in-edges) stay in one XCD's L2
+    const int b = blockIdx.x % G.B;
+    const int i = (blockIdx.x / G.B) * blockDim.x + threadIdx.x;
     if (i >= G.N) return;
     const int N = G.N, nt = G.ntiles;
     const size_t bi = (size_t)b * N + i;
@@ -1594,8 +1598,9 @@ hipError_t enqueue_check(const Graph &g, const Work &w, const HP &hp, float *mu,
 // ---------------------------------------------------------------------------
 hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const LaunchCfg &lc,
                              const PolyArgs &pa, const IterArgs &a, hipStream_t st) {
-    hipLaunchKernelGGL(k_flags, dim3(g.ngroups, (g.B + kFlagPack - 1) / kFlagPack), dim3(256 * kFlagPack), 0, st,
+    hipLaunchKernelGGL(k_flags, dim3((g.N + 63) / 64, (g.B + kFlagPack - 1) / kFlagPack), dim3(64 * kFlagPack), 0, st,
                        g, pa, a.sigma, w, (hp.gamma != 0.0f && pa.enabled) ? 1 : 0);
+    hipLaunchKernelGGL(k_gbits, dim3(g.ngroups, g.B), dim3(256), 0, st, g, w);
     hipError_t e;
     if (a.ops_begin) (void)hipEventRecord(a.ops_begin, st);
     if ((e = launch_ops(g, w, lc, a.mu, a.sigma, st)) != hipSuccess) return e;
@@ -1644,7 +1649,7 @@ hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const 
     }
     if (g.nbig > 0) hipLaunchKernelGGL(k_gather_big, dim3(g.nbig, g.B), dim3(256), 0, st, g, w, hp, a.mu);
     {
-        dim3 grid((g.N + 255) / 256, g.B);
+        dim3 grid((unsigned)(((g.N + 255) / 256) * g.B));
         hipLaunchKernelGGL(k_final, grid, dim3(256), 0, st, g, w, hp, a.mu, a.sigma, a.gmu, a.gsig,
                            a.mu_io, a.sig_io, a.m, a.v, a.adam_t, a.mode);
     }

@@ -73,11 +73,11 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
     const int grp = blockIdx.x / split, sub = blockIdx.x - grp * split;
     const int N = G.N, D = G.D, B = G.B;
     if constexpr (TIERS == kPolyNarrow) {   // no op of the group takes degree 8 or 6
-        if (!W.gnarrow[(size_t)blockIdx.y * G.ngroups + grp]) return;
+        if (!(W.gbits[(size_t)blockIdx.y * G.ngroups + grp] & kGbNarrow)) return;
     }
     // no op of the group on this grid (in every restart of the pack): nothing
     // to write, the readers skip the group
-    if (!W.gwork[((size_t)GI * B + blockIdx.y * P) * G.ngroups + grp]) return;
+    if (!(W.gbits[(size_t)blockIdx.y * P * G.ngroups + grp] & (kGbGrid << GI))) return;
     // dynamic LDS: per (wave, restart) 6 rows of SP strip values and 3 rows of
     // SP + kStripExtra raw CDF values, then per (wave, restart) SP strip usages
     extern __shared__ float sDyn[];

@@ -322,7 +322,7 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
     // them (group and op flags).  Otherwise thread t looks at op q0 + t*parts
     // (groups hold at most as many ops as the work-group has threads); ops and
     // edges on the chunk-polynomial path are left to k_poly.
-    if (!W.gflag[(size_t)b * G.ngroups + grp]) return;
+    if (!(W.gbits[(size_t)b * G.ngroups + grp] & kGbStep)) return;
     // Each op is sorted for this tile by its thread: nothing to do (no
     // step-by-step work), constant (every spread misses the tile: its terms
     // are integer counts, finished here), tiny or narrow (lane groups, below)
