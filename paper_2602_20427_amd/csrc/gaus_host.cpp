@@ -508,6 +508,9 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     g.N = h.N; g.E = h.E; g.K = h.K; g.D = h.D; g.II = h.II; g.T = h.II > 0 ? h.II : h.D;
     g.nb = h.nb; g.B = B; g.tile = tile; g.ntiles = ntiles;
     g.ngroups = (int)h.grp_start.size() - 1;
+    // the narrow kernel pays off where the op kernel would visit each op in
+    // several tiles; its usage row must fit LDS
+    g.nar_on = (ntiles > 1 && h.D <= kNarMaxD) ? 1 : 0;
     {
         // a small op-kernel grid (few tiles) over many ops leaves the last round
         // of work-groups mostly idle: split each (group, tile) over up to 4
@@ -686,6 +689,9 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     AL(dflag, BN);
     AL(ptier, BN);
     AL(gbits, (size_t)B * g.ngroups);
+    AL(gnar, (size_t)B * g.ngroups);
+    AL(Unar, g.nar_on ? (size_t)B * g.ngroups * h.D : 1);
+    AL(gsum_nar, (size_t)B * g.ngroups * 2);
     AL(gsum_ops, (size_t)B * g.ngroups * g.parts * ntiles * 2);
     AL(gsum_poly, (size_t)std::max(c->poly_slots, 1) * 2);
     AL(gsel, BN);

@@ -276,36 +276,46 @@ template <int RP>   // threads per slot, each summing every RP-th step-by-step r
 __global__ __launch_bounds__(kUsageBS) void k_usage(Graph G, PolyArgs pa, Work W) {
     constexpr int kMaxAct = 1024;
     __shared__ float sC[kGrids][kUcEntries];
-    __shared__ int sAct[kMaxAct];
-    __shared__ int wcount[kUsageBS / 64];
-    __shared__ int base;
+    __shared__ int sAct[kMaxAct], sActN[kMaxAct];
+    __shared__ int wcount[2][kUsageBS / 64];
+    __shared__ int base[2];
     const int k = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
     const int lane = tid & 63, wid = tid >> 6;
     const int g0 = G.type_grp[k], g1 = G.type_grp[k + 1];
     const int D = G.D, T = G.T;
 
-    // the type's groups with step-by-step partials, compacted in order
-    if (tid == 0) base = 0;
+    // the type's groups with step-by-step partials of the op kernel (sAct) and
+    // of the narrow kernel (sActN), compacted in order
+    auto has_rows = [&](int g, int which) {
+        const size_t bg = (size_t)b * G.ngroups + g;
+        if (!(W.gbits[bg] & kGbStep)) return false;
+        if (!G.nar_on) return which == 0;
+        return (W.gnar[bg] & (which == 0 ? kNarLeft : kNarTaken)) != 0u;
+    };
+    if (tid < 2) base[tid] = 0;
     __syncthreads();
     for (int c0 = g0; c0 < g1; c0 += kUsageBS) {
         const int g = c0 + tid;
-        const bool f = g < g1 && (W.gbits[(size_t)b * G.ngroups + g] & kGbStep) != 0u;
-        const unsigned long long bal = __ballot(f);
-        const int before = __popcll(bal & ((1ull << lane) - 1ull));
-        if (lane == 0) wcount[wid] = __popcll(bal);
-        __syncthreads();
-        int off = base;
-        for (int w = 0; w < wid; ++w) off += wcount[w];
-        if (f && off + before < kMaxAct) sAct[off + before] = g;
-        __syncthreads();
-        if (tid == 0) {
-            int tot = 0;
-            for (int w = 0; w < kUsageBS / 64; ++w) tot += wcount[w];
-            base += tot;
+#pragma unroll
+        for (int which = 0; which < 2; ++which) {
+            const bool f = g < g1 && has_rows(g, which);
+            const unsigned long long bal = __ballot(f);
+            const int before = __popcll(bal & ((1ull << lane) - 1ull));
+            if (lane == 0) wcount[which][wid] = __popcll(bal);
+            __syncthreads();
+            int off = base[which];
+            for (int w = 0; w < wid; ++w) off += wcount[which][w];
+            if (f && off + before < kMaxAct) (which == 0 ? sAct : sActN)[off + before] = g;
+            __syncthreads();
+            if (tid == 0) {
+                int tot = 0;
+                for (int w = 0; w < kUsageBS / 64; ++w) tot += wcount[which][w];
+                base[which] += tot;
+            }
+            __syncthreads();
         }
-        __syncthreads();
     }
-    const int nact = base;   // > kMaxAct: scan the flags instead of the list
+    const int nact = base[0], nactN = base[1];   // > kMaxAct: scan the flags instead of the list
     for (int gi = 0; gi < kGrids; ++gi) {
         const GridArgs &gd = pa.gr[gi];
         if (!gd.on) continue;
@@ -340,8 +350,25 @@ __global__ __launch_bounds__(kUsageBS) void k_usage(Graph G, PolyArgs pa, Work W
                     rows += W.Upart[(((size_t)b * G.ngroups + sAct[r / P]) * P + r % P) * D + t];
             } else if (ry == 0) {
                 for (int g = g0; g < g1; ++g)
-                    if (W.gbits[(size_t)b * G.ngroups + g] & kGbStep)
+                    if (has_rows(g, 0))
                         for (int pt = 0; pt < P; ++pt) rows += W.Upart[(((size_t)b * G.ngroups + g) * P + pt) * D + t];
+            }
+            // the narrow kernel's rows (one per group), eight loads in flight
+            // (the sum order stays the row order)
+            if (nactN <= kMaxAct) {
+                const float *nb = W.Unar + (size_t)b * G.ngroups * D + t;
+                int r = ry;
+                for (; r + 7 * RP < nactN; r += 8 * RP) {
+                    float u8[8];
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) u8[k] = nb[(size_t)sActN[r + k * RP] * D];
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) rows += u8[k];
+                }
+                for (; r < nactN; r += RP) rows += nb[(size_t)sActN[r] * D];
+            } else if (ry == 0) {
+                for (int g = g0; g < g1; ++g)
+                    if (has_rows(g, 1)) rows += W.Unar[((size_t)b * G.ngroups + g) * D + t];
             }
         }
     }
@@ -580,10 +607,14 @@ __global__ __launch_bounds__(kCombineBS) void k_combine(Graph G, PolyArgs pa, Wo
         }
     }
     for (int g = tid; g < G.ngroups; g += kCombineBS) {
-        if (W.gbits[(size_t)b * G.ngroups + g] & kGbStep) {
-            const float *go = W.gsum_ops + ((size_t)b * G.ngroups + g) * G.parts * G.ntiles * 2;
+        const size_t bg = (size_t)b * G.ngroups + g;
+        if (!(W.gbits[bg] & kGbStep)) continue;
+        const unsigned nar = G.nar_on ? W.gnar[bg] : kNarLeft;
+        if (nar & kNarLeft) {
+            const float *go = W.gsum_ops + bg * G.parts * G.ntiles * 2;
             for (int tl = 0; tl < G.parts * G.ntiles; ++tl) { vdep += go[2 * tl]; lcom += go[2 * tl + 1]; }
         }
+        if (nar & kNarTaken) { vdep += W.gsum_nar[bg * 2]; lcom += W.gsum_nar[bg * 2 + 1]; }
     }
     const size_t nbp = (size_t)G.nb * G.ntiles;
     const float *bp = W.bpart + (size_t)b * nbp * kBP;
@@ -667,7 +698,8 @@ __global__ __launch_bounds__(256) void k_gather_big(Graph G, Work W, HP hp, cons
     double acc[6] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
     for (int q = G.pred_ptr[i] + tid; q < G.pred_ptr[i + 1]; q += 256) {
         const int e = G.pred_eid[q];
-        if (poly_i && W.cls[(size_t)b * N + G.pred_src[q]]) {
+        const size_t bs = (size_t)b * N + G.pred_src[q];
+        if ((poly_i && W.cls[bs]) || W.dflag[bs] == 2) {   // single record of the edge
             const float *cp = W.cpoly + ((size_t)b * G.E + e) * kCP;
             for (int c = 0; c < 4; ++c) acc[c] += cp[c];
         } else {
@@ -755,7 +787,8 @@ __global__ __launch_bounds__(256) void k_final(Graph G, Work W, HP hp, const flo
         return tile_cons_rec(kZF, m_i, rs, t0, min(t0 + G.tile, G.D));
     };
     double dm = 0.0, ds = 0.0, cm = 0.0, cs = 0.0;
-    if (W.dflag[bi]) {
+    const int dfl = W.dflag[bi];   // 1: op-kernel records per tile, 2: narrow kernel's single record
+    if (dfl == 1) {
         const float *pp = W.ppart + bi * nt * kPP;
         const int lat_i = G.delay[i];
         for (int tl = 0; tl < nt; ++tl) {
@@ -766,7 +799,7 @@ __global__ __launch_bounds__(256) void k_final(Graph G, Work W, HP hp, const flo
         }
     }
     const bool poly_i = W.cls[bi] != 0;
-    if (poly_i) {   // producer records of the polynomial path (written for its ops only)
+    if (poly_i || dfl == 2) {   // single producer record (polynomial path, or the narrow kernel)
         const float *ppy = W.ppoly + bi * kPP;
         dm += ppy[2]; ds += ppy[3]; cm += ppy[4]; cs += ppy[5];
     }
@@ -775,7 +808,8 @@ __global__ __launch_bounds__(256) void k_final(Graph G, Work W, HP hp, const flo
     if (bsum) { dm += bsum[0]; ds += bsum[1]; cm += bsum[2]; cs += bsum[3]; }
     for (int q = bsum ? G.pred_ptr[i + 1] : G.pred_ptr[i]; q < G.pred_ptr[i + 1]; ++q) {
         const int e = G.pred_eid[q];
-        if (poly_i && W.cls[(size_t)b * N + G.pred_src[q]]) {
+        const size_t bs = (size_t)b * N + G.pred_src[q];
+        if ((poly_i && W.cls[bs]) || W.dflag[bs] == 2) {   // single record of the edge
             const float *cp = W.cpoly + ((size_t)b * G.E + e) * kCP;
             dm += cp[0]; ds += cp[1]; cm += cp[2]; cs += cp[3];
             continue;
@@ -1603,6 +1637,7 @@ hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const 
     hipLaunchKernelGGL(k_gbits, dim3(g.ngroups, g.B), dim3(256), 0, st, g, w);
     hipError_t e;
     if (a.ops_begin) (void)hipEventRecord(a.ops_begin, st);
+    if (g.nar_on && (e = launch_narrow(g, w, lc, a.mu, st)) != hipSuccess) return e;
     if ((e = launch_ops(g, w, lc, a.mu, a.sigma, st)) != hipSuccess) return e;
     if (a.ops_end) (void)hipEventRecord(a.ops_end, st);
     if (pa.enabled) {

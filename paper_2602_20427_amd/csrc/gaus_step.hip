@@ -72,15 +72,31 @@ __device__ __forceinline__ float uniformf(float x) {
 
 // Narrow ops of class `want` from the group's list, NP at a time by each wave,
 // one op per lane group of 64/NP lanes (the loads of the ops and their
-// consumers overlap; loops run to the lane groups' maximum).  The wave's
-// usage goes to sU (its own LDS row), its V_dep and L_com to g0 and g1 of the
-// lanes 0 and 2 of each lane group.
-template <int FAM, int NP, int BS>
+// consumers overlap; loops run to the lane groups' maximum).  Its V_dep and
+// L_com go to g0 and g1 of the lanes 0 and 2 of each lane group.
+// In a step tile of the op kernel (ONE = false): the wave's usage goes to sU
+// (its own LDS row of the tile), the records to the per-tile ppart / cpart.
+// Over the whole horizon (ONE = true, k_narrow): the usage goes to sU64, one
+// row of the work-group in fixed point (2^-40 units, integer LDS atomics:
+// the sum does not depend on the order), the records to the single ppoly /
+// cpoly slots of the op and its edges.
+constexpr float kUsageFix = 1099511627776.0f;   // 2^40
+
+// Maximum over the wave of a value that is the same on every lane of each
+// lane group of 64/NP lanes: one read per lane group, no cross-lane traffic.
+template <int NP>
+__device__ __forceinline__ int group_max(int v) {
+    int m = __builtin_amdgcn_readlane(v, 0);
+#pragma unroll
+    for (int k = 1; k < NP; ++k) m = max(m, __builtin_amdgcn_readlane(v, k * (64 / NP)));
+    return m;
+}
+template <int FAM, int NP, int BS, bool ONE = false>
 __device__ __forceinline__ void narrow_ops(const Graph &G, const Work &W, const float *__restrict__ mub,
                                            const float *__restrict__ rsb, const unsigned char *__restrict__ clsb,
                                            const OpStage &st, const unsigned char *sCls, const int *sDirect,
-                                           float *sU, unsigned char want, int nq, int t0, int tb, int tile, int b,
-                                           float &g0, float &g1) {
+                                           float *sU, long long *sU64, unsigned char want, int nq, int t0, int tb,
+                                           int tile, int b, float &g0, float &g1) {
     constexpr int NW = BS / 64, GL = 64 / NP;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int grl = lane / GL, gl = lane % GL;   // lane group, lane in the group
@@ -127,7 +143,7 @@ __device__ __forceinline__ void narrow_ops(const Graph &G, const Work &W, const 
 
             // usage: P_i^u = F_i(u) - F_i(u-1) is 0 off X1 but at u = 0 and D-1
             const int nu = (ok && !poly_i) ? n1 + 2 : 0;
-            const int nu_max = (int)wave_max((float)nu);
+            const int nu_max = group_max<NP>(nu);
             for (int x0 = 0; x0 < nu_max; x0 += GL) {
                 const int xx = x0 + gl;
                 int u = x1l + xx;
@@ -137,12 +153,18 @@ __device__ __forceinline__ void narrow_ops(const Graph &G, const Work &W, const 
                     take = u >= t0 && u < tb && !(u >= x1l && u <= x1h) && !(xx > n1 && u == 0);
                 }
                 const float P = take ? st_mass(st_at<FAM>(u - 1, D, m_i, rs), st_at<FAM>(u, D, m_i, rs)) : 0.0f;
-                // lane groups may share a step: their additions go one group
-                // at a time (kept apart by the compiler barriers)
+                if constexpr (ONE) {
+                    if (take)
+                        atomicAdd(reinterpret_cast<unsigned long long *>(sU64 + u),
+                                  (unsigned long long)__float2ll_rn(P * kUsageFix));
+                } else {
+                    // lane groups may share a step: their additions go one
+                    // group at a time (kept apart by the compiler barriers)
 #pragma unroll
-                for (int k = 0; k < NP; ++k) {
-                    if (take && grl == k) sU[u - t0] += P;
-                    asm volatile("" ::: "memory");
+                    for (int k = 0; k < NP; ++k) {
+                        if (take && grl == k) sU[u - t0] += P;
+                        asm volatile("" ::: "memory");
+                    }
                 }
             }
 
@@ -155,7 +177,7 @@ __device__ __forceinline__ void narrow_ops(const Graph &G, const Work &W, const 
             constexpr int R = kNarrowPass;
             static_assert(R * GL >= 2 * (NP == 1 ? kNarrowSpan : kTinySpan), "passes cover X1 and X2");
             const int n12 = n1 + n2;
-            const int n12_max = (int)wave_max((float)n12);
+            const int n12_max = group_max<NP>(n12);
             float cSt[R], cFm[R], cFs[R], cA[R], cFms[R], cFss[R];
             int cu[R];
             bool cin2[R];
@@ -183,7 +205,7 @@ __device__ __forceinline__ void narrow_ops(const Graph &G, const Work &W, const 
             float pr[6] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
             int cnt = 0;   // steps between the spreads, summed over the edges
             const int deg = ok ? e1 - e0 : 0;
-            const int deg_max = (int)wave_max((float)deg);
+            const int deg_max = group_max<NP>(deg);
             for (int t = 0; t < deg_max; ++t) {
                 const int e = e0 + t;
                 bool ev = t < deg;
@@ -201,6 +223,10 @@ __device__ __forceinline__ void narrow_ops(const Graph &G, const Work &W, const 
                 spread<FAM>(m_j, rsj, t0 - 1, tb, cl, ch);
                 const int x3l = max(cl, t0), x3h = min(ch + 1, tb - 1);
                 const int n3 = max(x3h - x3l + 1, 0);
+                // off X3 the consumer's CDF is the exact constant cdf_at returns
+                // there (0 below its spread, 1 above it and at D-1; zero
+                // derivatives), so only steps of X3 evaluate it
+                auto Fcj = [&](int v) { return v < 0 ? 0 : (v >= D - 1 || v > ch) ? 1 : 0; };
                 // F_i(u) (1 - F_j(u)) = 1 on [r0, r1) off the evaluated steps
                 const int r0 = max(t0, ph + 1), r1 = min(min(tb, D - 1), cl);
                 if (ev) cnt += max(r1 - r0, 0);
@@ -211,10 +237,12 @@ __device__ __forceinline__ void narrow_ops(const Graph &G, const Work &W, const 
                     if (r * GL >= n12_max) break;
                     const int u = cu[r];
                     if (!ev || u < 0) continue;
-                    float st_j, Fmj, Fsj;
-                    cdf_at<FAM>(u, D, m_j, rsj, cj, st_j, Fmj, Fsj);
+                    const bool vary = u >= x3l && u <= x3h;
+                    float st_j = Fcj(u) ? -0.0f : 0.0f, Fmj = 0.0f, Fsj = 0.0f;
+                    if (vary) cdf_at<FAM>(u, D, m_j, rsj, cj, st_j, Fmj, Fsj);
                     if (cin2[r]) {
-                        const float dS = st_mass(st_at<FAM>(u - 1, D, m_j, rsj), st_j);
+                        const float dS = vary ? st_mass(st_at<FAM>(u - 1, D, m_j, rsj), st_j)
+                                              : (float)(Fcj(u) - Fcj(u - 1));
                         pr[2] = fmaf(-cFms[r], dS, pr[2]);
                         pr[3] = fmaf(-cFss[r], dS, pr[3]);
                     }
@@ -235,7 +263,7 @@ __device__ __forceinline__ void narrow_ops(const Graph &G, const Work &W, const 
                 // X3 \ (X1 u X2), then the steps 0, s-1, D-2, D-1 off all three:
                 // F_i is constant there (no producer derivatives)
                 const int ntot = ev ? n3 + 4 : 0;
-                const int ntot_max = (int)wave_max((float)ntot);
+                const int ntot_max = group_max<NP>(ntot);
                 for (int x0 = 0; x0 < ntot_max; x0 += GL) {
                     const int xx = x0 + gl;
                     int u;
@@ -251,8 +279,8 @@ __device__ __forceinline__ void narrow_ops(const Graph &G, const Work &W, const 
                                !(k == 3 && u == D - 2);
                     }
                     if (!take) continue;
-                    float st_j, Fmj, Fsj;
-                    cdf_at<FAM>(u, D, m_j, rsj, cj, st_j, Fmj, Fsj);
+                    float st_j = Fcj(u) ? -0.0f : 0.0f, Fmj = 0.0f, Fsj = 0.0f;   // the four steps: off X3
+                    if (xx < n3) cdf_at<FAM>(u, D, m_j, rsj, cj, st_j, Fmj, Fsj);
                     if (u < D - 1) {
                         const float Fi = (float)Fc(u), A = (float)(Fc(u - s + 1) - Fc(u - s));
                         const float Rj = st_1mF(st_j);
@@ -267,13 +295,17 @@ __device__ __forceinline__ void narrow_ops(const Graph &G, const Work &W, const 
                     }
                 }
                 const float r = group_sum4<NP>(c4[0], c4[1], c4[2], c4[3], lane);
-                if (ev && gl < 4) W.cpart[(((size_t)b * G.E + e) * G.ntiles + tile) * kCP + wave4_comp(gl)] = r;
+                if (ev && gl < 4) {
+                    if constexpr (ONE) W.cpoly[((size_t)b * G.E + e) * kCP + wave4_comp(gl)] = r;
+                    else W.cpart[(((size_t)b * G.E + e) * G.ntiles + tile) * kCP + wave4_comp(gl)] = r;
+                }
             }
             if (gl == 0) pr[1] += (float)cnt;
             const float ra = group_sum4<NP>(pr[0], pr[1], pr[2], pr[3], lane);
             const float rb = group_sum2<NP>(pr[4], pr[5], lane);
             if (ok) {
-                float *pp = W.ppart + (((size_t)b * N + i) * G.ntiles + tile) * kPP;
+                float *pp = ONE ? W.ppoly + ((size_t)b * N + i) * kPP
+                                : W.ppart + (((size_t)b * N + i) * G.ntiles + tile) * kPP;
                 if (gl < 4) pp[wave4_comp(gl)] = m > 0 ? ra : 0.0f;
                 if (gl < 2) pp[4 + gl] = m > 0 ? rb : 0.0f;
                 if (m > 0 && gl == 0) g0 += ra;   // V_dep (component 0 at lane 0 of the group)
@@ -323,6 +355,8 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
     // (groups hold at most as many ops as the work-group has threads); ops and
     // edges on the chunk-polynomial path are left to k_poly.
     if (!(W.gbits[(size_t)b * G.ngroups + grp] & kGbStep)) return;
+    // with the narrow kernel on, only the ops it left (step-by-step flag 1)
+    if (G.nar_on && !(W.gnar[(size_t)b * G.ngroups + grp] & kNarLeft)) return;
     // Each op is sorted for this tile by its thread: nothing to do (no
     // step-by-step work), constant (every spread misses the tile: its terms
     // are integer counts, finished here), tiny or narrow (lane groups, below)
@@ -344,7 +378,7 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
         bool poly_i = false, on = false;
         if (tid < nq) {
             i = G.perm[q0 + tid * G.parts];
-            on = W.dflag[(size_t)b * N + i] != 0;
+            on = W.dflag[(size_t)b * N + i] == 1;
             if (on) {
                 e0 = G.row_ptr[i]; deg = G.row_ptr[i + 1] - e0;
                 poly_i = clsb[i] != 0;
@@ -440,8 +474,10 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
         float *sU = sBuf + w * TILE;
         for (int p = lane; p < TILE; p += 64) sU[p] = 0.0f;
         float g0 = 0.0f, g1 = 0.0f;
-        narrow_ops<FAM, 4, BS>(G, W, mub, rsb, clsb, st, sCls, sDirect, sU, kTiny, nq, t0, tb, tile, b, g0, g1);
-        narrow_ops<FAM, 1, BS>(G, W, mub, rsb, clsb, st, sCls, sDirect, sU, kNarrow, nq, t0, tb, tile, b, g0, g1);
+        narrow_ops<FAM, 4, BS>(G, W, mub, rsb, clsb, st, sCls, sDirect, sU, nullptr, kTiny, nq, t0, tb, tile, b,
+                               g0, g1);
+        narrow_ops<FAM, 1, BS>(G, W, mub, rsb, clsb, st, sCls, sDirect, sU, nullptr, kNarrow, nq, t0, tb, tile, b,
+                               g0, g1);
         const float s0 = wave_sum((lane & 15) == 0 ? g0 : 0.0f), s1 = wave_sum((lane & 15) == 2 ? g1 : 0.0f);
         if (lane == 0) { sGw[w][0] = s0; sGw[w][1] = s1; }
     }
@@ -674,6 +710,123 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
     }
 }
 
+
+// ---------------------------------------------------------------------------
+// Narrow kernel: the step-by-step ops whose spreads are short, each taken once
+// over the whole horizon instead of once per step tile.  Work-group = (op
+// group, restart), thread per op for the sorting (the op kernel's spread tests
+// with one tile [0, D)): an op off the polynomial path whose own spreads and
+// whose consumers' spreads span at most kNarrowSpan steps is taken here (its
+// step-by-step flag becomes 2, and the op kernel leaves it); the others stay
+// with the op kernel.  The taken ops run through narrow_ops over the horizon:
+// usage into one fixed-point LDS row of D steps, records into the single
+// ppoly / cpoly slots (free for ops off the polynomial path), V_dep and L_com
+// per (restart, group).  gnar[b][group] tells the readers which parts exist.
+// ---------------------------------------------------------------------------
+template <int FAM>
+__global__ __launch_bounds__(kNarBS) void k_narrow(Graph G, const float *__restrict__ mu, Work W) {
+    constexpr int BS = kNarBS, NW = BS / 64;
+    extern __shared__ long long sRow[];   // [D] usage of the taken ops, 2^-40 units
+    __shared__ int sDirect[BS];
+    __shared__ unsigned char sCls[BS];
+    __shared__ int sOpI[BS], sOpE0[BS], sOpDeg[BS], sOpS[BS], sOpOff[BS], sWsum[NW];
+    __shared__ float sOpMu[BS], sOpRs[BS], sEmu[kStage], sErs[kStage];
+    __shared__ unsigned char sOpPoly[BS], sEon[kStage];
+    __shared__ int sAny[2];                // an op left to the op kernel / taken here
+    __shared__ float sGw[NW][2];
+    const OpStage st{sOpI, sOpE0, sOpDeg, sOpS, sOpOff, sOpMu, sOpRs, sOpPoly, sEmu, sErs, sEon};
+    const int grp = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+    const int lane = tid & 63, w = tid >> 6;
+    const int D = G.D, N = G.N;
+    const size_t bg = (size_t)b * G.ngroups + grp;
+    // no step-by-step work in the group: the readers skip it before reading gnar
+    if (!(W.gbits[bg] & kGbStep)) return;
+    const float *mub = mu + (size_t)b * N;
+    const float *rsb = W.rsig + (size_t)b * N;
+    const unsigned char *clsb = W.cls + (size_t)b * N;
+    const int q0 = G.grp_start[grp], nq = G.grp_start[grp + 1] - q0;
+    for (int u = tid; u < D; u += BS) sRow[u] = 0;
+    if (tid < 2) sAny[tid] = 0;
+    {
+        int i = 0, e0 = 0, deg = 0, s = 0;
+        float m_i = 0.0f, rs = 1.0f;
+        bool poly_i = false, on = false;
+        if (tid < nq) {
+            i = G.perm[q0 + tid];
+            on = W.dflag[(size_t)b * N + i] == 1;
+            if (on) {
+                e0 = G.row_ptr[i]; deg = G.row_ptr[i + 1] - e0;
+                poly_i = clsb[i] != 0;
+                s = G.delay[i];
+                m_i = mub[i]; rs = rsb[i];
+            }
+        }
+        // LDS offsets of the ops' edges: exclusive scan of the out-degrees
+        int x = deg;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int y = __shfl_up(x, o, 64);
+            if (lane >= o) x += y;
+        }
+        if (lane == 63) sWsum[w] = x;
+        __syncthreads();
+        int off = x - deg;
+        for (int k = 0; k < w; ++k) off += sWsum[k];
+        if (!on || off + deg > kStage) off = -1;
+        sOpI[tid] = i; sOpE0[tid] = e0; sOpDeg[tid] = deg; sOpS[tid] = s; sOpOff[tid] = off;
+        sOpMu[tid] = m_i; sOpRs[tid] = rs; sOpPoly[tid] = poly_i ? 1 : 0;
+        unsigned char c = kNone;
+        int flag = 0;
+        if (on) {
+            int pl, ph;   // F_i is read at the bin edges u - s .. u (u in [0, D))
+            spread<FAM>(m_i, rs, -s - 1, D, pl, ph);
+            const int n1 = min(ph + 1, D - 1) - max(pl, 0) + 1;
+            const int n2 = min(ph + s, D - 1) - max(pl + s - 1, 0) + 1;
+            int span = max(max(n1, n2), 0);
+            int m = 0;
+            for (int e = e0; e < e0 + deg; ++e) {
+                const int j = G.col[e];
+                const bool sbs = !(poly_i && clsb[j]);
+                float m_j = 0.0f, rsj = 1.0f;
+                if (sbs) { m_j = mub[j]; rsj = rsb[j]; }
+                if (off >= 0) {
+                    sEmu[off + e - e0] = m_j; sErs[off + e - e0] = rsj; sEon[off + e - e0] = sbs ? 1 : 0;
+                }
+                if (!sbs) continue;
+                ++m;
+                int cl, ch;
+                spread<FAM>(m_j, rsj, -1, D, cl, ch);
+                span = max(span, min(ch + 1, D - 1) - max(cl, 0) + 1);
+            }
+            flag = 1 + m;
+            const bool take = !poly_i && span <= kNarrowSpan;
+            c = take ? (span <= kTinySpan ? kTiny : kNarrow) : kNone;
+            if (take) W.dflag[(size_t)b * N + i] = 2;
+            sAny[take ? 1 : 0] = 1;
+        }
+        sDirect[tid] = flag;
+        sCls[tid] = c;
+    }
+    __syncthreads();
+    if (tid == 0) W.gnar[bg] = (sAny[0] ? kNarLeft : 0u) | (sAny[1] ? kNarTaken : 0u);
+    if (!sAny[1]) return;
+    float g0 = 0.0f, g1 = 0.0f;
+    narrow_ops<FAM, 4, BS, true>(G, W, mub, rsb, clsb, st, sCls, sDirect, nullptr, sRow, kTiny, nq, 0, D, 0, b,
+                                 g0, g1);
+    narrow_ops<FAM, 1, BS, true>(G, W, mub, rsb, clsb, st, sCls, sDirect, nullptr, sRow, kNarrow, nq, 0, D, 0, b,
+                                 g0, g1);
+    const float s0 = wave_sum((lane & 15) == 0 ? g0 : 0.0f), s1 = wave_sum((lane & 15) == 2 ? g1 : 0.0f);
+    if (lane == 0) { sGw[w][0] = s0; sGw[w][1] = s1; }
+    __syncthreads();
+    float *row = W.Unar + bg * D;
+    for (int u = tid; u < D; u += BS) row[u] = (float)((double)sRow[u] * (1.0 / 1099511627776.0));
+    if (tid < 2) {
+        float v = sGw[0][tid];
+#pragma unroll
+        for (int k = 1; k < NW; ++k) v += sGw[k][tid];
+        W.gsum_nar[bg * 2 + tid] = v;
+    }
+}
 
 // ---------------------------------------------------------------------------
 // Back-edge kernel (modulo scheduling).  Work-group = (back-edge block, tile,
@@ -977,6 +1130,19 @@ hipError_t launch_ops(const Graph &g, const Work &w, const LaunchCfg &lc, const 
         hipLaunchKernelGGL((k_ops<decltype(fam)::value, decltype(bs)::value, decltype(spt)::value>), grid,
                            dim3(decltype(bs)::value), 0, st, g, mu, sigma, w);
     });
+}
+
+hipError_t launch_narrow(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu, hipStream_t st) {
+    const dim3 grid(g.ngroups, g.B);
+    const size_t lds = sizeof(long long) * (size_t)g.D;
+    switch (lc.fam) {
+        case 0: hipLaunchKernelGGL(k_narrow<0>, grid, dim3(kNarBS), lds, st, g, mu, w); break;
+        case 1: hipLaunchKernelGGL(k_narrow<1>, grid, dim3(kNarBS), lds, st, g, mu, w); break;
+        case 2: hipLaunchKernelGGL(k_narrow<2>, grid, dim3(kNarBS), lds, st, g, mu, w); break;
+        case 3: hipLaunchKernelGGL(k_narrow<3>, grid, dim3(kNarBS), lds, st, g, mu, w); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
 }
 
 hipError_t launch_back(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu, const float *sigma,

@@ -109,6 +109,25 @@ def test_loss_grad_large_after_steps():
     _check(p, mu_h, sg_h, lam_h, hp, [0, 1, 2, B - 1], "large/after 20 steps")
 
 
+@pytest.mark.parametrize("sigma,restarts", [(0.4, range(8)), (3.0, [0, 5])])
+def test_loss_grad_large_sharpened(sigma, restarts):
+    """The 50k-op workload at full size in a sharpened state (the paper's
+    initial means, every sigma the same small value, as bench.py --sigma
+    times it): at sigma = 0.4 every op and edge runs through the narrow
+    kernel over the whole horizon, at sigma = 3 most do."""
+    cfg = CONFIGS["large"]
+    p = make_problem(cfg, seed=0)
+    B = cfg.B
+    u = restart_uniforms(p.n_ops, B, seed=0)
+    mu, sg, rc = oracle.init_state(p, B, u)
+    assert rc == 0
+    mu = mu.astype(np.float32)
+    sg = np.full(mu.shape, sigma, np.float32)
+    hp = bd.default_hparams()
+    hp.lr = cfg.lr
+    _check(p, mu, sg, _lam(B, 7), hp, restarts, f"large/sigma={sigma}")
+
+
 def test_loss_grad_pipelined_random():
     p = make_problem("pipelined", seed=0)
     B = 4
@@ -397,13 +416,16 @@ def test_small_edge_cases():
         _check(p, mu, sg, _lam(2, 4), hparams(alpha=0.5, rho=0.1), range(2), f"edge D={D} N={N}")
 
 
-def test_sigma_to_zero_usage_bit_exact():
+@pytest.mark.parametrize("D", [200, 3000])
+def test_sigma_to_zero_usage_bit_exact(D):
     """sigma -> 0: usage is the integer histogram of the rounded schedule,
-    bit for bit; the violation and edge-length terms are exact counts."""
+    bit for bit; the violation and edge-length terms are exact counts (one
+    op-kernel tile at D = 200; at D = 3000 the narrow kernel takes every op
+    over the whole horizon)."""
     for II in (0, 5):
-        p = _ragged_problem(21, N=300, D=200, II=II, n_back=8 if II else 0, big_delay=False)
+        p = _ragged_problem(21, N=300, D=D, II=II, n_back=8 if II else 0, big_delay=False)
         rng = np.random.default_rng(22)
-        s_int = rng.integers(-3, 205, size=(2, p.n_ops))
+        s_int = rng.integers(-3, D + 5, size=(2, p.n_ops))
         mu = (s_int + rng.uniform(-0.4, 0.4, size=s_int.shape)).astype(np.float32)
         sg = np.full(mu.shape, 1e-5, np.float32)
         g = gpu_loss_grad(p, mu, sg, np.zeros((2, 3), np.float32), hparams(alpha=0.0, rho=0.0))
