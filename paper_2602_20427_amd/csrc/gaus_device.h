@@ -92,16 +92,29 @@ __device__ __forceinline__ float fam_h(float z) {
     }
 }
 
-// |z| beyond which the density factor and the tail are exactly 0 in fp32
-// (the exponential underflows past the smallest subnormal, 2^-149): then a
-// CDF value is exactly 0 or 1 and its derivatives exactly 0.  The Cauchy
-// tails never vanish.
+// |z| beyond which the step-by-step evaluations flush the tail and the
+// density factor to exactly 0 (fam_tail_h_fl): both are below 3e-16 there
+// (relative to the peak density for the factor: Gaussian e^-32, logistic
+// and Laplace e^-35), far below fp32 resolution.  A CDF value is then
+// exactly 0 or 1 and its derivatives exactly 0, which the spread tests below
+// rely on.  The Cauchy tails never vanish.
 template <int FAM>
 __host__ __device__ constexpr float fam_zflush() {
-    return FAM == 0 ? 15.0f      // exp2(-z^2 log2(e)/2) = 0 for |z| > 14.4
-         : FAM == 1 ? 60.0f      // exp2(-|z| pi/sqrt(3) log2(e)) = 0 for |z| > 57.4
-         : FAM == 2 ? 75.0f      // exp2(-|z| sqrt(2) log2(e)) = 0 for |z| > 73.6
+    return FAM == 0 ? 8.0f       // Phi(-8) = 6.2e-16
+         : FAM == 1 ? 20.0f      // exp(-20 pi/sqrt(3)) = 1.7e-16
+         : FAM == 2 ? 25.0f      // exp(-25 sqrt(2))/2 = 2.0e-16
          : 3.0e38f;
+}
+
+// fam_tail_h with the far tails flushed (every step-by-step evaluation)
+template <int FAM>
+__device__ __forceinline__ void fam_tail_h_fl(float z, float &tail, float &g) {
+    fam_tail_h<FAM>(z, tail, g);
+    if constexpr (FAM != 3) {
+        const bool far = fabsf(z) > fam_zflush<FAM>();
+        tail = far ? 0.0f : tail;
+        g = far ? 0.0f : g;
+    }
 }
 
 // Bin edges [lo, hi] (clamped into [a - 1 .. b + 1]) outside which an op's CDF
@@ -189,7 +202,7 @@ __device__ __forceinline__ void cdf_at(long long v, int D, float mu, float rs, f
     if (v >= D - 1) { st = -0.0f; Fm = 0.0f; Fs = 0.0f; return; }
     const float z = ((float)v + 0.5f - mu) * rs;
     float tail, g;
-    fam_tail_h<FAM>(z, tail, g);
+    fam_tail_h_fl<FAM>(z, tail, g);
     st = (z >= 0.0f) ? -tail : tail;
     Fm = -g * cinv;
     Fs = Fm * z;
@@ -203,7 +216,7 @@ __device__ __forceinline__ void cdf_at(int v, int D, float mu, float rs, float c
     if (v >= D - 1) { st = -0.0f; Fm = 0.0f; Fs = 0.0f; return; }
     const float z = ((float)v + 0.5f - mu) * rs;
     float tail, g;
-    fam_tail_h<FAM>(z, tail, g);
+    fam_tail_h_fl<FAM>(z, tail, g);
     st = (z >= 0.0f) ? -tail : tail;
     Fm = -g * cinv;
     Fs = Fm * z;
@@ -215,7 +228,7 @@ __device__ __forceinline__ float st_at(long long v, int D, float mu, float rs) {
     if (v >= D - 1) return -0.0f;
     const float z = ((float)v + 0.5f - mu) * rs;
     float tail, g;
-    fam_tail_h<FAM>(z, tail, g);
+    fam_tail_h_fl<FAM>(z, tail, g);
     return (z >= 0.0f) ? -tail : tail;
 }
 

@@ -600,7 +600,7 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
                 if (u < D - 1) {
                     const float z = ((float)u + 0.5f - m_j) * rsj;
                     float tl, gj;
-                    fam_tail_h<FAM>(z, tl, gj);
+                    fam_tail_h_fl<FAM>(z, tl, gj);
                     const bool up = z >= 0.0f;
                     SL[k] += up ? 0.0f : tl;
                     SU[k] += up ? tl : 0.0f;
@@ -615,7 +615,7 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
             if (tid == 0 && t0 > 0) {
                 const float z = ((float)(t0 - 1) + 0.5f - m_j) * rsj;
                 float tl, gj;
-                fam_tail_h<FAM>(z, tl, gj);
+                fam_tail_h_fl<FAM>(z, tl, gj);
                 if (z >= 0.0f) { pU += tl; pC += 1.0f; } else { pL += tl; }
             }
             const float r = wave_sum4(acc[0], acc[1], acc[2], acc[3], lane);
