@@ -806,19 +806,38 @@ __global__ __launch_bounds__(256) void k_final(Graph G, Work W, HP hp, const flo
     const int big = G.big_of[i];
     const double *bsum = big >= 0 ? W.bigsum + ((size_t)b * G.nbig + big) * 6 : nullptr;
     if (bsum) { dm += bsum[0]; ds += bsum[1]; cm += bsum[2]; cs += bsum[3]; }
-    for (int q = bsum ? G.pred_ptr[i + 1] : G.pred_ptr[i]; q < G.pred_ptr[i + 1]; ++q) {
-        const int e = G.pred_eid[q];
-        const size_t bs = (size_t)b * N + G.pred_src[q];
-        if ((poly_i && W.cls[bs]) || W.dflag[bs] == 2) {   // single record of the edge
-            const float *cp = W.cpoly + ((size_t)b * G.E + e) * kCP;
-            dm += cp[0]; ds += cp[1]; cm += cp[2]; cs += cp[3];
-            continue;
+    // in-edges four at a time: their ids, then the producers' flags and the
+    // single records (loaded whether used or not), then the sums in edge order
+    constexpr int kInB = 4;
+    const int qa = bsum ? G.pred_ptr[i + 1] : G.pred_ptr[i], qb = G.pred_ptr[i + 1];
+    for (int q0 = qa; q0 < qb; q0 += kInB) {
+        int ev[kInB], sv[kInB];
+#pragma unroll
+        for (int k = 0; k < kInB; ++k) {
+            const int q = min(q0 + k, qb - 1);
+            ev[k] = G.pred_eid[q]; sv[k] = G.pred_src[q];
         }
-        const float *cp = W.cpart + (((size_t)b * G.E + e) * nt) * kCP;
-        for (int tl = 0; tl < nt; ++tl) {
-            if (!cons_tile(tl)) continue;
-            dm += cp[tl * kCP + 0]; ds += cp[tl * kCP + 1];
-            cm += cp[tl * kCP + 2]; cs += cp[tl * kCP + 3];
+        bool one[kInB];
+        float4 r4[kInB];
+#pragma unroll
+        for (int k = 0; k < kInB; ++k) {
+            const size_t bs = (size_t)b * N + sv[k];
+            one[k] = (poly_i && W.cls[bs]) || W.dflag[bs] == 2;   // single record of the edge
+            r4[k] = *reinterpret_cast<const float4 *>(W.cpoly + ((size_t)b * G.E + ev[k]) * kCP);
+        }
+#pragma unroll
+        for (int k = 0; k < kInB; ++k) {
+            if (q0 + k >= qb) break;
+            if (one[k]) {
+                dm += r4[k].x; ds += r4[k].y; cm += r4[k].z; cs += r4[k].w;
+                continue;
+            }
+            const float *cp = W.cpart + (((size_t)b * G.E + ev[k]) * nt) * kCP;
+            for (int tl = 0; tl < nt; ++tl) {
+                if (!cons_tile(tl)) continue;
+                dm += cp[tl * kCP + 0]; ds += cp[tl * kCP + 1];
+                cm += cp[tl * kCP + 2]; cs += cp[tl * kCP + 3];
+            }
         }
     }
     double qm = 0.0, qs = 0.0;
