@@ -34,8 +34,9 @@ namespace gaus {
 // near the two ops' spreads and the horizon's ends; elsewhere each summand
 // above is 0, except F_i(u)(1 - F_j(u)) = 1 between the spreads (i done, j
 // not started).  When these spreads are short, a lane group takes the op (a
-// quarter of a wave when every spread has at most kTinySpan steps, else the
-// whole wave): it evaluates every summand on the steps where one may vary
+// quarter of a wave when every spread has at most kTinySpan steps, half a
+// wave up to kMidSpan, else the whole wave): it evaluates every summand on
+// the steps where one may vary
 // (the spread of F_i(u), that of A(u) and F_i'(u-s), that of F_j(u), and the
 // steps 0, s-1, D-2, D-1) and counts the steps between the spreads, with no
 // work-group barrier; the other ops of the group follow the row path above.
@@ -43,6 +44,7 @@ namespace gaus {
 // the unit masses at the horizon's ends) and the op's own thread finishes it
 // while the group is sorted.
 constexpr int kNarrowSpan = 128;   // widest spread (in steps) on the narrow path
+constexpr int kMidSpan = 64;       // widest spread of the ops taken two per wave
 constexpr int kTinySpan = 32;      // widest spread of the ops taken four per wave
 constexpr int kNarrowPass = 4;     // passes of a lane group over the producer's steps
 
@@ -52,7 +54,7 @@ __device__ __forceinline__ void spread(float mu, float rs, int a, int b, int &lo
 }
 
 // classes of an op in a step tile
-enum : unsigned char { kNone = 0, kConst = 1, kTiny = 2, kNarrow = 3, kWide = 4 };
+enum : unsigned char { kNone = 0, kConst = 1, kTiny = 2, kNarrow = 3, kWide = 4, kMid = 5 };
 
 // A group's ops and their consumers as the op kernel reads them, staged in
 // LDS once per work-group (the consumers of at most kStage edges; an op whose
@@ -175,7 +177,8 @@ __device__ __forceinline__ void narrow_ops(const Graph &G, const Work &W, const 
             // out-edge: kNarrowPass passes of GL lanes (x < n1: X1; then X2,
             // less the steps of X1).  At u = D-1 the A slot holds 1 - F_i(D-1-s).
             constexpr int R = kNarrowPass;
-            static_assert(R * GL >= 2 * (NP == 1 ? kNarrowSpan : kTinySpan), "passes cover X1 and X2");
+            static_assert(R * GL >= 2 * (NP == 1 ? kNarrowSpan : NP == 2 ? kMidSpan : kTinySpan),
+                          "passes cover X1 and X2");
             const int n12 = n1 + n2;
             const int n12_max = group_max<NP>(n12);
             float cSt[R], cFm[R], cFs[R], cA[R], cFms[R], cFss[R];
@@ -446,7 +449,10 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
                 for (int k = 0; k < 3; ++k) dep += ua[k] * (us[k] > ch ? 1 : 0);
             }
             flag = 1 + m;
-            c = !act ? kConst : span <= kTinySpan ? kTiny : span <= kNarrowSpan ? kNarrow : kWide;
+            c = !act ? kConst
+                : span <= kTinySpan ? kTiny
+                : span <= kMidSpan ? kMid
+                : span <= kNarrowSpan ? kNarrow : kWide;
             if (c == kConst) {
                 // no records: every derivative is 0 here, and the readers skip
                 // this tile (tile_prod_rec / tile_cons_rec are false for it)
@@ -465,8 +471,8 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
     float gsum0 = 0.0f, gsum1 = 0.0f;  // V_dep, L_com of the work-group (threads 0, 1)
     __syncthreads();
 
-    // Narrow ops: the shortest spreads four at a time per wave, the others one
-    // at a time.  Each wave's usage row is folded into the step owners' sums
+    // Narrow ops: the shortest spreads four at a time per wave, then two, the
+    // others one at a time.  Each wave's usage row is folded into the step owners' sums
     // before the row path takes the buffer.
     __shared__ float sGw[NW][2];          // the narrow ops' V_dep and L_com
     {
@@ -475,6 +481,8 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
         for (int p = lane; p < TILE; p += 64) sU[p] = 0.0f;
         float g0 = 0.0f, g1 = 0.0f;
         narrow_ops<FAM, 4, BS>(G, W, mub, rsb, clsb, st, sCls, sDirect, sU, nullptr, kTiny, nq, t0, tb, tile, b,
+                               g0, g1);
+        narrow_ops<FAM, 2, BS>(G, W, mub, rsb, clsb, st, sCls, sDirect, sU, nullptr, kMid, nq, t0, tb, tile, b,
                                g0, g1);
         narrow_ops<FAM, 1, BS>(G, W, mub, rsb, clsb, st, sCls, sDirect, sU, nullptr, kNarrow, nq, t0, tb, tile, b,
                                g0, g1);
@@ -800,7 +808,7 @@ __global__ __launch_bounds__(kNarBS) void k_narrow(Graph G, const float *__restr
             }
             flag = 1 + m;
             const bool take = !poly_i && span <= kNarrowSpan;
-            c = take ? (span <= kTinySpan ? kTiny : kNarrow) : kNone;
+            c = take ? (span <= kTinySpan ? kTiny : span <= kMidSpan ? kMid : kNarrow) : kNone;
             if (take) W.dflag[(size_t)b * N + i] = 2;
             sAny[take ? 1 : 0] = 1;
         }
@@ -812,6 +820,8 @@ __global__ __launch_bounds__(kNarBS) void k_narrow(Graph G, const float *__restr
     if (!sAny[1]) return;
     float g0 = 0.0f, g1 = 0.0f;
     narrow_ops<FAM, 4, BS, true>(G, W, mub, rsb, clsb, st, sCls, sDirect, nullptr, sRow, kTiny, nq, 0, D, 0, b,
+                                 g0, g1);
+    narrow_ops<FAM, 2, BS, true>(G, W, mub, rsb, clsb, st, sCls, sDirect, nullptr, sRow, kMid, nq, 0, D, 0, b,
                                  g0, g1);
     narrow_ops<FAM, 1, BS, true>(G, W, mub, rsb, clsb, st, sCls, sDirect, nullptr, sRow, kNarrow, nq, 0, D, 0, b,
                                  g0, g1);
