@@ -54,7 +54,7 @@ constexpr int kGridP[kGrids] = {1, 2, 4};
 constexpr unsigned char kNoGrid = 255;
 // bits of Work::gbits
 constexpr unsigned kGbStep = 1u, kGbNarrow = 2u, kGbGrid = 4u;
-// bits of Work::gnar: step-by-step ops left to the op kernel / taken by k_narrow
+// bits of Work::gnar: step-by-step ops left to the op kernel / taken by k_group
 constexpr unsigned kNarLeft = 1u, kNarTaken = 2u;
 // the narrow kernel: threads per work-group (at least the largest group), and
 // the longest horizon its fixed-point usage row (8 bytes per step) takes
@@ -109,7 +109,7 @@ struct Graph {
                                          // kLegPre predecessors (32-byte aligned)
     const int *leg_over;                 // predecessors past the first kLegPre, in level order
     int leg_ring;                        // 1: II = 0 legalization through the LDS ring (k_legalize_ring)
-    int nar_on;                          // 1: short-spread step-by-step ops go to k_narrow (several
+    int nar_on;                          // 1: short-spread step-by-step ops go to k_group (several
                                          // op-kernel tiles and D <= kNarMaxD)
     int leg_ring_items, leg_ring_over;   // items and overflow predecessors one ring half holds
     int leg_nbatch;                      // ring batches: contiguous ranges of the items of levels >= 1
@@ -169,14 +169,14 @@ struct Work {
     unsigned char *cls;  // [B][N]          1 = op on the chunk-polynomial path this iteration
     float *rsig;           // [B][N]        1/sigma of this iteration (written by k_flags)
     unsigned char *dflag;  // [B][N]        1 = op has step-by-step work (own terms or out-edges),
-                           //               2 = that work is done by k_narrow (records in ppoly / cpoly)
-    unsigned *gnar;        // [B][ngroups]  k_narrow's split of a group with step-by-step work
+                           //               2 = that work is done by k_group (records in ppoly / cpoly)
+    unsigned *gnar;        // [B][ngroups]  k_group's split of a group with step-by-step work
                            //               (kNarLeft, kNarTaken); valid where gbits has kGbStep
-    float *Unar;           // [B][ngroups][D]  usage of the ops k_narrow took
+    float *Unar;           // [B][ngroups][D]  usage of the ops k_group took
     float *gsum_nar;       // [B][ngroups][2]  their V_dep, L_com
     unsigned char *ptier;  // [B][N]        polynomial op: tier of its vectors, the smallest over
                            //               itself and its polynomial consumers (highest degree)
-    unsigned *gbits;  // [B][ngroups]      work of the group this iteration (k_gbits):
+    unsigned *gbits;  // [B][ngroups]      work of the group this iteration (k_group):
                       //                   kGbStep = some op has step-by-step work,
                       //                   kGbNarrow = some op takes polynomial degree 8 or 6,
                       //                   kGbGrid << g = ops on grid g; only such groups'
@@ -232,7 +232,7 @@ hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const 
                              const PolyArgs &pa, const IterArgs &a, hipStream_t st);
 
 // Per-step kernels (gaus_step.hip: step by step; gaus_poly.hip: chunk polynomials).
-hipError_t launch_narrow(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu, hipStream_t st);
+hipError_t launch_group(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu, hipStream_t st);
 hipError_t launch_ops(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu, const float *sigma,
                       hipStream_t st);
 hipError_t launch_back(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu, const float *sigma,

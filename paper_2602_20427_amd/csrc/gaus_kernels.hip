@@ -82,7 +82,7 @@ __device__ __forceinline__ int grid_tier(const GridArgs &gr, float s, int delay)
 //     (the highest degree of its members'); else grid 0 with the op's own
 //     tier, or kNoGrid on the step-by-step path.  Polynomial records (ppoly,
 //     cpoly) are written only for ops on a grid; every reader checks cls.
-// The per-(restart, group) OR of these flags (gbits) follows in k_gbits.
+// The per-(restart, group) OR of these flags (gbits) follows in k_group.
 // The consumers' tiers are recomputed here from their sigmas.  With the
 // storage term on, also whether a holder's storage term is taken on the
 // chunk polynomials (Gaussian start times only; kMemPolyDeg, kMemRhoMax).
@@ -157,29 +157,6 @@ __global__ __launch_bounds__(64 * kFlagPack) void k_flags(Graph G, PolyArgs pa, 
         W.gsel[bi] = (unsigned char)g_sel;
         W.gtier[bi] = (unsigned char)(g_sel == kNoGrid ? 0 : tier);
     }
-}
-
-// Work bits of each (restart, group): the OR over its ops of kGbStep (step-by-
-// step work), kGbNarrow (degree 8 or 6) and kGbGrid << grid.  Work-group =
-// (group, restart), thread per op; one plain store per (restart, group).
-__global__ __launch_bounds__(256) void k_gbits(Graph G, Work W) {
-    __shared__ unsigned sW[4];
-    const int grp = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid & 63;
-    const int q0 = G.grp_start[grp], q1 = G.grp_start[grp + 1];
-    unsigned bits = 0u;
-    for (int q = q0 + tid; q < q1; q += 256) {
-        const size_t bi = (size_t)b * G.N + G.perm[q];
-        const int t = W.ptier[bi], gs = W.gsel[bi];
-        bits |= W.dflag[bi] ? kGbStep : 0u;
-        bits |= (t == 1 || t == 2) ? kGbNarrow : 0u;
-        bits |= gs < kGrids ? kGbGrid << gs : 0u;
-    }
-    unsigned v = 0u;
-#pragma unroll
-    for (int k = 0; k < 2 + kGrids; ++k) v |= __ballot((bits >> k) & 1u) ? 1u << k : 0u;
-    if (lane == 0) sW[tid >> 6] = v;
-    __syncthreads();
-    if (tid == 0) W.gbits[(size_t)b * G.ngroups + grp] = (sW[0] | sW[1]) | (sW[2] | sW[3]);
 }
 
 // ---------------------------------------------------------------------------
@@ -1653,10 +1630,9 @@ hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const 
                              const PolyArgs &pa, const IterArgs &a, hipStream_t st) {
     hipLaunchKernelGGL(k_flags, dim3((g.N + 63) / 64, (g.B + kFlagPack - 1) / kFlagPack), dim3(64 * kFlagPack), 0, st,
                        g, pa, a.sigma, w, (hp.gamma != 0.0f && pa.enabled) ? 1 : 0);
-    hipLaunchKernelGGL(k_gbits, dim3(g.ngroups, g.B), dim3(256), 0, st, g, w);
     hipError_t e;
     if (a.ops_begin) (void)hipEventRecord(a.ops_begin, st);
-    if (g.nar_on && (e = launch_narrow(g, w, lc, a.mu, st)) != hipSuccess) return e;
+    if ((e = launch_group(g, w, lc, a.mu, st)) != hipSuccess) return e;
     if ((e = launch_ops(g, w, lc, a.mu, a.sigma, st)) != hipSuccess) return e;
     if (a.ops_end) (void)hipEventRecord(a.ops_end, st);
     if (pa.enabled) {

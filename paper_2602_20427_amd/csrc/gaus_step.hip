@@ -78,7 +78,7 @@ __device__ __forceinline__ float uniformf(float x) {
 // L_com go to g0 and g1 of the lanes 0 and 2 of each lane group.
 // In a step tile of the op kernel (ONE = false): the wave's usage goes to sU
 // (its own LDS row of the tile), the records to the per-tile ppart / cpart.
-// Over the whole horizon (ONE = true, k_narrow): the usage goes to sU64, one
+// Over the whole horizon (ONE = true, k_group): the usage goes to sU64, one
 // row of the work-group in fixed point (2^-40 units, integer LDS atomics:
 // the sum does not depend on the order), the records to the single ppoly /
 // cpoly slots of the op and its edges.
@@ -720,19 +720,24 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
 
 
 // ---------------------------------------------------------------------------
-// Narrow kernel: the step-by-step ops whose spreads are short, each taken once
-// over the whole horizon instead of once per step tile.  Work-group = (op
-// group, restart), thread per op for the sorting (the op kernel's spread tests
-// with one tile [0, D)): an op off the polynomial path whose own spreads and
-// whose consumers' spreads span at most kNarrowSpan steps is taken here (its
-// step-by-step flag becomes 2, and the op kernel leaves it); the others stay
-// with the op kernel.  The taken ops run through narrow_ops over the horizon:
-// usage into one fixed-point LDS row of D steps, records into the single
-// ppoly / cpoly slots (free for ops off the polynomial path), V_dep and L_com
-// per (restart, group).  gnar[b][group] tells the readers which parts exist.
+// Group kernel.  Work-group = (op group, restart).
+// (1) The group's work bits this iteration (gbits): the OR over its ops of
+//     kGbStep (step-by-step work), kGbNarrow (degree 8 or 6) and kGbGrid <<
+//     grid; one plain store per (restart, group).
+// (2) With the narrow path on (G.nar_on): the step-by-step ops whose spreads
+//     are short, each taken once over the whole horizon instead of once per
+//     step tile.  Thread per op for the sorting (the op kernel's spread tests
+//     with one tile [0, D)): an op off the polynomial path whose own spreads
+//     and whose consumers' spreads span at most kNarrowSpan steps is taken
+//     here (its step-by-step flag becomes 2, and the op kernel leaves it); the
+//     others stay with the op kernel.  The taken ops run through narrow_ops
+//     over the horizon: usage into one fixed-point LDS row of D steps, records
+//     into the single ppoly / cpoly slots (free for ops off the polynomial
+//     path), V_dep and L_com per (restart, group).  gnar[b][group] tells the
+//     readers which parts exist.
 // ---------------------------------------------------------------------------
 template <int FAM>
-__global__ __launch_bounds__(kNarBS) void k_narrow(Graph G, const float *__restrict__ mu, Work W) {
+__global__ __launch_bounds__(kNarBS) void k_group(Graph G, const float *__restrict__ mu, Work W) {
     constexpr int BS = kNarBS, NW = BS / 64;
     extern __shared__ long long sRow[];   // [D] usage of the taken ops, 2^-40 units
     __shared__ int sDirect[BS];
@@ -747,12 +752,32 @@ __global__ __launch_bounds__(kNarBS) void k_narrow(Graph G, const float *__restr
     const int lane = tid & 63, w = tid >> 6;
     const int D = G.D, N = G.N;
     const size_t bg = (size_t)b * G.ngroups + grp;
-    // no step-by-step work in the group: the readers skip it before reading gnar
-    if (!(W.gbits[bg] & kGbStep)) return;
+    const int q0 = G.grp_start[grp], nq = G.grp_start[grp + 1] - q0;
+    {   // (1) work bits
+        __shared__ unsigned sW[NW];
+        unsigned bits = 0u;
+        for (int q = tid; q < nq; q += BS) {
+            const size_t bi = (size_t)b * N + G.perm[q0 + q];
+            const int t = W.ptier[bi], gs = W.gsel[bi];
+            bits |= W.dflag[bi] ? kGbStep : 0u;
+            bits |= (t == 1 || t == 2) ? kGbNarrow : 0u;
+            bits |= gs < kGrids ? kGbGrid << gs : 0u;
+        }
+        unsigned v = 0u;
+#pragma unroll
+        for (int k = 0; k < 2 + kGrids; ++k) v |= __ballot((bits >> k) & 1u) ? 1u << k : 0u;
+        if (lane == 0) sW[w] = v;
+        __syncthreads();
+        v = 0u;
+#pragma unroll
+        for (int k = 0; k < NW; ++k) v |= sW[k];
+        if (tid == 0) W.gbits[bg] = v;
+        // no step-by-step work in the group: the readers skip it before reading gnar
+        if (!(v & kGbStep) || !G.nar_on) return;
+    }
     const float *mub = mu + (size_t)b * N;
     const float *rsb = W.rsig + (size_t)b * N;
     const unsigned char *clsb = W.cls + (size_t)b * N;
-    const int q0 = G.grp_start[grp], nq = G.grp_start[grp + 1] - q0;
     for (int u = tid; u < D; u += BS) sRow[u] = 0;
     if (tid < 2) sAny[tid] = 0;
     {
@@ -1142,14 +1167,14 @@ hipError_t launch_ops(const Graph &g, const Work &w, const LaunchCfg &lc, const 
     });
 }
 
-hipError_t launch_narrow(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu, hipStream_t st) {
+hipError_t launch_group(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu, hipStream_t st) {
     const dim3 grid(g.ngroups, g.B);
-    const size_t lds = sizeof(long long) * (size_t)g.D;
+    const size_t lds = g.nar_on ? sizeof(long long) * (size_t)g.D : 0;
     switch (lc.fam) {
-        case 0: hipLaunchKernelGGL(k_narrow<0>, grid, dim3(kNarBS), lds, st, g, mu, w); break;
-        case 1: hipLaunchKernelGGL(k_narrow<1>, grid, dim3(kNarBS), lds, st, g, mu, w); break;
-        case 2: hipLaunchKernelGGL(k_narrow<2>, grid, dim3(kNarBS), lds, st, g, mu, w); break;
-        case 3: hipLaunchKernelGGL(k_narrow<3>, grid, dim3(kNarBS), lds, st, g, mu, w); break;
+        case 0: hipLaunchKernelGGL(k_group<0>, grid, dim3(kNarBS), lds, st, g, mu, w); break;
+        case 1: hipLaunchKernelGGL(k_group<1>, grid, dim3(kNarBS), lds, st, g, mu, w); break;
+        case 2: hipLaunchKernelGGL(k_group<2>, grid, dim3(kNarBS), lds, st, g, mu, w); break;
+        case 3: hipLaunchKernelGGL(k_group<3>, grid, dim3(kNarBS), lds, st, g, mu, w); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
