@@ -337,7 +337,12 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
     __shared__ float sLast[NW][SPT][3];           // each wave's last S_i(u) terms (lower, upper, count)
     int cpar = 0;
 
-    const int grp = blockIdx.x / G.parts, part = blockIdx.x % G.parts, tile = blockIdx.y, b = blockIdx.z;
+    // work-group x serves restart x mod B (the XCDs receive work-groups in
+    // turn: with B a multiple of 8 a restart's gathered means and widths stay
+    // in one XCD's L2), then (group, part) and tile
+    const int b = blockIdx.x % G.B, xr = blockIdx.x / G.B;
+    const int gp = xr % (G.ngroups * G.parts), tile = xr / (G.ngroups * G.parts);
+    const int grp = gp / G.parts, part = gp % G.parts;
     const int tid = threadIdx.x;
     const int lane = tid & 63, wid = tid >> 6;
     const int D = G.D, N = G.N;
@@ -748,7 +753,8 @@ __global__ __launch_bounds__(kNarBS) void k_group(Graph G, const float *__restri
     __shared__ int sAny[2];                // an op left to the op kernel / taken here
     __shared__ float sGw[NW][2];
     const OpStage st{sOpI, sOpE0, sOpDeg, sOpS, sOpOff, sOpMu, sOpRs, sOpPoly, sEmu, sErs, sEon};
-    const int grp = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+    // work-group x serves restart x mod B (as in the op kernel)
+    const int b = blockIdx.x % G.B, grp = blockIdx.x / G.B, tid = threadIdx.x;
     const int lane = tid & 63, w = tid >> 6;
     const int D = G.D, N = G.N;
     const size_t bg = (size_t)b * G.ngroups + grp;
@@ -1160,7 +1166,9 @@ hipError_t dispatch(const LaunchCfg &lc, F &&f) {
 
 hipError_t launch_ops(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu, const float *sigma,
                       hipStream_t st) {
-    const dim3 grid(g.ngroups * g.parts, g.ntiles, g.B);
+    const size_t nwg = (size_t)g.ngroups * g.parts * g.ntiles * g.B;
+    if (nwg > 0x7fffffffu) return hipErrorInvalidConfiguration;
+    const dim3 grid((unsigned)nwg);
     return dispatch(lc, [&](auto fam, auto bs, auto spt) {
         hipLaunchKernelGGL((k_ops<decltype(fam)::value, decltype(bs)::value, decltype(spt)::value>), grid,
                            dim3(decltype(bs)::value), 0, st, g, mu, sigma, w);
@@ -1168,7 +1176,7 @@ hipError_t launch_ops(const Graph &g, const Work &w, const LaunchCfg &lc, const 
 }
 
 hipError_t launch_group(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu, hipStream_t st) {
-    const dim3 grid(g.ngroups, g.B);
+    const dim3 grid((unsigned)((size_t)g.ngroups * g.B));
     const size_t lds = g.nar_on ? sizeof(long long) * (size_t)g.D : 0;
     switch (lc.fam) {
         case 0: hipLaunchKernelGGL(k_group<0>, grid, dim3(kNarBS), lds, st, g, mu, w); break;
