@@ -45,8 +45,8 @@ namespace gaus {
 // while the group is sorted.
 constexpr int kNarrowSpan = 128;   // widest spread (in steps) on the narrow path
 constexpr int kMidSpan = 64;       // widest spread of the ops taken two per wave
-constexpr int kTinySpan = 32;      // widest spread of the ops taken four per wave
-constexpr int kNarrowPass = 4;     // passes of a lane group over the producer's steps
+constexpr int kTinySpan = 16;      // widest spread of the ops taken four per wave
+constexpr int kNarrowPass = 4;     // passes of a lane group over the producer's steps (2 for four per wave)
 
 template <int FAM>
 __device__ __forceinline__ void spread(float mu, float rs, int a, int b, int &lo, int &hi) {
@@ -176,7 +176,7 @@ __device__ __forceinline__ void narrow_ops(const Graph &G, const Work &W, const 
             // Producer values on X1 and X2 \ X1, the same steps for every
             // out-edge: kNarrowPass passes of GL lanes (x < n1: X1; then X2,
             // less the steps of X1).  At u = D-1 the A slot holds 1 - F_i(D-1-s).
-            constexpr int R = kNarrowPass;
+            constexpr int R = NP == 4 ? 2 : kNarrowPass;
             static_assert(R * GL >= 2 * (NP == 1 ? kNarrowSpan : NP == 2 ? kMidSpan : kTinySpan),
                           "passes cover X1 and X2");
             const int n12 = n1 + n2;
