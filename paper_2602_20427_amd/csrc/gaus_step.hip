@@ -9,9 +9,11 @@
 namespace gaus {
 
 // ---------------------------------------------------------------------------
-// Op kernel.  Work-group = (op group, step tile, restart).  Threads own steps
-// u = t0 + k*BS + tid (k < SPT).  For each op i of the group (all of one
-// resource type, out-degree m, delay s = Lat(v_i)):
+// Op kernel.  Work-group = (op group, step tile, restart).  Its ops (all of
+// one resource type) are sorted by how far their spreads reach into the tile
+// (below) and taken by lane groups, by single waves, or by the row path.
+// Row path: threads own steps u = t0 + k*BS + tid (k < SPT).  For each op i
+// (out-degree m, delay s = Lat(v_i)):
 //   * its CDF row over the tile plus a left halo of s steps goes to LDS; the
 //     mass P_i^u is added to the group's usage;
 //   * for each out-edge (i -> j) the consumer's CDF and density factor are
@@ -39,7 +41,9 @@ namespace gaus {
 // the steps where one may vary
 // (the spread of F_i(u), that of A(u) and F_i'(u-s), that of F_j(u), and the
 // steps 0, s-1, D-2, D-1) and counts the steps between the spreads, with no
-// work-group barrier; the other ops of the group follow the row path above.
+// work-group barrier.  Wider ops take a wave each (wide_ops below) when their
+// consumers' spreads cover less than half the tile on average (the summands
+// are then evaluated on those spreads only), else the row path above.
 // When no spread meets the tile at all, every term is an integer (counts and
 // the unit masses at the horizon's ends) and the op's own thread finishes it
 // while the group is sorted.
@@ -54,12 +58,14 @@ __device__ __forceinline__ void spread(float mu, float rs, int a, int b, int &lo
 }
 
 // classes of an op in a step tile
-enum : unsigned char { kNone = 0, kConst = 1, kTiny = 2, kNarrow = 3, kWide = 4, kMid = 5 };
+enum : unsigned char { kNone = 0, kConst = 1, kTiny = 2, kNarrow = 3, kWide = 4, kMid = 5, kRow = 6 };
 
-// A group's ops and their consumers as the op kernel reads them, staged in
-// LDS once per work-group (the consumers of at most kStage edges; an op whose
-// edges do not fit reads them from global memory).
+// A group's ops and their consumers as the op and group kernels read them,
+// staged in LDS once per work-group (the consumers of at most kStage edges in
+// k_group, kStageOps in k_ops, whose LDS also holds the wide ops' rows; an op
+// whose edges do not fit reads them from global memory).
 constexpr int kStage = 1024;
+constexpr int kStageOps = 512;
 struct OpStage {
     int *i, *e0, *deg, *s, *off;   // op id, first edge, out-degree, delay, first staged edge (-1: none)
     float *mu, *rs;                // mean and 1/sigma
@@ -75,13 +81,12 @@ __device__ __forceinline__ float uniformf(float x) {
 // Narrow ops of class `want` from the group's list, NP at a time by each wave,
 // one op per lane group of 64/NP lanes (the loads of the ops and their
 // consumers overlap; loops run to the lane groups' maximum).  Its V_dep and
-// L_com go to g0 and g1 of the lanes 0 and 2 of each lane group.
-// In a step tile of the op kernel (ONE = false): the wave's usage goes to sU
-// (its own LDS row of the tile), the records to the per-tile ppart / cpart.
-// Over the whole horizon (ONE = true, k_group): the usage goes to sU64, one
-// row of the work-group in fixed point (2^-40 units, integer LDS atomics:
-// the sum does not depend on the order), the records to the single ppoly /
-// cpoly slots of the op and its edges.
+// L_com go to g0 and g1 of the lanes 0 and 2 of each lane group.  The usage
+// goes to sU64, the work-group's row of the steps from t0 in fixed point
+// (2^-40 units, integer LDS atomics: the sum does not depend on the order).
+// In a step tile of the op kernel (ONE = false) the records go to the
+// per-tile ppart / cpart; over the whole horizon (ONE = true, k_group) to the
+// single ppoly / cpoly slots of the op and its edges.
 constexpr float kUsageFix = 1099511627776.0f;   // 2^40
 
 // Maximum over the wave of a value that is the same on every lane of each
@@ -97,7 +102,7 @@ template <int FAM, int NP, int BS, bool ONE = false>
 __device__ __forceinline__ void narrow_ops(const Graph &G, const Work &W, const float *__restrict__ mub,
                                            const float *__restrict__ rsb, const unsigned char *__restrict__ clsb,
                                            const OpStage &st, const unsigned char *sCls, const int *sDirect,
-                                           float *sU, long long *sU64, unsigned char want, int nq, int t0, int tb,
+                                           long long *sU64, unsigned char want, int nq, int t0, int tb,
                                            int tile, int b, float &g0, float &g1) {
     constexpr int NW = BS / 64, GL = 64 / NP;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -155,19 +160,9 @@ __device__ __forceinline__ void narrow_ops(const Graph &G, const Work &W, const 
                     take = u >= t0 && u < tb && !(u >= x1l && u <= x1h) && !(xx > n1 && u == 0);
                 }
                 const float P = take ? st_mass(st_at<FAM>(u - 1, D, m_i, rs), st_at<FAM>(u, D, m_i, rs)) : 0.0f;
-                if constexpr (ONE) {
-                    if (take)
-                        atomicAdd(reinterpret_cast<unsigned long long *>(sU64 + u),
-                                  (unsigned long long)__float2ll_rn(P * kUsageFix));
-                } else {
-                    // lane groups may share a step: their additions go one
-                    // group at a time (kept apart by the compiler barriers)
-#pragma unroll
-                    for (int k = 0; k < NP; ++k) {
-                        if (take && grl == k) sU[u - t0] += P;
-                        asm volatile("" ::: "memory");
-                    }
-                }
+                if (take)
+                    atomicAdd(reinterpret_cast<unsigned long long *>(sU64 + (u - t0)),
+                              (unsigned long long)__float2ll_rn(P * kUsageFix));
             }
 
             // F_i off its spread (every step of the tile outside X1 u X2 sees
@@ -318,24 +313,214 @@ __device__ __forceinline__ void narrow_ops(const Graph &G, const Work &W, const 
     }
 }
 
+// Wide ops (a spread past kNarrowSpan steps in the tile): one wave per op,
+// lanes over steps, no work-group barrier.  The producer's signed-tail CDF on
+// the positions of its spread within [t0 - kWideHalo - 1, tb] goes to the wave's
+// LDS row once (positions below it are evaluated directly).  For each
+// step-by-step out-edge (i -> j), the summands are evaluated one by one only
+// on X3 (the tile's steps where F_j(u) or F_j(u) - F_j(u-1) may vary: the
+// consumer's spread and the step after it) and at u = D-1.  Off X3, F_j is
+// the exact constant 0 (below) or 1 (above), so
+//   * below X3 the summands of L_com and dLcom/dth_i are F_i(u) and F_i'(u)
+//     (sums over the producer's row, densities recomputed from z), those of
+//     V_dep and dVdep/dth_i are 0;
+//   * above X3 the summands A(u) of V_dep add up to F_i(b - s) - F_i(a - s)
+//     over [a, b) (a telescoping sum), the others are 0;
+//   * the consumer-side derivatives are 0.
+// The usage of an op off the polynomial path goes to the fixed-point row sU64.
+constexpr int kWideHalo = 8;   // producer positions held below the tile start (delays up to this)
+
+template <int FAM>
+__device__ __forceinline__ float dens_at(int v, int D, float z) {   // density factor, 0 where cdf_at's is
+    const bool off = v < 0 || v >= D - 1 || (FAM != 3 && fabsf(z) > fam_zflush<FAM>());
+    return off ? 0.0f : fam_h<FAM>(z);
+}
+
+// cdf_at without branches (both sides are evaluated, then selected)
+template <int FAM>
+__device__ __forceinline__ void cdf_sel(int v, int D, float mu, float rs, float cinv, float &st, float &Fm,
+                                        float &Fs) {
+    const float z = ((float)v + 0.5f - mu) * rs;
+    float tail, g;
+    fam_tail_h_fl<FAM>(z, tail, g);
+    const bool lo = v < 0, hi = v >= D - 1;
+    st = hi ? -0.0f : lo ? 0.0f : (z >= 0.0f ? -tail : tail);
+    Fm = (lo || hi) ? 0.0f : -g * cinv;
+    Fs = (lo || hi) ? 0.0f : Fm * z;
+}
+template <int FAM>
+__device__ __forceinline__ float st_sel(int v, int D, float mu, float rs) {
+    const float z = ((float)v + 0.5f - mu) * rs;
+    float tail, g;
+    fam_tail_h_fl<FAM>(z, tail, g);
+    return v >= D - 1 ? -0.0f : v < 0 ? 0.0f : (z >= 0.0f ? -tail : tail);
+}
+
+template <int FAM, int BS, int RS>
+__device__ __forceinline__ void wide_ops(const Graph &G, const Work &W, const float *__restrict__ mub,
+                                         const float *__restrict__ rsb, const unsigned char *__restrict__ clsb,
+                                         const OpStage &st, const int *sDirect, const int *sWide, int nWide,
+                                         float *sRows, long long *sU64, int t0, int tb, int tile, int b,
+                                         float &g0, float &g1) {
+    constexpr int NW = BS / 64;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int D = G.D, N = G.N;
+    float *row = sRows + w * RS;          // positions rb .. rb + RS - 1
+    const int rb = t0 - kWideHalo - 1;
+    for (int kk = w; kk < nWide; kk += NW) {
+        const int x = uniform(sWide[kk]);
+        const int i = uniform(st.i[x]), e0 = uniform(st.e0[x]), deg = uniform(st.deg[x]);
+        const bool poly_i = uniform(st.poly[x]) != 0;
+        const int m = uniform(sDirect[x] - 1), s = uniform(st.s[x]), off = uniform(st.off[x]);
+        const float m_i = uniformf(st.mu[x]), rs = uniformf(st.rs[x]);
+        const float cinv = rs * fam_k<FAM>();
+        int pl, ph;   // F_i is read at the bin edges u - s - 1 .. u (u in the tile)
+        spread<FAM>(m_i, rs, t0 - s - 1, tb, pl, ph);
+        const int R0 = max(pl, rb), R1 = min(ph, tb);       // held in the row
+        const bool far = s > kWideHalo;                     // positions below the row: evaluated
+        __asm__ volatile("" ::: "memory");   // the previous op's reads of the row come first
+        for (int v = R0 + lane; v <= R1; v += 64) row[v - rb] = st_sel<FAM>(v, D, m_i, rs);
+        __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // a wave's LDS accesses complete in order
+        auto stv = [&](int v) {   // signed tail of F_i at bin edge v
+            if (far && v < rb && v >= pl && v >= 0) return st_sel<FAM>(v, D, m_i, rs);
+            const float r = row[min(max(v - rb, 0), RS - 1)];
+            const float c = (v >= 0 && (v >= D - 1 || v > ph)) ? -0.0f : 0.0f;   // off the spread
+            return (v >= R0 && v <= R1) ? r : c;
+        };
+
+        // usage P_i^u: 0 off the spread X1 but at u = 0 and D-1
+        if (!poly_i) {
+            const int x1l = max(pl, t0), x1h = min(ph + 1, tb - 1);
+            const int n1 = max(x1h - x1l + 1, 0);
+            for (int x0 = 0; x0 < n1 + 2; x0 += 64) {
+                const int xx = x0 + lane;
+                int u = x1l + xx;
+                bool take = xx < n1 + 2;
+                if (take && xx >= n1) {
+                    u = xx == n1 ? 0 : D - 1;
+                    take = u >= t0 && u < tb && !(u >= x1l && u <= x1h) && !(xx > n1 && u == 0);
+                }
+                if (take) {
+                    const float P = st_mass(stv(u - 1), stv(u));
+                    atomicAdd(reinterpret_cast<unsigned long long *>(sU64 + (u - t0)),
+                              (unsigned long long)__float2ll_rn(P * kUsageFix));
+                }
+            }
+        }
+
+        float pr[6] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+        float cnt = 0.0f;   // below X3 and past the producer's spread: F_i = 1
+        for (int t = 0; t < deg; ++t) {
+            const int e = e0 + t;
+            bool ev;
+            float m_j = 0.0f, rsj = 1.0f;
+            if (off >= 0) {
+                ev = uniform(st.eon[off + t]) != 0;
+                m_j = uniformf(st.emu[off + t]); rsj = uniformf(st.ers[off + t]);
+            } else {
+                const int j = uniform(G.col[e]);
+                ev = !(poly_i && clsb[j]);
+                if (ev) { m_j = uniformf(mub[j]); rsj = uniformf(rsb[j]); }
+            }
+            if (!ev) continue;   // both ends on the polynomial path
+            const float cj = rsj * fam_k<FAM>();
+            int cl, ch;
+            spread<FAM>(m_j, rsj, t0 - 1, tb, cl, ch);
+            const int x3l = max(cl, t0), x3h = min(ch + 1, tb - 1);
+            const int n3 = max(x3h - x3l + 1, 0);
+            float c4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+            // one step u of X3 or u = D-1, with the consumer's signed tails at
+            // u and u-1 and its derivatives at u
+            auto term = [&](int u, float st_j, float st_jm, float Fmj, float Fsj) __attribute__((always_inline)) {
+                const float dS = st_mass(st_jm, st_j);   // F_j(u) - F_j(u-1)
+                const float ss0 = stv(u - s);
+                const float zs = ((float)(u - s) + 0.5f - m_i) * rs;
+                const float Fms = -dens_at<FAM>(u - s, D, zs) * cinv;   // F_i'(u - s)
+                pr[2] = fmaf(-Fms, dS, pr[2]);
+                pr[3] = fmaf(-Fms * zs, dS, pr[3]);
+                if (u < D - 1) {
+                    const float A = st_mass(ss0, stv(u - s + 1));
+                    const float Fi = st_F(stv(u)), Rj = st_1mF(st_j);
+                    const float zi = ((float)u + 0.5f - m_i) * rs;
+                    const float Fmi = -dens_at<FAM>(u, D, zi) * cinv;
+                    pr[0] = fmaf(A, st_F(st_j), pr[0]);
+                    pr[1] = fmaf(Fi, Rj, pr[1]);
+                    pr[4] = fmaf(Fmi, Rj, pr[4]);
+                    pr[5] = fmaf(Fmi * zi, Rj, pr[5]);
+                    c4[0] = fmaf(A, Fmj, c4[0]);
+                    c4[1] = fmaf(A, Fsj, c4[1]);
+                    c4[2] = fmaf(-Fi, Fmj, c4[2]);
+                    c4[3] = fmaf(-Fi, Fsj, c4[3]);
+                } else {
+                    pr[0] += st_1mF(ss0);   // 1 - F_i(D-1-s)
+                }
+            };
+            // X3: lanes over the positions x3l - 1 .. x3h, one evaluation of
+            // F_j each; the step u takes F_j(u-1) from the lane below (lane 0
+            // from lane 63 of the previous pass)
+            float carry = 0.0f;
+            for (int x0 = 0; x0 < n3 + 1 && n3 > 0; x0 += 64) {
+                const int p = x3l - 1 + x0 + lane;
+                float st_j, Fmj, Fsj;
+                cdf_sel<FAM>(p, D, m_j, rsj, cj, st_j, Fmj, Fsj);
+                float stm = __shfl_up(st_j, 1, 64);
+                if (lane == 0) stm = carry;
+                carry = __shfl(st_j, 63, 64);
+                if (x0 + lane >= 1 && x0 + lane <= n3) term(p, st_j, stm, Fmj, Fsj);
+            }
+            // u = D-1 off X3 (F_j(D-1) = 1 by the open end bin)
+            if (D - 1 >= t0 && D - 1 < tb && !(D - 1 >= x3l && D - 1 <= x3h) && lane == 0)
+                term(D - 1, -0.0f, st_sel<FAM>(D - 2, D, m_j, rsj), 0.0f, 0.0f);
+            // below X3: u in [t0, lo), F_j(u) = 0 (u < D-1)
+            const int lo = min(n3 > 0 ? x3l : (cl > tb - 1 ? tb : t0), D - 1);
+            const int q0 = max(t0, pl), q1 = min(lo, ph + 1);
+            float sg = 0.0f, sgz = 0.0f;
+            for (int u = q0 + lane; u < q1; u += 64) {
+                const float z = ((float)u + 0.5f - m_i) * rs;
+                const float g = dens_at<FAM>(u, D, z);
+                pr[1] += st_F(stv(u));
+                sg += g;
+                sgz = fmaf(g, z, sgz);
+            }
+            pr[4] = fmaf(-cinv, sg, pr[4]);
+            pr[5] = fmaf(-cinv, sgz, pr[5]);
+            cnt += (float)max(lo - max(t0, ph + 1), 0);
+            // above X3: u in [a, bb), F_j(u) = 1
+            const int a = n3 > 0 ? x3h + 1 : (cl > tb - 1 ? tb : t0), bb = min(tb, D - 1);
+            if (lane == 0 && a < bb) pr[0] += st_mass(stv(a - s), stv(bb - s));
+            const float r = wave_sum4(c4[0], c4[1], c4[2], c4[3], lane);
+            if (lane < 4) W.cpart[(((size_t)b * G.E + e) * G.ntiles + tile) * kCP + wave4_comp(lane)] = r;
+        }
+        if (lane == 0) pr[1] += cnt;
+        const float ra = wave_sum4(pr[0], pr[1], pr[2], pr[3], lane);
+        const float rc = wave_sum2(pr[4], pr[5], lane);
+        float *pp = W.ppart + (((size_t)b * N + i) * G.ntiles + tile) * kPP;
+        if (lane < 4) pp[wave4_comp(lane)] = m > 0 ? ra : 0.0f;
+        if (lane < 2) pp[4 + lane] = m > 0 ? rc : 0.0f;
+        if (m > 0 && lane == 0) g0 += ra;   // V_dep
+        if (m > 0 && lane == 2) g1 += ra;   // L_com
+    }
+}
+
 template <int FAM, int BS, int SPT>
-__global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ mu,
+__global__ __launch_bounds__(BS) __attribute__((amdgpu_waves_per_eu(4))) void k_ops(Graph G, const float *__restrict__ mu,
                                             const float *__restrict__ sigma, Work W) {
     constexpr int TILE = BS * SPT;
-    constexpr int WIN = TILE + kHalo + 1;
     constexpr int NW = BS / 64;
-    // the narrow ops' usage rows (one per wave), then the row path's window
-    constexpr int kBuf = NW * TILE > 3 * WIN ? NW * TILE : 3 * WIN;
-    __shared__ float sBuf[kBuf];
-    float *sT = sBuf, *sFm = sBuf + WIN, *sFs = sBuf + 2 * WIN;
+    constexpr int RS = TILE + kWideHalo + 2;   // a wave's row of producer values: positions t0-kWideHalo-1 .. t0+TILE
+    constexpr int WIN = TILE + kHalo + 1;      // the row path's window
+    constexpr int kBuf = NW * RS > 3 * WIN ? NW * RS : 3 * WIN;
+    __shared__ long long sU64[TILE];           // the tile's usage, 2^-40 units
+    __shared__ float sBuf[kBuf];               // the wide ops' rows, then the row path's window
+    float *sRows = sBuf, *sT = sBuf, *sFm = sBuf + WIN, *sFs = sBuf + 2 * WIN;
     __shared__ float sRed[2][BS / 64][8];
     __shared__ float sPrev[3];
-    constexpr int kEdgeBatch = 16;
+    constexpr int kEdgeBatch = 8;
     __shared__ float sCp[2][kEdgeBatch][NW][4];   // wave partials of the out-edges' derivatives
     __shared__ int sCpE[2][kEdgeBatch];           // their edges
     __shared__ float sCpC[2][kEdgeBatch];         // and fam_k/sigma_j
     __shared__ float sLast[NW][SPT][3];           // each wave's last S_i(u) terms (lower, upper, count)
-    int cpar = 0;
+    int cpar = 0, par = 0;
 
     // work-group x serves restart x mod B (the XCDs receive work-groups in
     // turn: with B a multiple of 8 a restart's gathered means and widths stay
@@ -356,7 +541,6 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
     float accU[SPT];
 #pragma unroll
     for (int k = 0; k < SPT; ++k) accU[k] = 0.0f;
-    int par = 0;
 
     // Groups without step-by-step work leave nothing here: their readers skip
     // them (group and op flags).  Otherwise thread t looks at op q0 + t*parts
@@ -367,18 +551,20 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
     if (G.nar_on && !(W.gnar[(size_t)b * G.ngroups + grp] & kNarLeft)) return;
     // Each op is sorted for this tile by its thread: nothing to do (no
     // step-by-step work), constant (every spread misses the tile: its terms
-    // are integer counts, finished here), tiny or narrow (lane groups, below)
-    // or wide (the row path).
+    // are integer counts, finished here), tiny or narrow (lane groups, below),
+    // wide (a wave each) or the row path.
     __shared__ int sDirect[BS];   // 1 + number of step-by-step out-edges
     __shared__ unsigned char sCls[BS];
     __shared__ int sConst[4];     // constant ops: V_dep, L_com, P^0, P^{D-1}
+    __shared__ int sWide[BS], sWcnt[NW];   // the wide ops in list order
     __shared__ int sOpI[BS], sOpE0[BS], sOpDeg[BS], sOpS[BS], sOpOff[BS], sWsum[NW];
-    __shared__ float sOpMu[BS], sOpRs[BS], sEmu[kStage], sErs[kStage];
-    __shared__ unsigned char sOpPoly[BS], sEon[kStage];
+    __shared__ float sOpMu[BS], sOpRs[BS], sEmu[kStageOps], sErs[kStageOps];
+    __shared__ unsigned char sOpPoly[BS], sEon[kStageOps];
     const OpStage st{sOpI, sOpE0, sOpDeg, sOpS, sOpOff, sOpMu, sOpRs, sOpPoly, sEmu, sErs, sEon};
     const unsigned char *clsb = W.cls + (size_t)b * N;
     const int tb = min(t0 + TILE, D);   // the tile's steps are [t0, tb)
     if (tid < 4) sConst[tid] = 0;
+    for (int p = tid; p < TILE; p += BS) sU64[p] = 0;
     {
         const int lane = tid & 63, w = tid >> 6;
         int i = 0, e0 = 0, deg = 0, s = 0;
@@ -405,7 +591,7 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
         __syncthreads();
         int off = x - deg;
         for (int k = 0; k < w; ++k) off += sWsum[k];
-        if (!on || off + deg > kStage) off = -1;
+        if (!on || off + deg > kStageOps) off = -1;
         sOpI[tid] = i; sOpE0[tid] = e0; sOpDeg[tid] = deg; sOpS[tid] = s; sOpOff[tid] = off;
         sOpMu[tid] = m_i; sOpRs[tid] = rs; sOpPoly[tid] = poly_i ? 1 : 0;
 
@@ -432,7 +618,7 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
                 const bool fresh = (k < 1 || u != us[0]) && (k < 2 || u != us[1]);
                 ua[k] = (fresh && u >= t0 && u < tb && u < D - 1) ? Fc(u - s + 1) - Fc(u - s) : 0;
             }
-            int m = 0, cnt = 0, dep = 0;
+            int m = 0, cnt = 0, dep = 0, sum3 = 0;
             for (int e = e0; e < e1; ++e) {
                 const int j = G.col[e];
                 const bool sbs = !(poly_i && clsb[j]);
@@ -447,6 +633,7 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
                 spread<FAM>(m_j, rsj, t0 - 1, tb, cl, ch);
                 const int n3 = min(ch + 1, tb - 1) - max(cl, t0) + 1;
                 span = max(span, n3);
+                sum3 += max(n3, 0);
                 act = act || n3 > 0;
                 // F_i(u) (1 - F_j(u)) = 1 for ph < u < cl
                 cnt += max(min(min(tb, D - 1), cl) - max(t0, ph + 1), 0);
@@ -454,10 +641,14 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
                 for (int k = 0; k < 3; ++k) dep += ua[k] * (us[k] > ch ? 1 : 0);
             }
             flag = 1 + m;
+            // wide: one wave per op when the consumers' spreads cover less
+            // than half the tile on average, else the row path (its producer
+            // values serve every edge at every step of the tile)
             c = !act ? kConst
                 : span <= kTinySpan ? kTiny
                 : span <= kMidSpan ? kMid
-                : span <= kNarrowSpan ? kNarrow : kWide;
+                : span <= kNarrowSpan ? kNarrow
+                : (m == 0 || 2 * sum3 < m * (tb - t0)) ? kWide : kRow;
             if (c == kConst) {
                 // no records: every derivative is 0 here, and the readers skip
                 // this tile (tile_prod_rec / tile_cons_rec are false for it)
@@ -472,40 +663,42 @@ __global__ __launch_bounds__(BS) void k_ops(Graph G, const float *__restrict__ m
         }
         sDirect[tid] = flag;
         sCls[tid] = c;
+        const unsigned long long bw = __ballot(c == kWide);
+        if (lane == 0) sWcnt[w] = __popcll(bw);
+        __syncthreads();
+        int ow = __popcll(bw & ((1ull << lane) - 1ull));
+        for (int k = 0; k < w; ++k) ow += sWcnt[k];
+        if (c == kWide) sWide[ow] = tid;
     }
     float gsum0 = 0.0f, gsum1 = 0.0f;  // V_dep, L_com of the work-group (threads 0, 1)
     __syncthreads();
 
     // Narrow ops: the shortest spreads four at a time per wave, then two, the
-    // others one at a time.  Each wave's usage row is folded into the step owners' sums
-    // before the row path takes the buffer.
-    __shared__ float sGw[NW][2];          // the narrow ops' V_dep and L_com
+    // others one at a time; then the wide ops, one per wave.
+    __shared__ float sGw[NW][2];          // the narrow and wide ops' V_dep and L_com
     {
         const int lane = tid & 63, w = tid >> 6;
-        float *sU = sBuf + w * TILE;
-        for (int p = lane; p < TILE; p += 64) sU[p] = 0.0f;
+        int nWide = 0;
+#pragma unroll
+        for (int k = 0; k < NW; ++k) nWide += sWcnt[k];
         float g0 = 0.0f, g1 = 0.0f;
-        narrow_ops<FAM, 4, BS>(G, W, mub, rsb, clsb, st, sCls, sDirect, sU, nullptr, kTiny, nq, t0, tb, tile, b,
-                               g0, g1);
-        narrow_ops<FAM, 2, BS>(G, W, mub, rsb, clsb, st, sCls, sDirect, sU, nullptr, kMid, nq, t0, tb, tile, b,
-                               g0, g1);
-        narrow_ops<FAM, 1, BS>(G, W, mub, rsb, clsb, st, sCls, sDirect, sU, nullptr, kNarrow, nq, t0, tb, tile, b,
-                               g0, g1);
+        narrow_ops<FAM, 4, BS>(G, W, mub, rsb, clsb, st, sCls, sDirect, sU64, kTiny, nq, t0, tb, tile, b, g0, g1);
+        narrow_ops<FAM, 2, BS>(G, W, mub, rsb, clsb, st, sCls, sDirect, sU64, kMid, nq, t0, tb, tile, b, g0, g1);
+        narrow_ops<FAM, 1, BS>(G, W, mub, rsb, clsb, st, sCls, sDirect, sU64, kNarrow, nq, t0, tb, tile, b, g0,
+                               g1);
+        wide_ops<FAM, BS, RS>(G, W, mub, rsb, clsb, st, sDirect, sWide, nWide, sRows, sU64, t0, tb, tile, b, g0,
+                              g1);
         const float s0 = wave_sum((lane & 15) == 0 ? g0 : 0.0f), s1 = wave_sum((lane & 15) == 2 ? g1 : 0.0f);
         if (lane == 0) { sGw[w][0] = s0; sGw[w][1] = s1; }
     }
     __syncthreads();
 #pragma unroll
-    for (int k = 0; k < SPT; ++k) {
-        float v = sBuf[k * BS + tid];
-#pragma unroll
-        for (int w = 1; w < NW; ++w) v += sBuf[w * TILE + k * BS + tid];
-        accU[k] += v;
-    }
-    __syncthreads();
+    for (int k = 0; k < SPT; ++k) accU[k] += (float)((double)sU64[k * BS + tid] * (1.0 / 1099511627776.0));
 
+    // Row path: the other wide ops one at a time by the whole work-group
+    // (the op kernel's description at the top of this file).
     for (int x = 0; x < nq; ++x) {
-        if (sCls[x] != kWide) continue;
+        if (sCls[x] != kRow) continue;
         const int i = uniform(sOpI[x]);
         const int e0 = uniform(sOpE0[x]), e1 = e0 + uniform(sOpDeg[x]);
         const int off = uniform(sOpOff[x]);
@@ -850,11 +1043,11 @@ __global__ __launch_bounds__(kNarBS) void k_group(Graph G, const float *__restri
     if (tid == 0) W.gnar[bg] = (sAny[0] ? kNarLeft : 0u) | (sAny[1] ? kNarTaken : 0u);
     if (!sAny[1]) return;
     float g0 = 0.0f, g1 = 0.0f;
-    narrow_ops<FAM, 4, BS, true>(G, W, mub, rsb, clsb, st, sCls, sDirect, nullptr, sRow, kTiny, nq, 0, D, 0, b,
+    narrow_ops<FAM, 4, BS, true>(G, W, mub, rsb, clsb, st, sCls, sDirect, sRow, kTiny, nq, 0, D, 0, b,
                                  g0, g1);
-    narrow_ops<FAM, 2, BS, true>(G, W, mub, rsb, clsb, st, sCls, sDirect, nullptr, sRow, kMid, nq, 0, D, 0, b,
+    narrow_ops<FAM, 2, BS, true>(G, W, mub, rsb, clsb, st, sCls, sDirect, sRow, kMid, nq, 0, D, 0, b,
                                  g0, g1);
-    narrow_ops<FAM, 1, BS, true>(G, W, mub, rsb, clsb, st, sCls, sDirect, nullptr, sRow, kNarrow, nq, 0, D, 0, b,
+    narrow_ops<FAM, 1, BS, true>(G, W, mub, rsb, clsb, st, sCls, sDirect, sRow, kNarrow, nq, 0, D, 0, b,
                                  g0, g1);
     const float s0 = wave_sum((lane & 15) == 0 ? g0 : 0.0f), s1 = wave_sum((lane & 15) == 2 ? g1 : 0.0f);
     if (lane == 0) { sGw[w][0] = s0; sGw[w][1] = s1; }
