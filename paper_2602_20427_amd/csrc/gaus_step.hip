@@ -376,13 +376,11 @@ __device__ __forceinline__ void wide_ops(const Graph &G, const Work &W, const fl
         const float cinv = rs * fam_k<FAM>();
         int pl, ph;   // F_i is read at the bin edges u - s - 1 .. u (u in the tile)
         spread<FAM>(m_i, rs, t0 - s - 1, tb, pl, ph);
-        const int R0 = max(pl, rb), R1 = min(ph, tb);       // held in the row
-        const bool far = s > kWideHalo;                     // positions below the row: evaluated
+        const int R0 = max(pl, rb), R1 = min(ph, tb);       // held in the row (s <= kWideHalo)
         __asm__ volatile("" ::: "memory");   // the previous op's reads of the row come first
         for (int v = R0 + lane; v <= R1; v += 64) row[v - rb] = st_sel<FAM>(v, D, m_i, rs);
         __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // a wave's LDS accesses complete in order
-        auto stv = [&](int v) {   // signed tail of F_i at bin edge v
-            if (far && v < rb && v >= pl && v >= 0) return st_sel<FAM>(v, D, m_i, rs);
+        auto stv = [&](int v) {   // signed tail of F_i at bin edge v in [t0 - s - 1, tb]
             const float r = row[min(max(v - rb, 0), RS - 1)];
             const float c = (v >= 0 && (v >= D - 1 || v > ph)) ? -0.0f : 0.0f;   // off the spread
             return (v >= R0 && v <= R1) ? r : c;
@@ -431,6 +429,8 @@ __device__ __forceinline__ void wide_ops(const Graph &G, const Work &W, const fl
             float c4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
             // one step u of X3 or u = D-1, with the consumer's signed tails at
             // u and u-1 and its derivatives at u
+            // (at u = D-1, F_j = 1 and F_j' = 0 make every summand but V_dep's
+            // and dVdep/dth_i's vanish by themselves; V_dep takes 1 - F_i(D-1-s))
             auto term = [&](int u, float st_j, float st_jm, float Fmj, float Fsj) __attribute__((always_inline)) {
                 const float dS = st_mass(st_jm, st_j);   // F_j(u) - F_j(u-1)
                 const float ss0 = stv(u - s);
@@ -438,22 +438,19 @@ __device__ __forceinline__ void wide_ops(const Graph &G, const Work &W, const fl
                 const float Fms = -dens_at<FAM>(u - s, D, zs) * cinv;   // F_i'(u - s)
                 pr[2] = fmaf(-Fms, dS, pr[2]);
                 pr[3] = fmaf(-Fms * zs, dS, pr[3]);
-                if (u < D - 1) {
-                    const float A = st_mass(ss0, stv(u - s + 1));
-                    const float Fi = st_F(stv(u)), Rj = st_1mF(st_j);
-                    const float zi = ((float)u + 0.5f - m_i) * rs;
-                    const float Fmi = -dens_at<FAM>(u, D, zi) * cinv;
-                    pr[0] = fmaf(A, st_F(st_j), pr[0]);
-                    pr[1] = fmaf(Fi, Rj, pr[1]);
-                    pr[4] = fmaf(Fmi, Rj, pr[4]);
-                    pr[5] = fmaf(Fmi * zi, Rj, pr[5]);
-                    c4[0] = fmaf(A, Fmj, c4[0]);
-                    c4[1] = fmaf(A, Fsj, c4[1]);
-                    c4[2] = fmaf(-Fi, Fmj, c4[2]);
-                    c4[3] = fmaf(-Fi, Fsj, c4[3]);
-                } else {
-                    pr[0] += st_1mF(ss0);   // 1 - F_i(D-1-s)
-                }
+                const bool last = u >= D - 1;
+                const float A = st_mass(ss0, stv(u - s + 1));
+                const float Fi = st_F(stv(u)), Rj = st_1mF(st_j);
+                const float zi = ((float)u + 0.5f - m_i) * rs;
+                const float Fmi = -dens_at<FAM>(u, D, zi) * cinv;
+                pr[0] = fmaf(last ? st_1mF(ss0) : A, last ? 1.0f : st_F(st_j), pr[0]);
+                pr[1] = fmaf(Fi, Rj, pr[1]);
+                pr[4] = fmaf(Fmi, Rj, pr[4]);
+                pr[5] = fmaf(Fmi * zi, Rj, pr[5]);
+                c4[0] = fmaf(A, Fmj, c4[0]);
+                c4[1] = fmaf(A, Fsj, c4[1]);
+                c4[2] = fmaf(-Fi, Fmj, c4[2]);
+                c4[3] = fmaf(-Fi, Fsj, c4[3]);
             };
             // X3: lanes over the positions x3l - 1 .. x3h, one evaluation of
             // F_j each; the step u takes F_j(u-1) from the lane below (lane 0
@@ -642,13 +639,14 @@ __global__ __launch_bounds__(BS) __attribute__((amdgpu_waves_per_eu(4))) void k_
             }
             flag = 1 + m;
             // wide: one wave per op when the consumers' spreads cover less
-            // than half the tile on average, else the row path (its producer
-            // values serve every edge at every step of the tile)
+            // than half the tile on average (and the delay fits the wave's
+            // row), else the row path (its producer values serve every edge
+            // at every step of the tile)
             c = !act ? kConst
                 : span <= kTinySpan ? kTiny
                 : span <= kMidSpan ? kMid
                 : span <= kNarrowSpan ? kNarrow
-                : (m == 0 || 2 * sum3 < m * (tb - t0)) ? kWide : kRow;
+                : (s <= kWideHalo && (m == 0 || 2 * sum3 < m * (tb - t0))) ? kWide : kRow;
             if (c == kConst) {
                 // no records: every derivative is 0 here, and the readers skip
                 // this tile (tile_prod_rec / tile_cons_rec are false for it)
