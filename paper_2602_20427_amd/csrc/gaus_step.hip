@@ -329,6 +329,7 @@ __device__ __forceinline__ void narrow_ops(const Graph &G, const Work &W, const 
 //   * the consumer-side derivatives are 0.
 // The usage of an op off the polynomial path goes to the fixed-point row sU64.
 constexpr int kWideHalo = 8;   // producer positions held below the tile start (delays up to this)
+constexpr float kGsumFix = 4294967296.0f;   // 2^32
 
 template <int FAM>
 __device__ __forceinline__ float dens_at(int v, int D, float z) {   // density factor, 0 where cdf_at's is
@@ -360,14 +361,19 @@ template <int FAM, int BS, int RS>
 __device__ __forceinline__ void wide_ops(const Graph &G, const Work &W, const float *__restrict__ mub,
                                          const float *__restrict__ rsb, const unsigned char *__restrict__ clsb,
                                          const OpStage &st, const int *sDirect, const int *sWide, int nWide,
-                                         float *sRows, long long *sU64, int t0, int tb, int tile, int b,
-                                         float &g0, float &g1) {
-    constexpr int NW = BS / 64;
+                                         int *sNext, float *sRows, long long *sU64, long long *sG64, int t0,
+                                         int tb, int tile, int b) {
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int D = G.D, N = G.N;
     float *row = sRows + w * RS;          // positions rb .. rb + RS - 1
     const int rb = t0 - kWideHalo - 1;
-    for (int kk = w; kk < nWide; kk += NW) {
+    // the waves take the next op of the list as they come free (the results
+    // do not depend on which wave takes which: per-op records, fixed-point sums)
+    while (true) {
+        int kk = 0;
+        if (lane == 0) kk = atomicAdd(sNext, 1);
+        kk = __shfl(kk, 0, 64);
+        if (kk >= nWide) break;
         const int x = uniform(sWide[kk]);
         const int i = uniform(st.i[x]), e0 = uniform(st.e0[x]), deg = uniform(st.deg[x]);
         const bool poly_i = uniform(st.poly[x]) != 0;
@@ -494,8 +500,11 @@ __device__ __forceinline__ void wide_ops(const Graph &G, const Work &W, const fl
         float *pp = W.ppart + (((size_t)b * N + i) * G.ntiles + tile) * kPP;
         if (lane < 4) pp[wave4_comp(lane)] = m > 0 ? ra : 0.0f;
         if (lane < 2) pp[4 + lane] = m > 0 ? rc : 0.0f;
-        if (m > 0 && lane == 0) g0 += ra;   // V_dep
-        if (m > 0 && lane == 2) g1 += ra;   // L_com
+        // V_dep and L_com of the work-group in fixed point (2^-32 units)
+        if (m > 0 && lane == 0) atomicAdd(reinterpret_cast<unsigned long long *>(sG64),
+                                          (unsigned long long)__float2ll_rn(ra * kGsumFix));
+        if (m > 0 && lane == 2) atomicAdd(reinterpret_cast<unsigned long long *>(sG64 + 1),
+                                          (unsigned long long)__float2ll_rn(ra * kGsumFix));
     }
 }
 
@@ -554,6 +563,8 @@ __global__ __launch_bounds__(BS) __attribute__((amdgpu_waves_per_eu(4))) void k_
     __shared__ unsigned char sCls[BS];
     __shared__ int sConst[4];     // constant ops: V_dep, L_com, P^0, P^{D-1}
     __shared__ int sWide[BS], sWcnt[NW];   // the wide ops in list order
+    __shared__ int sNextWide;
+    __shared__ long long sG64[2];          // the wide ops' V_dep and L_com, 2^-32 units
     __shared__ int sOpI[BS], sOpE0[BS], sOpDeg[BS], sOpS[BS], sOpOff[BS], sWsum[NW];
     __shared__ float sOpMu[BS], sOpRs[BS], sEmu[kStageOps], sErs[kStageOps];
     __shared__ unsigned char sOpPoly[BS], sEon[kStageOps];
@@ -561,6 +572,8 @@ __global__ __launch_bounds__(BS) __attribute__((amdgpu_waves_per_eu(4))) void k_
     const unsigned char *clsb = W.cls + (size_t)b * N;
     const int tb = min(t0 + TILE, D);   // the tile's steps are [t0, tb)
     if (tid < 4) sConst[tid] = 0;
+    if (tid < 2) sG64[tid] = 0;
+    if (tid == 0) sNextWide = 0;
     for (int p = tid; p < TILE; p += BS) sU64[p] = 0;
     {
         const int lane = tid & 63, w = tid >> 6;
@@ -673,7 +686,7 @@ __global__ __launch_bounds__(BS) __attribute__((amdgpu_waves_per_eu(4))) void k_
 
     // Narrow ops: the shortest spreads four at a time per wave, then two, the
     // others one at a time; then the wide ops, one per wave.
-    __shared__ float sGw[NW][2];          // the narrow and wide ops' V_dep and L_com
+    __shared__ float sGw[NW][2];          // the narrow ops' V_dep and L_com per wave
     {
         const int lane = tid & 63, w = tid >> 6;
         int nWide = 0;
@@ -684,8 +697,8 @@ __global__ __launch_bounds__(BS) __attribute__((amdgpu_waves_per_eu(4))) void k_
         narrow_ops<FAM, 2, BS>(G, W, mub, rsb, clsb, st, sCls, sDirect, sU64, kMid, nq, t0, tb, tile, b, g0, g1);
         narrow_ops<FAM, 1, BS>(G, W, mub, rsb, clsb, st, sCls, sDirect, sU64, kNarrow, nq, t0, tb, tile, b, g0,
                                g1);
-        wide_ops<FAM, BS, RS>(G, W, mub, rsb, clsb, st, sDirect, sWide, nWide, sRows, sU64, t0, tb, tile, b, g0,
-                              g1);
+        wide_ops<FAM, BS, RS>(G, W, mub, rsb, clsb, st, sDirect, sWide, nWide, &sNextWide, sRows, sU64, sG64, t0, tb,
+                              tile, b);
         const float s0 = wave_sum((lane & 15) == 0 ? g0 : 0.0f), s1 = wave_sum((lane & 15) == 2 ? g1 : 0.0f);
         if (lane == 0) { sGw[w][0] = s0; sGw[w][1] = s1; }
     }
@@ -898,6 +911,7 @@ __global__ __launch_bounds__(BS) __attribute__((amdgpu_waves_per_eu(4))) void k_
 #pragma unroll
         for (int w = 1; w < NW; ++w) v += sGw[w][tid];
         v += (float)sConst[tid];
+        v += (float)((double)sG64[tid] * (1.0 / 4294967296.0));
         if (tid == 0) gsum0 += v; else gsum1 += v;
     }
     {
