@@ -513,11 +513,13 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     g.nar_on = (ntiles > 1 && h.D <= kNarMaxD) ? 1 : 0;
     {
         // a small op-kernel grid (few tiles) over many ops leaves the last round
-        // of work-groups mostly idle: split each (group, tile) over up to 4
-        // work-groups (small problems keep one: their op kernel is short)
+        // of work-groups mostly idle: split each (group, tile) over 2
+        // work-groups (small problems keep one: their op kernel is short).
+        // Each part writes a usage row of its own, which k_usage reads: 4
+        // parts cost more there than they saved in the op kernel.
         const long long wgs = (long long)g.ngroups * ntiles * B;
         g.parts = (wgs >= 4096 || (long long)h.N * B < (1 << 18))
-                      ? 1 : (int)std::min<long long>(4, (8192 + wgs - 1) / wgs);
+                      ? 1 : (int)std::min<long long>(2, (8192 + wgs - 1) / wgs);
     }
     if (c->pa.enabled) {
         // polynomial work-groups per op group: at most 16 ops per wave, so that
