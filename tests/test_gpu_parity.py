@@ -109,6 +109,26 @@ def test_loss_grad_large_after_steps():
     _check(p, mu_h, sg_h, lam_h, hp, [0, 1, 2, B - 1], "large/after 20 steps")
 
 
+def test_loss_grad_tight_horizon_full_size():
+    """The 50k-op workload with the tight horizon (D = longest delay-weighted
+    path + 8 = 793: one step tile) at full size from the paper's
+    initialization, as bench.py --workload large-tight times it: a quarter of
+    the (restart, op) pairs off the chunk polynomials, most of them wide
+    (one wave per op, or the row path when the consumers span the tile),
+    polynomial producers with such consumers, and the op kernel split over
+    two work-groups per group."""
+    cfg = CONFIGS["large-tight"]
+    p = make_problem(cfg, seed=0)
+    B = cfg.B
+    u = restart_uniforms(p.n_ops, B, seed=0)
+    mu, sg, rc = oracle.init_state(p, B, u)
+    assert rc == 0
+    mu, sg = mu.astype(np.float32), sg.astype(np.float32)
+    hp = bd.default_hparams()
+    hp.lr = cfg.lr
+    _check(p, mu, sg, np.full((B, 3), hp.lambda0, np.float32), hp, [0, 3, B - 1], "large-tight/init")
+
+
 @pytest.mark.parametrize("sigma,restarts", [(0.4, range(8)), (3.0, [0, 5])])
 def test_loss_grad_large_sharpened(sigma, restarts):
     """The 50k-op workload at full size in a sharpened state (the paper's
