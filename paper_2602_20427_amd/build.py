@@ -11,7 +11,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libgaus.so")
 MICROBENCH = os.path.join(PKG, "gaus_microbench")
-SOURCES = ["gaus_host.cpp", "gaus_kernels.hip", "gaus_step.hip", "gaus_poly.hip"]
+SOURCES = ["gaus_host.cpp", "gaus_kernels.hip", "gaus_step.hip", "gaus_poly.hip", "gaus_laplace.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 # Packed-FP32 instructions are disabled for device code (they are not needed:

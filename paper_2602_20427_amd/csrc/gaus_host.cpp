@@ -510,7 +510,10 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     g.ngroups = (int)h.grp_start.size() - 1;
     // the narrow kernel pays off where the op kernel would visit each op in
     // several tiles; its usage row must fit LDS
-    g.nar_on = (ntiles > 1 && h.D <= kNarMaxD) ? 1 : 0;
+    // Laplace start times: the forward edges in closed form (the op kernel
+    // keeps the usage), so the narrow kernel has nothing to take
+    g.lap_on = hp.family == 2 ? 1 : 0;
+    g.nar_on = (ntiles > 1 && h.D <= kNarMaxD && !g.lap_on) ? 1 : 0;
     {
         // a small op-kernel grid (few tiles) over many ops leaves the last round
         // of work-groups mostly idle: split each (group, tile) over 2
@@ -694,6 +697,7 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     AL(gnar, (size_t)B * g.ngroups);
     AL(Unar, g.nar_on ? (size_t)B * g.ngroups * h.D : 1);
     AL(gsum_nar, (size_t)B * g.ngroups * 2);
+    AL(gsum_lap, g.lap_on ? (size_t)B * g.ngroups * 2 : 1);
     AL(gsum_ops, (size_t)B * g.ngroups * g.parts * ntiles * 2);
     AL(gsum_poly, (size_t)std::max(c->poly_slots, 1) * 2);
     AL(gsel, BN);

@@ -111,6 +111,7 @@ struct Graph {
     int leg_ring;                        // 1: II = 0 legalization through the LDS ring (k_legalize_ring)
     int nar_on;                          // 1: short-spread step-by-step ops go to k_group (several
                                          // op-kernel tiles and D <= kNarMaxD)
+    int lap_on;                          // 1: Laplace start times: the edge terms in closed form (k_lap_edges)
     int leg_ring_items, leg_ring_over;   // items and overflow predecessors one ring half holds
     int leg_nbatch;                      // ring batches: contiguous ranges of the items of levels >= 1
     const int *leg_batch;                // [nbatch+1][3] level of the first item, first item, first
@@ -174,6 +175,7 @@ struct Work {
                            //               (kNarLeft, kNarTaken); valid where gbits has kGbStep
     float *Unar;           // [B][ngroups][D]  usage of the ops k_group took
     float *gsum_nar;       // [B][ngroups][2]  their V_dep, L_com
+    float *gsum_lap;       // [B][ngroups][2]  V_dep, L_com of the group's edges in closed form (Laplace)
     unsigned char *ptier;  // [B][N]        polynomial op: tier of its vectors, the smallest over
                            //               itself and its polynomial consumers (highest degree)
     unsigned *gbits;  // [B][ngroups]      work of the group this iteration (k_group):
@@ -233,6 +235,8 @@ hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const 
 
 // Per-step kernels (gaus_step.hip: step by step; gaus_poly.hip: chunk polynomials).
 hipError_t launch_group(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu, hipStream_t st);
+// Laplace start times: every forward edge's terms in closed form (records in ppoly / cpoly, sums in gsum_lap).
+hipError_t launch_lap_edges(const Graph &g, const Work &w, const float *mu, const float *sigma, hipStream_t st);
 hipError_t launch_ops(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu, const float *sigma,
                       hipStream_t st);
 hipError_t launch_back(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu, const float *sigma,

@@ -592,6 +592,7 @@ __global__ __launch_bounds__(kCombineBS) void k_combine(Graph G, PolyArgs pa, Wo
             for (int tl = 0; tl < G.parts * G.ntiles; ++tl) { vdep += go[2 * tl]; lcom += go[2 * tl + 1]; }
         }
         if (nar & kNarTaken) { vdep += W.gsum_nar[bg * 2]; lcom += W.gsum_nar[bg * 2 + 1]; }
+        if (G.lap_on) { vdep += W.gsum_lap[bg * 2]; lcom += W.gsum_lap[bg * 2 + 1]; }
     }
     const size_t nbp = (size_t)G.nb * G.ntiles;
     const float *bp = W.bpart + (size_t)b * nbp * kBP;
@@ -676,7 +677,7 @@ __global__ __launch_bounds__(256) void k_gather_big(Graph G, Work W, HP hp, cons
     for (int q = G.pred_ptr[i] + tid; q < G.pred_ptr[i + 1]; q += 256) {
         const int e = G.pred_eid[q];
         const size_t bs = (size_t)b * N + G.pred_src[q];
-        if ((poly_i && W.cls[bs]) || W.dflag[bs] == 2) {   // single record of the edge
+        if ((poly_i && W.cls[bs]) || W.dflag[bs] == 2 || G.lap_on) {   // single record of the edge
             const float *cp = W.cpoly + ((size_t)b * G.E + e) * kCP;
             for (int c = 0; c < 4; ++c) acc[c] += cp[c];
         } else {
@@ -765,7 +766,7 @@ __global__ __launch_bounds__(256) void k_final(Graph G, Work W, HP hp, const flo
     };
     double dm = 0.0, ds = 0.0, cm = 0.0, cs = 0.0;
     const int dfl = W.dflag[bi];   // 1: op-kernel records per tile, 2: narrow kernel's single record
-    if (dfl == 1) {
+    if (dfl == 1 && !G.lap_on) {   // (Laplace: the producer terms are all in the closed-form record)
         const float *pp = W.ppart + bi * nt * kPP;
         const int lat_i = G.delay[i];
         for (int tl = 0; tl < nt; ++tl) {
@@ -776,7 +777,7 @@ __global__ __launch_bounds__(256) void k_final(Graph G, Work W, HP hp, const flo
         }
     }
     const bool poly_i = W.cls[bi] != 0;
-    if (poly_i || dfl == 2) {   // single producer record (polynomial path, or the narrow kernel)
+    if (poly_i || dfl == 2 || G.lap_on) {   // single producer record (polynomial path, narrow kernel, Laplace edges)
         const float *ppy = W.ppoly + bi * kPP;
         dm += ppy[2]; ds += ppy[3]; cm += ppy[4]; cs += ppy[5];
     }
@@ -799,7 +800,7 @@ __global__ __launch_bounds__(256) void k_final(Graph G, Work W, HP hp, const flo
 #pragma unroll
         for (int k = 0; k < kInB; ++k) {
             const size_t bs = (size_t)b * N + sv[k];
-            one[k] = (poly_i && W.cls[bs]) || W.dflag[bs] == 2;   // single record of the edge
+            one[k] = (poly_i && W.cls[bs]) || W.dflag[bs] == 2 || G.lap_on;   // single record of the edge
             r4[k] = *reinterpret_cast<const float4 *>(W.cpoly + ((size_t)b * G.E + ev[k]) * kCP);
         }
 #pragma unroll
@@ -1634,6 +1635,7 @@ hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const 
     if (a.ops_begin) (void)hipEventRecord(a.ops_begin, st);
     if ((e = launch_group(g, w, lc, a.mu, st)) != hipSuccess) return e;
     if ((e = launch_ops(g, w, lc, a.mu, a.sigma, st)) != hipSuccess) return e;
+    if (g.lap_on && (e = launch_lap_edges(g, w, a.mu, a.sigma, st)) != hipSuccess) return e;
     if (a.ops_end) (void)hipEventRecord(a.ops_end, st);
     if (pa.enabled) {
         if (a.poly_begin) (void)hipEventRecord(a.poly_begin, st);

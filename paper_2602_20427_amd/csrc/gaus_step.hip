@@ -58,7 +58,7 @@ __device__ __forceinline__ void spread(float mu, float rs, int a, int b, int &lo
 }
 
 // classes of an op in a step tile
-enum : unsigned char { kNone = 0, kConst = 1, kTiny = 2, kNarrow = 3, kWide = 4, kMid = 5, kRow = 6 };
+enum : unsigned char { kNone = 0, kConst = 1, kTiny = 2, kNarrow = 3, kWide = 4, kMid = 5, kRow = 6, kLapU = 7 };
 
 // A group's ops and their consumers as the op and group kernels read them,
 // staged in LDS once per work-group (the consumers of at most kStage edges in
@@ -213,7 +213,7 @@ __device__ __forceinline__ void narrow_ops(const Graph &G, const Work &W, const 
                     m_j = st.emu[off + t]; rsj = st.ers[off + t];
                 } else if (ev) {
                     const int j = G.col[e];
-                    ev = !(poly_i && clsb[j]);
+                    ev = !(poly_i && clsb[j]) && !G.lap_on;
                     if (ev) { m_j = mub[j]; rsj = rsb[j]; }
                 }
                 const float cj = rsj * fam_k<FAM>();
@@ -423,7 +423,7 @@ __device__ __forceinline__ void wide_ops(const Graph &G, const Work &W, const fl
                 m_j = uniformf(st.emu[off + t]); rsj = uniformf(st.ers[off + t]);
             } else {
                 const int j = uniform(G.col[e]);
-                ev = !(poly_i && clsb[j]);
+                ev = !(poly_i && clsb[j]) && !G.lap_on;
                 if (ev) { m_j = uniformf(mub[j]); rsj = uniformf(rsb[j]); }
             }
             if (!ev) continue;   // both ends on the polynomial path
@@ -506,6 +506,68 @@ __device__ __forceinline__ void wide_ops(const Graph &G, const Work &W, const fl
         if (m > 0 && lane == 2) atomicAdd(reinterpret_cast<unsigned long long *>(sG64 + 1),
                                           (unsigned long long)__float2ll_rn(ra * kGsumFix));
     }
+}
+
+// Usage of the wide Laplace ops (their edges are in closed form): wave w takes
+// every NW-th op of the list, lane l the TILE/64 consecutive steps from
+// t0 + l TILE/64.  A lane whose steps have their bin edges (one step below
+// them included) all on one side of the median gets the masses from one
+// evaluation and the ratio e^(-lam) per step (lam = sqrt(2)/sigma, the
+// Laplace masses being geometric there): from its last step down on the
+// lower side, from its first step up on the upper side, so the series runs
+// from the largest value; the steps of the other lanes are evaluated one by
+// one, a lane's steps at a time across the wave.  The sums go to the
+// fixed-point row sU64.
+template <int BS, int TILE>
+__device__ __forceinline__ void lap_usage(const Graph &G, const unsigned char *sCls, const OpStage &st, int nq,
+                                          int t0, int tb, long long *sU64) {
+    constexpr int NW = BS / 64, L = TILE / 64;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int D = G.D;
+    const int u0 = t0 + L * lane;
+    float acc[L];
+#pragma unroll
+    for (int k = 0; k < L; ++k) acc[k] = 0.0f;
+    for (int x = w; x < nq; x += NW) {
+        if (uniform(sCls[x]) != kLapU) continue;
+        const float m_i = uniformf(st.mu[x]), rs = uniformf(st.rs[x]);
+        auto direct = [&](int u) {   // P_i^u, 0 past the tile
+            return u < tb ? st_mass(st_sel<2>(u - 1, D, m_i, rs), st_sel<2>(u, D, m_i, rs)) : 0.0f;
+        };
+        const int ul = u0 + L - 1;
+        const bool inner = u0 - 1 >= 0 && ul <= D - 2 && ul < tb;   // bin edges u0-1 .. ul interior, in the tile
+        const bool below = inner && (float)ul + 0.5f - m_i < 0.0f;           // edge ul below the median
+        const bool above = inner && (float)(u0 - 1) + 0.5f - m_i >= 0.0f;   // edge u0-1 at or above it
+        if (below || above) {
+            const float r = __builtin_amdgcn_exp2f(-1.4142135623730951f * rs * kLog2e);   // e^(-lam)
+            float P = direct(below ? ul : u0);
+            // (fixed register indices in both branches: an index that differs
+            // between lanes would make the compiler walk the lanes)
+            if (below) {
+#pragma unroll
+                for (int k = L - 1; k >= 0; --k) { acc[k] += P; P *= r; }
+            } else {
+#pragma unroll
+                for (int k = 0; k < L; ++k) { acc[k] += P; P *= r; }
+            }
+        }
+        // the other lanes' steps (the median's, the horizon ends'): every
+        // step evaluated, one lane each, one such lane at a time
+        unsigned long long rest = __ballot(u0 < tb && !(below || above));
+        while (rest) {
+            const int l = __builtin_ctzll(rest);
+            rest &= rest - 1;
+            const int u = t0 + L * l + lane;
+            if (lane < L && u < tb)
+                atomicAdd(reinterpret_cast<unsigned long long *>(sU64 + (u - t0)),
+                          (unsigned long long)__float2ll_rn(direct(u) * kUsageFix));
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < L; ++k)
+        if (u0 + k < tb && acc[k] != 0.0f)
+            atomicAdd(reinterpret_cast<unsigned long long *>(sU64 + (u0 + k - t0)),
+                      (unsigned long long)__float2ll_rn(acc[k] * kUsageFix));
 }
 
 template <int FAM, int BS, int SPT>
@@ -631,7 +693,7 @@ __global__ __launch_bounds__(BS) __attribute__((amdgpu_waves_per_eu(4))) void k_
             int m = 0, cnt = 0, dep = 0, sum3 = 0;
             for (int e = e0; e < e1; ++e) {
                 const int j = G.col[e];
-                const bool sbs = !(poly_i && clsb[j]);
+                const bool sbs = !(poly_i && clsb[j]) && !G.lap_on;   // Laplace: edges in closed form
                 float m_j = 0.0f, rsj = 1.0f;
                 if (sbs) { m_j = mub[j]; rsj = rsb[j]; }
                 if (off >= 0) {
@@ -659,6 +721,7 @@ __global__ __launch_bounds__(BS) __attribute__((amdgpu_waves_per_eu(4))) void k_
                 : span <= kTinySpan ? kTiny
                 : span <= kMidSpan ? kMid
                 : span <= kNarrowSpan ? kNarrow
+                : G.lap_on ? kLapU   // Laplace: usage only (the edges are in closed form)
                 : (s <= kWideHalo && (m == 0 || 2 * sum3 < m * (tb - t0))) ? kWide : kRow;
             if (c == kConst) {
                 // no records: every derivative is 0 here, and the readers skip
@@ -699,6 +762,7 @@ __global__ __launch_bounds__(BS) __attribute__((amdgpu_waves_per_eu(4))) void k_
                                g1);
         wide_ops<FAM, BS, RS>(G, W, mub, rsb, clsb, st, sDirect, sWide, nWide, &sNextWide, sRows, sU64, sG64, t0, tb,
                               tile, b);
+        if (FAM == 2 && G.lap_on) lap_usage<BS, TILE>(G, sCls, st, nq, t0, tb, sU64);
         const float s0 = wave_sum((lane & 15) == 0 ? g0 : 0.0f), s1 = wave_sum((lane & 15) == 2 ? g1 : 0.0f);
         if (lane == 0) { sGw[w][0] = s0; sGw[w][1] = s1; }
     }
@@ -792,7 +856,7 @@ __global__ __launch_bounds__(BS) __attribute__((amdgpu_waves_per_eu(4))) void k_
                 m_j = uniformf(sEmu[off + e - e0]); rsj = uniformf(sErs[off + e - e0]);
             } else {
                 const int j = uniform(G.col[e]);
-                if (poly_i && clsb[j]) continue;
+                if ((poly_i && clsb[j]) || G.lap_on) continue;
                 m_j = mub[j]; rsj = rsb[j];
             }
             // steps t0-1 .. t0+TILE-1 all past fam_zflush on one side of the
@@ -1030,7 +1094,7 @@ __global__ __launch_bounds__(kNarBS) void k_group(Graph G, const float *__restri
             int m = 0;
             for (int e = e0; e < e0 + deg; ++e) {
                 const int j = G.col[e];
-                const bool sbs = !(poly_i && clsb[j]);
+                const bool sbs = !(poly_i && clsb[j]) && !G.lap_on;   // Laplace: edges in closed form
                 float m_j = 0.0f, rsj = 1.0f;
                 if (sbs) { m_j = mub[j]; rsj = rsb[j]; }
                 if (off >= 0) {
