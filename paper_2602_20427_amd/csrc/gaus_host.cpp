@@ -230,6 +230,7 @@ gaus_status dupload(gaus_ctx *c, const T **out, const std::vector<T> &h) {
 struct HostGraph {
     int N = 0, E = 0, K = 0, D = 0, II = 0, nb = 0;
     std::vector<int> row_ptr, col, delay, rtype, bsrc, bdst, bdist;
+    std::vector<int> esrc;                   // producer of each CSR edge
     std::vector<float> cap, bmem;
     std::vector<int> pred_ptr, pred_eid, pred_src;
     std::vector<int> bin_ptr, bin, bout_ptr, bout;
@@ -630,6 +631,10 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     std::vector<float> cap(h.cap);
     const size_t BN = (size_t)B * h.N;
 #define UP(field, vec) do { s = dupload(c, &g.field, vec); if (s != GAUS_OK) goto fail_alloc; } while (0)
+    h.esrc.assign(std::max(h.E, 1), 0);
+    for (int i = 0; i < h.N; ++i)
+        for (int e = h.row_ptr[i]; e < h.row_ptr[i + 1]; ++e) h.esrc[e] = i;
+    UP(esrc, h.esrc);
     UP(row_ptr, h.row_ptr); UP(col, h.col); UP(pred_ptr, h.pred_ptr); UP(pred_eid, h.pred_eid);
     UP(pred_src, h.pred_src); UP(delay, h.delay); UP(rtype, h.rtype); UP(cap, cap);
     UP(bsrc, h.bsrc); UP(bdst, h.bdst); UP(bdist, h.bdist); UP(bin_ptr, h.bin_ptr); UP(bin, h.bin);
@@ -697,7 +702,8 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     AL(gnar, (size_t)B * g.ngroups);
     AL(Unar, g.nar_on ? (size_t)B * g.ngroups * h.D : 1);
     AL(gsum_nar, (size_t)B * g.ngroups * 2);
-    AL(gsum_lap, g.lap_on ? (size_t)B * g.ngroups * 2 : 1);
+    AL(gsum_lap, g.lap_on ? (size_t)B * lap_blocks(g) * 2 : 1);
+    AL(pedge, g.lap_on ? (size_t)B * std::max(h.E, 1) * 4 : 1);
     AL(gsum_ops, (size_t)B * g.ngroups * g.parts * ntiles * 2);
     AL(gsum_poly, (size_t)std::max(c->poly_slots, 1) * 2);
     AL(gsel, BN);

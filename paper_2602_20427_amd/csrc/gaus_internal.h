@@ -93,6 +93,7 @@ struct Graph {
     int nlevels;               // topological levels (legalization)
     int leg_mode;              // legalization schedule: 0 global int64, 1 LDS int16, 2 LDS int32
     const int *row_ptr, *col;            // CSR by producer
+    const int *esrc;                     // producer of each CSR edge (Laplace edges: thread per edge)
     const int *pred_ptr, *pred_eid;      // CSC: CSR edge id of each in-edge
     const int *pred_src;                 // CSC: producer of each in-edge
     const int *delay, *rtype;
@@ -175,7 +176,8 @@ struct Work {
                            //               (kNarLeft, kNarTaken); valid where gbits has kGbStep
     float *Unar;           // [B][ngroups][D]  usage of the ops k_group took
     float *gsum_nar;       // [B][ngroups][2]  their V_dep, L_com
-    float *gsum_lap;       // [B][ngroups][2]  V_dep, L_com of the group's edges in closed form (Laplace)
+    float *gsum_lap;       // [B][nlap][2]  V_dep, L_com of each block of edges in closed form (Laplace)
+    float *pedge;          // [B][E][4]  producer-side derivatives of each edge in closed form (Laplace)
     unsigned char *ptier;  // [B][N]        polynomial op: tier of its vectors, the smallest over
                            //               itself and its polynomial consumers (highest degree)
     unsigned *gbits;  // [B][ngroups]      work of the group this iteration (k_group):
@@ -235,7 +237,10 @@ hipError_t enqueue_iteration(const Graph &g, const Work &w, const HP &hp, const 
 
 // Per-step kernels (gaus_step.hip: step by step; gaus_poly.hip: chunk polynomials).
 hipError_t launch_group(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu, hipStream_t st);
-// Laplace start times: every forward edge's terms in closed form (records in ppoly / cpoly, sums in gsum_lap).
+// Laplace start times: every forward edge's terms in closed form, a thread per
+// edge (records in pedge / cpoly, V_dep and L_com per block of kLapBS edges in gsum_lap).
+constexpr int kLapBS = 256;
+__host__ __device__ inline int lap_blocks(const Graph &g) { return (g.E + kLapBS - 1) / kLapBS; }
 hipError_t launch_lap_edges(const Graph &g, const Work &w, const float *mu, const float *sigma, hipStream_t st);
 hipError_t launch_ops(const Graph &g, const Work &w, const LaunchCfg &lc, const float *mu, const float *sigma,
                       hipStream_t st);

@@ -592,8 +592,12 @@ __global__ __launch_bounds__(kCombineBS) void k_combine(Graph G, PolyArgs pa, Wo
             for (int tl = 0; tl < G.parts * G.ntiles; ++tl) { vdep += go[2 * tl]; lcom += go[2 * tl + 1]; }
         }
         if (nar & kNarTaken) { vdep += W.gsum_nar[bg * 2]; lcom += W.gsum_nar[bg * 2 + 1]; }
-        if (G.lap_on) { vdep += W.gsum_lap[bg * 2]; lcom += W.gsum_lap[bg * 2 + 1]; }
     }
+    if (G.lap_on)   // Laplace: the closed-form edge sums per block of edges
+        for (int k = tid; k < lap_blocks(G); k += kCombineBS) {
+            vdep += W.gsum_lap[((size_t)b * lap_blocks(G) + k) * 2];
+            lcom += W.gsum_lap[((size_t)b * lap_blocks(G) + k) * 2 + 1];
+        }
     const size_t nbp = (size_t)G.nb * G.ntiles;
     const float *bp = W.bpart + (size_t)b * nbp * kBP;
     for (size_t r = tid; r < nbp; r += kCombineBS) vrec += bp[r * kBP + 0];
@@ -777,7 +781,12 @@ __global__ __launch_bounds__(256) void k_final(Graph G, Work W, HP hp, const flo
         }
     }
     const bool poly_i = W.cls[bi] != 0;
-    if (poly_i || dfl == 2 || G.lap_on) {   // single producer record (polynomial path, narrow kernel, Laplace edges)
+    if (G.lap_on) {   // Laplace: the closed-form records of the out-edges
+        for (int e = G.row_ptr[i]; e < G.row_ptr[i + 1]; ++e) {
+            const float4 p4 = *reinterpret_cast<const float4 *>(W.pedge + ((size_t)b * G.E + e) * 4);
+            dm += p4.x; ds += p4.y; cm += p4.z; cs += p4.w;
+        }
+    } else if (poly_i || dfl == 2) {   // single producer record (polynomial path, or the narrow kernel)
         const float *ppy = W.ppoly + bi * kPP;
         dm += ppy[2]; ds += ppy[3]; cm += ppy[4]; cs += ppy[5];
     }

@@ -66,6 +66,15 @@ struct GW {
 __device__ __forceinline__ GW run_weights(double g, int n) {
     GW r;
     if (n == 1) { r.w0 = 1.0; r.w1 = 0.0; r.atB = false; return r; }
+    if (n <= 4) {   // a few steps: the powers of e^(-|g|) from the larger end
+        const double q = exp(-fabs(g));
+        double G0 = 1.0, G1 = 0.0, qk = 1.0;
+        for (int k = 1; k < n; ++k) { qk *= q; G0 += qk; G1 = fma((double)k, qk, G1); }
+        r.w0 = G0;
+        r.w1 = g <= 0.0 ? G1 : (n - 1.0) * G0 - G1;
+        r.atB = g > 0.0;
+        return r;
+    }
     double G0, G1;
     if (g <= 0.0) {
         geo_sums(g, n, G0, G1);
@@ -81,14 +90,23 @@ __device__ __forceinline__ GW run_weights(double g, int n) {
 struct RunW {
     GW w[3][3];
 };
-__device__ __forceinline__ RunW run_table(double li, double lj, int n) {
+__device__ __forceinline__ RunW run_table(double li, double lj, int n, const bool ui[3], const bool uj[3]) {
     RunW t;
     const double gi[3] = {0.0, li, -li}, gj[3] = {0.0, lj, -lj};
 #pragma unroll
     for (int x = 0; x < 3; ++x)
 #pragma unroll
-        for (int y = 0; y < 3; ++y) t.w[x][y] = run_weights(gi[x] + gj[y], n);
+        for (int y = 0; y < 3; ++y) {
+            if (ui[x] && uj[y]) t.w[x][y] = run_weights(gi[x] + gj[y], n);
+            else t.w[x][y] = GW{0.0, 0.0, false};   // no factor of the run has these slots
+        }
     return t;
+}
+// the slots a factor holds (constant, growing, decaying)
+__device__ __forceinline__ void mark(const LF &f, bool u[3]) {
+    u[0] = u[0] || f.c != 0.0;
+    u[1] = u[1] || f.loA != 0.0 || f.loB != 0.0;
+    u[2] = u[2] || f.upA != 0.0 || f.upB != 0.0;
 }
 
 // sums over the run of f*h (f a producer factor, h a consumer factor):
@@ -161,11 +179,15 @@ __device__ void laplace_edge(const LOp &oi, double sg_i, int s, const LOp &oj, d
         for (int k = 0; k < 12; ++k) nx = cand[k] > a && cand[k] < nx ? cand[k] : nx;
         const int b = (int)nx - 1;
         const int n = b - a + 1;
-        const RunW t = run_table(oi.lam, oj.lam, n);
         const LF Fi = factor(oi, 0, 0, a, b, D), dFi = factor(oi, 2, 0, a, b, D);
         const LF dFis = factor(oi, 2, -s, a, b, D);
         const LF A = fsub(factor(oi, 0, 1 - s, a, b, D), factor(oi, 0, -s, a, b, D));
         const LF Fj = factor(oj, 0, 0, a, b, D), Rj = factor(oj, 1, 0, a, b, D), dFj = factor(oj, 2, 0, a, b, D);
+        const LF dSj = fsub(Fj, factor(oj, 0, -1, a, b, D));
+        bool ui[3] = {false, false, false}, uj[3] = {false, false, false};
+        mark(Fi, ui); mark(dFi, ui); mark(dFis, ui); mark(A, ui);
+        mark(Fj, uj); mark(Rj, uj); mark(dFj, uj); mark(dSj, uj);
+        const RunW t = run_table(oi.lam, oj.lam, n, ui, uj);
         double s0, s1;
         if (b <= D - 2) {   // the interior edges u <= D-2
             prod_sums(A, Fj, t, s0, s1);
@@ -183,7 +205,6 @@ __device__ void laplace_edge(const LOp &oi, double sg_i, int s, const LOp &oj, d
             P[5] += (s1 + ((double)a - oi.m) * s0) / sg_i;
         }
         // dVdep/dth_i runs to u = D-1, with F_j(D-1) = 1
-        const LF dSj = fsub(Fj, factor(oj, 0, -1, a, b, D));
         prod_sums(dFis, dSj, t, s0, s1);
         P[2] -= s0;
         P[3] -= (s1 + ((double)(a - s) - oi.m) * s0) / sg_i;
@@ -192,43 +213,32 @@ __device__ void laplace_edge(const LOp &oi, double sg_i, int s, const LOp &oj, d
     P[0] += 1.0 - cdf_lap(oi, D - 1 - s, D);
 }
 
-// Work-group = (op group, restart), thread per op: the op's out-edges in
-// closed form.  Records: the op's producer sums in its single ppoly slot,
-// each edge's consumer sums in its single cpoly slot (the op kernel leaves
-// the edges to this kernel and writes zero producer records per tile); V_dep
-// and L_com of the group per restart in gsum_lap.
-constexpr int kLapBS = 256;
-__global__ __launch_bounds__(kLapBS) void k_lap_edges(Graph G, const float *__restrict__ mu,
+// Work-group = (block of kLapBS edges, restart), thread per edge: its sums
+// in closed form.  Records: the producer-side derivatives in pedge, the
+// consumer-side ones in the edge's single cpoly slot (the op kernel leaves
+// the forward edges to this kernel); V_dep and L_com of the block per restart
+// in gsum_lap.  Work-group x serves restart x mod B (as the op kernel).
+__global__ __launch_bounds__(kLapBS) __attribute__((amdgpu_waves_per_eu(2))) void k_lap_edges(Graph G, const float *__restrict__ mu,
                                                       const float *__restrict__ sigma, Work W) {
-    const int b = blockIdx.x % G.B, grp = blockIdx.x / G.B, tid = threadIdx.x;
+    const int b = blockIdx.x % G.B, blk = blockIdx.x / G.B, tid = threadIdx.x;
     const int N = G.N, D = G.D;
-    const int q0 = G.grp_start[grp], nq = G.grp_start[grp + 1] - q0;
+    const int e = blk * kLapBS + tid;
     double vdep = 0.0, lcom = 0.0;
-    if (tid < nq) {
-        const int i = G.perm[q0 + tid];
-        const size_t bi = (size_t)b * N + i;
-        const double sg_i = sigma[bi];
+    if (e < G.E) {
+        const int i = G.esrc[e], j = G.col[e];
+        const size_t bi = (size_t)b * N + i, bj = (size_t)b * N + j;
+        const double sg_i = sigma[bi], sg_j = sigma[bj];
         const LOp oi{(double)mu[bi] - 0.5, 1.4142135623730951 / sg_i};
-        const int s = G.delay[i];
-        double P[6] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
-        for (int e = G.row_ptr[i]; e < G.row_ptr[i + 1]; ++e) {
-            const int j = G.col[e];
-            const size_t bj = (size_t)b * N + j;
-            const double sg_j = sigma[bj];
-            const LOp oj{(double)mu[bj] - 0.5, 1.4142135623730951 / sg_j};
-            double Pe[6], Ce[4];
-            laplace_edge(oi, sg_i, s, oj, sg_j, D, Pe, Ce);
-            for (int k = 0; k < 6; ++k) P[k] += Pe[k];
-            float4 c4;
-            c4.x = (float)Ce[0]; c4.y = (float)Ce[1]; c4.z = (float)Ce[2]; c4.w = (float)Ce[3];
-            *reinterpret_cast<float4 *>(W.cpoly + ((size_t)b * G.E + e) * kCP) = c4;
-        }
-        float *pp = W.ppoly + bi * kPP;
-        for (int k = 0; k < kPP; ++k) pp[k] = (float)P[k];
+        const LOp oj{(double)mu[bj] - 0.5, 1.4142135623730951 / sg_j};
+        double P[6], C[4];
+        laplace_edge(oi, sg_i, G.delay[i], oj, sg_j, D, P, C);
+        const size_t be = (size_t)b * G.E + e;
+        *reinterpret_cast<float4 *>(W.cpoly + be * kCP) = make_float4((float)C[0], (float)C[1], (float)C[2], (float)C[3]);
+        *reinterpret_cast<float4 *>(W.pedge + be * 4) = make_float4((float)P[2], (float)P[3], (float)P[4], (float)P[5]);
         vdep = P[0];
         lcom = P[1];
     }
-    // the group's sums: per wave, then the waves in order
+    // the block's sums: per wave, then the waves in order
     __shared__ double sW[kLapBS / 64][2];
     const int lane = tid & 63, w = tid >> 6;
     for (int o = 32; o >= 1; o >>= 1) {
@@ -240,12 +250,13 @@ __global__ __launch_bounds__(kLapBS) void k_lap_edges(Graph G, const float *__re
     if (tid < 2) {
         double v = 0.0;
         for (int k = 0; k < kLapBS / 64; ++k) v += sW[k][tid];
-        W.gsum_lap[((size_t)b * G.ngroups + grp) * 2 + tid] = (float)v;
+        W.gsum_lap[((size_t)b * lap_blocks(G) + blk) * 2 + tid] = (float)v;
     }
 }
 
 hipError_t launch_lap_edges(const Graph &g, const Work &w, const float *mu, const float *sigma, hipStream_t st) {
-    hipLaunchKernelGGL(k_lap_edges, dim3((unsigned)((size_t)g.ngroups * g.B)), dim3(kLapBS), 0, st, g, mu, sigma, w);
+    if (g.E == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_lap_edges, dim3((unsigned)((size_t)lap_blocks(g) * g.B)), dim3(kLapBS), 0, st, g, mu, sigma, w);
     return hipGetLastError();
 }
 
