@@ -63,7 +63,7 @@ struct GW {
     double w0, w1;
     bool atB;
 };
-__device__ __forceinline__ GW run_weights(double g, int n) {
+__device__ __attribute__((noinline)) GW run_weights(double g, int n) {   // (a call: fewer live registers)
     GW r;
     if (n == 1) { r.w0 = 1.0; r.w1 = 0.0; r.atB = false; return r; }
     if (n <= 4) {   // a few steps: the powers of e^(-|g|) from the larger end
