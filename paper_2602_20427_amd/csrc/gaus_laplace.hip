@@ -41,16 +41,28 @@ __device__ __forceinline__ void geo_sums(double g, int n, double &G0, double &G1
         G1 = 0.5 * n * (n - 1.0);
         return;
     }
-    const double e1 = -expm1(-x), en = -expm1(-xn);   // 1 - e^(-x), 1 - e^(-x n)
-    G0 = en / e1;
-    if (xn < 0.02) {   // power sums S_p = sum k^p, k < n, and the series of e^(-x k)
-        const double nn = n, s1 = 0.5 * nn * (nn - 1.0), s2 = (nn - 1.0) * nn * (2.0 * nn - 1.0) / 6.0;
-        const double s3 = s1 * s1, s4 = (nn - 1.0) * nn * (2.0 * nn - 1.0) * (3.0 * nn * nn - 3.0 * nn - 1.0) / 30.0;
-        const double s5 = s1 * s1 * (2.0 * nn * nn - 2.0 * nn - 1.0) / 3.0;
-        G1 = s1 - x * s2 + x * x * s3 / 2.0 - x * x * x * s4 / 6.0 + x * x * x * x * s5 / 24.0;
+    const double e1 = -expm1(-x);   // 1 - e^(-x)
+    if (xn < 0.5) {
+        const double en = -expm1(-xn);   // 1 - e^(-x n)
+        G0 = en / e1;
+        if (xn < 0.02) {   // power sums S_p = sum k^p, k < n, and the series of e^(-x k)
+            const double nn = n, s1 = 0.5 * nn * (nn - 1.0), s2 = (nn - 1.0) * nn * (2.0 * nn - 1.0) / 6.0;
+            const double s3 = s1 * s1, s4 = (nn - 1.0) * nn * (2.0 * nn - 1.0) * (3.0 * nn * nn - 3.0 * nn - 1.0) / 30.0;
+            const double s5 = s1 * s1 * (2.0 * nn * nn - 2.0 * nn - 1.0) / 3.0;
+            G1 = s1 - x * s2 + x * x * s3 / 2.0 - x * x * x * s4 / 6.0 + x * x * x * x * s5 / 24.0;
+        } else {
+            // sum k q^k = q (1 - q^(n-1) (1 + (n-1)(1-q))) / (1-q)^2, q = e^(-x);
+            // here q > 0.6 and q^(n-1) > 0.6, both exact enough from e1, en
+            const double q = 1.0 - e1, qn1 = (1.0 - en) / q;
+            G1 = q * (1.0 - qn1 * (1.0 + (n - 1.0) * e1)) / (e1 * e1);
+        }
     } else {
-        // sum k q^k = q (1 - q^(n-1) (1 + (n-1)(1-q))) / (1-q)^2, q = e^(-x)
-        const double q = 1.0 - e1, qn1 = (1.0 - en) / q;
+        // e^(-x n) < 0.61: 1 - e^(-x n) from the product without cancellation.
+        // q^(n-1), and q once x >= 0.5, come from exp itself: through e1 and
+        // en they would carry an absolute error of an ulp of 1, which is no
+        // small error once they are tiny (0/0 once e1 rounds to 1)
+        const double q = x < 0.5 ? 1.0 - e1 : exp(-x), qn1 = exp(-x * (n - 1.0));
+        G0 = (1.0 - q * qn1) / e1;
         G1 = q * (1.0 - qn1 * (1.0 + (n - 1.0) * e1)) / (e1 * e1);
     }
 }
@@ -127,27 +139,42 @@ __device__ __forceinline__ void prod_sums(const LF &f, const LF &h, const RunW &
         }
 }
 
-// The op's CDF at the bin edges u + off, u in [a, b] (one case throughout):
-// kind 0: F, 1: 1 - F, 2: dF/dmu.
+// The op at the bin edges u + off, u in [a, b] (one case throughout): past
+// an end of the horizon (F = 0 below it, 1 at its last edge and beyond) or
+// on one side of the median, with e/2 at both ends, e = e^(-lam |v - m|).
 struct LOp {
     double m, lam;
 };
-__device__ __forceinline__ LF factor(const LOp &o, int kind, int off, int a, int b, int D) {
-    LF f{0.0, 0.0, 0.0, 0.0, 0.0};
+struct LV {
+    int endv;   // 0: F = 0, 1: F = 1, -1: inside
+    bool up;    // at or above the median
+    double ea, eb;
+};
+__device__ __forceinline__ LV lval(const LOp &o, int off, int a, int b, int D) {
+    LV v;
     const int va = a + off, vb = b + off;
-    const bool zero = va < 0, one = va >= D - 1;
-    if (zero || one) {
-        f.c = ((kind == 0 && one) || (kind == 1 && zero)) ? 1.0 : 0.0;
+    v.endv = va < 0 ? 0 : va >= D - 1 ? 1 : -1;
+    v.up = (double)va >= o.m;
+    v.ea = v.eb = 0.0;
+    if (v.endv < 0) {
+        const double sg = v.up ? -1.0 : 1.0;   // e^(+lam (v-m)) below the median, e^(-lam (v-m)) above
+        v.ea = 0.5 * exp(sg * o.lam * ((double)va - o.m));
+        v.eb = 0.5 * exp(sg * o.lam * ((double)vb - o.m));
+    }
+    return v;
+}
+// kind 0: F, 1: 1 - F, 2: dF/dmu
+__device__ __forceinline__ LF factor(const LV &v, double lam, int kind) {
+    LF f{0.0, 0.0, 0.0, 0.0, 0.0};
+    if (v.endv >= 0) {
+        f.c = ((kind == 0 && v.endv == 1) || (kind == 1 && v.endv == 0)) ? 1.0 : 0.0;
         return f;
     }
-    const bool up = (double)va >= o.m;
-    const double sg = up ? -1.0 : 1.0;   // e^(+lam (v-m)) below the median, e^(-lam (v-m)) above
-    const double ea = 0.5 * exp(sg * o.lam * ((double)va - o.m)), eb = 0.5 * exp(sg * o.lam * ((double)vb - o.m));
     // F: e/2 below, 1 - e/2 above; 1 - F: the complement; dF/dmu = -lam e/2
-    const double w = kind == 2 ? -o.lam : (kind == 0) == up ? -1.0 : 1.0;
-    f.c = kind == 2 ? 0.0 : (kind == 0) == up ? 1.0 : 0.0;
-    if (up) { f.upA = w * ea; f.upB = w * eb; }
-    else { f.loA = w * ea; f.loB = w * eb; }
+    const double w = kind == 2 ? -lam : (kind == 0) == v.up ? -1.0 : 1.0;
+    f.c = kind == 2 ? 0.0 : (kind == 0) == v.up ? 1.0 : 0.0;
+    if (v.up) { f.upA = w * v.ea; f.upB = w * v.eb; }
+    else { f.loA = w * v.ea; f.loB = w * v.eb; }
     return f;
 }
 
@@ -168,9 +195,12 @@ __device__ void laplace_edge(const LOp &oi, double sg_i, int s, const LOp &oj, d
                              double C[4]) {
     // the steps where a case changes (the first step of the new case),
     // taken in increasing order by a scan over the candidates
-    const long long ci = (long long)ceil(oi.m), cj = (long long)ceil(oj.m);
-    long long cand[15] = {s, (long long)s - 1, D - 1, (long long)D - 1 + s, (long long)D - 2 + s,
-                          ci, ci + s, ci + s - 1, 1, D, cj, cj + 1, 0, 0, 0};
+    // (medians clamped to +-2^50 before the conversion: cuts that far out
+    // never fall inside the horizon)
+    const double mcl = 1125899906842624.0;
+    const long long ci = (long long)ceil(fmin(fmax(oi.m, -mcl), mcl)), cj = (long long)ceil(fmin(fmax(oj.m, -mcl), mcl));
+    const long long cand[12] = {s, (long long)s - 1, D - 1, (long long)D - 1 + s, (long long)D - 2 + s,
+                                ci, ci + s, ci + s - 1, 1, D, cj, cj + 1};
     for (int k = 0; k < 6; ++k) P[k] = 0.0;
     for (int k = 0; k < 4; ++k) C[k] = 0.0;
     for (int a = 0; a < D;) {
@@ -179,11 +209,14 @@ __device__ void laplace_edge(const LOp &oi, double sg_i, int s, const LOp &oj, d
         for (int k = 0; k < 12; ++k) nx = cand[k] > a && cand[k] < nx ? cand[k] : nx;
         const int b = (int)nx - 1;
         const int n = b - a + 1;
-        const LF Fi = factor(oi, 0, 0, a, b, D), dFi = factor(oi, 2, 0, a, b, D);
-        const LF dFis = factor(oi, 2, -s, a, b, D);
-        const LF A = fsub(factor(oi, 0, 1 - s, a, b, D), factor(oi, 0, -s, a, b, D));
-        const LF Fj = factor(oj, 0, 0, a, b, D), Rj = factor(oj, 1, 0, a, b, D), dFj = factor(oj, 2, 0, a, b, D);
-        const LF dSj = fsub(Fj, factor(oj, 0, -1, a, b, D));
+        // each op's values at the five shifts, once (ten exponentials per run)
+        const LV vi = lval(oi, 0, a, b, D), vis = lval(oi, -s, a, b, D), vis1 = lval(oi, 1 - s, a, b, D);
+        const LV vj = lval(oj, 0, a, b, D), vjm = lval(oj, -1, a, b, D);
+        const LF Fi = factor(vi, oi.lam, 0), dFi = factor(vi, oi.lam, 2);
+        const LF dFis = factor(vis, oi.lam, 2);
+        const LF A = fsub(factor(vis1, oi.lam, 0), factor(vis, oi.lam, 0));
+        const LF Fj = factor(vj, oj.lam, 0), Rj = factor(vj, oj.lam, 1), dFj = factor(vj, oj.lam, 2);
+        const LF dSj = fsub(Fj, factor(vjm, oj.lam, 0));
         bool ui[3] = {false, false, false}, uj[3] = {false, false, false};
         mark(Fi, ui); mark(dFi, ui); mark(dFis, ui); mark(A, ui);
         mark(Fj, uj); mark(Rj, uj); mark(dFj, uj); mark(dSj, uj);

@@ -8,8 +8,8 @@ import pytest
 
 import oracle
 from paper_2602_20427_amd import binding as bd
-from paper_2602_20427_amd.workloads import (CONFIGS, make_problem, random_state, restart_uniforms, uniform_state,
-                                            with_storage)
+from paper_2602_20427_amd.workloads import (CONFIGS, Problem, make_problem, random_state, restart_uniforms,
+                                            uniform_state, with_storage)
 from tests.gpu_common import TOL, gpu_loss_grad, hparams, oracle_compare, poly_sigma_thresholds, say
 
 pytestmark = pytest.mark.gpu
@@ -87,8 +87,8 @@ def test_family_loss_grad_initial_state(family, cfg):
 @pytest.mark.parametrize("family", FAMS)
 def test_family_polynomial_path_switch(family):
     """The logistic and Cauchy CDFs are analytic and take the chunk
-    polynomials; the Laplace CDF has a kink at the median and runs step by
-    step."""
+    polynomials; the Laplace CDF has a kink at the median and takes its own
+    closed forms instead."""
     p = make_problem("medium", seed=0)
     ctx = bd.Context(p, 1, _hp(family))
     try:
@@ -186,3 +186,67 @@ def test_family_large_full_size(family):
     lam = np.full((B, 3), hp.lambda0, np.float32)
     say(f"[family] {family} large: N={p.n_ops} D={p.D} B={B}")
     _compare(p, mu, sg, lam, hp, family, f"large/{family}", restarts=(0, 1, 2, B - 1))
+
+
+def _bipartite_problem(seed, N, D):
+    """Producers 0..N/2-1 (sources) feeding consumers N/2..N-1 (sinks), so any
+    producer delay up to D-1 fits the horizon: delays 0 and D-1, a few around
+    D/2 and small ones."""
+    rng = np.random.default_rng(seed)
+    h = N // 2
+    rows = [np.unique(rng.integers(h, N, size=1 + rng.poisson(2.0))) for _ in range(h)]
+    rows += [np.zeros(0, np.int64)] * (N - h)
+    row_ptr = np.zeros(N + 1, np.int32)
+    row_ptr[1:] = np.cumsum([len(r) for r in rows])
+    col = np.concatenate(rows).astype(np.int32)
+    delay = np.zeros(N, np.int32)
+    delay[:h] = np.where(rng.random(h) < 0.5, rng.integers(0, 9, size=h), rng.integers(0, D, size=h))
+    delay[:4] = [0, D - 1, D // 2, max(D - 2, 0)]
+    rtype = rng.integers(0, 3, size=N).astype(np.int32)
+    cap = np.array([3.0, 1.5, 0.7], np.float32)
+    e = np.zeros(0, np.int32)
+    return Problem(n_ops=N, row_ptr=row_ptr, col_idx=col, delay=delay, rtype=rtype, capacity=cap, D=D, II=0,
+                   back_src=e, back_dst=e, back_dist=e)
+
+
+@pytest.mark.parametrize("D", [50, 300, 1500])
+def test_laplace_closed_form_extremes(D):
+    """The Laplace edge sums in closed form at the ends of their ranges:
+    widths from 0.02 to 5000 steps (log-uniform, so the ratio e^-lam of the
+    geometric sums runs from 0 to within 3e-4 of 1 and the sums take their
+    direct, expm1 and power-series forms), means on the horizon's ends, on
+    half steps (a median exactly on a bin edge, where the cases change) and
+    far outside it, and producer delays from 0 to D-1."""
+    N = 400 if D > 100 else 120
+    p = _bipartite_problem(60 + D, N, D)
+    B = 3
+    rng = np.random.default_rng(61 + D)
+    ends = np.array([0.0, D - 1.0, D / 2.0])[rng.integers(0, 3, size=(B, N))] + rng.normal(0.0, 2.0, size=(B, N))
+    half = rng.integers(-3, D + 3, size=(B, N)) + 0.5
+    far = rng.uniform(-3.0 * D, 4.0 * D, size=(B, N))
+    pick = rng.integers(0, 3, size=(B, N))
+    mu = np.choose(pick, [ends, half, far]).astype(np.float32)
+    sg = np.exp(rng.uniform(np.log(0.02), np.log(5000.0), size=(B, N))).astype(np.float32)
+    lam = np.random.default_rng(62 + D).uniform(0.05, 1.0, size=(B, 3)).astype(np.float32)
+    hp = _hp("laplace", alpha=0.3, rho=0.02)
+    say(f"[family] laplace extremes: N={N} E={p.n_edges} D={D} B={B}")
+    _compare(p, mu, sg, lam, hp, "laplace", f"extremes D={D}/laplace", restarts=range(B))
+
+
+def test_laplace_tight_horizon_full_size():
+    """Laplace on the 50k-op workload with the tight horizon (D = longest
+    delay-weighted path + 8, one step tile) at full size from the paper's
+    initialization, as bench.py --workload large-tight --family laplace times
+    it: the producers' delays cut most runs near the horizon's end."""
+    cfg = CONFIGS["large-tight"]
+    p = make_problem(cfg, seed=0)
+    B = cfg.B
+    mu, sg, rc = oracle.init_state(p, B, restart_uniforms(p.n_ops, B, seed=0))
+    assert rc == 0
+    hp = bd.default_hparams()
+    hp.lr = cfg.lr
+    hp.family = bd.FAMILIES["laplace"]
+    lam = np.full((B, 3), hp.lambda0, np.float32)
+    say(f"[family] laplace large-tight: N={p.n_ops} D={p.D} B={B}")
+    _compare(p, mu.astype(np.float32), sg.astype(np.float32), lam, hp, "laplace", "large-tight/laplace",
+             restarts=(0, B - 1))
