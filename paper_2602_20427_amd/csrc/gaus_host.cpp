@@ -185,6 +185,10 @@ void setup_poly(int D, int requested, int pack, int fam, int B, PolyArgs &pa) {
     pa.W = W; pa.nc = nc; pa.L0 = pa.gr[0].L0; pa.SP = pa.gr[0].SP; pa.lam = pa.gr[0].lam;
     for (int t = 0; t <= kTiers; ++t) pa.sig_thr[t] = pa.gr[0].sig_thr[t];
     for (int k = 0; k <= kDeg; ++k) pa.H[k] = pa.gr[0].H[k];
+    // storage holders: the Gaussian's 1/4, scaled for the other families as
+    // their degree-8 rho is to the Gaussian's (the rho at which the family's
+    // truncation bound equals the Gaussian one)
+    pa.mem_rho = fam == 0 ? kMemRhoMax : (float)(kMemRhoMax / kRhoMax * pa.lam / pa.sig_thr[1]);
     // Packed grids: 64/P lanes per restart, at most that many chunks and a
     // strip of at most that many positions (one pass); the smallest such W
     // (W <= 256 keeps the degree-16 moments within fp32 range).

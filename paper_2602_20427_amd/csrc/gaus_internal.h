@@ -38,8 +38,10 @@ constexpr int kMaxChunks = 64;                // one chunk per lane of a wave
 constexpr int kStripMax = 320;                 // step-by-step strip positions per op, at most
 // Storage term on the chunk polynomials: a holder whose successors are all
 // polynomial, at most kMemPolyDeg of them, with rho summed over the holder
-// and its successors at most kMemRhoMax (the product of their series keeps
-// the degree-8 accuracy); every other holder is evaluated step by step.
+// and its successors at most kMemRhoMax for Gaussian start times (the
+// product of their series keeps the degree-8 accuracy) and at most the
+// family's own degree-8 rho for the others (PolyArgs::mem_rho); every other
+// holder is evaluated step by step.
 constexpr int kMemPolyDeg = 4;
 constexpr float kMemRhoMax = 0.25f;
 
@@ -81,6 +83,7 @@ struct PolyArgs {
     float lam;            // chunk half-width (W-1)/2
     float sig_thr[kTiers + 1];   // sigma >= sig_thr[t]: tier t (decreasing degree); [1] = path threshold
     float H[kDeg + 1];    // even moments: H[k] = sum over a chunk's points y of y^(2k)
+    float mem_rho;        // storage holders: bound of rho summed over a holder and its successors
     GridArgs gr[kGrids];  // [0] = the fields above; [1], [2] = packed grids
 };
 

@@ -85,7 +85,7 @@ __device__ __forceinline__ int grid_tier(const GridArgs &gr, float s, int delay)
 // The per-(restart, group) OR of these flags (gbits) follows in k_group.
 // The consumers' tiers are recomputed here from their sigmas.  With the
 // storage term on, also whether a holder's storage term is taken on the
-// chunk polynomials (Gaussian start times only; kMemPolyDeg, kMemRhoMax).
+// chunk polynomials (kMemPolyDeg, PolyArgs::mem_rho).
 constexpr int kFlagPack = 4;   // the largest restart pack of a grid
 static_assert(kGridP[kGrids - 1] == kFlagPack, "packs nest in the flag kernel's restarts");
 
@@ -134,8 +134,8 @@ __global__ __launch_bounds__(64 * kFlagPack) void k_flags(Graph G, PolyArgs pa, 
 #pragma unroll
         for (int g = 1; g < kGrids; ++g) sTp[q][g][lane] = (unsigned char)tp[g];
         W.dflag[bi] = (unsigned char)d;
-        W.mpoly[bi] = (unsigned char)(mem_on && pa.fam == 0 && ci != 0 && d == 0 && e1 > e0 &&
-                                      e1 - e0 <= kMemPolyDeg && pa.lam * rsum <= kMemRhoMax);
+        W.mpoly[bi] = (unsigned char)(mem_on && ci != 0 && d == 0 && e1 > e0 &&
+                                      e1 - e0 <= kMemPolyDeg && pa.lam * rsum <= pa.mem_rho);
         W.ptier[bi] = (unsigned char)t;
     }
     __syncthreads();

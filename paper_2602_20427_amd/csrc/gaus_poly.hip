@@ -498,7 +498,7 @@ __global__ __launch_bounds__(64 * kPolyWaves) void k_lse_poly(Graph G, PolyArgs 
 // restart, split slot) as in k_poly; per work-group the chunk coefficients and
 // strip values of its holders are summed in fp64.
 // ---------------------------------------------------------------------------
-template <int NP>
+template <int NP, int FAM>
 __global__ __launch_bounds__(64 * kPolyWaves) void k_mem_poly_fwd(Graph G, PolyArgs pa, const float *__restrict__ mu,
                                                                   Work W) {
     __shared__ double sMc[kPolyWaves][kNC][kMaxChunks];
@@ -537,11 +537,11 @@ __global__ __launch_bounds__(64 * kPolyWaves) void k_mem_poly_fwd(Graph G, PolyA
             const int p = ps * 64 + lane;
             if (p < SP) {
                 const int u = p < L0 ? p : D - 2 + (p - L0);
-                const float Fh = st_F(st_at(u, D, m_i, rs));
+                const float Fh = st_F(st_at<FAM>(u, D, m_i, rs));
                 float Q = 1.0f, R = 0.0f;
                 for (int e = e0; e < e1; ++e) {
                     const int j = G.col[e];
-                    const float st = st_at(u, D, mub[j], rsb[j]);
+                    const float st = st_at<FAM>(u, D, mub[j], rsb[j]);
                     R = fmaf(Q, st_1mF(st), R);
                     Q *= st_F(st);
                 }
@@ -550,14 +550,14 @@ __global__ __launch_bounds__(64 * kPolyWaves) void k_mem_poly_fwd(Graph G, PolyA
         }
         // chunks: truncated series products
         Expansion<kNC, kNC> eh;
-        expand(m_i, rs, tcen, eh);
+        expand<FAM>(m_i, rs, tcen, eh);
         float Q[kNC], R[kNC];
 #pragma unroll
         for (int k = 0; k < kNC; ++k) { Q[k] = k == 0 ? 1.0f : 0.0f; R[k] = 0.0f; }
         for (int e = e0; e < e1; ++e) {
             const int j = G.col[e];
             Expansion<kNC, kNC> ej;
-            expand(mub[j], rsb[j], tcen, ej);
+            expand<FAM>(mub[j], rsb[j], tcen, ej);
             float omF[kNC], Fj[kNC], t[kNC];
 #pragma unroll
             for (int k = 0; k < kNC; ++k) { omF[k] = k == 0 ? ej.G0 : -ej.T[k]; Fj[k] = ej.T[k]; }
@@ -635,13 +635,13 @@ __global__ __launch_bounds__(256) void k_mem_mom(Graph G, PolyArgs pa, Work W) {
 //   successor j:  -sum_t c(t) b_h F_h(t) prod_{k != j} F_k(t) dF_j(t)
 // (dF = dF/dmu or dF/dsigma).  Chunks: the products as truncated series,
 // dotted with the chunk moments; strip: step by step.  DEG successors.
-template <int DEG, int NP>
+template <int DEG, int NP, int FAM>
 __device__ __forceinline__ void mem_poly_holder(const Graph &G, const PolyArgs &pa, const Work &W, int b, int h,
                                                 int e0, const float *mub, const float *rsb, const float *ms,
                                                 const float (&cm)[kNC], bool cact, float tcen, int lane) {
     const int SP = pa.SP, L0 = pa.L0, D = G.D, T = G.T;
     const float m_h = mub[h], rs_h = rsb[h], bh = G.bmem[h];
-    const float cinv_h = rs_h * kInvSqrt2Pi;
+    const float cinv_h = rs_h * fam_k<FAM>();
     float mj[DEG], rj[DEG];
 #pragma unroll
     for (int q = 0; q < DEG; ++q) {
@@ -659,14 +659,14 @@ __device__ __forceinline__ void mem_poly_holder(const Graph &G, const PolyArgs &
             const int u = p < L0 ? p : D - 2 + (p - L0);
             const float c = u <= D - 2 ? ms[u % T] : 0.0f;
             float st, Fm, Fs;
-            cdf_at(u, D, m_h, rs_h, cinv_h, st, Fm, Fs);
+            cdf_at<FAM>(u, D, m_h, rs_h, cinv_h, st, Fm, Fs);
             const float Fh = st_F(st);
             float F[DEG], Fmj[DEG], Fsj[DEG];
             float Q = 1.0f, R = 0.0f;
 #pragma unroll
             for (int q = 0; q < DEG; ++q) {
                 float sj;
-                cdf_at(u, D, mj[q], rj[q], rj[q] * kInvSqrt2Pi, sj, Fmj[q], Fsj[q]);
+                cdf_at<FAM>(u, D, mj[q], rj[q], rj[q] * fam_k<FAM>(), sj, Fmj[q], Fsj[q]);
                 F[q] = st_F(sj);
                 R = fmaf(Q, st_1mF(sj), R);
                 Q *= F[q];
@@ -688,12 +688,12 @@ __device__ __forceinline__ void mem_poly_holder(const Graph &G, const PolyArgs &
     // chunks
     if (cact) {
         Expansion<kNC, kNC + 1> eh;
-        expand(m_h, rs_h, tcen, eh);
+        expand<FAM>(m_h, rs_h, tcen, eh);
         float T_[DEG][kNC + 1], G0[DEG], Z0[DEG];
 #pragma unroll
         for (int q = 0; q < DEG; ++q) {
             Expansion<kNC, kNC + 1> ej;
-            expand(mj[q], rj[q], tcen, ej);
+            expand<FAM>(mj[q], rj[q], tcen, ej);
 #pragma unroll
             for (int k = 0; k <= kNC; ++k) T_[q][k] = ej.T[k];
             G0[q] = ej.G0; Z0[q] = ej.z0;
@@ -758,7 +758,7 @@ __device__ __forceinline__ void mem_poly_holder(const Graph &G, const PolyArgs &
     }
 }
 
-template <int NP>
+template <int NP, int FAM>
 __global__ __launch_bounds__(64 * kPolyWaves) void k_mem_poly_bwd(Graph G, PolyArgs pa, const float *__restrict__ mu,
                                                                   Work W) {
     const int split = pa.split;
@@ -787,10 +787,10 @@ __global__ __launch_bounds__(64 * kPolyWaves) void k_mem_poly_bwd(Graph G, PolyA
         const int h = __builtin_amdgcn_readlane(l_i, oq);
         const int e0 = G.row_ptr[h], deg = G.row_ptr[h + 1] - e0;   // 1 .. kMemPolyDeg
         switch (deg) {
-            case 1: mem_poly_holder<1, NP>(G, pa, W, b, h, e0, mub, rsb, ms, cm, cact, tcen, lane); break;
-            case 2: mem_poly_holder<2, NP>(G, pa, W, b, h, e0, mub, rsb, ms, cm, cact, tcen, lane); break;
-            case 3: mem_poly_holder<3, NP>(G, pa, W, b, h, e0, mub, rsb, ms, cm, cact, tcen, lane); break;
-            default: mem_poly_holder<kMemPolyDeg, NP>(G, pa, W, b, h, e0, mub, rsb, ms, cm, cact, tcen, lane); break;
+            case 1: mem_poly_holder<1, NP, FAM>(G, pa, W, b, h, e0, mub, rsb, ms, cm, cact, tcen, lane); break;
+            case 2: mem_poly_holder<2, NP, FAM>(G, pa, W, b, h, e0, mub, rsb, ms, cm, cact, tcen, lane); break;
+            case 3: mem_poly_holder<3, NP, FAM>(G, pa, W, b, h, e0, mub, rsb, ms, cm, cact, tcen, lane); break;
+            default: mem_poly_holder<kMemPolyDeg, NP, FAM>(G, pa, W, b, h, e0, mub, rsb, ms, cm, cact, tcen, lane); break;
         }
     }
 }
@@ -842,30 +842,50 @@ hipError_t launch_poly(const Graph &g, const Work &w, const PolyArgs &pa, const 
 hipError_t launch_mem_poly_fwd(const Graph &g, const Work &w, const PolyArgs &pa, const float *mu,
                                hipStream_t st) {
     const dim3 grid(g.ngroups * pa.split, g.B), block(64 * kPolyWaves);
-    switch ((pa.SP + 63) / 64) {
-    case 1: hipLaunchKernelGGL(k_mem_poly_fwd<1>, grid, block, 0, st, g, pa, mu, w); break;
-    case 2: hipLaunchKernelGGL(k_mem_poly_fwd<2>, grid, block, 0, st, g, pa, mu, w); break;
-    case 3: hipLaunchKernelGGL(k_mem_poly_fwd<3>, grid, block, 0, st, g, pa, mu, w); break;
-    case 4: hipLaunchKernelGGL(k_mem_poly_fwd<4>, grid, block, 0, st, g, pa, mu, w); break;
-    case kStripPassesMax: hipLaunchKernelGGL(k_mem_poly_fwd<kStripPassesMax>, grid, block, 0, st, g, pa, mu, w); break;
+    auto run = [&](auto fam_tag) -> hipError_t {
+        constexpr int FAM = decltype(fam_tag)::value;
+        switch ((pa.SP + 63) / 64) {
+        case 1: hipLaunchKernelGGL((k_mem_poly_fwd<1, FAM>), grid, block, 0, st, g, pa, mu, w); break;
+        case 2: hipLaunchKernelGGL((k_mem_poly_fwd<2, FAM>), grid, block, 0, st, g, pa, mu, w); break;
+        case 3: hipLaunchKernelGGL((k_mem_poly_fwd<3, FAM>), grid, block, 0, st, g, pa, mu, w); break;
+        case 4: hipLaunchKernelGGL((k_mem_poly_fwd<4, FAM>), grid, block, 0, st, g, pa, mu, w); break;
+        case kStripPassesMax:
+            hipLaunchKernelGGL((k_mem_poly_fwd<kStripPassesMax, FAM>), grid, block, 0, st, g, pa, mu, w); break;
+        default: return hipErrorInvalidValue;
+        }
+        return hipSuccess;
+    };
+    switch (pa.fam) {
+    case 0: return run(std::integral_constant<int, 0>{});
+    case 1: return run(std::integral_constant<int, 1>{});
+    case 3: return run(std::integral_constant<int, 3>{});
     default: return hipErrorInvalidValue;
     }
-    return hipSuccess;
 }
 
 hipError_t launch_mem_poly_bwd(const Graph &g, const Work &w, const PolyArgs &pa, const float *mu,
                                hipStream_t st) {
     hipLaunchKernelGGL(k_mem_mom, dim3(pa.nc, g.B), dim3(256), 0, st, g, pa, w);
     const dim3 grid(g.ngroups * pa.split, g.B), block(64 * kPolyWaves);
-    switch ((pa.SP + 63) / 64) {
-    case 1: hipLaunchKernelGGL(k_mem_poly_bwd<1>, grid, block, 0, st, g, pa, mu, w); break;
-    case 2: hipLaunchKernelGGL(k_mem_poly_bwd<2>, grid, block, 0, st, g, pa, mu, w); break;
-    case 3: hipLaunchKernelGGL(k_mem_poly_bwd<3>, grid, block, 0, st, g, pa, mu, w); break;
-    case 4: hipLaunchKernelGGL(k_mem_poly_bwd<4>, grid, block, 0, st, g, pa, mu, w); break;
-    case kStripPassesMax: hipLaunchKernelGGL(k_mem_poly_bwd<kStripPassesMax>, grid, block, 0, st, g, pa, mu, w); break;
+    auto run = [&](auto fam_tag) -> hipError_t {
+        constexpr int FAM = decltype(fam_tag)::value;
+        switch ((pa.SP + 63) / 64) {
+        case 1: hipLaunchKernelGGL((k_mem_poly_bwd<1, FAM>), grid, block, 0, st, g, pa, mu, w); break;
+        case 2: hipLaunchKernelGGL((k_mem_poly_bwd<2, FAM>), grid, block, 0, st, g, pa, mu, w); break;
+        case 3: hipLaunchKernelGGL((k_mem_poly_bwd<3, FAM>), grid, block, 0, st, g, pa, mu, w); break;
+        case 4: hipLaunchKernelGGL((k_mem_poly_bwd<4, FAM>), grid, block, 0, st, g, pa, mu, w); break;
+        case kStripPassesMax:
+            hipLaunchKernelGGL((k_mem_poly_bwd<kStripPassesMax, FAM>), grid, block, 0, st, g, pa, mu, w); break;
+        default: return hipErrorInvalidValue;
+        }
+        return hipSuccess;
+    };
+    switch (pa.fam) {
+    case 0: return run(std::integral_constant<int, 0>{});
+    case 1: return run(std::integral_constant<int, 1>{});
+    case 3: return run(std::integral_constant<int, 3>{});
     default: return hipErrorInvalidValue;
     }
-    return hipSuccess;
 }
 
 hipError_t launch_lse_poly(const Graph &g, const Work &w, const PolyArgs &pa, const float *mu,

@@ -159,7 +159,8 @@ def test_family_storage(family, cfg):
 def test_family_storage_initial_state(family):
     """Initial state of the 1k-op workload with storage units and a sink: the
     usage and edge terms of the wide ops run on the chunk polynomials, the
-    storage term of every holder step by step."""
+    storage term of the holders the rule admits too, the others step by
+    step."""
     p = with_storage(make_problem("small", seed=0), seed=4)
     B = 4
     mu, sg = _init_state("small", p, B)
@@ -168,6 +169,49 @@ def test_family_storage_initial_state(family):
     hp.gamma_mem = 1.0
     say(f"[family] {family} small-init storage tau=1: N={p.n_ops} D={p.D}")
     _compare(p, mu, sg, lam, hp, family, f"small-init-mem/{family}", tau=1.0, gamma=1.0)
+
+
+@pytest.mark.parametrize("tau", [1.0, 0.01])
+@pytest.mark.parametrize("family", ["logistic", "cauchy"])
+def test_family_storage_polynomial_holders(family, tau):
+    """Storage holders on the chunk polynomials with the logistic and Cauchy
+    laws (every successor polynomial, at most 4 of them, rho = ((W-1)/2)/sigma
+    summed over the holder and its successors at most the family's degree-8
+    rho, the Gaussian's 1/4 scaled as the tier bounds are) beside holders
+    evaluated step by step: sigmas are drawn around those bounds on a
+    1024-step horizon."""
+    p = with_storage(make_problem("medium", seed=2), seed=3)
+    B = 2
+    ctx = bd.Context(p, 1, _hp(family))
+    W = ctx.poly_config()["W"]
+    ctx.close()
+    lam_w = (W - 1) / 2.0
+    thr = poly_sigma_thresholds(family, W)[8]   # the polynomial path's sigma threshold
+    rho8 = lam_w / thr
+    rng = np.random.default_rng(23)
+    rho = np.exp(rng.uniform(np.log(0.08 * rho8), np.log(1.2 * rho8), size=(B, p.n_ops)))
+    sg = (lam_w / rho).astype(np.float32)
+    mu = rng.uniform(-50, p.D + 50, size=(B, p.n_ops)).astype(np.float32)
+    # the holders the rule puts on the polynomials (a coverage check only)
+    deg = np.diff(p.row_ptr)
+    n_poly = []
+    for b in range(B):
+        poly = (sg[b] >= thr) & (p.delay <= 8)
+        cnt = 0
+        for i in range(p.n_ops):
+            succ = p.col_idx[p.row_ptr[i]:p.row_ptr[i + 1]]
+            if poly[i] and 1 <= deg[i] <= 4 and poly[succ].all() and \
+                    lam_w * (1.0 / sg[b, i] + (1.0 / sg[b, succ]).sum()) <= rho8:
+                cnt += 1
+        n_poly.append(cnt)
+    holders = int((deg > 0).sum())
+    say(f"  {family} W={W} rho8={rho8:.4f}: polynomial holders {n_poly} of {holders}")
+    assert min(n_poly) > 0.15 * holders and max(n_poly) < 0.85 * holders
+    lam = np.random.default_rng(24).uniform(0.05, 1.0, size=(B, 3)).astype(np.float32)
+    hp = _hp(family, alpha=0.01, rho=1e-3, tau=tau)
+    hp.gamma_mem = 1.0
+    _compare(p, mu, sg, lam, hp, family, f"poly holders tau={tau}/{family}", tau=tau, gamma=1.0,
+             restarts=range(B))
 
 
 @pytest.mark.parametrize("family", FAMS)
