@@ -701,7 +701,6 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     AL(cls, BN);
     AL(rsig, BN);
     AL(dflag, BN);
-    AL(ptier, BN);
     AL(gbits, (size_t)B * g.ngroups);
     AL(gnar, (size_t)B * g.ngroups);
     AL(Unar, g.nar_on ? (size_t)B * g.ngroups * h.D : 1);

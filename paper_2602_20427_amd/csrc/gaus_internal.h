@@ -53,9 +53,10 @@ constexpr float kMemRhoMax = 0.25f;
 // for the grid's degree-8 bound.
 constexpr int kGrids = 3;
 constexpr int kGridP[kGrids] = {1, 2, 4};
+constexpr int kPackMax = 4;   // the largest restart pack
 constexpr unsigned char kNoGrid = 255;
 // bits of Work::gbits
-constexpr unsigned kGbStep = 1u, kGbNarrow = 2u, kGbGrid = 4u;
+constexpr unsigned kGbStep = 1u, kGbGrid = 4u;
 // bits of Work::gnar: step-by-step ops left to the op kernel / taken by k_group
 constexpr unsigned kNarLeft = 1u, kNarTaken = 2u;
 // the narrow kernel: threads per work-group (at least the largest group), and
@@ -72,6 +73,13 @@ struct GridArgs {
     float lam;            // chunk half-width (W-1)/2
     float sig_thr[kTiers + 1];   // sigma >= sig_thr[t]: tier t on this grid
     float H[kDeg + 1];    // even moments of a chunk's points
+};
+
+// Work-group segments of the one polynomial launch: [0] packed grid 2
+// (P = 4), [1] packed grid 1 (P = 2), [2] grid 0; n = work-groups, nx = their
+// x extent (op group slices; the rest is the restart pack).
+struct PolySegs {
+    int n[3], nx[3];
 };
 
 struct PolyArgs {
@@ -181,11 +189,8 @@ struct Work {
     float *gsum_nar;       // [B][ngroups][2]  their V_dep, L_com
     float *gsum_lap;       // [B][nlap][2]  V_dep, L_com of each block of edges in closed form (Laplace)
     float *pedge;          // [B][E][4]  producer-side derivatives of each edge in closed form (Laplace)
-    unsigned char *ptier;  // [B][N]        polynomial op: tier of its vectors, the smallest over
-                           //               itself and its polynomial consumers (highest degree)
     unsigned *gbits;  // [B][ngroups]      work of the group this iteration (k_group):
                       //                   kGbStep = some op has step-by-step work,
-                      //                   kGbNarrow = some op takes polynomial degree 8 or 6,
                       //                   kGbGrid << g = ops on grid g; only such groups'
                       //                   polynomial work-groups write outputs (ppoly / cpoly
                       //                   hold valid records for cls != 0 ops only: readers

@@ -136,7 +136,6 @@ __global__ __launch_bounds__(64 * kFlagPack) void k_flags(Graph G, PolyArgs pa, 
         W.dflag[bi] = (unsigned char)d;
         W.mpoly[bi] = (unsigned char)(mem_on && ci != 0 && d == 0 && e1 > e0 &&
                                       e1 - e0 <= kMemPolyDeg && pa.lam * rsum <= pa.mem_rho);
-        W.ptier[bi] = (unsigned char)t;
     }
     __syncthreads();
     if (act) {   // grid: the coarsest packed grid whose pack qualifies

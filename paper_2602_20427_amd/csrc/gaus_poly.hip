@@ -13,14 +13,6 @@ namespace gaus {
 constexpr int kStripExtra = 8;   // row slots past SP: [SP] = D-3, [SP+1 .. SP+4] = helper values
 constexpr int kStripPad = kSmax; // zero slots before position 0 (positions -kSmax .. -1, F = 0)
 
-// The degree tiers of grid 0 run as two kernels so that each has its own
-// register budget: kPolyWide (tier 3, degree 5; 4 waves per SIMD with one
-// strip pass) is launched first; it writes the per-work-group usage and
-// V_dep / L_com outputs.
-// kPolyNarrow (tiers 1 and 2) follows, adds to those outputs, and
-// work-groups without such ops exit at once.  The packed grids run every
-// tier in one kernel (kPolyAll), which writes its grid's outputs.
-constexpr int kPolyWide = 3, kPolyNarrow = 12, kPolyAll = 15;
 // Taylor coefficients kept past the degree (the shift series' extra terms)
 constexpr int kPolyExtraT = 2;
 
@@ -61,32 +53,30 @@ __device__ __forceinline__ float from_lane(float v, int src, int h) {
 // so its lane evaluates D-3 instead (the step before D-2, the first position
 // of the upper segment); the shifted values of the two upper positions and,
 // for Lat = 0, the value at L0 come from one more evaluation on four lanes.
-template <int NP, int TIERS, int FAM, int P>
-__global__ __launch_bounds__(64 * kPolyWaves) __attribute__((amdgpu_waves_per_eu(TIERS == kPolyWide && NP == 1 ? 4 : 3)))
-void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__restrict__ sigma, Work W) {
-    static_assert(P == 1 || (NP == 1 && TIERS == kPolyAll), "packed grids: one strip pass, one kernel");
+// One work-group of grid GI: (bx, by) = (op group slice, restart pack); sUc,
+// sGs: the work-group's LDS for the chunk coefficients and the edge sums.
+template <int NP, int FAM, int P>
+__device__ __forceinline__ void poly_wg(const Graph &G, const PolyArgs &pa, const float *__restrict__ mu,
+                                        const float *__restrict__ sigma, const Work &W, int bx, int by,
+                                        float (*sUc)[64][kNC], float (*sGs)[kPackMax][2]) {
+    static_assert(P == 1 || NP == 1, "packed grids: one strip pass");
+    static_assert(P <= kPackMax, "restart pack");
     constexpr int GI = P == 1 ? 0 : P == 2 ? 1 : 2;   // grid
     constexpr int L = 64 / P;                          // lanes per restart
-    constexpr bool kWrite = TIERS != kPolyNarrow;      // write (not add) the work-group outputs
     const GridArgs &gd = pa.gr[GI];
     const int split = gd.split;
-    const int grp = blockIdx.x / split, sub = blockIdx.x - grp * split;
+    const int grp = bx / split, sub = bx - grp * split;
     const int N = G.N, D = G.D, B = G.B;
-    if constexpr (TIERS == kPolyNarrow) {   // no op of the group takes degree 8 or 6
-        if (!(W.gbits[(size_t)blockIdx.y * G.ngroups + grp] & kGbNarrow)) return;
-    }
     // no op of the group on this grid (in every restart of the pack): nothing
     // to write, the readers skip the group
-    if (!(W.gbits[(size_t)blockIdx.y * P * G.ngroups + grp] & (kGbGrid << GI))) return;
+    if (!(W.gbits[(size_t)by * P * G.ngroups + grp] & (kGbGrid << GI))) return;
     // dynamic LDS: per (wave, restart) 6 rows of SP strip values and 3 rows of
     // SP + kStripExtra raw CDF values, then per (wave, restart) SP strip usages
     extern __shared__ float sDyn[];
-    __shared__ float sUc[kPolyWaves][64][kNC];
-    __shared__ float sGs[kPolyWaves][P][2];
     const int SP = gd.SP, L0 = gd.L0;
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     const int h = P == 1 ? 0 : lane / L, c = P == 1 ? lane : lane % L;
-    const int b0 = blockIdx.y * P, bh = b0 + h;    // this lane's restart
+    const int b0 = by * P, bh = b0 + h;    // this lane's restart
     const bool hact = P == 1 || bh < B;
     const bool cact = hact && c < gd.nc;
     const float tcen = (float)(L0 + c * gd.W) + gd.lam;
@@ -128,9 +118,6 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
             l_s = G.delay[i];
             l_e0 = G.row_ptr[i]; l_e1 = G.row_ptr[i + 1];
         }
-    }
-    if constexpr (TIERS == kPolyNarrow) {   // nothing to add unless the work-group has ops of these tiers
-        if (!__syncthreads_or(lane < nq && l_mine && (l_cls == 1 || l_cls == 2))) return;
     }
     float gsum = 0.0f;  // V_dep, L_com of this wave's ops (lanes c = 0 and 2)
     // polynomial ops, one pass per degree tier (NC coefficients per vector)
@@ -311,16 +298,10 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
         gsum += pt4;   // lane c = 0: V_dep, c = 2: L_com
     }
     };
-    if constexpr (TIERS == kPolyWide) {
-        tier_pass(std::integral_constant<int, kTierDeg[3] + 1>{}, 3);
-    } else if constexpr (TIERS == kPolyNarrow) {
-        tier_pass(std::integral_constant<int, kTierDeg[1] + 1>{}, 1);
-        tier_pass(std::integral_constant<int, kTierDeg[2] + 1>{}, 2);
-    } else {
-        tier_pass(std::integral_constant<int, kTierDeg[3] + 1>{}, 3);
-        tier_pass(std::integral_constant<int, kTierDeg[2] + 1>{}, 2);
-        tier_pass(std::integral_constant<int, kTierDeg[1] + 1>{}, 1);
-    }
+    // every degree tier: 5, 6, then 8
+    tier_pass(std::integral_constant<int, kTierDeg[3] + 1>{}, 3);
+    tier_pass(std::integral_constant<int, kTierDeg[2] + 1>{}, 2);
+    tier_pass(std::integral_constant<int, kTierDeg[1] + 1>{}, 1);
     if (c == 0) sGs[wv][h][0] = gsum;
     if (c == 2) sGs[wv][h][1] = gsum;
 
@@ -342,7 +323,7 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
 #pragma unroll
         for (int w = 0; w < kPolyWaves; ++w) acc += sUc[w][ln][k];
         float *dst = W.Ucoef + slot_of(b0 + hh) * kMaxChunks * kNC + cx * kNC + k;
-        *dst = kWrite ? acc : *dst + acc;
+        *dst = acc;
     }
     if (threadIdx.x < 2 * P) {
         const int hh = threadIdx.x >> 1, v = threadIdx.x & 1;
@@ -351,7 +332,7 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
 #pragma unroll
             for (int w = 0; w < kPolyWaves; ++w) acc += sGs[w][hh][v];
             float *gs = W.gsum_poly + slot_of(b0 + hh) * 2 + v;
-            *gs = kWrite ? acc : *gs + acc;
+            *gs = acc;
         }
     }
     for (int x = threadIdx.x; x < P * SP; x += 64 * kPolyWaves) {
@@ -361,8 +342,32 @@ void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__r
 #pragma unroll
         for (int w = 0; w < kPolyWaves; ++w) acc += sUs[(w * P + hh) * SP + p];
         float *usg = W.Ustrip + slot_of(b0 + hh) * kStripMax + p;
-        *usg = kWrite ? acc : *usg + acc;
+        *usg = acc;
     }
+}
+
+// The polynomial path in one launch: the work-groups of the packed grids
+// (P = 4, then P = 2) and of grid 0 (every tier) one after the other in x, so
+// a grid with no op costs its early exits inside the launch, not a launch of
+// its own.  Segment sizes in PolySegs (host: poly_segs).
+template <int NPV, int FAM>
+__global__ __launch_bounds__(64 * kPolyWaves) __attribute__((amdgpu_waves_per_eu(3)))
+void k_poly(Graph G, PolyArgs pa, const float *__restrict__ mu, const float *__restrict__ sigma, Work W,
+            PolySegs sg) {
+    __shared__ float sUc[kPolyWaves][64][kNC];
+    __shared__ float sGs[kPolyWaves][kPackMax][2];
+    int x = blockIdx.x;
+    if (x < sg.n[0]) {
+        poly_wg<1, FAM, 4>(G, pa, mu, sigma, W, x % sg.nx[0], x / sg.nx[0], sUc, sGs);
+        return;
+    }
+    x -= sg.n[0];
+    if (x < sg.n[1]) {
+        poly_wg<1, FAM, 2>(G, pa, mu, sigma, W, x % sg.nx[1], x / sg.nx[1], sUc, sGs);
+        return;
+    }
+    x -= sg.n[1];
+    poly_wg<NPV, FAM, 1>(G, pa, mu, sigma, W, x % sg.nx[2], x / sg.nx[2], sUc, sGs);
 }
 
 
@@ -801,35 +806,36 @@ __global__ __launch_bounds__(64 * kPolyWaves) void k_mem_poly_bwd(Graph G, PolyA
 // ---------------------------------------------------------------------------
 hipError_t launch_poly(const Graph &g, const Work &w, const PolyArgs &pa, const float *mu, const float *sigma,
                        hipStream_t st) {
-    const size_t lds = sizeof(float) * (size_t)kPolyWaves * (row_stride<1>(pa.SP) + pa.SP);
-    const dim3 grid(g.ngroups * pa.split, g.B), block(64 * kPolyWaves);
-    // packed grid G_: restart packs of P_ on the y axis, per-(wave, restart) LDS rows
-    auto packed = [&](auto fam_tag, auto p_tag) {
-        constexpr int FAM = decltype(fam_tag)::value, P_ = decltype(p_tag)::value;
-        constexpr int G_ = P_ == 2 ? 1 : 2;
-        const GridArgs &gd = pa.gr[G_];
+    // segments: packed grid 2 (P = 4), packed grid 1 (P = 2), grid 0; dynamic
+    // LDS for the largest of them
+    PolySegs sg{};
+    size_t lds = sizeof(float) * (size_t)kPolyWaves * (row_stride<1>(pa.SP) + pa.SP);
+    auto packed = [&](int gi, int P, auto p_tag) {
+        constexpr int P_ = decltype(p_tag)::value;
+        const GridArgs &gd = pa.gr[gi];
+        const int s = gi == 2 ? 0 : 1;
         if (!gd.on) return;
-        const size_t ldsp = sizeof(float) * (size_t)kPolyWaves * P_ * (row_stride<P_>(gd.SP) + gd.SP);
-        const dim3 gridp(g.ngroups * gd.split, (g.B + P_ - 1) / P_);
-        hipLaunchKernelGGL((k_poly<1, kPolyAll, FAM, P_>), gridp, block, ldsp, st, g, pa, mu, sigma, w);
+        sg.nx[s] = g.ngroups * gd.split;
+        sg.n[s] = sg.nx[s] * ((g.B + P - 1) / P);
+        lds = std::max(lds, sizeof(float) * (size_t)kPolyWaves * P_ * (row_stride<P_>(gd.SP) + gd.SP));
     };
+    packed(2, 4, std::integral_constant<int, 4>{});
+    packed(1, 2, std::integral_constant<int, 2>{});
+    sg.nx[2] = g.ngroups * pa.split;
+    sg.n[2] = sg.nx[2] * g.B;
+    const dim3 grid((unsigned)(sg.n[0] + sg.n[1] + sg.n[2])), block(64 * kPolyWaves);
     auto run = [&](auto fam_tag) -> hipError_t {
         constexpr int FAM = decltype(fam_tag)::value;
-#define GAUS_POLY_PAIR(NPV)                                                                              \
-        hipLaunchKernelGGL((k_poly<NPV, kPolyWide, FAM, 1>), grid, block, lds, st, g, pa, mu, sigma, w);   \
-        hipLaunchKernelGGL((k_poly<NPV, kPolyNarrow, FAM, 1>), grid, block, lds, st, g, pa, mu, sigma, w);
         switch ((pa.SP + 63) / 64) {
-        case 1: GAUS_POLY_PAIR(1) break;
-        case 2: GAUS_POLY_PAIR(2) break;
-        case 3: GAUS_POLY_PAIR(3) break;
-        case 4: GAUS_POLY_PAIR(4) break;
-        case kStripPassesMax: GAUS_POLY_PAIR(kStripPassesMax) break;
+        case 1: hipLaunchKernelGGL((k_poly<1, FAM>), grid, block, lds, st, g, pa, mu, sigma, w, sg); break;
+        case 2: hipLaunchKernelGGL((k_poly<2, FAM>), grid, block, lds, st, g, pa, mu, sigma, w, sg); break;
+        case 3: hipLaunchKernelGGL((k_poly<3, FAM>), grid, block, lds, st, g, pa, mu, sigma, w, sg); break;
+        case 4: hipLaunchKernelGGL((k_poly<4, FAM>), grid, block, lds, st, g, pa, mu, sigma, w, sg); break;
+        case kStripPassesMax:
+            hipLaunchKernelGGL((k_poly<kStripPassesMax, FAM>), grid, block, lds, st, g, pa, mu, sigma, w, sg); break;
         default: return hipErrorInvalidValue;
         }
-#undef GAUS_POLY_PAIR
-        packed(fam_tag, std::integral_constant<int, 2>{});
-        packed(fam_tag, std::integral_constant<int, 4>{});
-        return hipSuccess;
+        return hipGetLastError();
     };
     switch (pa.fam) {
     case 0: return run(std::integral_constant<int, 0>{});

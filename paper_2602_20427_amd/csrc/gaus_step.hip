@@ -996,8 +996,8 @@ __global__ __launch_bounds__(BS) __attribute__((amdgpu_waves_per_eu(4))) void k_
 // ---------------------------------------------------------------------------
 // Group kernel.  Work-group = (op group, restart).
 // (1) The group's work bits this iteration (gbits): the OR over its ops of
-//     kGbStep (step-by-step work), kGbNarrow (degree 8 or 6) and kGbGrid <<
-//     grid; one plain store per (restart, group).
+//     kGbStep (step-by-step work) and kGbGrid << grid; one plain store per
+//     (restart, group).
 // (2) With the narrow path on (G.nar_on): the step-by-step ops whose spreads
 //     are short, each taken once over the whole horizon instead of once per
 //     step tile.  Thread per op for the sorting (the op kernel's spread tests
@@ -1033,9 +1033,8 @@ __global__ __launch_bounds__(kNarBS) void k_group(Graph G, const float *__restri
         unsigned bits = 0u;
         for (int q = tid; q < nq; q += BS) {
             const size_t bi = (size_t)b * N + G.perm[q0 + q];
-            const int t = W.ptier[bi], gs = W.gsel[bi];
+            const int gs = W.gsel[bi];
             bits |= W.dflag[bi] ? kGbStep : 0u;
-            bits |= (t == 1 || t == 2) ? kGbNarrow : 0u;
             bits |= gs < kGrids ? kGbGrid << gs : 0u;
         }
         unsigned v = 0u;
