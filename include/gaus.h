@@ -94,7 +94,7 @@ typedef struct {
     int32_t poly_chunk;            /* chunk width W of the polynomial evaluation of wide
                                       start-time laws (one restart per wave): 0 = chosen
                                       from D, < 0 = off (every op evaluated step by step),
-                                      else W in [16, 256] */
+                                      else W in [12, 256] */
     float beta_res;                /* weight of the smooth peak usage L_res in L (>= 0;
                                       1 with alpha_com gives Formulation A, Sec. 4.1) */
     float tau;                     /* its temperature (> 0): L_res = sum_k tau log sum_t

@@ -160,8 +160,9 @@ void setup_grid(int D, int W, int nc, int fam, GridArgs &gr) {
 // path (families with an analytic CDF: Gaussian, logistic, Cauchy).
 // requested: grid-0 chunk width (0 = chosen here, < 0 = path off);
 // pack: packed grids (0 = when the width is chosen here, > 0 = on, < 0 = off),
-// used only for grids whose restart pack fits B.
-void setup_poly(int D, int requested, int pack, int fam, int B, PolyArgs &pa) {
+// used only for grids whose restart pack fits B; storage: the storage term
+// is on (a chosen width stays >= kMinChunkStorage).
+void setup_poly(int D, int requested, int pack, int fam, int B, bool storage, PolyArgs &pa) {
     pa = PolyArgs{};
     if (requested < 0 || !(fam == 0 || fam == 1 || fam == 3)) return;
     // Grid 0: chunks tile [L0, D-2) with nc <= 64 chunks (one per lane); the
@@ -169,7 +170,8 @@ void setup_poly(int D, int requested, int pack, int fam, int B, PolyArgs &pa) {
     // lanes.  Take the fewest strip passes, then the smallest W (the lowest
     // sigma threshold 2(W-1) for the polynomial path).
     int W = 0, nc = 0, best_passes = 1 << 30;
-    for (int w = 16; w <= 256; ++w) {
+    const int w0 = requested > 0 ? kMinChunk : storage ? kMinChunkStorage : kMinChunk;
+    for (int w = w0; w <= kMaxChunk; ++w) {
         if (requested > 0 && w != requested) continue;
         const int n = std::min(kMaxChunks, (D - 2 - kSmax) / w);
         if (n < 4) continue;
@@ -196,7 +198,7 @@ void setup_poly(int D, int requested, int pack, int fam, int B, PolyArgs &pa) {
     for (int g = 1; g < kGrids && packing; ++g) {
         const int P = kGridP[g], L = 64 / P;
         if (B < P) continue;
-        for (int w = 16; w <= 256; ++w) {
+        for (int w = kMinChunkStorage; w <= kMaxChunk; ++w) {
             const int n = std::min(L, (D - 2 - kSmax) / w);
             if (n < 4) continue;
             if (D - 2 - n * w + 2 > L) continue;
@@ -475,8 +477,9 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     if (s != GAUS_OK) return s;
     gaus_hparams hp;
     if (hp_in) hp = *hp_in; else gaus_default_hparams(&hp);
-    if (hp.poly_chunk > 0 && (hp.poly_chunk < 16 || hp.poly_chunk > 256))
-        return fail(nullptr, GAUS_E_INVALID_ARG, "poly_chunk must be 0 (auto), negative (off) or in [16, 256]");
+    if (hp.poly_chunk > 0 && (hp.poly_chunk < kMinChunk || hp.poly_chunk > kMaxChunk))
+        return fail(nullptr, GAUS_E_INVALID_ARG, "poly_chunk must be 0 (auto), negative (off) or in [%d, %d]", kMinChunk,
+                    kMaxChunk);
     if (!(hp.beta_res >= 0.0f) || !std::isfinite(hp.beta_res) || !(hp.tau > 0.0f) || !std::isfinite(hp.tau) ||
         !(hp.gamma_mem >= 0.0f) || !std::isfinite(hp.gamma_mem))
         return fail(nullptr, GAUS_E_INVALID_ARG, "beta_res and gamma_mem must be finite and >= 0, tau finite and > 0");
@@ -507,7 +510,7 @@ gaus_status gaus_init(const gaus_problem *prob, const gaus_hparams *hp_in, int32
     c->lc.fam = hp.family;
     // the chunk polynomials take the Gaussian, logistic and Cauchy laws; the
     // Laplace CDF has a kink at the median (no series over a chunk there)
-    setup_poly(h.D, hp.poly_chunk, hp.poly_pack, hp.family, B, c->pa);
+    setup_poly(h.D, hp.poly_chunk, hp.poly_pack, hp.family, B, hp.gamma_mem > 0.0f, c->pa);
 
     Graph &g = c->g;
     g.N = h.N; g.E = h.E; g.K = h.K; g.D = h.D; g.II = h.II; g.T = h.II > 0 ? h.II : h.D;

@@ -35,6 +35,12 @@ constexpr int kTN = kDeg + kShiftTerms + 2;   // scaled derivatives T_0 .. T_{kT
 constexpr int kSmax = 8;                      // largest producer delay on that path
 constexpr float kRhoMax = 0.25f;
 constexpr int kMaxChunks = 64;                // one chunk per lane of a wave
+// chunk widths W of the grids (W <= 256 keeps the degree-16 moments within
+// fp32 range; the smallest W gives the lowest sigma threshold of the path,
+// about 2 (W - 1) at degree 8).  With the storage term on, a chosen width
+// stays >= 16: its holders' gradients lose accuracy at narrower chunks
+// (measured at tau = 0.01: 1.2e-7 at W = 16, 7e-6 at 12, 4e-5 at 15).
+constexpr int kMinChunk = 12, kMinChunkStorage = 16, kMaxChunk = 256;
 constexpr int kStripMax = 320;                 // step-by-step strip positions per op, at most
 // Storage term on the chunk polynomials: a holder whose successors are all
 // polynomial, at most kMemPolyDeg of them, with rho summed over the holder

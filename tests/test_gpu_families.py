@@ -182,7 +182,9 @@ def test_family_storage_polynomial_holders(family, tau):
     1024-step horizon."""
     p = with_storage(make_problem("medium", seed=2), seed=3)
     B = 2
-    ctx = bd.Context(p, 1, _hp(family))
+    hw = _hp(family)
+    hw.gamma_mem = 1.0   # the chunk width chosen with the storage term on
+    ctx = bd.Context(p, 1, hw)
     W = ctx.poly_config()["W"]
     ctx.close()
     lam_w = (W - 1) / 2.0
