@@ -299,7 +299,7 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build runs the scheduling hot path on one GPU; multi-GPU runs "
+        print("bench.py: the library runs the scheduling hot path on one GPU; multi-GPU runs "
               "(--gpus > 1) are not supported", file=sys.stderr)
         sys.exit(2)
 
